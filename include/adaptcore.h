@@ -1,0 +1,229 @@
+/*
+ * adaptcore.h -- C ABI of the adaptive dynamic-shape GEMM library for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The library computes C = A * B for dense matrices of arbitrary (M, N, K),
+ * following "Adaptive Matrix Multiplication for Dynamic Shapes on Ascend
+ * NPUs" (AdaptCore), re-designed for gfx950:
+ *   - a shape is mapped to a template of the 2D tiling taxonomy (Section 4.2:
+ *     spatial parallelism x accumulation regime, worked cases in Section 4.3);
+ *   - a deterministic analytical latency model (Section 5.2, Eqs. 7-14)
+ *     selects the tile and the optimisation modules (Table 2) among the legal
+ *     candidates (Eq. 6);
+ *   - the selected configuration is cached under a 64-bit key of the shape
+ *     (Section 3.1, online phase), so a repeated shape dispatches in O(1).
+ *
+ * Conventions for every entry point:
+ *   - All functions are extern "C", never throw, and report failure through
+ *     the return code (or NULL); adaptcore_last_error() then returns a
+ *     thread-local message describing the last failure of the calling thread.
+ *   - Matrices are dense, row-major, with leading dimensions in ELEMENTS.
+ *     A is M x K (lda >= max(1, K)), B is K x N (ldb >= max(1, N)),
+ *     C is M x N (ldc >= max(1, N)). Inputs are bf16 (raw 16-bit storage);
+ *     accumulation is always fp32; C is fp32 or bf16 (round to nearest even)
+ *     as the plan's dtype says.
+ *   - A, B, C are device pointers owned by the caller; they must be aligned
+ *     to their element size and must not overlap C.
+ *   - The library is single-GPU: every call uses the HIP device current on
+ *     the calling thread.
+ */
+#ifndef ADAPTCORE_H
+#define ADAPTCORE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AC_OK = 0,
+  AC_ERR_INVALID_VALUE = -1,   /* bad dimension, leading dimension, pointer or key */
+  AC_ERR_UNSUPPORTED = -2,     /* dtype / layout not provided by this build */
+  AC_ERR_OUT_OF_MEMORY = -3,   /* workspace allocation failed */
+  AC_ERR_LAUNCH = -4,          /* the HIP runtime rejected a launch */
+  AC_ERR_NOT_INITIALIZED = -5, /* no GPU, or workspace missing under stream capture */
+  AC_ERR_INTERNAL = -6
+} adaptcore_status;
+
+/* Element types: bf16 inputs, fp32 accumulation, and the output type. */
+typedef enum {
+  AC_BF16_F32OUT = 0,  /* C is fp32 */
+  AC_BF16_BF16OUT = 1  /* C is bf16, rounded to nearest even */
+} adaptcore_dtype;
+
+/* Operand layouts. This build provides row-major A and row-major B. */
+enum { AC_LAYOUT_ROW_ROW = 0 };
+
+/* Templates of the 2D tiling taxonomy (Section 4.2). */
+typedef enum {
+  AC_CLASS_COMMON = 0,             /* P_m*P_n >= N_core, accumulator on chip */
+  AC_CLASS_SINGLE_CORE_SPLITK = 1, /* P_m*P_n >= N_core, accumulator spills  */
+  AC_CLASS_MULTI_CORE_SPLITK = 2,  /* P_m*P_n <  N_core, accumulator on chip */
+  AC_CLASS_HYBRID_SPLITK = 3       /* P_m*P_n <  N_core, accumulator spills  */
+} adaptcore_class;
+
+/* Kernel families of the variant space. */
+typedef enum {
+  AC_FAMILY_TILE = 0,     /* MFMA macro-tile kernel, P_k >= 1 */
+  AC_FAMILY_SKINNY_M = 1, /* Small-M Copy module: B streamed once, M <= 64 */
+  AC_FAMILY_SKINNY_N = 2, /* Small-M Copy by orientation: A streamed once, N <= 64 */
+  AC_FAMILY_STREAMK = 3   /* StreamK applied to the tile kernel */
+} adaptcore_family;
+
+typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */
+
+/* Description of a plan (adaptcore_plan_info). */
+typedef struct {
+  int64_t M, N, K;
+  int32_t dtype;
+  uint32_t layouts;
+  uint64_t shape_key;   /* 64-bit key of the shape (cache index) */
+  uint64_t variant_key; /* 64-bit key of the selected configuration */
+  int32_t cls;          /* adaptcore_class of the taxonomy for this shape */
+  int32_t family;       /* adaptcore_family of the selected kernel */
+  int32_t tile_m, tile_n, tile_k; /* m1, n1, k1 (workgroup output tile, k granule) */
+  int32_t pm, pn, pk;   /* task counts P_m, P_n, P_k of the selected kernel */
+  int32_t grid_x, grid_y; /* launch grid (workgroups of 256 threads) */
+  int32_t swizzle;      /* 1 = XCD-aware grouped tile order (ShuffleK analogue) */
+  int32_t n_candidates; /* legal candidates the model compared */
+  double predicted_s;   /* model latency of the selected configuration, seconds */
+  int64_t workspace_bytes; /* fp32 partial tiles + counters needed per stream */
+} adaptcore_plan_desc_t;
+
+/* One legal candidate of a shape (adaptcore_candidates). */
+typedef struct {
+  uint64_t variant_key;
+  int32_t cls, family, tile_m, tile_n, tile_k, pk, grid_x, grid_y;
+  double predicted_s;
+} adaptcore_candidate_t;
+
+/* Counters (adaptcore_stats). */
+typedef struct {
+  uint64_t lookups;       /* adaptcore_plan calls */
+  uint64_t hits;          /* served from the cache */
+  uint64_t misses;        /* planned (taxonomy + model) */
+  uint64_t entries;       /* plans held by the cache */
+  uint64_t launches;      /* kernels launched by adaptcore_matmul */
+  double miss_seconds;    /* total host time spent planning misses */
+  uint64_t class_count[4];/* misses per taxonomy class */
+} adaptcore_stats_t;
+
+/* Hardware profile used by the planner. Defaults describe one MI355X
+ * (256 CUs, 160 KiB LDS per CU); adaptcore_init() replaces the CU count with
+ * the device's. The latency constants are the model's lambda / eta / BW of
+ * Eq. 8, calibrated on the device. */
+typedef struct {
+  int32_t n_cu;          /* N_core: compute units */
+  int32_t lds_bytes;     /* LDS per CU */
+  int64_t s_acc_bytes;   /* accumulator capacity of one workgroup (S_L0C analogue) */
+  double clock_hz;       /* shader clock */
+  double hbm_bw;         /* peak HBM bandwidth, bytes/s */
+  double hbm_eta;        /* achievable fraction of hbm_bw for streaming reads */
+  double l2_bw_cu;       /* per-CU bandwidth for cache-resident reads, bytes/s */
+  double t_launch;       /* launch + dispatch cost of one kernel, s */
+  double t_mem_latency;  /* exposed latency of a workgroup's first load, s */
+  double t_wg;           /* fixed cost of one workgroup (setup, epilogue issue), s */
+  double mfma_eta;       /* achievable fraction of MFMA issue rate */
+  double lds_bw_cu;      /* LDS bytes per second per CU */
+  double unaligned_eta;  /* bandwidth factor for rows that are not 16-byte aligned */
+  double l2_hit;         /* fraction of tile re-reads served by L2 / MALL */
+  int32_t search_open;   /* 0: search inside the taxonomy's template (Eq. 6);
+                            1: search every template (the exhaustive reading) */
+  int32_t enable_streamk; /* 1: StreamK candidates take part in the search */
+} adaptcore_hw_t;
+
+/* Optional: bind the library to the current HIP device and read its CU count.
+ * Without it, planning uses the default MI355X profile. AC_ERR_NOT_INITIALIZED
+ * when no device is present. */
+adaptcore_status adaptcore_init(void);
+
+/* Returns the cached plan for (M, N, K, dtype, layouts), planning it on the
+ * first request (taxonomy, candidate enumeration, latency model, arg-min).
+ * The same arguments always return the same pointer until
+ * adaptcore_cache_clear(). M, N, K >= 0 and < 2^31. NULL on invalid or
+ * unsupported arguments (see adaptcore_last_error). Host-only: no GPU work,
+ * safe from many threads at once. */
+const adaptcore_plan_t* adaptcore_plan(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts);
+
+/* Like adaptcore_plan, but with the configuration forced to `variant_key`
+ * (one of the keys listed by adaptcore_candidates). For tests and the
+ * exhaustive model-accuracy experiment. NULL if the key is not legal for the
+ * shape. */
+const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, int32_t dtype,
+                                               uint32_t layouts, uint64_t variant_key);
+
+/* Runs a plan: C = A * B, asynchronously on `stream` (a hipStream_t; NULL is
+ * the null stream). Validates the leading dimensions against the plan's
+ * shape. M == 0 or N == 0: nothing is launched. K == 0: C is set to zero.
+ * Split-K plans use a workspace owned by the library for this (device,
+ * stream); it is allocated on the stream's first use (outside any stream
+ * capture: under capture a missing workspace gives AC_ERR_NOT_INITIALIZED)
+ * and grows monotonically. Concurrent calls on ONE stream are ordered by the
+ * stream; calls on different streams use different workspaces. */
+adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
+                                  int64_t ldb, void* C, int64_t ldc, void* stream);
+
+/* Allocates (if needed) the workspace of `stream` for plans needing up to
+ * `bytes`, so that later calls, also under capture, do not allocate. */
+adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes);
+
+/* Fills *out with the description of a plan. */
+adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out);
+
+/* Lists the legal candidates of a shape with their model latencies, ordered
+ * by the model's preference (best first). Returns the number of candidates
+ * (which may exceed cap; at most cap are written), or a negative status. */
+int64_t adaptcore_candidates(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts,
+                             adaptcore_candidate_t* out, int64_t cap);
+
+/* Planner profile. set() drops every cached plan (they depend on it). */
+adaptcore_status adaptcore_get_hw(adaptcore_hw_t* out);
+adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw);
+
+adaptcore_status adaptcore_stats(adaptcore_stats_t* out);
+
+/* Drops every cached plan. Plans returned earlier become invalid: call only
+ * when no other thread uses the library. */
+adaptcore_status adaptcore_cache_clear(void);
+
+/* Median host time of one cached lookup, in nanoseconds, measured over
+ * n_lookups lookups cycling through n_keys distinct shapes already planned
+ * (timed in C, without any binding overhead). */
+adaptcore_status adaptcore_bench_lookup(int64_t n_keys, int64_t n_lookups, double* ns_per_lookup);
+
+/* Thread-local message of the last failure ("" if none). */
+const char* adaptcore_last_error(void);
+
+/* Thread-local status of the last failure (AC_OK if none), e.g. the reason an
+ * adaptcore_plan call returned NULL. */
+adaptcore_status adaptcore_last_status(void);
+
+/* ---- planner arithmetic, exposed for testing against the paper ---------- */
+
+/* The taxonomy and data-volume terms for explicit tiling parameters and a
+ * hardware (n_core, s_acc): task counts (Table 1), the template of
+ * Section 4.2, D_r of Eq. 1 and D_w of Eqs. 2-5 (bytes; elem_bytes and
+ * out_bytes as Section 4.2 assumes fp16, i.e. 2 and 2). */
+typedef struct {
+  int64_t M, N, K, m, n, k, m1, n1, k1;
+  int64_t n_core, s_acc;
+  int32_t elem_bytes, out_bytes;
+} adaptcore_taxonomy_in_t;
+typedef struct {
+  int64_t pm, pn, pk;
+  int32_t cls;
+  int64_t acc_bytes;
+  double read_bytes;  /* Eq. 1 */
+  double write_bytes; /* Eqs. 2-5 for the template */
+} adaptcore_taxonomy_out_t;
+adaptcore_status adaptcore_taxonomy(const adaptcore_taxonomy_in_t* in, adaptcore_taxonomy_out_t* out);
+
+/* Pipeline schedules of Section 5.3: kind 0 = baseline (Eq. 12), 1 = double
+ * buffering (Eq. 13), 2 = preloading over Q tiles (Eq. 14). */
+double adaptcore_schedule(int32_t kind, int64_t Q, int64_t L, double t_m, double t_p, double t_drain);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ADAPTCORE_H */

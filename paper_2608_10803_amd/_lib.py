@@ -1,0 +1,269 @@
+"""ctypes binding of libadaptcore.so: argument marshalling only.
+
+Every function has the name and argument order of the C entry point in
+include/adaptcore.h. Device memory and streams are passed as integers
+(addresses / hipStream_t handles); `torch` is optional and only used by the
+convenience wrapper `matmul_tensors`. The library must be built
+(`python -m paper_2608_10803_amd.build`); there is no fallback.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libadaptcore.so")
+
+AC_OK = 0
+AC_ERR_INVALID_VALUE = -1
+AC_ERR_UNSUPPORTED = -2
+AC_ERR_OUT_OF_MEMORY = -3
+AC_ERR_LAUNCH = -4
+AC_ERR_NOT_INITIALIZED = -5
+AC_ERR_INTERNAL = -6
+
+AC_BF16_F32OUT = 0
+AC_BF16_BF16OUT = 1
+AC_LAYOUT_ROW_ROW = 0
+
+CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk"]
+
+
+class AdaptCoreError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("adaptcore error %d: %s" % (status, msg))
+        self.status = status
+
+
+class PlanDesc(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("dtype", ctypes.c_int32), ("layouts", ctypes.c_uint32),
+                ("shape_key", ctypes.c_uint64), ("variant_key", ctypes.c_uint64),
+                ("cls", ctypes.c_int32), ("family", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
+                ("pm", ctypes.c_int32), ("pn", ctypes.c_int32), ("pk", ctypes.c_int32),
+                ("grid_x", ctypes.c_int32), ("grid_y", ctypes.c_int32),
+                ("swizzle", ctypes.c_int32), ("n_candidates", ctypes.c_int32),
+                ("predicted_s", ctypes.c_double), ("workspace_bytes", ctypes.c_int64)]
+
+    def as_dict(self):
+        d = {f: getattr(self, f) for f, _ in self._fields_}
+        d["cls_name"] = CLASS_NAMES[self.cls]
+        d["family_name"] = FAMILY_NAMES[self.family]
+        return d
+
+
+class Candidate(ctypes.Structure):
+    _fields_ = [("variant_key", ctypes.c_uint64), ("cls", ctypes.c_int32), ("family", ctypes.c_int32),
+                ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("tile_k", ctypes.c_int32),
+                ("pk", ctypes.c_int32), ("grid_x", ctypes.c_int32), ("grid_y", ctypes.c_int32),
+                ("predicted_s", ctypes.c_double)]
+
+    def as_dict(self):
+        d = {f: getattr(self, f) for f, _ in self._fields_}
+        d["family_name"] = FAMILY_NAMES[self.family]
+        return d
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("lookups", ctypes.c_uint64), ("hits", ctypes.c_uint64), ("misses", ctypes.c_uint64),
+                ("entries", ctypes.c_uint64), ("launches", ctypes.c_uint64),
+                ("miss_seconds", ctypes.c_double), ("class_count", ctypes.c_uint64 * 4)]
+
+
+class Hw(ctypes.Structure):
+    _fields_ = [("n_cu", ctypes.c_int32), ("lds_bytes", ctypes.c_int32), ("s_acc_bytes", ctypes.c_int64),
+                ("clock_hz", ctypes.c_double), ("hbm_bw", ctypes.c_double), ("hbm_eta", ctypes.c_double),
+                ("l2_bw_cu", ctypes.c_double), ("t_launch", ctypes.c_double),
+                ("t_mem_latency", ctypes.c_double), ("t_wg", ctypes.c_double), ("mfma_eta", ctypes.c_double),
+                ("lds_bw_cu", ctypes.c_double), ("unaligned_eta", ctypes.c_double), ("l2_hit", ctypes.c_double),
+                ("search_open", ctypes.c_int32), ("enable_streamk", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class TaxIn(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("M", "N", "K", "m", "n", "k", "m1", "n1", "k1", "n_core", "s_acc")] + \
+               [("elem_bytes", ctypes.c_int32), ("out_bytes", ctypes.c_int32)]
+
+
+class TaxOut(ctypes.Structure):
+    _fields_ = [("pm", ctypes.c_int64), ("pn", ctypes.c_int64), ("pk", ctypes.c_int64), ("cls", ctypes.c_int32),
+                ("acc_bytes", ctypes.c_int64), ("read_bytes", ctypes.c_double), ("write_bytes", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libadaptcore.so is not built: run `python -m paper_2608_10803_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        i64, i32, u32, u64, p, d = (ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64,
+                                    ctypes.c_void_p, ctypes.c_double)
+        L.adaptcore_init.argtypes = []
+        L.adaptcore_init.restype = i32
+        L.adaptcore_plan.argtypes = [i64, i64, i64, i32, u32]
+        L.adaptcore_plan.restype = p
+        L.adaptcore_plan_variant.argtypes = [i64, i64, i64, i32, u32, u64]
+        L.adaptcore_plan_variant.restype = p
+        L.adaptcore_matmul.argtypes = [p, p, i64, p, i64, p, i64, p]
+        L.adaptcore_matmul.restype = i32
+        L.adaptcore_reserve_workspace.argtypes = [p, i64]
+        L.adaptcore_reserve_workspace.restype = i32
+        L.adaptcore_plan_info.argtypes = [p, ctypes.POINTER(PlanDesc)]
+        L.adaptcore_plan_info.restype = i32
+        L.adaptcore_candidates.argtypes = [i64, i64, i64, i32, u32, ctypes.POINTER(Candidate), i64]
+        L.adaptcore_candidates.restype = i64
+        L.adaptcore_get_hw.argtypes = [ctypes.POINTER(Hw)]
+        L.adaptcore_get_hw.restype = i32
+        L.adaptcore_set_hw.argtypes = [ctypes.POINTER(Hw)]
+        L.adaptcore_set_hw.restype = i32
+        L.adaptcore_stats.argtypes = [ctypes.POINTER(Stats)]
+        L.adaptcore_stats.restype = i32
+        L.adaptcore_cache_clear.argtypes = []
+        L.adaptcore_cache_clear.restype = i32
+        L.adaptcore_bench_lookup.argtypes = [i64, i64, ctypes.POINTER(d)]
+        L.adaptcore_bench_lookup.restype = i32
+        L.adaptcore_last_error.argtypes = []
+        L.adaptcore_last_error.restype = ctypes.c_char_p
+        L.adaptcore_last_status.argtypes = []
+        L.adaptcore_last_status.restype = i32
+        L.adaptcore_taxonomy.argtypes = [ctypes.POINTER(TaxIn), ctypes.POINTER(TaxOut)]
+        L.adaptcore_taxonomy.restype = i32
+        L.adaptcore_schedule.argtypes = [i32, i64, i64, d, d, d]
+        L.adaptcore_schedule.restype = d
+        _lib = L
+    return _lib
+
+
+def adaptcore_last_error():
+    return lib().adaptcore_last_error().decode()
+
+
+last_error = adaptcore_last_error
+
+
+def adaptcore_last_status():
+    return lib().adaptcore_last_status()
+
+
+def _check(status):
+    if status != AC_OK:
+        raise AdaptCoreError(status, last_error())
+    return status
+
+
+def adaptcore_init():
+    return _check(lib().adaptcore_init())
+
+
+def adaptcore_plan(M, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):
+    """Cached plan handle (int) for the shape."""
+    h = lib().adaptcore_plan(M, N, K, dtype, layouts)
+    if not h:
+        raise AdaptCoreError(adaptcore_last_status(), last_error())
+    return h
+
+
+def adaptcore_plan_variant(M, N, K, dtype, layouts, variant_key):
+    h = lib().adaptcore_plan_variant(M, N, K, dtype, layouts, variant_key)
+    if not h:
+        raise AdaptCoreError(adaptcore_last_status(), last_error())
+    return h
+
+
+def adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream=0):
+    """C = A * B on `stream`; A, B, C are device addresses (ints)."""
+    return _check(lib().adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream))
+
+
+def adaptcore_reserve_workspace(stream, nbytes):
+    return _check(lib().adaptcore_reserve_workspace(stream, nbytes))
+
+
+def adaptcore_plan_info(plan):
+    d = PlanDesc()
+    _check(lib().adaptcore_plan_info(plan, ctypes.byref(d)))
+    return d.as_dict()
+
+
+def adaptcore_candidates(M, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):
+    n = lib().adaptcore_candidates(M, N, K, dtype, layouts, None, 0)
+    if n < 0:
+        raise AdaptCoreError(n, last_error())
+    arr = (Candidate * max(n, 1))()
+    lib().adaptcore_candidates(M, N, K, dtype, layouts, arr, n)
+    return [arr[i].as_dict() for i in range(n)]
+
+
+def adaptcore_get_hw():
+    h = Hw()
+    _check(lib().adaptcore_get_hw(ctypes.byref(h)))
+    return h
+
+
+def adaptcore_set_hw(h):
+    return _check(lib().adaptcore_set_hw(ctypes.byref(h)))
+
+
+def adaptcore_stats():
+    s = Stats()
+    _check(lib().adaptcore_stats(ctypes.byref(s)))
+    d = {f: getattr(s, f) for f, _ in Stats._fields_ if f != "class_count"}
+    d["class_count"] = list(s.class_count)
+    return d
+
+
+def adaptcore_cache_clear():
+    return _check(lib().adaptcore_cache_clear())
+
+
+def adaptcore_bench_lookup(n_keys, n_lookups):
+    out = ctypes.c_double()
+    _check(lib().adaptcore_bench_lookup(n_keys, n_lookups, ctypes.byref(out)))
+    return out.value
+
+
+def adaptcore_taxonomy(M, N, K, m, n, k, m1, n1, k1, n_core, s_acc, elem_bytes=2, out_bytes=2):
+    i = TaxIn(M, N, K, m, n, k, m1, n1, k1, n_core, s_acc, elem_bytes, out_bytes)
+    o = TaxOut()
+    _check(lib().adaptcore_taxonomy(ctypes.byref(i), ctypes.byref(o)))
+    return {"pm": o.pm, "pn": o.pn, "pk": o.pk, "cls": CLASS_NAMES[o.cls], "acc_bytes": o.acc_bytes,
+            "read_bytes": o.read_bytes, "write_bytes": o.write_bytes}
+
+
+def adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain):
+    return lib().adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain)
+
+
+def matmul_tensors(A, B, C, stream=None, plan=None):
+    """C = A @ B for torch tensors on the GPU (2-D, row-major rows: stride(1)
+    == 1). A and B are torch.bfloat16, C torch.float32 or torch.bfloat16.
+    Marshals pointers and leading dimensions; all arithmetic runs in the
+    library's kernels."""
+    import torch
+    M, K = A.shape
+    K2, N = B.shape
+    if K2 != K or tuple(C.shape) != (M, N):
+        raise ValueError("shape mismatch")
+    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16:
+        raise TypeError("A and B must be bfloat16")
+    if C.dtype == torch.float32:
+        dt = AC_BF16_F32OUT
+    elif C.dtype == torch.bfloat16:
+        dt = AC_BF16_BF16OUT
+    else:
+        raise TypeError("C must be float32 or bfloat16")
+    for t in (A, B, C):
+        if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1) or not t.is_cuda:
+            raise ValueError("operands must be 2-D GPU tensors with unit column stride")
+    if plan is None:
+        plan = adaptcore_plan(M, N, K, dt, AC_LAYOUT_ROW_ROW)
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    adaptcore_matmul(plan, A.data_ptr(), max(A.stride(0), 1), B.data_ptr(), max(B.stride(0), 1),
+                     C.data_ptr(), max(C.stride(0), 1), s)
+    return C

@@ -1,0 +1,510 @@
+// C ABI: validation, the plan cache (O(1) online dispatch, Section 3.1),
+// per-stream workspaces and the launch.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/adaptcore.h"
+#include "planner.h"
+#include "registry.h"
+
+struct adaptcore_plan_s {
+  ac::Plan p;
+};
+
+namespace {
+
+thread_local std::string t_err;
+thread_local adaptcore_status t_status = AC_OK;
+
+adaptcore_status fail(adaptcore_status st, const std::string& msg) {
+  t_err = msg;
+  t_status = st;
+  return st;
+}
+
+std::mutex g_mu;  // planning, cache inserts, profile changes
+adaptcore_hw_t g_hw = ac::default_hw();
+
+std::atomic<uint64_t> st_lookups{0}, st_hits{0}, st_misses{0}, st_launches{0}, st_entries{0};
+std::atomic<uint64_t> st_class[4];
+double st_miss_seconds = 0;  // under g_mu
+
+// ---- plan cache: open addressing, lock-free reads --------------------------
+// A slot's key is published (release) after its plan pointer, so a reader that
+// sees the key also sees the plan. The table only grows; replaced tables stay
+// alive until adaptcore_cache_clear so concurrent readers never touch freed
+// memory.
+struct Slot {
+  std::atomic<uint64_t> key{0};  // shape key + 1; 0 = empty
+  std::atomic<adaptcore_plan_s*> plan{nullptr};
+};
+struct Table {
+  size_t cap;
+  size_t used = 0;
+  Slot* slots;
+  explicit Table(size_t c) : cap(c), slots(new Slot[c]) {}
+  ~Table() { delete[] slots; }
+};
+std::atomic<Table*> g_tab{nullptr};
+std::vector<Table*> g_retired;
+std::vector<adaptcore_plan_s*> g_owned;
+std::map<std::tuple<int64_t, int64_t, int64_t, int, uint32_t>, adaptcore_plan_s*> g_big;  // dims >= 2^17
+std::map<std::pair<std::tuple<int64_t, int64_t, int64_t, int, uint32_t>, uint64_t>, adaptcore_plan_s*> g_forced;
+
+inline uint64_t mix(uint64_t x) {
+  x ^= x >> 33;
+  x *= 0xff51afd7ed558ccdull;
+  x ^= x >> 33;
+  x *= 0xc4ceb9fe1a85ec53ull;
+  x ^= x >> 33;
+  return x;
+}
+
+inline adaptcore_plan_s* table_find(const Table* t, uint64_t k) {
+  if (!t) return nullptr;
+  const size_t m = t->cap - 1;
+  for (size_t i = mix(k) & m;; i = (i + 1) & m) {
+    const uint64_t s = t->slots[i].key.load(std::memory_order_acquire);
+    if (s == k) return t->slots[i].plan.load(std::memory_order_acquire);
+    if (s == 0) return nullptr;
+  }
+}
+
+void table_put(Table* t, uint64_t k, adaptcore_plan_s* p) {
+  const size_t m = t->cap - 1;
+  for (size_t i = mix(k) & m;; i = (i + 1) & m) {
+    if (t->slots[i].key.load(std::memory_order_relaxed) == 0) {
+      t->slots[i].plan.store(p, std::memory_order_relaxed);
+      t->slots[i].key.store(k, std::memory_order_release);
+      ++t->used;
+      return;
+    }
+  }
+}
+
+// Under g_mu.
+void cache_insert(uint64_t k, adaptcore_plan_s* p) {
+  Table* t = g_tab.load(std::memory_order_relaxed);
+  if (!t) {
+    t = new Table(1024);
+    g_tab.store(t, std::memory_order_release);
+  }
+  if ((t->used + 1) * 2 > t->cap) {
+    Table* n = new Table(t->cap * 2);
+    for (size_t i = 0; i < t->cap; ++i) {
+      const uint64_t kk = t->slots[i].key.load(std::memory_order_relaxed);
+      if (kk) table_put(n, kk, t->slots[i].plan.load(std::memory_order_relaxed));
+    }
+    g_tab.store(n, std::memory_order_release);
+    g_retired.push_back(t);
+    t = n;
+  }
+  table_put(t, k, p);
+}
+
+bool valid_args(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts, adaptcore_status* st) {
+  const int64_t lim = (1LL << 31) - 1;
+  if (M < 0 || N < 0 || K < 0 || M > lim || N > lim || K > lim) {
+    *st = fail(AC_ERR_INVALID_VALUE, "dimensions must be in [0, 2^31)");
+    return false;
+  }
+  if (dtype != AC_BF16_F32OUT && dtype != AC_BF16_BF16OUT) {
+    *st = fail(AC_ERR_UNSUPPORTED, "dtype not provided by this build (bf16 inputs with fp32 or bf16 output)");
+    return false;
+  }
+  if (layouts != AC_LAYOUT_ROW_ROW) {
+    *st = fail(AC_ERR_UNSUPPORTED, "layout not provided by this build (row-major A and B)");
+    return false;
+  }
+  return true;
+}
+
+adaptcore_plan_s* plan_miss(const ac::Shape& s) {
+  const auto t0 = std::chrono::steady_clock::now();
+  int cls = 0;
+  std::vector<ac::Plan> c = ac::enumerate(s, g_hw, &cls);
+  if (c.empty()) return nullptr;
+  auto* p = new adaptcore_plan_s{c.front()};
+  bool exact;
+  p->p.shape_key = ac::shape_key(s, &exact);
+  g_owned.push_back(p);
+  st_miss_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  st_misses.fetch_add(1, std::memory_order_relaxed);
+  st_class[cls & 3].fetch_add(1, std::memory_order_relaxed);
+  st_entries.fetch_add(1, std::memory_order_relaxed);
+  return p;
+}
+
+inline const adaptcore_plan_s* lookup(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts) {
+  st_lookups.fetch_add(1, std::memory_order_relaxed);
+  const ac::Shape s{M, N, K, dtype, layouts};
+  bool exact;
+  const uint64_t key = ac::shape_key(s, &exact);
+  if (exact) {
+    if (adaptcore_plan_s* p = table_find(g_tab.load(std::memory_order_acquire), key + 1)) {
+      st_hits.fetch_add(1, std::memory_order_relaxed);
+      return p;
+    }
+  }
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (exact) {
+    if (adaptcore_plan_s* p = table_find(g_tab.load(std::memory_order_acquire), key + 1)) {
+      st_hits.fetch_add(1, std::memory_order_relaxed);
+      return p;
+    }
+  } else {
+    auto it = g_big.find(std::make_tuple(M, N, K, (int)dtype, layouts));
+    if (it != g_big.end()) {
+      st_hits.fetch_add(1, std::memory_order_relaxed);
+      return it->second;
+    }
+  }
+  adaptcore_plan_s* p = plan_miss(s);
+  if (!p) {
+    fail(AC_ERR_INTERNAL, "no legal configuration for the shape");
+    return nullptr;
+  }
+  if (exact)
+    cache_insert(key + 1, p);
+  else
+    g_big[std::make_tuple(M, N, K, (int)dtype, layouts)] = p;
+  return p;
+}
+
+// ---- device and workspaces ------------------------------------------------
+constexpr int64_t kCounterInts = 1 << 16;            // per-tile counters; the last is the error flag
+constexpr int64_t kCounterBytes = kCounterInts * 4;  // fixed region at the start of a workspace
+
+struct Workspace {
+  char* ptr = nullptr;
+  int64_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, void*>, Workspace> g_ws;
+std::once_flag g_init_once;
+adaptcore_status g_init_status = AC_ERR_NOT_INITIALIZED;
+std::string g_init_msg;
+
+adaptcore_status do_init() {
+  int dev = 0, n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) {
+    g_init_msg = "no HIP device";
+    return AC_ERR_NOT_INITIALIZED;
+  }
+  if (hipGetDevice(&dev) != hipSuccess) {
+    g_init_msg = "hipGetDevice failed";
+    return AC_ERR_NOT_INITIALIZED;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+    g_init_msg = "hipGetDeviceProperties failed";
+    return AC_ERR_NOT_INITIALIZED;
+  }
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+    g_init_msg = std::string("kernels are built for gfx950, device is ") + prop.gcnArchName;
+    return AC_ERR_UNSUPPORTED;
+  }
+  ac::query_occupancy();
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (g_hw.n_cu != prop.multiProcessorCount) {
+    g_hw.n_cu = prop.multiProcessorCount;
+  }
+  return AC_OK;
+}
+
+adaptcore_status ensure_init() {
+  std::call_once(g_init_once, [] { g_init_status = do_init(); });
+  if (g_init_status != AC_OK) return fail(g_init_status, g_init_msg);
+  return AC_OK;
+}
+
+// Workspace of (current device, stream) with at least `need` bytes beyond the
+// counter region; allocates outside stream capture only.
+adaptcore_status get_workspace(hipStream_t stream, int64_t need, Workspace* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(AC_ERR_NOT_INITIALIZED, "hipGetDevice failed");
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace& w = g_ws[std::make_pair(dev, (void*)stream)];
+  const int64_t total = kCounterBytes + need;
+  if (w.ptr && w.bytes >= total) {
+    *out = w;
+    return AC_OK;
+  }
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
+    return fail(AC_ERR_NOT_INITIALIZED,
+                "split-K workspace missing for this stream under capture: call adaptcore_reserve_workspace first");
+  const int64_t grow = std::max<int64_t>(total, w.bytes + w.bytes / 2);
+  if (w.ptr) {
+    (void)hipStreamSynchronize(stream);  // kernels in flight may still use the old buffer
+    (void)hipFree(w.ptr);
+    w.ptr = nullptr;
+    w.bytes = 0;
+  }
+  void* p = nullptr;
+  if (hipMalloc(&p, (size_t)grow) != hipSuccess) return fail(AC_ERR_OUT_OF_MEMORY, "workspace allocation failed");
+  // counters start at zero; every kernel that uses one restores it to zero
+  if (hipMemsetAsync(p, 0, (size_t)kCounterBytes, stream) != hipSuccess || hipStreamSynchronize(stream) != hipSuccess) {
+    (void)hipFree(p);
+    return fail(AC_ERR_LAUNCH, "workspace initialisation failed");
+  }
+  w.ptr = static_cast<char*>(p);
+  w.bytes = grow;
+  *out = w;
+  return AC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+adaptcore_status adaptcore_init(void) { return ensure_init(); }
+
+const adaptcore_plan_t* adaptcore_plan(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts) {
+  adaptcore_status st;
+  if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  return lookup(M, N, K, dtype, layouts);
+}
+
+const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts,
+                                               uint64_t variant_key) {
+  adaptcore_status st;
+  if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  const auto tk = std::make_tuple(M, N, K, (int)dtype, layouts);
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_forced.find(std::make_pair(tk, variant_key));
+  if (it != g_forced.end()) return it->second;
+  ac::Plan p;
+  const ac::Shape s{M, N, K, dtype, layouts};
+  if (!ac::plan_for_key(s, g_hw, variant_key, &p)) {
+    fail(AC_ERR_INVALID_VALUE, "variant key is not legal for this shape");
+    return nullptr;
+  }
+  bool exact;
+  p.shape_key = ac::shape_key(s, &exact);
+  auto* pp = new adaptcore_plan_s{p};
+  g_owned.push_back(pp);
+  g_forced[std::make_pair(tk, variant_key)] = pp;
+  return pp;
+}
+
+adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes) {
+  if (bytes < 0) return fail(AC_ERR_INVALID_VALUE, "negative workspace size");
+  adaptcore_status st = ensure_init();
+  if (st != AC_OK) return st;
+  Workspace w;
+  return get_workspace(static_cast<hipStream_t>(stream), bytes, &w);
+}
+
+adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
+                                  void* C, int64_t ldc, void* stream) {
+  if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
+  const ac::Plan& p = plan->p;
+  const int64_t M = p.s.M, N = p.s.N, K = p.s.K;
+  if (M == 0 || N == 0) return AC_OK;
+  if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
+    return fail(AC_ERR_INVALID_VALUE, "leading dimension smaller than the row length");
+  if (!C || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null matrix pointer");
+  const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
+  if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)))
+    return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
+  adaptcore_status st = ensure_init();
+  if (st != AC_OK) return st;
+  if (p.family == ac::FAM_STREAMK && p.grid_x > g_hw.n_cu * ac::occupancy(ac::FAM_STREAMK, p.cfg))
+    return fail(AC_ERR_INVALID_VALUE, "stream-K grid exceeds the resident workgroups of this device");
+  if (p.n_counters >= kCounterInts) return fail(AC_ERR_INTERNAL, "plan needs more tile counters than reserved");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  ac::GemmArgs g;
+  std::memset(&g, 0, sizeof g);
+  g.A = static_cast<const uint16_t*>(A);
+  g.B = static_cast<const uint16_t*>(B);
+  g.C = C;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.pk = p.family == ac::FAM_STREAMK ? p.ws_pk : p.pk;
+  g.kper = p.kper;
+  g.tiles_m = p.pm;
+  g.tiles_n = p.pn;
+  g.swizzle = p.swizzle;
+  g.iters_per_wg = p.iters_per_wg;
+  g.sk_tiles = p.sk_tiles;
+  g.spin_limit = 1 << 22;
+  if (p.ws_bytes > 0) {
+    Workspace w;
+    st = get_workspace(s, p.ws_bytes, &w);
+    if (st != AC_OK) return st;
+    g.counters = reinterpret_cast<int*>(w.ptr);
+    g.err_flag = g.counters + (kCounterInts - 1);
+    g.ws = reinterpret_cast<float*>(w.ptr + kCounterBytes);
+  }
+  const hipError_t e = ac::launch_plan(p, g, s);
+  if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  st_launches.fetch_add(1, std::memory_order_relaxed);
+  return AC_OK;
+}
+
+adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out) {
+  if (!plan || !out) return fail(AC_ERR_INVALID_VALUE, "null argument");
+  const ac::Plan& p = plan->p;
+  std::memset(out, 0, sizeof *out);
+  out->M = p.s.M;
+  out->N = p.s.N;
+  out->K = p.s.K;
+  out->dtype = p.s.dtype;
+  out->layouts = p.s.layouts;
+  out->shape_key = p.shape_key;
+  out->variant_key = p.variant_key;
+  out->cls = p.cls;
+  out->family = p.family;
+  out->tile_m = p.tile_m;
+  out->tile_n = p.tile_n;
+  out->tile_k = p.tile_k;
+  out->pm = p.pm;
+  out->pn = p.pn;
+  out->pk = p.family == ac::FAM_STREAMK ? p.ws_pk : p.pk;
+  out->grid_x = p.grid_x;
+  out->grid_y = p.grid_y;
+  out->swizzle = p.swizzle;
+  out->n_candidates = p.n_candidates;
+  out->predicted_s = p.predicted;
+  out->workspace_bytes = p.ws_bytes > 0 ? p.ws_bytes + kCounterBytes : 0;
+  return AC_OK;
+}
+
+int64_t adaptcore_candidates(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts,
+                             adaptcore_candidate_t* out, int64_t cap) {
+  adaptcore_status st;
+  if (!valid_args(M, N, K, dtype, layouts, &st)) return st;
+  adaptcore_hw_t hw;
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    hw = g_hw;
+  }
+  const ac::Shape s{M, N, K, dtype, layouts};
+  std::vector<ac::Plan> c = ac::enumerate(s, hw, nullptr);
+  for (int64_t i = 0; i < (int64_t)c.size() && i < cap && out; ++i) {
+    const ac::Plan& p = c[i];
+    adaptcore_candidate_t& o = out[i];
+    o.variant_key = p.variant_key;
+    o.cls = p.cls;
+    o.family = p.family;
+    o.tile_m = p.tile_m;
+    o.tile_n = p.tile_n;
+    o.tile_k = p.tile_k;
+    o.pk = p.family == ac::FAM_STREAMK ? p.ws_pk : p.pk;
+    o.grid_x = p.grid_x;
+    o.grid_y = p.grid_y;
+    o.predicted_s = p.predicted;
+  }
+  return (int64_t)c.size();
+}
+
+adaptcore_status adaptcore_get_hw(adaptcore_hw_t* out) {
+  if (!out) return fail(AC_ERR_INVALID_VALUE, "null argument");
+  std::lock_guard<std::mutex> lk(g_mu);
+  *out = g_hw;
+  return AC_OK;
+}
+
+adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw) {
+  if (!hw) return fail(AC_ERR_INVALID_VALUE, "null argument");
+  if (hw->n_cu <= 0 || hw->lds_bytes <= 0 || hw->s_acc_bytes <= 0 || !(hw->clock_hz > 0) || !(hw->hbm_bw > 0) ||
+      !(hw->hbm_eta > 0) || !(hw->l2_bw_cu > 0) || !(hw->mfma_eta > 0) || !(hw->lds_bw_cu > 0) ||
+      !(hw->unaligned_eta > 0) || hw->l2_hit < 0 || hw->l2_hit > 1 || hw->t_launch < 0 || hw->t_mem_latency < 0 ||
+      hw->t_wg < 0)
+    return fail(AC_ERR_INVALID_VALUE, "profile field out of range");
+  adaptcore_cache_clear();
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_hw = *hw;
+  return AC_OK;
+}
+
+adaptcore_status adaptcore_stats(adaptcore_stats_t* out) {
+  if (!out) return fail(AC_ERR_INVALID_VALUE, "null argument");
+  std::memset(out, 0, sizeof *out);
+  out->lookups = st_lookups.load();
+  out->hits = st_hits.load();
+  out->misses = st_misses.load();
+  out->entries = st_entries.load();
+  out->launches = st_launches.load();
+  for (int i = 0; i < 4; ++i) out->class_count[i] = st_class[i].load();
+  std::lock_guard<std::mutex> lk(g_mu);
+  out->miss_seconds = st_miss_seconds;
+  return AC_OK;
+}
+
+adaptcore_status adaptcore_cache_clear(void) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  Table* t = g_tab.exchange(nullptr);
+  delete t;
+  for (Table* r : g_retired) delete r;
+  g_retired.clear();
+  for (adaptcore_plan_s* p : g_owned) delete p;
+  g_owned.clear();
+  g_big.clear();
+  g_forced.clear();
+  st_entries.store(0);
+  return AC_OK;
+}
+
+adaptcore_status adaptcore_bench_lookup(int64_t n_keys, int64_t n_lookups, double* ns_per_lookup) {
+  if (n_keys <= 0 || n_lookups <= 0 || !ns_per_lookup) return fail(AC_ERR_INVALID_VALUE, "bad argument");
+  std::vector<std::tuple<int64_t, int64_t, int64_t>> keys;
+  keys.reserve((size_t)n_keys);
+  uint64_t x = 0x2545F4914F6CDD1Dull;
+  for (int64_t i = 0; i < n_keys; ++i) {
+    x ^= x << 13;
+    x ^= x >> 7;
+    x ^= x << 17;
+    keys.emplace_back(1 + (int64_t)(x % 1000), 1 + (int64_t)((x >> 20) % 1000), 1 + (int64_t)((x >> 40) % 1000));
+  }
+  for (auto& k : keys)
+    if (!lookup(std::get<0>(k), std::get<1>(k), std::get<2>(k), AC_BF16_BF16OUT, 0)) return AC_ERR_INTERNAL;
+  const int64_t batch = std::max<int64_t>(1, std::min<int64_t>(n_lookups, 1000));
+  std::vector<double> per;
+  uintptr_t sink = 0;
+  for (int64_t done = 0, i = 0; done < n_lookups; done += batch) {
+    const auto t0 = std::chrono::steady_clock::now();
+    for (int64_t j = 0; j < batch; ++j, i = (i + 1) % n_keys) {
+      auto& k = keys[(size_t)i];
+      sink += (uintptr_t)lookup(std::get<0>(k), std::get<1>(k), std::get<2>(k), AC_BF16_BF16OUT, 0);
+    }
+    per.push_back(std::chrono::duration<double, std::nano>(std::chrono::steady_clock::now() - t0).count() / batch);
+  }
+  std::sort(per.begin(), per.end());
+  *ns_per_lookup = per[per.size() / 2] + (sink == 1 ? 1e-9 : 0.0);
+  return AC_OK;
+}
+
+const char* adaptcore_last_error(void) { return t_err.c_str(); }
+
+adaptcore_status adaptcore_last_status(void) { return t_status; }
+
+adaptcore_status adaptcore_taxonomy(const adaptcore_taxonomy_in_t* in, adaptcore_taxonomy_out_t* out) {
+  if (!in || !out) return fail(AC_ERR_INVALID_VALUE, "null argument");
+  if (in->M <= 0 || in->N <= 0 || in->K <= 0 || in->m <= 0 || in->n <= 0 || in->k <= 0 || in->m1 <= 0 ||
+      in->n1 <= 0 || in->k1 <= 0 || in->n_core <= 0 || in->s_acc <= 0)
+    return fail(AC_ERR_INVALID_VALUE, "taxonomy parameters must be positive");
+  ac::taxonomy(*in, out);
+  return AC_OK;
+}
+
+double adaptcore_schedule(int32_t kind, int64_t Q, int64_t L, double t_m, double t_p, double t_drain) {
+  return ac::schedule(kind, Q, L, t_m, t_p, t_drain);
+}
+
+}  // extern "C"

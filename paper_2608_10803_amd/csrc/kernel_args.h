@@ -1,0 +1,38 @@
+// Launch arguments shared by the host dispatcher and the gfx950 kernels.
+#pragma once
+#include <stdint.h>
+
+namespace ac {
+
+// Kernel families of the variant space.
+enum Family : int {
+  FAM_TILE = 0,      // MFMA macro-tile kernel; P_k == 1 is the Common template,
+                     // P_k > 1 the MultiCoreSplitK template (Section 4.2)
+  FAM_SKINNY_M = 1,  // Small-M Copy module: B streamed once, M <= 64
+  FAM_SKINNY_N = 2,  // the same module by orientation: A streamed once, N <= 64
+  FAM_STREAMK = 3,   // StreamK applied to the tile kernel (Section 4.2)
+  FAM_COUNT = 4
+};
+
+// Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N
+// row-major (ldb), C is M x N row-major (ldc); 16-bit inputs as raw bits.
+struct GemmArgs {
+  const uint16_t* A;
+  const uint16_t* B;
+  void* C;
+  int64_t M, N, K;
+  int64_t lda, ldb, ldc;
+  float* ws;         // fp32 partial tiles of split-K / stream-K (may be null)
+  int* counters;     // per-tile arrival counters, zero between launches
+  int pk;            // K partitions (1 = no split)
+  int kper;          // k-blocks per partition (block = kernel's k granule)
+  int tiles_m;       // output tiles along M of this kernel's tiling
+  int tiles_n;       // output tiles along N
+  int swizzle;       // 1 = XCD-aware, grouped tile order
+  int iters_per_wg;  // stream-K: MAC iterations per persistent workgroup
+  int sk_tiles;      // stream-K: tiles handled by the stream-K phase
+  int spin_limit;    // stream-K: bound on fix-up waits (then error flag)
+  int* err_flag;     // stream-K: set to 1 when a wait hit its bound
+};
+
+}  // namespace ac

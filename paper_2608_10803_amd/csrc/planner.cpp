@@ -1,0 +1,589 @@
+// Planner: taxonomy (Section 4.2 / 4.3), candidate enumeration and legality
+// (Eq. 6), and the analytical latency model (Section 5.2, Eqs. 7-13) with
+// MI355X stage costs.
+#include "planner.h"
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstring>
+
+namespace ac {
+
+namespace {
+
+std::atomic<int> g_occ[FAM_COUNT][16];
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int table_occ(int family, int cfg) {
+  switch (family) {
+    case FAM_TILE:
+    case FAM_STREAMK:
+      return kTileCfg[cfg].occ;
+    case FAM_SKINNY_M:
+      return kSkinnyMCfg[cfg].occ;
+    case FAM_SKINNY_N:
+      return kSkinnyNCfg[cfg].occ;
+  }
+  return 1;
+}
+
+int out_bytes(int dtype) { return dtype == AC_BF16_F32OUT ? 4 : 2; }
+
+// Tiles the taxonomy uses for its spatial predicate: the menu entries whose
+// accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
+// first. Smaller menu tiles remain candidates of the search.
+const int kBaseTiles[] = {0, 1, 2, 3};
+
+// Work of one candidate, in the terms of Eqs. 8-13.
+struct Work {
+  int64_t units = 0;     // workgroups
+  int occ = 1;           // workgroups per CU
+  double L = 0;          // main-loop iterations of the longest workgroup
+  double bytes_it = 0;   // global bytes loaded per iteration by one workgroup
+  double mfma_it = 0;    // MFMA cycles per iteration on each SIMD
+  double lds_it = 0;     // LDS bytes per iteration of one workgroup
+  double out_unit = 0;   // bytes a workgroup writes at the end (tile or partial)
+  double epi = 0;        // bytes read by the cross-workgroup reduction (Eq. 11)
+  double epi_out = 0;    // final output bytes written by the reducing workgroup
+  double setup = 0;      // bytes a workgroup stages before its main loop
+  double prefetch = 1;   // main-loop iterations of loads in flight
+  double total_read = 0; // sum over workgroups of bytes read (Eq. 1 analogue)
+  bool unaligned = false;
+};
+
+// Eq. 8 with shared bandwidth: per-workgroup share of HBM (compulsory
+// traffic) and of the CU's cache bandwidth (re-reads), and the Eq. 13
+// double-buffered schedule, summed over rounds of resident workgroups (Eq. 7:
+// the slowest CU decides; wave quantisation is the number of rounds).
+double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, double compulsory) {
+  if (w.units <= 0) return hw.t_launch;
+  const double slots = (double)hw.n_cu * std::max(1, w.occ);
+  const double eta = hw.hbm_eta * (w.unaligned ? hw.unaligned_eta : 1.0);
+  const double agg_hbm = hw.hbm_bw * eta;
+  // fraction of loaded bytes that come from HBM (the rest hits L2 / MALL)
+  double hbm_frac = 1.0;
+  if (w.total_read > compulsory && w.total_read > 0) {
+    const double hbm = compulsory + (w.total_read - compulsory) * (1.0 - hw.l2_hit);
+    hbm_frac = std::min(1.0, hbm / w.total_read);
+  }
+  auto unit_time = [&](double conc) {
+    const double per_cu = std::ceil(conc / hw.n_cu);
+    const double bw_hbm = std::min(agg_hbm / conc, hw.l2_bw_cu / per_cu);
+    const double bw_l2 = hw.l2_bw_cu / per_cu;
+    double tM = w.bytes_it * hbm_frac / bw_hbm + w.bytes_it * (1.0 - hbm_frac) / bw_l2;
+    tM = std::max(tM, hw.t_mem_latency / w.prefetch);
+    const double tP = std::max(w.mfma_it * per_cu / (hw.clock_hz * hw.mfma_eta), w.lds_it * per_cu / hw.lds_bw_cu);
+    const double t_fill = hw.t_mem_latency + tM + tP;  // first slice: load latency, load, compute
+    const double t_drain = w.out_unit / bw_hbm;
+    const double t_setup = w.setup > 0 ? hw.t_mem_latency + w.setup / bw_l2 : 0.0;
+    const double L = std::max(0.0, w.L);
+    if (L == 0) return hw.t_wg + t_setup + t_drain;
+    return hw.t_wg + t_setup + t_fill + (L - 1) * std::max(tM, tP) + t_drain;  // Eq. 13
+  };
+  const int64_t full = (int64_t)(w.units / slots);
+  const double rem = (double)w.units - full * slots;
+  double t_main = full * unit_time(slots);
+  if (rem > 0) t_main += unit_time(rem);
+  // aggregate HBM roof over the whole launch
+  const double hbm_bytes = compulsory + (w.total_read - std::min(w.total_read, compulsory)) * (1.0 - hw.l2_hit);
+  t_main = std::max(t_main, hbm_bytes / agg_hbm);
+  // cross-workgroup reduction of split-K (Eq. 11): the last arrival reads the
+  // partials (cache-resident) and writes the output
+  double t_epi = 0;
+  if (w.epi > 0) t_epi = hw.t_mem_latency + w.epi / hw.l2_bw_cu + w.epi_out / hw.l2_bw_cu;
+  (void)s;
+  return hw.t_launch + t_main + t_epi;  // Eq. 7 (T_pro = 0)
+}
+
+struct Ctx {
+  const Shape& s;
+  const adaptcore_hw_t& hw;
+  double compulsory;
+  int cbytes;
+  bool unaligned;
+};
+
+bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w) {
+  const TileCfg& t = kTileCfg[cfg];
+  const Shape& s = c.s;
+  const int64_t tm = cdiv(s.M, t.bm), tn = cdiv(s.N, t.bn);
+  const int64_t kt = cdiv(s.K, TILE_BK);
+  if (tm * tn > (1LL << 31) - 1) return false;
+  if (tile_lds_bytes(t) > c.hw.lds_bytes) return false;
+  int64_t pk = 1, kper = kt;
+  if (pk_req > 1) {
+    if (kt < 2) return false;
+    kper = cdiv(kt, pk_req);
+    pk = cdiv(kt, kper);
+    if (pk != pk_req) return false;  // an equivalent key with the effective P_k exists
+    if (pk > 65535) return false;
+  }
+  p->family = FAM_TILE;
+  p->cfg = cfg;
+  p->swizzle = swizzle;
+  p->tile_m = t.bm;
+  p->tile_n = t.bn;
+  p->tile_k = TILE_BK;
+  p->pm = (int)tm;
+  p->pn = (int)tn;
+  p->pk = (int)pk;
+  p->kper = (int)std::max<int64_t>(kper, 0);
+  p->grid_x = (int)(tm * tn);
+  p->grid_y = (int)pk;
+  if (pk > 1) {
+    p->ws_pk = (int)pk;
+    p->n_counters = (int)(tm * tn);
+    p->ws_bytes = (int64_t)tm * tn * pk * t.bm * t.bn * 4;
+  }
+  const int ks = t.ms == 32 ? 16 : 32, cyc = t.ms == 32 ? 32 : 16;
+  const int TM = t.bm / 2 / t.ms, TN = t.bn / 2 / t.ms;
+  const double bm_e = (double)s.M / tm, bn_e = (double)s.N / tn;
+  w->units = tm * tn * pk;
+  w->occ = occupancy(FAM_TILE, cfg);
+  w->L = (double)kper;
+  w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
+  w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
+  w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (t.bm + t.bn) * TILE_BK * 2;
+  w->out_unit = pk == 1 ? bm_e * bn_e * c.cbytes : (double)t.bm * t.bn * 4;
+  if (pk > 1) {
+    w->epi = (double)pk * t.bm * t.bn * 4;
+    w->epi_out = bm_e * bn_e * c.cbytes;
+  }
+  w->prefetch = 1;
+  w->total_read = (double)tm * tn * (bm_e + bn_e) * (double)s.K * 2;
+  w->unaligned = c.unaligned;
+  return true;
+}
+
+bool build_skinny_m(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
+  const SkinnyMCfg& k = kSkinnyMCfg[cfg];
+  const Shape& s = c.s;
+  if (s.M > 16 * k.mt) return false;
+  if (k.mt > 1 && s.M <= 16 * (k.mt / 2)) return false;  // a smaller row count fits
+  const int NB = skinny_m_cols(k);
+  const int64_t cb = cdiv(s.N, NB);
+  const int64_t kb = cdiv(s.K, SKINNY_BK);
+  int64_t pk = 1, kper = kb;
+  if (pk_req > 1) {
+    if (kb < 2) return false;
+    kper = cdiv(kb, pk_req);
+    pk = cdiv(kb, kper);
+    if (pk != pk_req || pk > 65535) return false;
+  }
+  if (cb > (1LL << 31) - 1) return false;
+  p->family = FAM_SKINNY_M;
+  p->cfg = cfg;
+  p->tile_m = 16 * k.mt;
+  p->tile_n = NB;
+  p->tile_k = SKINNY_BK;
+  p->pm = 1;
+  p->pn = (int)cb;
+  p->pk = (int)pk;
+  p->kper = (int)kper;
+  p->grid_x = (int)cb;
+  p->grid_y = (int)pk;
+  const double blk_floats = (4.0 / k.wkw) * k.mt * 8 * 64 * 4;
+  if (pk > 1) {
+    p->ws_pk = (int)pk;
+    p->n_counters = (int)cb;
+    p->ws_bytes = (int64_t)(cb * pk * blk_floats * 4);
+  }
+  const double nb_e = (double)s.N / cb;
+  w->units = cb * pk;
+  w->occ = occupancy(FAM_SKINNY_M, cfg);
+  w->L = std::ceil((double)kper / k.wkw);
+  w->bytes_it = 32.0 * k.wkw * nb_e * 2 + 4.0 * k.mt * 16 * 32 * 2;
+  w->mfma_it = 8.0 * k.mt * 16;
+  w->lds_it = 0;
+  w->out_unit = pk == 1 ? (double)s.M * nb_e * c.cbytes : blk_floats * 4;
+  if (pk > 1) {
+    w->epi = pk * blk_floats * 4;
+    w->epi_out = (double)s.M * nb_e * c.cbytes;
+  }
+  w->prefetch = 2;
+  w->total_read = 2.0 * s.K * s.N + 2.0 * s.M * s.K * cb;
+  w->unaligned = (s.N % 8) != 0;
+  return true;
+}
+
+bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
+  const SkinnyNCfg& k = kSkinnyNCfg[cfg];
+  const Shape& s = c.s;
+  if (s.N > 16 * k.nt) return false;
+  if (k.nt > 1 && s.N <= 16 * (k.nt / 2)) return false;
+  const int R = skinny_n_rows(k);
+  const int64_t rbk = cdiv(s.M, R);
+  const int64_t kb = cdiv(s.K, SKINNY_BK);
+  const int64_t kmax = SKINNY_N_KMAX / SKINNY_BK;
+  int64_t pk = 1, kper = kb;
+  if (pk_req > 1) {
+    if (kb < 2) return false;
+    kper = cdiv(kb, pk_req);
+    pk = cdiv(kb, kper);
+    if (pk != pk_req || pk > 65535) return false;
+  }
+  if (kper > kmax) return false;  // B^T slice must fit the LDS buffer
+  if (rbk > (1LL << 31) - 1) return false;
+  p->family = FAM_SKINNY_N;
+  p->cfg = cfg;
+  p->tile_m = R;
+  p->tile_n = 16 * k.nt;
+  p->tile_k = SKINNY_BK;
+  p->pm = (int)rbk;
+  p->pn = 1;
+  p->pk = (int)pk;
+  p->kper = (int)kper;
+  p->grid_x = (int)rbk;
+  p->grid_y = (int)pk;
+  const double blk_floats = 4.0 * k.rb * k.nt * 64 * 4;
+  if (pk > 1) {
+    p->ws_pk = (int)pk;
+    p->n_counters = (int)rbk;
+    p->ws_bytes = (int64_t)(rbk * pk * blk_floats * 4);
+  }
+  const double rows_e = (double)s.M / rbk;
+  w->units = rbk * pk;
+  w->occ = occupancy(FAM_SKINNY_N, cfg);
+  w->L = (double)kper;
+  w->bytes_it = rows_e * 32 * 2;
+  w->mfma_it = (double)k.rb * k.nt * 16;
+  w->lds_it = 64.0 * k.nt * 16 * 4;
+  w->setup = (double)kper * 32 * s.N * 2;
+  w->out_unit = pk == 1 ? rows_e * s.N * c.cbytes : blk_floats * 4;
+  if (pk > 1) {
+    w->epi = pk * blk_floats * 4;
+    w->epi_out = rows_e * s.N * c.cbytes;
+  }
+  w->prefetch = 2;
+  w->total_read = 2.0 * s.M * s.K + 2.0 * s.K * s.N * rbk;
+  w->unaligned = (s.K % 8) != 0;
+  return true;
+}
+
+// StreamK applied to the tile kernel: G persistent workgroups; the last
+// partial wave of tiles (plus one full wave when there are at least two) is
+// split evenly in MAC iterations, the rest runs data-parallel.
+bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
+  const TileCfg& t = kTileCfg[cfg];
+  const Shape& s = c.s;
+  const int64_t tm = cdiv(s.M, t.bm), tn = cdiv(s.N, t.bn);
+  const int64_t ntiles = tm * tn;
+  const int64_t ipt = cdiv(s.K, TILE_BK);
+  if (ipt < 2 || ntiles > (1LL << 30)) return false;
+  const int64_t G = (int64_t)c.hw.n_cu * occupancy(FAM_STREAMK, cfg);
+  int64_t sk;
+  if (ntiles >= G) {
+    sk = ntiles % G;
+    if (sk == 0) return false;  // a whole number of waves: data-parallel is already balanced
+    if (ntiles >= 2 * G) sk += G;
+  } else {
+    sk = ntiles;
+  }
+  const int64_t ipw = cdiv(sk * ipt, G);
+  const int64_t grid = std::min<int64_t>(G, std::max<int64_t>(cdiv(sk * ipt, ipw), 1));
+  p->family = FAM_STREAMK;
+  p->cfg = cfg;
+  p->swizzle = 0;
+  p->tile_m = t.bm;
+  p->tile_n = t.bn;
+  p->tile_k = TILE_BK;
+  p->pm = (int)tm;
+  p->pn = (int)tn;
+  p->pk = (int)G;  // key field: the persistent grid
+  p->kper = (int)ipt;
+  (void)grid;
+  p->grid_x = (int)G;
+  p->grid_y = 1;
+  p->iters_per_wg = (int)ipw;
+  p->sk_tiles = (int)sk;
+  p->ws_pk = (int)(cdiv(ipt, ipw) + 1);
+  p->n_counters = (int)sk;
+  p->ws_bytes = (int64_t)sk * p->ws_pk * t.bm * t.bn * 4;
+  const int ks = t.ms == 32 ? 16 : 32, cyc = t.ms == 32 ? 32 : 16;
+  const int TM = t.bm / 2 / t.ms, TN = t.bn / 2 / t.ms;
+  const double bm_e = (double)s.M / tm, bn_e = (double)s.N / tn;
+  w->units = G;
+  w->occ = occupancy(FAM_STREAMK, cfg);
+  w->L = (double)ipw + (double)((ntiles - sk) / G) * ipt;
+  w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
+  w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
+  w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (t.bm + t.bn) * TILE_BK * 2;
+  w->out_unit = 2.0 * t.bm * t.bn * 4 + (double)((ntiles - sk) / G) * bm_e * bn_e * c.cbytes;
+  w->epi = (double)p->ws_pk * t.bm * t.bn * 4;
+  w->epi_out = bm_e * bn_e * c.cbytes;
+  w->prefetch = 1;
+  w->total_read = (double)ntiles * (bm_e + bn_e) * (double)s.K * 2;
+  w->unaligned = c.unaligned;
+  return true;
+}
+
+const int kSplits[] = {2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32, 40, 48, 64, 80, 96, 128, 160, 192, 256, 384, 512, 768, 1024};
+
+bool finish(const Ctx& c, Plan* p, const Work& w) {
+  p->s = c.s;
+  p->predicted = model_time(c.s, w, c.hw, c.compulsory);
+  p->variant_key = make_variant_key(p->family, p->cfg, p->swizzle, p->pk, c.s.dtype, (int)c.s.layouts);
+  if (p->ws_bytes > (int64_t)2 << 30) return false;  // workspace cap
+  if (p->n_counters > 0) {
+    const int64_t fl = (p->ws_bytes + 255) / 256 * 256;
+    p->ws_bytes = fl + (int64_t)(p->n_counters + 1) * 4;
+  }
+  return true;
+}
+
+}  // namespace
+
+adaptcore_hw_t default_hw() {
+  adaptcore_hw_t h;
+  std::memset(&h, 0, sizeof h);
+  h.n_cu = 256;
+  h.lds_bytes = 160 * 1024;
+  h.s_acc_bytes = 256 * 1024;  // 4 waves x 64 lanes x 256 accumulation registers x 4 B
+  h.clock_hz = 2.4e9;
+  h.hbm_bw = 8.0e12;
+  h.hbm_eta = 0.80;
+  h.l2_bw_cu = 64.0 * 2.4e9;
+  h.t_launch = 2.0e-6;
+  h.t_mem_latency = 0.8e-6;
+  h.t_wg = 0.2e-6;
+  h.mfma_eta = 0.85;
+  h.lds_bw_cu = 128.0 * 2.4e9;
+  h.unaligned_eta = 0.85;
+  h.l2_hit = 0.7;
+  h.search_open = 0;
+  h.enable_streamk = 0;
+  return h;
+}
+
+void set_runtime_occupancy(int family, int cfg, int occ) {
+  if (family >= 0 && family < FAM_COUNT && cfg >= 0 && cfg < 16) g_occ[family][cfg].store(occ);
+}
+
+int occupancy(int family, int cfg) {
+  const int o = g_occ[family][cfg].load(std::memory_order_relaxed);
+  return o > 0 ? o : table_occ(family, cfg);
+}
+
+int classify_shape(const Shape& s, const adaptcore_hw_t& hw, int* base_cfg) {
+  int base = -1;
+  for (int cfg : kBaseTiles) {
+    const TileCfg& t = kTileCfg[cfg];
+    if (cdiv(s.M, t.bm) * cdiv(s.N, t.bn) >= hw.n_cu) {
+      base = cfg;
+      break;
+    }
+  }
+  bool spatial = base >= 0;
+  if (!spatial) base = kBaseTiles[sizeof(kBaseTiles) / sizeof(int) - 1];
+  if (base_cfg) *base_cfg = base;
+  const TileCfg& t = kTileCfg[base];
+  const bool onchip = (int64_t)t.bm * t.bn * 4 <= hw.s_acc_bytes;
+  if (spatial) return onchip ? AC_CLASS_COMMON : AC_CLASS_SINGLE_CORE_SPLITK;
+  return onchip ? AC_CLASS_MULTI_CORE_SPLITK : AC_CLASS_HYBRID_SPLITK;
+}
+
+static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
+  const Shape& s = c.s;
+  auto add = [&](Plan& p, Work& w) {
+    if (finish(c, &p, w)) out.push_back(p);
+  };
+  // tile kernel: every menu tile, P_k = 1 and the split counts
+  for (int cfg = 0; cfg < N_TILE_CFG; ++cfg) {
+    const TileCfg& t = kTileCfg[cfg];
+    // a tile more than twice the matrix in a dimension only adds padding
+    if ((t.bm > 2 * s.M && t.bm > 32) || (t.bn > 2 * s.N && t.bn > 32)) continue;
+    for (int sw = 0; sw < 2; ++sw) {
+      const int64_t ntiles = cdiv(s.M, t.bm) * cdiv(s.N, t.bn);
+      if (sw == 1 && ntiles < 16) continue;  // nothing to reorder
+      {
+        Plan p;
+        Work w;
+        if (build_tile(c, cfg, 1, sw, &p, &w)) add(p, w);
+      }
+      for (int pk : kSplits) {
+        if ((int64_t)pk * ntiles > 8LL * c.hw.n_cu * kTileCfg[cfg].occ) break;
+        Plan p;
+        Work w;
+        if (build_tile(c, cfg, pk, sw, &p, &w)) add(p, w);
+      }
+    }
+    if (c.hw.enable_streamk) {
+      Plan p;
+      Work w;
+      if (build_streamk(c, cfg, &p, &w)) add(p, w);
+    }
+  }
+  for (int cfg = 0; cfg < N_SKINNY_M_CFG; ++cfg) {
+    const int64_t cb = cdiv(s.N, skinny_m_cols(kSkinnyMCfg[cfg]));
+    {
+      Plan p;
+      Work w;
+      if (build_skinny_m(c, cfg, 1, &p, &w)) add(p, w);
+    }
+    for (int pk : kSplits) {
+      if ((int64_t)pk * cb > 8LL * c.hw.n_cu * kSkinnyMCfg[cfg].occ) break;
+      Plan p;
+      Work w;
+      if (build_skinny_m(c, cfg, pk, &p, &w)) add(p, w);
+    }
+  }
+  for (int cfg = 0; cfg < N_SKINNY_N_CFG; ++cfg) {
+    const int64_t rb = cdiv(s.M, skinny_n_rows(kSkinnyNCfg[cfg]));
+    const int64_t kb = cdiv(s.K, SKINNY_BK);
+    const int64_t min_pk = cdiv(kb, SKINNY_N_KMAX / SKINNY_BK);
+    {
+      Plan p;
+      Work w;
+      if (build_skinny_n(c, cfg, 1, &p, &w)) add(p, w);
+    }
+    for (int pk : kSplits) {
+      if (pk < min_pk) continue;
+      if ((int64_t)pk * rb > 8LL * c.hw.n_cu * kSkinnyNCfg[cfg].occ && pk > min_pk) break;
+      Plan p;
+      Work w;
+      if (build_skinny_n(c, cfg, pk, &p, &w)) add(p, w);
+    }
+    // splits needed to bound the LDS slice but absent from the list
+    if (min_pk > 1) {
+      Plan p;
+      Work w;
+      const int64_t kper = cdiv(kb, min_pk);
+      const int pk = (int)cdiv(kb, kper);
+      if (std::find(std::begin(kSplits), std::end(kSplits), pk) == std::end(kSplits) &&
+          build_skinny_n(c, cfg, pk, &p, &w))
+        add(p, w);
+    }
+  }
+}
+
+std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_out) {
+  int base = 0;
+  const int cls = classify_shape(s, hw, &base);
+  if (cls_out) *cls_out = cls;
+  const double compulsory = 2.0 * s.M * s.K + 2.0 * s.K * s.N;
+  const bool unaligned = (s.K % 8) != 0 || (s.N % 8) != 0;
+  Ctx c{s, hw, compulsory, out_bytes(s.dtype), unaligned};
+  std::vector<Plan> all;
+  enumerate_all(c, all);
+  std::vector<Plan> sel;
+  if (hw.search_open) {
+    sel = all;
+  } else {
+    // Eq. 6: the search stays inside the template the taxonomy chose. A
+    // K-parallel template needs a splittable K; with a single k granule the
+    // split degenerates to the Common template.
+    const bool ksplit = cls == AC_CLASS_MULTI_CORE_SPLITK || cls == AC_CLASS_HYBRID_SPLITK;
+    for (const Plan& p : all) {
+      const bool pk_split = p.family == FAM_STREAMK ? true : p.pk > 1;
+      if (pk_split == ksplit) sel.push_back(p);
+    }
+    if (sel.empty()) sel = all;
+  }
+  for (Plan& p : sel) p.cls = cls;
+  std::stable_sort(sel.begin(), sel.end(), [](const Plan& a, const Plan& b) {
+    if (a.predicted != b.predicted) return a.predicted < b.predicted;
+    return a.variant_key < b.variant_key;
+  });
+  for (Plan& p : sel) p.n_candidates = (int)sel.size();
+  return sel;
+}
+
+bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* out) {
+  if (vk_dtype(key) != s.dtype || vk_layouts(key) != (int)s.layouts) return false;
+  int base = 0;
+  const int cls = classify_shape(s, hw, &base);
+  const double compulsory = 2.0 * s.M * s.K + 2.0 * s.K * s.N;
+  const bool unaligned = (s.K % 8) != 0 || (s.N % 8) != 0;
+  Ctx c{s, hw, compulsory, out_bytes(s.dtype), unaligned};
+  const int fam = vk_family(key), cfg = vk_cfg(key), pk = vk_pk(key), sw = vk_swizzle(key);
+  Plan p;
+  Work w;
+  bool ok = false;
+  switch (fam) {
+    case FAM_TILE:
+      ok = cfg < N_TILE_CFG && pk >= 1 && build_tile(c, cfg, pk, sw, &p, &w);
+      break;
+    case FAM_SKINNY_M:
+      ok = sw == 0 && cfg < N_SKINNY_M_CFG && pk >= 1 && build_skinny_m(c, cfg, pk, &p, &w);
+      break;
+    case FAM_SKINNY_N:
+      ok = sw == 0 && cfg < N_SKINNY_N_CFG && pk >= 1 && build_skinny_n(c, cfg, pk, &p, &w);
+      break;
+    case FAM_STREAMK:
+      ok = sw == 0 && cfg < N_TILE_CFG && build_streamk(c, cfg, &p, &w) && p.pk == pk;
+      break;
+  }
+  if (!ok || !finish(c, &p, w)) return false;
+  if (p.variant_key != key) return false;
+  p.cls = cls;
+  p.n_candidates = 1;
+  *out = p;
+  return true;
+}
+
+uint64_t shape_key(const Shape& s, bool* exact) {
+  const int64_t lim = 1LL << 17;
+  if (s.M < lim && s.N < lim && s.K < lim && s.dtype >= 0 && s.dtype < 16 && s.layouts < 4) {
+    *exact = true;
+    return (uint64_t)s.M | ((uint64_t)s.N << 17) | ((uint64_t)s.K << 34) | ((uint64_t)s.dtype << 51) |
+           ((uint64_t)s.layouts << 55);
+  }
+  *exact = false;
+  uint64_t h = 0x9E3779B97F4A7C15ull;
+  const uint64_t v[5] = {(uint64_t)s.M, (uint64_t)s.N, (uint64_t)s.K, (uint64_t)s.dtype, (uint64_t)s.layouts};
+  for (uint64_t x : v) {
+    h ^= x + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
+    h *= 0xBF58476D1CE4E5B9ull;
+  }
+  return h | (1ull << 63);
+}
+
+// ---- paper arithmetic for explicit parameters ------------------------------
+
+void taxonomy(const adaptcore_taxonomy_in_t& in, adaptcore_taxonomy_out_t* out) {
+  out->pm = cdiv(in.M, in.m);
+  out->pn = cdiv(in.N, in.n);
+  out->pk = cdiv(in.K, in.k);
+  out->acc_bytes = in.m1 * in.n1 * 4;
+  const bool spatial = out->pm * out->pn >= in.n_core;
+  const bool onchip = out->acc_bytes <= in.s_acc;
+  out->cls = spatial ? (onchip ? AC_CLASS_COMMON : AC_CLASS_SINGLE_CORE_SPLITK)
+                     : (onchip ? AC_CLASS_MULTI_CORE_SPLITK : AC_CLASS_HYBRID_SPLITK);
+  // Eq. 1
+  out->read_bytes = (double)in.elem_bytes * (double)in.M * (double)in.N * (double)in.K *
+                    (1.0 / (double)in.m1 + 1.0 / (double)in.n1);
+  const double MN = (double)in.M * (double)in.N;
+  const double fin = (double)in.out_bytes * MN;
+  switch (out->cls) {
+    case AC_CLASS_COMMON:  // Eq. 2
+      out->write_bytes = fin;
+      break;
+    case AC_CLASS_SINGLE_CORE_SPLITK:  // Eq. 3
+      out->write_bytes = 4.0 * MN * (double)cdiv(in.K, in.k1) + fin;
+      break;
+    case AC_CLASS_MULTI_CORE_SPLITK:  // Eq. 4
+      out->write_bytes = 4.0 * MN * (double)cdiv(in.K, in.k) + fin;
+      break;
+    default: {  // Eq. 5, each partition with its actual length
+      double flushes = 0;
+      for (int64_t p0 = 0; p0 < in.K; p0 += in.k) flushes += (double)cdiv(std::min(in.k, in.K - p0), in.k1);
+      out->write_bytes = 4.0 * MN * flushes + fin;
+    }
+  }
+}
+
+double schedule(int kind, int64_t Q, int64_t L, double tm, double tp, double td) {
+  switch (kind) {
+    case 0:
+      return (double)L * (tm + tp) + td;  // Eq. 12
+    case 1:
+      return tm + (double)(L - 1) * std::max(tm, tp) + tp + td;  // Eq. 13
+    case 2:
+      return tm + (double)(Q * L - 1) * std::max(tm, tp) + tp + (double)Q * td;  // Eq. 14
+  }
+  return -1.0;
+}
+
+}  // namespace ac

@@ -1,0 +1,12 @@
+// Launch registry: plan -> kernel on a stream.
+#pragma once
+#include <hip/hip_runtime_api.h>
+
+#include "kernel_args.h"
+#include "planner.h"
+
+namespace ac {
+hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
+// Reads the device's occupancy of every kernel into the planner.
+void query_occupancy();
+}  // namespace ac

@@ -1,0 +1,59 @@
+// The variant space: the kernel configurations compiled into the library.
+// Shared by the planner (host arithmetic) and the launch registry.
+#pragma once
+#include <stdint.h>
+
+namespace ac {
+
+// Macro-tile configurations of the tile kernel (4 waves in a 2 x 2 grid, k
+// granule BK = 64, LDS double buffered). ms = MFMA tile (32: 32x32x16,
+// 16: 16x16x32). occ = workgroups per CU the planner assumes until the device
+// reports the real figure.
+struct TileCfg {
+  int bm, bn, ms, occ;
+};
+constexpr int TILE_BK = 64;
+constexpr TileCfg kTileCfg[] = {
+    {256, 256, 32, 1}, {256, 128, 32, 1}, {128, 256, 32, 1}, {128, 128, 32, 2},
+    {128, 64, 32, 2},  {64, 128, 32, 2},  {64, 64, 32, 4},   {32, 32, 16, 8},
+};
+constexpr int N_TILE_CFG = sizeof(kTileCfg) / sizeof(kTileCfg[0]);
+
+inline int tile_lds_bytes(const TileCfg& t) { return 2 * (t.bm + t.bn) * TILE_BK * 2 + 16; }
+
+// Small-M Copy configurations: M <= 16*mt rows, wkw waves split the k-range
+// of a workgroup (the others split its columns); a workgroup covers
+// 128 * (4 / wkw) columns; k granule 32.
+struct SkinnyMCfg {
+  int mt, wkw, occ;
+};
+constexpr int SKINNY_BK = 32;
+constexpr SkinnyMCfg kSkinnyMCfg[] = {{1, 1, 4}, {1, 4, 4}, {2, 1, 4}, {2, 4, 4}, {4, 1, 2}, {4, 4, 1}};
+constexpr int N_SKINNY_M_CFG = sizeof(kSkinnyMCfg) / sizeof(kSkinnyMCfg[0]);
+inline int skinny_m_cols(const SkinnyMCfg& c) { return 128 * (4 / c.wkw); }
+
+// Small-N configurations: N <= 16*nt columns, a workgroup covers 64*rb rows
+// and at most SKINNY_N_KMAX of K (the B^T slice it keeps in LDS).
+struct SkinnyNCfg {
+  int nt, rb, occ;
+};
+constexpr int SKINNY_N_KMAX = 512;
+constexpr SkinnyNCfg kSkinnyNCfg[] = {{1, 2, 4}, {2, 2, 4}, {4, 2, 2}};
+constexpr int N_SKINNY_N_CFG = sizeof(kSkinnyNCfg) / sizeof(kSkinnyNCfg[0]);
+inline int skinny_n_rows(const SkinnyNCfg& c) { return 64 * c.rb; }
+
+// 64-bit key of a configuration:
+//   bits  0- 3 family, 4-11 config index, 12 swizzle, 16-35 P_k (or the
+//   stream-K grid), 36-47 reserved, 48-51 dtype, 52-53 layouts.
+inline uint64_t make_variant_key(int family, int cfg, int swizzle, int pk, int dtype, int layouts) {
+  return (uint64_t)(family & 0xF) | ((uint64_t)(cfg & 0xFF) << 4) | ((uint64_t)(swizzle & 1) << 12) |
+         ((uint64_t)(pk & 0xFFFFF) << 16) | ((uint64_t)(dtype & 0xF) << 48) | ((uint64_t)(layouts & 0x3) << 52);
+}
+inline int vk_family(uint64_t k) { return (int)(k & 0xF); }
+inline int vk_cfg(uint64_t k) { return (int)((k >> 4) & 0xFF); }
+inline int vk_swizzle(uint64_t k) { return (int)((k >> 12) & 1); }
+inline int vk_pk(uint64_t k) { return (int)((k >> 16) & 0xFFFFF); }
+inline int vk_dtype(uint64_t k) { return (int)((k >> 48) & 0xF); }
+inline int vk_layouts(uint64_t k) { return (int)((k >> 52) & 0x3); }
+
+}  // namespace ac

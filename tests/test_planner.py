@@ -1,0 +1,210 @@
+"""Planner, plan cache and C-ABI checks that need no GPU.
+
+The planner's taxonomy and latency-model closed forms are compared with the
+oracle (oracle/taxonomy.py), which is itself pinned to the paper's worked
+cases and to brute force. The cache is checked for identity of plans, O(1)
+lookup cost and thread safety; the ABI for argument validation and for
+exporting every declared symbol.
+"""
+import ctypes
+import os
+import random
+import re
+import threading
+from fractions import Fraction
+
+import pytest
+
+import paper_2608_10803_amd as ac
+from oracle import taxonomy as tx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "adaptcore.h")).read()
+    names = set(re.findall(r"\b(adaptcore_[a-z_]+)\s*\(", hdr))
+    assert len(names) >= 15
+    L = ctypes.CDLL(ac._lib.LIB_PATH)
+    missing = [n for n in sorted(names) if not hasattr(L, n)]
+    assert not missing, missing
+    # and the binding exposes the same names
+    assert all(hasattr(ac, n) for n in names)
+
+
+@pytest.mark.parametrize("case", [
+    (1024, 1024, 1024, 128, 256, 1024, 128, 256, 64),
+    (4096, 4096, 1024, 256, 256, 1024, 256, 256, 64),
+    (128, 128, 4096, 64, 64, 1024, 64, 64, 64),
+    (256, 256, 8192, 256, 256, 2048, 256, 256, 64),
+])
+def test_paper_cases_through_abi(case):
+    """Section 4.3 cases on 16 cores / 128 KB, through the library."""
+    M, N, K, m, n, k, m1, n1, k1 = case
+    got = ac.adaptcore_taxonomy(M, N, K, m, n, k, m1, n1, k1, 16, 128 * 1024)
+    assert got["cls"] == tx.classify(M, N, m, n, m1, n1, 16, 128 * 1024)
+    assert got["acc_bytes"] == tx.acc_tile_bytes(m1, n1)
+
+
+def test_taxonomy_parity_random():
+    rnd = random.Random(5)
+    for _ in range(3000):
+        M, N, K = (rnd.randint(1, 5000) for _ in range(3))
+        m, n = rnd.choice([16, 32, 64, 128, 256]), rnd.choice([16, 32, 64, 128, 256])
+        k = rnd.randint(1, K)
+        m1, n1 = rnd.choice([16, 32, 64, 128, 256, 512]), rnd.choice([16, 32, 64, 128, 256])
+        k1 = rnd.randint(1, 256)
+        n_core = rnd.choice([16, 24, 256])
+        s_acc = rnd.choice([128 * 1024, 256 * 1024])
+        got = ac.adaptcore_taxonomy(M, N, K, m, n, k, m1, n1, k1, n_core, s_acc)
+        pm, pn, pk = tx.task_counts(M, N, K, m, n, k)
+        assert (got["pm"], got["pn"], got["pk"]) == (pm, pn, pk)
+        cls = tx.classify(M, N, m, n, m1, n1, n_core, s_acc)
+        assert got["cls"] == cls
+        assert got["read_bytes"] == pytest.approx(float(tx.read_volume(M, N, K, m1, n1)), rel=1e-12)
+        assert got["write_bytes"] == float(tx.write_volume(cls, M, N, K, k, k1))
+
+
+def test_schedule_parity():
+    rnd = random.Random(6)
+    for _ in range(2000):
+        Q, L = rnd.randint(1, 8), rnd.randint(1, 64)
+        tm, tp, td = (rnd.randint(0, 1000) / 8 for _ in range(3))
+        assert ac.adaptcore_schedule(0, Q, L, tm, tp, td) == float(tx.t_baseline(L, tm, tp, td))
+        assert ac.adaptcore_schedule(1, Q, L, tm, tp, td) == float(tx.t_double_buffer(L, tm, tp, td))
+        assert ac.adaptcore_schedule(2, Q, L, tm, tp, td) == float(tx.t_preload(Q, L, tm, tp, td))
+
+
+def test_shape_classes_follow_the_taxonomy():
+    # spatially saturated shapes are Common, starved ones MultiCoreSplitK
+    p = ac.adaptcore_plan_info(ac.adaptcore_plan(8192, 8192, 1024))
+    assert p["cls_name"] == "Common" and p["pk"] == 1
+    p = ac.adaptcore_plan_info(ac.adaptcore_plan(128, 128, 65536))
+    assert p["cls_name"] == "MultiCoreSplitK" and p["pk"] > 1
+    # a K that cannot be split falls back to the Common kernel inside the template
+    p = ac.adaptcore_plan_info(ac.adaptcore_plan(100, 100, 5))
+    assert p["pk"] == 1
+
+
+def test_plan_cache_identity_and_stats():
+    ac.adaptcore_cache_clear()
+    s0 = ac.adaptcore_stats()
+    h1 = ac.adaptcore_plan(777, 333, 999, ac.AC_BF16_F32OUT)
+    h2 = ac.adaptcore_plan(777, 333, 999, ac.AC_BF16_F32OUT)
+    h3 = ac.adaptcore_plan(777, 333, 999, ac.AC_BF16_BF16OUT)
+    assert h1 == h2 and h1 != h3
+    s1 = ac.adaptcore_stats()
+    assert s1["misses"] - s0["misses"] == 2 and s1["hits"] - s0["hits"] == 1
+    d = ac.adaptcore_plan_info(h1)
+    assert (d["M"], d["N"], d["K"], d["dtype"]) == (777, 333, 999, 0)
+    # large dimensions go through the exact fallback map
+    hb = ac.adaptcore_plan(1, 1 << 20, 3)
+    assert hb == ac.adaptcore_plan(1, 1 << 20, 3)
+    assert ac.adaptcore_plan_info(hb)["N"] == 1 << 20
+
+
+def test_lookup_is_constant_time_and_fast():
+    t_small = ac.adaptcore_bench_lookup(10, 200000)
+    t_big = ac.adaptcore_bench_lookup(20000, 200000)
+    assert t_small < 1000 and t_big < 1000  # < 1 us per cached lookup
+    assert t_big < 20 * max(t_small, 10.0)
+
+
+def test_concurrent_planning_returns_one_plan_per_shape():
+    ac.adaptcore_cache_clear()
+    shapes = [(m, n, k) for m in (3, 50, 700) for n in (9, 300) for k in (17, 4096)]
+    res = {}
+    lock = threading.Lock()
+
+    def worker(seed):
+        rnd = random.Random(seed)
+        for _ in range(200):
+            s = rnd.choice(shapes)
+            h = ac.adaptcore_plan(*s)
+            with lock:
+                res.setdefault(s, set()).add(h)
+
+    ts = [threading.Thread(target=worker, args=(i,)) for i in range(8)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    assert all(len(v) == 1 for v in res.values())
+
+
+def test_argument_validation():
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_plan(-1, 4, 4)
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_plan(4, 4, 4, 7)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_plan(4, 4, 4, ac.AC_BF16_F32OUT, 3)
+    h = ac.adaptcore_plan(64, 32, 16)
+    # leading dimensions shorter than the rows are rejected before any GPU work
+    for args in [(0x1000, 15, 0x2000, 32, 0x3000, 32), (0x1000, 16, 0x2000, 31, 0x3000, 32),
+                 (0x1000, 16, 0x2000, 32, 0x3000, 31), (0x1001, 16, 0x2000, 32, 0x3000, 32),
+                 (0, 16, 0x2000, 32, 0x3000, 32)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_matmul(h, *args)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    # an empty output launches nothing and succeeds anywhere
+    ac.adaptcore_matmul(ac.adaptcore_plan(0, 5, 7), 0, 7, 0x2000, 5, 0x3000, 5)
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_matmul(0, 0x1000, 16, 0x2000, 32, 0x3000, 32)
+
+
+def test_candidates_are_legal_and_keys_round_trip():
+    hw = ac.adaptcore_get_hw()
+    for s in [(1, 4096, 4096), (17, 300, 65536), (512, 512, 512), (3000, 5, 700), (64, 64, 65536),
+              (100000, 8, 5), (4096, 4096, 4096), (1, 1, 1)]:
+        cands = ac.adaptcore_candidates(*s)
+        assert cands, s
+        preds = [c["predicted_s"] for c in cands]
+        assert preds == sorted(preds)
+        best = ac.adaptcore_plan_info(ac.adaptcore_plan(*s))
+        assert best["variant_key"] == cands[0]["variant_key"]
+        for c in cands[:40]:
+            h = ac.adaptcore_plan_variant(*s, ac.AC_BF16_BF16OUT, 0, c["variant_key"])
+            d = ac.adaptcore_plan_info(h)
+            assert d["variant_key"] == c["variant_key"]
+            assert d["predicted_s"] == pytest.approx(c["predicted_s"])
+            assert d["workspace_bytes"] <= (2 << 30) + (1 << 20)
+            assert d["grid_y"] <= 65535 and d["grid_x"] >= 1
+            if d["family_name"] == "skinny_n":
+                assert d["pk"] >= 1 and -(-s[2] // d["pk"]) <= 512 + 32
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_plan_variant(5, 5, 5, ac.AC_BF16_BF16OUT, 0, 0xFFFF)
+    ac.adaptcore_set_hw(hw)
+
+
+def test_open_search_is_a_superset():
+    hw = ac.adaptcore_get_hw()
+    s = (200, 3000, 9000)
+    closed = {c["variant_key"] for c in ac.adaptcore_candidates(*s)}
+    h2 = ac.adaptcore_get_hw()
+    h2.search_open = 1
+    h2.enable_streamk = 1
+    ac.adaptcore_set_hw(h2)
+    try:
+        opened = {c["variant_key"] for c in ac.adaptcore_candidates(*s)}
+    finally:
+        ac.adaptcore_set_hw(hw)
+    assert closed < opened
+
+
+def test_profile_validation_and_cu_count_effect():
+    hw = ac.adaptcore_get_hw()
+    bad = ac.adaptcore_get_hw()
+    bad.n_cu = 0
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_set_hw(bad)
+    small = ac.adaptcore_get_hw()
+    small.n_cu = 16
+    ac.adaptcore_set_hw(small)
+    try:
+        # with 16 cores, 1024^3 saturates the device (Section 4.3, case 1 analogue)
+        assert ac.adaptcore_plan_info(ac.adaptcore_plan(1024, 1024, 1024))["cls_name"] == "Common"
+    finally:
+        ac.adaptcore_set_hw(hw)
+    assert ac.adaptcore_get_hw().n_cu == hw.n_cu
