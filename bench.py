@@ -1,0 +1,331 @@
+#!/usr/bin/env python3
+"""Benchmark of the adaptive dynamic-shape GEMM on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload sweep]
+
+Default workload: the dynamic-shape sweep -- 2,000 shapes with M, N, K
+log-uniform in [1, 100000] (seed 4), bf16 inputs uniform[-1, 1], fp32
+accumulation, bf16 output; each shape is planned once (plan-miss time is
+reported) and then run.
+
+One step = every shape of the sweep run as a batch of R back-to-back calls
+(replayed from a HIP graph captured once per shape), bracketed by HIP events
+on the launch stream; per-call time = batch time / R, median over the K
+timed steps. The calls of a batch cycle through distinct copies of the
+operands (as many as fit in 512 MiB per operand), so a shape whose copies
+exceed the 256 MiB Infinity Cache is read from HBM on every call; tiny
+shapes stay cache-resident.
+
+Metric (per shape): F = 2MNK, B = 2MK + 2KN + c*MN (c = 2 for bf16, 4 for fp32
+output); t_floor = max(F / 2.5 PFLOP/s, B / 8 TB/s); TFLOP/s = F / t and
+fraction = t_floor / t. `value` is the geomean TFLOP/s over the shapes,
+`frac_geomean` the geomean fraction of the per-shape roofline.
+
+Also printed in the same JSON line: per-t_floor-bucket fractions, the subset
+with t_floor >= 5 us, isolated single calls (512 MiB read between calls,
+each call bracketed by its own events: includes the event overhead), a
+secondary fraction against max(t_floor, measured empty-kernel launch floor),
+plan-miss and cached-lookup costs, the roofline of the dominant kernel, and
+the oracle timed on the host cores (cpu_baseline).
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FLOPS = 2.5e15  # dense bf16 MFMA
+PEAK_BW = 8.0e12     # HBM3E
+FLUSH_BYTES = 512 << 20
+
+METRIC = "geomean TFLOP/s and fraction of per-shape roofline over dynamic-shape sweep"
+
+
+def roof(M, N, K, cbytes):
+    F = 2.0 * M * N * K
+    B = 2.0 * M * K + 2.0 * K * N + cbytes * M * N
+    return F, B, max(F / PEAK_FLOPS, B / PEAK_BW)
+
+
+def gmean(xs):
+    xs = [x for x in xs]
+    if not xs:
+        return None
+    return math.exp(sum(math.log(max(x, 1e-300)) for x in xs) / len(xs))
+
+
+def workload_shapes(name):
+    from workloads import gen
+    if name == "sweep":
+        return gen.sweep(), 1  # bf16 output
+    if name == "single":
+        return gen.single_512(), 0
+    if name == "skinny":
+        return gen.skinny_m(), 1
+    if name == "splitk":
+        return gen.small_mn_large_k(), 0
+    raise SystemExit("unknown workload %s" % name)
+
+
+def kernel_name(d):
+    ob = "bf16" if d["dtype"] == 1 else "f32"
+    f = d["family_name"]
+    if f in ("tile", "streamk"):
+        return "k_%s<%d,%d,%s>" % (f, d["tile_m"], d["tile_n"], ob)
+    if f == "skinny_m":
+        return "k_skinny_m<mt=%d,n=%d,%s>" % (d["tile_m"] // 16, d["tile_n"], ob)
+    return "k_skinny_n<nt=%d,m=%d,%s>" % (d["tile_n"] // 16, d["tile_m"], ob)
+
+
+def cpu_baseline(shapes, cbytes, budget_s=15.0, seed=7):
+    """The oracle on the host cores, on a bounded sample of the workload:
+    a seeded sample of shapes, each computed in full when small and on a
+    seeded subset of its rows otherwise. Geomean TFLOP/s over the sample."""
+    from oracle import gemm_ref
+    from workloads import gen
+    rng = np.random.default_rng(seed)
+    order = rng.permutation(len(shapes))
+    per, used, t_total, rows_total = [], [], 0.0, 0
+    cap_mac = 2.0e8  # multiply-adds per sampled shape
+    for idx in order:
+        if t_total > budget_s or len(per) >= 60:
+            break
+        M, N, K = shapes[idx]
+        rows = max(1, min(M, int(cap_mac // max(1, N * K))))
+        if N * K > 5e7:  # B alone too large to generate for the sample
+            continue
+        r0 = int(rng.integers(0, M - rows + 1))
+        A = gen.uniform_bf16(rows, K, (seed, int(idx), 0))
+        B = gen.uniform_bf16(K, N, (seed, int(idx), 1))
+        t0 = time.perf_counter()
+        gemm_ref.gemm(A, B, want_d=False)
+        dt = time.perf_counter() - t0
+        t_total += dt
+        rows_total += rows
+        per.append(2.0 * rows * N * K / dt / 1e12)
+        used.append((M, N, K, rows))
+    return {"value": gmean(per), "unit": "TFLOP/s (geomean)", "cores": gemm_ref.threads(),
+            "kind": "oracle",
+            "sample": "%d sweep shapes (seeded), rows subsampled to <= 2e8 MAC per shape, %.1f s of CPU work"
+                      % (len(per), t_total)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-isolated", action="store_true")
+    ap.add_argument("--per-shape", default=None, help="write per-shape results to this JSON file")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_10803_amd as ac
+
+    if not torch.cuda.is_available():
+        raise SystemExit("no GPU")
+    ac.adaptcore_init()
+    dev = torch.device("cuda")
+    shapes, dtype = workload_shapes(args.workload)
+    cbytes = 4 if dtype == ac.AC_BF16_F32OUT else 2
+    out_t = torch.float32 if cbytes == 4 else torch.bfloat16
+
+    # --- planning: every shape once (misses), then cached lookups
+    t0 = time.perf_counter()
+    plans = [ac.adaptcore_plan(M, N, K, dtype) for (M, N, K) in shapes]
+    plan_miss_s = (time.perf_counter() - t0) / len(shapes)
+    lookup_ns = ac.adaptcore_bench_lookup(len(shapes), 1000000)
+    infos = [ac.adaptcore_plan_info(p) for p in plans]
+
+    # --- device operands: one arena per operand, filled once (seeded uniform[-1, 1])
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+    ROT_ELEMS = 320 << 20  # every operand arena holds >= 640 MiB of bf16 for rotating copies
+    maxA = max(max(M * K for M, N, K in shapes), ROT_ELEMS)
+    maxB = max(max(K * N for M, N, K in shapes), ROT_ELEMS)
+    maxC = max(max(M * N for M, N, K in shapes), ROT_ELEMS)
+    A = torch.empty(maxA, dtype=torch.bfloat16, device=dev).uniform_(-1, 1, generator=g)
+    B = torch.empty(maxB, dtype=torch.bfloat16, device=dev).uniform_(-1, 1, generator=g)
+    C = torch.empty(maxC, dtype=out_t, device=dev)
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    pa, pb, pc = A.data_ptr(), B.data_ptr(), C.data_ptr()
+
+    n = len(shapes)
+    red = torch.empty(1, dtype=torch.float32, device=dev)
+
+    def flush_read():
+        torch.sum(flush, dim=0, keepdim=True, out=red)
+
+    # launch floor: back-to-back empty kernels from a graph, and an isolated one
+    tiny = torch.empty(1, device=dev)
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    cs = torch.cuda.Stream()
+    ac.adaptcore_reserve_workspace(cs.cuda_stream, max(d["workspace_bytes"] for d in infos))
+    ac.adaptcore_reserve_workspace(sh, max(d["workspace_bytes"] for d in infos))
+    g0 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g0, stream=cs):
+        for _ in range(64):
+            tiny.zero_()
+    g0.replay()
+    e0, e1 = ev(), ev()
+    e0.record(); g0.replay(); e1.record(); torch.cuda.synchronize()
+    floor_graph = e0.elapsed_time(e1) * 1e-3 / 64
+    ts = []
+    for _ in range(30):
+        flush_read(); e0.record(); tiny.zero_(); e1.record(); torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    floor_isolated = statistics.median(ts)
+    del g0
+
+    # per-shape graphs of R calls over rotating operand copies
+    ROT = 512 << 20
+    graphs, reps = [], []
+    for i, (M, N, K) in enumerate(shapes):
+        fa, fb, fc = 2 * M * K, 2 * K * N, cbytes * M * N
+        R = int(min(64, max(8, math.ceil(30e-6 / max(infos[i]["predicted_s"], 1e-6)))))
+        def span(f, cap):
+            f = max((f + 255) // 256 * 256, 256)
+            return max(1, min(R, ROT // f, cap // f))
+        ca, cb_, cc = span(fa, A.numel() * 2), span(fb, B.numel() * 2), span(fc, C.numel() * cbytes)
+        sa, sb, sc = (max((fa + 255) // 256 * 256, 256), max((fb + 255) // 256 * 256, 256),
+                      max((fc + 255) // 256 * 256, 256))
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=cs):
+            for r in range(R):
+                ac.adaptcore_matmul(plans[i], pa + (r % ca) * sa, max(K, 1), pb + (r % cb_) * sb, max(N, 1),
+                                    pc + (r % cc) * sc, max(N, 1), cs.cuda_stream)
+        graphs.append(gr)
+        reps.append(R)
+    for _ in range(args.warmup):
+        for i in range(n):
+            graphs[i].replay()
+    torch.cuda.synchronize()
+
+    K_steps = args.steps
+    evs = [[(ev(), ev()) for _ in range(n)] for _ in range(K_steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(K_steps):
+        row = evs[k]
+        for i in range(n):
+            row[i][0].record()
+            graphs[i].replay()
+            row[i][1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    t_call = [statistics.median(evs[k][i][0].elapsed_time(evs[k][i][1]) * 1e-3 for k in range(K_steps)) / reps[i]
+              for i in range(n)]
+    del graphs
+
+    # isolated calls: cold caches, one call between its own events
+    iso = None
+    if not args.no_isolated:
+        iso = []
+        for i in range(n):
+            M, N, K = shapes[i]
+            ts = []
+            for _ in range(3):
+                flush_read()
+                e0.record()
+                ac.adaptcore_matmul(plans[i], pa, max(K, 1), pb, max(N, 1), pc, max(N, 1), sh)
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+            iso.append(statistics.median(ts))
+
+    # --- metric
+    rows = []
+    for i, (M, N, K) in enumerate(shapes):
+        F, Bb, tf = roof(M, N, K, cbytes)
+        d = infos[i]
+        r = {"M": M, "N": N, "K": K, "t": t_call[i], "t_floor": tf, "tflops": F / t_call[i] / 1e12,
+             "frac": tf / t_call[i], "frac_vs_launch": min(1.0, max(tf, floor_graph) / t_call[i]),
+             "bound": "mfma" if F / Bb >= PEAK_FLOPS / PEAK_BW else "hbm", "kernel": kernel_name(d),
+             "cls": d["cls_name"], "pk": d["pk"], "pred": d["predicted_s"], "F": F, "B": Bb}
+        if iso:
+            r["t_iso"] = iso[i]
+        rows.append(r)
+    value = gmean([r["tflops"] for r in rows])
+    frac = gmean([r["frac"] for r in rows])
+    buckets = {}
+    for lo, hi, name in [(0, 1e-6, "<1us"), (1e-6, 5e-6, "1-5us"), (5e-6, 50e-6, "5-50us"), (50e-6, 1e9, ">=50us")]:
+        sel = [r["frac"] for r in rows if lo <= r["t_floor"] < hi]
+        if sel:
+            buckets[name] = {"n": len(sel), "frac_geomean": round(gmean(sel), 4)}
+    big = [r for r in rows if r["t_floor"] >= 5e-6]
+
+    # dominant kernel: largest share of the summed per-call time
+    by_k = {}
+    for r in rows:
+        e = by_k.setdefault(r["kernel"], {"t": 0.0, "F": 0.0, "B": 0.0, "n": 0})
+        e["t"] += r["t"]
+        e["F"] += r["F"]
+        e["B"] += r["B"]
+        e["n"] += 1
+    dom_name, dom = max(by_k.items(), key=lambda kv: kv[1]["t"])
+    ai = dom["F"] / dom["B"]
+    if ai >= PEAK_FLOPS / PEAK_BW:
+        roofline = {"bound": "mfma", "achieved": round(dom["F"] / dom["t"] / 1e12, 2), "peak": 2500.0,
+                    "unit": "TFLOP/s"}
+        roofline["frac"] = round(roofline["achieved"] / 2500.0, 4)
+    else:
+        roofline = {"bound": "hbm", "achieved": round(dom["B"] / dom["t"] / 1e9, 1), "peak": 8000.0, "unit": "GB/s"}
+        roofline["frac"] = round(roofline["achieved"] / 8000.0, 4)
+    roofline.update({"traffic": None, "kernel": dom_name, "launches": dom["n"],
+                     "avg_launch_us": round(dom["t"] / dom["n"] * 1e6, 2),
+                     "share_of_time": round(dom["t"] / sum(r["t"] for r in rows), 3)})
+
+    line = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s (geomean)",
+        "frac_geomean": round(frac, 4),
+        "n_gpus": 1, "steps": K_steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / K_steps * 1e3, 2),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": {"sweep": "dynamic-shape sweep, 2000 shapes log-uniform [1,1e5], seed 4",
+                                "single": "512x512x512", "skinny": "skinny-M decode shapes (21)",
+                                "splitk": "small-MN large-K shapes (9)"}[args.workload],
+                   "shapes": n, "inputs": "bf16 uniform[-1,1]", "accumulate": "fp32",
+                   "output": "bf16" if cbytes == 2 else "fp32",
+                   "timing": "graph-replayed batches of back-to-back calls on rotating operand copies"},
+        "gpu_ms_per_pass": round(sum(t_call) * 1e3, 3),
+        "sum_t_floor_ms": round(sum(r["t_floor"] for r in rows) * 1e3, 3),
+        "frac_by_t_floor": buckets,
+        "t_floor_ge_5us": {"n": len(big), "frac_geomean": round(gmean([r["frac"] for r in big]), 4) if big else None,
+                           "tflops_geomean": round(gmean([r["tflops"] for r in big]), 3) if big else None},
+        "launch_floor_us": {"graph": round(floor_graph * 1e6, 2), "isolated": round(floor_isolated * 1e6, 2)},
+        "frac_geomean_vs_launch_floor": round(gmean([r["frac_vs_launch"] for r in rows]), 4),
+        "plan_miss_us": round(plan_miss_s * 1e6, 2), "plan_lookup_ns": round(lookup_ns, 1),
+        "roofline": roofline,
+    }
+    if iso:
+        line["isolated"] = {"tflops_geomean": round(gmean([r["F"] / r["t_iso"] / 1e12 for r in rows]), 3),
+                            "frac_geomean": round(gmean([r["t_floor"] / r["t_iso"] for r in rows]), 4),
+                            "timing": "one call after a 512 MiB read, bracketed by its own events"}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(shapes, cbytes)
+    if args.per_shape:
+        with open(args.per_shape, "w") as f:
+            json.dump({"line": line, "rows": rows}, f)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

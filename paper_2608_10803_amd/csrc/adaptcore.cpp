@@ -181,9 +181,6 @@ inline const adaptcore_plan_s* lookup(int64_t M, int64_t N, int64_t K, int32_t d
 }
 
 // ---- device and workspaces ------------------------------------------------
-constexpr int64_t kCounterInts = 1 << 16;            // per-tile counters; the last is the error flag
-constexpr int64_t kCounterBytes = kCounterInts * 4;  // fixed region at the start of a workspace
-
 struct Workspace {
   char* ptr = nullptr;
   int64_t bytes = 0;
@@ -227,15 +224,15 @@ adaptcore_status ensure_init() {
   return AC_OK;
 }
 
-// Workspace of (current device, stream) with at least `need` bytes beyond the
-// counter region; allocates outside stream capture only.
+// Workspace of (current device, stream) with at least `need` bytes; allocates
+// outside stream capture only. Partials are fully rewritten by every call that
+// uses them, so a workspace needs no initialisation.
 adaptcore_status get_workspace(hipStream_t stream, int64_t need, Workspace* out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(AC_ERR_NOT_INITIALIZED, "hipGetDevice failed");
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace& w = g_ws[std::make_pair(dev, (void*)stream)];
-  const int64_t total = kCounterBytes + need;
-  if (w.ptr && w.bytes >= total) {
+  if (w.ptr && w.bytes >= need) {
     *out = w;
     return AC_OK;
   }
@@ -243,7 +240,7 @@ adaptcore_status get_workspace(hipStream_t stream, int64_t need, Workspace* out)
   if (hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
     return fail(AC_ERR_NOT_INITIALIZED,
                 "split-K workspace missing for this stream under capture: call adaptcore_reserve_workspace first");
-  const int64_t grow = std::max<int64_t>(total, w.bytes + w.bytes / 2);
+  const int64_t grow = std::max<int64_t>(std::max<int64_t>(need, 1 << 20), w.bytes + w.bytes / 2);
   if (w.ptr) {
     (void)hipStreamSynchronize(stream);  // kernels in flight may still use the old buffer
     (void)hipFree(w.ptr);
@@ -252,11 +249,6 @@ adaptcore_status get_workspace(hipStream_t stream, int64_t need, Workspace* out)
   }
   void* p = nullptr;
   if (hipMalloc(&p, (size_t)grow) != hipSuccess) return fail(AC_ERR_OUT_OF_MEMORY, "workspace allocation failed");
-  // counters start at zero; every kernel that uses one restores it to zero
-  if (hipMemsetAsync(p, 0, (size_t)kCounterBytes, stream) != hipSuccess || hipStreamSynchronize(stream) != hipSuccess) {
-    (void)hipFree(p);
-    return fail(AC_ERR_LAUNCH, "workspace initialisation failed");
-  }
   w.ptr = static_cast<char*>(p);
   w.bytes = grow;
   *out = w;
@@ -319,9 +311,6 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
     return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
   adaptcore_status st = ensure_init();
   if (st != AC_OK) return st;
-  if (p.family == ac::FAM_STREAMK && p.grid_x > g_hw.n_cu * ac::occupancy(ac::FAM_STREAMK, p.cfg))
-    return fail(AC_ERR_INVALID_VALUE, "stream-K grid exceeds the resident workgroups of this device");
-  if (p.n_counters >= kCounterInts) return fail(AC_ERR_INTERNAL, "plan needs more tile counters than reserved");
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   ac::GemmArgs g;
@@ -335,25 +324,25 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   g.lda = lda;
   g.ldb = ldb;
   g.ldc = ldc;
-  g.pk = p.family == ac::FAM_STREAMK ? p.ws_pk : p.pk;
+  g.ldw = (N + 7) / 8 * 8;
+  g.pk = p.family == ac::FAM_STREAMK ? 1 : p.pk;
   g.kper = p.kper;
   g.tiles_m = p.pm;
   g.tiles_n = p.pn;
   g.swizzle = p.swizzle;
   g.iters_per_wg = p.iters_per_wg;
   g.sk_tiles = p.sk_tiles;
-  g.spin_limit = 1 << 22;
+  g.ws_pk = p.ws_pk;
+  g.grid = p.grid_x;
   if (p.ws_bytes > 0) {
     Workspace w;
     st = get_workspace(s, p.ws_bytes, &w);
     if (st != AC_OK) return st;
-    g.counters = reinterpret_cast<int*>(w.ptr);
-    g.err_flag = g.counters + (kCounterInts - 1);
-    g.ws = reinterpret_cast<float*>(w.ptr + kCounterBytes);
+    g.ws = reinterpret_cast<float*>(w.ptr);
   }
   const hipError_t e = ac::launch_plan(p, g, s);
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
-  st_launches.fetch_add(1, std::memory_order_relaxed);
+  st_launches.fetch_add((uint64_t)p.n_launch, std::memory_order_relaxed);
   return AC_OK;
 }
 
@@ -381,7 +370,7 @@ adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_pla
   out->swizzle = p.swizzle;
   out->n_candidates = p.n_candidates;
   out->predicted_s = p.predicted;
-  out->workspace_bytes = p.ws_bytes > 0 ? p.ws_bytes + kCounterBytes : 0;
+  out->workspace_bytes = p.ws_bytes;
   return AC_OK;
 }
 

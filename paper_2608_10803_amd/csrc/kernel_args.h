@@ -22,17 +22,18 @@ struct GemmArgs {
   void* C;
   int64_t M, N, K;
   int64_t lda, ldb, ldc;
-  float* ws;         // fp32 partial tiles of split-K / stream-K (may be null)
-  int* counters;     // per-tile arrival counters, zero between launches
+  float* ws;         // fp32 partials: split K uses pk slices of M x ldw,
+                     // stream-K uses ws_pk row-major tiles per split tile
+  int64_t ldw;       // leading dimension of a split-K partial slice (N rounded up to 8)
   int pk;            // K partitions (1 = no split)
-  int kper;          // k-blocks per partition (block = kernel's k granule)
+  int kper;          // k-blocks per partition (block = the kernel's k granule)
   int tiles_m;       // output tiles along M of this kernel's tiling
   int tiles_n;       // output tiles along N
   int swizzle;       // 1 = XCD-aware, grouped tile order
   int iters_per_wg;  // stream-K: MAC iterations per persistent workgroup
   int sk_tiles;      // stream-K: tiles handled by the stream-K phase
-  int spin_limit;    // stream-K: bound on fix-up waits (then error flag)
-  int* err_flag;     // stream-K: set to 1 when a wait hit its bound
+  int ws_pk;         // stream-K: partial slots per split tile
+  int grid;          // stream-K: persistent workgroups
 };
 
 }  // namespace ac

@@ -2,23 +2,23 @@
 // fp32 or bf16 output (RNE), for any M, N, K, leading dimensions and 2-byte
 // aligned pointers.
 //
-//   k_tile      MFMA macro-tile kernel with LDS double buffering. One launch
-//               per template: P_k == 1 is the Common template (k = K, one
-//               cast and one write per output, Eq. 2); P_k > 1 the
-//               MultiCoreSplitK template (K split across workgroups, fp32
-//               partials, cross-workgroup reduction, Eq. 4 / Eq. 11).
-//   k_streamk   StreamK applied to the tile kernel (Section 4.2): a
-//               persistent grid splits the MAC iterations of the last tiles
-//               evenly; partial tiles are fixed up in a fixed order.
+//   k_tile      MFMA macro-tile kernel, LDS double buffered, one or two
+//               k-blocks of global loads in flight. P_k == 1 is the Common template
+//               (k = K, one cast and one write per output, Eq. 2); P_k > 1 the
+//               MultiCoreSplitK template (each workgroup writes an fp32 partial
+//               of its K range, Eq. 4; k_reduce then sums them, Eq. 11).
+//   k_streamk   StreamK applied to the tile kernel (Section 4.2): a persistent
+//               grid splits the MAC iterations of the last tiles evenly and
+//               writes the pieces as fp32 partials; k_sk_fixup sums them.
 //   k_skinny_m  Small-M Copy module (Table 2) for M <= 64: B is streamed from
-//               HBM exactly once, A stays in cache; split K across CUs.
+//               HBM exactly once, A stays in cache; K split across CUs.
 //   k_skinny_n  the same module for N <= 64: A streamed once, the small B is
 //               kept resident in LDS (L1 Resident module, Table 2).
+//   k_reduce    deterministic cross-workgroup reduction of split-K partials:
+//               sum in partition order 0, 1, ..., P_k - 1, then cast.
 //
-// Cross-workgroup reductions are deterministic: the last workgroup to arrive
-// at a tile sums the fp32 partials in partition order 0, 1, ..., P_k - 1, so
-// a result does not depend on arrival order, and resets the tile's counter
-// to zero for the next launch.
+// Workgroups never wait on each other: partials are combined by a second
+// kernel, so a result never depends on arrival order and no kernel spins.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -41,23 +41,46 @@ __device__ __forceinline__ u32x4 load16(const uint16_t* p) {
   return v;
 }
 
-// The first `valid` (1..7) elements of a 16-byte vector, zeros after.
-__device__ __forceinline__ u32x4 load16_part(const uint16_t* p, int valid) {
-  uint32_t w[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint32_t lo = (2 * i < valid) ? (uint32_t)p[2 * i] : 0u;
-    uint32_t hi = (2 * i + 1 < valid) ? (uint32_t)p[2 * i + 1] : 0u;
-    w[i] = lo | (hi << 16);
-  }
-  return u32x4{w[0], w[1], w[2], w[3]};
+// Drops the first s (0..8) 16-bit elements of v, shifting the rest down and
+// filling with zeros. Branch-free (selects only).
+__device__ __forceinline__ u32x4 shift_down(u32x4 v, int s) {
+  const uint64_t lo = (uint64_t)v[0] | ((uint64_t)v[1] << 32);
+  const uint64_t hi = (uint64_t)v[2] | ((uint64_t)v[3] << 32);
+  const int sb = s * 16;  // 0 .. 128
+  const int s1 = sb & 63;
+  const uint64_t lo_a = (lo >> s1) | (s1 ? (hi << (64 - s1)) : 0ull);  // sb < 64
+  const uint64_t hi_a = hi >> s1;
+  const uint64_t lo_b = hi >> s1;                                       // 64 <= sb < 128
+  const uint64_t nlo = sb < 64 ? lo_a : (sb < 128 ? lo_b : 0ull);
+  const uint64_t nhi = sb < 64 ? hi_a : 0ull;
+  return u32x4{(uint32_t)nlo, (uint32_t)(nlo >> 32), (uint32_t)nhi, (uint32_t)(nhi >> 32)};
 }
 
-// Eight consecutive elements p[0..7], of which `valid` exist.
-__device__ __forceinline__ u32x4 load16_guard(const uint16_t* p, int64_t valid) {
-  if (valid >= 8) return load16(p);
-  if (valid <= 0) return u32x4{0u, 0u, 0u, 0u};
-  return load16_part(p, (int)valid);
+// Elements e .. e+7 of a row of `len` >= 8 elements; those at index >= len
+// read as zero. The 16-byte load ends at the row end at the latest, so it
+// never leaves the row, and no lane branches (no waits inside branches).
+__device__ __forceinline__ u32x4 load_row8(const uint16_t* row, int64_t e, int64_t len) {
+  const int64_t start = min(e, len - 8);
+  const int s = (int)min<int64_t>(e - start, 8);
+  return shift_down(load16(row + start), s);
+}
+
+// The same for rows of fewer than 8 elements: eight 2-byte loads at clamped
+// indices, then selects.
+__device__ __forceinline__ u32x4 load_row8_small(const uint16_t* row, int64_t e, int64_t len) {
+  uint32_t h[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int64_t idx = e + i;
+    const uint32_t v = row[min(max(idx, (int64_t)0), len - 1)];
+    h[i] = idx < len ? v : 0u;
+  }
+  return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+}
+
+// Elements e .. e+7 of a row of `len` >= 1 elements, zeros past the end.
+__device__ __forceinline__ u32x4 load_row(const uint16_t* row, int64_t e, int64_t len) {
+  return len >= 8 ? load_row8(row, e, len) : load_row8_small(row, e, len);
 }
 
 // Transpose an 8 x 8 block of 16-bit values: r[i] holds row i (8 columns),
@@ -120,7 +143,7 @@ __device__ __forceinline__ void store_c8(void* C, int64_t idx, const float (&v)[
 }
 
 // LDS rows are 16-byte chunks; the chunk index is XORed with low row bits so
-// that the 16 lanes reading 16 consecutive rows at one chunk hit distinct banks.
+// that the lanes reading consecutive rows at one chunk hit distinct banks.
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row & 7) ^ ((row >> 3) & 1)); }
 
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2):
@@ -148,28 +171,6 @@ __device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int
   tn = in / gsz;
 }
 
-// Last-arrival protocol of the deterministic cross-workgroup reduction.
-// Every thread has stored its partial; returns true in the workgroup that
-// arrived last, after which all partials of the tile are visible to it.
-__device__ __forceinline__ bool arrive_last(int* counter, int expected, int* s_flag) {
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int old = atomicAdd(counter, 1);
-    const int last = (old == expected - 1);
-    if (last) {
-      __threadfence();
-      // every other workgroup of the tile has arrived: reset for the next launch
-      __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    *s_flag = last;
-  }
-  __syncthreads();
-  const bool last = *s_flag != 0;
-  if (last) __threadfence();
-  return last;
-}
-
 // ------------------------------------------------------------ tile kernel
 
 template <int MS>
@@ -192,61 +193,142 @@ struct TileShape {
   static constexpr int TM = WTM / MS, TN = WTN / MS;
   static constexpr int KS = MS == 32 ? 16 : 32;
   static constexpr int NA = AccOf<MS>::n;
-  static constexpr int NACC = TM * TN * NA;  // accumulator floats per thread
-  static constexpr int AV = BM * CH;          // 16-byte vectors of an A stage
+  static constexpr int AV = BM * CH;  // 16-byte vectors of an A stage
   static constexpr int IA = (AV + NT - 1) / NT;
   static constexpr int IB = (BN + NT - 1) / NT;  // 8x8 blocks of a B stage (BK/8 * BN/8 = BN)
+  static constexpr int AB_BYTES = 2 * (BM + BN) * CH * 16;  // double-buffered A and B stages
+  static constexpr int CT_BYTES = BM * BN * 2;                // bf16 output tile
+  static constexpr int SMEM = AB_BYTES > CT_BYTES ? AB_BYTES : CT_BYTES;
   static_assert(WTM % MS == 0 && WTN % MS == 0, "wave tile must be a multiple of the MFMA tile");
 };
 
-// Computes the tile's accumulators over k-blocks [kt0, kt1).
+// Per-thread load geometry of a tile's stages (fixed for the tile). Offsets
+// are 32-bit byte offsets from the per-k-block uniform bases
+// A + m0*lda + kbase and B + kbase*ldb + n0; rows past M are clamped to row
+// M - 1 (their results are never stored). For B, the 16-byte column group of
+// a lane starts at min(gn, N - 8), so it never leaves the row; the lanes that
+// had to move left drop the extra leading elements when the stage goes to LDS.
 template <int BM, int BN, int MS>
-__device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int64_t n0, int kt0, int kt1,
-                                              typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
-                                                                         [TileShape<BM, BN, MS>::TN],
-                                              u32x4 (*sA)[BM * 8], u32x4 (*sB)[BN * 8]) {
+struct StageGeom {
   typedef TileShape<BM, BN, MS> S;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
-  const uint16_t* __restrict__ A = g.A;
-  const uint16_t* __restrict__ B = g.B;
-  const int64_t M = g.M, N = g.N, K = g.K, lda = g.lda, ldb = g.ldb;
+  uint32_t a_row[S::IA];  // bytes: clamped row * lda * 2 + 16
+  uint32_t b_col[S::IB];  // bytes: (start column - n0) * 2 + 16 (>= 0: start >= n0 - 8)
+  int32_t b_cs[S::IB];    // elements dropped at the N edge: 0..8 (8 = past N)
+  uint32_t ldb2;          // bytes per B row
+  __device__ __forceinline__ void init(const GemmArgs& g, int64_t m0, int64_t n0) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < S::IA; ++i) {
+      const int row = (tid + i * S::NT) >> 3;
+      a_row[i] = (uint32_t)((min(m0 + row, g.M - 1) - m0) * g.lda * 2 + 16);
+    }
+#pragma unroll
+    for (int bb = 0; bb < S::IB; ++bb) {
+      const int grp = min(tid + bb * S::NT, BN - 1) >> 3;
+      const int64_t gn = n0 + grp * 8;
+      const int64_t st = min(gn, g.N - 8);
+      b_col[bb] = (uint32_t)((st - n0) * 2 + 16);
+      b_cs[bb] = (int32_t)min(gn - st, (int64_t)8);
+    }
+    ldb2 = (uint32_t)(g.ldb * 2);
+  }
+};
 
+// base (uniform) + unsigned 32-bit byte offset: lets the compiler use the
+// scalar-base + vector-offset addressing of global loads.
+__device__ __forceinline__ const uint16_t* at(const uint16_t* base, uint32_t byte_off) {
+  return reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+
+// Global loads of one k-block stage into registers, then into LDS. The loads
+// are straight-line code for every block (interior or edge): a K tail moves
+// the A vectors left to end at the row end and clamps the B rows, exactly as
+// the N edge does for B columns; the recorded shifts are applied when the
+// stage is written to LDS, after all loads of the stage have been issued.
+template <int BM, int BN, int MS>
+struct Stage {
+  typedef TileShape<BM, BN, MS> S;
   u32x4 ra[S::IA];
   u32x4 rb[S::IB][8];
+  uint32_t code;  // bits 0-3: A elements to drop; bits 4-11: B rows past K
 
-  auto load_stage = [&](int kt) {
+  // Requires K >= 8 and N >= 8 (the small-row mode covers the rest). A
+  // thread's A vectors all sit at column (tid % 8) * 8 of the block and its B
+  // blocks all start at k-row (tid % 8) * 8, so one shift and one row mask
+  // serve all of them.
+  __device__ __forceinline__ void load(const GemmArgs& g, const StageGeom<BM, BN, MS>& o, int64_t m0,
+                                       int64_t n0, int kt) {
+    const int tid = threadIdx.x;
     const int64_t kbase = (int64_t)kt * S::BK;
+    const int rem = (int)min(g.K - kbase, (int64_t)(1 << 30));  // K left from this block on (uniform)
+    // bases 8 elements left of the block origin: every offset is >= 0
+    const uint16_t* Ab = g.A + m0 * g.lda + kbase - 8;
+    const uint16_t* Bb = g.B + kbase * g.ldb + n0 - 8;
+    const int c8 = (tid & 7) * 8;
+    const int st = min(c8, rem - 8);  // >= -8
+    uint32_t cd = (uint32_t)min(c8 - st, 8);
+#pragma unroll
+    for (int i = 0; i < S::IA; ++i)
+      if (S::AV % S::NT == 0 || tid + i * S::NT < S::AV) ra[i] = load16(at(Ab, o.a_row[i] + (uint32_t)(st * 2)));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int kr = min(c8 + i, rem - 1);
+      cd |= (uint32_t)(c8 + i >= rem) << (4 + i);
+#pragma unroll
+      for (int b = 0; b < S::IB; ++b) rb[b][i] = load16(at(Bb, (uint32_t)kr * o.ldb2 + o.b_col[b]));
+    }
+    code = cd;
+  }
+
+  // Small-row mode (K < 8 or N < 8): element loads, zeros outside the matrix.
+  __device__ __forceinline__ void load_small(const GemmArgs& g, int64_t m0, int64_t n0, int kt) {
+    const int tid = threadIdx.x;
+    const int64_t kbase = (int64_t)kt * S::BK;
+    code = 0;
 #pragma unroll
     for (int i = 0; i < S::IA; ++i) {
       const int idx = tid + i * S::NT;
       if (S::AV % S::NT == 0 || idx < S::AV) {
-        const int row = idx >> 3, c = idx & 7;
-        const int64_t gr = m0 + row, gk = kbase + c * 8;
-        ra[i] = gr < M ? load16_guard(A + gr * lda + gk, K - gk) : u32x4{0u, 0u, 0u, 0u};
+        const int64_t gr = min(m0 + (idx >> 3), g.M - 1), gk = kbase + (idx & 7) * 8;
+        ra[i] = load_row8_small(g.A + gr * g.lda, gk, g.K);
+        __builtin_amdgcn_sched_barrier(0);  // one vector at a time: few live registers
       }
     }
 #pragma unroll
     for (int b = 0; b < S::IB; ++b) {
       const int blk = tid + b * S::NT;
       if (BN % S::NT == 0 || blk < BN) {
-        const int c = blk & 7, grp = blk >> 3;
-        const int64_t gn = n0 + grp * 8;
+        const int64_t gn = n0 + (blk >> 3) * 8;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const int64_t gk = kbase + c * 8 + i;
-          rb[b][i] = gk < K ? load16_guard(B + gk * ldb + gn, N - gn) : u32x4{0u, 0u, 0u, 0u};
+          const int64_t gk = kbase + (blk & 7) * 8 + i;
+          const u32x4 v = load_row8_small(g.B + min(gk, g.K - 1) * g.ldb, gn, g.N);
+          rb[b][i] = gk < g.K ? v : u32x4{0u, 0u, 0u, 0u};
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
-  };
-  auto store_stage = [&](int buf) {
+  }
+
+  // edge: this stage's block needed shifts (uniform flag); `cs` is the
+  // tile's B column shift of this thread's blocks (StageGeom::b_cs).
+  __device__ __forceinline__ void store(u32x4* sA, u32x4* sB, bool edge, const int32_t (&cs)[S::IB]) {
+    const int tid = threadIdx.x;
+    if (edge) {
+      const int sa = (int)(code & 15);
+#pragma unroll
+      for (int i = 0; i < S::IA; ++i) ra[i] = shift_down(ra[i], sa);
+#pragma unroll
+      for (int b = 0; b < S::IB; ++b)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) rb[b][i] = shift_down(rb[b][i], ((code >> (4 + i)) & 1) ? 8 : cs[b]);
+    }
 #pragma unroll
     for (int i = 0; i < S::IA; ++i) {
       const int idx = tid + i * S::NT;
       if (S::AV % S::NT == 0 || idx < S::AV) {
         const int row = idx >> 3, c = idx & 7;
-        sA[buf][row * 8 + swz(row, c)] = ra[i];
+        sA[row * 8 + swz(row, c)] = ra[i];
       }
     }
 #pragma unroll
@@ -259,12 +341,43 @@ __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int n = grp * 8 + j;
-          sB[buf][n * 8 + swz(n, c)] = col[j];
+          sB[n * 8 + swz(n, c)] = col[j];
         }
       }
     }
-  };
-  auto compute = [&](int buf) {
+  }
+};
+
+// k-blocks of global loads in flight: the wide tiles hold one stage in
+// registers (their accumulators use the register file), the narrower tiles two.
+template <int BM, int BN>
+struct TileDepth {
+  static constexpr int value = (BM * BN > 64 * 64) ? 1 : 2;
+};
+
+// Accumulates the tile over k-blocks [kt0, kt1). With two stages in flight,
+// block kt is multiplied out of LDS while block kt+1 waits in registers and
+// block kt+2 is fetched. SMALL selects the element-load mode for K < 8 or
+// N < 8 (decided once per kernel, so the loop body has no per-block branches).
+template <int BM, int BN, int MS, bool SMALL>
+__device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0, int64_t n0, int kt0, int kt1,
+                                                   typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                              [TileShape<BM, BN, MS>::TN],
+                                                   char* smem) {
+  typedef TileShape<BM, BN, MS> S;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  u32x4* sA0 = reinterpret_cast<u32x4*>(smem);
+  u32x4* sA1 = sA0 + BM * 8;
+  u32x4* sB0 = sA1 + BM * 8;
+  u32x4* sB1 = sB0 + BN * 8;
+
+  const int kt_total = (int)((g.K + S::BK - 1) / S::BK);
+  const bool k_tail = (g.K % S::BK) != 0;
+  const bool n_edge = n0 + BN > g.N;
+  auto edge = [&](int kt) { return !SMALL && (n_edge || (k_tail && kt == kt_total - 1)); };
+
+  auto compute = [&](const u32x4* sA, const u32x4* sB) {
 #pragma unroll
     for (int ks = 0; ks < S::BK / S::KS; ++ks) {
       const int chunk = MS == 32 ? ks * 2 + (lane >> 5) : ks * 4 + (lane >> 4);
@@ -272,12 +385,12 @@ __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int
 #pragma unroll
       for (int i = 0; i < S::TM; ++i) {
         const int row = wr * S::WTM + i * MS + (lane % MS);
-        fa[i] = sA[buf][row * 8 + swz(row, chunk)];
+        fa[i] = sA[row * 8 + swz(row, chunk)];
       }
 #pragma unroll
       for (int j = 0; j < S::TN; ++j) {
         const int col = wc * S::WTN + j * MS + (lane % MS);
-        fb[j] = sB[buf][col * 8 + swz(col, chunk)];
+        fb[j] = sB[col * 8 + swz(col, chunk)];
       }
 #pragma unroll
       for (int i = 0; i < S::TM; ++i)
@@ -291,18 +404,62 @@ __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int
     }
   };
 
-  if (kt0 >= kt1) return;
-  load_stage(kt0);
-  store_stage(0);
-  __syncthreads();
-  for (int kt = kt0; kt < kt1; ++kt) {
-    const int buf = (kt - kt0) & 1;
-    const bool more = kt + 1 < kt1;
-    if (more) load_stage(kt + 1);
-    compute(buf);
-    if (more) store_stage(buf ^ 1);
+  StageGeom<BM, BN, MS> o;
+  o.init(g, m0, n0);  // (unused in the small-row mode)
+  auto load = [&](Stage<BM, BN, MS>& st, int kt) {
+    if constexpr (SMALL)
+      st.load_small(g, m0, n0, kt);
+    else
+      st.load(g, o, m0, n0, kt);
+  };
+
+  // The loop bodies are straight-line: the prefetch past the last block
+  // reloads the last block and the store of an unused stage is harmless, so
+  // no branch (and no conservative wait at a branch join) splits the pipeline.
+  if constexpr (TileDepth<BM, BN>::value == 1) {
+    Stage<BM, BN, MS> st;
+    load(st, kt0);
+    st.store(sA0, sB0, edge(kt0), o.b_cs);
     __syncthreads();
+    for (int kt = kt0; kt < kt1; ++kt) {
+      const int nx = min(kt + 1, kt1 - 1);
+      const bool odd = ((kt - kt0) & 1) != 0;  // uniform
+      load(st, nx);
+      compute(odd ? sA1 : sA0, odd ? sB1 : sB0);
+      st.store(odd ? sA0 : sA1, odd ? sB0 : sB1, edge(nx), o.b_cs);
+      __syncthreads();
+    }
+  } else {
+    Stage<BM, BN, MS> s0, s1;
+    load(s0, kt0);
+    load(s1, min(kt0 + 1, kt1 - 1));
+    s0.store(sA0, sB0, edge(kt0), o.b_cs);
+    __syncthreads();
+    for (int kt = kt0; kt < kt1; kt += 2) {
+      const int n1 = min(kt + 1, kt1 - 1), n2 = min(kt + 2, kt1 - 1), n3 = min(kt + 3, kt1 - 1);
+      load(s0, n2);
+      compute(sA0, sB0);
+      s1.store(sA1, sB1, edge(n1), o.b_cs);
+      __syncthreads();
+      if (kt + 1 >= kt1) break;
+      load(s1, n3);
+      compute(sA1, sB1);
+      s0.store(sA0, sB0, edge(n2), o.b_cs);
+      __syncthreads();
+    }
   }
+}
+
+template <int BM, int BN, int MS>
+__device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int64_t n0, int kt0, int kt1,
+                                              typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                         [TileShape<BM, BN, MS>::TN],
+                                              char* smem) {
+  if (kt0 >= kt1) return;
+  if (g.K < 8 || g.N < 8)
+    tile_mainloop_impl<BM, BN, MS, true>(g, m0, n0, kt0, kt1, acc, smem);
+  else
+    tile_mainloop_impl<BM, BN, MS, false>(g, m0, n0, kt0, kt1, acc, smem);
 }
 
 // Row (within the MFMA block) of accumulator element r of this lane.
@@ -314,25 +471,87 @@ __device__ __forceinline__ int acc_row(int r, int lane) {
     return (lane >> 4) * 4 + r;
 }
 
-// Stores accumulator element q (flattened (i, j, r)) of this thread to C.
-template <int BM, int BN, int MS, bool OBF>
-__device__ __forceinline__ void store_acc_elem(const GemmArgs& g, int64_t m0, int64_t n0, int q, float v) {
+// fp32 store of the accumulators to a row-major matrix (C or a partial),
+// rows < rmax and columns < cmax only.
+template <int BM, int BN, int MS>
+__device__ __forceinline__ void store_acc_f32(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                            [TileShape<BM, BN, MS>::TN],
+                                              float* dst, int64_t ld, int64_t m0, int64_t n0, int64_t rmax,
+                                              int64_t cmax) {
+  typedef TileShape<BM, BN, MS> S;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+#pragma unroll
+  for (int i = 0; i < S::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < S::TN; ++j) {
+      const int64_t col = n0 + wc * S::WTN + j * MS + (lane % MS);
+#pragma unroll
+      for (int r = 0; r < S::NA; ++r) {
+        const int64_t row = m0 + wr * S::WTM + i * MS + acc_row<MS>(r, lane);
+        if (row < rmax && col < cmax) dst[row * ld + col] = acc[i][j][r];
+      }
+    }
+}
+
+// bf16 output through LDS: the tile is converted into LDS row-major, then
+// written with 16-byte row segments.
+template <int BM, int BN, int MS>
+__device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                             [TileShape<BM, BN, MS>::TN],
+                                               const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
   typedef TileShape<BM, BN, MS> S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;
-  const int r = q % S::NA, ij = q / S::NA, i = ij / S::TN, j = ij % S::TN;
-  const int64_t row = m0 + wr * S::WTM + i * MS + acc_row<MS>(r, lane);
-  const int64_t col = n0 + wc * S::WTN + j * MS + (lane % MS);
-  if (row < g.M && col < g.N) store_c<OBF>(g.C, row * g.ldc + col, v);
+  uint16_t* ct = reinterpret_cast<uint16_t*>(smem);
+  __syncthreads();  // the main loop's last reads of the LDS stages are done
+  // row of accumulator element r = lane part + constant part
+  const int lrow = MS == 32 ? (lane >> 5) * 4 : (lane >> 4) * 4;
+#pragma unroll
+  for (int i = 0; i < S::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < S::TN; ++j) {
+      uint16_t* base = ct + (wr * S::WTM + i * MS + lrow) * BN + wc * S::WTN + j * MS + (lane % MS);
+#pragma unroll
+      for (int r = 0; r < S::NA; ++r) {
+        const int crow = MS == 32 ? (r >> 2) * 8 + (r & 3) : r;
+        base[crow * BN] = to_bf16(acc[i][j][r]);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // convert block by block (bounded live registers)
+    }
+  __syncthreads();
+  constexpr int GPR = BN / 8;  // 16-byte groups per tile row
+  uint16_t* C = static_cast<uint16_t*>(g.C);
+  for (int e = tid; e < BM * GPR; e += S::NT) {
+    const int row = e / GPR, grp = e % GPR;
+    const int64_t gr = m0 + row, gc = n0 + grp * 8;
+    if (gr >= g.M || gc >= g.N) continue;
+    const uint16_t* src = ct + row * BN + grp * 8;
+    uint16_t* dst = C + gr * g.ldc + gc;
+    if (gc + 8 <= g.N) {
+      u32x4 v = *reinterpret_cast<const u32x4*>(src);
+      __builtin_memcpy(dst, &v, 16);
+    } else {
+      for (int j = 0; j < (int)(g.N - gc); ++j) dst[j] = src[j];
+    }
+  }
+}
+
+template <int BM, int BN, int MS, bool OBF>
+__device__ __forceinline__ void store_tile_c(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                           [TileShape<BM, BN, MS>::TN],
+                                             const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
+  if constexpr (OBF)
+    store_acc_bf16<BM, BN, MS>(acc, g, m0, n0, smem);
+  else
+    store_acc_f32<BM, BN, MS>(acc, static_cast<float*>(g.C), g.ldc, m0, n0, g.M, g.N);
 }
 
 template <int BM, int BN, int MS, bool OBF>
 __global__ __launch_bounds__(256) void k_tile(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
-  __shared__ u32x4 sA[2][BM * 8];
-  __shared__ u32x4 sB[2][BN * 8];
-  __shared__ int s_flag;
+  __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
 
   const int ntiles = g.tiles_m * g.tiles_n;
   int tile = blockIdx.x;
@@ -351,67 +570,33 @@ __global__ __launch_bounds__(256) void k_tile(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
 
-  tile_mainloop<BM, BN, MS>(g, m0, n0, kt0, kt1, acc, sA, sB);
+  tile_mainloop<BM, BN, MS>(g, m0, n0, kt0, kt1, acc, smem);
 
-  if (g.pk == 1) {
-#pragma unroll
-    for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-        for (int r = 0; r < S::NA; ++r) store_acc_elem<BM, BN, MS, OBF>(g, m0, n0, (i * S::TN + j) * S::NA + r, acc[i][j][r]);
-    return;
-  }
-
-  // Split K: publish this partition's fp32 tile, the last arrival reduces.
-  const int tid = threadIdx.x;
-  const size_t tile_floats = (size_t)BM * BN;
-  float* wtile = g.ws + (size_t)tile * g.pk * tile_floats;
-  {
-    float* mine = wtile + (size_t)split * tile_floats;
-#pragma unroll
-    for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-        for (int r4 = 0; r4 < S::NA / 4; ++r4) {
-          const int c4 = (i * S::TN + j) * (S::NA / 4) + r4;
-          f32x4 v = {acc[i][j][r4 * 4], acc[i][j][r4 * 4 + 1], acc[i][j][r4 * 4 + 2], acc[i][j][r4 * 4 + 3]};
-          *reinterpret_cast<f32x4*>(mine + ((size_t)c4 * S::NT + tid) * 4) = v;
-        }
-  }
-  if (!arrive_last(g.counters + tile, g.pk, &s_flag)) return;
-#pragma unroll
-  for (int c4 = 0; c4 < S::NACC / 4; ++c4) {
-    f32x4 s = *reinterpret_cast<const f32x4*>(wtile + ((size_t)c4 * S::NT + tid) * 4);
-    for (int p = 1; p < g.pk; ++p) s += *reinterpret_cast<const f32x4*>(wtile + p * tile_floats + ((size_t)c4 * S::NT + tid) * 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) store_acc_elem<BM, BN, MS, OBF>(g, m0, n0, c4 * 4 + e, s[e]);
-  }
+  if (g.pk == 1)
+    store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
+  else  // this partition's fp32 partial, row-major slice `split`
+    store_acc_f32<BM, BN, MS>(acc, g.ws + (size_t)split * (size_t)g.M * (size_t)g.ldw, g.ldw, m0, n0, g.M, g.N);
 }
 
 // --------------------------------------------------------- stream-K kernel
-// A persistent grid of G workgroups. The first `sk_tiles` tiles (in tile id
-// order) are split into MAC iterations (one k-block each) and every
-// workgroup takes `iters_per_wg` consecutive iterations; a tile's pieces are
-// written as fp32 partials and the workgroup holding the tile's first
-// iteration sums them in iteration order once the others have arrived (it
-// processes that piece last, so its peers started earlier). The remaining
-// tiles are processed whole, data-parallel, by the grid afterwards.
+// A persistent grid of g.grid workgroups. The first `sk_tiles` tiles (in
+// tile-id order) are split into MAC iterations (one k-block each) and every
+// workgroup takes `iters_per_wg` consecutive iterations. A tile covered by
+// one workgroup is written to C directly; otherwise each piece goes to the
+// tile's slot (workgroup - first workgroup of the tile) as a row-major fp32
+// tile, summed later by k_sk_fixup. The remaining tiles are processed whole,
+// data-parallel, by the grid.
 template <int BM, int BN, int MS, bool OBF>
 __global__ __launch_bounds__(256) void k_streamk(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
-  __shared__ u32x4 sA[2][BM * 8];
-  __shared__ u32x4 sB[2][BN * 8];
-   const int tid = threadIdx.x;
+  __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
+
   const int ntiles = g.tiles_m * g.tiles_n;
-  const int ipt = (int)((g.K + S::BK - 1) / S::BK);  // iterations per tile
-  const int G = gridDim.x;
+  const int ipt = (int)((g.K + S::BK - 1) / S::BK);
   const size_t tile_floats = (size_t)BM * BN;
   const int64_t total_sk = (int64_t)g.sk_tiles * ipt;
 
-  // Stream-K phase.
   int64_t it = (int64_t)blockIdx.x * g.iters_per_wg;
   const int64_t it_end = min(it + (int64_t)g.iters_per_wg, total_sk);
   while (it < it_end) {
@@ -426,76 +611,21 @@ __global__ __launch_bounds__(256) void k_streamk(GemmArgs g) {
     for (int i = 0; i < S::TM; ++i)
 #pragma unroll
       for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
-    tile_mainloop<BM, BN, MS>(g, m0, n0, k_begin, k_end, acc, sA, sB);
     __syncthreads();
-
-    // Workgroups covering this tile: their first iterations are multiples of
-    // iters_per_wg; the owner holds k_begin == 0.
+    tile_mainloop<BM, BN, MS>(g, m0, n0, k_begin, k_end, acc, smem);
     const int64_t t0 = (int64_t)tile * ipt;
     const int first_wg = (int)(t0 / g.iters_per_wg);
-    const int last_wg = (int)min((int64_t)G - 1, (t0 + ipt - 1) / g.iters_per_wg);
-    const int slot = blockIdx.x - first_wg;  // piece index within the tile
-    const int pieces = last_wg - first_wg + 1;
-    float* wtile = g.ws + (size_t)tile * (size_t)g.pk * tile_floats;
-
-    if (pieces == 1) {
-#pragma unroll
-      for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-          for (int r = 0; r < S::NA; ++r)
-            store_acc_elem<BM, BN, MS, OBF>(g, m0, n0, (i * S::TN + j) * S::NA + r, acc[i][j][r]);
-    } else if (k_begin != 0) {
-      // Non-owner: publish the partial and raise this piece's flag.
-      float* mine = wtile + (size_t)slot * tile_floats;
-#pragma unroll
-      for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-          for (int r4 = 0; r4 < S::NA / 4; ++r4) {
-            const int c4 = (i * S::TN + j) * (S::NA / 4) + r4;
-            f32x4 v = {acc[i][j][r4 * 4], acc[i][j][r4 * 4 + 1], acc[i][j][r4 * 4 + 2], acc[i][j][r4 * 4 + 3]};
-            *reinterpret_cast<f32x4*>(mine + ((size_t)c4 * S::NT + tid) * 4) = v;
-          }
-      __threadfence();
-      __syncthreads();
-      if (tid == 0) atomicAdd(g.counters + tile, 1);
+    const int last_wg = (int)min((int64_t)g.grid - 1, (t0 + ipt - 1) / g.iters_per_wg);
+    if (first_wg == last_wg) {
+      store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
     } else {
-      // Owner: wait (bounded) for the other pieces, then sum in piece order.
-      if (tid == 0) {
-        int spins = 0;
-        while (__hip_atomic_load(g.counters + tile, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < pieces - 1) {
-          __builtin_amdgcn_s_sleep(2);
-          if (++spins > g.spin_limit) {
-            atomicExch(g.err_flag, 1);
-            break;
-          }
-        }
-        __hip_atomic_store(g.counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-      __syncthreads();
-      __threadfence();
-#pragma unroll
-      for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-          for (int r4 = 0; r4 < S::NA / 4; ++r4) {
-            const int c4 = (i * S::TN + j) * (S::NA / 4) + r4;
-            f32x4 s = {acc[i][j][r4 * 4], acc[i][j][r4 * 4 + 1], acc[i][j][r4 * 4 + 2], acc[i][j][r4 * 4 + 3]};
-            for (int p = 1; p < pieces; ++p)
-              s += *reinterpret_cast<const f32x4*>(wtile + p * tile_floats + ((size_t)c4 * S::NT + tid) * 4);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) store_acc_elem<BM, BN, MS, OBF>(g, m0, n0, c4 * 4 + e, s[e]);
-          }
+      float* slot = g.ws + ((size_t)tile * g.ws_pk + (blockIdx.x - first_wg)) * tile_floats;
+      store_acc_f32<BM, BN, MS>(acc, slot, BN, 0, 0, BM, BN);
     }
     it += k_end - k_begin;
   }
 
-  // Data-parallel phase: whole tiles after the stream-K ones.
-  for (int tile = g.sk_tiles + blockIdx.x; tile < ntiles; tile += G) {
+  for (int tile = g.sk_tiles + blockIdx.x; tile < ntiles; tile += g.grid) {
     int tm, tn;
     tile_coords(tile, g.tiles_m, g.tiles_n, g.swizzle, tm, tn);
     const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
@@ -505,15 +635,62 @@ __global__ __launch_bounds__(256) void k_streamk(GemmArgs g) {
 #pragma unroll
       for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
     __syncthreads();
-    tile_mainloop<BM, BN, MS>(g, m0, n0, 0, ipt, acc, sA, sB);
-#pragma unroll
-    for (int i = 0; i < S::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-        for (int r = 0; r < S::NA; ++r)
-          store_acc_elem<BM, BN, MS, OBF>(g, m0, n0, (i * S::TN + j) * S::NA + r, acc[i][j][r]);
+    tile_mainloop<BM, BN, MS>(g, m0, n0, 0, ipt, acc, smem);
+    store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
   }
+}
+
+// Sums the pieces of every split stream-K tile in workgroup order and writes
+// C. Grid: (sk_tiles, chunks); a thread handles 8 consecutive columns of a
+// tile row.
+template <bool OBF>
+__global__ __launch_bounds__(256) void k_sk_fixup(GemmArgs g, int BM, int BN) {
+  const int tile = blockIdx.x;
+  const int ipt = (int)((g.K + 63) / 64);
+  const int64_t t0 = (int64_t)tile * ipt;
+  const int first_wg = (int)(t0 / g.iters_per_wg);
+  const int last_wg = (int)min((int64_t)g.grid - 1, (t0 + ipt - 1) / g.iters_per_wg);
+  if (first_wg == last_wg) return;  // written directly by its workgroup
+  const int pieces = last_wg - first_wg + 1;
+  int tm, tn;
+  tile_coords(tile, g.tiles_m, g.tiles_n, g.swizzle, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  const size_t tile_floats = (size_t)BM * BN;
+  const float* base = g.ws + (size_t)tile * g.ws_pk * tile_floats;
+  const int gpr = BN / 8;
+  for (int e = blockIdx.y * 256 + threadIdx.x; e < BM * gpr; e += gridDim.y * 256) {
+    const int row = e / gpr, c0 = (e % gpr) * 8;
+    const int64_t gr = m0 + row, gc = n0 + c0;
+    if (gr >= g.M || gc >= g.N) continue;
+    const float* src = base + (size_t)row * BN + c0;
+    f32x4 s0 = *reinterpret_cast<const f32x4*>(src), s1 = *reinterpret_cast<const f32x4*>(src + 4);
+    for (int p = 1; p < pieces; ++p) {
+      s0 += *reinterpret_cast<const f32x4*>(src + p * tile_floats);
+      s1 += *reinterpret_cast<const f32x4*>(src + p * tile_floats + 4);
+    }
+    const float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+    store_c8<OBF>(g.C, gr * g.ldc + gc, v, g.N - gc);
+  }
+}
+
+// -------------------------------------------------- split-K reduction kernel
+// C = sum over p = 0 .. P_k - 1 (in this order) of the row-major fp32 slices
+// ws[p] (M x ldw, ldw a multiple of 8). A thread handles 8 columns of a row.
+template <bool OBF>
+__global__ __launch_bounds__(256) void k_reduce(GemmArgs g) {
+  const int64_t gpr = (g.N + 7) / 8;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= g.M * gpr) return;
+  const int64_t row = e / gpr, c0 = (e - row * gpr) * 8;
+  const size_t slice = (size_t)g.M * (size_t)g.ldw;
+  const float* src = g.ws + row * g.ldw + c0;
+  f32x4 s0 = *reinterpret_cast<const f32x4*>(src), s1 = *reinterpret_cast<const f32x4*>(src + 4);
+  for (int p = 1; p < g.pk; ++p) {
+    s0 += *reinterpret_cast<const f32x4*>(src + p * slice);
+    s1 += *reinterpret_cast<const f32x4*>(src + p * slice + 4);
+  }
+  const float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+  store_c8<OBF>(g.C, row * g.ldc + c0, v, g.N - c0);
 }
 
 // -------------------------------------------------------- skinny-M kernel
@@ -531,7 +708,6 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
   constexpr int U = 2;
   constexpr int NV = MT * 8;  // f32x4 accumulators per lane
   __shared__ f32x4 red[WKW > 1 ? (WKW - 1) * WNW * NV * 64 : 1];
-  __shared__ int s_flag;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wc = wave % WNW, wk = wave / WNW;
@@ -542,6 +718,8 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
   const int kb_total = (int)((K + 31) / 32);
   const int kb0 = min(split * g.kper, kb_total);
   const int kb1 = min(kb0 + g.kper, kb_total);
+  const bool k_tail = (K % 32) != 0;
+  const bool n_edge = (int64_t)(cb + 1) * NB > N;
 
   f32x4 acc[MT][8];
 #pragma unroll
@@ -550,26 +728,62 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
     for (int j = 0; j < 8; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int64_t nvalid = N - col0;
+  // Straight-line loads: the lane's 8 columns start at min(col0, N - 8) (never
+  // past the row end) and the leading extra columns are dropped afterwards;
+  // B rows past K are clamped and dropped; A vectors of the K tail end at the
+  // row end. K < 8 or N < 8 take element loads instead.
+  const bool small = K < 8 || N < 8;
+  const int64_t cst = small ? col0 : min(col0, N - 8);
+  const int cs = small ? 0 : (int)min(col0 - cst, (int64_t)8);
   for (int kb = kb0 + wk; kb < kb1; kb += WKW * U) {
     u32x4 rb[U][8];
     u32x4 fa[U][MT];
+    uint32_t past[U];
+    int sa[U];
+    bool edge = n_edge;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kbu = kb + u * WKW;
       const int64_t k = (int64_t)kbu * 32 + kg * 8;
-      const bool on = kbu < kb1;
+      const bool on = kbu < kb1;  // uniform over the wave
+      edge = edge || !on || (k_tail && kbu == kb_total - 1);
+      past[u] = 0;
+      if (!small) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        rb[u][i] = (on && k + i < K && nvalid > 0) ? load16_guard(g.B + (k + i) * ldb + col0, nvalid)
-                                                   : u32x4{0u, 0u, 0u, 0u};
+        for (int i = 0; i < 8; ++i) {
+          rb[u][i] = load16(g.B + min(k + i, K - 1) * ldb + cst);
+          past[u] |= (uint32_t)(!on || k + i >= K) << i;
+        }
+        const int64_t st = min(k, K - 8);
+        sa[u] = on ? (int)min(k - st, (int64_t)8) : 8;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int64_t row = mt * 16 + (lane & 15);
-        fa[u][mt] = (on && row < M) ? load16_guard(g.A + row * lda + k, K - k) : u32x4{0u, 0u, 0u, 0u};
+        for (int mt = 0; mt < MT; ++mt) {
+          const int64_t row = min((int64_t)(mt * 16 + (lane & 15)), M - 1);
+          fa[u][mt] = load16(g.A + row * lda + st);
+        }
+      } else {
+        sa[u] = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const u32x4 v = load_row8_small(g.B + min(k + i, K - 1) * ldb, col0, N);
+          rb[u][i] = (on && k + i < K) ? v : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int64_t row = min((int64_t)(mt * 16 + (lane & 15)), M - 1);
+          const u32x4 v = load_row8_small(g.A + row * lda, k, K);
+          fa[u][mt] = on ? v : u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
+      if (edge && !small) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) rb[u][i] = shift_down(rb[u][i], ((past[u] >> i) & 1) ? 8 : cs);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) fa[u][mt] = shift_down(fa[u][mt], sa[u]);
+      }
       u32x4 col[8];
       transpose8x8(rb[u], col);
 #pragma unroll
@@ -587,57 +801,31 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
         for (int j = 0; j < 8; ++j) red[(((wk - 1) * WNW + wc) * NV + mt * 8 + j) * 64 + lane] = acc[mt][j];
     }
     __syncthreads();
-    if (wk == 0) {
-      for (int w = 1; w < WKW; ++w)
+    if (wk != 0) return;
+    for (int w = 1; w < WKW; ++w)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int j = 0; j < 8; ++j) acc[mt][j] += red[(((w - 1) * WNW + wc) * NV + mt * 8 + j) * 64 + lane];
-    }
+        for (int j = 0; j < 8; ++j) acc[mt][j] += red[(((w - 1) * WNW + wc) * NV + mt * 8 + j) * 64 + lane];
   }
+  if (nvalid <= 0) return;
 
   // Output: lane holds rows mt*16 + 4*(l/16) + r, columns col0 .. col0+7.
-  auto store_out = [&](const f32x4 (&v)[MT][8]) {
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = mt * 16 + (lane >> 4) * 4 + r;
-        if (row < M && nvalid > 0) {
-          float o[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) o[j] = v[mt][j][r];
-          store_c8<OBF>(g.C, row * g.ldc + col0, o, nvalid);
-        }
-      }
-  };
-
-  if (g.pk == 1) {
-    if (wk == 0) store_out(acc);
-    return;
-  }
-  const size_t blk_floats = (size_t)WNW * NV * 64 * 4;
-  float* wblk = g.ws + (size_t)cb * g.pk * blk_floats;
-  if (wk == 0) {
-    float* mine = wblk + (size_t)split * blk_floats;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        *reinterpret_cast<f32x4*>(mine + (((size_t)wc * NV + mt * 8 + j) * 64 + lane) * 4) = acc[mt][j];
-  }
-  if (!arrive_last(g.counters + cb, g.pk, &s_flag)) return;
-  if (wk != 0) return;
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const size_t off = (((size_t)wc * NV + mt * 8 + j) * 64 + lane) * 4;
-      f32x4 s = *reinterpret_cast<const f32x4*>(wblk + off);
-      for (int p = 1; p < g.pk; ++p) s += *reinterpret_cast<const f32x4*>(wblk + p * blk_floats + off);
-      acc[mt][j] = s;
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = mt * 16 + (lane >> 4) * 4 + r;
+      if (row < M) {
+        float o[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] = acc[mt][j][r];
+        if (g.pk == 1)
+          store_c8<OBF>(g.C, row * g.ldc + col0, o, nvalid);
+        else
+          store_c8<false>(g.ws + (size_t)split * (size_t)M * (size_t)g.ldw, row * g.ldw + col0, o, nvalid);
+      }
     }
-  store_out(acc);
 }
 
 // -------------------------------------------------------- skinny-N kernel
@@ -653,7 +841,6 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
   constexpr int KCH = SKN_KMAX / 8;  // 16-byte chunks per LDS row
   constexpr int U = 2;
   __shared__ u32x4 sBt[NCOL * KCH];
-  __shared__ int s_flag;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rbk = blockIdx.x, split = blockIdx.y;
@@ -665,6 +852,7 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
   const int kb1 = min(min(kb0 + g.kper, kb_total), kb0 + SKN_KMAX / 32);
   const int64_t kbeg = (int64_t)kb0 * 32;
   const int nkc = (kb1 - kb0) * 4;  // 8-k chunks of this workgroup
+  const bool k_tail = (K % 32) != 0;
 
   // Stage B^T: block (kc, ng) = rows kbeg + 8kc .. +7, columns 8ng .. 8ng+7.
   for (int blk = tid; blk < nkc * (NCOL / 8); blk += 256) {
@@ -674,7 +862,8 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int64_t k = kbeg + kc * 8 + i;
-      r[i] = (k < K) ? load16_guard(g.B + k * ldb + n, N - n) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 v = load_row(g.B + min(k, K - 1) * ldb, n, N);
+      r[i] = k < K ? v : u32x4{0u, 0u, 0u, 0u};
     }
     transpose8x8(r, c);
 #pragma unroll
@@ -693,20 +882,38 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
 
   const int64_t row0 = (int64_t)rbk * (64 * RB) + wave * (16 * RB) + (lane & 15);
   const int kg = lane >> 4;
+  const bool small = K < 8;
   for (int kb = kb0; kb < kb1; kb += U) {
     u32x4 fa[U][RB];
+    int sa[U];
+    bool edge = false;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t k = (int64_t)(kb + u) * 32 + kg * 8;
+      const bool on = kb + u < kb1;  // uniform
+      edge = edge || !on || (k_tail && kb + u == kb_total - 1);
+      if (!small) {
+        // the K tail's vectors end at the row end; leading extras dropped below
+        const int64_t st = min(k, K - 8);
+        sa[u] = on ? (int)min(k - st, (int64_t)8) : 8;
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int64_t row = row0 + rb * 16;
-        fa[u][rb] = (kb + u < kb1 && row < M) ? load16_guard(g.A + row * lda + k, K - k) : u32x4{0u, 0u, 0u, 0u};
+        for (int rb = 0; rb < RB; ++rb) fa[u][rb] = load16(g.A + min(row0 + rb * 16, M - 1) * lda + st);
+      } else {
+        sa[u] = 0;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const u32x4 v = load_row8_small(g.A + min(row0 + rb * 16, M - 1) * lda, k, K);
+          fa[u][rb] = on ? v : u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (kb + u >= kb1) break;
+      if (edge && !small) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) fa[u][rb] = shift_down(fa[u][rb], sa[u]);
+      }
       const int kc = (kb + u - kb0) * 4 + kg;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -719,52 +926,30 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
   }
 
   // Output: lane holds column nt*16 + l%16 of rows base + rb*16 + 4*(l/16) + r.
-  auto store_out = [&](const f32x4 (&v)[RB][NT]) {
-    const int64_t rbase = (int64_t)rbk * (64 * RB) + wave * (16 * RB) + (lane >> 4) * 4;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int64_t col = nt * 16 + (lane & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t row = rbase + rb * 16 + r;
-          if (row < M && col < N) store_c<OBF>(g.C, row * g.ldc + col, v[rb][nt][r]);
-        }
-      }
-  };
-
-  if (g.pk == 1) {
-    store_out(acc);
-    return;
-  }
-  const size_t blk_floats = (size_t)4 * RB * NT * 64 * 4;
-  float* wblk = g.ws + (size_t)rbk * g.pk * blk_floats;
-  {
-    float* mine = wblk + (size_t)split * blk_floats;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        *reinterpret_cast<f32x4*>(mine + (((size_t)(wave * RB + rb) * NT + nt) * 64 + lane) * 4) = acc[rb][nt];
-  }
-  if (!arrive_last(g.counters + rbk, g.pk, &s_flag)) return;
+  const int64_t rbase = (int64_t)rbk * (64 * RB) + wave * (16 * RB) + (lane >> 4) * 4;
+  float* part = g.ws + (size_t)split * (size_t)M * (size_t)g.ldw;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const size_t off = (((size_t)(wave * RB + rb) * NT + nt) * 64 + lane) * 4;
-      f32x4 s = *reinterpret_cast<const f32x4*>(wblk + off);
-      for (int p = 1; p < g.pk; ++p) s += *reinterpret_cast<const f32x4*>(wblk + p * blk_floats + off);
-      acc[rb][nt] = s;
+      const int64_t col = nt * 16 + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = rbase + rb * 16 + r;
+        if (row < M && col < N) {
+          if (g.pk == 1)
+            store_c<OBF>(g.C, row * g.ldc + col, acc[rb][nt][r]);
+          else
+            part[row * g.ldw + col] = acc[rb][nt][r];
+        }
+      }
     }
-  store_out(acc);
 }
 
 }  // namespace ac
 
 // ------------------------------------------------------------- registry
-// VariantKey (family, config, output type) -> kernel; the launch boundary
+// VariantKey (family, config, output type) -> kernels; the launch boundary
 // between the host planner and the device.
 #include "planner.h"
 #include "registry.h"
@@ -776,6 +961,16 @@ namespace {
 typedef hipError_t (*LaunchFn)(const Plan&, const GemmArgs&, hipStream_t, bool);
 typedef int (*OccFn)();
 
+hipError_t launch_reduce(const GemmArgs& g, hipStream_t st, bool obf) {
+  const int64_t n = g.M * ((g.N + 7) / 8);
+  const dim3 grid((unsigned)((n + 255) / 256)), block(256);
+  if (obf)
+    hipLaunchKernelGGL((k_reduce<true>), grid, block, 0, st, g);
+  else
+    hipLaunchKernelGGL((k_reduce<false>), grid, block, 0, st, g);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int MS>
 hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, p.grid_y), block(256);
@@ -783,7 +978,9 @@ hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool ob
     hipLaunchKernelGGL((k_tile<BM, BN, MS, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_tile<BM, BN, MS, false>), grid, block, 0, st, g);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.pk == 1) return e;
+  return launch_reduce(g, st, obf);
 }
 template <int BM, int BN, int MS>
 hipError_t launch_streamk(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
@@ -792,6 +989,14 @@ hipError_t launch_streamk(const Plan& p, const GemmArgs& g, hipStream_t st, bool
     hipLaunchKernelGGL((k_streamk<BM, BN, MS, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_streamk<BM, BN, MS, false>), grid, block, 0, st, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.sk_tiles == 0) return e;
+  const int chunks = (BM * (BN / 8) + 255) / 256;
+  const dim3 fgrid(g.sk_tiles, chunks);
+  if (obf)
+    hipLaunchKernelGGL((k_sk_fixup<true>), fgrid, block, 0, st, g, BM, BN);
+  else
+    hipLaunchKernelGGL((k_sk_fixup<false>), fgrid, block, 0, st, g, BM, BN);
   return hipGetLastError();
 }
 template <int MT, int WKW>
@@ -801,7 +1006,9 @@ hipError_t launch_skinny_m(const Plan& p, const GemmArgs& g, hipStream_t st, boo
     hipLaunchKernelGGL((k_skinny_m<MT, WKW, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_skinny_m<MT, WKW, false>), grid, block, 0, st, g);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.pk == 1) return e;
+  return launch_reduce(g, st, obf);
 }
 template <int NT, int RB>
 hipError_t launch_skinny_n(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
@@ -810,7 +1017,9 @@ hipError_t launch_skinny_n(const Plan& p, const GemmArgs& g, hipStream_t st, boo
     hipLaunchKernelGGL((k_skinny_n<NT, RB, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_skinny_n<NT, RB, false>), grid, block, 0, st, g);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.pk == 1) return e;
+  return launch_reduce(g, st, obf);
 }
 
 template <typename F>

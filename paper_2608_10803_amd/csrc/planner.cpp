@@ -16,6 +16,9 @@ std::atomic<int> g_occ[FAM_COUNT][16];
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Leading dimension of a split-K partial slice: N rounded up to 8 floats.
+int64_t ldw8(int64_t n) { return (n + 7) / 8 * 8; }
+
 int table_occ(int family, int cfg) {
   switch (family) {
     case FAM_TILE:
@@ -45,8 +48,9 @@ struct Work {
   double mfma_it = 0;    // MFMA cycles per iteration on each SIMD
   double lds_it = 0;     // LDS bytes per iteration of one workgroup
   double out_unit = 0;   // bytes a workgroup writes at the end (tile or partial)
-  double epi = 0;        // bytes read by the cross-workgroup reduction (Eq. 11)
-  double epi_out = 0;    // final output bytes written by the reducing workgroup
+  double epi = 0;        // bytes read by the reduction kernel (Eq. 11), 0 = none
+  double epi_out = 0;    // output bytes written by the reduction kernel
+  double total_write = 0;// bytes written by the main kernel (output or partials)
   double setup = 0;      // bytes a workgroup stages before its main loop
   double prefetch = 1;   // main-loop iterations of loads in flight
   double total_read = 0; // sum over workgroups of bytes read (Eq. 1 analogue)
@@ -87,12 +91,13 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
   double t_main = full * unit_time(slots);
   if (rem > 0) t_main += unit_time(rem);
   // aggregate HBM roof over the whole launch
-  const double hbm_bytes = compulsory + (w.total_read - std::min(w.total_read, compulsory)) * (1.0 - hw.l2_hit);
+  const double hbm_bytes =
+      compulsory + (w.total_read - std::min(w.total_read, compulsory)) * (1.0 - hw.l2_hit) + w.total_write;
   t_main = std::max(t_main, hbm_bytes / agg_hbm);
-  // cross-workgroup reduction of split-K (Eq. 11): the last arrival reads the
-  // partials (cache-resident) and writes the output
+  // cross-workgroup reduction (Eq. 11) as a second kernel: one more launch, the
+  // partials read back and the output written once
   double t_epi = 0;
-  if (w.epi > 0) t_epi = hw.t_mem_latency + w.epi / hw.l2_bw_cu + w.epi_out / hw.l2_bw_cu;
+  if (w.epi > 0) t_epi = hw.t_launch + hw.t_mem_latency + (w.epi + w.epi_out) / (hw.hbm_bw * hw.hbm_eta);
   (void)s;
   return hw.t_launch + t_main + t_epi;  // Eq. 7 (T_pro = 0)
 }
@@ -133,9 +138,8 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
   p->grid_x = (int)(tm * tn);
   p->grid_y = (int)pk;
   if (pk > 1) {
-    p->ws_pk = (int)pk;
-    p->n_counters = (int)(tm * tn);
-    p->ws_bytes = (int64_t)tm * tn * pk * t.bm * t.bn * 4;
+    p->n_launch = 2;
+    p->ws_bytes = pk * s.M * ldw8(s.N) * 4;
   }
   const int ks = t.ms == 32 ? 16 : 32, cyc = t.ms == 32 ? 32 : 16;
   const int TM = t.bm / 2 / t.ms, TN = t.bn / 2 / t.ms;
@@ -146,12 +150,13 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
   w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
   w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
   w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (t.bm + t.bn) * TILE_BK * 2;
-  w->out_unit = pk == 1 ? bm_e * bn_e * c.cbytes : (double)t.bm * t.bn * 4;
+  w->out_unit = bm_e * bn_e * (pk == 1 ? c.cbytes : 4);
+  w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
   if (pk > 1) {
-    w->epi = (double)pk * t.bm * t.bn * 4;
-    w->epi_out = bm_e * bn_e * c.cbytes;
+    w->epi = (double)pk * s.M * s.N * 4;
+    w->epi_out = (double)s.M * s.N * c.cbytes;
   }
-  w->prefetch = 1;
+  w->prefetch = 2;
   w->total_read = (double)tm * tn * (bm_e + bn_e) * (double)s.K * 2;
   w->unaligned = c.unaligned;
   return true;
@@ -184,11 +189,9 @@ bool build_skinny_m(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   p->kper = (int)kper;
   p->grid_x = (int)cb;
   p->grid_y = (int)pk;
-  const double blk_floats = (4.0 / k.wkw) * k.mt * 8 * 64 * 4;
   if (pk > 1) {
-    p->ws_pk = (int)pk;
-    p->n_counters = (int)cb;
-    p->ws_bytes = (int64_t)(cb * pk * blk_floats * 4);
+    p->n_launch = 2;
+    p->ws_bytes = pk * s.M * ldw8(s.N) * 4;
   }
   const double nb_e = (double)s.N / cb;
   w->units = cb * pk;
@@ -197,10 +200,11 @@ bool build_skinny_m(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   w->bytes_it = 32.0 * k.wkw * nb_e * 2 + 4.0 * k.mt * 16 * 32 * 2;
   w->mfma_it = 8.0 * k.mt * 16;
   w->lds_it = 0;
-  w->out_unit = pk == 1 ? (double)s.M * nb_e * c.cbytes : blk_floats * 4;
+  w->out_unit = (double)s.M * nb_e * (pk == 1 ? c.cbytes : 4);
+  w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
   if (pk > 1) {
-    w->epi = pk * blk_floats * 4;
-    w->epi_out = (double)s.M * nb_e * c.cbytes;
+    w->epi = (double)pk * s.M * s.N * 4;
+    w->epi_out = (double)s.M * s.N * c.cbytes;
   }
   w->prefetch = 2;
   w->total_read = 2.0 * s.K * s.N + 2.0 * s.M * s.K * cb;
@@ -237,11 +241,9 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   p->kper = (int)kper;
   p->grid_x = (int)rbk;
   p->grid_y = (int)pk;
-  const double blk_floats = 4.0 * k.rb * k.nt * 64 * 4;
   if (pk > 1) {
-    p->ws_pk = (int)pk;
-    p->n_counters = (int)rbk;
-    p->ws_bytes = (int64_t)(rbk * pk * blk_floats * 4);
+    p->n_launch = 2;
+    p->ws_bytes = pk * s.M * ldw8(s.N) * 4;
   }
   const double rows_e = (double)s.M / rbk;
   w->units = rbk * pk;
@@ -251,10 +253,11 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   w->mfma_it = (double)k.rb * k.nt * 16;
   w->lds_it = 64.0 * k.nt * 16 * 4;
   w->setup = (double)kper * 32 * s.N * 2;
-  w->out_unit = pk == 1 ? rows_e * s.N * c.cbytes : blk_floats * 4;
+  w->out_unit = rows_e * s.N * (pk == 1 ? c.cbytes : 4);
+  w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
   if (pk > 1) {
-    w->epi = pk * blk_floats * 4;
-    w->epi_out = rows_e * s.N * c.cbytes;
+    w->epi = (double)pk * s.M * s.N * 4;
+    w->epi_out = (double)s.M * s.N * c.cbytes;
   }
   w->prefetch = 2;
   w->total_read = 2.0 * s.M * s.K + 2.0 * s.K * s.N * rbk;
@@ -299,7 +302,7 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
   p->iters_per_wg = (int)ipw;
   p->sk_tiles = (int)sk;
   p->ws_pk = (int)(cdiv(ipt, ipw) + 1);
-  p->n_counters = (int)sk;
+  p->n_launch = 2;
   p->ws_bytes = (int64_t)sk * p->ws_pk * t.bm * t.bn * 4;
   const int ks = t.ms == 32 ? 16 : 32, cyc = t.ms == 32 ? 32 : 16;
   const int TM = t.bm / 2 / t.ms, TN = t.bn / 2 / t.ms;
@@ -311,9 +314,10 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
   w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
   w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (t.bm + t.bn) * TILE_BK * 2;
   w->out_unit = 2.0 * t.bm * t.bn * 4 + (double)((ntiles - sk) / G) * bm_e * bn_e * c.cbytes;
-  w->epi = (double)p->ws_pk * t.bm * t.bn * 4;
-  w->epi_out = bm_e * bn_e * c.cbytes;
-  w->prefetch = 1;
+  w->total_write = (double)(ntiles - sk) * bm_e * bn_e * c.cbytes + (double)sk * 2 * t.bm * t.bn * 4;
+  w->epi = (double)sk * 2 * t.bm * t.bn * 4;
+  w->epi_out = (double)sk * bm_e * bn_e * c.cbytes;
+  w->prefetch = 2;
   w->total_read = (double)ntiles * (bm_e + bn_e) * (double)s.K * 2;
   w->unaligned = c.unaligned;
   return true;
@@ -325,12 +329,7 @@ bool finish(const Ctx& c, Plan* p, const Work& w) {
   p->s = c.s;
   p->predicted = model_time(c.s, w, c.hw, c.compulsory);
   p->variant_key = make_variant_key(p->family, p->cfg, p->swizzle, p->pk, c.s.dtype, (int)c.s.layouts);
-  if (p->ws_bytes > (int64_t)2 << 30) return false;  // workspace cap
-  if (p->n_counters > 0) {
-    const int64_t fl = (p->ws_bytes + 255) / 256 * 256;
-    p->ws_bytes = fl + (int64_t)(p->n_counters + 1) * 4;
-  }
-  return true;
+  return p->ws_bytes <= ((int64_t)2 << 30);  // workspace cap
 }
 
 }  // namespace

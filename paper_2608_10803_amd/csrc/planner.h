@@ -30,9 +30,9 @@ struct Plan {
   int grid_x = 0, grid_y = 1;
   int iters_per_wg = 0;  // stream-K
   int sk_tiles = 0;      // stream-K
-  int ws_pk = 0;         // partial slots per tile in the workspace
-  int n_counters = 0;
-  int64_t ws_bytes = 0;  // partials + counters
+  int ws_pk = 0;         // stream-K: partial slots per split tile
+  int n_launch = 1;      // kernels per call (split K and stream-K add a reduction)
+  int64_t ws_bytes = 0;  // fp32 partials
   int n_candidates = 0;
   double predicted = 0;
 };
