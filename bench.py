@@ -79,6 +79,8 @@ def kernel_name(d):
     f = d["family_name"]
     if f in ("tile", "streamk"):
         return "k_%s<%d,%d,%s>" % (f, d["tile_m"], d["tile_n"], ob)
+    if f == "smallk":
+        return "k_smallk<kmax=%d,%s>" % (d["tile_k"], ob)
     if f == "skinny_m":
         return "k_skinny_m<mt=%d,n=%d,%s>" % (d["tile_m"] // 16, d["tile_n"], ob)
     return "k_skinny_n<nt=%d,m=%d,%s>" % (d["tile_n"] // 16, d["tile_m"], ob)

@@ -68,7 +68,8 @@ typedef enum {
   AC_FAMILY_TILE = 0,     /* MFMA macro-tile kernel, P_k >= 1 */
   AC_FAMILY_SKINNY_M = 1, /* Small-M Copy module: B streamed once, M <= 64 */
   AC_FAMILY_SKINNY_N = 2, /* Small-M Copy by orientation: A streamed once, N <= 64 */
-  AC_FAMILY_STREAMK = 3   /* StreamK applied to the tile kernel */
+  AC_FAMILY_STREAMK = 3,  /* StreamK applied to the tile kernel */
+  AC_FAMILY_SMALLK = 4    /* K <= 16: rank-K update bound by writing C */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */
@@ -131,7 +132,17 @@ typedef struct {
   int32_t search_open;   /* 0: search inside the taxonomy's template (Eq. 6);
                             1: search every template (the exhaustive reading) */
   int32_t enable_streamk; /* 1: StreamK candidates take part in the search */
+  /* Per kernel configuration (index: adaptcore_config_index), calibrated by
+   * profiling: cost of one main-loop iteration of a workgroup that has its CU
+   * to itself, excluding memory transfer (the non-memory initiation interval
+   * of Eq. 9), and the fixed cost of a workgroup (prologue and epilogue).
+   * 0 = use the analytic estimate from MFMA issue and LDS traffic. */
+  double cfg_iter[32];
+  double cfg_wg[32];
 } adaptcore_hw_t;
+
+/* Index of a kernel configuration in adaptcore_hw_t::cfg_iter / cfg_wg, or -1. */
+int32_t adaptcore_config_index(int32_t family, int32_t cfg);
 
 /* Optional: bind the library to the current HIP device and read its CU count.
  * Without it, planning uses the default MI355X profile. AC_ERR_NOT_INITIALIZED

@@ -23,9 +23,10 @@ AC_ERR_INTERNAL = -6
 AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
 AC_LAYOUT_ROW_ROW = 0
+AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK = range(5)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
-FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk"]
 
 
 class AdaptCoreError(RuntimeError):
@@ -76,10 +77,20 @@ class Hw(ctypes.Structure):
                 ("l2_bw_cu", ctypes.c_double), ("t_launch", ctypes.c_double),
                 ("t_mem_latency", ctypes.c_double), ("t_wg", ctypes.c_double), ("mfma_eta", ctypes.c_double),
                 ("lds_bw_cu", ctypes.c_double), ("unaligned_eta", ctypes.c_double), ("l2_hit", ctypes.c_double),
-                ("search_open", ctypes.c_int32), ("enable_streamk", ctypes.c_int32)]
+                ("search_open", ctypes.c_int32), ("enable_streamk", ctypes.c_int32),
+                ("cfg_iter", ctypes.c_double * 32), ("cfg_wg", ctypes.c_double * 32)]
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_}
+        d = {}
+        for f, _ in self._fields_:
+            v = getattr(self, f)
+            d[f] = list(v) if f in ("cfg_iter", "cfg_wg") else v
+        return d
+
+    def copy(self):
+        h = Hw()
+        ctypes.memmove(ctypes.byref(h), ctypes.byref(self), ctypes.sizeof(Hw))
+        return h
 
 
 class TaxIn(ctypes.Structure):
@@ -136,6 +147,8 @@ def lib():
         L.adaptcore_taxonomy.restype = i32
         L.adaptcore_schedule.argtypes = [i32, i64, i64, d, d, d]
         L.adaptcore_schedule.restype = d
+        L.adaptcore_config_index.argtypes = [i32, i32]
+        L.adaptcore_config_index.restype = i32
         _lib = L
     return _lib
 
@@ -234,6 +247,10 @@ def adaptcore_taxonomy(M, N, K, m, n, k, m1, n1, k1, n_core, s_acc, elem_bytes=2
     _check(lib().adaptcore_taxonomy(ctypes.byref(i), ctypes.byref(o)))
     return {"pm": o.pm, "pn": o.pn, "pk": o.pk, "cls": CLASS_NAMES[o.cls], "acc_bytes": o.acc_bytes,
             "read_bytes": o.read_bytes, "write_bytes": o.write_bytes}
+
+
+def adaptcore_config_index(family, cfg):
+    return lib().adaptcore_config_index(family, cfg)
 
 
 def adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain):

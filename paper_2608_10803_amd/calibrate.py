@@ -1,0 +1,258 @@
+"""Offline calibration of the latency model and its accuracy check.
+
+The model's per-instruction costs and efficiencies (lambda and eta of Eq. 8,
+the launch cost and the memory latency) are not printed in the paper; they
+are obtained by profiling. This module
+
+  * measures every legal configuration of a sample of shapes on the GPU
+    (`measure`, run on the device: per-call time of back-to-back calls
+    replayed from a HIP graph, operands rotating through distinct copies),
+  * fits the profile constants so that the model's predictions match the
+    measurements in log space (`fit`, host only), and
+  * reports how well the model ranks: how often its choice is the measured
+    fastest configuration (top-1) and the time lost when it is not (regret)
+    (`evaluate`), for the search restricted to the taxonomy's template and
+    for the open search.
+
+    python -m paper_2608_10803_amd.calibrate measure OUT.json   (GPU)
+    python -m paper_2608_10803_amd.calibrate fit RECORDS.json   (CPU)
+"""
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+from . import _lib as ac
+
+# Global profile fields fitted (log-scale multiplicative factors on the
+# defaults); each kernel configuration additionally gets its own iteration and
+# workgroup costs (cfg_iter, cfg_wg).
+FIT_FIELDS = ["t_launch", "t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit"]
+BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.99)}
+N_CFG = 32
+
+
+def sample_shapes(n_sweep=120, seed=11):
+    """A stratified sample of the dynamic-shape sweep (evenly spaced in the
+    order of the roofline floor) plus the decode-style and small-MN large-K
+    shapes."""
+    from workloads import gen
+    sw = gen.sweep()
+
+    def floor(s):
+        M, N, K = s
+        return max(2.0 * M * N * K / 2.5e15, (2.0 * M * K + 2.0 * K * N + 2.0 * M * N) / 8e12)
+
+    order = sorted(range(len(sw)), key=lambda i: floor(sw[i]))
+    pick = [sw[order[int(j)]] for j in np.linspace(0, len(sw) - 1, n_sweep)]
+    return pick + gen.skinny_m() + gen.small_mn_large_k()
+
+
+def _open_profile():
+    h = ac.adaptcore_get_hw()
+    h.search_open = 1
+    h.enable_streamk = 1
+    return h
+
+
+def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=80, log=print):
+    """Time every legal configuration of each shape (GPU). Writes a JSON list
+    of records {M, N, K, key, family, cfg fields, t}."""
+    import torch
+    ac.adaptcore_init()
+    shapes = shapes or sample_shapes()
+    base = ac.adaptcore_get_hw()
+    ac.adaptcore_set_hw(_open_profile())
+    dev = torch.device("cuda")
+    cb = 2 if dtype == ac.AC_BF16_BF16OUT else 4
+    rot = 640 << 20
+    maxA = max(max(M * K for M, N, K in shapes) * 2, rot)
+    maxB = max(max(K * N for M, N, K in shapes) * 2, rot)
+    maxC = max(max(M * N for M, N, K in shapes) * cb, rot)
+    A = torch.empty(maxA // 2, dtype=torch.bfloat16, device=dev).uniform_(-1, 1)
+    B = torch.empty(maxB // 2, dtype=torch.bfloat16, device=dev).uniform_(-1, 1)
+    C = torch.empty(maxC // 2, dtype=torch.bfloat16, device=dev)
+    s = torch.cuda.Stream()
+    ac.adaptcore_reserve_workspace(s.cuda_stream, 2 << 30)
+    recs = []
+    t0 = time.time()
+    for si, (M, N, K) in enumerate(shapes):
+        cands = ac.adaptcore_candidates(M, N, K, dtype, 0)
+        if len(cands) > max_cands:  # keep the model's best and a spread of the rest
+            idx = sorted(set(list(range(20)) + list(np.linspace(20, len(cands) - 1, max_cands - 20).astype(int))))
+            cands = [cands[i] for i in idx]
+        fa, fb, fc = 2 * M * K, 2 * K * N, cb * M * N
+        for c in cands:
+            plan = ac.adaptcore_plan_variant(M, N, K, dtype, 0, c["variant_key"])
+            R = int(min(32, max(4, math.ceil(40e-6 / max(c["predicted_s"], 1e-6)))))
+
+            def span(f, cap):
+                f = max((f + 255) // 256 * 256, 256)
+                return f, max(1, min(R, (512 << 20) // f, cap // f))
+            sa, na = span(fa, maxA)
+            sb, nb = span(fb, maxB)
+            sc, nc = span(fc, maxC)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                for r in range(R):
+                    ac.adaptcore_matmul(plan, A.data_ptr() + (r % na) * sa, max(K, 1), B.data_ptr() + (r % nb) * sb,
+                                        max(N, 1), C.data_ptr() + (r % nc) * sc, max(N, 1), s.cuda_stream)
+            g.replay()
+            ts = []
+            for _ in range(3):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                g.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e-3 / R)
+            del g
+            rec = dict(M=M, N=N, K=K, dtype=dtype, key=c["variant_key"], family=c["family_name"],
+                       tile_m=c["tile_m"], tile_n=c["tile_n"], pk=c["pk"], grid=c["grid_x"] * c["grid_y"],
+                       pred=c["predicted_s"], t=float(np.median(ts)))
+            recs.append(rec)
+        log("[%d/%d] %s %d configurations, %.0f s" % (si + 1, len(shapes), (M, N, K), len(cands), time.time() - t0))
+    ac.adaptcore_set_hw(base)
+    with open(out_path, "w") as f:
+        json.dump(recs, f)
+    return recs
+
+
+def _by_shape(recs):
+    out = {}
+    for r in recs:
+        out.setdefault((r["M"], r["N"], r["K"], r["dtype"]), {})[r["key"]] = r["t"]
+    return out
+
+
+def predictions(hw, shapes_keys, open_search):
+    """Model predictions {shape: {key: seconds}} under profile `hw`."""
+    h = hw.copy()
+    h.search_open = 1 if open_search else 0
+    h.enable_streamk = 1
+    ac.adaptcore_set_hw(h)
+    out = {}
+    for (M, N, K, dt) in shapes_keys:
+        out[(M, N, K, dt)] = {c["variant_key"]: c["predicted_s"] for c in ac.adaptcore_candidates(M, N, K, dt, 0)}
+    return out
+
+
+def evaluate(recs, hw, open_search=False):
+    """Top-1 agreement and regret of the model's choice against the measured
+    times (only configurations that were measured are considered)."""
+    meas = _by_shape(recs)
+    pred = predictions(hw, list(meas), open_search)
+    top1, regrets = 0, []
+    for sk, mt in meas.items():
+        pk = {k: v for k, v in pred[sk].items() if k in mt}
+        if not pk:
+            continue
+        choice = min(pk, key=lambda k: (pk[k], k))
+        best = min(mt.values())
+        regrets.append(mt[choice] / best)
+        top1 += mt[choice] <= best * 1.0000001
+    r = np.array(regrets)
+    return {"shapes": len(r), "top1": top1 / max(len(r), 1), "regret_geomean": float(np.exp(np.mean(np.log(r)))),
+            "regret_mean": float(r.mean()), "within_10pct": float(np.mean(r <= 1.1)), "regret_max": float(r.max())}
+
+
+def config_of(key):
+    """Index of the calibrated cost slot of a variant key."""
+    return ac.adaptcore_config_index(int(key) & 0xF, (int(key) >> 4) & 0xFF)
+
+
+def _log_errors(hw, meas, keys_filter=None):
+    pred = predictions(hw, list(meas), True)
+    err = []
+    for sk, mt in meas.items():
+        for k, t in mt.items():
+            if keys_filter is not None and k not in keys_filter:
+                continue
+            p = pred[sk].get(k)
+            if p:
+                err.append(math.log(p / t))
+    return np.array(err)
+
+
+def fit(recs, hw0=None, rounds=3, iters=300, log=print):
+    """Fit the profile: minimise the squared log error of the model over all
+    measured configurations. Alternates a Nelder-Mead search over the global
+    constants (launch, latency, bandwidth, cache hit rate) with one over the
+    two costs of each kernel configuration on that configuration's records."""
+    from scipy.optimize import minimize
+    hw0 = (hw0 or ac.adaptcore_get_hw()).copy()
+    meas = _by_shape(recs)
+    by_cfg = {}
+    for r in recs:
+        by_cfg.setdefault(config_of(r["key"]), set()).add(r["key"])
+    cur = hw0.copy()
+
+    def loss_all(h):
+        e = _log_errors(h, meas)
+        return float(np.mean(np.square(e)))
+
+    def make_global(x, base):
+        h = base.copy()
+        for name, v in zip(FIT_FIELDS, x):
+            val = getattr(base, name) * math.exp(v)
+            lo, hi = BOUNDS.get(name, (1e-12, 1e30))
+            setattr(h, name, min(max(val, lo), hi))
+        return h
+
+    l0 = loss_all(cur)
+    evals = 0
+    for rnd in range(rounds):
+        base = cur.copy()
+        res = minimize(lambda x: loss_all(make_global(x, base)), np.zeros(len(FIT_FIELDS)), method="Nelder-Mead",
+                       options={"maxiter": iters, "xatol": 1e-3, "fatol": 1e-5})
+        cur = make_global(res.x, base)
+        evals += res.nfev
+        for idx in sorted(by_cfg):
+            if idx < 0:
+                continue
+            keys = by_cfg[idx]
+            sub = {sk: mt for sk, mt in meas.items() if any(k in keys for k in mt)}
+
+            def loss_cfg(x):
+                h = cur.copy()
+                h.cfg_iter[idx] = math.exp(min(max(x[0], -30.0), -7.0))
+                h.cfg_wg[idx] = math.exp(min(max(x[1], -30.0), -7.0))
+                e = _log_errors(h, sub, keys)
+                return float(np.mean(np.square(e))) if len(e) else 0.0
+            if cur.cfg_iter[idx] > 0:
+                x0 = np.array([math.log(cur.cfg_iter[idx]), math.log(max(cur.cfg_wg[idx], 1e-9))])
+            else:  # coarse grid for the first start
+                grid = [(a, b) for a in np.log(np.logspace(-9, -5, 17)) for b in np.log([1e-8, 1e-7, 3e-7, 1e-6])]
+                x0 = np.array(min(grid, key=lambda g: loss_cfg(g)))
+            r2 = minimize(loss_cfg, x0, method="Nelder-Mead", options={"maxiter": 200, "xatol": 1e-3, "fatol": 1e-6})
+            evals += r2.nfev
+            cur.cfg_iter[idx] = math.exp(min(max(r2.x[0], -30.0), -7.0))
+            cur.cfg_wg[idx] = math.exp(min(max(r2.x[1], -30.0), -7.0))
+        log("fit round %d: loss %.4f" % (rnd, loss_all(cur)))
+    l1 = loss_all(cur)
+    log("fit: loss %.4f -> %.4f (%d evaluations)" % (l0, l1, evals))
+    return cur, {"loss_before": l0, "loss_after": l1, "evals": int(evals)}
+
+
+def main(argv):
+    if len(argv) >= 2 and argv[0] == "measure":
+        measure(argv[1])
+    elif len(argv) >= 2 and argv[0] == "fit":
+        with open(argv[1]) as f:
+            recs = json.load(f)
+        hw0 = ac.adaptcore_get_hw()
+        before = {"class": evaluate(recs, hw0, False), "open": evaluate(recs, hw0, True)}
+        h, stats = fit(recs, hw0, log=lambda m: print(m, file=sys.stderr))
+        after = {"class": evaluate(recs, h, False), "open": evaluate(recs, h, True)}
+        out = {"profile": h.as_dict(), "fit": stats, "before": before, "after": after,
+               "records": len(recs), "shapes": len(_by_shape(recs))}
+        print(json.dumps(out, indent=1))
+    else:
+        print(__doc__)
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])

@@ -416,6 +416,9 @@ adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw) {
       !(hw->unaligned_eta > 0) || hw->l2_hit < 0 || hw->l2_hit > 1 || hw->t_launch < 0 || hw->t_mem_latency < 0 ||
       hw->t_wg < 0)
     return fail(AC_ERR_INVALID_VALUE, "profile field out of range");
+  for (int i = 0; i < 32; ++i)
+    if (!(hw->cfg_iter[i] >= 0 && hw->cfg_iter[i] < 1) || !(hw->cfg_wg[i] >= 0 && hw->cfg_wg[i] < 1))
+      return fail(AC_ERR_INVALID_VALUE, "calibrated configuration cost out of range");
   adaptcore_cache_clear();
   std::lock_guard<std::mutex> lk(g_mu);
   g_hw = *hw;
@@ -491,6 +494,8 @@ adaptcore_status adaptcore_taxonomy(const adaptcore_taxonomy_in_t* in, adaptcore
   ac::taxonomy(*in, out);
   return AC_OK;
 }
+
+int32_t adaptcore_config_index(int32_t family, int32_t cfg) { return ac::config_index(family, cfg); }
 
 double adaptcore_schedule(int32_t kind, int64_t Q, int64_t L, double t_m, double t_p, double t_drain) {
   return ac::schedule(kind, Q, L, t_m, t_p, t_drain);

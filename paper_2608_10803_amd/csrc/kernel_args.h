@@ -11,7 +11,8 @@ enum Family : int {
   FAM_SKINNY_M = 1,  // Small-M Copy module: B streamed once, M <= 64
   FAM_SKINNY_N = 2,  // the same module by orientation: A streamed once, N <= 64
   FAM_STREAMK = 3,   // StreamK applied to the tile kernel (Section 4.2)
-  FAM_COUNT = 4
+  FAM_SMALLK = 4,    // K <= 16: rank-K update, bound by writing C
+  FAM_COUNT = 5
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N

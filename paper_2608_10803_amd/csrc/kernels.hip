@@ -14,6 +14,7 @@
 //               HBM exactly once, A stays in cache; K split across CUs.
 //   k_skinny_n  the same module for N <= 64: A streamed once, the small B is
 //               kept resident in LDS (L1 Resident module, Table 2).
+//   k_smallk    K <= 16: rank-K update with fp32 FMAs, bound by writing C once.
 //   k_reduce    deterministic cross-workgroup reduction of split-K partials:
 //               sum in partition order 0, 1, ..., P_k - 1, then cast.
 //
@@ -946,6 +947,62 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
     }
 }
 
+// -------------------------------------------------------- small-K kernel
+// K <= KMAX (8 or 16): C is a rank-K update, bound by writing C once. Each
+// thread computes 4 rows x 8 columns with fp32 FMAs in ascending k; the B
+// rows it needs (K x 8 columns) and its 4 A rows are loaded once, the output
+// rows are stored as 16-byte (bf16) or 32-byte (fp32) segments. Thread t
+// takes column group t % ceil(N/8) and row group t / ceil(N/8), so
+// neighbouring threads write neighbouring segments of a row.
+template <int KMAX, bool OBF>
+__global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
+  constexpr int RT = 4;
+  const int64_t M = g.M, N = g.N, K = g.K;
+  const int64_t ncg = (N + 7) / 8;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= ncg * ((M + RT - 1) / RT)) return;
+  const int64_t rg = t / ncg, cg = t - rg * ncg;
+  const int64_t r0 = rg * RT, c0 = cg * 8;
+
+  // B rows 0..K-1, columns c0..c0+7 (zeros past N, rows past K zero)
+  float b[KMAX][8];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (k < K) v = load_row(g.B + (int64_t)k * g.ldb, c0, N);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      b[k][2 * e] = __uint_as_float(v[e] << 16);
+      b[k][2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
+    }
+  }
+  float acc[RT][8];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const int64_t row = min(r0 + r, M - 1);
+    float a[KMAX];
+#pragma unroll
+    for (int h = 0; h < KMAX / 8; ++h) {
+      const u32x4 v = load_row(g.A + row * g.lda, h * 8, K);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a[h * 8 + 2 * e] = __uint_as_float(v[e] << 16);
+        a[h * 8 + 2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float s = 0.f;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) s = __builtin_fmaf(a[k], b[k][j], s);
+      acc[r][j] = s;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+    if (r0 + r < M) store_c8<OBF>(g.C, (r0 + r) * g.ldc + c0, acc[r], N - c0);
+}
+
 }  // namespace ac
 
 // ------------------------------------------------------------- registry
@@ -1022,6 +1079,16 @@ hipError_t launch_skinny_n(const Plan& p, const GemmArgs& g, hipStream_t st, boo
   return launch_reduce(g, st, obf);
 }
 
+template <int KMAX>
+hipError_t launch_smallk(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
+  const dim3 grid(p.grid_x, 1), block(256);
+  if (obf)
+    hipLaunchKernelGGL((k_smallk<KMAX, true>), grid, block, 0, st, g);
+  else
+    hipLaunchKernelGGL((k_smallk<KMAX, false>), grid, block, 0, st, g);
+  return hipGetLastError();
+}
+
 template <typename F>
 int occ_of(F kernel_f32, F kernel_bf16) {
   int a = 0, b = 0;
@@ -1064,6 +1131,14 @@ const OccFn kSkinnyMOcc[] = {&occ_skinny_m<1, 1>, &occ_skinny_m<1, 4>, &occ_skin
                              &occ_skinny_m<2, 4>, &occ_skinny_m<4, 1>, &occ_skinny_m<4, 4>};
 const LaunchFn kSkinnyNFns[] = {&launch_skinny_n<1, 2>, &launch_skinny_n<2, 2>, &launch_skinny_n<4, 2>};
 const OccFn kSkinnyNOcc[] = {&occ_skinny_n<1, 2>, &occ_skinny_n<2, 2>, &occ_skinny_n<4, 2>};
+template <int KMAX>
+int occ_smallk() {
+  return occ_of(k_smallk<KMAX, false>, k_smallk<KMAX, true>);
+}
+const LaunchFn kSmallKFns[] = {&launch_smallk<8>, &launch_smallk<16>};
+const OccFn kSmallKOcc[] = {&occ_smallk<8>, &occ_smallk<16>};
+static_assert(sizeof(kSmallKFns) / sizeof(kSmallKFns[0]) == N_SMALLK_CFG, "small-K table");
+static_assert(kSmallKCfg[0].kmax == 8 && kSmallKCfg[1].kmax == 16, "small-K order");
 static_assert(sizeof(kTileFns) / sizeof(kTileFns[0]) == N_TILE_CFG, "tile table");
 static_assert(sizeof(kSkinnyMFns) / sizeof(kSkinnyMFns[0]) == N_SKINNY_M_CFG, "skinny-M table");
 static_assert(sizeof(kSkinnyNFns) / sizeof(kSkinnyNFns[0]) == N_SKINNY_N_CFG, "skinny-N table");
@@ -1094,6 +1169,8 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       return kSkinnyMFns[p.cfg](p, g, st, obf);
     case FAM_SKINNY_N:
       return kSkinnyNFns[p.cfg](p, g, st, obf);
+    case FAM_SMALLK:
+      return kSmallKFns[p.cfg](p, g, st, obf);
   }
   return hipErrorInvalidValue;
 }
@@ -1105,6 +1182,7 @@ void query_occupancy() {
   }
   for (int i = 0; i < N_SKINNY_M_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_M, i, kSkinnyMOcc[i]());
   for (int i = 0; i < N_SKINNY_N_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_N, i, kSkinnyNOcc[i]());
+  for (int i = 0; i < N_SMALLK_CFG; ++i) set_runtime_occupancy(FAM_SMALLK, i, kSmallKOcc[i]());
 }
 
 }  // namespace ac

@@ -28,11 +28,21 @@ int table_occ(int family, int cfg) {
       return kSkinnyMCfg[cfg].occ;
     case FAM_SKINNY_N:
       return kSkinnyNCfg[cfg].occ;
+    case FAM_SMALLK:
+      return kSmallKCfg[cfg].occ;
   }
   return 1;
 }
 
 int out_bytes(int dtype) { return dtype == AC_BF16_F32OUT ? 4 : 2; }
+
+// Offsets of each family's configurations in the calibrated cost tables.
+constexpr int IDX_TILE = 0;
+constexpr int IDX_SKINNY_M = IDX_TILE + N_TILE_CFG;
+constexpr int IDX_SKINNY_N = IDX_SKINNY_M + N_SKINNY_M_CFG;
+constexpr int IDX_SMALLK = IDX_SKINNY_N + N_SKINNY_N_CFG;
+constexpr int IDX_STREAMK = IDX_SMALLK + N_SMALLK_CFG;
+static_assert(IDX_STREAMK + N_TILE_CFG <= 32, "calibrated cost tables");
 
 // Tiles the taxonomy uses for its spatial predicate: the menu entries whose
 // accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
@@ -51,6 +61,7 @@ struct Work {
   double epi = 0;        // bytes read by the reduction kernel (Eq. 11), 0 = none
   double epi_out = 0;    // output bytes written by the reduction kernel
   double total_write = 0;// bytes written by the main kernel (output or partials)
+  int idx = -1;          // configuration index of the calibrated costs
   double setup = 0;      // bytes a workgroup stages before its main loop
   double prefetch = 1;   // main-loop iterations of loads in flight
   double total_read = 0; // sum over workgroups of bytes read (Eq. 1 analogue)
@@ -78,13 +89,19 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
     const double bw_l2 = hw.l2_bw_cu / per_cu;
     double tM = w.bytes_it * hbm_frac / bw_hbm + w.bytes_it * (1.0 - hbm_frac) / bw_l2;
     tM = std::max(tM, hw.t_mem_latency / w.prefetch);
-    const double tP = std::max(w.mfma_it * per_cu / (hw.clock_hz * hw.mfma_eta), w.lds_it * per_cu / hw.lds_bw_cu);
+    // non-memory initiation interval (Eq. 9): calibrated per configuration,
+    // else MFMA issue / LDS traffic; workgroups sharing a CU share it
+    const double tP0 = (w.idx >= 0 && hw.cfg_iter[w.idx] > 0)
+                           ? hw.cfg_iter[w.idx]
+                           : std::max(w.mfma_it / (hw.clock_hz * hw.mfma_eta), w.lds_it / hw.lds_bw_cu);
+    const double tP = tP0 * per_cu;
+    const double twg = (w.idx >= 0 && hw.cfg_wg[w.idx] > 0) ? hw.cfg_wg[w.idx] : hw.t_wg;
     const double t_fill = hw.t_mem_latency + tM + tP;  // first slice: load latency, load, compute
     const double t_drain = w.out_unit / bw_hbm;
     const double t_setup = w.setup > 0 ? hw.t_mem_latency + w.setup / bw_l2 : 0.0;
     const double L = std::max(0.0, w.L);
-    if (L == 0) return hw.t_wg + t_setup + t_drain;
-    return hw.t_wg + t_setup + t_fill + (L - 1) * std::max(tM, tP) + t_drain;  // Eq. 13
+    if (L == 0) return twg + t_setup + t_drain;
+    return twg + t_setup + t_fill + (L - 1) * std::max(tM, tP) + t_drain;  // Eq. 13
   };
   const int64_t full = (int64_t)(w.units / slots);
   const double rem = (double)w.units - full * slots;
@@ -146,6 +163,7 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
   const double bm_e = (double)s.M / tm, bn_e = (double)s.N / tn;
   w->units = tm * tn * pk;
   w->occ = occupancy(FAM_TILE, cfg);
+  w->idx = IDX_TILE + cfg;
   w->L = (double)kper;
   w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
   w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
@@ -196,6 +214,7 @@ bool build_skinny_m(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   const double nb_e = (double)s.N / cb;
   w->units = cb * pk;
   w->occ = occupancy(FAM_SKINNY_M, cfg);
+  w->idx = IDX_SKINNY_M + cfg;
   w->L = std::ceil((double)kper / k.wkw);
   w->bytes_it = 32.0 * k.wkw * nb_e * 2 + 4.0 * k.mt * 16 * 32 * 2;
   w->mfma_it = 8.0 * k.mt * 16;
@@ -248,6 +267,7 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   const double rows_e = (double)s.M / rbk;
   w->units = rbk * pk;
   w->occ = occupancy(FAM_SKINNY_N, cfg);
+  w->idx = IDX_SKINNY_N + cfg;
   w->L = (double)kper;
   w->bytes_it = rows_e * 32 * 2;
   w->mfma_it = (double)k.rb * k.nt * 16;
@@ -262,6 +282,42 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   w->prefetch = 2;
   w->total_read = 2.0 * s.M * s.K + 2.0 * s.K * s.N * rbk;
   w->unaligned = (s.K % 8) != 0;
+  return true;
+}
+
+// K <= 16: rank-K update with FMAs, one pass that writes C once.
+bool build_smallk(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
+  const SmallKCfg& k = kSmallKCfg[cfg];
+  const Shape& s = c.s;
+  if (pk_req != 1 || s.K > k.kmax || s.K < 1) return false;
+  if (cfg > 0 && s.K <= kSmallKCfg[cfg - 1].kmax) return false;  // a smaller K bound fits
+  const int64_t ncg = cdiv(s.N, 8), nrg = cdiv(s.M, 4);
+  const int64_t wgs = cdiv(ncg * nrg, 256);
+  if (wgs > (1LL << 31) - 1) return false;
+  p->family = FAM_SMALLK;
+  p->cfg = cfg;
+  p->tile_m = 4;
+  p->tile_n = 8;
+  p->tile_k = k.kmax;
+  p->pm = (int)std::min<int64_t>(nrg, (1LL << 31) - 1);
+  p->pn = (int)ncg;
+  p->pk = 1;
+  p->kper = 1;
+  p->grid_x = (int)wgs;
+  p->grid_y = 1;
+  w->units = wgs;
+  w->occ = occupancy(FAM_SMALLK, cfg);
+  w->idx = IDX_SMALLK + cfg;
+  w->L = 1;
+  // per workgroup: 256 threads x (K B-vectors + 4 A rows), mostly cache hits
+  w->bytes_it = 256.0 * (s.K * 16.0 + 4.0 * 16.0 * (k.kmax / 8));
+  w->mfma_it = 4.0 * 8 * k.kmax * 4;  // FMA issue cycles of one wave (VALU, 4 cycles each)
+  w->lds_it = 0;
+  w->out_unit = 256.0 * 4 * 8 * c.cbytes;
+  w->total_write = (double)s.M * s.N * c.cbytes;
+  w->prefetch = 1;
+  w->total_read = c.compulsory;  // re-reads of A rows and B rows stay in L1/L2
+  w->unaligned = (s.N % 8) != 0 || (s.K % 8) != 0;
   return true;
 }
 
@@ -309,6 +365,7 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
   const double bm_e = (double)s.M / tm, bn_e = (double)s.N / tn;
   w->units = G;
   w->occ = occupancy(FAM_STREAMK, cfg);
+  w->idx = IDX_STREAMK + cfg;
   w->L = (double)ipw + (double)((ntiles - sk) / G) * ipt;
   w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
   w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
@@ -455,6 +512,11 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
         add(p, w);
     }
   }
+  for (int cfg = 0; cfg < N_SMALLK_CFG; ++cfg) {
+    Plan p;
+    Work w;
+    if (build_smallk(c, cfg, 1, &p, &w)) add(p, w);
+  }
 }
 
 std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_out) {
@@ -470,13 +532,15 @@ std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_o
   if (hw.search_open) {
     sel = all;
   } else {
-    // Eq. 6: the search stays inside the template the taxonomy chose. A
-    // K-parallel template needs a splittable K; with a single k granule the
-    // split degenerates to the Common template.
+    // Eq. 6: the search stays inside the template the taxonomy chose. The
+    // spatially saturated templates keep k = K (no K split, no stream-K); the
+    // K-parallel templates search the split count P_k, whose degenerate value
+    // P_k = 1 is kept because a small problem can lose more to the reduction
+    // than it gains from the idle cores.
     const bool ksplit = cls == AC_CLASS_MULTI_CORE_SPLITK || cls == AC_CLASS_HYBRID_SPLITK;
     for (const Plan& p : all) {
       const bool pk_split = p.family == FAM_STREAMK ? true : p.pk > 1;
-      if (pk_split == ksplit) sel.push_back(p);
+      if (ksplit || !pk_split) sel.push_back(p);
     }
     if (sel.empty()) sel = all;
   }
@@ -513,6 +577,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
     case FAM_STREAMK:
       ok = sw == 0 && cfg < N_TILE_CFG && build_streamk(c, cfg, &p, &w) && p.pk == pk;
       break;
+    case FAM_SMALLK:
+      ok = sw == 0 && cfg < N_SMALLK_CFG && build_smallk(c, cfg, pk, &p, &w);
+      break;
   }
   if (!ok || !finish(c, &p, w)) return false;
   if (p.variant_key != key) return false;
@@ -520,6 +587,22 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
   p.n_candidates = 1;
   *out = p;
   return true;
+}
+
+int config_index(int family, int cfg) {
+  switch (family) {
+    case FAM_TILE:
+      return cfg >= 0 && cfg < N_TILE_CFG ? IDX_TILE + cfg : -1;
+    case FAM_SKINNY_M:
+      return cfg >= 0 && cfg < N_SKINNY_M_CFG ? IDX_SKINNY_M + cfg : -1;
+    case FAM_SKINNY_N:
+      return cfg >= 0 && cfg < N_SKINNY_N_CFG ? IDX_SKINNY_N + cfg : -1;
+    case FAM_SMALLK:
+      return cfg >= 0 && cfg < N_SMALLK_CFG ? IDX_SMALLK + cfg : -1;
+    case FAM_STREAMK:
+      return cfg >= 0 && cfg < N_TILE_CFG ? IDX_STREAMK + cfg : -1;
+  }
+  return -1;
 }
 
 uint64_t shape_key(const Shape& s, bool* exact) {

@@ -66,6 +66,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
 // dimensions below 2^17; larger shapes set bit 63 and hash all fields.
 uint64_t shape_key(const Shape& s, bool* exact);
 
+// Index of a configuration in the calibrated cost tables of the profile.
+int config_index(int family, int cfg);
+
 // Paper arithmetic for explicit tiling parameters (adaptcore_taxonomy).
 void taxonomy(const adaptcore_taxonomy_in_t& in, adaptcore_taxonomy_out_t* out);
 double schedule(int kind, int64_t Q, int64_t L, double tm, double tp, double tdrain);

@@ -42,6 +42,13 @@ constexpr SkinnyNCfg kSkinnyNCfg[] = {{1, 2, 4}, {2, 2, 4}, {4, 2, 2}};
 constexpr int N_SKINNY_N_CFG = sizeof(kSkinnyNCfg) / sizeof(kSkinnyNCfg[0]);
 inline int skinny_n_rows(const SkinnyNCfg& c) { return 64 * c.rb; }
 
+// Small-K configurations: K <= kmax; a thread computes 4 rows x 8 columns.
+struct SmallKCfg {
+  int kmax, occ;
+};
+constexpr SmallKCfg kSmallKCfg[] = {{8, 4}, {16, 2}};
+constexpr int N_SMALLK_CFG = sizeof(kSmallKCfg) / sizeof(kSmallKCfg[0]);
+
 // 64-bit key of a configuration:
 //   bits  0- 3 family, 4-11 config index, 12 swizzle, 16-35 P_k (or the
 //   stream-K grid), 36-47 reserved, 48-51 dtype, 52-53 layouts.
