@@ -135,8 +135,10 @@ typedef struct {
   /* Per kernel configuration (index: adaptcore_config_index), calibrated by
    * profiling: cost of one main-loop iteration of a workgroup that has its CU
    * to itself, excluding memory transfer (the non-memory initiation interval
-   * of Eq. 9), and the fixed cost of a workgroup (prologue and epilogue).
-   * 0 = use the analytic estimate from MFMA issue and LDS traffic. */
+   * of Eq. 9), and the fixed cost of a workgroup (prologue, first-load
+   * latency and epilogue together). 0 = use the analytic estimate: MFMA issue
+   * and LDS traffic for the iteration, t_wg plus t_mem_latency per dependent
+   * load phase for the fixed cost. Each value must lie in [0, 1) seconds. */
   double cfg_iter[32];
   double cfg_wg[32];
 } adaptcore_hw_t;
@@ -181,6 +183,12 @@ adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes);
 
 /* Fills *out with the description of a plan. */
 adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out);
+
+/* Writes the kernels one call of the plan launches, in launch order, as
+ * "name<template arguments>" separated by ';' (the names a profiler shows,
+ * without namespace and parameter list) into buf (capacity len bytes,
+ * NUL-terminated). AC_ERR_INVALID_VALUE if buf is too small. */
+adaptcore_status adaptcore_plan_kernels(const adaptcore_plan_t* plan, char* buf, int64_t len);
 
 /* Lists the legal candidates of a shape with their model latencies, ordered
  * by the model's preference (best first). Returns the number of candidates

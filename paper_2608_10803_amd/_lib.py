@@ -127,6 +127,8 @@ def lib():
         L.adaptcore_reserve_workspace.restype = i32
         L.adaptcore_plan_info.argtypes = [p, ctypes.POINTER(PlanDesc)]
         L.adaptcore_plan_info.restype = i32
+        L.adaptcore_plan_kernels.argtypes = [p, ctypes.c_char_p, i64]
+        L.adaptcore_plan_kernels.restype = i32
         L.adaptcore_candidates.argtypes = [i64, i64, i64, i32, u32, ctypes.POINTER(Candidate), i64]
         L.adaptcore_candidates.restype = i64
         L.adaptcore_get_hw.argtypes = [ctypes.POINTER(Hw)]
@@ -202,6 +204,13 @@ def adaptcore_plan_info(plan):
     d = PlanDesc()
     _check(lib().adaptcore_plan_info(plan, ctypes.byref(d)))
     return d.as_dict()
+
+
+def adaptcore_plan_kernels(plan):
+    """Kernels one call of the plan launches, in launch order."""
+    buf = ctypes.create_string_buffer(512)
+    _check(lib().adaptcore_plan_kernels(plan, buf, len(buf)))
+    return buf.value.decode().split(";")
 
 
 def adaptcore_candidates(M, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):

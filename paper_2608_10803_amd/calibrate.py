@@ -16,6 +16,7 @@ are obtained by profiling. This module
 
     python -m paper_2608_10803_amd.calibrate measure OUT.json   (GPU)
     python -m paper_2608_10803_amd.calibrate fit RECORDS.json   (CPU)
+    python -m paper_2608_10803_amd.calibrate emit FIT.json      (C++ defaults)
 """
 import json
 import math
@@ -30,7 +31,9 @@ from . import _lib as ac
 # Global profile fields fitted (log-scale multiplicative factors on the
 # defaults); each kernel configuration additionally gets its own iteration and
 # workgroup costs (cfg_iter, cfg_wg).
-FIT_FIELDS = ["t_launch", "t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit"]
+# The launch cost is not fitted: it is the measured per-kernel floor of
+# back-to-back launches, and the fixed part of each configuration is in cfg_wg.
+FIT_FIELDS = ["t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit"]
 BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.99)}
 N_CFG = 32
 
@@ -222,6 +225,8 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print):
                 h.cfg_wg[idx] = math.exp(min(max(x[1], -30.0), -7.0))
                 e = _log_errors(h, sub, keys)
                 return float(np.mean(np.square(e))) if len(e) else 0.0
+            if not len(_log_errors(cur, sub, keys)):
+                continue  # none of this configuration's records is a candidate now
             if cur.cfg_iter[idx] > 0:
                 x0 = np.array([math.log(cur.cfg_iter[idx]), math.log(max(cur.cfg_wg[idx], 1e-9))])
             else:  # coarse grid for the first start
@@ -237,6 +242,20 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print):
     return cur, {"loss_before": l0, "loss_after": l1, "evals": int(evals)}
 
 
+def emit_cpp(profile):
+    """C++ initialisers of the fitted constants, for the library's default
+    profile."""
+    p = profile
+    lines = ["  h.t_launch = %.4g;" % p["t_launch"], "  h.t_mem_latency = %.4g;" % p["t_mem_latency"],
+             "  h.hbm_eta = %.4g;" % p["hbm_eta"], "  h.l2_bw_cu = %.4g;" % p["l2_bw_cu"],
+             "  h.unaligned_eta = %.4g;" % p["unaligned_eta"], "  h.l2_hit = %.4g;" % p["l2_hit"]]
+    it = ", ".join("%.4g" % v for v in p["cfg_iter"])
+    wg = ", ".join("%.4g" % v for v in p["cfg_wg"])
+    lines.append("  static const double kIter[32] = {%s};" % it)
+    lines.append("  static const double kWg[32] = {%s};" % wg)
+    return "\n".join(lines)
+
+
 def main(argv):
     if len(argv) >= 2 and argv[0] == "measure":
         measure(argv[1])
@@ -250,6 +269,9 @@ def main(argv):
         out = {"profile": h.as_dict(), "fit": stats, "before": before, "after": after,
                "records": len(recs), "shapes": len(_by_shape(recs))}
         print(json.dumps(out, indent=1))
+    elif len(argv) >= 2 and argv[0] == "emit":
+        with open(argv[1]) as f:
+            print(emit_cpp(json.load(f)["profile"]))
     else:
         print(__doc__)
 

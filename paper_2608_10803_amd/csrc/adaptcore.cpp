@@ -374,6 +374,14 @@ adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_pla
   return AC_OK;
 }
 
+adaptcore_status adaptcore_plan_kernels(const adaptcore_plan_t* plan, char* buf, int64_t len) {
+  if (!plan || !buf) return fail(AC_ERR_INVALID_VALUE, "null argument");
+  const std::string names = ac::kernel_names(plan->p);
+  if (len < (int64_t)names.size() + 1) return fail(AC_ERR_INVALID_VALUE, "buffer too small");
+  std::memcpy(buf, names.c_str(), names.size() + 1);
+  return AC_OK;
+}
+
 int64_t adaptcore_candidates(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts,
                              adaptcore_candidate_t* out, int64_t cap) {
   adaptcore_status st;

@@ -548,7 +548,11 @@ __device__ __forceinline__ void store_tile_c(const typename AccOf<MS>::T (&acc)[
     store_acc_f32<BM, BN, MS>(acc, static_cast<float*>(g.C), g.ldc, m0, n0, g.M, g.N);
 }
 
-template <int BM, int BN, int MS, bool OBF>
+// Output of the tile kernel: C in fp32, C in bf16, or (P_k > 1) the fp32
+// partial of the workgroup's K partition.
+enum TileOut : int { OUT_F32 = 0, OUT_BF16 = 1, OUT_PARTIAL = 2 };
+
+template <int BM, int BN, int MS, int OUT>
 __global__ __launch_bounds__(256) void k_tile(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
@@ -573,10 +577,10 @@ __global__ __launch_bounds__(256) void k_tile(GemmArgs g) {
 
   tile_mainloop<BM, BN, MS>(g, m0, n0, kt0, kt1, acc, smem);
 
-  if (g.pk == 1)
-    store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
-  else  // this partition's fp32 partial, row-major slice `split`
+  if constexpr (OUT == OUT_PARTIAL)  // this partition's fp32 partial, row-major slice `split`
     store_acc_f32<BM, BN, MS>(acc, g.ws + (size_t)split * (size_t)g.M * (size_t)g.ldw, g.ldw, m0, n0, g.M, g.N);
+  else
+    store_tile_c<BM, BN, MS, OUT == OUT_BF16>(acc, g, m0, n0, smem);
 }
 
 // --------------------------------------------------------- stream-K kernel
@@ -675,21 +679,49 @@ __global__ __launch_bounds__(256) void k_sk_fixup(GemmArgs g, int BM, int BN) {
 }
 
 // -------------------------------------------------- split-K reduction kernel
-// C = sum over p = 0 .. P_k - 1 (in this order) of the row-major fp32 slices
-// ws[p] (M x ldw, ldw a multiple of 8). A thread handles 8 columns of a row.
+// C = sum over p = 0 .. P_k - 1 of the row-major fp32 slices ws[p] (M x ldw,
+// ldw a multiple of 8). A thread handles 8 columns of a row; when there are
+// few outputs and many partitions, G = 2^lg threads share one group of 8
+// columns: thread j sums the contiguous partitions [j*P_k/G, (j+1)*P_k/G) in
+// ascending order and the G sums are added in a fixed pairwise tree through
+// LDS. The order depends only on (P_k, G), never on timing.
 template <bool OBF>
-__global__ __launch_bounds__(256) void k_reduce(GemmArgs g) {
+__global__ __launch_bounds__(256) void k_reduce(GemmArgs g, int lg) {
+  __shared__ f32x4 red[2][256];
+  const int G = 1 << lg, EB = 256 >> lg;
+  const int t = threadIdx.x, el = t & (EB - 1), j = t >> (8 - lg);
   const int64_t gpr = (g.N + 7) / 8;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= g.M * gpr) return;
-  const int64_t row = e / gpr, c0 = (e - row * gpr) * 8;
+  const int64_t e = (int64_t)blockIdx.x * EB + el;
+  const bool live = e < g.M * gpr;
+  const int64_t row = live ? e / gpr : 0, c0 = live ? (e - row * gpr) * 8 : 0;
   const size_t slice = (size_t)g.M * (size_t)g.ldw;
   const float* src = g.ws + row * g.ldw + c0;
-  f32x4 s0 = *reinterpret_cast<const f32x4*>(src), s1 = *reinterpret_cast<const f32x4*>(src + 4);
-  for (int p = 1; p < g.pk; ++p) {
-    s0 += *reinterpret_cast<const f32x4*>(src + p * slice);
-    s1 += *reinterpret_cast<const f32x4*>(src + p * slice + 4);
+  const int p0 = (int)(((int64_t)j * g.pk) >> lg), p1 = (int)(((int64_t)(j + 1) * g.pk) >> lg);
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = s0;
+  if (live && p0 < p1) {
+    s0 = *reinterpret_cast<const f32x4*>(src + p0 * slice);
+    s1 = *reinterpret_cast<const f32x4*>(src + p0 * slice + 4);
+    for (int p = p0 + 1; p < p1; ++p) {
+      s0 += *reinterpret_cast<const f32x4*>(src + p * slice);
+      s1 += *reinterpret_cast<const f32x4*>(src + p * slice + 4);
+    }
   }
+  if (lg > 0) {
+    // pairwise tree over j: at step h, thread j (a multiple of 2h) adds j + h
+    red[0][t] = s0;
+    red[1][t] = s1;
+    __syncthreads();
+    for (int h = 1; h < G; h <<= 1) {
+      if ((j & (2 * h - 1)) == 0) {
+        s0 += red[0][t + h * EB];
+        s1 += red[1][t + h * EB];
+        red[0][t] = s0;
+        red[1][t] = s1;
+      }
+      __syncthreads();
+    }
+  }
+  if (!live || j != 0) return;
   const float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
   store_c8<OBF>(g.C, row * g.ldc + c0, v, g.N - c0);
 }
@@ -830,16 +862,18 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
 }
 
 // -------------------------------------------------------- skinny-N kernel
-// C (M x N, N <= 16*NT) = A * B with A streamed once. The workgroup's k-range
-// of B (at most SKN_KMAX) is transposed into LDS once; each wave then streams
-// 16*RB rows of A, one 16-byte fragment per lane per 32-k block, and issues
-// RB*NT 16x16x32 MFMAs against the resident B fragments.
+// C (M x N, N <= 16*NT) = A * B with A streamed once. The workgroup walks its
+// k-range in chunks of at most SKN_KMAX: each chunk of B is transposed into
+// LDS (B is small and comes from cache), then each wave streams 16*RB rows
+// of A over the chunk, one 16-byte fragment per lane per 32-k block, and
+// issues RB*NT 16x16x32 MFMAs against the resident B fragments.
 constexpr int SKN_KMAX = 512;
 
 template <int NT, int RB, bool OBF>
 __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
   constexpr int NCOL = NT * 16;
   constexpr int KCH = SKN_KMAX / 8;  // 16-byte chunks per LDS row
+  constexpr int CKB = SKN_KMAX / 32; // 32-k blocks per chunk
   constexpr int U = 2;
   __shared__ u32x4 sBt[NCOL * KCH];
 
@@ -848,32 +882,8 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
   const int64_t M = g.M, N = g.N, K = g.K, lda = g.lda, ldb = g.ldb;
   const int kb_total = (int)((K + 31) / 32);
   const int kb0 = min(split * g.kper, kb_total);
-  // the host never plans more than SKN_KMAX of K per workgroup; the clamp keeps
-  // the LDS slice in bounds regardless
-  const int kb1 = min(min(kb0 + g.kper, kb_total), kb0 + SKN_KMAX / 32);
-  const int64_t kbeg = (int64_t)kb0 * 32;
-  const int nkc = (kb1 - kb0) * 4;  // 8-k chunks of this workgroup
+  const int kb1 = min(kb0 + g.kper, kb_total);
   const bool k_tail = (K % 32) != 0;
-
-  // Stage B^T: block (kc, ng) = rows kbeg + 8kc .. +7, columns 8ng .. 8ng+7.
-  for (int blk = tid; blk < nkc * (NCOL / 8); blk += 256) {
-    const int ng = blk % (NCOL / 8), kc = blk / (NCOL / 8);
-    const int64_t n = (int64_t)ng * 8;
-    u32x4 r[8], c[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int64_t k = kbeg + kc * 8 + i;
-      const u32x4 v = load_row(g.B + min(k, K - 1) * ldb, n, N);
-      r[i] = k < K ? v : u32x4{0u, 0u, 0u, 0u};
-    }
-    transpose8x8(r, c);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int nn = ng * 8 + j;
-      sBt[nn * KCH + (kc ^ (nn & 15))] = c[j];
-    }
-  }
-  __syncthreads();
 
   f32x4 acc[RB][NT];
 #pragma unroll
@@ -884,44 +894,70 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
   const int64_t row0 = (int64_t)rbk * (64 * RB) + wave * (16 * RB) + (lane & 15);
   const int kg = lane >> 4;
   const bool small = K < 8;
-  for (int kb = kb0; kb < kb1; kb += U) {
-    u32x4 fa[U][RB];
-    int sa[U];
-    bool edge = false;
+  for (int cb0 = kb0; cb0 < kb1; cb0 += CKB) {
+    const int cb1 = min(cb0 + CKB, kb1);
+    const int64_t kbeg = (int64_t)cb0 * 32;
+    const int nkc = (cb1 - cb0) * 4;  // 8-k chunks of this chunk
+    if (cb0 != kb0) __syncthreads();  // every wave is done with the previous chunk
+    // Stage B^T: block (kc, ng) = rows kbeg + 8kc .. +7, columns 8ng .. 8ng+7.
+    for (int blk = tid; blk < nkc * (NCOL / 8); blk += 256) {
+      const int ng = blk % (NCOL / 8), kc = blk / (NCOL / 8);
+      const int64_t n = (int64_t)ng * 8;
+      u32x4 r[8], c[8];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t k = (int64_t)(kb + u) * 32 + kg * 8;
-      const bool on = kb + u < kb1;  // uniform
-      edge = edge || !on || (k_tail && kb + u == kb_total - 1);
-      if (!small) {
-        // the K tail's vectors end at the row end; leading extras dropped below
-        const int64_t st = min(k, K - 8);
-        sa[u] = on ? (int)min(k - st, (int64_t)8) : 8;
+      for (int i = 0; i < 8; ++i) {
+        const int64_t k = kbeg + kc * 8 + i;
+        const u32x4 v = load_row(g.B + min(k, K - 1) * ldb, n, N);
+        r[i] = k < K ? v : u32x4{0u, 0u, 0u, 0u};
+      }
+      transpose8x8(r, c);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) fa[u][rb] = load16(g.A + min(row0 + rb * 16, M - 1) * lda + st);
-      } else {
-        sa[u] = 0;
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const u32x4 v = load_row8_small(g.A + min(row0 + rb * 16, M - 1) * lda, k, K);
-          fa[u][rb] = on ? v : u32x4{0u, 0u, 0u, 0u};
-        }
+      for (int j = 0; j < 8; ++j) {
+        const int nn = ng * 8 + j;
+        sBt[nn * KCH + (kc ^ (nn & 15))] = c[j];
       }
     }
+    __syncthreads();
+
+    for (int kb = cb0; kb < cb1; kb += U) {
+      u32x4 fa[U][RB];
+      int sa[U];
+      bool edge = false;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (kb + u >= kb1) break;
-      if (edge && !small) {
+      for (int u = 0; u < U; ++u) {
+        const int64_t k = (int64_t)(kb + u) * 32 + kg * 8;
+        const bool on = kb + u < cb1;  // uniform
+        edge = edge || !on || (k_tail && kb + u == kb_total - 1);
+        if (!small) {
+          // the K tail's vectors end at the row end; leading extras dropped below
+          const int64_t st = min(k, K - 8);
+          sa[u] = on ? (int)min(k - st, (int64_t)8) : 8;
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) fa[u][rb] = shift_down(fa[u][rb], sa[u]);
+          for (int rb = 0; rb < RB; ++rb) fa[u][rb] = load16(g.A + min(row0 + rb * 16, M - 1) * lda + st);
+        } else {
+          sa[u] = 0;
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const u32x4 v = load_row8_small(g.A + min(row0 + rb * 16, M - 1) * lda, k, K);
+            fa[u][rb] = on ? v : u32x4{0u, 0u, 0u, 0u};
+          }
+        }
       }
-      const int kc = (kb + u - kb0) * 4 + kg;
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int nn = nt * 16 + (lane & 15);
-        const u32x4 fb = sBt[nn * KCH + (kc ^ (nn & 15))];
+      for (int u = 0; u < U; ++u) {
+        if (kb + u >= cb1) break;
+        if (edge && !small) {
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) acc[rb][nt] = mfma16(fa[u][rb], fb, acc[rb][nt]);
+          for (int rb = 0; rb < RB; ++rb) fa[u][rb] = shift_down(fa[u][rb], sa[u]);
+        }
+        const int kc = (kb + u - cb0) * 4 + kg;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int nn = nt * 16 + (lane & 15);
+          const u32x4 fb = sBt[nn * KCH + (kc ^ (nn & 15))];
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) acc[rb][nt] = mfma16(fa[u][rb], fb, acc[rb][nt]);
+        }
       }
     }
   }
@@ -948,21 +984,25 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
 }
 
 // -------------------------------------------------------- small-K kernel
-// K <= KMAX (8 or 16): C is a rank-K update, bound by writing C once. Each
-// thread computes 4 rows x 8 columns with fp32 FMAs in ascending k; the B
-// rows it needs (K x 8 columns) and its 4 A rows are loaded once, the output
-// rows are stored as 16-byte (bf16) or 32-byte (fp32) segments. Thread t
-// takes column group t % ceil(N/8) and row group t / ceil(N/8), so
-// neighbouring threads write neighbouring segments of a row.
+// K <= KMAX (8 or 16): C is a rank-K update, bound by writing C once. A
+// thread owns 8 columns and a run of R = g.kper rows (a multiple of 4): it
+// keeps the K x 8 block of B it needs in registers, then for each group of 4
+// rows loads the 4 A rows (K values each), forms the 4 x 8 outputs with fp32
+// FMAs in ascending k and stores them as 16-byte (bf16) or 32-byte (fp32)
+// row segments. Thread t takes column group t % ceil(N/8) and row run
+// t / ceil(N/8), so neighbouring threads write neighbouring segments of a
+// row; B is read once per R rows, the A rows are shared by the threads of a
+// row run.
 template <int KMAX, bool OBF>
 __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
-  constexpr int RT = 4;
   const int64_t M = g.M, N = g.N, K = g.K;
+  const int64_t R = g.kper;
   const int64_t ncg = (N + 7) / 8;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= ncg * ((M + RT - 1) / RT)) return;
+  if (t >= ncg * ((M + R - 1) / R)) return;
   const int64_t rg = t / ncg, cg = t - rg * ncg;
-  const int64_t r0 = rg * RT, c0 = cg * 8;
+  const int64_t r0 = rg * R, c0 = cg * 8;
+  const int64_t rend = min(r0 + R, M);
 
   // B rows 0..K-1, columns c0..c0+7 (zeros past N, rows past K zero)
   float b[KMAX][8];
@@ -976,31 +1016,30 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
       b[k][2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
     }
   }
-  float acc[RT][8];
+  for (int64_t rb = r0; rb < rend; rb += 4) {
+    // the 4 A rows of this group as raw bf16 (rows past M repeat row M-1)
+    u32x4 av[4][KMAX / 8];
 #pragma unroll
-  for (int r = 0; r < RT; ++r) {
-    const int64_t row = min(r0 + r, M - 1);
-    float a[KMAX];
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = min(rb + r, M - 1);
 #pragma unroll
-    for (int h = 0; h < KMAX / 8; ++h) {
-      const u32x4 v = load_row(g.A + row * g.lda, h * 8, K);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a[h * 8 + 2 * e] = __uint_as_float(v[e] << 16);
-        a[h * 8 + 2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
-      }
+      for (int h = 0; h < KMAX / 8; ++h) av[r][h] = load_row(g.A + row * g.lda, h * 8, K);
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      float s = 0.f;
+    for (int r = 0; r < 4; ++r) {
+      float acc[8];
 #pragma unroll
-      for (int k = 0; k < KMAX; ++k) s = __builtin_fmaf(a[k], b[k][j], s);
-      acc[r][j] = s;
+      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+#pragma unroll
+      for (int k = 0; k < KMAX; ++k) {
+        const uint32_t w = av[r][k / 8][(k % 8) / 2];
+        const float a = __uint_as_float((k & 1) ? (w & 0xFFFF0000u) : (w << 16));
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(a, b[k][j], acc[j]);
+      }
+      if (rb + r < rend) store_c8<OBF>(g.C, (rb + r) * g.ldc + c0, acc, N - c0);
     }
   }
-#pragma unroll
-  for (int r = 0; r < RT; ++r)
-    if (r0 + r < M) store_c8<OBF>(g.C, (r0 + r) * g.ldc + c0, acc[r], N - c0);
 }
 
 }  // namespace ac
@@ -1018,23 +1057,35 @@ namespace {
 typedef hipError_t (*LaunchFn)(const Plan&, const GemmArgs&, hipStream_t, bool);
 typedef int (*OccFn)();
 
+// Threads per output group of the reduction: enough threads in flight to
+// cover the partial-slice read latency when the output is small.
+int reduce_lg(int64_t outputs, int pk) {
+  int lg = 0;
+  while (lg < 6 && (2 << lg) <= pk && (outputs << lg) < (1 << 18)) ++lg;
+  return lg;
+}
+
 hipError_t launch_reduce(const GemmArgs& g, hipStream_t st, bool obf) {
   const int64_t n = g.M * ((g.N + 7) / 8);
-  const dim3 grid((unsigned)((n + 255) / 256)), block(256);
+  const int lg = reduce_lg(n, g.pk);
+  const int64_t eb = 256 >> lg;
+  const dim3 grid((unsigned)((n + eb - 1) / eb)), block(256);
   if (obf)
-    hipLaunchKernelGGL((k_reduce<true>), grid, block, 0, st, g);
+    hipLaunchKernelGGL((k_reduce<true>), grid, block, 0, st, g, lg);
   else
-    hipLaunchKernelGGL((k_reduce<false>), grid, block, 0, st, g);
+    hipLaunchKernelGGL((k_reduce<false>), grid, block, 0, st, g, lg);
   return hipGetLastError();
 }
 
 template <int BM, int BN, int MS>
 hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, p.grid_y), block(256);
-  if (obf)
-    hipLaunchKernelGGL((k_tile<BM, BN, MS, true>), grid, block, 0, st, g);
+  if (p.pk > 1)
+    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_PARTIAL>), grid, block, 0, st, g);
+  else if (obf)
+    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_BF16>), grid, block, 0, st, g);
   else
-    hipLaunchKernelGGL((k_tile<BM, BN, MS, false>), grid, block, 0, st, g);
+    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_F32>), grid, block, 0, st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.pk == 1) return e;
   return launch_reduce(g, st, obf);
@@ -1100,7 +1151,9 @@ int occ_of(F kernel_f32, F kernel_bf16) {
 }
 template <int BM, int BN, int MS>
 int occ_tile() {
-  return occ_of(k_tile<BM, BN, MS, false>, k_tile<BM, BN, MS, true>);
+  const int a = occ_of(k_tile<BM, BN, MS, OUT_F32>, k_tile<BM, BN, MS, OUT_BF16>);
+  const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL>, k_tile<BM, BN, MS, OUT_PARTIAL>);
+  return a < b ? a : b;
 }
 template <int BM, int BN, int MS>
 int occ_streamk() {

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 
 namespace ac {
@@ -63,6 +64,7 @@ struct Work {
   double total_write = 0;// bytes written by the main kernel (output or partials)
   int idx = -1;          // configuration index of the calibrated costs
   double setup = 0;      // bytes a workgroup stages before its main loop
+  double extra_lat = 0;  // further dependent load phases (memory latencies)
   double prefetch = 1;   // main-loop iterations of loads in flight
   double total_read = 0; // sum over workgroups of bytes read (Eq. 1 analogue)
   bool unaligned = false;
@@ -95,10 +97,15 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
                            ? hw.cfg_iter[w.idx]
                            : std::max(w.mfma_it / (hw.clock_hz * hw.mfma_eta), w.lds_it / hw.lds_bw_cu);
     const double tP = tP0 * per_cu;
-    const double twg = (w.idx >= 0 && hw.cfg_wg[w.idx] > 0) ? hw.cfg_wg[w.idx] : hw.t_wg;
-    const double t_fill = hw.t_mem_latency + tM + tP;  // first slice: load latency, load, compute
+    // fixed cost of a workgroup: calibrated per configuration (prologue,
+    // first-load latency and epilogue latency together), else the generic
+    // workgroup cost plus one memory latency per dependent load phase
+    const bool cal = w.idx >= 0 && hw.cfg_wg[w.idx] > 0;
+    const double twg = cal ? hw.cfg_wg[w.idx] : hw.t_wg;
+    const double lat = cal ? 0.0 : hw.t_mem_latency;
+    const double t_fill = lat + tM + tP;  // first slice: load latency, load, compute
     const double t_drain = w.out_unit / bw_hbm;
-    const double t_setup = w.setup > 0 ? hw.t_mem_latency + w.setup / bw_l2 : 0.0;
+    const double t_setup = (w.setup > 0 ? lat + w.setup / bw_l2 : 0.0) + w.extra_lat * hw.t_mem_latency;
     const double L = std::max(0.0, w.L);
     if (L == 0) return twg + t_setup + t_drain;
     return twg + t_setup + t_fill + (L - 1) * std::max(tM, tP) + t_drain;  // Eq. 13
@@ -239,7 +246,6 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   const int R = skinny_n_rows(k);
   const int64_t rbk = cdiv(s.M, R);
   const int64_t kb = cdiv(s.K, SKINNY_BK);
-  const int64_t kmax = SKINNY_N_KMAX / SKINNY_BK;
   int64_t pk = 1, kper = kb;
   if (pk_req > 1) {
     if (kb < 2) return false;
@@ -247,7 +253,6 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
     pk = cdiv(kb, kper);
     if (pk != pk_req || pk > 65535) return false;
   }
-  if (kper > kmax) return false;  // B^T slice must fit the LDS buffer
   if (rbk > (1LL << 31) - 1) return false;
   p->family = FAM_SKINNY_N;
   p->cfg = cfg;
@@ -272,7 +277,10 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   w->bytes_it = rows_e * 32 * 2;
   w->mfma_it = (double)k.rb * k.nt * 16;
   w->lds_it = 64.0 * k.nt * 16 * 4;
+  // B staged into LDS chunk by chunk (SKINNY_N_KMAX of K each); every chunk
+  // after the first adds a dependent load phase
   w->setup = (double)kper * 32 * s.N * 2;
+  w->extra_lat = (double)(cdiv(kper * SKINNY_BK, SKINNY_N_KMAX) - 1);
   w->out_unit = rows_e * s.N * (pk == 1 ? c.cbytes : 4);
   w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
   if (pk > 1) {
@@ -291,29 +299,35 @@ bool build_smallk(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   const Shape& s = c.s;
   if (pk_req != 1 || s.K > k.kmax || s.K < 1) return false;
   if (cfg > 0 && s.K <= kSmallKCfg[cfg - 1].kmax) return false;  // a smaller K bound fits
-  const int64_t ncg = cdiv(s.N, 8), nrg = cdiv(s.M, 4);
+  const int64_t ncg = cdiv(s.N, 8);
+  // rows per thread: the longest run (B read once per run) that still leaves
+  // about 2048 threads per CU
+  int64_t rpt = 4;
+  while (rpt < SMALLK_MAX_ROWS && ncg * cdiv(s.M, 2 * rpt) >= (int64_t)c.hw.n_cu * 2048) rpt *= 2;
+  const int64_t nrg = cdiv(s.M, rpt);
   const int64_t wgs = cdiv(ncg * nrg, 256);
   if (wgs > (1LL << 31) - 1) return false;
   p->family = FAM_SMALLK;
   p->cfg = cfg;
-  p->tile_m = 4;
+  p->tile_m = (int)rpt;
   p->tile_n = 8;
   p->tile_k = k.kmax;
   p->pm = (int)std::min<int64_t>(nrg, (1LL << 31) - 1);
   p->pn = (int)ncg;
   p->pk = 1;
-  p->kper = 1;
+  p->kper = (int)rpt;
   p->grid_x = (int)wgs;
   p->grid_y = 1;
   w->units = wgs;
   w->occ = occupancy(FAM_SMALLK, cfg);
   w->idx = IDX_SMALLK + cfg;
-  w->L = 1;
-  // per workgroup: 256 threads x (K B-vectors + 4 A rows), mostly cache hits
-  w->bytes_it = 256.0 * (s.K * 16.0 + 4.0 * 16.0 * (k.kmax / 8));
+  // one iteration = 4 rows of every thread: A rows (shared, cache hits)
+  w->L = (double)rpt / 4;
+  w->bytes_it = 256.0 * 4 * 16.0 * (k.kmax / 8);
   w->mfma_it = 4.0 * 8 * k.kmax * 4;  // FMA issue cycles of one wave (VALU, 4 cycles each)
   w->lds_it = 0;
-  w->out_unit = 256.0 * 4 * 8 * c.cbytes;
+  w->setup = 256.0 * s.K * 16.0;      // the B block of every thread
+  w->out_unit = 256.0 * rpt * 8 * c.cbytes;
   w->total_write = (double)s.M * s.N * c.cbytes;
   w->prefetch = 1;
   w->total_read = c.compulsory;  // re-reads of A rows and B rows stay in L1/L2
@@ -399,17 +413,37 @@ adaptcore_hw_t default_hw() {
   h.s_acc_bytes = 256 * 1024;  // 4 waves x 64 lanes x 256 accumulation registers x 4 B
   h.clock_hz = 2.4e9;
   h.hbm_bw = 8.0e12;
-  h.hbm_eta = 0.80;
-  h.l2_bw_cu = 64.0 * 2.4e9;
-  h.t_launch = 2.0e-6;
-  h.t_mem_latency = 0.8e-6;
-  h.t_wg = 0.2e-6;
   h.mfma_eta = 0.85;
   h.lds_bw_cu = 128.0 * 2.4e9;
-  h.unaligned_eta = 0.85;
-  h.l2_hit = 0.7;
+  h.t_wg = 0.2e-6;
   h.search_open = 0;
   h.enable_streamk = 0;
+  // Constants fitted to per-configuration timings of 150 shapes of the
+  // dynamic-shape, decode-style and small-MN large-K workloads on one MI355X
+  // (squared log error of the model over every measured configuration). The
+  // launch cost is the measured per-kernel floor of back-to-back launches.
+  h.t_launch = 1.9e-06;
+  h.t_mem_latency = 2.797e-06;
+  h.hbm_eta = 0.5673;
+  h.l2_bw_cu = 2.636e+10;
+  h.unaligned_eta = 1;
+  h.l2_hit = 0.4221;
+  // per configuration (tile 0-7, skinny-M 8-13, skinny-N 14-16, small-K
+  // 17-18, stream-K 19-26; 0 = analytic estimate, no timing data)
+  static const double kIter[32] = {
+      2.832e-06, 2.516e-06, 2.304e-06, 1.745e-06, 9.358e-14, 9.358e-14, 1.239e-06, 1.003e-06,
+      9.358e-14, 9.358e-14, 9.358e-14, 2.815e-08, 2.009e-06, 2.275e-06, 5.595e-07, 1.399e-06,
+      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 1.124e-13, 0, 0,
+      9.358e-14, 0, 0, 0, 0, 0, 0, 0};
+  static const double kWg[32] = {
+      1.602e-05, 4.67e-06, 3.346e-06, 2.32e-06, 4.959e-06, 3.442e-06, 4.11e-06, 5.494e-06,
+      3.344e-07, 7.961e-07, 1.991e-06, 3.049e-06, 3.536e-06, 3.595e-06, 9.275e-08, 6.396e-07,
+      1.616e-06, 3.506e-07, 3.529e-07, 1.459e-05, 9.358e-14, 1.951e-06, 0, 0,
+      4.361e-06, 0, 0, 0, 0, 0, 0, 0};
+  for (int i = 0; i < 32; ++i) {
+    h.cfg_iter[i] = kIter[i];
+    h.cfg_wg[i] = kWg[i];
+  }
   return h;
 }
 
@@ -487,29 +521,16 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
   }
   for (int cfg = 0; cfg < N_SKINNY_N_CFG; ++cfg) {
     const int64_t rb = cdiv(s.M, skinny_n_rows(kSkinnyNCfg[cfg]));
-    const int64_t kb = cdiv(s.K, SKINNY_BK);
-    const int64_t min_pk = cdiv(kb, SKINNY_N_KMAX / SKINNY_BK);
     {
       Plan p;
       Work w;
       if (build_skinny_n(c, cfg, 1, &p, &w)) add(p, w);
     }
     for (int pk : kSplits) {
-      if (pk < min_pk) continue;
-      if ((int64_t)pk * rb > 8LL * c.hw.n_cu * kSkinnyNCfg[cfg].occ && pk > min_pk) break;
+      if ((int64_t)pk * rb > 8LL * c.hw.n_cu * kSkinnyNCfg[cfg].occ) break;
       Plan p;
       Work w;
       if (build_skinny_n(c, cfg, pk, &p, &w)) add(p, w);
-    }
-    // splits needed to bound the LDS slice but absent from the list
-    if (min_pk > 1) {
-      Plan p;
-      Work w;
-      const int64_t kper = cdiv(kb, min_pk);
-      const int pk = (int)cdiv(kb, kper);
-      if (std::find(std::begin(kSplits), std::end(kSplits), pk) == std::end(kSplits) &&
-          build_skinny_n(c, cfg, pk, &p, &w))
-        add(p, w);
     }
   }
   for (int cfg = 0; cfg < N_SMALLK_CFG; ++cfg) {
@@ -587,6 +608,44 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
   p.n_candidates = 1;
   *out = p;
   return true;
+}
+
+std::string kernel_names(const Plan& p) {
+  const int obf = p.s.dtype == AC_BF16_BF16OUT;
+  const char* b = obf ? "true" : "false";
+  char buf[160];
+  switch (p.family) {
+    case FAM_TILE: {
+      const TileCfg& t = kTileCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_tile<%d, %d, %d, %d>", t.bm, t.bn, t.ms, p.pk > 1 ? 2 : obf);
+      std::string r(buf);
+      if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
+      return r;
+    }
+    case FAM_STREAMK: {
+      const TileCfg& t = kTileCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_streamk<%d, %d, %d, %s>;k_sk_fixup<%s>", t.bm, t.bn, t.ms, b, b);
+      return buf;
+    }
+    case FAM_SKINNY_M: {
+      const SkinnyMCfg& k = kSkinnyMCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_skinny_m<%d, %d, %s>", k.mt, k.wkw, b);
+      std::string r(buf);
+      if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
+      return r;
+    }
+    case FAM_SKINNY_N: {
+      const SkinnyNCfg& k = kSkinnyNCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_skinny_n<%d, %d, %s>", k.nt, k.rb, b);
+      std::string r(buf);
+      if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
+      return r;
+    }
+    case FAM_SMALLK:
+      std::snprintf(buf, sizeof buf, "k_smallk<%d, %s>", kSmallKCfg[p.cfg].kmax, b);
+      return buf;
+  }
+  return "";
 }
 
 int config_index(int family, int cfg) {

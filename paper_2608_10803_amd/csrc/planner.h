@@ -4,6 +4,7 @@
 #pragma once
 #include <stdint.h>
 
+#include <string>
 #include <vector>
 
 #include "../../include/adaptcore.h"
@@ -65,6 +66,10 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
 // 64-bit shape key: M | N << 17 | K << 34 | dtype << 51 | layouts << 55, for
 // dimensions below 2^17; larger shapes set bit 63 and hash all fields.
 uint64_t shape_key(const Shape& s, bool* exact);
+
+// Kernels one call of the plan launches, ';'-separated (template arguments
+// as a profiler prints them).
+std::string kernel_names(const Plan& p);
 
 // Index of a configuration in the calibrated cost tables of the profile.
 int config_index(int family, int cfg);

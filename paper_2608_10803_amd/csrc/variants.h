@@ -33,7 +33,8 @@ constexpr int N_SKINNY_M_CFG = sizeof(kSkinnyMCfg) / sizeof(kSkinnyMCfg[0]);
 inline int skinny_m_cols(const SkinnyMCfg& c) { return 128 * (4 / c.wkw); }
 
 // Small-N configurations: N <= 16*nt columns, a workgroup covers 64*rb rows
-// and at most SKINNY_N_KMAX of K (the B^T slice it keeps in LDS).
+// and walks its K range in chunks of SKINNY_N_KMAX (the B^T slice it keeps
+// in LDS).
 struct SkinnyNCfg {
   int nt, rb, occ;
 };
@@ -42,12 +43,14 @@ constexpr SkinnyNCfg kSkinnyNCfg[] = {{1, 2, 4}, {2, 2, 4}, {4, 2, 2}};
 constexpr int N_SKINNY_N_CFG = sizeof(kSkinnyNCfg) / sizeof(kSkinnyNCfg[0]);
 inline int skinny_n_rows(const SkinnyNCfg& c) { return 64 * c.rb; }
 
-// Small-K configurations: K <= kmax; a thread computes 4 rows x 8 columns.
+// Small-K configurations: K <= kmax; a thread computes a run of rows (a
+// multiple of 4, at most SMALLK_MAX_ROWS) x 8 columns.
 struct SmallKCfg {
   int kmax, occ;
 };
 constexpr SmallKCfg kSmallKCfg[] = {{8, 4}, {16, 2}};
 constexpr int N_SMALLK_CFG = sizeof(kSmallKCfg) / sizeof(kSmallKCfg[0]);
+constexpr int SMALLK_MAX_ROWS = 32;
 
 // 64-bit key of a configuration:
 //   bits  0- 3 family, 4-11 config index, 12 swizzle, 16-35 P_k (or the

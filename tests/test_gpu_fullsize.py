@@ -1,0 +1,166 @@
+"""Parity at the full workload sizes, in the configuration the benchmark runs
+(the planner's own choice for each shape, packed row-major operands).
+
+The outputs are too large for the oracle to compute whole, so each shape is
+checked on sampled entries: the four corners, the last rows and columns of
+ragged tiles and a seeded random sample. The oracle computes those entries
+one by one from the A rows and B columns they need, read back from the
+device buffers the kernels consumed (the inputs come from torch's seeded
+generator, never from this library). Bar: the error metric per entry,
+|C - C_ref| / sum_k |A_ik B_kj|, within the tolerance of the output type.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2608_10803_amd as ac
+from oracle import gemm_ref
+from workloads import gen
+
+from gpu_util import tol
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16 = ac.AC_BF16_F32OUT, ac.AC_BF16_BF16OUT
+N_RANDOM = 28
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU tests need a GPU")
+    return torch
+
+
+class Arena:
+    """Device buffers large enough for every operand of a workload; operand
+    values drawn once per buffer from a seeded generator."""
+
+    def __init__(self, shapes, dtype, seed, dist="uniform"):
+        t = _torch()
+        self.t = t
+        na = max(max(M * K for M, N, K in shapes), 1)
+        nb = max(max(K * N for M, N, K in shapes), 1)
+        nc = max(max(M * N for M, N, K in shapes), 1)
+        g = t.Generator(device="cuda")
+        g.manual_seed(seed)
+        self.A = t.empty(na, dtype=t.bfloat16, device="cuda")
+        self.B = t.empty(nb, dtype=t.bfloat16, device="cuda")
+        if dist == "uniform":
+            self.A.uniform_(-1, 1, generator=g)
+            self.B.uniform_(-1, 1, generator=g)
+        self.dist = dist
+        self.g = g
+        self.C = t.empty(nc, dtype=t.float32 if dtype == F32 else t.bfloat16, device="cuda")
+
+    def fill_normal(self, M, N, K):
+        s = 1.0 / math.sqrt(K)
+        self.A[:M * K].normal_(0.0, s, generator=self.g)
+        self.B[:K * N].normal_(0.0, s, generator=self.g)
+
+
+def sample_entries(M, N, seed, tile=256):
+    rng = np.random.default_rng(seed)
+    I = [0, M - 1, 0, M - 1, (M - 1) // tile * tile, M - 1, max(M - 1 - tile // 2, 0)]
+    J = [0, N - 1, N - 1, 0, N - 1, (N - 1) // tile * tile, max(N - 1 - tile // 2, 0)]
+    I += list(rng.integers(0, M, N_RANDOM))
+    J += list(rng.integers(0, N, N_RANDOM))
+    return np.array(I, np.int64), np.array(J, np.int64)
+
+
+def check_shape(arena, M, N, K, dtype, seed, label):
+    t = arena.t
+    plan = ac.adaptcore_plan(M, N, K, dtype, 0)
+    A = arena.A[:M * K].view(M, K) if K else arena.A[:0]
+    B = arena.B[:K * N].view(K, N) if K else arena.B[:0]
+    C = arena.C[:M * N].view(M, N)
+    C.fill_(float("nan"))
+    ac.adaptcore_matmul(plan, arena.A.data_ptr(), max(K, 1), arena.B.data_ptr(), max(N, 1),
+                        arena.C.data_ptr(), max(N, 1), 0)
+    t.cuda.synchronize()
+    I, J = sample_entries(M, N, seed)
+    got = C[t.from_numpy(I).cuda(), t.from_numpy(J).cuda()]
+    if dtype == F32:
+        vals = got.cpu().numpy().astype(np.float64)
+    else:
+        vals = gemm_ref.decode(got.view(t.int16).cpu().numpy().view(np.uint16))
+    # the A rows and B columns the sampled entries need, as raw bf16 bits
+    ui, inv_i = np.unique(I, return_inverse=True)
+    uj, inv_j = np.unique(J, return_inverse=True)
+    Ar = A[t.from_numpy(ui).cuda()].contiguous().view(t.int16).cpu().numpy().view(np.uint16)
+    Bc = B[:, t.from_numpy(uj).cuda()].contiguous().view(t.int16).cpu().numpy().view(np.uint16)
+    C_ref, D = gemm_ref.gemm_entries(Ar, Bc, inv_i, inv_j, M=len(ui), N=len(uj), K=K)
+    err = gemm_ref.err_metric(vals, C_ref, D)
+    d = ac.adaptcore_plan_info(plan)
+    assert err <= tol(dtype), "%s %s err %.3g (%s %dx%d pk %d)" % (
+        label, (M, N, K), err, d["family_name"], d["tile_m"], d["tile_n"], d["pk"])
+    return err, d["family_name"]
+
+
+def _progress(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def test_single_512_full_output():
+    """The 512^3 case with fp32 output: every entry against the oracle."""
+    t = _torch()
+    (M, N, K), = gen.single_512()
+    A, B = gen.operands(M, N, K, seed=1)
+    C_ref, D = gemm_ref.gemm(A, B)
+    plan = ac.adaptcore_plan(M, N, K, F32, 0)
+    Ad = t.from_numpy(A.view(np.int16)).cuda()
+    Bd = t.from_numpy(B.view(np.int16)).cuda()
+    Cd = t.full((M, N), float("nan"), dtype=t.float32, device="cuda")
+    ac.adaptcore_matmul(plan, Ad.data_ptr(), K, Bd.data_ptr(), N, Cd.data_ptr(), N, 0)
+    t.cuda.synchronize()
+    err = gemm_ref.err_metric(Cd.cpu().numpy().astype(np.float64), C_ref, D)
+    assert err <= tol(F32), err
+
+
+def test_skinny_m_full_size():
+    shapes = gen.skinny_m()
+    arena = Arena(shapes, BF16, seed=2)
+    for i, (M, N, K) in enumerate(shapes):
+        _progress("skinny %s" % ((M, N, K),))
+        check_shape(arena, M, N, K, BF16, 100 + i, "skinny-M")
+
+
+def test_small_mn_large_k_full_size():
+    shapes = gen.small_mn_large_k()
+    arena = Arena(shapes, F32, seed=3, dist="normal")
+    for i, (M, N, K) in enumerate(shapes):
+        _progress("split-K %s" % ((M, N, K),))
+        arena.fill_normal(M, N, K)
+        check_shape(arena, M, N, K, F32, 200 + i, "small-MN large-K")
+
+
+def test_sweep_full_size():
+    """Every shape of the 2,000-shape sweep, each with its planned
+    configuration, on sampled entries."""
+    shapes = gen.sweep()
+    arena = Arena(shapes, BF16, seed=4)
+    fams = {}
+    for i, (M, N, K) in enumerate(shapes):
+        if i % 250 == 0:
+            _progress("sweep %d/%d" % (i, len(shapes)))
+        _, f = check_shape(arena, M, N, K, BF16, 1000 + i, "sweep #%d" % i)
+        fams[f] = fams.get(f, 0) + 1
+    _progress("sweep families %s" % fams)
+
+
+def test_moe_stream_full_size():
+    """Two routing steps of the MoE stream: every expert's up- and
+    down-projection (including experts with no tokens)."""
+    shapes = []
+    for counts in gen.moe_counts(steps=2):
+        shapes += [(M, N, K) for (_, _, M, N, K) in gen.moe_shapes(counts)]
+    arena = Arena([s for s in shapes if s[0] > 0] or [(1, 1, 1)], BF16, seed=5)
+    for i, (M, N, K) in enumerate(shapes):
+        if M == 0:
+            plan = ac.adaptcore_plan(M, N, K, BF16, 0)
+            ac.adaptcore_matmul(plan, arena.A.data_ptr(), K, arena.B.data_ptr(), N, arena.C.data_ptr(), N, 0)
+            continue
+        check_shape(arena, M, N, K, BF16, 5000 + i, "moe #%d" % i)
