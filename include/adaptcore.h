@@ -69,7 +69,8 @@ typedef enum {
   AC_FAMILY_SKINNY_M = 1, /* Small-M Copy module: B streamed once, M <= 64 */
   AC_FAMILY_SKINNY_N = 2, /* Small-M Copy by orientation: A streamed once, N <= 64 */
   AC_FAMILY_STREAMK = 3,  /* StreamK applied to the tile kernel */
-  AC_FAMILY_SMALLK = 4    /* K <= 16: rank-K update bound by writing C */
+  AC_FAMILY_SMALLK = 4,   /* K <= 16: rank-K update bound by writing C */
+  AC_FAMILY_DIRECT = 5    /* small problems: MFMA fragments straight from memory, no LDS */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */
@@ -166,9 +167,17 @@ const adaptcore_plan_t* adaptcore_plan(int64_t M, int64_t N, int64_t K, int32_t 
 const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, int32_t dtype,
                                                uint32_t layouts, uint64_t variant_key);
 
+/* Largest leading dimension (exclusive, in elements) of A and B accepted by
+ * adaptcore_matmul: the kernels address operand tiles with 32-bit byte
+ * offsets from a row base. */
+#define AC_MAX_LD (1LL << 23)
+
 /* Runs a plan: C = A * B, asynchronously on `stream` (a hipStream_t; NULL is
  * the null stream). Validates the leading dimensions against the plan's
- * shape. M == 0 or N == 0: nothing is launched. K == 0: C is set to zero.
+ * shape (lda >= K, ldb >= N, ldc >= N, all >= 1: AC_ERR_INVALID_VALUE;
+ * lda or ldb >= AC_MAX_LD: AC_ERR_UNSUPPORTED) and the pointer alignment
+ * (A, B: 2 bytes; C: its element size). M == 0 or N == 0: nothing is
+ * launched. K == 0: C is set to zero.
  * Split-K plans use a workspace owned by the library for this (device,
  * stream); it is allocated on the stream's first use (outside any stream
  * capture: under capture a missing workspace gives AC_ERR_NOT_INITIALIZED)

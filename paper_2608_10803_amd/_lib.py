@@ -23,10 +23,10 @@ AC_ERR_INTERNAL = -6
 AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
 AC_LAYOUT_ROW_ROW = 0
-AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK = range(5)
+AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT = range(6)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
-FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct"]
 
 
 class AdaptCoreError(RuntimeError):

@@ -12,7 +12,7 @@
 #include <tuple>
 #include <vector>
 
-#include "../../include/adaptcore.h"
+#include "adaptcore.h"
 #include "planner.h"
 #include "registry.h"
 
@@ -305,6 +305,9 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   if (M == 0 || N == 0) return AC_OK;
   if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
     return fail(AC_ERR_INVALID_VALUE, "leading dimension smaller than the row length");
+  // the kernels address A and B tiles with 32-bit byte offsets from a row base
+  if (lda >= AC_MAX_LD || ldb >= AC_MAX_LD)
+    return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
   if (!C || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null matrix pointer");
   const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
   if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)))

@@ -12,7 +12,8 @@ enum Family : int {
   FAM_SKINNY_N = 2,  // the same module by orientation: A streamed once, N <= 64
   FAM_STREAMK = 3,   // StreamK applied to the tile kernel (Section 4.2)
   FAM_SMALLK = 4,    // K <= 16: rank-K update, bound by writing C
-  FAM_COUNT = 5
+  FAM_DIRECT = 5,    // small problems: MFMA fragments loaded straight from memory
+  FAM_COUNT = 6
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N

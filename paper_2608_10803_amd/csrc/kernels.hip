@@ -15,6 +15,8 @@
 //   k_skinny_n  the same module for N <= 64: A streamed once, the small B is
 //               kept resident in LDS (L1 Resident module, Table 2).
 //   k_smallk    K <= 16: rank-K update with fp32 FMAs, bound by writing C once.
+//   k_direct    small problems: MFMA fragments straight from global memory,
+//               no LDS staging, the fewest instructions between load and store.
 //   k_reduce    deterministic cross-workgroup reduction of split-K partials:
 //               sum in partition order 0, 1, ..., P_k - 1, then cast.
 //
@@ -198,7 +200,8 @@ struct TileShape {
   static constexpr int IA = (AV + NT - 1) / NT;
   static constexpr int IB = (BN + NT - 1) / NT;  // 8x8 blocks of a B stage (BK/8 * BN/8 = BN)
   static constexpr int AB_BYTES = 2 * (BM + BN) * CH * 16;  // double-buffered A and B stages
-  static constexpr int CT_BYTES = BM * BN * 2;                // bf16 output tile
+  static constexpr int CT_LD = BN + 4;                        // padded LDS row of the output tile
+  static constexpr int CT_BYTES = BM * CT_LD * 2;             // bf16 output tile
   static constexpr int SMEM = AB_BYTES > CT_BYTES ? AB_BYTES : CT_BYTES;
   static_assert(WTM % MS == 0 && WTN % MS == 0, "wave tile must be a multiple of the MFMA tile");
 };
@@ -397,10 +400,12 @@ __device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0
       for (int i = 0; i < S::TM; ++i)
 #pragma unroll
         for (int j = 0; j < S::TN; ++j) {
+          // operands swapped: the MFMA forms the transposed tile, so a lane
+          // holds one row of C and runs of 4 consecutive columns
           if constexpr (MS == 32)
-            acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
+            acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
           else
-            acc[i][j] = mfma16(fa[i], fb[j], acc[i][j]);
+            acc[i][j] = mfma16(fb[j], fa[i], acc[i][j]);
         }
     }
   };
@@ -414,39 +419,62 @@ __device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0
       st.load(g, o, m0, n0, kt);
   };
 
-  // The loop bodies are straight-line: the prefetch past the last block
-  // reloads the last block and the store of an unused stage is harmless, so
-  // no branch (and no conservative wait at a branch join) splits the pipeline.
+  // The loop bodies are straight-line (no per-lane branch, so no conservative
+  // wait at a branch join splits the pipeline) and every load they issue is
+  // of a block that is used: the last blocks are peeled off the loops.
   if constexpr (TileDepth<BM, BN>::value == 1) {
     Stage<BM, BN, MS> st;
     load(st, kt0);
     st.store(sA0, sB0, edge(kt0), o.b_cs);
     __syncthreads();
-    for (int kt = kt0; kt < kt1; ++kt) {
-      const int nx = min(kt + 1, kt1 - 1);
+    int kt = kt0;
+    for (; kt + 1 < kt1; ++kt) {
       const bool odd = ((kt - kt0) & 1) != 0;  // uniform
-      load(st, nx);
+      load(st, kt + 1);
       compute(odd ? sA1 : sA0, odd ? sB1 : sB0);
-      st.store(odd ? sA0 : sA1, odd ? sB0 : sB1, edge(nx), o.b_cs);
+      st.store(odd ? sA0 : sA1, odd ? sB0 : sB1, edge(kt + 1), o.b_cs);
       __syncthreads();
     }
+    const bool odd = ((kt - kt0) & 1) != 0;
+    compute(odd ? sA1 : sA0, odd ? sB1 : sB0);
   } else {
     Stage<BM, BN, MS> s0, s1;
+    if (kt0 + 1 == kt1) {  // a single block
+      load(s0, kt0);
+      s0.store(sA0, sB0, edge(kt0), o.b_cs);
+      __syncthreads();
+      compute(sA0, sB0);
+      return;
+    }
     load(s0, kt0);
-    load(s1, min(kt0 + 1, kt1 - 1));
+    load(s1, kt0 + 1);
     s0.store(sA0, sB0, edge(kt0), o.b_cs);
     __syncthreads();
-    for (int kt = kt0; kt < kt1; kt += 2) {
-      const int n1 = min(kt + 1, kt1 - 1), n2 = min(kt + 2, kt1 - 1), n3 = min(kt + 3, kt1 - 1);
-      load(s0, n2);
+    int kt = kt0;
+    for (; kt + 3 < kt1; kt += 2) {  // blocks kt + 2 and kt + 3 exist
+      load(s0, kt + 2);
       compute(sA0, sB0);
-      s1.store(sA1, sB1, edge(n1), o.b_cs);
+      s1.store(sA1, sB1, edge(kt + 1), o.b_cs);
       __syncthreads();
-      if (kt + 1 >= kt1) break;
-      load(s1, n3);
+      load(s1, kt + 3);
       compute(sA1, sB1);
-      s0.store(sA0, sB0, edge(n2), o.b_cs);
+      s0.store(sA0, sB0, edge(kt + 2), o.b_cs);
       __syncthreads();
+    }
+    if (kt + 2 < kt1) {  // three blocks left: kt (in LDS), kt + 1 (in s1), kt + 2
+      load(s0, kt + 2);
+      compute(sA0, sB0);
+      s1.store(sA1, sB1, edge(kt + 1), o.b_cs);
+      __syncthreads();
+      compute(sA1, sB1);
+      s0.store(sA0, sB0, edge(kt + 2), o.b_cs);
+      __syncthreads();
+      compute(sA0, sB0);
+    } else {  // two blocks left: kt (in LDS), kt + 1 (in s1)
+      compute(sA0, sB0);
+      s1.store(sA1, sB1, edge(kt + 1), o.b_cs);
+      __syncthreads();
+      compute(sA1, sB1);
     }
   }
 }
@@ -463,9 +491,11 @@ __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int
     tile_mainloop_impl<BM, BN, MS, false>(g, m0, n0, kt0, kt1, acc, smem);
 }
 
-// Row (within the MFMA block) of accumulator element r of this lane.
+// Column (within the MFMA block) of accumulator element r of this lane; the
+// lane's row is lane % MS (the MFMA forms the transposed block). Elements
+// 4q .. 4q+3 are four consecutive columns.
 template <int MS>
-__device__ __forceinline__ int acc_row(int r, int lane) {
+__device__ __forceinline__ int acc_col(int r, int lane) {
   if constexpr (MS == 32)
     return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
   else
@@ -483,20 +513,30 @@ __device__ __forceinline__ void store_acc_f32(const typename AccOf<MS>::T (&acc)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wr = wave >> 1, wc = wave & 1;
 #pragma unroll
-  for (int i = 0; i < S::TM; ++i)
+  for (int i = 0; i < S::TM; ++i) {
+    const int64_t row = m0 + wr * S::WTM + i * MS + (lane % MS);
+    if (row >= rmax) continue;
 #pragma unroll
-    for (int j = 0; j < S::TN; ++j) {
-      const int64_t col = n0 + wc * S::WTN + j * MS + (lane % MS);
+    for (int j = 0; j < S::TN; ++j)
 #pragma unroll
-      for (int r = 0; r < S::NA; ++r) {
-        const int64_t row = m0 + wr * S::WTM + i * MS + acc_row<MS>(r, lane);
-        if (row < rmax && col < cmax) dst[row * ld + col] = acc[i][j][r];
+      for (int q = 0; q < S::NA / 4; ++q) {
+        // elements 4q .. 4q+3: four consecutive columns of the lane's row
+        const int64_t col = n0 + wc * S::WTN + j * MS + acc_col<MS>(4 * q, lane);
+        float* d = dst + row * ld + col;
+        if (col + 4 <= cmax) {
+          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          __builtin_memcpy(d, &v, 16);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < cmax) d[e] = acc[i][j][4 * q + e];
+        }
       }
-    }
+  }
 }
 
-// bf16 output through LDS: the tile is converted into LDS row-major, then
-// written with 16-byte row segments.
+// bf16 output through LDS: the tile is converted into LDS row-major (rows
+// padded to BN + 4 elements), then written with 16-byte row segments.
 template <int BM, int BN, int MS>
 __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                              [TileShape<BM, BN, MS>::TN],
@@ -506,17 +546,20 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
   const int wr = wave >> 1, wc = wave & 1;
   uint16_t* ct = reinterpret_cast<uint16_t*>(smem);
   __syncthreads();  // the main loop's last reads of the LDS stages are done
-  // row of accumulator element r = lane part + constant part
-  const int lrow = MS == 32 ? (lane >> 5) * 4 : (lane >> 4) * 4;
+  // the lane's row of each MFMA tile, written 4 columns (8 bytes) at a time
 #pragma unroll
   for (int i = 0; i < S::TM; ++i)
 #pragma unroll
     for (int j = 0; j < S::TN; ++j) {
-      uint16_t* base = ct + (wr * S::WTM + i * MS + lrow) * BN + wc * S::WTN + j * MS + (lane % MS);
+      // rows padded by 8 bytes: the 32 lanes writing 32 rows of one column
+      // group fall on different banks
+      uint16_t* base = ct + (wr * S::WTM + i * MS + (lane % MS)) * S::CT_LD + wc * S::WTN + j * MS;
 #pragma unroll
-      for (int r = 0; r < S::NA; ++r) {
-        const int crow = MS == 32 ? (r >> 2) * 8 + (r & 3) : r;
-        base[crow * BN] = to_bf16(acc[i][j][r]);
+      for (int q = 0; q < S::NA / 4; ++q) {
+        const uint32_t lo = (uint32_t)to_bf16(acc[i][j][4 * q]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 3]) << 16);
+        const uint64_t v = (uint64_t)lo | ((uint64_t)hi << 32);
+        *reinterpret_cast<uint64_t*>(base + acc_col<MS>(4 * q, lane)) = v;
       }
       __builtin_amdgcn_sched_barrier(0);  // convert block by block (bounded live registers)
     }
@@ -527,11 +570,14 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
     const int row = e / GPR, grp = e % GPR;
     const int64_t gr = m0 + row, gc = n0 + grp * 8;
     if (gr >= g.M || gc >= g.N) continue;
-    const uint16_t* src = ct + row * BN + grp * 8;
+    const uint16_t* src = ct + row * S::CT_LD + grp * 8;
     uint16_t* dst = C + gr * g.ldc + gc;
     if (gc + 8 <= g.N) {
-      u32x4 v = *reinterpret_cast<const u32x4*>(src);
-      __builtin_memcpy(dst, &v, 16);
+      // the padded rows are 8-byte aligned in LDS: two 8-byte reads
+      const uint64_t lo = *reinterpret_cast<const uint64_t*>(src);
+      const uint64_t hi = *reinterpret_cast<const uint64_t*>(src + 4);
+      const uint64_t v[2] = {lo, hi};
+      __builtin_memcpy(dst, v, 16);
     } else {
       for (int j = 0; j < (int)(g.N - gc); ++j) dst[j] = src[j];
     }
@@ -1042,6 +1088,153 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
   }
 }
 
+// ---------------------------------------------------------- direct kernel
+// Latency-lean kernel for small problems: no LDS staging, no register
+// transposes. A wave computes one 32 x 32 block of C with 32x32x16 MFMAs,
+// reading its operand fragments straight from global memory (they come from
+// cache): lane l takes row l % 32 of A and column l % 32 of B, k-group l / 32
+// (8 consecutive k). The A fragment is one 16-byte load; the B fragment is 8
+// two-byte loads down the column. B is passed as the MFMA's first operand, so
+// the accumulators hold the transposed block: one row of C per lane, in runs
+// of four consecutive columns (8- or 16-byte stores). Rows past M and columns past N are clamped
+// (their results are never stored); k past K reads as zero. WK = 1: the four
+// waves cover a 64 x 64 block of C, each over all of K. WK = 4: the four waves
+// split the 32-k blocks of one 32 x 32 block evenly and wave 0 adds the four
+// partial sums in wave order through LDS.
+template <int WK, int OUT>
+__global__ __launch_bounds__(256) void k_direct(GemmArgs g) {
+  constexpr int U = 4;  // 32-k blocks whose loads are issued together
+  __shared__ f32x16 red[WK > 1 ? (WK - 1) * 64 : 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t M = g.M, N = g.N, K = g.K;
+  const int tm = blockIdx.x / g.tiles_n, tn = blockIdx.x - tm * g.tiles_n;
+  int64_t m0, n0;
+  int kb0, kb1;
+  const int kb_total = (int)((K + 31) / 32);
+  // this workgroup's K partition (P_k > 1: blockIdx.y of g.pk, g.kper blocks)
+  const int split = blockIdx.y;
+  const int pb0 = min(split * g.kper, kb_total), pb1 = min(pb0 + g.kper, kb_total);
+  if constexpr (WK == 1) {
+    m0 = (int64_t)tm * 64 + (wave >> 1) * 32;
+    n0 = (int64_t)tn * 64 + (wave & 1) * 32;
+    kb0 = pb0;
+    kb1 = pb1;
+  } else {
+    m0 = (int64_t)tm * 32;
+    n0 = (int64_t)tn * 32;
+    const int per = (pb1 - pb0 + WK - 1) / WK;
+    kb0 = min(pb0 + wave * per, pb1);
+    kb1 = min(kb0 + per, pb1);
+  }
+  const int kg = lane >> 5;
+  const int64_t lda = g.lda, ldb = g.ldb;
+  // Loads take a wave-uniform base (row m0 of A, row k of B) plus a per-lane
+  // 32-bit byte offset (the host keeps lda, ldb < 2^23), so the address
+  // arithmetic runs on the scalar unit.
+  // (A's base row is clamped like the lanes' rows: a wave of the 64 x 64
+  // layout can start past M, and the offsets must stay non-negative.)
+  const int64_t ma = min(m0, M - 1);
+  const uint32_t a_off = (uint32_t)(((min(m0 + (lane & 31), M - 1) - ma) * lda + kg * 8) * 2);
+  const uint32_t b_off = (uint32_t)((min(n0 + (lane & 31), N - 1) + (int64_t)kg * 8 * ldb) * 2);
+  const uint16_t* A0 = g.A + ma * lda;
+
+  f32x16 acc = {};
+  // whole 32-k blocks: no k checks
+  const int kbf = min(kb1, (int)(K / 32));
+  int kb = kb0;
+  auto block = [&](int kbk, u32x4 (&a)[2], u32x4 (&b)[2]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t k = (int64_t)kbk * 32 + h * 16;
+      a[h] = load16(at(A0 + k, a_off));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t lo = *at(g.B + (k + 2 * e) * ldb, b_off);
+        const uint32_t hi = *at(g.B + (k + 2 * e + 1) * ldb, b_off);
+        b[h][e] = lo | (hi << 16);
+      }
+    }
+  };
+  for (; kb + U <= kbf; kb += U) {
+    u32x4 a[U][2], b[U][2];
+#pragma unroll
+    for (int u = 0; u < U; ++u) block(kb + u, a[u], b[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) acc = mfma32(b[u][h], a[u][h], acc);
+  }
+  for (; kb < kbf; ++kb) {
+    u32x4 a[2], b[2];
+    block(kb, a, b);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) acc = mfma32(b[h], a[h], acc);
+  }
+  const uint16_t* pa = g.A + min(m0 + (lane & 31), M - 1) * lda + kg * 8;
+  const uint16_t* pb = g.B + min(n0 + (lane & 31), N - 1) + (int64_t)kg * 8 * ldb;
+  // the partial last 32-k block (if this wave owns it): element loads, zero past K
+  if (kb < kb1) {
+    const int64_t kbase = (int64_t)kb * 32 + kg * 8;
+    const uint16_t* ra = pa - kg * 8;
+    const uint16_t* cb = pb - (int64_t)kg * 8 * ldb;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      u32x4 a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        // clamped loads are always in bounds; issue them unconditionally and
+        // zero the values past K afterwards
+        const int64_t k0 = kbase + h * 16 + 2 * e, k1 = k0 + 1;
+        const int64_t c0 = min(k0, K - 1), c1 = min(k1, K - 1);
+        const uint32_t va0 = ra[c0], va1 = ra[c1], vb0 = cb[c0 * ldb], vb1 = cb[c1 * ldb];
+        a[e] = (k0 < K ? va0 : 0u) | ((k1 < K ? va1 : 0u) << 16);
+        b[e] = (k0 < K ? vb0 : 0u) | ((k1 < K ? vb1 : 0u) << 16);
+      }
+      acc = mfma32(b, a, acc);
+    }
+  }
+
+  if constexpr (WK > 1) {
+    if (wave > 0) red[(wave - 1) * 64 + lane] = acc;
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int w = 1; w < WK; ++w) acc += red[(w - 1) * 64 + lane];
+  }
+  // (operands swapped: the MFMA forms the transposed block) the lane holds
+  // row m0 + lane % 32 and, for q = 0..3, the four consecutive columns
+  // n0 + 8q + 4 * (lane / 32) .. +3
+  const int64_t row = m0 + (lane & 31);
+  if (row >= M) return;
+  float* part = g.ws + (size_t)split * (size_t)M * (size_t)g.ldw;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int64_t col = n0 + 8 * q + 4 * (lane >> 5);
+    const float v[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+    if (col + 4 <= N) {
+      if constexpr (OUT == OUT_PARTIAL) {
+        __builtin_memcpy(part + row * g.ldw + col, v, 16);
+      } else if constexpr (OUT == OUT_BF16) {
+        const uint32_t lo = (uint32_t)to_bf16(v[0]) | ((uint32_t)to_bf16(v[1]) << 16);
+        const uint32_t hi = (uint32_t)to_bf16(v[2]) | ((uint32_t)to_bf16(v[3]) << 16);
+        const uint64_t w = (uint64_t)lo | ((uint64_t)hi << 32);
+        __builtin_memcpy(static_cast<uint16_t*>(g.C) + row * g.ldc + col, &w, 8);
+      } else {
+        __builtin_memcpy(static_cast<float*>(g.C) + row * g.ldc + col, v, 16);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (col + e >= N) break;
+        if constexpr (OUT == OUT_PARTIAL)
+          part[row * g.ldw + col + e] = v[e];
+        else
+          store_c<OUT == OUT_BF16>(g.C, row * g.ldc + col + e, v[e]);
+      }
+    }
+  }
+}
+
 }  // namespace ac
 
 // ------------------------------------------------------------- registry
@@ -1140,6 +1333,20 @@ hipError_t launch_smallk(const Plan& p, const GemmArgs& g, hipStream_t st, bool 
   return hipGetLastError();
 }
 
+template <int WK>
+hipError_t launch_direct(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
+  const dim3 grid(p.grid_x, p.grid_y), block(256);
+  if (p.pk > 1)
+    hipLaunchKernelGGL((k_direct<WK, OUT_PARTIAL>), grid, block, 0, st, g);
+  else if (obf)
+    hipLaunchKernelGGL((k_direct<WK, OUT_BF16>), grid, block, 0, st, g);
+  else
+    hipLaunchKernelGGL((k_direct<WK, OUT_F32>), grid, block, 0, st, g);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.pk == 1) return e;
+  return launch_reduce(g, st, obf);
+}
+
 template <typename F>
 int occ_of(F kernel_f32, F kernel_bf16) {
   int a = 0, b = 0;
@@ -1188,7 +1395,18 @@ template <int KMAX>
 int occ_smallk() {
   return occ_of(k_smallk<KMAX, false>, k_smallk<KMAX, true>);
 }
+template <int WK>
+int occ_direct() {
+  const int a = occ_of(k_direct<WK, OUT_F32>, k_direct<WK, OUT_BF16>);
+  const int b = occ_of(k_direct<WK, OUT_PARTIAL>, k_direct<WK, OUT_PARTIAL>);
+  return a < b ? a : b;
+}
+
 const LaunchFn kSmallKFns[] = {&launch_smallk<8>, &launch_smallk<16>};
+const LaunchFn kDirectFns[] = {&launch_direct<1>, &launch_direct<4>};
+const OccFn kDirectOcc[] = {&occ_direct<1>, &occ_direct<4>};
+static_assert(sizeof(kDirectFns) / sizeof(kDirectFns[0]) == N_DIRECT_CFG, "direct table");
+static_assert(kDirectCfg[0].wk == 1 && kDirectCfg[1].wk == 4, "direct order");
 const OccFn kSmallKOcc[] = {&occ_smallk<8>, &occ_smallk<16>};
 static_assert(sizeof(kSmallKFns) / sizeof(kSmallKFns[0]) == N_SMALLK_CFG, "small-K table");
 static_assert(kSmallKCfg[0].kmax == 8 && kSmallKCfg[1].kmax == 16, "small-K order");
@@ -1224,6 +1442,8 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       return kSkinnyNFns[p.cfg](p, g, st, obf);
     case FAM_SMALLK:
       return kSmallKFns[p.cfg](p, g, st, obf);
+    case FAM_DIRECT:
+      return kDirectFns[p.cfg](p, g, st, obf);
   }
   return hipErrorInvalidValue;
 }
@@ -1236,6 +1456,7 @@ void query_occupancy() {
   for (int i = 0; i < N_SKINNY_M_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_M, i, kSkinnyMOcc[i]());
   for (int i = 0; i < N_SKINNY_N_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_N, i, kSkinnyNOcc[i]());
   for (int i = 0; i < N_SMALLK_CFG; ++i) set_runtime_occupancy(FAM_SMALLK, i, kSmallKOcc[i]());
+  for (int i = 0; i < N_DIRECT_CFG; ++i) set_runtime_occupancy(FAM_DIRECT, i, kDirectOcc[i]());
 }
 
 }  // namespace ac

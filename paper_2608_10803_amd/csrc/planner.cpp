@@ -31,6 +31,8 @@ int table_occ(int family, int cfg) {
       return kSkinnyNCfg[cfg].occ;
     case FAM_SMALLK:
       return kSmallKCfg[cfg].occ;
+    case FAM_DIRECT:
+      return kDirectCfg[cfg].occ;
   }
   return 1;
 }
@@ -43,7 +45,8 @@ constexpr int IDX_SKINNY_M = IDX_TILE + N_TILE_CFG;
 constexpr int IDX_SKINNY_N = IDX_SKINNY_M + N_SKINNY_M_CFG;
 constexpr int IDX_SMALLK = IDX_SKINNY_N + N_SKINNY_N_CFG;
 constexpr int IDX_STREAMK = IDX_SMALLK + N_SMALLK_CFG;
-static_assert(IDX_STREAMK + N_TILE_CFG <= 32, "calibrated cost tables");
+constexpr int IDX_DIRECT = IDX_STREAMK + N_TILE_CFG;
+static_assert(IDX_DIRECT + N_DIRECT_CFG <= 32, "calibrated cost tables");
 
 // Tiles the taxonomy uses for its spatial predicate: the menu entries whose
 // accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
@@ -293,6 +296,62 @@ bool build_skinny_n(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   return true;
 }
 
+// Small problems: MFMA fragments straight from global memory, no LDS. One
+// workgroup per 64 x 64 (wk = 1) or per 32 x 32 block of C with K split over
+// its four waves (wk = 4).
+bool build_direct(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
+  const DirectCfg& d = kDirectCfg[cfg];
+  const Shape& s = c.s;
+  if (s.K < 1) return false;
+  const int T = direct_tile(d);
+  const int64_t tm = cdiv(s.M, T), tn = cdiv(s.N, T);
+  if (tm * tn > (1LL << 31) - 1) return false;
+  const int64_t kb = cdiv(s.K, 32);
+  int64_t pk = 1, kper = kb;
+  if (pk_req > 1) {
+    if (kb < 2) return false;
+    kper = cdiv(kb, pk_req);
+    pk = cdiv(kb, kper);
+    if (pk != pk_req || pk > 65535) return false;
+  }
+  const int64_t kb_wave = d.wk == 1 ? kper : cdiv(kper, d.wk);
+  p->family = FAM_DIRECT;
+  p->cfg = cfg;
+  p->tile_m = T;
+  p->tile_n = T;
+  p->tile_k = 32;
+  p->pm = (int)tm;
+  p->pn = (int)tn;
+  p->pk = (int)pk;
+  p->kper = (int)kper;
+  p->grid_x = (int)(tm * tn);
+  p->grid_y = (int)pk;
+  if (pk > 1) {
+    p->n_launch = 2;
+    p->ws_bytes = pk * s.M * ldw8(s.N) * 4;
+  }
+  w->units = tm * tn * pk;
+  w->occ = occupancy(FAM_DIRECT, cfg);
+  w->idx = IDX_DIRECT + cfg;
+  // one iteration = one 32-k block of every wave: 16 B of A and 16 B of B
+  // per lane and k-group, four waves
+  w->L = (double)kb_wave;
+  w->bytes_it = 4.0 * 64 * 32 * 2;
+  w->mfma_it = 2.0 * 16;  // two 32x32x16 MFMAs of 16 cycles on each SIMD
+  w->lds_it = 0;
+  w->out_unit = (double)T * T * (pk == 1 ? c.cbytes : 4);
+  w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
+  if (pk > 1) {
+    w->epi = (double)pk * s.M * s.N * 4;
+    w->epi_out = (double)s.M * s.N * c.cbytes;
+  }
+  w->prefetch = 4;
+  const double rows_read = (double)tn * s.M * s.K * 2, cols_read = (double)tm * s.K * s.N * 2;
+  w->total_read = rows_read + cols_read;
+  w->unaligned = (s.K % 8) != 0;
+  return true;
+}
+
 // K <= 16: rank-K update with FMAs, one pass that writes C once.
 bool build_smallk(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   const SmallKCfg& k = kSmallKCfg[cfg];
@@ -423,23 +482,24 @@ adaptcore_hw_t default_hw() {
   // (squared log error of the model over every measured configuration). The
   // launch cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 2.797e-06;
-  h.hbm_eta = 0.5673;
-  h.l2_bw_cu = 2.636e+10;
+  h.t_mem_latency = 2.423e-06;
+  h.hbm_eta = 0.8356;
+  h.l2_bw_cu = 3.043e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 0.4221;
+  h.l2_hit = 5.516e-33;
   // per configuration (tile 0-7, skinny-M 8-13, skinny-N 14-16, small-K
-  // 17-18, stream-K 19-26; 0 = analytic estimate, no timing data)
+  // 17-18, stream-K 19-26, direct 27-28; 0 = analytic estimate, no timing
+  // data)
   static const double kIter[32] = {
-      2.832e-06, 2.516e-06, 2.304e-06, 1.745e-06, 9.358e-14, 9.358e-14, 1.239e-06, 1.003e-06,
-      9.358e-14, 9.358e-14, 9.358e-14, 2.815e-08, 2.009e-06, 2.275e-06, 5.595e-07, 1.399e-06,
-      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 1.124e-13, 0, 0,
-      9.358e-14, 0, 0, 0, 0, 0, 0, 0};
+      3.018e-06, 2.53e-06, 2.36e-06, 1.74e-06, 1.586e-06, 9.358e-14, 1.284e-06, 9.955e-07,
+      7.938e-07, 2.418e-07, 1.346e-06, 1.499e-06, 1.858e-06, 2.125e-06, 5.096e-07, 1.212e-06,
+      6.151e-07, 1.764e-07, 5.277e-07, 9.358e-14, 9.358e-14, 9.358e-14, 0, 0,
+      9.575e-14, 0, 0, 9.358e-14, 9.358e-14, 0, 0, 0};
   static const double kWg[32] = {
-      1.602e-05, 4.67e-06, 3.346e-06, 2.32e-06, 4.959e-06, 3.442e-06, 4.11e-06, 5.494e-06,
-      3.344e-07, 7.961e-07, 1.991e-06, 3.049e-06, 3.536e-06, 3.595e-06, 9.275e-08, 6.396e-07,
-      1.616e-06, 3.506e-07, 3.529e-07, 1.459e-05, 9.358e-14, 1.951e-06, 0, 0,
-      4.361e-06, 0, 0, 0, 0, 0, 0, 0};
+      8.825e-06, 5.392e-06, 4.229e-06, 2.697e-06, 2.008e-06, 4.76e-06, 4.319e-06, 5.671e-06,
+      1.505e-07, 1.45e-06, 1.269e-06, 2.288e-06, 4.835e-06, 4.909e-06, 9.358e-14, 9.358e-14,
+      5.469e-07, 9.358e-14, 9.358e-14, 3.841e-05, 1.147e-05, 1.167e-05, 0, 0,
+      9.874e-06, 0, 0, 9.358e-14, 3.155e-07, 0, 0, 0};
   for (int i = 0; i < 32; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];
@@ -538,6 +598,21 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
     Work w;
     if (build_smallk(c, cfg, 1, &p, &w)) add(p, w);
   }
+  for (int cfg = 0; cfg < N_DIRECT_CFG; ++cfg) {
+    const int T = direct_tile(kDirectCfg[cfg]);
+    const int64_t tiles = cdiv(s.M, T) * cdiv(s.N, T);
+    {
+      Plan p;
+      Work w;
+      if (build_direct(c, cfg, 1, &p, &w)) add(p, w);
+    }
+    for (int pk : kSplits) {
+      if ((int64_t)pk * tiles > 8LL * c.hw.n_cu * kDirectCfg[cfg].occ) break;
+      Plan p;
+      Work w;
+      if (build_direct(c, cfg, pk, &p, &w)) add(p, w);
+    }
+  }
 }
 
 std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_out) {
@@ -601,6 +676,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
     case FAM_SMALLK:
       ok = sw == 0 && cfg < N_SMALLK_CFG && build_smallk(c, cfg, pk, &p, &w);
       break;
+    case FAM_DIRECT:
+      ok = sw == 0 && cfg < N_DIRECT_CFG && build_direct(c, cfg, pk, &p, &w);
+      break;
   }
   if (!ok || !finish(c, &p, w)) return false;
   if (p.variant_key != key) return false;
@@ -644,6 +722,12 @@ std::string kernel_names(const Plan& p) {
     case FAM_SMALLK:
       std::snprintf(buf, sizeof buf, "k_smallk<%d, %s>", kSmallKCfg[p.cfg].kmax, b);
       return buf;
+    case FAM_DIRECT: {
+      std::snprintf(buf, sizeof buf, "k_direct<%d, %d>", kDirectCfg[p.cfg].wk, p.pk > 1 ? 2 : obf);
+      std::string r(buf);
+      if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
+      return r;
+    }
   }
   return "";
 }
@@ -660,6 +744,8 @@ int config_index(int family, int cfg) {
       return cfg >= 0 && cfg < N_SMALLK_CFG ? IDX_SMALLK + cfg : -1;
     case FAM_STREAMK:
       return cfg >= 0 && cfg < N_TILE_CFG ? IDX_STREAMK + cfg : -1;
+    case FAM_DIRECT:
+      return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
   }
   return -1;
 }

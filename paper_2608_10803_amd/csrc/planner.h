@@ -7,7 +7,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/adaptcore.h"
+#include "adaptcore.h"
 #include "kernel_args.h"
 #include "variants.h"
 

@@ -52,6 +52,15 @@ constexpr SmallKCfg kSmallKCfg[] = {{8, 4}, {16, 2}};
 constexpr int N_SMALLK_CFG = sizeof(kSmallKCfg) / sizeof(kSmallKCfg[0]);
 constexpr int SMALLK_MAX_ROWS = 32;
 
+// Direct configurations: wk = 1: four waves cover 64 x 64 of C, each over
+// all of K; wk = 4: four waves split the K range of one 32 x 32 block.
+struct DirectCfg {
+  int wk, occ;
+};
+constexpr DirectCfg kDirectCfg[] = {{1, 4}, {4, 4}};
+constexpr int N_DIRECT_CFG = sizeof(kDirectCfg) / sizeof(kDirectCfg[0]);
+inline int direct_tile(const DirectCfg& c) { return c.wk == 1 ? 64 : 32; }
+
 // 64-bit key of a configuration:
 //   bits  0- 3 family, 4-11 config index, 12 swizzle, 16-35 P_k (or the
 //   stream-K grid), 36-47 reserved, 48-51 dtype, 52-53 layouts.

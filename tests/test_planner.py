@@ -148,6 +148,11 @@ def test_argument_validation():
         with pytest.raises(ac.AdaptCoreError) as e:
             ac.adaptcore_matmul(h, *args)
         assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    # leading dimensions at or past 2^23 are unsupported (32-bit tile offsets)
+    for args in [(0x1000, 1 << 23, 0x2000, 32, 0x3000, 32), (0x1000, 16, 0x2000, 1 << 23, 0x3000, 32)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_matmul(h, *args)
+        assert e.value.status == ac.AC_ERR_UNSUPPORTED
     # an empty output launches nothing and succeeds anywhere
     ac.adaptcore_matmul(ac.adaptcore_plan(0, 5, 7), 0, 7, 0x2000, 5, 0x3000, 5)
     with pytest.raises(ac.AdaptCoreError):
