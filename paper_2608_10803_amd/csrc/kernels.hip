@@ -352,11 +352,13 @@ struct Stage {
   }
 };
 
-// k-blocks of global loads in flight: the wide tiles hold one stage in
-// registers (their accumulators use the register file), the narrower tiles two.
+// k-blocks of global loads in flight (one or two stages held in registers).
 template <int BM, int BN>
 struct TileDepth {
-  static constexpr int value = (BM * BN > 64 * 64) ? 1 : 2;
+  // two stages where the registers allow it and it pays: the small tiles and
+  // the 128 x 256 / 256 x 128 tiles (measured); 128 x 128 and the 64-wide
+  // tiles keep one stage and two to three workgroups per CU instead
+  static constexpr int value = (BM * BN <= 64 * 64 || BM * BN == 128 * 256) ? 2 : 1;
 };
 
 // Accumulates the tile over k-blocks [kt0, kt1). With two stages in flight,

@@ -482,24 +482,24 @@ adaptcore_hw_t default_hw() {
   // (squared log error of the model over every measured configuration). The
   // launch cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 2.423e-06;
-  h.hbm_eta = 0.8356;
-  h.l2_bw_cu = 3.043e+10;
+  h.t_mem_latency = 2.171e-06;
+  h.hbm_eta = 0.906;
+  h.l2_bw_cu = 3.397e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 5.516e-33;
+  h.l2_hit = 5.458e-33;
   // per configuration (tile 0-7, skinny-M 8-13, skinny-N 14-16, small-K
   // 17-18, stream-K 19-26, direct 27-28; 0 = analytic estimate, no timing
   // data)
   static const double kIter[32] = {
-      3.018e-06, 2.53e-06, 2.36e-06, 1.74e-06, 1.586e-06, 9.358e-14, 1.284e-06, 9.955e-07,
-      7.938e-07, 2.418e-07, 1.346e-06, 1.499e-06, 1.858e-06, 2.125e-06, 5.096e-07, 1.212e-06,
-      6.151e-07, 1.764e-07, 5.277e-07, 9.358e-14, 9.358e-14, 9.358e-14, 0, 0,
-      9.575e-14, 0, 0, 9.358e-14, 9.358e-14, 0, 0, 0};
+      3.085e-06, 2.166e-06, 1.814e-06, 1.798e-06, 1.6e-06, 9.358e-14, 1.23e-06, 9.727e-07,
+      1.085e-06, 3.382e-07, 1.222e-06, 1.586e-06, 1.958e-06, 2.197e-06, 5.326e-07, 1.086e-06,
+      6.284e-07, 4.374e-07, 9.337e-07, 1.407e-13, 9.358e-14, 1.22e-13, 0, 0,
+      9.358e-14, 0, 0, 9.358e-14, 9.358e-14, 0, 0, 0};
   static const double kWg[32] = {
-      8.825e-06, 5.392e-06, 4.229e-06, 2.697e-06, 2.008e-06, 4.76e-06, 4.319e-06, 5.671e-06,
-      1.505e-07, 1.45e-06, 1.269e-06, 2.288e-06, 4.835e-06, 4.909e-06, 9.358e-14, 9.358e-14,
-      5.469e-07, 9.358e-14, 9.358e-14, 3.841e-05, 1.147e-05, 1.167e-05, 0, 0,
-      9.874e-06, 0, 0, 9.358e-14, 3.155e-07, 0, 0, 0};
+      7.734e-06, 4.188e-06, 3.544e-06, 1.115e-06, 2.633e-07, 3.558e-06, 6.296e-07, 1.331e-06,
+      5.786e-07, 2.056e-06, 2.138e-06, 2.454e-06, 4.658e-06, 4.422e-06, 9.358e-14, 2.623e-07,
+      9.173e-07, 9.358e-14, 9.358e-14, 2.485e-05, 3.014e-05, 1.561e-05, 0, 0,
+      9.414e-06, 0, 0, 9.358e-14, 3.179e-07, 0, 0, 0};
   for (int i = 0; i < 32; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];
