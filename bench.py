@@ -30,6 +30,7 @@ plan-miss and cached-lookup costs, the roofline of the dominant kernel, and
 the oracle timed on the host cores (cpu_baseline).
 """
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -75,6 +76,32 @@ def workload_shapes(name):
     raise SystemExit("unknown workload %s" % name)
 
 
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "sweep_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_10803_amd", "csrc", "kernels.hip")
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the counters read
+    for a 1 GiB copy), or None if the kernel is not in it or the kernel
+    source has changed since the counters were taken."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    kv = dict(l.split(":", 1) for l in text.splitlines() if l.startswith("- ") and ":" in l)
+    kv = {k[2:].strip(): v.strip().strip("`") for k, v in kv.items()}
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    if kv.get("kernels.hip sha256") != src:
+        return None
+    ff, fw = float(kv["fetch factor"]), float(kv["write factor"])
+    for l in text.splitlines():
+        cells = [c.strip().strip("`") for c in l.strip().strip("|").split("|")]
+        if len(cells) >= 4 and cells[0] == kernel:
+            return (float(cells[2]) * ff + float(cells[3]) * fw) * 1024.0
+    return None
+
+
 def cpu_baseline(shapes, cbytes, budget_s=15.0, seed=7, max_shapes=200):
     """The oracle on the host cores, on a bounded sample of the workload:
     a seeded sample of shapes, each computed in full when small and on a
@@ -117,6 +144,15 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true")
     ap.add_argument("--per-shape", default=None, help="write per-shape results to this JSON file")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch the batches directly instead of replaying HIP graphs (for counter "
+                         "collection, which does not follow graph launches; timings then include the "
+                         "host launch cost)")
+    ap.add_argument("--only-kernel", default=None,
+                    help="run only the shapes whose plan launches exactly this kernel (counter collection "
+                         "of one kernel; the metric then covers those shapes only)")
+    ap.add_argument("--copy-ref", action="store_true",
+                    help="first copy 1 GiB device to device (the reference kernel of the traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
@@ -129,6 +165,12 @@ def main():
         raise SystemExit("no GPU")
     ac.adaptcore_init()
     dev = torch.device("cuda")
+    if args.copy_ref:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     shapes, dtype = workload_shapes(args.workload)
     cbytes = 4 if dtype == ac.AC_BF16_F32OUT else 2
     out_t = torch.float32 if cbytes == 4 else torch.bfloat16
@@ -140,6 +182,14 @@ def main():
     lookup_ns = ac.adaptcore_bench_lookup(len(shapes), 1000000)
     infos = [ac.adaptcore_plan_info(p) for p in plans]
     kernels = [ac.adaptcore_plan_kernels(p) for p in plans]
+    if args.only_kernel:
+        keep = [i for i in range(len(shapes)) if kernels[i] == [args.only_kernel]]
+        if not keep:
+            raise SystemExit("no shape of the workload is planned with %s" % args.only_kernel)
+        shapes = [shapes[i] for i in keep]
+        plans = [plans[i] for i in keep]
+        infos = [infos[i] for i in keep]
+        kernels = [kernels[i] for i in keep]
 
     # --- device operands: one arena per operand, filled once (seeded uniform[-1, 1])
     g = torch.Generator(device=dev)
@@ -188,7 +238,7 @@ def main():
 
     # per-shape graphs of R calls over rotating operand copies
     ROT = 512 << 20
-    graphs, reps = [], []
+    graphs, reps, graph_objs = [], [], []
     for i, (M, N, K) in enumerate(shapes):
         fa, fb, fc = 2 * M * K, 2 * K * N, cbytes * M * N
         # enough calls per graph (>= ~250 us of work) that the graph launch
@@ -200,12 +250,19 @@ def main():
         ca, cb_, cc = span(fa, A.numel() * 2), span(fb, B.numel() * 2), span(fc, C.numel() * cbytes)
         sa, sb, sc = (max((fa + 255) // 256 * 256, 256), max((fb + 255) // 256 * 256, 256),
                       max((fc + 255) // 256 * 256, 256))
-        gr = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(gr, stream=cs):
+        def batch(i=i, R=R, ca=ca, cb_=cb_, cc=cc, sa=sa, sb=sb, sc=sc, K=K, N=N, stream=None):
+            st = stream if stream is not None else cs.cuda_stream
             for r in range(R):
                 ac.adaptcore_matmul(plans[i], pa + (r % ca) * sa, max(K, 1), pb + (r % cb_) * sb, max(N, 1),
-                                    pc + (r % cc) * sc, max(N, 1), cs.cuda_stream)
-        graphs.append(gr)
+                                    pc + (r % cc) * sc, max(N, 1), st)
+        if args.eager:
+            graphs.append(lambda b=batch: b(stream=torch.cuda.current_stream().cuda_stream))
+        else:
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=cs):
+                batch()
+            graphs.append(gr.replay)
+            graph_objs.append(gr)
         reps.append(R)
     # bring the clocks up before the warmup passes (a torch elementwise
     # kernel, so that the profile of this library's kernels is not mixed)
@@ -216,7 +273,7 @@ def main():
         torch.cuda.synchronize()
     for _ in range(args.warmup):
         for i in range(n):
-            graphs[i].replay()
+            graphs[i]()
     torch.cuda.synchronize()
 
     K_steps = args.steps
@@ -227,13 +284,13 @@ def main():
         row = evs[k]
         for i in range(n):
             row[i][0].record()
-            graphs[i].replay()
+            graphs[i]()
             row[i][1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     t_call = [statistics.median(evs[k][i][0].elapsed_time(evs[k][i][1]) * 1e-3 for k in range(K_steps)) / reps[i]
               for i in range(n)]
-    del graphs
+    del graphs, graph_objs
 
     # isolated calls: cold caches, one call between its own events
     iso = None
@@ -298,7 +355,10 @@ def main():
     else:
         roofline = {"bound": "hbm", "achieved": round(dom["B"] / dom["t"] / 1e9, 1), "peak": 8000.0, "unit": "GB/s"}
         roofline["frac"] = round(roofline["achieved"] / 8000.0, 4)
-    roofline.update({"traffic": None, "kernel": dom_name, "shapes": dom["shapes"],
+    traffic = measured_traffic(dom_name)
+    roofline.update({"traffic": round(traffic) if traffic else None,
+                     "traffic_vs_algorithmic": round(traffic / (dom["B"] / dom["n"]), 3) if traffic else None,
+                     "kernel": dom_name, "shapes": dom["shapes"],
                      "launches_per_step": dom["n"], "avg_launch_us": round(dom["t"] / dom["n"] * 1e6, 2),
                      "share_of_pass": round(dom["pass"] / sum(r["t"] for r in rows), 3)})
 
