@@ -189,16 +189,28 @@ struct AccOf<16> {
   static constexpr int n = 4;
 };
 
+// Waves of a tile workgroup: 4 in a 2 x 2 grid, or 8 in a 2 x 4 grid for the
+// 256-row tiles (two waves per SIMD hide each other's waits; measured faster
+// than 4 waves for 256 x 256 and 256 x 128, slower for 128 x 256).
+constexpr int tile_waves(int bm, int bn) { return bm == 256 ? 8 : 4; }
+
 template <int BM, int BN, int MS>
 struct TileShape {
-  static constexpr int NT = 256, BK = 64, CH = 8;
-  static constexpr int WTM = BM / 2, WTN = BN / 2;
+  static constexpr int NW = tile_waves(BM, BN), WC = NW / 2;
+  static constexpr int NT = 64 * NW, BK = 64, CH = 8;
+  static constexpr int WTM = BM / 2, WTN = BN / WC;
   static constexpr int TM = WTM / MS, TN = WTN / MS;
   static constexpr int KS = MS == 32 ? 16 : 32;
   static constexpr int NA = AccOf<MS>::n;
   static constexpr int AV = BM * CH;  // 16-byte vectors of an A stage
   static constexpr int IA = (AV + NT - 1) / NT;
-  static constexpr int IB = (BN + NT - 1) / NT;  // 8x8 blocks of a B stage (BK/8 * BN/8 = BN)
+  // B stage: BK/8 * BN/8 = BN blocks of 8 k-rows x 8 columns; each block is
+  // shared by BP threads, each taking BR = 8 / BP consecutive k-rows, so that
+  // (where possible) every thread of the workgroup has one unit of B work.
+  static constexpr int BP = (NT / BN >= 4) ? 4 : (NT / BN >= 2 ? 2 : 1);
+  static constexpr int BR = 8 / BP;
+  static constexpr int BU = BN * BP;                // B units of a stage
+  static constexpr int IB = (BU + NT - 1) / NT;     // B units per thread
   static constexpr int AB_BYTES = 2 * (BM + BN) * CH * 16;  // double-buffered A and B stages
   static constexpr int CT_LD = BN + 4;                        // padded LDS row of the output tile
   static constexpr int CT_BYTES = BM * CT_LD * 2;             // bf16 output tile
@@ -228,7 +240,7 @@ struct StageGeom {
     }
 #pragma unroll
     for (int bb = 0; bb < S::IB; ++bb) {
-      const int grp = min(tid + bb * S::NT, BN - 1) >> 3;
+      const int grp = (min(tid + bb * S::NT, S::BU - 1) / S::BP) >> 3;
       const int64_t gn = n0 + grp * 8;
       const int64_t st = min(gn, g.N - 8);
       b_col[bb] = (uint32_t)((st - n0) * 2 + 16);
@@ -253,7 +265,7 @@ template <int BM, int BN, int MS>
 struct Stage {
   typedef TileShape<BM, BN, MS> S;
   u32x4 ra[S::IA];
-  u32x4 rb[S::IB][8];
+  u32x4 rb[S::IB][S::BR];
   uint32_t code;  // bits 0-3: A elements to drop; bits 4-11: B rows past K
 
   // Requires K >= 8 and N >= 8 (the small-row mode covers the rest). A
@@ -274,12 +286,18 @@ struct Stage {
 #pragma unroll
     for (int i = 0; i < S::IA; ++i)
       if (S::AV % S::NT == 0 || tid + i * S::NT < S::AV) ra[i] = load16(at(Ab, o.a_row[i] + (uint32_t)(st * 2)));
+    // B: this thread's rows of its block(s): k-rows (blk % 8) * 8 + part * BR
+    // + i, where unit u = tid + b * NT = blk * BP + part; all units of a
+    // thread share blk % 8 and part (NT is a multiple of 8 * BP)
+    const int bk0 = ((tid / S::BP) & 7) * 8 + (tid % S::BP) * S::BR;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int kr = min(c8 + i, rem - 1);
-      cd |= (uint32_t)(c8 + i >= rem) << (4 + i);
+    for (int i = 0; i < S::BR; ++i) {
+      const int kr = min(bk0 + i, rem - 1);
+      cd |= (uint32_t)(bk0 + i >= rem) << (4 + i);
 #pragma unroll
-      for (int b = 0; b < S::IB; ++b) rb[b][i] = load16(at(Bb, (uint32_t)kr * o.ldb2 + o.b_col[b]));
+      for (int b = 0; b < S::IB; ++b)
+        if (S::BU % S::NT == 0 || tid + b * S::NT < S::BU)  // uniform over a wave
+          rb[b][i] = load16(at(Bb, (uint32_t)kr * o.ldb2 + o.b_col[b]));
     }
     code = cd;
   }
@@ -300,12 +318,13 @@ struct Stage {
     }
 #pragma unroll
     for (int b = 0; b < S::IB; ++b) {
-      const int blk = tid + b * S::NT;
-      if (BN % S::NT == 0 || blk < BN) {
+      const int u = tid + b * S::NT;
+      if (S::BU % S::NT == 0 || u < S::BU) {
+        const int blk = u / S::BP, part = u % S::BP;
         const int64_t gn = n0 + (blk >> 3) * 8;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int64_t gk = kbase + (blk & 7) * 8 + i;
+        for (int i = 0; i < S::BR; ++i) {
+          const int64_t gk = kbase + (blk & 7) * 8 + part * S::BR + i;
           const u32x4 v = load_row8_small(g.B + min(gk, g.K - 1) * g.ldb, gn, g.N);
           rb[b][i] = gk < g.K ? v : u32x4{0u, 0u, 0u, 0u};
           __builtin_amdgcn_sched_barrier(0);
@@ -325,7 +344,7 @@ struct Stage {
 #pragma unroll
       for (int b = 0; b < S::IB; ++b)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) rb[b][i] = shift_down(rb[b][i], ((code >> (4 + i)) & 1) ? 8 : cs[b]);
+        for (int i = 0; i < S::BR; ++i) rb[b][i] = shift_down(rb[b][i], ((code >> (4 + i)) & 1) ? 8 : cs[b]);
     }
 #pragma unroll
     for (int i = 0; i < S::IA; ++i) {
@@ -337,15 +356,35 @@ struct Stage {
     }
 #pragma unroll
     for (int b = 0; b < S::IB; ++b) {
-      const int blk = tid + b * S::NT;
-      if (BN % S::NT == 0 || blk < BN) {
+      const int u = tid + b * S::NT;
+      if (S::BU % S::NT == 0 || u < S::BU) {
+        const int blk = u / S::BP, part = u % S::BP;
         const int c = blk & 7, grp = blk >> 3;
-        u32x4 col[8];
-        transpose8x8(rb[b], col);
+        if constexpr (S::BR == 8) {
+          u32x4 col[8];
+          transpose8x8(rb[b], col);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int n = grp * 8 + j;
-          sB[n * 8 + swz(n, c)] = col[j];
+          for (int j = 0; j < 8; ++j) {
+            const int n = grp * 8 + j;
+            sB[n * 8 + swz(n, c)] = col[j];
+          }
+        } else {
+          // column j of this thread's BR rows: BR / 2 dwords, written into
+          // part `part` of the column's 16-byte k-chunk
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int n = grp * 8 + j, d = j >> 1;
+            const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+            uint32_t* dst = reinterpret_cast<uint32_t*>(&sB[n * 8 + swz(n, c)]) + part * (S::BR / 2);
+            if constexpr (S::BR == 4) {
+              const uint32_t w0 = __builtin_amdgcn_perm(rb[b][1][d], rb[b][0][d], sel);
+              const uint32_t w1 = __builtin_amdgcn_perm(rb[b][3][d], rb[b][2][d], sel);
+              const uint64_t w = (uint64_t)w0 | ((uint64_t)w1 << 32);
+              *reinterpret_cast<uint64_t*>(dst) = w;
+            } else {
+              *dst = __builtin_amdgcn_perm(rb[b][1][d], rb[b][0][d], sel);
+            }
+          }
         }
       }
     }
@@ -355,10 +394,10 @@ struct Stage {
 // k-blocks of global loads in flight (one or two stages held in registers).
 template <int BM, int BN>
 struct TileDepth {
-  // two stages where the registers allow it and it pays: the small tiles and
-  // the 128 x 256 / 256 x 128 tiles (measured); 128 x 128 and the 64-wide
-  // tiles keep one stage and two to three workgroups per CU instead
-  static constexpr int value = (BM * BN <= 64 * 64 || BM * BN == 128 * 256) ? 2 : 1;
+  // two stages where the registers allow it and it pays (measured): the
+  // small tiles and 128 x 256; the others keep one stage and rely on more
+  // waves or workgroups per CU
+  static constexpr int value = (BM * BN <= 64 * 64 || (BM == 128 && BN == 256)) ? 2 : 1;
 };
 
 // Accumulates the tile over k-blocks [kt0, kt1). With two stages in flight,
@@ -372,7 +411,7 @@ __device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0
                                                    char* smem) {
   typedef TileShape<BM, BN, MS> S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / S::WC, wc = wave % S::WC;
   u32x4* sA0 = reinterpret_cast<u32x4*>(smem);
   u32x4* sA1 = sA0 + BM * 8;
   u32x4* sB0 = sA1 + BM * 8;
@@ -513,7 +552,7 @@ __device__ __forceinline__ void store_acc_f32(const typename AccOf<MS>::T (&acc)
                                               int64_t cmax) {
   typedef TileShape<BM, BN, MS> S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / S::WC, wc = wave % S::WC;
 #pragma unroll
   for (int i = 0; i < S::TM; ++i) {
     const int64_t row = m0 + wr * S::WTM + i * MS + (lane % MS);
@@ -545,7 +584,7 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
                                                const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
   typedef TileShape<BM, BN, MS> S;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / S::WC, wc = wave % S::WC;
   uint16_t* ct = reinterpret_cast<uint16_t*>(smem);
   __syncthreads();  // the main loop's last reads of the LDS stages are done
   // the lane's row of each MFMA tile, written 4 columns (8 bytes) at a time
@@ -586,6 +625,40 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
   }
 }
 
+// bf16 output straight from the accumulators: each lane writes its row's
+// runs of 4 columns as 8-byte stores (no LDS round trip, no barrier).
+template <int BM, int BN, int MS>
+__device__ __forceinline__ void store_acc_bf16_direct(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                                    [TileShape<BM, BN, MS>::TN],
+                                                      const GemmArgs& g, int64_t m0, int64_t n0) {
+  typedef TileShape<BM, BN, MS> S;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wr = wave / S::WC, wc = wave % S::WC;
+  uint16_t* C = static_cast<uint16_t*>(g.C);
+#pragma unroll
+  for (int i = 0; i < S::TM; ++i) {
+    const int64_t row = m0 + wr * S::WTM + i * MS + (lane % MS);
+    if (row >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < S::TN; ++j)
+#pragma unroll
+      for (int q = 0; q < S::NA / 4; ++q) {
+        const int64_t col = n0 + wc * S::WTN + j * MS + acc_col<MS>(4 * q, lane);
+        uint16_t* d = C + row * g.ldc + col;
+        if (col + 4 <= g.N) {
+          const uint32_t lo = (uint32_t)to_bf16(acc[i][j][4 * q]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 1]) << 16);
+          const uint32_t hi = (uint32_t)to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 3]) << 16);
+          const uint64_t v = (uint64_t)lo | ((uint64_t)hi << 32);
+          __builtin_memcpy(d, &v, 8);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < g.N) d[e] = to_bf16(acc[i][j][4 * q + e]);
+        }
+      }
+  }
+}
+
 template <int BM, int BN, int MS, bool OBF>
 __device__ __forceinline__ void store_tile_c(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                            [TileShape<BM, BN, MS>::TN],
@@ -601,7 +674,7 @@ __device__ __forceinline__ void store_tile_c(const typename AccOf<MS>::T (&acc)[
 enum TileOut : int { OUT_F32 = 0, OUT_BF16 = 1, OUT_PARTIAL = 2 };
 
 template <int BM, int BN, int MS, int OUT>
-__global__ __launch_bounds__(256) void k_tile(GemmArgs g) {
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
@@ -640,7 +713,7 @@ __global__ __launch_bounds__(256) void k_tile(GemmArgs g) {
 // tile, summed later by k_sk_fixup. The remaining tiles are processed whole,
 // data-parallel, by the grid.
 template <int BM, int BN, int MS, bool OBF>
-__global__ __launch_bounds__(256) void k_streamk(GemmArgs g) {
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
@@ -1274,7 +1347,7 @@ hipError_t launch_reduce(const GemmArgs& g, hipStream_t st, bool obf) {
 
 template <int BM, int BN, int MS>
 hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
-  const dim3 grid(p.grid_x, p.grid_y), block(256);
+  const dim3 grid(p.grid_x, p.grid_y), block(TileShape<BM, BN, MS>::NT);
   if (p.pk > 1)
     hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_PARTIAL>), grid, block, 0, st, g);
   else if (obf)
@@ -1287,7 +1360,7 @@ hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool ob
 }
 template <int BM, int BN, int MS>
 hipError_t launch_streamk(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
-  const dim3 grid(p.grid_x, 1), block(256);
+  const dim3 grid(p.grid_x, 1), block(TileShape<BM, BN, MS>::NT), fblock(256);
   if (obf)
     hipLaunchKernelGGL((k_streamk<BM, BN, MS, true>), grid, block, 0, st, g);
   else
@@ -1297,9 +1370,9 @@ hipError_t launch_streamk(const Plan& p, const GemmArgs& g, hipStream_t st, bool
   const int chunks = (BM * (BN / 8) + 255) / 256;
   const dim3 fgrid(g.sk_tiles, chunks);
   if (obf)
-    hipLaunchKernelGGL((k_sk_fixup<true>), fgrid, block, 0, st, g, BM, BN);
+    hipLaunchKernelGGL((k_sk_fixup<true>), fgrid, fblock, 0, st, g, BM, BN);
   else
-    hipLaunchKernelGGL((k_sk_fixup<false>), fgrid, block, 0, st, g, BM, BN);
+    hipLaunchKernelGGL((k_sk_fixup<false>), fgrid, fblock, 0, st, g, BM, BN);
   return hipGetLastError();
 }
 template <int MT, int WKW>
@@ -1350,23 +1423,26 @@ hipError_t launch_direct(const Plan& p, const GemmArgs& g, hipStream_t st, bool 
 }
 
 template <typename F>
-int occ_of(F kernel_f32, F kernel_bf16) {
+int occ_of(F kernel_f32, F kernel_bf16, int threads = 256) {
   int a = 0, b = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, reinterpret_cast<const void*>(kernel_f32), 256, 0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, reinterpret_cast<const void*>(kernel_f32), threads, 0) !=
+      hipSuccess)
     a = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, reinterpret_cast<const void*>(kernel_bf16), 256, 0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, reinterpret_cast<const void*>(kernel_bf16), threads, 0) !=
+      hipSuccess)
     b = 0;
   return a < b ? a : b;
 }
 template <int BM, int BN, int MS>
 int occ_tile() {
-  const int a = occ_of(k_tile<BM, BN, MS, OUT_F32>, k_tile<BM, BN, MS, OUT_BF16>);
-  const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL>, k_tile<BM, BN, MS, OUT_PARTIAL>);
+  constexpr int nt = TileShape<BM, BN, MS>::NT;
+  const int a = occ_of(k_tile<BM, BN, MS, OUT_F32>, k_tile<BM, BN, MS, OUT_BF16>, nt);
+  const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL>, k_tile<BM, BN, MS, OUT_PARTIAL>, nt);
   return a < b ? a : b;
 }
 template <int BM, int BN, int MS>
 int occ_streamk() {
-  return occ_of(k_streamk<BM, BN, MS, false>, k_streamk<BM, BN, MS, true>);
+  return occ_of(k_streamk<BM, BN, MS, false>, k_streamk<BM, BN, MS, true>, TileShape<BM, BN, MS>::NT);
 }
 template <int MT, int WKW>
 int occ_skinny_m() {
