@@ -482,24 +482,24 @@ adaptcore_hw_t default_hw() {
   // (squared log error of the model over every measured configuration). The
   // launch cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 2.171e-06;
-  h.hbm_eta = 0.906;
-  h.l2_bw_cu = 3.397e+10;
+  h.t_mem_latency = 1.416e-06;
+  h.hbm_eta = 1;
+  h.l2_bw_cu = 3.038e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 5.458e-33;
+  h.l2_hit = 5.731e-33;
   // per configuration (tile 0-7, skinny-M 8-13, skinny-N 14-16, small-K
   // 17-18, stream-K 19-26, direct 27-28; 0 = analytic estimate, no timing
   // data)
   static const double kIter[32] = {
-      3.085e-06, 2.166e-06, 1.814e-06, 1.798e-06, 1.6e-06, 9.358e-14, 1.23e-06, 9.727e-07,
-      1.085e-06, 3.382e-07, 1.222e-06, 1.586e-06, 1.958e-06, 2.197e-06, 5.326e-07, 1.086e-06,
-      6.284e-07, 4.374e-07, 9.337e-07, 1.407e-13, 9.358e-14, 1.22e-13, 0, 0,
+      2.819e-06, 2.023e-06, 1.804e-06, 1.347e-06, 9.407e-07, 9.358e-14, 5.394e-07, 3.621e-07,
+      1.201e-06, 8.341e-10, 1.348e-06, 1.601e-06, 1.877e-06, 2.15e-06, 5.5e-07, 7.079e-07,
+      7.624e-07, 5.394e-07, 2.959e-07, 1.052e-13, 1.116e-13, 1.286e-13, 1.324e-06, 8.09e-07,
       9.358e-14, 0, 0, 9.358e-14, 9.358e-14, 0, 0, 0};
   static const double kWg[32] = {
-      7.734e-06, 4.188e-06, 3.544e-06, 1.115e-06, 2.633e-07, 3.558e-06, 6.296e-07, 1.331e-06,
-      5.786e-07, 2.056e-06, 2.138e-06, 2.454e-06, 4.658e-06, 4.422e-06, 9.358e-14, 2.623e-07,
-      9.173e-07, 9.358e-14, 9.358e-14, 2.485e-05, 3.014e-05, 1.561e-05, 0, 0,
-      9.414e-06, 0, 0, 9.358e-14, 3.179e-07, 0, 0, 0};
+      2.92e-06, 1.345e-06, 3.678e-06, 1.517e-06, 2.678e-07, 2.58e-06, 4.234e-07, 3.439e-07,
+      5.461e-07, 3.735e-06, 2.377e-06, 2.876e-06, 4.669e-06, 4.995e-06, 6.572e-07, 1.424e-06,
+      1.739e-06, 4.114e-07, 1.126e-06, 2.344e-05, 4.891e-06, 1.97e-05, 6.434e-06, 9.839e-06,
+      1.067e-05, 0, 0, 9.358e-14, 6.55e-07, 0, 0, 0};
   for (int i = 0; i < 32; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];
