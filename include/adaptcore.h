@@ -115,6 +115,9 @@ typedef struct {
  * (256 CUs, 160 KiB LDS per CU); adaptcore_init() replaces the CU count with
  * the device's. The latency constants are the model's lambda / eta / BW of
  * Eq. 8, calibrated on the device. */
+/* Number of kernel configurations with calibrated costs (table size). */
+#define AC_N_CFG 64
+
 typedef struct {
   int32_t n_cu;          /* N_core: compute units */
   int32_t lds_bytes;     /* LDS per CU */
@@ -140,8 +143,8 @@ typedef struct {
    * latency and epilogue together). 0 = use the analytic estimate: MFMA issue
    * and LDS traffic for the iteration, t_wg plus t_mem_latency per dependent
    * load phase for the fixed cost. Each value must lie in [0, 1) seconds. */
-  double cfg_iter[32];
-  double cfg_wg[32];
+  double cfg_iter[AC_N_CFG];
+  double cfg_wg[AC_N_CFG];
 } adaptcore_hw_t;
 
 /* Index of a kernel configuration in adaptcore_hw_t::cfg_iter / cfg_wg, or -1. */

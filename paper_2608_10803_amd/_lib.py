@@ -12,6 +12,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libadaptcore.so")
 
+AC_N_CFG = 64  # calibrated cost table size (include/adaptcore.h)
 AC_OK = 0
 AC_ERR_INVALID_VALUE = -1
 AC_ERR_UNSUPPORTED = -2
@@ -78,7 +79,7 @@ class Hw(ctypes.Structure):
                 ("t_mem_latency", ctypes.c_double), ("t_wg", ctypes.c_double), ("mfma_eta", ctypes.c_double),
                 ("lds_bw_cu", ctypes.c_double), ("unaligned_eta", ctypes.c_double), ("l2_hit", ctypes.c_double),
                 ("search_open", ctypes.c_int32), ("enable_streamk", ctypes.c_int32),
-                ("cfg_iter", ctypes.c_double * 32), ("cfg_wg", ctypes.c_double * 32)]
+                ("cfg_iter", ctypes.c_double * AC_N_CFG), ("cfg_wg", ctypes.c_double * AC_N_CFG)]
 
     def as_dict(self):
         d = {}

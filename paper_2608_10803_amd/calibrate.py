@@ -35,7 +35,7 @@ from . import _lib as ac
 # back-to-back launches, and the fixed part of each configuration is in cfg_wg.
 FIT_FIELDS = ["t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit"]
 BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.99)}
-N_CFG = 32
+N_CFG = ac.AC_N_CFG
 
 
 def sample_shapes(n_sweep=120, seed=11):
@@ -265,8 +265,8 @@ def emit_cpp(profile):
              "  h.unaligned_eta = %.4g;" % p["unaligned_eta"], "  h.l2_hit = %.4g;" % p["l2_hit"]]
     it = ", ".join("%.4g" % v for v in p["cfg_iter"])
     wg = ", ".join("%.4g" % v for v in p["cfg_wg"])
-    lines.append("  static const double kIter[32] = {%s};" % it)
-    lines.append("  static const double kWg[32] = {%s};" % wg)
+    lines.append("  static const double kIter[AC_N_CFG] = {%s};" % it)
+    lines.append("  static const double kWg[AC_N_CFG] = {%s};" % wg)
     return "\n".join(lines)
 
 

@@ -427,7 +427,7 @@ adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw) {
       !(hw->unaligned_eta > 0) || hw->l2_hit < 0 || hw->l2_hit > 1 || hw->t_launch < 0 || hw->t_mem_latency < 0 ||
       hw->t_wg < 0)
     return fail(AC_ERR_INVALID_VALUE, "profile field out of range");
-  for (int i = 0; i < 32; ++i)
+  for (int i = 0; i < AC_N_CFG; ++i)
     if (!(hw->cfg_iter[i] >= 0 && hw->cfg_iter[i] < 1) || !(hw->cfg_wg[i] >= 0 && hw->cfg_wg[i] < 1))
       return fail(AC_ERR_INVALID_VALUE, "calibrated configuration cost out of range");
   adaptcore_cache_clear();

@@ -391,20 +391,15 @@ struct Stage {
   }
 };
 
-// k-blocks of global loads in flight (one or two stages held in registers).
-template <int BM, int BN>
-struct TileDepth {
-  // two stages where the registers allow it and it pays (measured): the
-  // small tiles and 128 x 256; the others keep one stage and rely on more
-  // waves or workgroups per CU
-  static constexpr int value = (BM * BN <= 64 * 64 || (BM == 128 && BN == 256)) ? 2 : 1;
-};
+// k-blocks of global loads in flight of the stream-K kernel (the tile kernel
+// takes it from its configuration): two where the registers allow it.
+constexpr int streamk_depth(int bm, int bn) { return (bm * bn <= 64 * 64 || (bm == 128 && bn == 256)) ? 2 : 1; }
 
 // Accumulates the tile over k-blocks [kt0, kt1). With two stages in flight,
 // block kt is multiplied out of LDS while block kt+1 waits in registers and
 // block kt+2 is fetched. SMALL selects the element-load mode for K < 8 or
 // N < 8 (decided once per kernel, so the loop body has no per-block branches).
-template <int BM, int BN, int MS, bool SMALL>
+template <int BM, int BN, int MS, int DEPTH, bool SMALL>
 __device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0, int64_t n0, int kt0, int kt1,
                                                    typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                               [TileShape<BM, BN, MS>::TN],
@@ -463,7 +458,7 @@ __device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0
   // The loop bodies are straight-line (no per-lane branch, so no conservative
   // wait at a branch join splits the pipeline) and every load they issue is
   // of a block that is used: the last blocks are peeled off the loops.
-  if constexpr (TileDepth<BM, BN>::value == 1) {
+  if constexpr (DEPTH == 1) {
     Stage<BM, BN, MS> st;
     load(st, kt0);
     st.store(sA0, sB0, edge(kt0), o.b_cs);
@@ -520,16 +515,16 @@ __device__ __forceinline__ void tile_mainloop_impl(const GemmArgs& g, int64_t m0
   }
 }
 
-template <int BM, int BN, int MS>
+template <int BM, int BN, int MS, int DEPTH>
 __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int64_t m0, int64_t n0, int kt0, int kt1,
                                               typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                          [TileShape<BM, BN, MS>::TN],
                                               char* smem) {
   if (kt0 >= kt1) return;
   if (g.K < 8 || g.N < 8)
-    tile_mainloop_impl<BM, BN, MS, true>(g, m0, n0, kt0, kt1, acc, smem);
+    tile_mainloop_impl<BM, BN, MS, DEPTH, true>(g, m0, n0, kt0, kt1, acc, smem);
   else
-    tile_mainloop_impl<BM, BN, MS, false>(g, m0, n0, kt0, kt1, acc, smem);
+    tile_mainloop_impl<BM, BN, MS, DEPTH, false>(g, m0, n0, kt0, kt1, acc, smem);
 }
 
 // Column (within the MFMA block) of accumulator element r of this lane; the
@@ -673,7 +668,7 @@ __device__ __forceinline__ void store_tile_c(const typename AccOf<MS>::T (&acc)[
 // partial of the workgroup's K partition.
 enum TileOut : int { OUT_F32 = 0, OUT_BF16 = 1, OUT_PARTIAL = 2 };
 
-template <int BM, int BN, int MS, int OUT>
+template <int BM, int BN, int MS, int OUT, int DEPTH>
 __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
@@ -696,7 +691,7 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
 
-  tile_mainloop<BM, BN, MS>(g, m0, n0, kt0, kt1, acc, smem);
+  tile_mainloop<BM, BN, MS, DEPTH>(g, m0, n0, kt0, kt1, acc, smem);
 
   if constexpr (OUT == OUT_PARTIAL)  // this partition's fp32 partial, row-major slice `split`
     store_acc_f32<BM, BN, MS>(acc, g.ws + (size_t)split * (size_t)g.M * (size_t)g.ldw, g.ldw, m0, n0, g.M, g.N);
@@ -738,7 +733,7 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g)
 #pragma unroll
       for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
     __syncthreads();
-    tile_mainloop<BM, BN, MS>(g, m0, n0, k_begin, k_end, acc, smem);
+    tile_mainloop<BM, BN, MS, streamk_depth(BM, BN)>(g, m0, n0, k_begin, k_end, acc, smem);
     const int64_t t0 = (int64_t)tile * ipt;
     const int first_wg = (int)(t0 / g.iters_per_wg);
     const int last_wg = (int)min((int64_t)g.grid - 1, (t0 + ipt - 1) / g.iters_per_wg);
@@ -761,7 +756,7 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g)
 #pragma unroll
       for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
     __syncthreads();
-    tile_mainloop<BM, BN, MS>(g, m0, n0, 0, ipt, acc, smem);
+    tile_mainloop<BM, BN, MS, streamk_depth(BM, BN)>(g, m0, n0, 0, ipt, acc, smem);
     store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
   }
 }
@@ -1173,11 +1168,11 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
 // the accumulators hold the transposed block: one row of C per lane, in runs
 // of four consecutive columns (8- or 16-byte stores). Rows past M and columns past N are clamped
 // (their results are never stored); k past K reads as zero. WK = 1: the four
-// waves cover a 64 x 64 block of C, each over all of K. WK = 4: the four waves
-// split the 32-k blocks of one 32 x 32 block evenly and wave 0 adds the four
-// partial sums in wave order through LDS.
+// waves cover a 64 x 64 block of C, each over all of K. WK = 4 or 16: the WK
+// waves split the 32-k blocks of one 32 x 32 block evenly and wave 0 adds
+// the partial sums in wave order through LDS.
 template <int WK, int OUT>
-__global__ __launch_bounds__(256) void k_direct(GemmArgs g) {
+__global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) {
   constexpr int U = 4;  // 32-k blocks whose loads are issued together
   __shared__ f32x16 red[WK > 1 ? (WK - 1) * 64 : 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1345,15 +1340,15 @@ hipError_t launch_reduce(const GemmArgs& g, hipStream_t st, bool obf) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int MS>
+template <int BM, int BN, int MS, int D>
 hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, p.grid_y), block(TileShape<BM, BN, MS>::NT);
   if (p.pk > 1)
-    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_PARTIAL>), grid, block, 0, st, g);
+    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_PARTIAL, D>), grid, block, 0, st, g);
   else if (obf)
-    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_BF16>), grid, block, 0, st, g);
+    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_BF16, D>), grid, block, 0, st, g);
   else
-    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_F32>), grid, block, 0, st, g);
+    hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_F32, D>), grid, block, 0, st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.pk == 1) return e;
   return launch_reduce(g, st, obf);
@@ -1410,7 +1405,7 @@ hipError_t launch_smallk(const Plan& p, const GemmArgs& g, hipStream_t st, bool 
 
 template <int WK>
 hipError_t launch_direct(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
-  const dim3 grid(p.grid_x, p.grid_y), block(256);
+  const dim3 grid(p.grid_x, p.grid_y), block(WK == 1 ? 256 : 64 * WK);
   if (p.pk > 1)
     hipLaunchKernelGGL((k_direct<WK, OUT_PARTIAL>), grid, block, 0, st, g);
   else if (obf)
@@ -1433,11 +1428,11 @@ int occ_of(F kernel_f32, F kernel_bf16, int threads = 256) {
     b = 0;
   return a < b ? a : b;
 }
-template <int BM, int BN, int MS>
+template <int BM, int BN, int MS, int D>
 int occ_tile() {
   constexpr int nt = TileShape<BM, BN, MS>::NT;
-  const int a = occ_of(k_tile<BM, BN, MS, OUT_F32>, k_tile<BM, BN, MS, OUT_BF16>, nt);
-  const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL>, k_tile<BM, BN, MS, OUT_PARTIAL>, nt);
+  const int a = occ_of(k_tile<BM, BN, MS, OUT_F32, D>, k_tile<BM, BN, MS, OUT_BF16, D>, nt);
+  const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL, D>, k_tile<BM, BN, MS, OUT_PARTIAL, D>, nt);
   return a < b ? a : b;
 }
 template <int BM, int BN, int MS>
@@ -1453,16 +1448,22 @@ int occ_skinny_n() {
   return occ_of(k_skinny_n<NT, RB, false>, k_skinny_n<NT, RB, true>);
 }
 
-#define TILES(X) X(256, 256, 32), X(256, 128, 32), X(128, 256, 32), X(128, 128, 32), \
-                 X(128, 64, 32), X(64, 128, 32), X(64, 64, 32), X(32, 32, 16)
-#define L_TILE(a, b, c) &launch_tile<a, b, c>
-#define L_SK(a, b, c) &launch_streamk<a, b, c>
-#define O_TILE(a, b, c) &occ_tile<a, b, c>
-#define O_SK(a, b, c) &occ_streamk<a, b, c>
+// the entries of kTileCfg, in order: (bm, bn, ms, depth)
+#define TILES(X)                                                                                               \
+  X(256, 256, 32, 1), X(256, 128, 32, 1), X(128, 256, 32, 2), X(128, 128, 32, 1), X(128, 64, 32, 1),         \
+      X(64, 128, 32, 1), X(64, 64, 32, 2), X(32, 32, 16, 2), X(128, 128, 32, 2), X(128, 64, 32, 2),           \
+      X(64, 128, 32, 2)
+#define L_TILE(a, b, c, d) &launch_tile<a, b, c, d>
+#define O_TILE(a, b, c, d) &occ_tile<a, b, c, d>
 const LaunchFn kTileFns[] = {TILES(L_TILE)};
-const LaunchFn kStreamKFns[] = {TILES(L_SK)};
 const OccFn kTileOcc[] = {TILES(O_TILE)};
-const OccFn kStreamKOcc[] = {TILES(O_SK)};
+#define STREAMK_TILES(X)                                                                                       \
+  X(256, 256, 32), X(256, 128, 32), X(128, 256, 32), X(128, 128, 32), X(128, 64, 32), X(64, 128, 32),        \
+      X(64, 64, 32), X(32, 32, 16)
+#define L_SK(a, b, c) &launch_streamk<a, b, c>
+#define O_SK(a, b, c) &occ_streamk<a, b, c>
+const LaunchFn kStreamKFns[] = {STREAMK_TILES(L_SK)};
+const OccFn kStreamKOcc[] = {STREAMK_TILES(O_SK)};
 const LaunchFn kSkinnyMFns[] = {&launch_skinny_m<1, 1>, &launch_skinny_m<1, 4>, &launch_skinny_m<2, 1>,
                                 &launch_skinny_m<2, 4>, &launch_skinny_m<4, 1>, &launch_skinny_m<4, 4>};
 const OccFn kSkinnyMOcc[] = {&occ_skinny_m<1, 1>, &occ_skinny_m<1, 4>, &occ_skinny_m<2, 1>,
@@ -1475,32 +1476,45 @@ int occ_smallk() {
 }
 template <int WK>
 int occ_direct() {
-  const int a = occ_of(k_direct<WK, OUT_F32>, k_direct<WK, OUT_BF16>);
-  const int b = occ_of(k_direct<WK, OUT_PARTIAL>, k_direct<WK, OUT_PARTIAL>);
+  constexpr int nt = WK == 1 ? 256 : 64 * WK;
+  const int a = occ_of(k_direct<WK, OUT_F32>, k_direct<WK, OUT_BF16>, nt);
+  const int b = occ_of(k_direct<WK, OUT_PARTIAL>, k_direct<WK, OUT_PARTIAL>, nt);
   return a < b ? a : b;
 }
 
 const LaunchFn kSmallKFns[] = {&launch_smallk<8>, &launch_smallk<16>};
-const LaunchFn kDirectFns[] = {&launch_direct<1>, &launch_direct<4>};
-const OccFn kDirectOcc[] = {&occ_direct<1>, &occ_direct<4>};
+const LaunchFn kDirectFns[] = {&launch_direct<1>, &launch_direct<4>, &launch_direct<16>};
+const OccFn kDirectOcc[] = {&occ_direct<1>, &occ_direct<4>, &occ_direct<16>};
 static_assert(sizeof(kDirectFns) / sizeof(kDirectFns[0]) == N_DIRECT_CFG, "direct table");
-static_assert(kDirectCfg[0].wk == 1 && kDirectCfg[1].wk == 4, "direct order");
+static_assert(kDirectCfg[0].wk == 1 && kDirectCfg[1].wk == 4 && kDirectCfg[2].wk == 16, "direct order");
 const OccFn kSmallKOcc[] = {&occ_smallk<8>, &occ_smallk<16>};
 static_assert(sizeof(kSmallKFns) / sizeof(kSmallKFns[0]) == N_SMALLK_CFG, "small-K table");
 static_assert(kSmallKCfg[0].kmax == 8 && kSmallKCfg[1].kmax == 16, "small-K order");
 static_assert(sizeof(kTileFns) / sizeof(kTileFns[0]) == N_TILE_CFG, "tile table");
+static_assert(sizeof(kStreamKFns) / sizeof(kStreamKFns[0]) == N_STREAMK_CFG, "stream-K table");
+#define CHK_TILE(a, b, c, d) {a, b, c, d}
+constexpr int kTileCheck[][4] = {TILES(CHK_TILE)};
+constexpr bool tiles_match() {
+  for (int i = 0; i < N_TILE_CFG; ++i)
+    if (kTileCheck[i][0] != kTileCfg[i].bm || kTileCheck[i][1] != kTileCfg[i].bn ||
+        kTileCheck[i][2] != kTileCfg[i].ms || kTileCheck[i][3] != kTileCfg[i].depth)
+      return false;
+  return true;
+}
+static_assert(tiles_match(), "tile kernels must follow kTileCfg");
 static_assert(sizeof(kSkinnyMFns) / sizeof(kSkinnyMFns[0]) == N_SKINNY_M_CFG, "skinny-M table");
 static_assert(sizeof(kSkinnyNFns) / sizeof(kSkinnyNFns[0]) == N_SKINNY_N_CFG, "skinny-N table");
 
-// The tables above must list the configurations in the order of variants.h.
-constexpr bool tile_order_ok() {
+// The tables above must list the configurations in the order of variants.h
+// (the tile kernels are checked by tiles_match).
+constexpr bool streamk_order_ok() {
   const int e[][3] = {{256, 256, 32}, {256, 128, 32}, {128, 256, 32}, {128, 128, 32},
                       {128, 64, 32},  {64, 128, 32},  {64, 64, 32},   {32, 32, 16}};
-  for (int i = 0; i < N_TILE_CFG; ++i)
+  for (int i = 0; i < N_STREAMK_CFG; ++i)
     if (kTileCfg[i].bm != e[i][0] || kTileCfg[i].bn != e[i][1] || kTileCfg[i].ms != e[i][2]) return false;
   return true;
 }
-static_assert(tile_order_ok(), "tile configuration order");
+static_assert(streamk_order_ok(), "stream-K configuration order");
 static_assert(kSkinnyMCfg[0].mt == 1 && kSkinnyMCfg[1].wkw == 4 && kSkinnyMCfg[4].mt == 4, "skinny-M order");
 static_assert(kSkinnyNCfg[0].nt == 1 && kSkinnyNCfg[2].nt == 4 && kSkinnyNCfg[0].rb == 2, "skinny-N order");
 static_assert(SKINNY_N_KMAX == SKN_KMAX, "skinny-N LDS slice");
@@ -1527,10 +1541,8 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
 }
 
 void query_occupancy() {
-  for (int i = 0; i < N_TILE_CFG; ++i) {
-    set_runtime_occupancy(FAM_TILE, i, kTileOcc[i]());
-    set_runtime_occupancy(FAM_STREAMK, i, kStreamKOcc[i]());
-  }
+  for (int i = 0; i < N_TILE_CFG; ++i) set_runtime_occupancy(FAM_TILE, i, kTileOcc[i]());
+  for (int i = 0; i < N_STREAMK_CFG; ++i) set_runtime_occupancy(FAM_STREAMK, i, kStreamKOcc[i]());
   for (int i = 0; i < N_SKINNY_M_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_M, i, kSkinnyMOcc[i]());
   for (int i = 0; i < N_SKINNY_N_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_N, i, kSkinnyNOcc[i]());
   for (int i = 0; i < N_SMALLK_CFG; ++i) set_runtime_occupancy(FAM_SMALLK, i, kSmallKOcc[i]());

@@ -45,8 +45,8 @@ constexpr int IDX_SKINNY_M = IDX_TILE + N_TILE_CFG;
 constexpr int IDX_SKINNY_N = IDX_SKINNY_M + N_SKINNY_M_CFG;
 constexpr int IDX_SMALLK = IDX_SKINNY_N + N_SKINNY_N_CFG;
 constexpr int IDX_STREAMK = IDX_SMALLK + N_SMALLK_CFG;
-constexpr int IDX_DIRECT = IDX_STREAMK + N_TILE_CFG;
-static_assert(IDX_DIRECT + N_DIRECT_CFG <= 32, "calibrated cost tables");
+constexpr int IDX_DIRECT = IDX_STREAMK + N_STREAMK_CFG;
+static_assert(IDX_DIRECT + N_DIRECT_CFG <= AC_N_CFG, "calibrated cost tables");
 
 // Tiles the taxonomy uses for its spatial predicate: the menu entries whose
 // accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
@@ -184,7 +184,7 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
     w->epi = (double)pk * s.M * s.N * 4;
     w->epi_out = (double)s.M * s.N * c.cbytes;
   }
-  w->prefetch = 2;
+  w->prefetch = t.depth;
   w->total_read = (double)tm * tn * (bm_e + bn_e) * (double)s.K * 2;
   w->unaligned = c.unaligned;
   return true;
@@ -334,9 +334,10 @@ bool build_direct(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   w->occ = occupancy(FAM_DIRECT, cfg);
   w->idx = IDX_DIRECT + cfg;
   // one iteration = one 32-k block of every wave: 16 B of A and 16 B of B
-  // per lane and k-group, four waves
+  // per lane and k-group
+  const int waves = d.wk == 1 ? 4 : d.wk;
   w->L = (double)kb_wave;
-  w->bytes_it = 4.0 * 64 * 32 * 2;
+  w->bytes_it = (double)waves * 64 * 32 * 2;
   w->mfma_it = 2.0 * 16;  // two 32x32x16 MFMAs of 16 cycles on each SIMD
   w->lds_it = 0;
   w->out_unit = (double)T * T * (pk == 1 ? c.cbytes : 4);
@@ -482,25 +483,33 @@ adaptcore_hw_t default_hw() {
   // (squared log error of the model over every measured configuration). The
   // launch cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 1.416e-06;
+  h.t_mem_latency = 1.569e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 3.038e+10;
+  h.l2_bw_cu = 2.828e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 5.731e-33;
-  // per configuration (tile 0-7, skinny-M 8-13, skinny-N 14-16, small-K
-  // 17-18, stream-K 19-26, direct 27-28; 0 = analytic estimate, no timing
+  h.l2_hit = 5.433e-33;
+  // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
+  // 20-21, stream-K 22-29, direct 30-32; 0 = analytic estimate, no timing
   // data)
-  static const double kIter[32] = {
-      2.819e-06, 2.023e-06, 1.804e-06, 1.347e-06, 9.407e-07, 9.358e-14, 5.394e-07, 3.621e-07,
-      1.201e-06, 8.341e-10, 1.348e-06, 1.601e-06, 1.877e-06, 2.15e-06, 5.5e-07, 7.079e-07,
-      7.624e-07, 5.394e-07, 2.959e-07, 1.052e-13, 1.116e-13, 1.286e-13, 1.324e-06, 8.09e-07,
-      9.358e-14, 0, 0, 9.358e-14, 9.358e-14, 0, 0, 0};
-  static const double kWg[32] = {
-      2.92e-06, 1.345e-06, 3.678e-06, 1.517e-06, 2.678e-07, 2.58e-06, 4.234e-07, 3.439e-07,
-      5.461e-07, 3.735e-06, 2.377e-06, 2.876e-06, 4.669e-06, 4.995e-06, 6.572e-07, 1.424e-06,
-      1.739e-06, 4.114e-07, 1.126e-06, 2.344e-05, 4.891e-06, 1.97e-05, 6.434e-06, 9.839e-06,
-      1.067e-05, 0, 0, 9.358e-14, 6.55e-07, 0, 0, 0};
-  for (int i = 0; i < 32; ++i) {
+  static const double kIter[AC_N_CFG] = {
+      2.819e-06, 2.005e-06, 1.786e-06, 9.358e-14, 3.963e-07, 2.836e-07, 5.422e-07, 3.634e-07,
+      1.013e-06, 9.358e-14, 9.358e-14, 1.187e-06, 1.232e-06, 1.448e-06, 1.613e-06, 1.854e-06,
+      2.387e-06, 5.448e-07, 7.844e-07, 6.38e-07, 2.835e-07, 5.052e-08, 4.306e-06, 2.349e-06,
+      2.627e-06, 1.462e-06, 1.002e-06, 1.112e-06, 0, 0, 9.358e-14, 9.358e-14,
+      2.556e-09, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0};
+  static const double kWg[AC_N_CFG] = {
+      2.414e-06, 1.037e-06, 3.354e-06, 2.741e-06, 2.526e-07, 5.547e-07, 2.316e-07, 1.259e-07,
+      2.254e-06, 1.694e-06, 1.928e-06, 3.536e-07, 6.864e-07, 2.198e-06, 3.013e-06, 5.389e-06,
+      4.376e-06, 5.049e-07, 1.191e-06, 1.886e-06, 5.397e-07, 1.19e-06, 4.181e-06, 9.358e-14,
+      7.701e-06, 3.483e-06, 4.402e-06, 4.075e-06, 0, 0, 9.358e-14, 3.17e-07,
+      1.05e-07, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0};
+  for (int i = 0; i < AC_N_CFG; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];
   }
@@ -559,7 +568,7 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
         if (build_tile(c, cfg, pk, sw, &p, &w)) add(p, w);
       }
     }
-    if (c.hw.enable_streamk) {
+    if (c.hw.enable_streamk && cfg < N_STREAMK_CFG) {
       Plan p;
       Work w;
       if (build_streamk(c, cfg, &p, &w)) add(p, w);
@@ -671,7 +680,7 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
       ok = sw == 0 && cfg < N_SKINNY_N_CFG && pk >= 1 && build_skinny_n(c, cfg, pk, &p, &w);
       break;
     case FAM_STREAMK:
-      ok = sw == 0 && cfg < N_TILE_CFG && build_streamk(c, cfg, &p, &w) && p.pk == pk;
+      ok = sw == 0 && cfg < N_STREAMK_CFG && build_streamk(c, cfg, &p, &w) && p.pk == pk;
       break;
     case FAM_SMALLK:
       ok = sw == 0 && cfg < N_SMALLK_CFG && build_smallk(c, cfg, pk, &p, &w);
@@ -695,7 +704,7 @@ std::string kernel_names(const Plan& p) {
   switch (p.family) {
     case FAM_TILE: {
       const TileCfg& t = kTileCfg[p.cfg];
-      std::snprintf(buf, sizeof buf, "k_tile<%d, %d, %d, %d>", t.bm, t.bn, t.ms, p.pk > 1 ? 2 : obf);
+      std::snprintf(buf, sizeof buf, "k_tile<%d, %d, %d, %d, %d>", t.bm, t.bn, t.ms, p.pk > 1 ? 2 : obf, t.depth);
       std::string r(buf);
       if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
       return r;
@@ -743,7 +752,7 @@ int config_index(int family, int cfg) {
     case FAM_SMALLK:
       return cfg >= 0 && cfg < N_SMALLK_CFG ? IDX_SMALLK + cfg : -1;
     case FAM_STREAMK:
-      return cfg >= 0 && cfg < N_TILE_CFG ? IDX_STREAMK + cfg : -1;
+      return cfg >= 0 && cfg < N_STREAMK_CFG ? IDX_STREAMK + cfg : -1;
     case FAM_DIRECT:
       return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
   }

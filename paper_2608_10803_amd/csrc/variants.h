@@ -5,19 +5,24 @@
 
 namespace ac {
 
-// Macro-tile configurations of the tile kernel (4 waves in a 2 x 2 grid, k
-// granule BK = 64, LDS double buffered). ms = MFMA tile (32: 32x32x16,
-// 16: 16x16x32). occ = workgroups per CU the planner assumes until the device
-// reports the real figure.
+// Macro-tile configurations of the tile kernel (k granule BK = 64, LDS
+// double buffered; 4 waves in a 2 x 2 grid, 8 waves in 2 x 4 for the 256-row
+// tiles). ms = MFMA tile (32: 32x32x16, 16: 16x16x32). depth = k-blocks of
+// global loads held in registers ahead of the LDS stage (1 or 2: two hide more
+// latency on long K, one keeps more workgroups per CU). occ = workgroups per
+// CU the planner assumes until the device reports the real figure. The first
+// N_STREAMK_CFG configurations also have a stream-K kernel.
 struct TileCfg {
-  int bm, bn, ms, occ;
+  int bm, bn, ms, occ, depth;
 };
 constexpr int TILE_BK = 64;
 constexpr TileCfg kTileCfg[] = {
-    {256, 256, 32, 1}, {256, 128, 32, 1}, {128, 256, 32, 1}, {128, 128, 32, 2},
-    {128, 64, 32, 2},  {64, 128, 32, 2},  {64, 64, 32, 4},   {32, 32, 16, 8},
+    {256, 256, 32, 1, 1}, {256, 128, 32, 1, 1}, {128, 256, 32, 1, 2}, {128, 128, 32, 2, 1},
+    {128, 64, 32, 2, 1},  {64, 128, 32, 2, 1},  {64, 64, 32, 4, 2},   {32, 32, 16, 8, 2},
+    {128, 128, 32, 1, 2}, {128, 64, 32, 2, 2},  {64, 128, 32, 2, 2},
 };
 constexpr int N_TILE_CFG = sizeof(kTileCfg) / sizeof(kTileCfg[0]);
+constexpr int N_STREAMK_CFG = 8;
 
 inline int tile_lds_bytes(const TileCfg& t) { return 2 * (t.bm + t.bn) * TILE_BK * 2 + 16; }
 
@@ -53,11 +58,12 @@ constexpr int N_SMALLK_CFG = sizeof(kSmallKCfg) / sizeof(kSmallKCfg[0]);
 constexpr int SMALLK_MAX_ROWS = 32;
 
 // Direct configurations: wk = 1: four waves cover 64 x 64 of C, each over
-// all of K; wk = 4: four waves split the K range of one 32 x 32 block.
+// all of K; wk = 4 or 16: that many waves split the K range of one 32 x 32
+// block (a workgroup of 64 * wk threads).
 struct DirectCfg {
   int wk, occ;
 };
-constexpr DirectCfg kDirectCfg[] = {{1, 4}, {4, 4}};
+constexpr DirectCfg kDirectCfg[] = {{1, 4}, {4, 4}, {16, 1}};
 constexpr int N_DIRECT_CFG = sizeof(kDirectCfg) / sizeof(kDirectCfg[0]);
 inline int direct_tile(const DirectCfg& c) { return c.wk == 1 ? 64 : 32; }
 
