@@ -404,17 +404,22 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
   const int64_t tm = cdiv(s.M, t.bm), tn = cdiv(s.N, t.bn);
   const int64_t ntiles = tm * tn;
   const int64_t ipt = cdiv(s.K, TILE_BK);
-  if (ipt < 2 || ntiles > (1LL << 30)) return false;
+  if (ntiles > (1LL << 30)) return false;
   const int64_t G = (int64_t)c.hw.n_cu * occupancy(FAM_STREAMK, cfg);
   int64_t sk;
-  if (ntiles >= G) {
+  if (ipt < 2) {
+    sk = 0;  // one k-block per tile: nothing to split, persistent data-parallel only
+    if (ntiles <= G) return false;  // one tile per workgroup: the tile kernel itself
+  } else if (ntiles >= G) {
+    // a whole number of waves stays data-parallel (persistent workgroups,
+    // each running its tiles back to back), otherwise the last partial wave
+    // (plus one full wave when there are at least two) is split
     sk = ntiles % G;
-    if (sk == 0) return false;  // a whole number of waves: data-parallel is already balanced
-    if (ntiles >= 2 * G) sk += G;
+    if (sk != 0 && ntiles >= 2 * G) sk += G;
   } else {
     sk = ntiles;
   }
-  const int64_t ipw = cdiv(sk * ipt, G);
+  const int64_t ipw = sk > 0 ? cdiv(sk * ipt, G) : 0;
   const int64_t grid = std::min<int64_t>(G, std::max<int64_t>(cdiv(sk * ipt, ipw), 1));
   p->family = FAM_STREAMK;
   p->cfg = cfg;
@@ -431,8 +436,8 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
   p->grid_y = 1;
   p->iters_per_wg = (int)ipw;
   p->sk_tiles = (int)sk;
-  p->ws_pk = (int)(cdiv(ipt, ipw) + 1);
-  p->n_launch = 2;
+  p->ws_pk = sk > 0 ? (int)(cdiv(ipt, ipw) + 1) : 0;
+  p->n_launch = sk > 0 ? 2 : 1;
   p->ws_bytes = (int64_t)sk * p->ws_pk * t.bm * t.bn * 4;
   const int ks = t.ms == 32 ? 16 : 32, cyc = t.ms == 32 ? 32 : 16;
   const int TM = t.bm / 2 / t.ms, TN = t.bn / 2 / t.ms;
@@ -440,7 +445,7 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
   w->units = G;
   w->occ = occupancy(FAM_STREAMK, cfg);
   w->idx = IDX_STREAMK + cfg;
-  w->L = (double)ipw + (double)((ntiles - sk) / G) * ipt;
+  w->L = (double)ipw + (double)cdiv(ntiles - sk, G) * ipt;
   w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
   w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
   w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (t.bm + t.bn) * TILE_BK * 2;
@@ -711,8 +716,10 @@ std::string kernel_names(const Plan& p) {
     }
     case FAM_STREAMK: {
       const TileCfg& t = kTileCfg[p.cfg];
-      std::snprintf(buf, sizeof buf, "k_streamk<%d, %d, %d, %s>;k_sk_fixup<%s>", t.bm, t.bn, t.ms, b, b);
-      return buf;
+      std::snprintf(buf, sizeof buf, "k_streamk<%d, %d, %d, %s>", t.bm, t.bn, t.ms, b);
+      std::string r(buf);
+      if (p.sk_tiles > 0) r += std::string(";k_sk_fixup<") + b + ">";
+      return r;
     }
     case FAM_SKINNY_M: {
       const SkinnyMCfg& k = kSkinnyMCfg[p.cfg];

@@ -168,3 +168,20 @@ def test_workspace_reuse_across_plans_and_streams():
         for stream in (0, s2.cuda_stream):
             vals, ok = run(ac.adaptcore_plan(M, N, K, F32), A, B, M, N, K, F32, stream=stream)
             assert ok and np.array_equal(vals, exact.astype(np.float64)), (M, N, K)
+
+
+@pytest.mark.parametrize("shape", [(4096, 2048, 40), (3000, 2000, 64), (1500, 1300, 130)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_persistent_streamk_configurations(shape):
+    """Stream-K with more tiles than persistent workgroups, including the
+    pure data-parallel form (one k-block per tile, or a whole number of
+    waves), against the oracle."""
+    M, N, K = shape
+    A, B = gen.operands(M, N, K, seed=M + N + K)
+    ref = gemm_ref.gemm(A, B)
+    cands = [c for c in all_candidates(M, N, K, BF16) if c["family_name"] == "streamk"]
+    assert cands
+    for c in cands:
+        plan = forced_plan(M, N, K, BF16, c["variant_key"])
+        vals, ok = run(plan, A, B, M, N, K, BF16)
+        check(vals, ok, A, B, BF16, ref=ref, label="%s %s" % (shape, c))
