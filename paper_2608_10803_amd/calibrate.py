@@ -38,7 +38,7 @@ BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.
 N_CFG = ac.AC_N_CFG
 
 
-def sample_shapes(n_sweep=120, seed=11):
+def sample_shapes(n_sweep=200, seed=11):
     """A stratified sample of the dynamic-shape sweep (evenly spaced in the
     order of the roofline floor) plus the decode-style and small-MN large-K
     shapes."""

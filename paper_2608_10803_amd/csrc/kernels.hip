@@ -25,6 +25,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kernel_args.h"
 
 namespace ac {
@@ -1274,6 +1276,47 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
   // (operands swapped: the MFMA forms the transposed block) the lane holds
   // row m0 + lane % 32 and, for q = 0..3, the four consecutive columns
   // n0 + 8q + 4 * (lane / 32) .. +3
+  if constexpr (WK == 1) {
+    // the workgroup's 64 x 64 block goes through LDS (rows padded by 4
+    // elements) and leaves as whole 16-byte row segments
+    typedef typename std::conditional<OUT == OUT_BF16, uint16_t, float>::type T;
+    constexpr int LD = 64 + 4, VEC = 16 / sizeof(T);  // elements per 16-byte chunk
+    __shared__ __attribute__((aligned(16))) T ct[64 * LD];
+    const int r = (wave >> 1) * 32 + (lane & 31);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c = (wave & 1) * 32 + 8 * q + 4 * (lane >> 5);
+      if constexpr (OUT == OUT_BF16) {
+        const uint32_t lo = (uint32_t)to_bf16(acc[4 * q]) | ((uint32_t)to_bf16(acc[4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)to_bf16(acc[4 * q + 2]) | ((uint32_t)to_bf16(acc[4 * q + 3]) << 16);
+        *reinterpret_cast<uint64_t*>(ct + r * LD + c) = (uint64_t)lo | ((uint64_t)hi << 32);
+      } else {
+        const f32x4 v = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+        *reinterpret_cast<f32x4*>(ct + r * LD + c) = v;
+      }
+    }
+    __syncthreads();
+    const int64_t tm0 = (int64_t)tm * 64, tn0 = (int64_t)tn * 64;
+    T* dst = OUT == OUT_PARTIAL ? reinterpret_cast<T*>(g.ws + (size_t)split * (size_t)M * (size_t)g.ldw)
+                                : static_cast<T*>(g.C);
+    const int64_t ldd = OUT == OUT_PARTIAL ? g.ldw : g.ldc;
+    constexpr int CPR = 64 / VEC;  // chunks per row
+    for (int e = threadIdx.x; e < 64 * CPR; e += 256) {
+      const int rr = e / CPR, cc = (e % CPR) * VEC;
+      const int64_t gr = tm0 + rr, gc = tn0 + cc;
+      if (gr >= M || gc >= N) continue;
+      const T* src = ct + rr * LD + cc;  // 8-byte aligned
+      T* d = dst + gr * ldd + gc;
+      if (gc + VEC <= N) {
+        const uint64_t v[2] = {*reinterpret_cast<const uint64_t*>(src),
+                               *reinterpret_cast<const uint64_t*>(src + VEC / 2)};
+        __builtin_memcpy(d, v, 16);
+      } else {
+        for (int j = 0; j < (int)(N - gc); ++j) d[j] = src[j];
+      }
+    }
+    return;
+  }
   const int64_t row = m0 + (lane & 31);
   if (row >= M) return;
   float* part = g.ws + (size_t)split * (size_t)M * (size_t)g.ldw;
