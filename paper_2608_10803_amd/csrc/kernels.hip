@@ -1276,9 +1276,11 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
   // (operands swapped: the MFMA forms the transposed block) the lane holds
   // row m0 + lane % 32 and, for q = 0..3, the four consecutive columns
   // n0 + 8q + 4 * (lane / 32) .. +3
-  if constexpr (WK == 1) {
-    // the workgroup's 64 x 64 block goes through LDS (rows padded by 4
-    // elements) and leaves as whole 16-byte row segments
+  // Wide outputs over many workgroups are bound by writing C: the 64 x 64
+  // configuration then sends its block through LDS (rows padded by 4
+  // elements) so that it leaves as whole 16-byte row segments. Small grids
+  // are bound by latency and store straight from the registers.
+  if (WK == 1 && N >= 64 && gridDim.x * gridDim.y >= 256) {
     typedef typename std::conditional<OUT == OUT_BF16, uint16_t, float>::type T;
     constexpr int LD = 64 + 4, VEC = 16 / sizeof(T);  // elements per 16-byte chunk
     __shared__ __attribute__((aligned(16))) T ct[64 * LD];

@@ -488,29 +488,29 @@ adaptcore_hw_t default_hw() {
   // (squared log error of the model over every measured configuration). The
   // launch cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 1.569e-06;
+  h.t_mem_latency = 1.413e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 2.828e+10;
+  h.l2_bw_cu = 2.924e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 5.433e-33;
+  h.l2_hit = 5.38e-33;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
   // 20-21, stream-K 22-29, direct 30-32; 0 = analytic estimate, no timing
   // data)
   static const double kIter[AC_N_CFG] = {
-      2.819e-06, 2.005e-06, 1.786e-06, 9.358e-14, 3.963e-07, 2.836e-07, 5.422e-07, 3.634e-07,
-      1.013e-06, 9.358e-14, 9.358e-14, 1.187e-06, 1.232e-06, 1.448e-06, 1.613e-06, 1.854e-06,
-      2.387e-06, 5.448e-07, 7.844e-07, 6.38e-07, 2.835e-07, 5.052e-08, 4.306e-06, 2.349e-06,
-      2.627e-06, 1.462e-06, 1.002e-06, 1.112e-06, 0, 0, 9.358e-14, 9.358e-14,
-      2.556e-09, 0, 0, 0, 0, 0, 0, 0,
+      2.815e-06, 2.118e-06, 1.926e-06, 2.437e-07, 5.203e-07, 1.698e-07, 5.358e-07, 3.969e-07,
+      1.12e-06, 1.247e-08, 9.358e-14, 1.227e-06, 1.261e-06, 1.401e-06, 1.449e-06, 1.766e-06,
+      1.927e-06, 6.713e-07, 6.871e-07, 8.035e-07, 2.977e-07, 2.297e-07, 4.526e-06, 2.412e-06,
+      3.436e-06, 1.552e-06, 9.109e-07, 9.865e-07, 0, 0, 9.358e-14, 9.358e-14,
+      7.418e-10, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      2.414e-06, 1.037e-06, 3.354e-06, 2.741e-06, 2.526e-07, 5.547e-07, 2.316e-07, 1.259e-07,
-      2.254e-06, 1.694e-06, 1.928e-06, 3.536e-07, 6.864e-07, 2.198e-06, 3.013e-06, 5.389e-06,
-      4.376e-06, 5.049e-07, 1.191e-06, 1.886e-06, 5.397e-07, 1.19e-06, 4.181e-06, 9.358e-14,
-      7.701e-06, 3.483e-06, 4.402e-06, 4.075e-06, 0, 0, 9.358e-14, 3.17e-07,
-      1.05e-07, 0, 0, 0, 0, 0, 0, 0,
+      2.444e-06, 1.089e-06, 3.064e-06, 2.587e-06, 1.625e-07, 8.336e-07, 3.744e-07, 6.185e-08,
+      1.997e-06, 1.815e-06, 2.047e-06, 7.784e-07, 1.236e-06, 2.791e-06, 4.058e-06, 6.408e-06,
+      7.185e-06, 7.458e-07, 1.118e-06, 1.8e-06, 8.864e-07, 1.308e-06, 9.358e-14, 1.519e-06,
+      8.521e-06, 1.478e-07, 3.444e-06, 1.381e-06, 0, 0, 1.011e-07, 3.985e-07,
+      2.047e-07, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
