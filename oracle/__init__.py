@@ -3,6 +3,8 @@ path computes. TEST INFRASTRUCTURE ONLY: imported by tests, by the smoke
 check and by the benchmark's CPU-baseline leg, never by the product.
 
   gemm_ref.c / gemm_ref.py  C = A * B in fp64 from bf16/fp16 inputs
+  grouped_ref.py            the grouped product (one plain product per
+                            group of consecutive rows, per-group B)
   taxonomy.py               the tiling taxonomy and the latency model's
                             closed forms, in exact rational arithmetic
 
