@@ -70,7 +70,8 @@ typedef enum {
   AC_FAMILY_SKINNY_N = 2, /* Small-M Copy by orientation: A streamed once, N <= 64 */
   AC_FAMILY_STREAMK = 3,  /* StreamK applied to the tile kernel */
   AC_FAMILY_SMALLK = 4,   /* K <= 16: rank-K update bound by writing C */
-  AC_FAMILY_DIRECT = 5    /* small problems: MFMA fragments straight from memory, no LDS */
+  AC_FAMILY_DIRECT = 5,   /* small problems: MFMA fragments straight from memory, no LDS */
+  AC_FAMILY_GROUPED = 6   /* the tile kernel over the groups of a grouped product */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */
@@ -91,6 +92,7 @@ typedef struct {
   int32_t n_candidates; /* legal candidates the model compared */
   double predicted_s;   /* model latency of the selected configuration, seconds */
   int64_t workspace_bytes; /* fp32 partial tiles + counters needed per stream */
+  int64_t groups;       /* grouped plans: number of groups (M is the row capacity); else 0 */
 } adaptcore_plan_desc_t;
 
 /* One legal candidate of a shape (adaptcore_candidates). */
@@ -188,6 +190,53 @@ const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, 
  * stream; calls on different streams use different workspaces. */
 adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
                                   int64_t ldb, void* C, int64_t ldc, void* stream);
+
+/* ---- Grouped product (GroupMM) ---------------------------------------------
+ * The paper replaces the grouped products of its end-to-end models (GroupMM,
+ * Section 6.5; operator scope, Section 7) as well as plain ones, and names
+ * MoE routing as a source of run-time shape changes (Section 2.2). Here a
+ * grouped product computes, for g = 0 .. groups-1,
+ *     C[rows of g] = A[rows of g] * B_g,
+ * in the contiguous form an MoE layer has after sorting tokens by expert:
+ *   - A (rows x K, lda) and C (rows x N, ldc) are row-major with the rows of
+ *     group 0, then group 1, ...; `rows` is the row capacity of A and C;
+ *   - group g owns counts[g] consecutive rows; `counts` is a DEVICE array of
+ *     `groups` int32 values that the host never reads (no synchronisation),
+ *     so every count array is given a meaning: a negative count is read as
+ *     0, and rows at or past `rows` are dropped -- group g covers rows
+ *     [min(P_{g-1}, rows), min(P_g, rows)), P_g the running sum of the
+ *     non-negative counts;
+ *   - B_g (K x N, ldb, row-major) starts stride_b elements after B_{g-1}
+ *     (stride_b = 0: all groups share one B).
+ * Rows covered by no group are not written. Inputs bf16, fp32 accumulation,
+ * C fp32 or bf16 as the plan's dtype says. One kernel launch per call.
+ *
+ * Returns the cached plan for (rows, groups, N, K, dtype, layouts): rows, N,
+ * K in [0, 2^31), groups in [0, 2^20]. The model prices the balanced split
+ * of the rows (the counts are not known when planning). NULL on invalid or
+ * unsupported arguments. Host-only. */
+const adaptcore_plan_t* adaptcore_grouped_plan(int64_t rows, int64_t groups, int64_t N, int64_t K, int32_t dtype,
+                                               uint32_t layouts);
+
+/* Like adaptcore_grouped_plan with the configuration forced to variant_key
+ * (family AC_FAMILY_GROUPED, P_k = 1, a tile configuration that has a
+ * grouped kernel). For tests. NULL if the key is not legal. */
+const adaptcore_plan_t* adaptcore_grouped_plan_variant(int64_t rows, int64_t groups, int64_t N, int64_t K,
+                                                       int32_t dtype, uint32_t layouts, uint64_t variant_key);
+
+/* Runs a grouped plan asynchronously on `stream`. counts: device pointer to
+ * the plan's `groups` int32 counts, read by the kernel when it runs. A, B, C
+ * device pointers (A, B 2-byte aligned, C aligned to its element size; C
+ * must not overlap A or B). Checks: lda >= K, ldb >= N, ldc >= N, all >= 1,
+ * 0 <= stride_b < 2^40 (AC_ERR_INVALID_VALUE); lda or ldb >= AC_MAX_LD
+ * (AC_ERR_UNSUPPORTED); a plan of adaptcore_plan given here, or a grouped
+ * plan given to adaptcore_matmul: AC_ERR_INVALID_VALUE. rows, groups or N
+ * equal to 0: nothing is launched. K == 0: the covered rows of C are set to
+ * zero. The caller guarantees that B holds every group's matrix:
+ * (groups - 1) * stride_b + (K - 1) * ldb + N elements. No workspace. */
+adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
+                                          int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
+                                          int64_t ldc, void* stream);
 
 /* Allocates (if needed) the workspace of `stream` for plans needing up to
  * `bytes`, so that later calls, also under capture, do not allocate. */

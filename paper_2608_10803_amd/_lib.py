@@ -24,10 +24,11 @@ AC_ERR_INTERNAL = -6
 AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
 AC_LAYOUT_ROW_ROW = 0
-AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT = range(6)
+(AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
+ AC_FAMILY_GROUPED) = range(7)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
-FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped"]
 
 
 class AdaptCoreError(RuntimeError):
@@ -45,7 +46,8 @@ class PlanDesc(ctypes.Structure):
                 ("pm", ctypes.c_int32), ("pn", ctypes.c_int32), ("pk", ctypes.c_int32),
                 ("grid_x", ctypes.c_int32), ("grid_y", ctypes.c_int32),
                 ("swizzle", ctypes.c_int32), ("n_candidates", ctypes.c_int32),
-                ("predicted_s", ctypes.c_double), ("workspace_bytes", ctypes.c_int64)]
+                ("predicted_s", ctypes.c_double), ("workspace_bytes", ctypes.c_int64),
+                ("groups", ctypes.c_int64)]
 
     def as_dict(self):
         d = {f: getattr(self, f) for f, _ in self._fields_}
@@ -124,6 +126,12 @@ def lib():
         L.adaptcore_plan_variant.restype = p
         L.adaptcore_matmul.argtypes = [p, p, i64, p, i64, p, i64, p]
         L.adaptcore_matmul.restype = i32
+        L.adaptcore_grouped_plan.argtypes = [i64, i64, i64, i64, i32, u32]
+        L.adaptcore_grouped_plan.restype = p
+        L.adaptcore_grouped_plan_variant.argtypes = [i64, i64, i64, i64, i32, u32, u64]
+        L.adaptcore_grouped_plan_variant.restype = p
+        L.adaptcore_grouped_matmul.argtypes = [p, p, p, i64, p, i64, i64, p, i64, p]
+        L.adaptcore_grouped_matmul.restype = i32
         L.adaptcore_reserve_workspace.argtypes = [p, i64]
         L.adaptcore_reserve_workspace.restype = i32
         L.adaptcore_plan_info.argtypes = [p, ctypes.POINTER(PlanDesc)]
@@ -195,6 +203,26 @@ def adaptcore_plan_variant(M, N, K, dtype, layouts, variant_key):
 def adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream=0):
     """C = A * B on `stream`; A, B, C are device addresses (ints)."""
     return _check(lib().adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream))
+
+
+def adaptcore_grouped_plan(rows, groups, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):
+    """Cached grouped-product plan handle (int)."""
+    h = lib().adaptcore_grouped_plan(rows, groups, N, K, dtype, layouts)
+    if not h:
+        raise AdaptCoreError(adaptcore_last_status(), last_error())
+    return h
+
+
+def adaptcore_grouped_plan_variant(rows, groups, N, K, dtype, layouts, variant_key):
+    h = lib().adaptcore_grouped_plan_variant(rows, groups, N, K, dtype, layouts, variant_key)
+    if not h:
+        raise AdaptCoreError(adaptcore_last_status(), last_error())
+    return h
+
+
+def adaptcore_grouped_matmul(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream=0):
+    """Grouped product on `stream`; counts, A, B, C are device addresses."""
+    return _check(lib().adaptcore_grouped_matmul(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream))
 
 
 def adaptcore_reserve_workspace(stream, nbytes):

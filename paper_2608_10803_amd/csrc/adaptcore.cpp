@@ -59,6 +59,10 @@ std::vector<Table*> g_retired;
 std::vector<adaptcore_plan_s*> g_owned;
 std::map<std::tuple<int64_t, int64_t, int64_t, int, uint32_t>, adaptcore_plan_s*> g_big;  // dims >= 2^17
 std::map<std::pair<std::tuple<int64_t, int64_t, int64_t, int, uint32_t>, uint64_t>, adaptcore_plan_s*> g_forced;
+// grouped plans: (rows, groups, N, K, dtype, layouts) [, forced key]
+typedef std::tuple<int64_t, int64_t, int64_t, int64_t, int, uint32_t> GroupKey;
+std::map<GroupKey, adaptcore_plan_s*> g_grouped;
+std::map<std::pair<GroupKey, uint64_t>, adaptcore_plan_s*> g_grouped_forced;
 
 inline uint64_t mix(uint64_t x) {
   x ^= x >> 33;
@@ -301,6 +305,8 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
                                   void* C, int64_t ldc, void* stream) {
   if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
   const ac::Plan& p = plan->p;
+  if (p.family == ac::FAM_GROUPED)
+    return fail(AC_ERR_INVALID_VALUE, "grouped plan: run it with adaptcore_grouped_matmul");
   const int64_t M = p.s.M, N = p.s.N, K = p.s.K;
   if (M == 0 || N == 0) return AC_OK;
   if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
@@ -349,6 +355,114 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   return AC_OK;
 }
 
+const adaptcore_plan_t* adaptcore_grouped_plan(int64_t rows, int64_t groups, int64_t N, int64_t K, int32_t dtype,
+                                               uint32_t layouts) {
+  adaptcore_status st;
+  if (!valid_args(rows, N, K, dtype, layouts, &st)) return nullptr;
+  if (groups < 0 || groups > (1LL << 20)) {
+    fail(AC_ERR_INVALID_VALUE, "groups must be in [0, 2^20]");
+    return nullptr;
+  }
+  st_lookups.fetch_add(1, std::memory_order_relaxed);
+  const GroupKey k = std::make_tuple(rows, groups, N, K, (int)dtype, layouts);
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_grouped.find(k);
+  if (it != g_grouped.end()) {
+    st_hits.fetch_add(1, std::memory_order_relaxed);
+    return it->second;
+  }
+  const auto t0 = std::chrono::steady_clock::now();
+  ac::Plan p;
+  const ac::Shape s{rows, N, K, dtype, layouts};
+  if (!ac::plan_grouped(s, groups, g_hw, &p)) {
+    fail(AC_ERR_UNSUPPORTED, "no grouped configuration fits (launch grid too large)");
+    return nullptr;
+  }
+  bool exact;
+  p.shape_key = ac::shape_key(s, &exact);
+  auto* pp = new adaptcore_plan_s{p};
+  g_owned.push_back(pp);
+  g_grouped[k] = pp;
+  st_miss_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  st_misses.fetch_add(1, std::memory_order_relaxed);
+  st_entries.fetch_add(1, std::memory_order_relaxed);
+  return pp;
+}
+
+const adaptcore_plan_t* adaptcore_grouped_plan_variant(int64_t rows, int64_t groups, int64_t N, int64_t K,
+                                                       int32_t dtype, uint32_t layouts, uint64_t variant_key) {
+  adaptcore_status st;
+  if (!valid_args(rows, N, K, dtype, layouts, &st)) return nullptr;
+  if (groups < 0 || groups > (1LL << 20)) {
+    fail(AC_ERR_INVALID_VALUE, "groups must be in [0, 2^20]");
+    return nullptr;
+  }
+  const GroupKey k = std::make_tuple(rows, groups, N, K, (int)dtype, layouts);
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_grouped_forced.find(std::make_pair(k, variant_key));
+  if (it != g_grouped_forced.end()) return it->second;
+  ac::Plan p;
+  const ac::Shape s{rows, N, K, dtype, layouts};
+  if (!ac::grouped_for_key(s, groups, g_hw, variant_key, &p)) {
+    fail(AC_ERR_INVALID_VALUE, "variant key is not a legal grouped configuration");
+    return nullptr;
+  }
+  bool exact;
+  p.shape_key = ac::shape_key(s, &exact);
+  auto* pp = new adaptcore_plan_s{p};
+  g_owned.push_back(pp);
+  g_grouped_forced[std::make_pair(k, variant_key)] = pp;
+  return pp;
+}
+
+adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
+                                          int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
+                                          int64_t ldc, void* stream) {
+  if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
+  const ac::Plan& p = plan->p;
+  if (p.family != ac::FAM_GROUPED)
+    return fail(AC_ERR_INVALID_VALUE, "not a grouped plan: run it with adaptcore_matmul");
+  const int64_t rows = p.s.M, N = p.s.N, K = p.s.K;
+  if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
+    return fail(AC_ERR_INVALID_VALUE, "leading dimension smaller than the row length");
+  if (stride_b < 0 || stride_b >= (1LL << 40)) return fail(AC_ERR_INVALID_VALUE, "stride_b must be in [0, 2^40)");
+  if (lda >= AC_MAX_LD || ldb >= AC_MAX_LD)
+    return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
+  if (rows == 0 || p.groups == 0 || N == 0 || p.grid_x == 0) return AC_OK;
+  if (!C || !counts || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null pointer");
+  const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
+  if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)) || ((uintptr_t)counts & 3))
+    return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
+  adaptcore_status st = ensure_init();
+  if (st != AC_OK) return st;
+
+  ac::GroupArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.g.A = static_cast<const uint16_t*>(A);
+  a.g.B = static_cast<const uint16_t*>(B);
+  a.g.C = C;
+  a.g.M = rows;
+  a.g.N = N;
+  a.g.K = K;
+  a.g.lda = lda;
+  a.g.ldb = ldb;
+  a.g.ldc = ldc;
+  a.g.pk = 1;
+  a.g.kper = p.kper;
+  a.g.tiles_m = p.pm;
+  a.g.tiles_n = p.pn;
+  a.g.swizzle = p.swizzle;
+  a.counts = counts;
+  a.rows = rows;
+  a.stride_b = stride_b;
+  a.groups = (int)p.groups;
+  a.slots = p.pm;
+  const hipError_t e = ac::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  st_launches.fetch_add(1, std::memory_order_relaxed);
+  return AC_OK;
+}
+
 adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out) {
   if (!plan || !out) return fail(AC_ERR_INVALID_VALUE, "null argument");
   const ac::Plan& p = plan->p;
@@ -374,6 +488,7 @@ adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_pla
   out->n_candidates = p.n_candidates;
   out->predicted_s = p.predicted;
   out->workspace_bytes = p.ws_bytes;
+  out->groups = p.groups;
   return AC_OK;
 }
 
@@ -460,6 +575,8 @@ adaptcore_status adaptcore_cache_clear(void) {
   g_owned.clear();
   g_big.clear();
   g_forced.clear();
+  g_grouped.clear();
+  g_grouped_forced.clear();
   st_entries.store(0);
   return AC_OK;
 }

@@ -13,7 +13,8 @@ enum Family : int {
   FAM_STREAMK = 3,   // StreamK applied to the tile kernel (Section 4.2)
   FAM_SMALLK = 4,    // K <= 16: rank-K update, bound by writing C
   FAM_DIRECT = 5,    // small problems: MFMA fragments loaded straight from memory
-  FAM_COUNT = 6
+  FAM_GROUPED = 6,   // the tile kernel over the groups of a grouped product
+  FAM_COUNT = 7
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N
@@ -36,6 +37,19 @@ struct GemmArgs {
   int sk_tiles;      // stream-K: tiles handled by the stream-K phase
   int ws_pk;         // stream-K: partial slots per split tile
   int grid;          // stream-K: persistent workgroups
+};
+
+// Arguments of the grouped kernel. Group g owns rows [min(P_{g-1}, rows),
+// min(P_g, rows)) of A and C (P: running sum of max(counts, 0)) and
+// multiplies them by the K x N matrix at B + g * stride_b. g.M is unused;
+// g.tiles_n is the tile count along N.
+struct GroupArgs {
+  GemmArgs g;
+  const int32_t* counts;  // device, `groups` entries
+  int64_t rows;           // rows of A and C (capacity)
+  int64_t stride_b;       // elements between the B matrices of two groups
+  int groups;
+  int slots;              // row-tile slots launched (an upper bound of the tiles along M)
 };
 
 }  // namespace ac

@@ -701,6 +701,133 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
     store_tile_c<BM, BN, MS, OUT == OUT_BF16>(acc, g, m0, n0, smem);
 }
 
+// --------------------------------------------------------- grouped kernel
+// One launch for all groups of a grouped product (an MoE layer's experts).
+// The grid covers an upper bound of the row tiles (slots) times the column
+// tiles; every workgroup derives its group and row tile from the device
+// counts itself, so the host needs neither the counts nor a second kernel.
+
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Row ranges and row-tile counts of 64 consecutive groups, one per lane, as
+// wave-wide inclusive prefix sums (rows_incl clamped by the caller).
+template <int BM>
+struct GroupChunk {
+  int64_t lo, r;  // first row and row count of the lane's group
+  int t, ts;      // row tiles of the lane's group, inclusive sum over the chunk
+  int64_t rsum;   // rows of the whole chunk (unclamped)
+  __device__ __forceinline__ void load(const GroupArgs& a, int c, int64_t row_base) {
+    const int lane = threadIdx.x & 63;
+    const int gi = c + lane;
+    const int64_t cnt = gi < a.groups ? (int64_t)max(a.counts[gi], 0) : 0;
+    int64_t p = cnt;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int64_t o = __shfl_up(p, d);
+      if (lane >= d) p += o;
+    }
+    const int64_t hi = min(row_base + p, a.rows);
+    lo = min(row_base + p - cnt, a.rows);
+    r = hi - lo;
+    t = (int)((r + BM - 1) / BM);
+    ts = t;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int o = __shfl_up(ts, d);
+      if (lane >= d) ts += o;
+    }
+    rsum = __shfl(p, 63);
+  }
+};
+
+// Total row tiles of all groups.
+template <int BM>
+__device__ __forceinline__ int group_tiles_total(const GroupArgs& a, const GroupChunk<BM>& first) {
+  int total = __shfl(first.ts, 63);
+  int64_t row_base = min(first.rsum, a.rows);
+  for (int c = 64; c < a.groups; c += 64) {
+    GroupChunk<BM> k;
+    k.load(a, c, row_base);
+    total += __shfl(k.ts, 63);
+    row_base = min(row_base + k.rsum, a.rows);
+  }
+  return total;
+}
+
+// Group, first row, row count and row tile of `slot`; false if the slot is
+// past the last tile.
+template <int BM>
+__device__ __forceinline__ bool group_of_slot(const GroupArgs& a, const GroupChunk<BM>& first, int slot, int& grp,
+                                              int64_t& row0, int64_t& rows_g, int& tm) {
+  int tile_base = 0;
+  int64_t row_base = 0;
+  GroupChunk<BM> k = first;
+  for (int c = 0; c < a.groups; c += 64) {
+    if (c > 0) k.load(a, c, row_base);
+    const uint64_t hit = __ballot(tile_base + k.ts > slot);
+    if (hit) {
+      const int f = __builtin_ctzll(hit);
+      grp = c + f;
+      row0 = __shfl(k.lo, f);
+      rows_g = __shfl(k.r, f);
+      tm = slot - (tile_base + __shfl(k.ts, f) - __shfl(k.t, f));
+      return true;
+    }
+    tile_base += __shfl(k.ts, 63);
+    row_base = min(row_base + k.rsum, a.rows);
+  }
+  return false;
+}
+
+template <int BM, int BN, int MS, int OUT, int DEPTH>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a) {
+  typedef TileShape<BM, BN, MS> S;
+  typedef typename AccOf<MS>::T Acc;
+  __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
+
+  const int tiles_n = a.g.tiles_n;
+  GroupChunk<BM> first;
+  first.load(a, 0, 0);
+  int t = blockIdx.x;
+  if (a.g.swizzle) {
+    // XCD-aware order over the tiles that exist: each XCD takes a contiguous
+    // range of (row tile, column tile) ids, the surplus blocks leave
+    const int n = group_tiles_total<BM>(a, first) * tiles_n;
+    if (t >= n) return;
+    t = xcd_remap(t, n);
+  }
+  const int slot = t / tiles_n, tn = t - slot * tiles_n;
+  int grp = 0, tm = 0;
+  int64_t row0 = 0, rows_g = 0;
+  if (!group_of_slot<BM>(a, first, slot, grp, row0, rows_g, tm)) return;
+  // the same values in every lane: keep them scalar for the address bases
+  grp = __builtin_amdgcn_readfirstlane(grp);
+  tm = __builtin_amdgcn_readfirstlane(tm);
+  row0 = uniform64(row0);
+  rows_g = uniform64(rows_g);
+
+  GemmArgs g = a.g;
+  g.A += row0 * g.lda;
+  g.B += (int64_t)grp * a.stride_b;
+  g.C = static_cast<char*>(g.C) + row0 * g.ldc * (OUT == OUT_BF16 ? 2 : 4);
+  g.M = rows_g;
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  const int kt_total = (int)((g.K + S::BK - 1) / S::BK);
+
+  Acc acc[S::TM][S::TN];
+#pragma unroll
+  for (int i = 0; i < S::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
+
+  tile_mainloop<BM, BN, MS, DEPTH>(g, m0, n0, 0, kt_total, acc, smem);
+  store_tile_c<BM, BN, MS, OUT == OUT_BF16>(acc, g, m0, n0, smem);
+}
+
 // --------------------------------------------------------- stream-K kernel
 // A persistent grid of g.grid workgroups. The first `sk_tiles` tiles (in
 // tile-id order) are split into MAC iterations (one k-block each) and every
@@ -1462,6 +1589,17 @@ hipError_t launch_direct(const Plan& p, const GemmArgs& g, hipStream_t st, bool 
   return launch_reduce(g, st, obf);
 }
 
+template <int BM, int BN, int MS, int D>
+hipError_t launch_grouped(const Plan& p, const GroupArgs& a, hipStream_t st, bool obf) {
+  const dim3 grid(p.grid_x), block(TileShape<BM, BN, MS>::NT);
+  if (obf)
+    hipLaunchKernelGGL((k_grouped<BM, BN, MS, OUT_BF16, D>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((k_grouped<BM, BN, MS, OUT_F32, D>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+typedef hipError_t (*GroupLaunchFn)(const Plan&, const GroupArgs&, hipStream_t, bool);
+
 template <typename F>
 int occ_of(F kernel_f32, F kernel_bf16, int threads = 256) {
   int a = 0, b = 0;
@@ -1479,6 +1617,10 @@ int occ_tile() {
   const int a = occ_of(k_tile<BM, BN, MS, OUT_F32, D>, k_tile<BM, BN, MS, OUT_BF16, D>, nt);
   const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL, D>, k_tile<BM, BN, MS, OUT_PARTIAL, D>, nt);
   return a < b ? a : b;
+}
+template <int BM, int BN, int MS, int D>
+int occ_grouped() {
+  return occ_of(k_grouped<BM, BN, MS, OUT_F32, D>, k_grouped<BM, BN, MS, OUT_BF16, D>, TileShape<BM, BN, MS>::NT);
 }
 template <int BM, int BN, int MS>
 int occ_streamk() {
@@ -1564,6 +1706,31 @@ static_assert(kSkinnyMCfg[0].mt == 1 && kSkinnyMCfg[1].wkw == 4 && kSkinnyMCfg[4
 static_assert(kSkinnyNCfg[0].nt == 1 && kSkinnyNCfg[2].nt == 4 && kSkinnyNCfg[0].rb == 2, "skinny-N order");
 static_assert(SKINNY_N_KMAX == SKN_KMAX, "skinny-N LDS slice");
 
+// Grouped kernels of the configurations kGroupedCfg enables (null otherwise).
+template <int I>
+constexpr GroupLaunchFn grouped_fn() {
+  constexpr TileCfg t = kTileCfg[I];
+  if constexpr (kGroupedCfg[I])
+    return &launch_grouped<t.bm, t.bn, t.ms, t.depth>;
+  else
+    return nullptr;
+}
+template <int I>
+constexpr OccFn grouped_occ() {
+  constexpr TileCfg t = kTileCfg[I];
+  if constexpr (kGroupedCfg[I])
+    return &occ_grouped<t.bm, t.bn, t.ms, t.depth>;
+  else
+    return nullptr;
+}
+static_assert(N_TILE_CFG == 11, "grouped tables list every tile configuration");
+const GroupLaunchFn kGroupedFns[] = {grouped_fn<0>(), grouped_fn<1>(), grouped_fn<2>(), grouped_fn<3>(),
+                                     grouped_fn<4>(), grouped_fn<5>(), grouped_fn<6>(), grouped_fn<7>(),
+                                     grouped_fn<8>(), grouped_fn<9>(), grouped_fn<10>()};
+const OccFn kGroupedOcc[] = {grouped_occ<0>(), grouped_occ<1>(), grouped_occ<2>(), grouped_occ<3>(),
+                             grouped_occ<4>(), grouped_occ<5>(), grouped_occ<6>(), grouped_occ<7>(),
+                             grouped_occ<8>(), grouped_occ<9>(), grouped_occ<10>()};
+
 }  // namespace
 
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
@@ -1585,6 +1752,12 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st) {
+  if (p.family != FAM_GROUPED || p.cfg < 0 || p.cfg >= N_TILE_CFG || !kGroupedFns[p.cfg])
+    return hipErrorInvalidValue;
+  return kGroupedFns[p.cfg](p, a, st, p.s.dtype == AC_BF16_BF16OUT);
+}
+
 void query_occupancy() {
   for (int i = 0; i < N_TILE_CFG; ++i) set_runtime_occupancy(FAM_TILE, i, kTileOcc[i]());
   for (int i = 0; i < N_STREAMK_CFG; ++i) set_runtime_occupancy(FAM_STREAMK, i, kStreamKOcc[i]());
@@ -1592,6 +1765,8 @@ void query_occupancy() {
   for (int i = 0; i < N_SKINNY_N_CFG; ++i) set_runtime_occupancy(FAM_SKINNY_N, i, kSkinnyNOcc[i]());
   for (int i = 0; i < N_SMALLK_CFG; ++i) set_runtime_occupancy(FAM_SMALLK, i, kSmallKOcc[i]());
   for (int i = 0; i < N_DIRECT_CFG; ++i) set_runtime_occupancy(FAM_DIRECT, i, kDirectOcc[i]());
+  for (int i = 0; i < N_TILE_CFG; ++i)
+    if (kGroupedOcc[i]) set_runtime_occupancy(FAM_GROUPED, i, kGroupedOcc[i]());
 }
 
 }  // namespace ac

@@ -24,6 +24,7 @@ int table_occ(int family, int cfg) {
   switch (family) {
     case FAM_TILE:
     case FAM_STREAMK:
+    case FAM_GROUPED:
       return kTileCfg[cfg].occ;
     case FAM_SKINNY_M:
       return kSkinnyMCfg[cfg].occ;
@@ -468,6 +469,56 @@ bool finish(const Ctx& c, Plan* p, const Work& w) {
   return p->ws_bytes <= ((int64_t)2 << 30);  // workspace cap
 }
 
+// The grouped kernel for one tile configuration. Launch: an upper bound of
+// the row tiles over any split of the rows into `groups` groups -- at most
+// ne = min(groups, rows) groups hold rows, each adds at most one partial
+// tile -- times the column tiles. Model: the counts are on the device, so
+// the plan assumes the balanced split (ne groups of rows / ne rows) and
+// prices it as ne independent products of that shape sharing the GPU.
+bool build_grouped(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, int cfg, int swizzle, Plan* p) {
+  if (cfg < 0 || cfg >= N_TILE_CFG || !kGroupedCfg[cfg]) return false;
+  const TileCfg& t = kTileCfg[cfg];
+  if (tile_lds_bytes(t) > hw.lds_bytes) return false;
+  const int64_t ne = std::min<int64_t>(groups, s.M);
+  const int64_t slots = ne > 0 ? (s.M - ne) / t.bm + ne : 0;
+  const int64_t tn = cdiv(s.N, t.bn);
+  const int64_t threads = t.bm == 256 ? 512 : 256;
+  if (slots * tn > (1LL << 31) - 1 || slots * tn * threads >= (1LL << 32)) return false;
+  p->s = s;
+  p->groups = groups;
+  p->family = FAM_GROUPED;
+  p->cfg = cfg;
+  p->swizzle = swizzle;
+  p->tile_m = t.bm;
+  p->tile_n = t.bn;
+  p->tile_k = TILE_BK;
+  p->pm = (int)slots;
+  p->pn = (int)tn;
+  p->pk = 1;
+  p->kper = (int)cdiv(s.K, TILE_BK);
+  p->grid_x = (int)(slots * tn);
+  p->grid_y = 1;
+  p->n_launch = p->grid_x > 0 ? 1 : 0;
+  p->ws_bytes = 0;
+  p->variant_key = make_variant_key(FAM_GROUPED, cfg, swizzle, 1, s.dtype, (int)s.layouts);
+  if (p->grid_x == 0) {
+    p->predicted = 0;
+    return true;
+  }
+  const Shape sg{cdiv(s.M, ne), s.N, s.K, s.dtype, s.layouts};
+  const double compulsory = 2.0 * sg.M * sg.K + 2.0 * sg.K * sg.N;
+  const bool unaligned = (s.K % 8) != 0 || (s.N % 8) != 0;
+  const Ctx c{sg, hw, compulsory, out_bytes(s.dtype), unaligned};
+  Plan one;
+  Work w;
+  if (!build_tile(c, cfg, 1, swizzle, &one, &w)) return false;
+  w.units *= ne;
+  w.total_read *= (double)ne;
+  w.total_write *= (double)ne;
+  p->predicted = model_time(sg, w, hw, compulsory * (double)ne);
+  return true;
+}
+
 }  // namespace
 
 adaptcore_hw_t default_hw() {
@@ -702,6 +753,39 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
   return true;
 }
 
+bool plan_grouped(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, Plan* out) {
+  bool found = false;
+  int n = 0;
+  for (int cfg = 0; cfg < N_TILE_CFG; ++cfg) {
+    Plan p;
+    if (!build_grouped(s, groups, hw, cfg, 1, &p)) continue;
+    ++n;
+    if (!found || p.predicted < out->predicted) {
+      *out = p;
+      found = true;
+    }
+  }
+  if (found) {
+    int base = 0;
+    out->n_candidates = n;
+    out->cls = classify_shape(s, hw, &base);
+  }
+  return found;
+}
+
+bool grouped_for_key(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, uint64_t key, Plan* out) {
+  if (vk_family(key) != FAM_GROUPED || vk_pk(key) != 1 || vk_dtype(key) != s.dtype ||
+      vk_layouts(key) != (int)s.layouts)
+    return false;
+  Plan p;
+  if (!build_grouped(s, groups, hw, vk_cfg(key), vk_swizzle(key), &p) || p.variant_key != key) return false;
+  int base = 0;
+  p.n_candidates = 1;
+  p.cls = classify_shape(s, hw, &base);
+  *out = p;
+  return true;
+}
+
 std::string kernel_names(const Plan& p) {
   const int obf = p.s.dtype == AC_BF16_BF16OUT;
   const char* b = obf ? "true" : "false";
@@ -738,6 +822,11 @@ std::string kernel_names(const Plan& p) {
     case FAM_SMALLK:
       std::snprintf(buf, sizeof buf, "k_smallk<%d, %s>", kSmallKCfg[p.cfg].kmax, b);
       return buf;
+    case FAM_GROUPED: {
+      const TileCfg& t = kTileCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_grouped<%d, %d, %d, %d, %d>", t.bm, t.bn, t.ms, obf, t.depth);
+      return buf;
+    }
     case FAM_DIRECT: {
       std::snprintf(buf, sizeof buf, "k_direct<%d, %d>", kDirectCfg[p.cfg].wk, p.pk > 1 ? 2 : obf);
       std::string r(buf);
@@ -762,6 +851,8 @@ int config_index(int family, int cfg) {
       return cfg >= 0 && cfg < N_STREAMK_CFG ? IDX_STREAMK + cfg : -1;
     case FAM_DIRECT:
       return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
+    case FAM_GROUPED:  // the tile kernel's costs
+      return cfg >= 0 && cfg < N_TILE_CFG && kGroupedCfg[cfg] ? IDX_TILE + cfg : -1;
   }
   return -1;
 }

@@ -36,6 +36,7 @@ struct Plan {
   int64_t ws_bytes = 0;  // fp32 partials
   int n_candidates = 0;
   double predicted = 0;
+  int64_t groups = 0;    // grouped product: groups (s.M is then the row capacity)
 };
 
 struct Candidate {
@@ -62,6 +63,12 @@ std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_o
 // Fills launch fields and predicted latency for one configuration key;
 // returns false if the key is not legal for the shape.
 bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* out);
+
+// Grouped product of `groups` groups over a row capacity of s.M rows: the
+// model's choice among the grouped tile configurations (plan_grouped), or
+// one configuration forced by its key (grouped_for_key).
+bool plan_grouped(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, Plan* out);
+bool grouped_for_key(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, uint64_t key, Plan* out);
 
 // 64-bit shape key: M | N << 17 | K << 34 | dtype << 51 | layouts << 55, for
 // dimensions below 2^17; larger shapes set bit 63 and hash all fields.

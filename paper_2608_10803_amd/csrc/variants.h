@@ -26,6 +26,11 @@ constexpr int N_STREAMK_CFG = 8;
 
 inline int tile_lds_bytes(const TileCfg& t) { return 2 * (t.bm + t.bn) * TILE_BK * 2 + 16; }
 
+// Tile configurations that also have a grouped kernel (the tile kernel over
+// the groups of a grouped product).
+constexpr bool kGroupedCfg[] = {false, true, true, true, true, true, true, false, true, false, false};
+static_assert(sizeof(kGroupedCfg) / sizeof(kGroupedCfg[0]) == N_TILE_CFG, "grouped configurations");
+
 // Small-M Copy configurations: M <= 16*mt rows, wkw waves split the k-range
 // of a workgroup (the others split its columns); a workgroup covers
 // 128 * (4 / wkw) columns; k granule 32.

@@ -1,0 +1,239 @@
+"""GPU parity of the grouped product (adaptcore_grouped_matmul) against the
+grouped oracle (oracle/grouped_ref.py).
+
+Every grouped configuration runs on ragged sizes with padded leading
+dimensions, empty groups and rows left uncovered; the counts live on the
+device. Output buffers carry canaries: rows that no group covers, the row
+above and below C and the columns past N must keep them. The MoE stream's
+full-size steps (8192 tokens over 64 experts, both routing readings, up- and
+down-projection) are checked on sampled entries. Bar: the error metric
+max |C - C_ref| / sum_k |A_ik B_kj| within 1e-3 (fp32 out) or 8e-3 (bf16 out).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2608_10803_amd as ac
+from oracle import gemm_ref, grouped_ref
+from workloads import gen
+
+from gpu_util import BF16_CANARY, F32_CANARY, Out, to_device, tol, torch
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16 = ac.AC_BF16_F32OUT, ac.AC_BF16_BF16OUT
+
+
+def note(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    torch()
+    ac.adaptcore_init()
+    yield
+
+
+def grouped_keys(rows, G, N, K, dtype):
+    """Every legal forced grouped configuration (both tile orders)."""
+    keys = []
+    for cfg in range(16):
+        for sw in (0, 1):
+            key = ac.AC_FAMILY_GROUPED | (cfg << 4) | (sw << 12) | (1 << 16) | (dtype << 48)
+            try:
+                ac.adaptcore_grouped_plan_variant(rows, G, N, K, dtype, 0, key)
+            except ac.AdaptCoreError:
+                continue
+            keys.append(key)
+    return keys
+
+
+class Case:
+    """Host operands of a grouped product: A (rows x K, lda), the groups' B
+    matrices at multiples of stride_b (ldb), the counts."""
+
+    def __init__(self, counts, rows, N, K, lda=None, ldb=None, stride_b=None, seed=0, shared_b=False):
+        self.counts = np.asarray(counts, np.int32)
+        self.G = len(counts)
+        self.rows, self.N, self.K = rows, N, K
+        self.lda = max(K, 1) if lda is None else lda
+        self.ldb = max(N, 1) if ldb is None else ldb
+        self.stride_b = (K * self.ldb if stride_b is None else stride_b) if not shared_b else 0
+        self.A = gen.uniform_bf16(rows, K, seed) if rows and K else np.zeros((rows, K), np.uint16)
+        nb = max(self.G - 1, 0) * self.stride_b + max(K - 1, 0) * self.ldb + N + 8
+        self.B = np.zeros(nb, np.uint16)
+        for g in range(self.G if not shared_b else 1):
+            if K and N:
+                m = gen.uniform_bf16(K, N, seed + 1 + g)
+                view = np.lib.stride_tricks.as_strided(self.B[g * self.stride_b:], shape=(K, N),
+                                                       strides=(self.ldb * 2, 2))
+                view[...] = m
+
+    def reference(self):
+        Apad = np.zeros((self.rows, self.lda), np.uint16)
+        Apad[:, :self.K] = self.A
+        return grouped_ref.grouped_gemm(Apad, self.B, self.counts, self.rows, self.N, self.K, self.lda,
+                                        self.ldb, self.stride_b)
+
+    def run(self, plan, dtype, ldc=None, a_off=0):
+        t = torch()
+        ldc = max(self.N, 1) if ldc is None else ldc
+        Ad, a = to_device(self.A, self.lda, a_off)
+        Bd = t.from_numpy(self.B.view(np.int16)).to("cuda")
+        cnt = t.from_numpy(self.counts).to("cuda")
+        out = Out(self.rows, self.N, ldc, dtype)
+        ac.adaptcore_grouped_matmul(plan, cnt.data_ptr(), a, self.lda, Bd.data_ptr(), self.ldb, self.stride_b,
+                                    out.addr, ldc, 0)
+        t.cuda.synchronize()
+        vals, ok = out.read()
+        raw = out.dev.cpu().numpy()
+        if dtype == F32:
+            body = raw.reshape(self.rows + 2, ldc)[1:self.rows + 1, :self.N]
+            canary_rows = np.all(body == F32_CANARY, axis=1)
+        else:
+            body = raw.view(np.uint16).reshape(self.rows + 2, ldc)[1:self.rows + 1, :self.N]
+            canary_rows = np.all(body == BF16_CANARY, axis=1)
+        del Ad, Bd, cnt
+        return vals, ok, canary_rows
+
+
+def check(case, vals, ok, canary_rows, dtype, ref, label):
+    C_ref, D, cov = ref
+    assert ok, "write outside C %s" % label
+    assert np.all(canary_rows[~cov]), "a row no group covers was written %s" % label
+    err = gemm_ref.err_metric(vals[cov], C_ref[cov], D[cov])
+    assert err <= tol(dtype), "err %.3g > %.3g %s" % (err, tol(dtype), label)
+    return err
+
+
+RAGGED = dict(counts=[100, 0, 37, 250, 1, 0, 129, 64, 50], rows=700, N=300, K=197)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+def test_every_grouped_configuration(dtype):
+    c = RAGGED
+    case = Case(c["counts"], c["rows"], c["N"], c["K"], lda=c["K"] + 5, ldb=c["N"] + 3,
+                stride_b=c["K"] * (c["N"] + 3) + 11, seed=11)
+    ref = case.reference()
+    keys = grouped_keys(c["rows"], len(c["counts"]), c["N"], c["K"], dtype)
+    assert len(keys) >= 10
+    for key in keys:
+        plan = ac.adaptcore_grouped_plan_variant(c["rows"], len(c["counts"]), c["N"], c["K"], dtype, 0, key)
+        d = ac.adaptcore_plan_info(plan)
+        label = "%s %dx%d sw%d" % (hex(key), d["tile_m"], d["tile_n"], d["swizzle"])
+        note("grouped", label)
+        vals, ok, canary = case.run(plan, dtype, ldc=c["N"] + 7)
+        check(case, vals, ok, canary, dtype, ref, label)
+
+
+SHAPES = [
+    # (counts, rows, N, K)
+    ([3, 5, 0, 9], 17, 3, 5),                 # N < 8 and K < 8: the element-load path
+    ([64, 128, 0, 256, 64], 512, 256, 256),   # whole tiles, aligned rows
+    ([1] * 40, 40, 129, 64),                  # one row per group
+    ([0, 0, 1000], 1000, 70, 1),              # K = 1
+    ([300, 301], 700, 8, 1000),               # long K, narrow N
+]
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "%dx%d_g%d" % (s[2], s[3], len(s[0])))
+def test_default_plan_shapes(shape, dtype):
+    counts, rows, N, K = shape
+    case = Case(counts, rows, N, K, seed=rows + N + K)
+    plan = ac.adaptcore_grouped_plan(rows, len(counts), N, K, dtype)
+    note("grouped", shape, ac.adaptcore_plan_kernels(plan))
+    vals, ok, canary = case.run(plan, dtype, a_off=1)
+    check(case, vals, ok, canary, dtype, case.reference(), str(shape))
+
+
+@pytest.mark.parametrize("sw", [0, 1])
+def test_many_groups_scan_several_chunks(sw):
+    """200 groups: the kernel's prefix scan spans four 64-group chunks."""
+    rng = np.random.default_rng(5)
+    w = rng.zipf(1.2, 200).astype(float)
+    counts = rng.multinomial(3000, w / w.sum())
+    rows, N, K = 3100, 130, 72
+    case = Case(counts, rows, N, K, seed=7)
+    ref = case.reference()
+    for cfg in (3, 6):
+        key = ac.AC_FAMILY_GROUPED | (cfg << 4) | (sw << 12) | (1 << 16) | (BF16 << 48)
+        plan = ac.adaptcore_grouped_plan_variant(rows, 200, N, K, BF16, 0, key)
+        vals, ok, canary = case.run(plan, BF16)
+        check(case, vals, ok, canary, BF16, ref, "cfg %d sw %d" % (cfg, sw))
+
+
+def test_negative_and_over_capacity_counts():
+    """Negative counts read as 0; rows at or past the capacity are dropped."""
+    counts = [50, -7, 80, 0, 200, 90]  # non-negative sum 420 > 300 rows
+    case = Case(counts, 300, 96, 128, seed=9)
+    ref = case.reference()
+    assert ref[2].all()
+    plan = ac.adaptcore_grouped_plan(300, len(counts), 96, 128, F32)
+    vals, ok, canary = case.run(plan, F32)
+    check(case, vals, ok, canary, F32, ref, "negative/over-capacity")
+
+
+def test_shared_b_and_empty_cases():
+    # stride_b = 0: every group multiplies by the same B
+    case = Case([10, 0, 33, 70], 120, 40, 50, seed=13, shared_b=True)
+    plan = ac.adaptcore_grouped_plan(120, 4, 40, 50, BF16)
+    vals, ok, canary = case.run(plan, BF16)
+    check(case, vals, ok, canary, BF16, case.reference(), "shared B")
+    # all counts zero: nothing is written
+    case = Case([0, 0, 0], 64, 32, 16, seed=14)
+    vals, ok, canary = case.run(ac.adaptcore_grouped_plan(64, 3, 32, 16, F32), F32)
+    assert ok and canary.all()
+    # K = 0: covered rows become zero, the others keep their canaries
+    case = Case([5, 0, 7], 20, 24, 0, seed=15)
+    vals, ok, canary = case.run(ac.adaptcore_grouped_plan(20, 3, 24, 0, F32), F32)
+    assert ok and np.all(vals[:12] == 0) and canary[12:].all() and not canary[:12].any()
+
+
+def _sample_rows(counts, rows, rng, per_group=3):
+    I = []
+    for s, e in grouped_ref.group_rows(counts, rows):
+        if e > s:
+            I += [s, e - 1] + list(rng.integers(s, e, per_group))
+    return np.array(I, np.int64)
+
+
+@pytest.mark.parametrize("reading", ["B", "A"])
+def test_moe_stream_full_size(reading):
+    """Two routing steps of the MoE stream (8192 tokens, 64 experts): the
+    up-projection (K 4096 -> N 1536) and down-projection (1536 -> 4096) of
+    all experts, one grouped call each, checked on sampled entries."""
+    t = torch()
+    rows, G = 8192, 64
+    for step, counts in enumerate(gen.moe_counts(steps=2, reading=reading)):
+        for (N, K) in [(gen.MOE_FFN, gen.MOE_HIDDEN), (gen.MOE_HIDDEN, gen.MOE_FFN)]:
+            note("moe", reading, step, (N, K))
+            g = t.Generator(device="cuda")
+            g.manual_seed(100 + step)
+            A = t.empty(rows * K, dtype=t.bfloat16, device="cuda").uniform_(-1, 1, generator=g)
+            B = t.empty(G * K * N, dtype=t.bfloat16, device="cuda").uniform_(-1, 1, generator=g)
+            C = t.full((rows, N), float("nan"), dtype=t.bfloat16, device="cuda")
+            cnt = t.from_numpy(np.asarray(counts, np.int32)).cuda()
+            plan = ac.adaptcore_grouped_plan(rows, G, N, K, BF16)
+            ac.adaptcore_grouped_matmul(plan, cnt.data_ptr(), A.data_ptr(), K, B.data_ptr(), N, K * N,
+                                        C.data_ptr(), N, 0)
+            t.cuda.synchronize()
+            rng = np.random.default_rng(step)
+            I = _sample_rows(counts, rows, rng)
+            J = np.concatenate([[0, N - 1], rng.integers(0, N, len(I) - 2)])
+            got = C[t.from_numpy(I).cuda(), t.from_numpy(J).cuda()]
+            vals = gemm_ref.decode(got.view(t.int16).cpu().numpy().view(np.uint16))
+            # the A rows and B columns the sampled entries need, as bf16 bits
+            bounds = grouped_ref.group_rows(counts, rows)
+            grp = np.array([next(k for k, (s, e) in enumerate(bounds) if s <= i < e) for i in I], np.int64)
+            Ar = A.view(rows, K)[t.from_numpy(I).cuda()].view(t.int16).cpu().numpy().view(np.uint16)
+            Bc = B.view(G, K, N)[t.from_numpy(grp).cuda(), :, t.from_numpy(J).cuda()]  # (samples, K)
+            Bc = np.ascontiguousarray(Bc.view(t.int16).cpu().numpy().view(np.uint16).T)  # (K, samples)
+            n = len(I)
+            C_ref, D = gemm_ref.gemm_entries(Ar, Bc, np.arange(n), np.arange(n), M=n, N=n, K=K)
+            err = gemm_ref.err_metric(vals, C_ref, D)
+            assert err <= tol(BF16), "moe %s step %d %s err %.3g" % (reading, step, (N, K), err)
+            # every covered row was written (no NaN left from the fill)
+            assert not t.isnan(C[:int(np.clip(counts, 0, None).sum())]).any().item()

@@ -1,0 +1,125 @@
+"""Grouped-product planning and C-ABI validation (no GPU).
+
+The grouped kernel's grid must cover every row tile for ANY device count
+array (the host never sees the counts): checked here against brute force
+over random splits, including negative and over-capacity counts. Plans are
+cached, forced configurations round-trip through their keys, and the entry
+points reject bad arguments before any GPU work.
+"""
+import numpy as np
+import pytest
+
+import paper_2608_10803_amd as ac
+
+GROUPED_TILES = {(256, 128), (128, 256), (128, 128), (128, 64), (64, 128), (64, 64)}
+
+
+def _row_tiles(counts, rows, bm):
+    """Row tiles of a split under the stated readings (negative -> 0, rows past
+    the capacity dropped), written out directly."""
+    total, p = 0, 0
+    for c in counts:
+        c = max(int(c), 0)
+        s, e = min(p, rows), min(p + c, rows)
+        total += -(-(e - s) // bm)
+        p += c
+    return total
+
+
+def test_plan_fields_and_cache():
+    h = ac.adaptcore_grouped_plan(8192, 64, 1536, 4096)
+    assert h == ac.adaptcore_grouped_plan(8192, 64, 1536, 4096)
+    d = ac.adaptcore_plan_info(h)
+    assert d["family_name"] == "grouped" and d["groups"] == 64 and d["M"] == 8192
+    assert (d["tile_m"], d["tile_n"]) in GROUPED_TILES
+    assert d["pn"] == -(-1536 // d["tile_n"]) and d["grid_x"] == d["pm"] * d["pn"] and d["pk"] == 1
+    assert d["workspace_bytes"] == 0 and d["predicted_s"] > 0
+    names = ac.adaptcore_plan_kernels(h)
+    assert len(names) == 1 and names[0].startswith("k_grouped<%d, %d, " % (d["tile_m"], d["tile_n"]))
+    # a plain plan of the same dimensions is a different object
+    assert ac.adaptcore_plan(8192, 1536, 4096) != h
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_grid_covers_every_split(seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(60):
+        G = int(rng.integers(1, 300))
+        rows = int(rng.integers(1, 5000))
+        N, K = int(rng.integers(1, 5000)), int(rng.integers(0, 5000))
+        d = ac.adaptcore_plan_info(ac.adaptcore_grouped_plan(rows, G, N, K))
+        bm = d["tile_m"]
+        splits = [rng.multinomial(rows, np.ones(G) / G), rng.integers(-3, 2 * rows // G + 3, G),
+                  np.r_[np.zeros(G - 1, int), rows], np.ones(G, int) * (rows // G + 1)]
+        w = rng.zipf(1.2, G).astype(float)
+        splits.append(rng.multinomial(rows, w / w.sum()))
+        for counts in splits:
+            assert _row_tiles(counts, rows, bm) <= d["pm"], (rows, G, bm, d["pm"])
+        # the bound is reached by one row in each of min(G, rows) groups plus the rest in one group
+        ne = min(G, rows)
+        worst = np.r_[np.ones(ne - 1, int), rows - ne + 1, np.zeros(G - ne, int)]
+        assert _row_tiles(worst, rows, bm) <= d["pm"]
+
+
+def test_forced_configurations_round_trip():
+    for cfg in range(16):
+        for sw in (0, 1):
+            key = ac.AC_FAMILY_GROUPED | (cfg << 4) | (sw << 12) | (1 << 16) | (ac.AC_BF16_BF16OUT << 48)
+            try:
+                h = ac.adaptcore_grouped_plan_variant(700, 9, 300, 197, ac.AC_BF16_BF16OUT, 0, key)
+            except ac.AdaptCoreError:
+                continue
+            d = ac.adaptcore_plan_info(h)
+            assert d["variant_key"] == key and d["swizzle"] == sw
+            assert (d["tile_m"], d["tile_n"]) in GROUPED_TILES
+    # a plain-family key is not a grouped configuration
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_grouped_plan_variant(700, 9, 300, 197, ac.AC_BF16_BF16OUT, 0,
+                                          (3 << 4) | (1 << 16) | (ac.AC_BF16_BF16OUT << 48))
+
+
+def test_argument_validation():
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_grouped_plan(10, -1, 4, 4)
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_grouped_plan(10, (1 << 20) + 1, 4, 4)
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_grouped_plan(-1, 3, 4, 4)
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_grouped_plan(10, 3, 4, 4, 9)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    hg = ac.adaptcore_grouped_plan(64, 4, 32, 16)
+    hp = ac.adaptcore_plan(64, 32, 16)
+    # the two kinds of plan are not interchangeable
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_matmul(hg, 0x1000, 16, 0x2000, 32, 0x3000, 32)
+    assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_grouped_matmul(hp, 0x4000, 0x1000, 16, 0x2000, 32, 512, 0x3000, 32)
+    assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    good = (0x4000, 0x1000, 16, 0x2000, 32, 512, 0x3000, 32)
+    bad = [
+        (0x4000, 0x1000, 15, 0x2000, 32, 512, 0x3000, 32),   # lda < K
+        (0x4000, 0x1000, 16, 0x2000, 31, 512, 0x3000, 32),   # ldb < N
+        (0x4000, 0x1000, 16, 0x2000, 32, 512, 0x3000, 31),   # ldc < N
+        (0x4000, 0x1000, 16, 0x2000, 32, -1, 0x3000, 32),    # stride_b < 0
+        (0x4000, 0x1000, 16, 0x2000, 32, 1 << 40, 0x3000, 32),
+        (0, 0x1000, 16, 0x2000, 32, 512, 0x3000, 32),        # null counts
+        (0x4002, 0x1000, 16, 0x2000, 32, 512, 0x3000, 32),   # misaligned counts
+        (0x4000, 0x1001, 16, 0x2000, 32, 512, 0x3000, 32),   # misaligned A
+        (0x4000, 0x1000, 16, 0x2000, 32, 512, 0, 32),        # null C
+    ]
+    for args in bad:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_grouped_matmul(hg, *args)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE, args
+    for args in [(0x4000, 0x1000, 1 << 23, 0x2000, 32, 512, 0x3000, 32),
+                 (0x4000, 0x1000, 16, 0x2000, 1 << 23, 512, 0x3000, 32)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_grouped_matmul(hg, *args)
+        assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    # nothing to compute: no launch, success anywhere
+    for h in [ac.adaptcore_grouped_plan(0, 4, 32, 16), ac.adaptcore_grouped_plan(64, 0, 32, 16),
+              ac.adaptcore_grouped_plan(64, 4, 0, 16)]:
+        ac.adaptcore_grouped_matmul(h, *good)
+    assert good  # the good tuple is only launched on a GPU (tests/test_gpu_grouped.py)
