@@ -135,12 +135,147 @@ def cpu_baseline(shapes, cbytes, budget_s=15.0, seed=7, max_shapes=200):
                       % (len(per), t_total)}
 
 
+def moe_stream(ac, torch, counts, steps, warmup, grouped):
+    """Seconds per routing step of the MoE stream, median over `steps` timed
+    passes over all routing steps (each step replayed from a HIP graph
+    captured once): every expert's up-projection then every expert's
+    down-projection, either one call per non-empty expert (plans of the
+    dynamic shapes from the cache) or one grouped call per projection."""
+    from workloads import gen
+    dev = torch.device("cuda")
+    T, E, H, F = 8192, len(counts[0]), gen.MOE_HIDDEN, gen.MOE_FFN
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    X = torch.empty(T * H, dtype=torch.bfloat16, device=dev).uniform_(-1, 1, generator=g)
+    Wu = torch.empty(E * H * F, dtype=torch.bfloat16, device=dev).uniform_(-1, 1, generator=g)
+    Wd = torch.empty(E * F * H, dtype=torch.bfloat16, device=dev).uniform_(-1, 1, generator=g)
+    Hb = torch.empty(T * F, dtype=torch.bfloat16, device=dev)
+    Y = torch.empty(T * H, dtype=torch.bfloat16, device=dev)
+    cnt = torch.from_numpy(np.stack(counts).astype(np.int32)).to(dev)
+    bf = ac.AC_BF16_BF16OUT
+    cs = torch.cuda.Stream()
+    st = cs.cuda_stream
+    if grouped:
+        pu = ac.adaptcore_grouped_plan(T, E, F, H, bf)
+        pd = ac.adaptcore_grouped_plan(T, E, H, F, bf)
+        kernels = ac.adaptcore_plan_kernels(pu) + ac.adaptcore_plan_kernels(pd)
+    else:
+        ws = 0
+        kernels = set()
+        for c in counts:
+            for n in c:
+                if n > 0:
+                    for (N, K) in [(F, H), (H, F)]:
+                        d = ac.adaptcore_plan_info(ac.adaptcore_plan(int(n), N, K, bf))
+                        ws = max(ws, d["workspace_bytes"])
+                        kernels.update(ac.adaptcore_plan_kernels(ac.adaptcore_plan(int(n), N, K, bf)))
+        ac.adaptcore_reserve_workspace(st, ws)
+        kernels = sorted(kernels)
+
+    def step_calls(s):
+        if grouped:
+            cp = cnt[s].data_ptr()
+            ac.adaptcore_grouped_matmul(pu, cp, X.data_ptr(), H, Wu.data_ptr(), F, H * F, Hb.data_ptr(), F, st)
+            ac.adaptcore_grouped_matmul(pd, cp, Hb.data_ptr(), F, Wd.data_ptr(), H, F * H, Y.data_ptr(), H, st)
+            return
+        offs = np.concatenate([[0], np.cumsum(counts[s])])
+        for e, n in enumerate(counts[s]):
+            if n > 0:
+                ac.adaptcore_matmul(ac.adaptcore_plan(int(n), F, H, bf), X.data_ptr() + 2 * int(offs[e]) * H, H,
+                                    Wu.data_ptr() + 2 * e * H * F, F, Hb.data_ptr() + 2 * int(offs[e]) * F, F, st)
+        for e, n in enumerate(counts[s]):
+            if n > 0:
+                ac.adaptcore_matmul(ac.adaptcore_plan(int(n), H, F, bf), Hb.data_ptr() + 2 * int(offs[e]) * F, F,
+                                    Wd.data_ptr() + 2 * e * F * H, H, Y.data_ptr() + 2 * int(offs[e]) * H, H, st)
+
+    graphs = []
+    for s in range(len(counts)):
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=cs):
+            step_calls(s)
+        graphs.append(gr)
+    for _ in range(warmup):
+        for gr in graphs:
+            gr.replay()
+    torch.cuda.synchronize()
+    per_pass = []
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    step_t = np.zeros((steps, len(counts)))
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in graphs]
+           for _ in range(steps)]
+    for k in range(steps):
+        e0.record()
+        for s, gr in enumerate(graphs):
+            evs[k][s][0].record()
+            gr.replay()
+            evs[k][s][1].record()
+        e1.record()
+        torch.cuda.synchronize()
+        per_pass.append(e0.elapsed_time(e1) * 1e-3)
+        step_t[k] = [a.elapsed_time(b) * 1e-3 for a, b in evs[k]]
+    del graphs
+    return statistics.median(per_pass) / len(counts), np.median(step_t, axis=0), kernels
+
+
+def moe_main(args):
+    """MoE-style variable-token GEMM stream: 8192 tokens over 64 experts,
+    Zipf(1.2) routing counts (seed 5), up-projection 4096 -> 1536 and
+    down-projection 1536 -> 4096 per expert, bf16 in and out, 100 routing
+    steps. Reported for one grouped call per projection (value) and for one
+    dynamic-shape call per non-empty expert."""
+    import torch
+    import paper_2608_10803_amd as ac
+    from workloads import gen
+    H, F = gen.MOE_HIDDEN, gen.MOE_FFN
+    out = {}
+    for reading in ("B", "A"):
+        counts = gen.moe_counts(steps=100, reading=reading)
+        flops = sum(2.0 * int(n) * F * H * 2 for c in counts for n in c)
+        floor = sum(roof(int(n), F, H, 2)[2] + roof(int(n), H, F, 2)[2] for c in counts for n in c if n > 0)
+        nb = sum(roof(int(n), F, H, 2)[1] + roof(int(n), H, F, 2)[1] for c in counts for n in c if n > 0)
+        r = {}
+        for mode in ("grouped", "per_call"):
+            t_step, t_steps, kernels = moe_stream(ac, torch, counts, args.steps, args.warmup, mode == "grouped")
+            r[mode] = {"us_per_step": round(t_step * 1e6, 2), "tflops": round(flops / len(counts) / t_step / 1e12, 2),
+                       "frac_of_sum_t_floor": round(floor / len(counts) / t_step, 4),
+                       "step_us_min_median_max": [round(float(x) * 1e6, 1) for x in
+                                                  (t_steps.min(), np.median(t_steps), t_steps.max())],
+                       "kernels": kernels if len(kernels) <= 8 else "%d distinct kernels" % len(kernels)}
+        r["speedup_grouped_vs_per_call"] = round(r["per_call"]["us_per_step"] / r["grouped"]["us_per_step"], 3)
+        r["sum_t_floor_us_per_step"] = round(floor / len(counts) * 1e6, 2)
+        r["nonempty_experts_per_step"] = round(sum(int((c > 0).sum()) for c in counts) / len(counts), 2)
+        r["ai_flop_per_byte"] = round(flops / nb, 1)
+        out[reading] = r
+    p = out["B"]
+    t = p["grouped"]["us_per_step"] * 1e-6
+    flops_step = p["grouped"]["tflops"] * 1e12 * t
+    bound = "mfma" if p["ai_flop_per_byte"] >= PEAK_FLOPS / PEAK_BW else "hbm"
+    line = {
+        "metric": "MoE stream TFLOP/s and fraction of per-call roofline (grouped product)",
+        "value": p["grouped"]["tflops"], "unit": "TFLOP/s",
+        "frac": p["grouped"]["frac_of_sum_t_floor"],
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(t * 1e3, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "MoE stream: 8192 tokens, 64 experts, Zipf(1.2) counts (seed 5, reading B primary), "
+                               "up 4096->1536 then down 1536->4096, 100 routing steps",
+                   "timing": "each routing step replayed from a HIP graph; median over passes"},
+        "roofline": {"bound": bound, "achieved": round(flops_step / t / 1e12, 2) if bound == "mfma" else None,
+                     "peak": 2500.0 if bound == "mfma" else 8000.0,
+                     "unit": "TFLOP/s" if bound == "mfma" else "GB/s",
+                     "frac": round(flops_step / t / 2.5e15, 4) if bound == "mfma" else None,
+                     "traffic": None},
+        "readings": out,
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true")
     ap.add_argument("--per-shape", default=None, help="write per-shape results to this JSON file")
@@ -164,6 +299,8 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("no GPU")
     ac.adaptcore_init()
+    if args.workload == "moe":
+        return moe_main(args)
     dev = torch.device("cuda")
     if args.copy_ref:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
