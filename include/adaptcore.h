@@ -71,7 +71,9 @@ typedef enum {
   AC_FAMILY_STREAMK = 3,  /* StreamK applied to the tile kernel */
   AC_FAMILY_SMALLK = 4,   /* K <= 16: rank-K update bound by writing C */
   AC_FAMILY_DIRECT = 5,   /* small problems: MFMA fragments straight from memory, no LDS */
-  AC_FAMILY_GROUPED = 6   /* the tile kernel over the groups of a grouped product */
+  AC_FAMILY_GROUPED = 6,  /* the tile kernel over the groups of a grouped product */
+  AC_FAMILY_PERSIST = 7   /* persistent tile kernel: the next tile's first k-block is fetched
+                             before the current tile's epilogue (K >= 8, N >= 8) */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */

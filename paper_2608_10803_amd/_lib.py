@@ -25,10 +25,10 @@ AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
 AC_LAYOUT_ROW_ROW = 0
 (AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
- AC_FAMILY_GROUPED) = range(7)
+ AC_FAMILY_GROUPED, AC_FAMILY_PERSIST) = range(8)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
-FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped", "persist"]
 
 
 class AdaptCoreError(RuntimeError):

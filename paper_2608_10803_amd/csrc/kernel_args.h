@@ -14,7 +14,8 @@ enum Family : int {
   FAM_SMALLK = 4,    // K <= 16: rank-K update, bound by writing C
   FAM_DIRECT = 5,    // small problems: MFMA fragments loaded straight from memory
   FAM_GROUPED = 6,   // the tile kernel over the groups of a grouped product
-  FAM_COUNT = 7
+  FAM_PERSIST = 7,   // persistent tile kernel, next tile's first block fetched before the epilogue
+  FAM_COUNT = 8
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N

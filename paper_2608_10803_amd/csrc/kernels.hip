@@ -701,6 +701,108 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
     store_tile_c<BM, BN, MS, OUT == OUT_BF16>(acc, g, m0, n0, smem);
 }
 
+// ------------------------------------------------- persistent tile kernel
+// A grid of at most (CUs x workgroups per CU) walks the tiles in strides of
+// the grid. The first k-block of a workgroup's next tile is loaded into
+// registers right after the last k-block of the current tile went to LDS,
+// i.e. before the current tile's last MFMAs and its epilogue: that load's
+// memory latency is hidden behind the stores of C. Loads issued before the
+// stores do not wait for them (vector memory operations complete in issue
+// order). Requires K >= 8 and N >= 8 (the planner offers it only then).
+template <int BM, int BN, int MS, bool OBF>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g) {
+  typedef TileShape<BM, BN, MS> S;
+  typedef typename AccOf<MS>::T Acc;
+  __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
+  u32x4* sA0 = reinterpret_cast<u32x4*>(smem);
+  u32x4* sA1 = sA0 + BM * 8;
+  u32x4* sB0 = sA1 + BM * 8;
+  u32x4* sB1 = sB0 + BN * 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wr = wave / S::WC, wc = wave % S::WC;
+
+  const int ntiles = g.tiles_m * g.tiles_n;
+  const int kt_total = (int)((g.K + S::BK - 1) / S::BK);
+  const bool k_tail = (g.K % S::BK) != 0;
+  int t = blockIdx.x;
+  if (t >= ntiles) return;
+  auto coords = [&](int tt, int64_t& m0, int64_t& n0) {
+    const int tile = g.swizzle ? xcd_remap(tt, ntiles) : tt;
+    int tm, tn;
+    tile_coords(tile, g.tiles_m, g.tiles_n, g.swizzle, tm, tn);
+    m0 = (int64_t)tm * BM;
+    n0 = (int64_t)tn * BN;
+  };
+  auto compute = [&](const u32x4* sA, const u32x4* sB, Acc (&acc)[S::TM][S::TN]) {
+#pragma unroll
+    for (int ks = 0; ks < S::BK / S::KS; ++ks) {
+      const int chunk = MS == 32 ? ks * 2 + (lane >> 5) : ks * 4 + (lane >> 4);
+      u32x4 fa[S::TM], fb[S::TN];
+#pragma unroll
+      for (int i = 0; i < S::TM; ++i) {
+        const int row = wr * S::WTM + i * MS + (lane % MS);
+        fa[i] = sA[row * 8 + swz(row, chunk)];
+      }
+#pragma unroll
+      for (int j = 0; j < S::TN; ++j) {
+        const int col = wc * S::WTN + j * MS + (lane % MS);
+        fb[j] = sB[col * 8 + swz(col, chunk)];
+      }
+#pragma unroll
+      for (int i = 0; i < S::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < S::TN; ++j) {
+          if constexpr (MS == 32)
+            acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
+          else
+            acc[i][j] = mfma16(fb[j], fa[i], acc[i][j]);
+        }
+    }
+  };
+
+  int64_t m0, n0;
+  coords(t, m0, n0);
+  StageGeom<BM, BN, MS> o;
+  o.init(g, m0, n0);
+  Stage<BM, BN, MS> st;
+  st.load(g, o, m0, n0, 0);
+  for (;;) {
+    Acc acc[S::TM][S::TN];
+#pragma unroll
+    for (int i = 0; i < S::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
+    const bool n_edge = n0 + BN > g.N;
+    st.store(sA0, sB0, n_edge || (k_tail && kt_total == 1), o.b_cs);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 1 < kt_total; ++kt) {
+      const bool odd = (kt & 1) != 0;
+      st.load(g, o, m0, n0, kt + 1);
+      compute(odd ? sA1 : sA0, odd ? sB1 : sB0, acc);
+      st.store(odd ? sA0 : sA1, odd ? sB0 : sB1, n_edge || (k_tail && kt + 1 == kt_total - 1), o.b_cs);
+      __syncthreads();
+    }
+    // the last block of this tile is in LDS: fetch the next tile's first
+    // block now, then finish this tile
+    const int tn_next = t + (int)gridDim.x;
+    int64_t m1 = 0, n1 = 0;
+    if (tn_next < ntiles) {
+      coords(tn_next, m1, n1);
+      o.init(g, m1, n1);
+      st.load(g, o, m1, n1, 0);
+    }
+    const bool odd = (kt & 1) != 0;
+    compute(odd ? sA1 : sA0, odd ? sB1 : sB0, acc);
+    store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
+    if (tn_next >= ntiles) break;
+    __syncthreads();  // every wave is done with LDS before the next stage is written
+    t = tn_next;
+    m0 = m1;
+    n0 = n1;
+  }
+}
+
 // --------------------------------------------------------- grouped kernel
 // One launch for all groups of a grouped product (an MoE layer's experts).
 // The grid covers an upper bound of the row tiles (slots) times the column
@@ -1589,6 +1691,16 @@ hipError_t launch_direct(const Plan& p, const GemmArgs& g, hipStream_t st, bool 
   return launch_reduce(g, st, obf);
 }
 
+template <int BM, int BN, int MS>
+hipError_t launch_persist(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
+  const dim3 grid(p.grid_x), block(TileShape<BM, BN, MS>::NT);
+  if (obf)
+    hipLaunchKernelGGL((k_tile_pp<BM, BN, MS, true>), grid, block, 0, st, g);
+  else
+    hipLaunchKernelGGL((k_tile_pp<BM, BN, MS, false>), grid, block, 0, st, g);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int MS, int D>
 hipError_t launch_grouped(const Plan& p, const GroupArgs& a, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x), block(TileShape<BM, BN, MS>::NT);
@@ -1617,6 +1729,10 @@ int occ_tile() {
   const int a = occ_of(k_tile<BM, BN, MS, OUT_F32, D>, k_tile<BM, BN, MS, OUT_BF16, D>, nt);
   const int b = occ_of(k_tile<BM, BN, MS, OUT_PARTIAL, D>, k_tile<BM, BN, MS, OUT_PARTIAL, D>, nt);
   return a < b ? a : b;
+}
+template <int BM, int BN, int MS>
+int occ_persist() {
+  return occ_of(k_tile_pp<BM, BN, MS, false>, k_tile_pp<BM, BN, MS, true>, TileShape<BM, BN, MS>::NT);
 }
 template <int BM, int BN, int MS, int D>
 int occ_grouped() {
@@ -1723,7 +1839,29 @@ constexpr OccFn grouped_occ() {
   else
     return nullptr;
 }
-static_assert(N_TILE_CFG == 11, "grouped tables list every tile configuration");
+template <int I>
+constexpr LaunchFn persist_fn() {
+  constexpr TileCfg t = kTileCfg[I];
+  if constexpr (kPersistCfg[I])
+    return &launch_persist<t.bm, t.bn, t.ms>;
+  else
+    return nullptr;
+}
+template <int I>
+constexpr OccFn persist_occ() {
+  constexpr TileCfg t = kTileCfg[I];
+  if constexpr (kPersistCfg[I])
+    return &occ_persist<t.bm, t.bn, t.ms>;
+  else
+    return nullptr;
+}
+static_assert(N_TILE_CFG == 11, "grouped and persistent tables list every tile configuration");
+const LaunchFn kPersistFns[] = {persist_fn<0>(), persist_fn<1>(), persist_fn<2>(), persist_fn<3>(),
+                                persist_fn<4>(), persist_fn<5>(), persist_fn<6>(), persist_fn<7>(),
+                                persist_fn<8>(), persist_fn<9>(), persist_fn<10>()};
+const OccFn kPersistOcc[] = {persist_occ<0>(), persist_occ<1>(), persist_occ<2>(), persist_occ<3>(),
+                             persist_occ<4>(), persist_occ<5>(), persist_occ<6>(), persist_occ<7>(),
+                             persist_occ<8>(), persist_occ<9>(), persist_occ<10>()};
 const GroupLaunchFn kGroupedFns[] = {grouped_fn<0>(), grouped_fn<1>(), grouped_fn<2>(), grouped_fn<3>(),
                                      grouped_fn<4>(), grouped_fn<5>(), grouped_fn<6>(), grouped_fn<7>(),
                                      grouped_fn<8>(), grouped_fn<9>(), grouped_fn<10>()};
@@ -1748,6 +1886,9 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       return kSmallKFns[p.cfg](p, g, st, obf);
     case FAM_DIRECT:
       return kDirectFns[p.cfg](p, g, st, obf);
+    case FAM_PERSIST:
+      if (p.cfg < 0 || p.cfg >= N_TILE_CFG || !kPersistFns[p.cfg] || g.K < 8 || g.N < 8) return hipErrorInvalidValue;
+      return kPersistFns[p.cfg](p, g, st, obf);
   }
   return hipErrorInvalidValue;
 }
@@ -1767,6 +1908,8 @@ void query_occupancy() {
   for (int i = 0; i < N_DIRECT_CFG; ++i) set_runtime_occupancy(FAM_DIRECT, i, kDirectOcc[i]());
   for (int i = 0; i < N_TILE_CFG; ++i)
     if (kGroupedOcc[i]) set_runtime_occupancy(FAM_GROUPED, i, kGroupedOcc[i]());
+  for (int i = 0; i < N_TILE_CFG; ++i)
+    if (kPersistOcc[i]) set_runtime_occupancy(FAM_PERSIST, i, kPersistOcc[i]());
 }
 
 }  // namespace ac

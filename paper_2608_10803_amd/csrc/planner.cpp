@@ -25,6 +25,7 @@ int table_occ(int family, int cfg) {
     case FAM_TILE:
     case FAM_STREAMK:
     case FAM_GROUPED:
+    case FAM_PERSIST:
       return kTileCfg[cfg].occ;
     case FAM_SKINNY_M:
       return kSkinnyMCfg[cfg].occ;
@@ -47,7 +48,8 @@ constexpr int IDX_SKINNY_N = IDX_SKINNY_M + N_SKINNY_M_CFG;
 constexpr int IDX_SMALLK = IDX_SKINNY_N + N_SKINNY_N_CFG;
 constexpr int IDX_STREAMK = IDX_SMALLK + N_SMALLK_CFG;
 constexpr int IDX_DIRECT = IDX_STREAMK + N_STREAMK_CFG;
-static_assert(IDX_DIRECT + N_DIRECT_CFG <= AC_N_CFG, "calibrated cost tables");
+constexpr int IDX_PERSIST = IDX_DIRECT + N_DIRECT_CFG;
+static_assert(IDX_PERSIST + N_TILE_CFG <= AC_N_CFG, "calibrated cost tables");
 
 // Tiles the taxonomy uses for its spatial predicate: the menu entries whose
 // accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
@@ -188,6 +190,30 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
   w->prefetch = t.depth;
   w->total_read = (double)tm * tn * (bm_e + bn_e) * (double)s.K * 2;
   w->unaligned = c.unaligned;
+  return true;
+}
+
+// Persistent tile kernel: min(tiles, CUs x occupancy) workgroups, each
+// walking ceil(tiles / grid) tiles back to back (Eq. 13 over all of its
+// k-blocks, the first block of every later tile fetched during the previous
+// tile's epilogue).
+bool build_persist(const Ctx& c, int cfg, int swizzle, Plan* p, Work* w) {
+  if (cfg < 0 || cfg >= N_TILE_CFG || !kPersistCfg[cfg]) return false;
+  const Shape& s = c.s;
+  if (s.K < 8 || s.N < 8) return false;
+  if (!build_tile(c, cfg, 1, swizzle, p, w)) return false;
+  const int64_t ntiles = (int64_t)p->pm * p->pn;
+  const int occ = occupancy(FAM_PERSIST, cfg);
+  const int64_t grid = std::min<int64_t>(ntiles, (int64_t)c.hw.n_cu * std::max(1, occ));
+  const int64_t per = cdiv(ntiles, grid);
+  p->family = FAM_PERSIST;
+  p->grid_x = (int)grid;
+  p->grid_y = 1;
+  w->units = grid;
+  w->occ = occ;
+  w->idx = IDX_PERSIST + cfg;
+  w->L = (double)per * (double)p->kper;
+  w->out_unit *= (double)per;
   return true;
 }
 
@@ -541,27 +567,27 @@ adaptcore_hw_t default_hw() {
   h.t_launch = 1.9e-06;
   h.t_mem_latency = 1.413e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 2.924e+10;
+  h.l2_bw_cu = 2.926e+10;
   h.unaligned_eta = 1;
   h.l2_hit = 5.38e-33;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
   // 20-21, stream-K 22-29, direct 30-32; 0 = analytic estimate, no timing
   // data)
   static const double kIter[AC_N_CFG] = {
-      2.815e-06, 2.118e-06, 1.926e-06, 2.437e-07, 5.203e-07, 1.698e-07, 5.358e-07, 3.969e-07,
-      1.12e-06, 1.247e-08, 9.358e-14, 1.227e-06, 1.261e-06, 1.401e-06, 1.449e-06, 1.766e-06,
-      1.927e-06, 6.713e-07, 6.871e-07, 8.035e-07, 2.977e-07, 2.297e-07, 4.526e-06, 2.412e-06,
-      3.436e-06, 1.552e-06, 9.109e-07, 9.865e-07, 0, 0, 9.358e-14, 9.358e-14,
-      7.418e-10, 0, 0, 0, 0, 0, 0, 0,
+      2.843e-06, 2.05e-06, 1.918e-06, 3.911e-07, 5.432e-07, 2.177e-07, 5.382e-07, 3.955e-07,
+      1.111e-06, 2.515e-08, 9.358e-14, 1.229e-06, 1.26e-06, 1.4e-06, 1.405e-06, 1.777e-06,
+      1.905e-06, 6.727e-07, 6.909e-07, 7.981e-07, 2.84e-07, 2.206e-07, 4.678e-06, 2.461e-06,
+      3.445e-06, 1.498e-06, 1.11e-06, 1.072e-06, 0, 0, 9.358e-14, 9.358e-14,
+      1.177e-10, 2.978e-06, 2.153e-06, 0, 5.64e-07, 2.811e-07, 3.431e-07, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      2.444e-06, 1.089e-06, 3.064e-06, 2.587e-06, 1.625e-07, 8.336e-07, 3.744e-07, 6.185e-08,
-      1.997e-06, 1.815e-06, 2.047e-06, 7.784e-07, 1.236e-06, 2.791e-06, 4.058e-06, 6.408e-06,
-      7.185e-06, 7.458e-07, 1.118e-06, 1.8e-06, 8.864e-07, 1.308e-06, 9.358e-14, 1.519e-06,
-      8.521e-06, 1.478e-07, 3.444e-06, 1.381e-06, 0, 0, 1.011e-07, 3.985e-07,
-      2.047e-07, 0, 0, 0, 0, 0, 0, 0,
+      2.279e-06, 1.156e-06, 3.112e-06, 2.405e-06, 1.321e-07, 7.565e-07, 3.633e-07, 3.08e-08,
+      1.991e-06, 1.779e-06, 2.028e-06, 7.933e-07, 1.174e-06, 2.798e-06, 4.069e-06, 6.439e-06,
+      7.013e-06, 6.975e-07, 1.164e-06, 1.996e-06, 9.117e-07, 1.322e-06, 9.358e-14, 1.32e-06,
+      7.478e-06, 2.293e-07, 8.497e-07, 1.111e-06, 0, 0, 9.358e-14, 3.564e-07,
+      1.646e-07, 1.025e-05, 4.617e-06, 0, 3.107e-06, 3.021e-06, 3.526e-06, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
@@ -628,6 +654,23 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
       Plan p;
       Work w;
       if (build_streamk(c, cfg, &p, &w)) add(p, w);
+    }
+  }
+  // persistent tile kernels: only where a workgroup gets more than one tile
+  // (else they equal the tile kernel), and in the class-fixed search only
+  // once their costs are calibrated
+  for (int cfg = 0; cfg < N_TILE_CFG; ++cfg) {
+    if (!kPersistCfg[cfg]) continue;
+    const int idx = IDX_PERSIST + cfg;
+    if (!c.hw.search_open && !(c.hw.cfg_iter[idx] > 0 && c.hw.cfg_wg[idx] > 0)) continue;
+    const TileCfg& t = kTileCfg[cfg];
+    if ((t.bm > 2 * s.M && t.bm > 32) || (t.bn > 2 * s.N && t.bn > 32)) continue;
+    const int64_t ntiles = cdiv(s.M, t.bm) * cdiv(s.N, t.bn);
+    if (ntiles <= (int64_t)c.hw.n_cu * std::max(1, occupancy(FAM_PERSIST, cfg))) continue;
+    for (int sw = 0; sw < 2; ++sw) {
+      Plan p;
+      Work w;
+      if (build_persist(c, cfg, sw, &p, &w)) add(p, w);
     }
   }
   for (int cfg = 0; cfg < N_SKINNY_M_CFG; ++cfg) {
@@ -744,6 +787,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
     case FAM_DIRECT:
       ok = sw == 0 && cfg < N_DIRECT_CFG && build_direct(c, cfg, pk, &p, &w);
       break;
+    case FAM_PERSIST:
+      ok = pk == 1 && build_persist(c, cfg, sw, &p, &w);
+      break;
   }
   if (!ok || !finish(c, &p, w)) return false;
   if (p.variant_key != key) return false;
@@ -822,6 +868,11 @@ std::string kernel_names(const Plan& p) {
     case FAM_SMALLK:
       std::snprintf(buf, sizeof buf, "k_smallk<%d, %s>", kSmallKCfg[p.cfg].kmax, b);
       return buf;
+    case FAM_PERSIST: {
+      const TileCfg& t = kTileCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_tile_pp<%d, %d, %d, %s>", t.bm, t.bn, t.ms, b);
+      return buf;
+    }
     case FAM_GROUPED: {
       const TileCfg& t = kTileCfg[p.cfg];
       std::snprintf(buf, sizeof buf, "k_grouped<%d, %d, %d, %d, %d>", t.bm, t.bn, t.ms, obf, t.depth);
@@ -851,6 +902,8 @@ int config_index(int family, int cfg) {
       return cfg >= 0 && cfg < N_STREAMK_CFG ? IDX_STREAMK + cfg : -1;
     case FAM_DIRECT:
       return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
+    case FAM_PERSIST:
+      return cfg >= 0 && cfg < N_TILE_CFG && kPersistCfg[cfg] ? IDX_PERSIST + cfg : -1;
     case FAM_GROUPED:  // the tile kernel's costs
       return cfg >= 0 && cfg < N_TILE_CFG && kGroupedCfg[cfg] ? IDX_TILE + cfg : -1;
   }

@@ -31,6 +31,11 @@ inline int tile_lds_bytes(const TileCfg& t) { return 2 * (t.bm + t.bn) * TILE_BK
 constexpr bool kGroupedCfg[] = {false, true, true, true, true, true, true, false, true, false, false};
 static_assert(sizeof(kGroupedCfg) / sizeof(kGroupedCfg[0]) == N_TILE_CFG, "grouped configurations");
 
+// Tile configurations that also have a persistent kernel (one k-block of
+// global loads ahead, carried across tiles): the depth-1 configurations.
+constexpr bool kPersistCfg[] = {true, true, false, true, true, true, false, false, false, false, false};
+static_assert(sizeof(kPersistCfg) / sizeof(kPersistCfg[0]) == N_TILE_CFG, "persistent configurations");
+
 // Small-M Copy configurations: M <= 16*mt rows, wkw waves split the k-range
 // of a workgroup (the others split its columns); a workgroup covers
 // 128 * (4 / wkw) columns; k granule 32.

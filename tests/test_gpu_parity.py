@@ -185,3 +185,34 @@ def test_persistent_streamk_configurations(shape):
         plan = forced_plan(M, N, K, BF16, c["variant_key"])
         vals, ok = run(plan, A, B, M, N, K, BF16)
         check(vals, ok, A, B, BF16, ref=ref, label="%s %s" % (shape, c))
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+@pytest.mark.parametrize("shape", [(4200, 4200, 72), (2100, 3000, 200), (3001, 2999, 129)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_persistent_tile_configurations(shape, dtype):
+    """The persistent tile kernels (more tiles than workgroups, the next
+    tile's first k-block fetched before the epilogue) against the oracle, and
+    bitwise equal to the depth-1 tile kernel of the same tile and order (the
+    same k-order for every output)."""
+    M, N, K = shape
+    A, B = gen.operands(M, N, K, seed=M + N + K + 5)
+    ref = gemm_ref.gemm(A, B)
+    cands = all_candidates(M, N, K, dtype)
+    pers = [c for c in cands if c["family_name"] == "persist"]
+    assert pers
+    twins = {}
+    for c in cands:
+        if c["family_name"] == "tile" and c["pk"] == 1:
+            name = ac.adaptcore_plan_kernels(forced_plan(M, N, K, dtype, c["variant_key"]))[0]
+            if name.endswith(", 1>"):  # depth 1
+                twins[(c["tile_m"], c["tile_n"], (c["variant_key"] >> 12) & 1)] = c["variant_key"]
+    for c in pers:
+        note("persistent", shape, c["tile_m"], c["tile_n"], hex(c["variant_key"]))
+        plan = forced_plan(M, N, K, dtype, c["variant_key"])
+        vals, ok = run(plan, A, B, M, N, K, dtype)
+        check(vals, ok, A, B, dtype, ref=ref, label="%s %s" % (shape, c))
+        key = twins.get((c["tile_m"], c["tile_n"], (c["variant_key"] >> 12) & 1))
+        if key is not None:
+            vt, ok2 = run(forced_plan(M, N, K, dtype, key), A, B, M, N, K, dtype)
+            assert ok2 and np.array_equal(vt, vals), "persistent differs from the tile kernel %s" % c
