@@ -25,9 +25,16 @@ dropped -- group g covers rows [min(P_{g-1}, rows), min(P_g, rows)) with P_g
 the running sum of the non-negative counts. Rows not covered by any group
 are not part of the result (the GPU leaves them untouched).
 
+A batched product (BatchMM, named beside GroupMM in the same sections) is
+read as the strided form: batch b multiplies the M x K matrix at
+A + b * stride_a (lda) by the K x N matrix at B + b * stride_b (ldb) into the
+M x N matrix at C + b * stride_c (ldc); batched_gemm writes it out.
+
 Parity pins: tests/test_oracle_grouped.py (shared weights reduce to one plain
 product, per-group scaled identities in exact arithmetic, empty, negative and
-truncated counts, group permutation, pure-Python brute force on tiny inputs).
+truncated counts, group permutation, pure-Python brute force on tiny inputs;
+for the batched form: contiguous batches equal the grouped product with equal
+counts, per-batch scaled identities, brute force).
 """
 import numpy as np
 
@@ -112,3 +119,22 @@ def grouped_entries(A, B, counts, rows, N, K, lda, ldb, stride_b, I, J, fmt="bf1
         c, d = gemm_ref.gemm_entries(Ar, Bc, [0], [0], M=1, N=1, K=K, lda=K, ldb=1, fmt=fmt, lib=lib)
         C[t], D[t] = c[0], d[0]
     return C, D, ok
+
+
+def batched_gemm(A, B, batch, M, N, K, lda, ldb, stride_a, stride_b, fmt="bf16", lib=None):
+    """C_ref and D of a strided batched product, shape (batch, M, N) in fp64.
+    A and B are flat uint16 arrays holding every batch's matrix."""
+    A = np.ascontiguousarray(A).reshape(-1)
+    B = np.ascontiguousarray(B).reshape(-1)
+    C = np.zeros((batch, M, N), np.float64)
+    D = np.zeros((batch, M, N), np.float64)
+    if M == 0 or N == 0 or K == 0:
+        return C, D
+    for b in range(batch):
+        a0 = b * stride_a
+        if a0 + (M - 1) * lda + K > A.size:
+            raise ValueError("A does not hold batch %d" % b)
+        Ab = np.lib.stride_tricks.as_strided(A[a0:], shape=(M, K), strides=(lda * 2, 2))
+        Bb = np.ascontiguousarray(group_b(B, b, K, N, ldb, stride_b))
+        C[b], D[b] = gemm_ref.gemm(np.ascontiguousarray(Ab), Bb, fmt=fmt, lib=lib)
+    return C, D

@@ -126,7 +126,51 @@ def pin_brute_force(gr, seed=0):
     return all(abs(Fraction(C[i, j]) - e) <= tol * Fraction(D[i, j]) for (i, j), e in E.items())
 
 
-PINS = [pin_shared_weights, pin_scaled_identity, pin_negative_and_truncated, pin_permutation, pin_brute_force]
+def pin_batched_is_grouped_with_equal_counts(gr):
+    """Contiguous batches (stride_a = M * lda) are the grouped product with
+    every count equal to M."""
+    batch, M, N, K = 5, 13, 11, 17
+    lda, ldb = K + 2, N + 1
+    A = gen.uniform_bf16(batch * M, lda, 101).reshape(-1)
+    mats = [gen.uniform_bf16(K, ldb, 102 + b) for b in range(batch)]
+    B = _flat_b(mats, K * ldb + 4)
+    C, D = gr.batched_gemm(A, B, batch, M, N, K, lda, ldb, M * lda, K * ldb + 4)
+    Cg, Dg, cov = gr.grouped_gemm(A, B, [M] * batch, batch * M, N, K, lda, ldb, K * ldb + 4)
+    return cov.all() and np.array_equal(C.reshape(batch * M, N), Cg) and np.array_equal(D.reshape(batch * M, N), Dg)
+
+
+def pin_batched_scaled_identity(gr):
+    """B_b = (b + 1) * I with gaps between the A matrices: exact closed form."""
+    batch, M, K = 4, 6, 10
+    stride_a = M * K + 7
+    A = np.zeros(stride_a * batch, np.uint16)
+    a_vals = []
+    for b in range(batch):
+        Ab = gen.operands(M, K, K, seed=110 + b, dist="int")[0]
+        A[b * stride_a:b * stride_a + M * K] = Ab.reshape(-1)
+        a_vals.append(gemm_ref.decode(Ab))
+    mats = [gen.bf16_bits((b + 1) * np.eye(K, dtype=np.float32)) for b in range(batch)]
+    C, D = gr.batched_gemm(A, _flat_b(mats, K * K), batch, M, K, K, K, K, stride_a, K * K)
+    return all(np.array_equal(C[b], (b + 1) * a_vals[b]) and np.array_equal(D[b], (b + 1) * np.abs(a_vals[b]))
+               for b in range(batch))
+
+
+def pin_batched_brute_force(gr):
+    rng = np.random.default_rng(120)
+    batch, M, N, K = 3, 3, 4, 5
+    A = gen.uniform_bf16(batch * M, K, 121)
+    mats = [gen.uniform_bf16(K, N, 122 + b) for b in range(batch)]
+    C, D = gr.batched_gemm(A.reshape(-1), _flat_b(mats, K * N), batch, M, N, K, K, N, M * K, K * N)
+    tol = Fraction(gamma(K))
+    for b in range(batch):
+        E = brute_grouped(A[b * M:(b + 1) * M], [mats[b]], [M], M)
+        if not all(abs(Fraction(C[b, i, j]) - e) <= tol * Fraction(D[b, i, j]) for (i, j), e in E.items()):
+            return False
+    return rng is not None
+
+
+PINS = [pin_shared_weights, pin_scaled_identity, pin_negative_and_truncated, pin_permutation, pin_brute_force,
+        pin_batched_is_grouped_with_equal_counts, pin_batched_scaled_identity, pin_batched_brute_force]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -167,6 +211,7 @@ MUTATIONS = [
     ("end past the capacity", "out.append((s, min(p, rows)))", "out.append((s, p))"),
     ("off-by-one start", "Ag = A[s * lda:(e - 1) * lda + K].copy()", "Ag = A[(s + 1) * lda:e * lda + K].copy()"),
     ("wrong group matrix", "off = g * stride_b\n", "off = max(g - 1, 0) * stride_b\n"),
+    ("batch ignores stride_a", "a0 = b * stride_a\n", "a0 = b * M * lda\n"),
 ]
 
 
