@@ -72,8 +72,9 @@ typedef enum {
   AC_FAMILY_SMALLK = 4,   /* K <= 16: rank-K update bound by writing C */
   AC_FAMILY_DIRECT = 5,   /* small problems: MFMA fragments straight from memory, no LDS */
   AC_FAMILY_GROUPED = 6,  /* the tile kernel over the groups of a grouped product */
-  AC_FAMILY_PERSIST = 7   /* persistent tile kernel: the next tile's first k-block is fetched
+  AC_FAMILY_PERSIST = 7,  /* persistent tile kernel: the next tile's first k-block is fetched
                              before the current tile's epilogue (K >= 8, N >= 8) */
+  AC_FAMILY_BATCHED = 8   /* the grouped kernel over a strided batch of equal shapes */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */
@@ -94,7 +95,8 @@ typedef struct {
   int32_t n_candidates; /* legal candidates the model compared */
   double predicted_s;   /* model latency of the selected configuration, seconds */
   int64_t workspace_bytes; /* fp32 partial tiles + counters needed per stream */
-  int64_t groups;       /* grouped plans: number of groups (M is the row capacity); else 0 */
+  int64_t groups;       /* grouped plans: number of groups (M is the row capacity); batched
+                           plans: batch count (M, N, K of every batch); else 0 */
 } adaptcore_plan_desc_t;
 
 /* One legal candidate of a shape (adaptcore_candidates). */
@@ -239,6 +241,39 @@ const adaptcore_plan_t* adaptcore_grouped_plan_variant(int64_t rows, int64_t gro
 adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
                                           int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
                                           int64_t ldc, void* stream);
+
+/* ---- Batched product (BatchMM) ---------------------------------------------
+ * The other batched operator the paper replaces in its end-to-end models
+ * (BatchMM, Section 6.5; operator scope, Section 7), in the strided form:
+ * for b = 0 .. batch-1,
+ *     C_b = A_b * B_b,  A_b = A + b*stride_a (M x K, lda),
+ *                        B_b = B + b*stride_b (K x N, ldb),
+ *                        C_b = C + b*stride_c (M x N, ldc),
+ * strides in elements (0 repeats one matrix for every batch). It runs on the
+ * grouped product's kernel with every group the same shape: one launch, no
+ * workspace, no device counts.
+ *
+ * Returns the cached plan for (batch, M, N, K, dtype, layouts): M, N, K in
+ * [0, 2^31), batch in [0, 2^24]. NULL on invalid or unsupported arguments. */
+const adaptcore_plan_t* adaptcore_batched_plan(int64_t batch, int64_t M, int64_t N, int64_t K, int32_t dtype,
+                                               uint32_t layouts);
+
+/* Like adaptcore_batched_plan with the configuration forced to variant_key
+ * (family AC_FAMILY_BATCHED, P_k = 1). For tests. NULL if not legal. */
+const adaptcore_plan_t* adaptcore_batched_plan_variant(int64_t batch, int64_t M, int64_t N, int64_t K,
+                                                       int32_t dtype, uint32_t layouts, uint64_t variant_key);
+
+/* Runs a batched plan asynchronously on `stream`. A, B, C device pointers
+ * (A, B 2-byte aligned, C aligned to its element size; C must not overlap A
+ * or B). Checks: lda >= K, ldb >= N, ldc >= N, all >= 1; strides in
+ * [0, 2^40); for batch > 1, stride_c >= (M-1)*ldc + N so that no two C
+ * matrices overlap (AC_ERR_INVALID_VALUE); lda or ldb >= AC_MAX_LD
+ * (AC_ERR_UNSUPPORTED); a plan of another kind: AC_ERR_INVALID_VALUE.
+ * batch, M or N equal to 0: nothing is launched. K == 0: C is set to zero.
+ * The caller guarantees that A, B and C hold every batch's matrix. */
+adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
+                                          const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
+                                          int64_t stride_c, void* stream);
 
 /* Allocates (if needed) the workspace of `stream` for plans needing up to
  * `bytes`, so that later calls, also under capture, do not allocate. */

@@ -25,10 +25,10 @@ AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
 AC_LAYOUT_ROW_ROW = 0
 (AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
- AC_FAMILY_GROUPED, AC_FAMILY_PERSIST) = range(8)
+ AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED) = range(9)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
-FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped", "persist"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped", "persist", "batched"]
 
 
 class AdaptCoreError(RuntimeError):
@@ -132,6 +132,12 @@ def lib():
         L.adaptcore_grouped_plan_variant.restype = p
         L.adaptcore_grouped_matmul.argtypes = [p, p, p, i64, p, i64, i64, p, i64, p]
         L.adaptcore_grouped_matmul.restype = i32
+        L.adaptcore_batched_plan.argtypes = [i64, i64, i64, i64, i32, u32]
+        L.adaptcore_batched_plan.restype = p
+        L.adaptcore_batched_plan_variant.argtypes = [i64, i64, i64, i64, i32, u32, u64]
+        L.adaptcore_batched_plan_variant.restype = p
+        L.adaptcore_batched_matmul.argtypes = [p, p, i64, i64, p, i64, i64, p, i64, i64, p]
+        L.adaptcore_batched_matmul.restype = i32
         L.adaptcore_reserve_workspace.argtypes = [p, i64]
         L.adaptcore_reserve_workspace.restype = i32
         L.adaptcore_plan_info.argtypes = [p, ctypes.POINTER(PlanDesc)]
@@ -223,6 +229,26 @@ def adaptcore_grouped_plan_variant(rows, groups, N, K, dtype, layouts, variant_k
 def adaptcore_grouped_matmul(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream=0):
     """Grouped product on `stream`; counts, A, B, C are device addresses."""
     return _check(lib().adaptcore_grouped_matmul(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream))
+
+
+def adaptcore_batched_plan(batch, M, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):
+    """Cached strided-batch plan handle (int)."""
+    h = lib().adaptcore_batched_plan(batch, M, N, K, dtype, layouts)
+    if not h:
+        raise AdaptCoreError(adaptcore_last_status(), last_error())
+    return h
+
+
+def adaptcore_batched_plan_variant(batch, M, N, K, dtype, layouts, variant_key):
+    h = lib().adaptcore_batched_plan_variant(batch, M, N, K, dtype, layouts, variant_key)
+    if not h:
+        raise AdaptCoreError(adaptcore_last_status(), last_error())
+    return h
+
+
+def adaptcore_batched_matmul(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, stream=0):
+    """Strided batched product on `stream`; A, B, C are device addresses."""
+    return _check(lib().adaptcore_batched_matmul(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, stream))
 
 
 def adaptcore_reserve_workspace(stream, nbytes):

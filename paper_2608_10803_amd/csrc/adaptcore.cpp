@@ -63,6 +63,8 @@ std::map<std::pair<std::tuple<int64_t, int64_t, int64_t, int, uint32_t>, uint64_
 typedef std::tuple<int64_t, int64_t, int64_t, int64_t, int, uint32_t> GroupKey;
 std::map<GroupKey, adaptcore_plan_s*> g_grouped;
 std::map<std::pair<GroupKey, uint64_t>, adaptcore_plan_s*> g_grouped_forced;
+std::map<GroupKey, adaptcore_plan_s*> g_batched;  // (M, batch, N, K, dtype, layouts)
+std::map<std::pair<GroupKey, uint64_t>, adaptcore_plan_s*> g_batched_forced;
 
 inline uint64_t mix(uint64_t x) {
   x ^= x >> 33;
@@ -307,6 +309,8 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   const ac::Plan& p = plan->p;
   if (p.family == ac::FAM_GROUPED)
     return fail(AC_ERR_INVALID_VALUE, "grouped plan: run it with adaptcore_grouped_matmul");
+  if (p.family == ac::FAM_BATCHED)
+    return fail(AC_ERR_INVALID_VALUE, "batched plan: run it with adaptcore_batched_matmul");
   const int64_t M = p.s.M, N = p.s.N, K = p.s.K;
   if (M == 0 || N == 0) return AC_OK;
   if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
@@ -463,6 +467,121 @@ adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const in
   return AC_OK;
 }
 
+const adaptcore_plan_t* adaptcore_batched_plan(int64_t batch, int64_t M, int64_t N, int64_t K, int32_t dtype,
+                                               uint32_t layouts) {
+  adaptcore_status st;
+  if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  if (batch < 0 || batch > (1LL << 24)) {
+    fail(AC_ERR_INVALID_VALUE, "batch must be in [0, 2^24]");
+    return nullptr;
+  }
+  st_lookups.fetch_add(1, std::memory_order_relaxed);
+  const GroupKey k = std::make_tuple(M, batch, N, K, (int)dtype, layouts);
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_batched.find(k);
+  if (it != g_batched.end()) {
+    st_hits.fetch_add(1, std::memory_order_relaxed);
+    return it->second;
+  }
+  const auto t0 = std::chrono::steady_clock::now();
+  ac::Plan p;
+  const ac::Shape s{M, N, K, dtype, layouts};
+  if (!ac::plan_batched(s, batch, g_hw, &p)) {
+    fail(AC_ERR_UNSUPPORTED, "no batched configuration fits (launch grid too large)");
+    return nullptr;
+  }
+  bool exact;
+  p.shape_key = ac::shape_key(s, &exact);
+  auto* pp = new adaptcore_plan_s{p};
+  g_owned.push_back(pp);
+  g_batched[k] = pp;
+  st_miss_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  st_misses.fetch_add(1, std::memory_order_relaxed);
+  st_entries.fetch_add(1, std::memory_order_relaxed);
+  return pp;
+}
+
+const adaptcore_plan_t* adaptcore_batched_plan_variant(int64_t batch, int64_t M, int64_t N, int64_t K,
+                                                       int32_t dtype, uint32_t layouts, uint64_t variant_key) {
+  adaptcore_status st;
+  if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  if (batch < 0 || batch > (1LL << 24)) {
+    fail(AC_ERR_INVALID_VALUE, "batch must be in [0, 2^24]");
+    return nullptr;
+  }
+  const GroupKey k = std::make_tuple(M, batch, N, K, (int)dtype, layouts);
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_batched_forced.find(std::make_pair(k, variant_key));
+  if (it != g_batched_forced.end()) return it->second;
+  ac::Plan p;
+  const ac::Shape s{M, N, K, dtype, layouts};
+  if (!ac::batched_for_key(s, batch, g_hw, variant_key, &p)) {
+    fail(AC_ERR_INVALID_VALUE, "variant key is not a legal batched configuration");
+    return nullptr;
+  }
+  bool exact;
+  p.shape_key = ac::shape_key(s, &exact);
+  auto* pp = new adaptcore_plan_s{p};
+  g_owned.push_back(pp);
+  g_batched_forced[std::make_pair(k, variant_key)] = pp;
+  return pp;
+}
+
+adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
+                                          const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
+                                          int64_t stride_c, void* stream) {
+  if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
+  const ac::Plan& p = plan->p;
+  if (p.family != ac::FAM_BATCHED)
+    return fail(AC_ERR_INVALID_VALUE, "not a batched plan (adaptcore_batched_plan)");
+  const int64_t M = p.s.M, N = p.s.N, K = p.s.K, batch = p.groups;
+  if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
+    return fail(AC_ERR_INVALID_VALUE, "leading dimension smaller than the row length");
+  const int64_t lim = 1LL << 40;
+  if (stride_a < 0 || stride_b < 0 || stride_c < 0 || stride_a >= lim || stride_b >= lim || stride_c >= lim)
+    return fail(AC_ERR_INVALID_VALUE, "batch strides must be in [0, 2^40)");
+  if (batch > 1 && M > 0 && N > 0 && stride_c < (M - 1) * ldc + N)
+    return fail(AC_ERR_INVALID_VALUE, "the C matrices of two batches overlap (stride_c too small)");
+  if (lda >= AC_MAX_LD || ldb >= AC_MAX_LD)
+    return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
+  if (batch == 0 || M == 0 || N == 0 || p.grid_x == 0) return AC_OK;
+  if (!C || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null matrix pointer");
+  const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
+  if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)))
+    return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
+  adaptcore_status st = ensure_init();
+  if (st != AC_OK) return st;
+
+  ac::GroupArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.g.A = static_cast<const uint16_t*>(A);
+  a.g.B = static_cast<const uint16_t*>(B);
+  a.g.C = C;
+  a.g.M = M;
+  a.g.N = N;
+  a.g.K = K;
+  a.g.lda = lda;
+  a.g.ldb = ldb;
+  a.g.ldc = ldc;
+  a.g.pk = 1;
+  a.g.kper = p.kper;
+  a.g.tiles_m = p.pm;
+  a.g.tiles_n = p.pn;
+  a.g.swizzle = p.swizzle;
+  a.counts = nullptr;
+  a.rows = M;
+  a.stride_a = stride_a;
+  a.stride_b = stride_b;
+  a.stride_c = stride_c;
+  a.groups = (int)batch;
+  a.slots = p.pm;
+  a.tiles_per_group = (int)((M + p.tile_m - 1) / p.tile_m);
+  const hipError_t e = ac::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  st_launches.fetch_add(1, std::memory_order_relaxed);
+  return AC_OK;
+}
+
 adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out) {
   if (!plan || !out) return fail(AC_ERR_INVALID_VALUE, "null argument");
   const ac::Plan& p = plan->p;
@@ -577,6 +696,8 @@ adaptcore_status adaptcore_cache_clear(void) {
   g_forced.clear();
   g_grouped.clear();
   g_grouped_forced.clear();
+  g_batched.clear();
+  g_batched_forced.clear();
   st_entries.store(0);
   return AC_OK;
 }

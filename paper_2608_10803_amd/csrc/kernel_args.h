@@ -15,7 +15,8 @@ enum Family : int {
   FAM_DIRECT = 5,    // small problems: MFMA fragments loaded straight from memory
   FAM_GROUPED = 6,   // the tile kernel over the groups of a grouped product
   FAM_PERSIST = 7,   // persistent tile kernel, next tile's first block fetched before the epilogue
-  FAM_COUNT = 8
+  FAM_BATCHED = 8,   // the grouped kernel over a strided batch (every group the same shape)
+  FAM_COUNT = 9
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N
@@ -40,17 +41,22 @@ struct GemmArgs {
   int grid;          // stream-K: persistent workgroups
 };
 
-// Arguments of the grouped kernel. Group g owns rows [min(P_{g-1}, rows),
-// min(P_g, rows)) of A and C (P: running sum of max(counts, 0)) and
-// multiplies them by the K x N matrix at B + g * stride_b. g.M is unused;
-// g.tiles_n is the tile count along N.
+// Arguments of the grouped kernel. With counts: group g owns rows
+// [min(P_{g-1}, rows), min(P_g, rows)) of A and C (P: running sum of
+// max(counts, 0)). Without counts (a strided batch): every group has `rows`
+// rows, its A at A + g * stride_a and its C at C + g * stride_c. Either way
+// group g multiplies its rows by the K x N matrix at B + g * stride_b. g.M is
+// unused; g.tiles_n is the tile count along N.
 struct GroupArgs {
   GemmArgs g;
-  const int32_t* counts;  // device, `groups` entries
-  int64_t rows;           // rows of A and C (capacity)
+  const int32_t* counts;  // device, `groups` entries; null = strided batch
+  int64_t rows;           // rows of A and C (capacity), or rows of every batch
+  int64_t stride_a;       // strided batch: elements between two A matrices (else 0)
   int64_t stride_b;       // elements between the B matrices of two groups
+  int64_t stride_c;       // strided batch: elements between two C matrices (else 0)
   int groups;
   int slots;              // row-tile slots launched (an upper bound of the tiles along M)
+  int tiles_per_group;    // strided batch: row tiles of every group
 };
 
 }  // namespace ac

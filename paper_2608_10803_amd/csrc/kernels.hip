@@ -892,20 +892,32 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
 
   const int tiles_n = a.g.tiles_n;
-  GroupChunk<BM> first;
-  first.load(a, 0, 0);
   int t = blockIdx.x;
-  if (a.g.swizzle) {
-    // XCD-aware order over the tiles that exist: each XCD takes a contiguous
-    // range of (row tile, column tile) ids, the surplus blocks leave
-    const int n = group_tiles_total<BM>(a, first) * tiles_n;
-    if (t >= n) return;
-    t = xcd_remap(t, n);
-  }
-  const int slot = t / tiles_n, tn = t - slot * tiles_n;
-  int grp = 0, tm = 0;
+  int grp = 0, tm = 0, tn = 0;
   int64_t row0 = 0, rows_g = 0;
-  if (!group_of_slot<BM>(a, first, slot, grp, row0, rows_g, tm)) return;
+  if (a.counts == nullptr) {
+    // strided batch: the grid is exactly groups x row tiles x column tiles
+    if (a.g.swizzle) t = xcd_remap(t, (int)gridDim.x);
+    const int slot = t / tiles_n;
+    tn = t - slot * tiles_n;
+    grp = slot / a.tiles_per_group;
+    tm = slot - grp * a.tiles_per_group;
+    rows_g = a.rows;
+  } else {
+    GroupChunk<BM> first;
+    first.load(a, 0, 0);
+    if (a.g.swizzle) {
+      // XCD-aware order over the tiles that exist: each XCD takes a
+      // contiguous range of (row tile, column tile) ids, the surplus blocks
+      // leave
+      const int n = group_tiles_total<BM>(a, first) * tiles_n;
+      if (t >= n) return;
+      t = xcd_remap(t, n);
+    }
+    const int slot = t / tiles_n;
+    tn = t - slot * tiles_n;
+    if (!group_of_slot<BM>(a, first, slot, grp, row0, rows_g, tm)) return;
+  }
   // the same values in every lane: keep them scalar for the address bases
   grp = __builtin_amdgcn_readfirstlane(grp);
   tm = __builtin_amdgcn_readfirstlane(tm);
@@ -913,9 +925,9 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a
   rows_g = uniform64(rows_g);
 
   GemmArgs g = a.g;
-  g.A += row0 * g.lda;
+  g.A += row0 * g.lda + (int64_t)grp * a.stride_a;
   g.B += (int64_t)grp * a.stride_b;
-  g.C = static_cast<char*>(g.C) + row0 * g.ldc * (OUT == OUT_BF16 ? 2 : 4);
+  g.C = static_cast<char*>(g.C) + (row0 * g.ldc + (int64_t)grp * a.stride_c) * (OUT == OUT_BF16 ? 2 : 4);
   g.M = rows_g;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int kt_total = (int)((g.K + S::BK - 1) / S::BK);
@@ -1894,7 +1906,8 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
 }
 
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st) {
-  if (p.family != FAM_GROUPED || p.cfg < 0 || p.cfg >= N_TILE_CFG || !kGroupedFns[p.cfg])
+  if ((p.family != FAM_GROUPED && p.family != FAM_BATCHED) || p.cfg < 0 || p.cfg >= N_TILE_CFG ||
+      !kGroupedFns[p.cfg])
     return hipErrorInvalidValue;
   return kGroupedFns[p.cfg](p, a, st, p.s.dtype == AC_BF16_BF16OUT);
 }

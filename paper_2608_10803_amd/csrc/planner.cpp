@@ -26,6 +26,7 @@ int table_occ(int family, int cfg) {
     case FAM_STREAMK:
     case FAM_GROUPED:
     case FAM_PERSIST:
+    case FAM_BATCHED:
       return kTileCfg[cfg].occ;
     case FAM_SKINNY_M:
       return kSkinnyMCfg[cfg].occ;
@@ -799,6 +800,51 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
   return true;
 }
 
+// The grouped kernel over a strided batch: every group has the shape s, so
+// the grid is exact (batch x row tiles x column tiles) and the model prices
+// `batch` independent products of shape s sharing the GPU.
+bool build_batched(const Shape& s, int64_t batch, const adaptcore_hw_t& hw, int cfg, int swizzle, Plan* p) {
+  if (cfg < 0 || cfg >= N_TILE_CFG || !kGroupedCfg[cfg]) return false;
+  const TileCfg& t = kTileCfg[cfg];
+  if (tile_lds_bytes(t) > hw.lds_bytes) return false;
+  const int64_t tpg = cdiv(s.M, t.bm), tn = cdiv(s.N, t.bn);
+  const int64_t slots = batch * tpg;
+  const int64_t threads = t.bm == 256 ? 512 : 256;
+  if (slots * tn > (1LL << 31) - 1 || slots * tn * threads >= (1LL << 32)) return false;
+  p->s = s;
+  p->groups = batch;
+  p->family = FAM_BATCHED;
+  p->cfg = cfg;
+  p->swizzle = swizzle;
+  p->tile_m = t.bm;
+  p->tile_n = t.bn;
+  p->tile_k = TILE_BK;
+  p->pm = (int)slots;
+  p->pn = (int)tn;
+  p->pk = 1;
+  p->kper = (int)cdiv(s.K, TILE_BK);
+  p->grid_x = (int)(slots * tn);
+  p->grid_y = 1;
+  p->n_launch = p->grid_x > 0 ? 1 : 0;
+  p->ws_bytes = 0;
+  p->variant_key = make_variant_key(FAM_BATCHED, cfg, swizzle, 1, s.dtype, (int)s.layouts);
+  if (p->grid_x == 0) {
+    p->predicted = 0;
+    return true;
+  }
+  const double compulsory = 2.0 * s.M * s.K + 2.0 * s.K * s.N;
+  const bool unaligned = (s.K % 8) != 0 || (s.N % 8) != 0;
+  const Ctx c{s, hw, compulsory, out_bytes(s.dtype), unaligned};
+  Plan one;
+  Work w;
+  if (!build_tile(c, cfg, 1, swizzle, &one, &w)) return false;
+  w.units *= batch;
+  w.total_read *= (double)batch;
+  w.total_write *= (double)batch;
+  p->predicted = model_time(s, w, hw, compulsory * (double)batch);
+  return true;
+}
+
 bool plan_grouped(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, Plan* out) {
   bool found = false;
   int n = 0;
@@ -825,6 +871,39 @@ bool grouped_for_key(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, u
     return false;
   Plan p;
   if (!build_grouped(s, groups, hw, vk_cfg(key), vk_swizzle(key), &p) || p.variant_key != key) return false;
+  int base = 0;
+  p.n_candidates = 1;
+  p.cls = classify_shape(s, hw, &base);
+  *out = p;
+  return true;
+}
+
+bool plan_batched(const Shape& s, int64_t batch, const adaptcore_hw_t& hw, Plan* out) {
+  bool found = false;
+  int n = 0;
+  for (int cfg = 0; cfg < N_TILE_CFG; ++cfg) {
+    Plan p;
+    if (!build_batched(s, batch, hw, cfg, 1, &p)) continue;
+    ++n;
+    if (!found || p.predicted < out->predicted) {
+      *out = p;
+      found = true;
+    }
+  }
+  if (found) {
+    int base = 0;
+    out->n_candidates = n;
+    out->cls = classify_shape(s, hw, &base);
+  }
+  return found;
+}
+
+bool batched_for_key(const Shape& s, int64_t batch, const adaptcore_hw_t& hw, uint64_t key, Plan* out) {
+  if (vk_family(key) != FAM_BATCHED || vk_pk(key) != 1 || vk_dtype(key) != s.dtype ||
+      vk_layouts(key) != (int)s.layouts)
+    return false;
+  Plan p;
+  if (!build_batched(s, batch, hw, vk_cfg(key), vk_swizzle(key), &p) || p.variant_key != key) return false;
   int base = 0;
   p.n_candidates = 1;
   p.cls = classify_shape(s, hw, &base);
@@ -873,7 +952,8 @@ std::string kernel_names(const Plan& p) {
       std::snprintf(buf, sizeof buf, "k_tile_pp<%d, %d, %d, %s>", t.bm, t.bn, t.ms, b);
       return buf;
     }
-    case FAM_GROUPED: {
+    case FAM_GROUPED:
+    case FAM_BATCHED: {
       const TileCfg& t = kTileCfg[p.cfg];
       std::snprintf(buf, sizeof buf, "k_grouped<%d, %d, %d, %d, %d>", t.bm, t.bn, t.ms, obf, t.depth);
       return buf;
@@ -904,6 +984,7 @@ int config_index(int family, int cfg) {
       return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
     case FAM_PERSIST:
       return cfg >= 0 && cfg < N_TILE_CFG && kPersistCfg[cfg] ? IDX_PERSIST + cfg : -1;
+    case FAM_BATCHED:
     case FAM_GROUPED:  // the tile kernel's costs
       return cfg >= 0 && cfg < N_TILE_CFG && kGroupedCfg[cfg] ? IDX_TILE + cfg : -1;
   }

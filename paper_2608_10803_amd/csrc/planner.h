@@ -36,7 +36,8 @@ struct Plan {
   int64_t ws_bytes = 0;  // fp32 partials
   int n_candidates = 0;
   double predicted = 0;
-  int64_t groups = 0;    // grouped product: groups (s.M is then the row capacity)
+  int64_t groups = 0;    // grouped product: groups (s.M is then the row capacity);
+                         // strided batch: batch count (s is every batch's shape)
 };
 
 struct Candidate {
@@ -69,6 +70,10 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
 // one configuration forced by its key (grouped_for_key).
 bool plan_grouped(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, Plan* out);
 bool grouped_for_key(const Shape& s, int64_t groups, const adaptcore_hw_t& hw, uint64_t key, Plan* out);
+
+// Strided batch of `batch` products of shape s on the grouped kernel.
+bool plan_batched(const Shape& s, int64_t batch, const adaptcore_hw_t& hw, Plan* out);
+bool batched_for_key(const Shape& s, int64_t batch, const adaptcore_hw_t& hw, uint64_t key, Plan* out);
 
 // 64-bit shape key: M | N << 17 | K << 34 | dtype << 51 | layouts << 55, for
 // dimensions below 2^17; larger shapes set bit 63 and hash all fields.

@@ -7,7 +7,7 @@
 
 namespace ac {
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
-// Launch of a grouped plan (family FAM_GROUPED).
+// Launch of a grouped or batched plan (families FAM_GROUPED, FAM_BATCHED).
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 // Reads the device's occupancy of every kernel into the planner.
 void query_occupancy();

@@ -237,3 +237,114 @@ def test_moe_stream_full_size(reading):
             assert err <= tol(BF16), "moe %s step %d %s err %.3g" % (reading, step, (N, K), err)
             # every covered row was written (no NaN left from the fill)
             assert not t.isnan(C[:int(np.clip(counts, 0, None).sum())]).any().item()
+
+
+# ---- strided batch (BatchMM)
+
+
+def batched_case(batch, M, N, K, lda, ldb, ldc, stride_a, stride_b, stride_c, seed):
+    """Flat host operands of a strided batch (gaps between matrices stay 0)."""
+    A = np.zeros(max((batch - 1) * stride_a + (M - 1) * lda + K, 1) + 8, np.uint16)
+    B = np.zeros(max((batch - 1) * stride_b + (K - 1) * ldb + N, 1) + 8, np.uint16)
+    for b in range(batch):
+        if M and K:
+            np.lib.stride_tricks.as_strided(A[b * stride_a:], shape=(M, K), strides=(lda * 2, 2))[...] = \
+                gen.uniform_bf16(M, K, seed + 2 * b)
+        if K and N and (stride_b or b == 0):
+            np.lib.stride_tricks.as_strided(B[b * stride_b:], shape=(K, N), strides=(ldb * 2, 2))[...] = \
+                gen.uniform_bf16(K, N, seed + 2 * b + 1)
+    return A, B
+
+
+def run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, stride_a, stride_b, stride_c, dtype):
+    """One adaptcore_batched_matmul; returns (values (batch, M, N), every
+    element outside the C matrices still holds its canary)."""
+    t = torch()
+    n = (batch - 1) * stride_c + (M - 1) * ldc + N + 2 * ldc
+    if dtype == F32:
+        host = np.full(n, F32_CANARY, np.float32)
+        dev = t.from_numpy(host.copy()).to("cuda")
+        addr = dev.data_ptr() + 4 * ldc
+    else:
+        host = np.full(n, BF16_CANARY, np.uint16)
+        dev = t.from_numpy(host.view(np.int16).copy()).to("cuda")
+        addr = dev.data_ptr() + 2 * ldc
+    Ad = t.from_numpy(A.view(np.int16)).to("cuda")
+    Bd = t.from_numpy(B.view(np.int16)).to("cuda")
+    ac.adaptcore_batched_matmul(plan, Ad.data_ptr(), lda, stride_a, Bd.data_ptr(), ldb, stride_b, addr, ldc, stride_c, 0)
+    t.cuda.synchronize()
+    raw = dev.cpu().numpy()
+    raw = raw if dtype == F32 else raw.view(np.uint16)
+    inside = np.zeros(n, bool)
+    vals = np.zeros((batch, M, N))
+    for b in range(batch):
+        for i in range(M):
+            o = ldc + b * stride_c + i * ldc
+            inside[o:o + N] = True
+            row = raw[o:o + N]
+            vals[b, i] = row.astype(np.float64) if dtype == F32 else gemm_ref.decode(np.ascontiguousarray(row))
+    canary = F32_CANARY if dtype == F32 else BF16_CANARY
+    return vals, bool(np.all(raw[~inside] == canary))
+
+
+def batched_keys(batch, M, N, K, dtype):
+    keys = []
+    for cfg in range(16):
+        for sw in (0, 1):
+            key = ac.AC_FAMILY_BATCHED | (cfg << 4) | (sw << 12) | (1 << 16) | (dtype << 48)
+            try:
+                ac.adaptcore_batched_plan_variant(batch, M, N, K, dtype, 0, key)
+            except ac.AdaptCoreError:
+                continue
+            keys.append(key)
+    return keys
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+def test_every_batched_configuration(dtype):
+    """Five batches of 70 x 300 x 197 with padded leading dimensions and gaps
+    between the matrices (which must keep their canaries)."""
+    batch, M, N, K = 5, 70, 300, 197
+    lda, ldb, ldc = K + 3, N + 5, N + 7
+    sa, sb, sc = M * lda + 11, K * ldb + 13, M * ldc + 17
+    A, B = batched_case(batch, M, N, K, lda, ldb, ldc, sa, sb, sc, seed=31)
+    C_ref, D = grouped_ref.batched_gemm(A, B, batch, M, N, K, lda, ldb, sa, sb)
+    keys = batched_keys(batch, M, N, K, dtype)
+    assert len(keys) >= 10
+    for key in keys:
+        plan = ac.adaptcore_batched_plan_variant(batch, M, N, K, dtype, 0, key)
+        note("batched", hex(key), ac.adaptcore_plan_kernels(plan))
+        vals, ok = run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, sa, sb, sc, dtype)
+        assert ok, "write outside the C matrices %s" % hex(key)
+        err = gemm_ref.err_metric(vals.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N))
+        assert err <= tol(dtype), "err %.3g %s" % (err, hex(key))
+
+
+@pytest.mark.parametrize("case", [
+    (1, 300, 200, 100, False),     # one batch: a plain product
+    (64, 32, 32, 32, False),       # many small matrices
+    (12, 17, 5, 3, False),         # N < 8 and K < 8
+    (9, 100, 64, 48, True),        # shared B (stride_b = 0)
+    (4, 256, 256, 256, False),     # whole tiles
+], ids=lambda c: "b%d_%dx%dx%d%s" % (c[0], c[1], c[2], c[3], "_sharedB" if c[4] else ""))
+def test_batched_default_plans(case):
+    batch, M, N, K, shared = case
+    lda, ldb, ldc = K, N, N
+    sa, sb, sc = M * K, (0 if shared else K * N), M * N
+    A, B = batched_case(batch, M, N, K, lda, ldb, ldc, sa, sb, sc, seed=batch + M)
+    C_ref, D = grouped_ref.batched_gemm(A, B, batch, M, N, K, lda, ldb, sa, sb)
+    for dtype in (F32, BF16):
+        plan = ac.adaptcore_batched_plan(batch, M, N, K, dtype)
+        vals, ok = run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, sa, sb, sc, dtype)
+        assert ok
+        err = gemm_ref.err_metric(vals.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N))
+        assert err <= tol(dtype), (case, dtype, err)
+
+
+def test_batched_k_zero():
+    batch, M, N = 3, 20, 24
+    A = np.zeros(8, np.uint16)
+    B = np.zeros(8, np.uint16)
+    plan = ac.adaptcore_batched_plan(batch, M, N, 0, F32)
+    vals, ok = run_batched(plan, A, B, batch, M, N, 0, 1, N, N, 0, 0, M * N + 5, F32)
+    assert ok and not vals.any()

@@ -123,3 +123,64 @@ def test_argument_validation():
               ac.adaptcore_grouped_plan(64, 4, 0, 16)]:
         ac.adaptcore_grouped_matmul(h, *good)
     assert good  # the good tuple is only launched on a GPU (tests/test_gpu_grouped.py)
+
+
+# ---- strided batch (BatchMM) on the grouped kernel
+
+
+def test_batched_plan_fields_and_cache():
+    h = ac.adaptcore_batched_plan(64, 130, 300, 197)
+    assert h == ac.adaptcore_batched_plan(64, 130, 300, 197)
+    d = ac.adaptcore_plan_info(h)
+    assert d["family_name"] == "batched" and d["groups"] == 64 and (d["M"], d["N"], d["K"]) == (130, 300, 197)
+    tpg = -(-130 // d["tile_m"])
+    assert d["pm"] == 64 * tpg and d["pn"] == -(-300 // d["tile_n"]) and d["grid_x"] == d["pm"] * d["pn"]
+    assert ac.adaptcore_plan_kernels(h)[0].startswith("k_grouped<")
+    # distinct from the grouped plan of the same numbers
+    assert h != ac.adaptcore_grouped_plan(130, 64, 300, 197)
+    for cfg in range(16):
+        key = ac.AC_FAMILY_BATCHED | (cfg << 4) | (1 << 12) | (1 << 16) | (ac.AC_BF16_BF16OUT << 48)
+        try:
+            hv = ac.adaptcore_batched_plan_variant(64, 130, 300, 197, ac.AC_BF16_BF16OUT, 0, key)
+        except ac.AdaptCoreError:
+            continue
+        assert ac.adaptcore_plan_info(hv)["variant_key"] == key
+
+
+def test_batched_argument_validation():
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_batched_plan(-1, 4, 4, 4)
+    with pytest.raises(ac.AdaptCoreError):
+        ac.adaptcore_batched_plan((1 << 24) + 1, 4, 4, 4)
+    hb = ac.adaptcore_batched_plan(3, 16, 32, 8)
+    hg = ac.adaptcore_grouped_plan(48, 3, 32, 8)
+    hp = ac.adaptcore_plan(16, 32, 8)
+    ok = (0x1000, 8, 128, 0x2000, 32, 256, 0x3000, 32, 512)
+    # every kind of plan only runs through its own entry point
+    for h in (hg, hp):
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_batched_matmul(h, *ok)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    for f, args in [(ac.adaptcore_matmul, (0x1000, 8, 0x2000, 32, 0x3000, 32)),
+                    (ac.adaptcore_grouped_matmul, (0x4000, 0x1000, 8, 0x2000, 32, 256, 0x3000, 32))]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            f(hb, *args)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    bad = [
+        (0x1000, 7, 128, 0x2000, 32, 256, 0x3000, 32, 512),     # lda < K
+        (0x1000, 8, -1, 0x2000, 32, 256, 0x3000, 32, 512),      # negative stride
+        (0x1000, 8, 128, 0x2000, 32, 256, 0x3000, 32, 1 << 40),
+        (0x1000, 8, 128, 0x2000, 32, 256, 0x3000, 32, 15 * 32 + 31),  # C matrices overlap
+        (0x1000, 8, 128, 0x2000, 32, 256, 0x3001, 32, 512),     # misaligned C (bf16: 2 bytes)
+        (0x1000, 8, 128, 0x2000, 32, 256, 0, 32, 512),          # null C
+    ]
+    for args in bad:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_batched_matmul(hb, *args)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE, args
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_batched_matmul(hb, 0x1000, 1 << 23, 128, 0x2000, 32, 256, 0x3000, 32, 512)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    # the smallest stride that keeps the C matrices apart is accepted before any GPU work is needed
+    for h in (ac.adaptcore_batched_plan(0, 16, 32, 8), ac.adaptcore_batched_plan(3, 0, 32, 8)):
+        ac.adaptcore_batched_matmul(h, 0x1000, 8, 128, 0x2000, 32, 256, 0x3000, 32, 15 * 32 + 32)
