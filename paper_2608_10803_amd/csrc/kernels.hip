@@ -702,13 +702,88 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
 }
 
 // ------------------------------------------------- persistent tile kernel
+// Epilogues of the persistent kernel. Every thread issues the same, fixed
+// number of 16-byte stores through a buffer resource whose range ends at the
+// tile's last element of C; a lane whose 16 bytes lie outside C stores at an
+// offset past that range, which the hardware drops. With a fixed count the
+// compiler knows how many stores follow the next tile's prefetched loads, so
+// waiting for those loads does not wait for the stores (vector memory
+// operations complete in issue order). Only a last, partial group of columns
+// (N not a multiple of 8) adds element stores. Requires the tile's span of C
+// below 2^31 bytes (the launcher checks ldc). bf16 output only; fp32 output
+// keeps the conditional register-to-memory stores.
+constexpr int32_t OOB_OFF = (int32_t)0x80000000u;  // past every tile's range
+constexpr uint32_t RSRC_WORD3 = 0x00020000u;      // raw buffer, 32-bit data
+
+template <int BM, int BN, int MS>
+__device__ __forceinline__ void store_acc_bf16_fixed(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
+                                                                                   [TileShape<BM, BN, MS>::TN],
+                                                     const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
+  typedef TileShape<BM, BN, MS> S;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave / S::WC, wc = wave % S::WC;
+  uint16_t* ct = reinterpret_cast<uint16_t*>(smem);
+  __syncthreads();  // the main loop's last reads of the LDS stages are done
+#pragma unroll
+  for (int i = 0; i < S::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < S::TN; ++j) {
+      uint16_t* base = ct + (wr * S::WTM + i * MS + (lane % MS)) * S::CT_LD + wc * S::WTN + j * MS;
+#pragma unroll
+      for (int q = 0; q < S::NA / 4; ++q) {
+        const uint32_t lo = (uint32_t)to_bf16(acc[i][j][4 * q]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 3]) << 16);
+        *reinterpret_cast<uint64_t*>(base + acc_col<MS>(4 * q, lane)) = (uint64_t)lo | ((uint64_t)hi << 32);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  __syncthreads();
+  constexpr int GPR = BN / 8;  // 16-byte groups per tile row
+  constexpr int ITER = BM * GPR / S::NT;
+  static_assert(BM * GPR % S::NT == 0, "whole store rounds");
+  const int rows = (int)min(g.M - m0, (int64_t)BM), cols = (int)min(g.N - n0, (int64_t)BN);
+  // the row pitch is made opaque here so that the per-store offsets are
+  // computed in the epilogue, not hoisted out of the tile loop (where they
+  // would stay live through the main loop)
+  int32_t ldc2 = (int32_t)(g.ldc * 2);
+  asm volatile("" : "+s"(ldc2));
+  uint16_t* cbase = static_cast<uint16_t*>(g.C) + m0 * g.ldc + n0;
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(cbase, (short)0, (rows - 1) * ldc2 + cols * 2, (int)RSRC_WORD3);
+  // in batches of at most 8 stores (bounded live registers)
+  constexpr int BATCH = ITER < 8 ? ITER : 8;
+  static_assert(ITER % BATCH == 0, "whole batches");
+#pragma unroll
+  for (int i0 = 0; i0 < ITER; i0 += BATCH) {
+    u32x4 v[BATCH];
+    int32_t off[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int e = tid + (i0 + u) * S::NT, row = e / GPR, grp = e % GPR;
+      const uint16_t* src = ct + row * S::CT_LD + grp * 8;  // 8-byte aligned
+      const uint64_t a = *reinterpret_cast<const uint64_t*>(src);
+      const uint64_t b = *reinterpret_cast<const uint64_t*>(src + 4);
+      v[u] = u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)};
+      const bool ok = row < rows && grp * 8 + 8 <= cols;
+      off[u] = ok ? row * ldc2 + grp * 16 : OOB_OFF;
+    }
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) __builtin_amdgcn_raw_buffer_store_b128(v[u], rs, off[u], 0, 0);
+  }
+  if ((cols & 7) != 0) {  // a partial last group of columns (uniform)
+    const int c0 = cols & ~7;
+    for (int r = tid; r < rows; r += S::NT)
+      for (int j = c0; j < cols; ++j) cbase[(int64_t)r * g.ldc + j] = ct[r * S::CT_LD + j];
+  }
+}
+
 // A grid of at most (CUs x workgroups per CU) walks the tiles in strides of
 // the grid. The first k-block of a workgroup's next tile is loaded into
 // registers right after the last k-block of the current tile went to LDS,
-// i.e. before the current tile's last MFMAs and its epilogue: that load's
-// memory latency is hidden behind the stores of C. Loads issued before the
-// stores do not wait for them (vector memory operations complete in issue
-// order). Requires K >= 8 and N >= 8 (the planner offers it only then).
+// i.e. before the current tile's last MFMAs and its epilogue, and goes to LDS
+// at the end of the iteration: its memory latency is spent under the stores
+// of C. Requires K >= 8 and N >= 8 (the planner offers it only then) and a
+// row pitch of C below 2^23 bytes (the launcher checks it).
 template <int BM, int BN, int MS, bool OBF>
 __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g) {
   typedef TileShape<BM, BN, MS> S;
@@ -766,15 +841,16 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g)
   o.init(g, m0, n0);
   Stage<BM, BN, MS> st;
   st.load(g, o, m0, n0, 0);
+  bool n_edge = n0 + BN > g.N;
+  st.store(sA0, sB0, n_edge || (k_tail && kt_total == 1), o.b_cs);
+  __syncthreads();
   for (;;) {
+    // block 0 of tile t is in LDS stage 0
     Acc acc[S::TM][S::TN];
 #pragma unroll
     for (int i = 0; i < S::TM; ++i)
 #pragma unroll
       for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
-    const bool n_edge = n0 + BN > g.N;
-    st.store(sA0, sB0, n_edge || (k_tail && kt_total == 1), o.b_cs);
-    __syncthreads();
     int kt = 0;
     for (; kt + 1 < kt_total; ++kt) {
       const bool odd = (kt & 1) != 0;
@@ -784,20 +860,31 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g)
       __syncthreads();
     }
     // the last block of this tile is in LDS: fetch the next tile's first
-    // block now, then finish this tile
-    const int tn_next = t + (int)gridDim.x;
+    // block now, finish this tile, then move the block to LDS
+    const int t_next = t + (int)gridDim.x;
+    const bool more = t_next < ntiles;
     int64_t m1 = 0, n1 = 0;
-    if (tn_next < ntiles) {
-      coords(tn_next, m1, n1);
+    if (more) {
+      coords(t_next, m1, n1);
       o.init(g, m1, n1);
       st.load(g, o, m1, n1, 0);
     }
     const bool odd = (kt & 1) != 0;
     compute(odd ? sA1 : sA0, odd ? sB1 : sB0, acc);
-    store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
-    if (tn_next >= ntiles) break;
-    __syncthreads();  // every wave is done with LDS before the next stage is written
-    t = tn_next;
+    // The fixed-count epilogue for bf16 output; fp32 output and the 256 x 256
+    // tile keep the conditional stores (their fixed-count forms keep more
+    // registers live than those tiles afford: spills, whose reloads wait for
+    // every memory operation, cost more than the overlap gains).
+    if constexpr (OBF && !(BM == 256 && BN == 256))
+      store_acc_bf16_fixed<BM, BN, MS>(acc, g, m0, n0, smem);
+    else
+      store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
+    if (!more) break;
+    __syncthreads();  // every wave is done with LDS (last MFMAs, epilogue reads)
+    n_edge = n1 + BN > g.N;
+    st.store(sA0, sB0, n_edge || (k_tail && kt_total == 1), o.b_cs);
+    __syncthreads();
+    t = t_next;
     m0 = m1;
     n0 = n1;
   }
@@ -1705,6 +1792,16 @@ hipError_t launch_direct(const Plan& p, const GemmArgs& g, hipStream_t st, bool 
 
 template <int BM, int BN, int MS>
 hipError_t launch_persist(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
+  // the buffer-store epilogue addresses a tile of C with 31-bit offsets
+  if (g.ldc * (obf ? 2 : 4) >= (1LL << 23)) {
+    static_assert(kTileCfg[0].depth == 1, "the persistent kernels are the depth-1 tile kernels");
+    const dim3 grid(p.pm * p.pn), block(TileShape<BM, BN, MS>::NT);
+    if (obf)
+      hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_BF16, 1>), grid, block, 0, st, g);
+    else
+      hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_F32, 1>), grid, block, 0, st, g);
+    return hipGetLastError();
+  }
   const dim3 grid(p.grid_x), block(TileShape<BM, BN, MS>::NT);
   if (obf)
     hipLaunchKernelGGL((k_tile_pp<BM, BN, MS, true>), grid, block, 0, st, g);

@@ -568,27 +568,27 @@ adaptcore_hw_t default_hw() {
   h.t_launch = 1.9e-06;
   h.t_mem_latency = 1.413e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 2.926e+10;
+  h.l2_bw_cu = 2.928e+10;
   h.unaligned_eta = 1;
   h.l2_hit = 5.38e-33;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
   // 20-21, stream-K 22-29, direct 30-32; 0 = analytic estimate, no timing
   // data)
   static const double kIter[AC_N_CFG] = {
-      2.843e-06, 2.05e-06, 1.918e-06, 3.911e-07, 5.432e-07, 2.177e-07, 5.382e-07, 3.955e-07,
-      1.111e-06, 2.515e-08, 9.358e-14, 1.229e-06, 1.26e-06, 1.4e-06, 1.405e-06, 1.777e-06,
-      1.905e-06, 6.727e-07, 6.909e-07, 7.981e-07, 2.84e-07, 2.206e-07, 4.678e-06, 2.461e-06,
-      3.445e-06, 1.498e-06, 1.11e-06, 1.072e-06, 0, 0, 9.358e-14, 9.358e-14,
-      1.177e-10, 2.978e-06, 2.153e-06, 0, 5.64e-07, 2.811e-07, 3.431e-07, 0,
+      2.853e-06, 2.085e-06, 1.938e-06, 3.052e-07, 5.513e-07, 2.327e-07, 5.38e-07, 3.959e-07,
+      1.119e-06, 2.57e-08, 9.358e-14, 1.231e-06, 1.259e-06, 1.399e-06, 1.399e-06, 1.761e-06,
+      1.964e-06, 6.729e-07, 6.937e-07, 8.013e-07, 2.712e-07, 2.062e-07, 4.752e-06, 2.484e-06,
+      3.088e-06, 1.534e-06, 1.002e-06, 1.065e-06, 0, 0, 9.358e-14, 9.358e-14,
+      3.967e-11, 2.943e-06, 2.043e-06, 0, 4.402e-07, 1.36e-07, 1.521e-07, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      2.279e-06, 1.156e-06, 3.112e-06, 2.405e-06, 1.321e-07, 7.565e-07, 3.633e-07, 3.08e-08,
-      1.991e-06, 1.779e-06, 2.028e-06, 7.933e-07, 1.174e-06, 2.798e-06, 4.069e-06, 6.439e-06,
-      7.013e-06, 6.975e-07, 1.164e-06, 1.996e-06, 9.117e-07, 1.322e-06, 9.358e-14, 1.32e-06,
-      7.478e-06, 2.293e-07, 8.497e-07, 1.111e-06, 0, 0, 9.358e-14, 3.564e-07,
-      1.646e-07, 1.025e-05, 4.617e-06, 0, 3.107e-06, 3.021e-06, 3.526e-06, 0,
+      2.31e-06, 1.15e-06, 3.06e-06, 2.529e-06, 1.161e-07, 7.499e-07, 3.608e-07, 3.72e-08,
+      1.987e-06, 1.794e-06, 2.042e-06, 7.819e-07, 1.181e-06, 2.927e-06, 4.094e-06, 6.485e-06,
+      7.368e-06, 7.191e-07, 1.131e-06, 1.954e-06, 9.492e-07, 1.392e-06, 2.626e-06, 1.239e-06,
+      8.657e-06, 9.358e-14, 1.078e-06, 2.487e-06, 0, 0, 9.358e-14, 3.788e-07,
+      1.919e-07, 9.099e-06, 5.193e-06, 0, 3.237e-06, 2.595e-06, 2.819e-06, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
