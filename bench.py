@@ -270,12 +270,157 @@ def moe_main(args):
     print(json.dumps(line), flush=True)
 
 
+def time_plan(ac, torch, plan, M, N, K, dtype, copies=8, target_s=250e-6, steps=5):
+    """Seconds per call of a forced plan: graph-replayed batches of back-to-back
+    calls cycling through up to `copies` copies of each operand (so that a
+    shape whose copies exceed the 256 MB Infinity Cache is read from HBM),
+    median over `steps` batches."""
+    dev = torch.device("cuda")
+    cb = 4 if dtype == ac.AC_BF16_F32OUT else 2
+    fa, fb, fc = 2 * M * K, 2 * K * N, cb * M * N
+    budget = 3 << 30  # bytes per operand
+    na, nb, nc = (max(1, min(copies, budget // max(f, 1))) for f in (fa, fb, fc))
+    A = torch.empty(na * M * K, dtype=torch.bfloat16, device=dev).uniform_(-1, 1)
+    B = torch.empty(nb * K * N, dtype=torch.bfloat16, device=dev).uniform_(-1, 1)
+    C = torch.empty(nc * M * N, dtype=torch.float32 if cb == 4 else torch.bfloat16, device=dev)
+    cs = torch.cuda.Stream()
+    ac.adaptcore_reserve_workspace(cs.cuda_stream, max(ac.adaptcore_plan_info(plan)["workspace_bytes"], 1))
+
+    def call(r):
+        ac.adaptcore_matmul(plan, A.data_ptr() + (r % na) * fa, K, B.data_ptr() + (r % nb) * fb, N,
+                            C.data_ptr() + (r % nc) * fc, N, cs.cuda_stream)
+    for r in range(3):
+        call(r)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(cs):
+        e0.record()
+        call(0)
+        e1.record()
+    torch.cuda.synchronize()
+    R = int(min(64, max(4, math.ceil(target_s / max(e0.elapsed_time(e1) * 1e-3, 1e-7)))))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cs):
+        for r in range(R):
+            call(r)
+    g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(steps):
+        with torch.cuda.stream(cs):
+            e0.record()
+            g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3 / R)
+    del g, A, B, C
+    return statistics.median(ts)
+
+
+def ablation_main(args):
+    """The paper's two single-shape experiments replayed on MI355X (Section 6.3
+    module ablation, Section 6.4 scalability), bf16 output:
+      * modules on 12288 x 688 x 16991, added one at a time to the Common
+        template's 128 x 128 tile: XCD-aware tile order, two k-blocks in
+        flight, split-K, the persistent kernel with next-tile preloading,
+        stream-K; then the best measured configuration and the model's pick;
+      * CU scaling on 3 x 256 x 87087: the MultiCoreSplitK kernel (small-M
+        kernel, K split P_k ways) with P_k = c workgroups, i.e. c CUs busy."""
+    import torch
+    import paper_2608_10803_amd as ac
+    bf = ac.AC_BF16_BF16OUT
+    hw = ac.adaptcore_get_hw()
+    out = {}
+
+    def key(fam, cfg, sw, pk):
+        return fam | (cfg << 4) | (sw << 12) | (pk << 16) | (bf << 48)
+
+    # -- module ablation
+    M, N, K = 12288, 688, 16991
+    F, Bb, tf = roof(M, N, K, 2)
+    h2 = ac.adaptcore_get_hw()
+    h2.search_open = 1
+    h2.enable_streamk = 1
+    ac.adaptcore_set_hw(h2)
+    cands = ac.adaptcore_candidates(M, N, K, bf, 0)
+    by_key = {c["variant_key"]: c for c in cands}
+    splits = sorted((c for c in cands if c["family_name"] == "tile" and c["tile_m"] == 128 and c["tile_n"] == 128
+                     and c["pk"] > 1 and (c["variant_key"] >> 12) & 1 and ((c["variant_key"] >> 4) & 0xFF) == 8),
+                    key=lambda c: c["predicted_s"])
+    ladder = [("Common template: 128x128, 1 k-block in flight, row-major tile order", key(0, 3, 0, 1)),
+              ("+ XCD-aware tile order", key(0, 3, 1, 1)),
+              ("+ 2 k-blocks in flight", key(0, 8, 1, 1))]
+    if splits:
+        ladder.append(("+ split-K (model's best P_k = %d)" % splits[0]["pk"], splits[0]["variant_key"]))
+    ladder += [("persistent 128x128 with next-tile preloading", key(7, 3, 1, 1)),
+               ("stream-K 128x128", next((c["variant_key"] for c in cands if c["family_name"] == "streamk"
+                                         and c["tile_m"] == 128 and c["tile_n"] == 128), None))]
+    rows = []
+    for name, k in ladder:
+        if k is None or k not in by_key:
+            continue
+        t = time_plan(ac, torch, ac.adaptcore_plan_variant(M, N, K, bf, 0, k), M, N, K, bf)
+        rows.append({"variant": name, "kernels": ac.adaptcore_plan_kernels(ac.adaptcore_plan_variant(M, N, K, bf, 0, k)),
+                     "us": round(t * 1e6, 1), "tflops": round(F / t / 1e12, 1), "frac": round(tf / t, 4),
+                     "pred_us": round(by_key[k]["predicted_s"] * 1e6, 1)})
+        print("ablation", rows[-1], file=sys.stderr, flush=True)
+    # the best measured configuration among the model's 24 best candidates
+    best = None
+    for c in cands[:24]:
+        t = time_plan(ac, torch, ac.adaptcore_plan_variant(M, N, K, bf, 0, c["variant_key"]), M, N, K, bf, steps=3)
+        if best is None or t < best[0]:
+            best = (t, c)
+    ac.adaptcore_set_hw(hw)
+    pick = ac.adaptcore_plan(M, N, K, bf)
+    tp = time_plan(ac, torch, pick, M, N, K, bf)
+    rows.append({"variant": "best of the model's 24 best candidates (measured)",
+                 "kernels": ac.adaptcore_plan_kernels(ac.adaptcore_plan_variant(M, N, K, bf, 0, best[1]["variant_key"])),
+                 "us": round(best[0] * 1e6, 1), "tflops": round(F / best[0] / 1e12, 1), "frac": round(tf / best[0], 4),
+                 "pred_us": round(best[1]["predicted_s"] * 1e6, 1)})
+    rows.append({"variant": "the model's pick (default plan)", "kernels": ac.adaptcore_plan_kernels(pick),
+                 "us": round(tp * 1e6, 1), "tflops": round(F / tp / 1e12, 1), "frac": round(tf / tp, 4),
+                 "pred_us": round(ac.adaptcore_plan_info(pick)["predicted_s"] * 1e6, 1)})
+    out["module_ablation"] = {"shape": [M, N, K], "t_floor_us": round(tf * 1e6, 2),
+                              "bound": "mfma" if F / Bb >= PEAK_FLOPS / PEAK_BW else "hbm", "rows": rows}
+
+    # -- CU scaling
+    M, N, K = 3, 256, 87087
+    F, Bb, tf = roof(M, N, K, 2)
+    kb = -(-K // 32)
+    scal = []
+    for c in (4, 8, 16, 32, 64, 128, 256):
+        kper = -(-kb // c)
+        pk = -(-kb // kper)  # the nearest legal split count (every partition non-empty)
+        k = key(1, 0, 0, pk)  # small-M kernel, 1 x 16 rows, 512 columns per workgroup: grid = P_k
+        try:
+            plan = ac.adaptcore_plan_variant(M, N, K, bf, 0, k)
+        except ac.AdaptCoreError:
+            continue
+        d = ac.adaptcore_plan_info(plan)
+        t = time_plan(ac, torch, plan, M, N, K, bf)
+        scal.append({"cus": d["grid_x"] * d["grid_y"], "pk": pk, "us": round(t * 1e6, 2),
+                     "gbps": round(Bb / t / 1e9, 1), "frac": round(tf / t, 4)})
+        print("scaling", scal[-1], file=sys.stderr, flush=True)
+    base = scal[0]["us"] * scal[0]["cus"] if scal else None
+    for r in scal:
+        r["efficiency_vs_first"] = round(base / (r["us"] * r["cus"]), 3)
+    pick = ac.adaptcore_plan(M, N, K, bf)
+    tp = time_plan(ac, torch, pick, M, N, K, bf)
+    out["cu_scaling"] = {"shape": [M, N, K], "t_floor_us": round(tf * 1e6, 2), "kernel": "k_skinny_m<1, 1, true>;k_reduce<true>",
+                         "rows": scal, "model_pick": {"kernels": ac.adaptcore_plan_kernels(pick),
+                                                      "us": round(tp * 1e6, 2), "frac": round(tf / tp, 4)}}
+    line = {"metric": "single-shape experiments (module ablation, CU scaling)", "value": None, "unit": "us",
+            "n_gpus": 1, "dtype": "bf16", "data": "synthetic", "higher_is_better": False,
+            "config": {"workload": "12288x688x16991 module ablation; 3x256x87087 CU scaling"}, **out}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe", "ablation"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true")
     ap.add_argument("--per-shape", default=None, help="write per-shape results to this JSON file")
@@ -301,6 +446,8 @@ def main():
     ac.adaptcore_init()
     if args.workload == "moe":
         return moe_main(args)
+    if args.workload == "ablation":
+        return ablation_main(args)
     dev = torch.device("cuda")
     if args.copy_ref:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)

@@ -742,10 +742,18 @@ std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_o
     // K-parallel templates search the split count P_k, whose degenerate value
     // P_k = 1 is kept because a small problem can lose more to the reduction
     // than it gains from the idle cores.
+    //
+    // The spatial predicate P_m * P_n >= N_core is a property of the tiling
+    // (Section 4.2), so it is applied to each candidate's own tile: a tile
+    // that leaves CUs idle on this shape belongs to a K-parallel template and
+    // keeps its split variants even when the taxonomy's base tile fills the
+    // GPU.
     const bool ksplit = cls == AC_CLASS_MULTI_CORE_SPLITK || cls == AC_CLASS_HYBRID_SPLITK;
     for (const Plan& p : all) {
       const bool pk_split = p.family == FAM_STREAMK ? true : p.pk > 1;
-      if (ksplit || !pk_split) sel.push_back(p);
+      const bool tile_idle = p.tile_m > 0 && p.tile_n > 0 &&
+                             cdiv(s.M, p.tile_m) * cdiv(s.N, p.tile_n) < (int64_t)hw.n_cu;
+      if (ksplit || tile_idle || !pk_split) sel.push_back(p);
     }
     if (sel.empty()) sel = all;
   }
