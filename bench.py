@@ -73,6 +73,8 @@ def workload_shapes(name):
         return gen.skinny_m(), 1
     if name == "splitk":
         return gen.small_mn_large_k(), 0
+    if name == "mfma":  # compute-bound squares and slabs, for MFMA-utilisation counters
+        return [(4096, 4096, 4096), (8192, 8192, 8192), (16384, 16384, 4096), (6144, 6144, 16384)], 1
     raise SystemExit("unknown workload %s" % name)
 
 
@@ -420,7 +422,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe", "ablation"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe", "ablation", "mfma"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true")
     ap.add_argument("--per-shape", default=None, help="write per-shape results to this JSON file")
@@ -655,7 +657,8 @@ def main():
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": {"sweep": "dynamic-shape sweep, 2000 shapes log-uniform [1,1e5], seed 4",
                                 "single": "512x512x512", "skinny": "skinny-M decode shapes (21)",
-                                "splitk": "small-MN large-K shapes (9)"}[args.workload],
+                                "splitk": "small-MN large-K shapes (9)",
+                                "mfma": "compute-bound shapes: 4096^3, 8192^3, 16384x16384x4096, 6144x6144x16384"}[args.workload],
                    "shapes": n, "inputs": "bf16 uniform[-1,1]", "accumulate": "fp32",
                    "output": "bf16" if cbytes == 2 else "fp32",
                    "timing": "graph-replayed batches of back-to-back calls on rotating operand copies"},
