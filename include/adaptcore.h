@@ -19,9 +19,9 @@
  *     thread-local message describing the last failure of the calling thread.
  *   - Matrices are dense, row-major, with leading dimensions in ELEMENTS.
  *     A is M x K (lda >= max(1, K)), B is K x N (ldb >= max(1, N)),
- *     C is M x N (ldc >= max(1, N)). Inputs are bf16 (raw 16-bit storage);
- *     accumulation is always fp32; C is fp32 or bf16 (round to nearest even)
- *     as the plan's dtype says.
+ *     C is M x N (ldc >= max(1, N)). Inputs are bf16 or fp16 (raw 16-bit
+ *     storage); accumulation is always fp32; C is fp32 or 16-bit in the
+ *     input format (round to nearest even) as the plan's dtype says.
  *   - A, B, C are device pointers owned by the caller; they must be aligned
  *     to their element size and must not overlap C.
  *   - The library is single-GPU: every call uses the HIP device current on
@@ -46,10 +46,13 @@ typedef enum {
   AC_ERR_INTERNAL = -6
 } adaptcore_status;
 
-/* Element types: bf16 inputs, fp32 accumulation, and the output type. */
+/* Element types: 16-bit inputs (A and B in the same format), fp32
+ * accumulation, and the output type. */
 typedef enum {
-  AC_BF16_F32OUT = 0,  /* C is fp32 */
-  AC_BF16_BF16OUT = 1  /* C is bf16, rounded to nearest even */
+  AC_BF16_F32OUT = 0,  /* bf16 inputs, C is fp32 */
+  AC_BF16_BF16OUT = 1, /* bf16 inputs, C is bf16, rounded to nearest even */
+  AC_F16_F32OUT = 2,   /* fp16 inputs, C is fp32 */
+  AC_F16_F16OUT = 3    /* fp16 inputs, C is fp16, rounded to nearest even */
 } adaptcore_dtype;
 
 /* Operand layouts. This build provides row-major A and row-major B. */

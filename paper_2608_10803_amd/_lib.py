@@ -23,6 +23,8 @@ AC_ERR_INTERNAL = -6
 
 AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
+AC_F16_F32OUT = 2
+AC_F16_F16OUT = 3
 AC_LAYOUT_ROW_ROW = 0
 (AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
  AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED) = range(9)
@@ -323,7 +325,8 @@ def adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain):
 
 def matmul_tensors(A, B, C, stream=None, plan=None):
     """C = A @ B for torch tensors on the GPU (2-D, row-major rows: stride(1)
-    == 1). A and B are torch.bfloat16, C torch.float32 or torch.bfloat16.
+    == 1). A and B are both torch.bfloat16 or both torch.float16, C
+    torch.float32 or the input type.
     Marshals pointers and leading dimensions; all arithmetic runs in the
     library's kernels."""
     import torch
@@ -331,14 +334,15 @@ def matmul_tensors(A, B, C, stream=None, plan=None):
     K2, N = B.shape
     if K2 != K or tuple(C.shape) != (M, N):
         raise ValueError("shape mismatch")
-    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16:
-        raise TypeError("A and B must be bfloat16")
+    if A.dtype != B.dtype or A.dtype not in (torch.bfloat16, torch.float16):
+        raise TypeError("A and B must both be bfloat16 or both float16")
+    f16 = A.dtype == torch.float16
     if C.dtype == torch.float32:
-        dt = AC_BF16_F32OUT
-    elif C.dtype == torch.bfloat16:
-        dt = AC_BF16_BF16OUT
+        dt = AC_F16_F32OUT if f16 else AC_BF16_F32OUT
+    elif C.dtype == A.dtype:
+        dt = AC_F16_F16OUT if f16 else AC_BF16_BF16OUT
     else:
-        raise TypeError("C must be float32 or bfloat16")
+        raise TypeError("C must be float32 or the input type")
     for t in (A, B, C):
         if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1) or not t.is_cuda:
             raise ValueError("operands must be 2-D GPU tensors with unit column stride")

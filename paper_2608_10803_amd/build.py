@@ -20,6 +20,10 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["kernels.hip", "planner.cpp", "adaptcore.cpp"]
+# compilation units: (source, object name, extra flags); the kernels are
+# compiled once per input format (bf16, and fp16 in namespace ac::f16)
+UNITS = [("kernels.hip", "kernels.hip.o", []), ("kernels.hip", "kernels_f16.hip.o", ["-DAC_INPUT_F16=1"]),
+         ("planner.cpp", "planner.cpp.o", []), ("adaptcore.cpp", "adaptcore.cpp.o", [])]
 HEADERS = ["kernel_args.h", "variants.h", "planner.h", "registry.h"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-Wall", "-Wno-unused-function",
@@ -40,10 +44,11 @@ def stale():
     return any(os.path.getmtime(f) > t for f in _inputs())
 
 
-def _compile(src):
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+def _compile(unit):
+    src, name, extra = unit
+    obj = os.path.join(BUILD, name)
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC] + COMMON + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC] + COMMON + extra + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
     if r.returncode != 0:
@@ -53,8 +58,8 @@ def _compile(src):
 
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(len(SOURCES)) as ex:
-        results = list(ex.map(_compile, SOURCES))
+    with cf.ThreadPoolExecutor(len(UNITS)) as ex:
+        results = list(ex.map(_compile, UNITS))
     objs = []
     for obj, err in results:
         objs.append(obj)

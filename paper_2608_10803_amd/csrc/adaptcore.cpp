@@ -123,8 +123,8 @@ bool valid_args(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts
     *st = fail(AC_ERR_INVALID_VALUE, "dimensions must be in [0, 2^31)");
     return false;
   }
-  if (dtype != AC_BF16_F32OUT && dtype != AC_BF16_BF16OUT) {
-    *st = fail(AC_ERR_UNSUPPORTED, "dtype not provided by this build (bf16 inputs with fp32 or bf16 output)");
+  if (dtype != AC_BF16_F32OUT && dtype != AC_BF16_BF16OUT && dtype != AC_F16_F32OUT && dtype != AC_F16_F16OUT) {
+    *st = fail(AC_ERR_UNSUPPORTED, "dtype not provided by this build (bf16 or fp16 inputs, fp32 or 16-bit output)");
     return false;
   }
   if (layouts != AC_LAYOUT_ROW_ROW) {
@@ -319,7 +319,7 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   if (lda >= AC_MAX_LD || ldb >= AC_MAX_LD)
     return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
   if (!C || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null matrix pointer");
-  const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
+  const int cbytes = ac::dtype_out_bytes(p.s.dtype);
   if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)))
     return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
   adaptcore_status st = ensure_init();
@@ -353,7 +353,7 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
     if (st != AC_OK) return st;
     g.ws = reinterpret_cast<float*>(w.ptr);
   }
-  const hipError_t e = ac::launch_plan(p, g, s);
+  const hipError_t e = ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(p, g, s) : ac::launch_plan(p, g, s);
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add((uint64_t)p.n_launch, std::memory_order_relaxed);
   return AC_OK;
@@ -434,7 +434,7 @@ adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const in
     return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
   if (rows == 0 || p.groups == 0 || N == 0 || p.grid_x == 0) return AC_OK;
   if (!C || !counts || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null pointer");
-  const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
+  const int cbytes = ac::dtype_out_bytes(p.s.dtype);
   if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)) || ((uintptr_t)counts & 3))
     return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
   adaptcore_status st = ensure_init();
@@ -461,7 +461,8 @@ adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const in
   a.stride_b = stride_b;
   a.groups = (int)p.groups;
   a.slots = p.pm;
-  const hipError_t e = ac::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream));
+  const hipError_t e = ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream))
+                                                       : ac::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add(1, std::memory_order_relaxed);
   return AC_OK;
@@ -546,7 +547,7 @@ adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const vo
     return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
   if (batch == 0 || M == 0 || N == 0 || p.grid_x == 0) return AC_OK;
   if (!C || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null matrix pointer");
-  const int cbytes = p.s.dtype == AC_BF16_F32OUT ? 4 : 2;
+  const int cbytes = ac::dtype_out_bytes(p.s.dtype);
   if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)))
     return fail(AC_ERR_INVALID_VALUE, "pointer not aligned to its element size");
   adaptcore_status st = ensure_init();
@@ -576,7 +577,8 @@ adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const vo
   a.groups = (int)batch;
   a.slots = p.pm;
   a.tiles_per_group = (int)((M + p.tile_m - 1) / p.tile_m);
-  const hipError_t e = ac::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream));
+  const hipError_t e = ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream))
+                                                       : ac::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add(1, std::memory_order_relaxed);
   return AC_OK;

@@ -4,6 +4,12 @@
 
 namespace ac {
 
+// Element types of adaptcore_dtype: 0 bf16 in / fp32 out, 1 bf16 in / bf16
+// out, 2 fp16 in / fp32 out, 3 fp16 in / fp16 out.
+constexpr bool dtype_f16_input(int dtype) { return dtype == 2 || dtype == 3; }
+constexpr bool dtype_out16(int dtype) { return dtype == 1 || dtype == 3; }
+constexpr int dtype_out_bytes(int dtype) { return dtype_out16(dtype) ? 2 : 4; }
+
 // Kernel families of the variant space.
 enum Family : int {
   FAM_TILE = 0,      // MFMA macro-tile kernel; P_k == 1 is the Common template,

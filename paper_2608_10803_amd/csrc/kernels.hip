@@ -1,6 +1,9 @@
-// gfx950 GEMM kernels: C = A * B with bf16 inputs, fp32 accumulation and
-// fp32 or bf16 output (RNE), for any M, N, K, leading dimensions and 2-byte
-// aligned pointers.
+// gfx950 GEMM kernels: C = A * B with 16-bit inputs, fp32 accumulation and
+// fp32 or 16-bit output (RNE), for any M, N, K, leading dimensions and 2-byte
+// aligned pointers. The file is compiled twice: for bf16 inputs (namespace ac)
+// and, with AC_INPUT_F16=1, for fp16 inputs (namespace ac::f16). Only the MFMA
+// instructions, the 16-bit output rounding and the small-K kernel's input
+// decode depend on the format; 16-bit outputs are in the input format.
 //
 //   k_tile      MFMA macro-tile kernel, LDS double buffered, one or two
 //               k-blocks of global loads in flight. P_k == 1 is the Common template
@@ -29,12 +32,23 @@
 
 #include "kernel_args.h"
 
+#ifndef AC_INPUT_F16
+#define AC_INPUT_F16 0
+#endif
+
 namespace ac {
+#if AC_INPUT_F16
+namespace f16 {
+#endif
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+#if AC_INPUT_F16
+typedef _Float16 in16x8 __attribute__((ext_vector_type(8)));
+#else
+typedef __bf16 in16x8 __attribute__((ext_vector_type(8)));
+#endif
 
 // ---------------------------------------------------------------- helpers
 
@@ -100,24 +114,36 @@ __device__ __forceinline__ void transpose8x8(const u32x4 (&r)[8], u32x4 (&c)[8])
   }
 }
 
+#if AC_INPUT_F16
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
+                                                0, 0);
 }
 __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
+                                                0, 0);
 }
-
-__device__ __forceinline__ uint16_t to_bf16(float f) {
-  __bf16 h = (__bf16)f;  // round to nearest even; NaN stays NaN
-  return __builtin_bit_cast(uint16_t, h);
+// fp32 -> the 16-bit output format, round to nearest even; NaN stays NaN
+__device__ __forceinline__ uint16_t to16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+// the value of a 16-bit input element (low 16 bits of h)
+__device__ __forceinline__ float from16(uint32_t h) { return (float)__builtin_bit_cast(_Float16, (uint16_t)h); }
+#else
+__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
+                                                 0, 0);
 }
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
+                                                 0, 0);
+}
+__device__ __forceinline__ uint16_t to16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ float from16(uint32_t h) { return __uint_as_float(h << 16); }
+#endif
 
 template <bool OBF>
 __device__ __forceinline__ void store_c(void* C, int64_t idx, float v) {
   if constexpr (OBF)
-    static_cast<uint16_t*>(C)[idx] = to_bf16(v);
+    static_cast<uint16_t*>(C)[idx] = to16(v);
   else
     static_cast<float*>(C)[idx] = v;
 }
@@ -130,10 +156,10 @@ __device__ __forceinline__ void store_c8(void* C, int64_t idx, const float (&v)[
     if (valid >= 8) {
       u32x4 w;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)to_bf16(v[2 * e]) | ((uint32_t)to_bf16(v[2 * e + 1]) << 16);
+      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)to16(v[2 * e]) | ((uint32_t)to16(v[2 * e + 1]) << 16);
       __builtin_memcpy(p, &w, 16);
     } else {
-      for (int j = 0; j < valid; ++j) p[j] = to_bf16(v[j]);
+      for (int j = 0; j < valid; ++j) p[j] = to16(v[j]);
     }
   } else {
     float* p = static_cast<float*>(C) + idx;
@@ -594,8 +620,8 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
       uint16_t* base = ct + (wr * S::WTM + i * MS + (lane % MS)) * S::CT_LD + wc * S::WTN + j * MS;
 #pragma unroll
       for (int q = 0; q < S::NA / 4; ++q) {
-        const uint32_t lo = (uint32_t)to_bf16(acc[i][j][4 * q]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 1]) << 16);
-        const uint32_t hi = (uint32_t)to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 3]) << 16);
+        const uint32_t lo = (uint32_t)to16(acc[i][j][4 * q]) | ((uint32_t)to16(acc[i][j][4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)to16(acc[i][j][4 * q + 2]) | ((uint32_t)to16(acc[i][j][4 * q + 3]) << 16);
         const uint64_t v = (uint64_t)lo | ((uint64_t)hi << 32);
         *reinterpret_cast<uint64_t*>(base + acc_col<MS>(4 * q, lane)) = v;
       }
@@ -619,40 +645,6 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
     } else {
       for (int j = 0; j < (int)(g.N - gc); ++j) dst[j] = src[j];
     }
-  }
-}
-
-// bf16 output straight from the accumulators: each lane writes its row's
-// runs of 4 columns as 8-byte stores (no LDS round trip, no barrier).
-template <int BM, int BN, int MS>
-__device__ __forceinline__ void store_acc_bf16_direct(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
-                                                                                    [TileShape<BM, BN, MS>::TN],
-                                                      const GemmArgs& g, int64_t m0, int64_t n0) {
-  typedef TileShape<BM, BN, MS> S;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wr = wave / S::WC, wc = wave % S::WC;
-  uint16_t* C = static_cast<uint16_t*>(g.C);
-#pragma unroll
-  for (int i = 0; i < S::TM; ++i) {
-    const int64_t row = m0 + wr * S::WTM + i * MS + (lane % MS);
-    if (row >= g.M) continue;
-#pragma unroll
-    for (int j = 0; j < S::TN; ++j)
-#pragma unroll
-      for (int q = 0; q < S::NA / 4; ++q) {
-        const int64_t col = n0 + wc * S::WTN + j * MS + acc_col<MS>(4 * q, lane);
-        uint16_t* d = C + row * g.ldc + col;
-        if (col + 4 <= g.N) {
-          const uint32_t lo = (uint32_t)to_bf16(acc[i][j][4 * q]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 1]) << 16);
-          const uint32_t hi = (uint32_t)to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 3]) << 16);
-          const uint64_t v = (uint64_t)lo | ((uint64_t)hi << 32);
-          __builtin_memcpy(d, &v, 8);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (col + e < g.N) d[e] = to_bf16(acc[i][j][4 * q + e]);
-        }
-      }
   }
 }
 
@@ -731,8 +723,8 @@ __device__ __forceinline__ void store_acc_bf16_fixed(const typename AccOf<MS>::T
       uint16_t* base = ct + (wr * S::WTM + i * MS + (lane % MS)) * S::CT_LD + wc * S::WTN + j * MS;
 #pragma unroll
       for (int q = 0; q < S::NA / 4; ++q) {
-        const uint32_t lo = (uint32_t)to_bf16(acc[i][j][4 * q]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 1]) << 16);
-        const uint32_t hi = (uint32_t)to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)to_bf16(acc[i][j][4 * q + 3]) << 16);
+        const uint32_t lo = (uint32_t)to16(acc[i][j][4 * q]) | ((uint32_t)to16(acc[i][j][4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)to16(acc[i][j][4 * q + 2]) | ((uint32_t)to16(acc[i][j][4 * q + 3]) << 16);
         *reinterpret_cast<uint64_t*>(base + acc_col<MS>(4 * q, lane)) = (uint64_t)lo | ((uint64_t)hi << 32);
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -1458,12 +1450,12 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
     if (k < K) v = load_row(g.B + (int64_t)k * g.ldb, c0, N);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      b[k][2 * e] = __uint_as_float(v[e] << 16);
-      b[k][2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
+      b[k][2 * e] = from16(v[e] & 0xFFFFu);
+      b[k][2 * e + 1] = from16(v[e] >> 16);
     }
   }
   for (int64_t rb = r0; rb < rend; rb += 4) {
-    // the 4 A rows of this group as raw bf16 (rows past M repeat row M-1)
+    // the 4 A rows of this group as raw 16-bit values (rows past M repeat row M-1)
     u32x4 av[4][KMAX / 8];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -1479,7 +1471,7 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
 #pragma unroll
       for (int k = 0; k < KMAX; ++k) {
         const uint32_t w = av[r][k / 8][(k % 8) / 2];
-        const float a = __uint_as_float((k & 1) ? (w & 0xFFFF0000u) : (w << 16));
+        const float a = from16((k & 1) ? (w >> 16) : (w & 0xFFFFu));
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(a, b[k][j], acc[j]);
       }
@@ -1617,8 +1609,8 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
     for (int q = 0; q < 4; ++q) {
       const int c = (wave & 1) * 32 + 8 * q + 4 * (lane >> 5);
       if constexpr (OUT == OUT_BF16) {
-        const uint32_t lo = (uint32_t)to_bf16(acc[4 * q]) | ((uint32_t)to_bf16(acc[4 * q + 1]) << 16);
-        const uint32_t hi = (uint32_t)to_bf16(acc[4 * q + 2]) | ((uint32_t)to_bf16(acc[4 * q + 3]) << 16);
+        const uint32_t lo = (uint32_t)to16(acc[4 * q]) | ((uint32_t)to16(acc[4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)to16(acc[4 * q + 2]) | ((uint32_t)to16(acc[4 * q + 3]) << 16);
         *reinterpret_cast<uint64_t*>(ct + r * LD + c) = (uint64_t)lo | ((uint64_t)hi << 32);
       } else {
         const f32x4 v = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
@@ -1658,8 +1650,8 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
       if constexpr (OUT == OUT_PARTIAL) {
         __builtin_memcpy(part + row * g.ldw + col, v, 16);
       } else if constexpr (OUT == OUT_BF16) {
-        const uint32_t lo = (uint32_t)to_bf16(v[0]) | ((uint32_t)to_bf16(v[1]) << 16);
-        const uint32_t hi = (uint32_t)to_bf16(v[2]) | ((uint32_t)to_bf16(v[3]) << 16);
+        const uint32_t lo = (uint32_t)to16(v[0]) | ((uint32_t)to16(v[1]) << 16);
+        const uint32_t hi = (uint32_t)to16(v[2]) | ((uint32_t)to16(v[3]) << 16);
         const uint64_t w = (uint64_t)lo | ((uint64_t)hi << 32);
         __builtin_memcpy(static_cast<uint16_t*>(g.C) + row * g.ldc + col, &w, 8);
       } else {
@@ -1678,6 +1670,9 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
   }
 }
 
+#if AC_INPUT_F16
+}  // namespace f16
+#endif
 }  // namespace ac
 
 // ------------------------------------------------------------- registry
@@ -1687,6 +1682,9 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
 #include "registry.h"
 
 namespace ac {
+#if AC_INPUT_F16
+namespace f16 {
+#endif
 
 namespace {
 
@@ -1981,7 +1979,7 @@ const OccFn kGroupedOcc[] = {grouped_occ<0>(), grouped_occ<1>(), grouped_occ<2>(
 }  // namespace
 
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
-  const bool obf = p.s.dtype == AC_BF16_BF16OUT;
+  const bool obf = dtype_out16(p.s.dtype);
   switch (p.family) {
     case FAM_TILE:
       return kTileFns[p.cfg](p, g, st, obf);
@@ -2006,7 +2004,7 @@ hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st
   if ((p.family != FAM_GROUPED && p.family != FAM_BATCHED) || p.cfg < 0 || p.cfg >= N_TILE_CFG ||
       !kGroupedFns[p.cfg])
     return hipErrorInvalidValue;
-  return kGroupedFns[p.cfg](p, a, st, p.s.dtype == AC_BF16_BF16OUT);
+  return kGroupedFns[p.cfg](p, a, st, dtype_out16(p.s.dtype));
 }
 
 void query_occupancy() {
@@ -2022,4 +2020,7 @@ void query_occupancy() {
     if (kPersistOcc[i]) set_runtime_occupancy(FAM_PERSIST, i, kPersistOcc[i]());
 }
 
+#if AC_INPUT_F16
+}  // namespace f16
+#endif
 }  // namespace ac

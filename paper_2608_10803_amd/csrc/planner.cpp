@@ -40,7 +40,7 @@ int table_occ(int family, int cfg) {
   return 1;
 }
 
-int out_bytes(int dtype) { return dtype == AC_BF16_F32OUT ? 4 : 2; }
+int out_bytes(int dtype) { return dtype_out_bytes(dtype); }
 
 // Offsets of each family's configurations in the calibrated cost tables.
 constexpr int IDX_TILE = 0;
@@ -919,8 +919,22 @@ bool batched_for_key(const Shape& s, int64_t batch, const adaptcore_hw_t& hw, ui
   return true;
 }
 
+static std::string kernel_names_fmt(const Plan& p);
+
 std::string kernel_names(const Plan& p) {
-  const int obf = p.s.dtype == AC_BF16_BF16OUT;
+  // the fp16-input kernels live in the nested namespace f16
+  std::string r = kernel_names_fmt(p);
+  if (!dtype_f16_input(p.s.dtype) || r.empty()) return r;
+  std::string out = "f16::";
+  for (char ch : r) {
+    out += ch;
+    if (ch == ';') out += "f16::";
+  }
+  return out;
+}
+
+static std::string kernel_names_fmt(const Plan& p) {
+  const int obf = dtype_out16(p.s.dtype);
   const char* b = obf ? "true" : "false";
   char buf[160];
   switch (p.family) {

@@ -6,9 +6,16 @@
 #include "planner.h"
 
 namespace ac {
+// bf16 inputs (dtypes 0 and 1)
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
 // Launch of a grouped or batched plan (families FAM_GROUPED, FAM_BATCHED).
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 // Reads the device's occupancy of every kernel into the planner.
 void query_occupancy();
+// the same kernels for fp16 inputs (dtypes 2 and 3)
+namespace f16 {
+hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
+hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
+void query_occupancy();
+}  // namespace f16
 }  // namespace ac

@@ -30,6 +30,15 @@ def to_device(bits, ld=None, offset=0):
     return dev, dev.data_ptr() + 2 * offset
 
 
+def fp32_out(dtype):
+    return dtype in (ac.AC_BF16_F32OUT, ac.AC_F16_F32OUT)
+
+
+def fmt_of(dtype):
+    """Format of the inputs (and of a 16-bit output) of a dtype."""
+    return "fp16" if dtype in (ac.AC_F16_F32OUT, ac.AC_F16_F16OUT) else "bf16"
+
+
 class Out:
     """Output buffer of M x N with leading dimension ldc, a canary row above
     and below and canary columns beyond N."""
@@ -38,7 +47,7 @@ class Out:
         t = torch()
         self.M, self.N, self.ldc, self.dtype = M, N, ldc, dtype
         n = (M + 2) * ldc
-        if dtype == ac.AC_BF16_F32OUT:
+        if fp32_out(dtype):
             self.host = np.full(n, F32_CANARY, np.float32)
             self.dev = t.from_numpy(self.host.copy()).to("cuda")
             self.addr = self.dev.data_ptr() + 4 * ldc
@@ -50,13 +59,13 @@ class Out:
     def read(self):
         """(values as fp64 M x N, canaries intact?)"""
         raw = self.dev.cpu().numpy()
-        if self.dtype == ac.AC_BF16_F32OUT:
+        if fp32_out(self.dtype):
             full = raw.reshape(self.M + 2, self.ldc)
             vals = full[1:self.M + 1, :self.N].astype(np.float64)
             canary = F32_CANARY
         else:
             full = raw.view(np.uint16).reshape(self.M + 2, self.ldc)
-            vals = gemm_ref.decode(np.ascontiguousarray(full[1:self.M + 1, :self.N]))
+            vals = gemm_ref.decode(np.ascontiguousarray(full[1:self.M + 1, :self.N]), fmt=fmt_of(self.dtype))
             canary = BF16_CANARY
         mask = np.ones(full.shape, bool)
         mask[1:self.M + 1, :self.N] = False
@@ -81,12 +90,22 @@ def run(plan, A, B, M, N, K, dtype, lda=None, ldb=None, ldc=None, a_off=0, b_off
 
 
 def tol(dtype):
-    return gemm_ref.TOL["f32" if dtype == ac.AC_BF16_F32OUT else "bf16"]
+    if fp32_out(dtype):
+        return gemm_ref.TOL["f32"]
+    return gemm_ref.TOL[fmt_of(dtype)]
+
+
+# fp16 output: rounding to nearest even has relative error <= 2^-11 in the
+# normal range (inside the 1e-3 bar) but absolute error up to half the
+# subnormal spacing, 2^-25, below 2^-14; differences within that are exact.
+F16_SUBNORMAL_HALF_ULP = 2.0 ** -25
 
 
 def check(vals, ok, A, B, dtype, ref=None, label=""):
     assert ok, "write outside C (canary overwritten) %s" % label
-    C_ref, D = ref if ref is not None else gemm_ref.gemm(A, B)
+    C_ref, D = ref if ref is not None else gemm_ref.gemm(A, B, fmt=fmt_of(dtype))
+    if dtype == ac.AC_F16_F16OUT:
+        vals = np.where(np.abs(vals - C_ref) <= F16_SUBNORMAL_HALF_ULP, C_ref, vals)
     err = gemm_ref.err_metric(vals, C_ref, D)
     assert err <= tol(dtype), "err %.3g > %.3g %s" % (err, tol(dtype), label)
     return err

@@ -348,3 +348,37 @@ def test_batched_k_zero():
     plan = ac.adaptcore_batched_plan(batch, M, N, 0, F32)
     vals, ok = run_batched(plan, A, B, batch, M, N, 0, 1, N, N, 0, 0, M * N + 5, F32)
     assert ok and not vals.any()
+
+
+
+def test_fp16_grouped_and_batched():
+    """The grouped and batched products with fp16 inputs and output."""
+    F16 = ac.AC_F16_F16OUT
+    counts, rows, N, K = [90, 0, 37, 200, 1], 400, 200, 130
+    A = gen.uniform_f16(rows, K, 41)
+    mats = [gen.uniform_f16(K, N, 42 + g) for g in range(len(counts))]
+    B = np.concatenate([m.reshape(-1) for m in mats])
+    t = torch()
+    Ad = t.from_numpy(A.view(np.int16)).cuda()
+    Bd = t.from_numpy(B.view(np.int16)).cuda()
+    cnt = t.from_numpy(np.asarray(counts, np.int32)).cuda()
+    Cd = t.zeros(rows * N, dtype=t.int16, device="cuda")
+    plan = ac.adaptcore_grouped_plan(rows, len(counts), N, K, F16)
+    assert ac.adaptcore_plan_kernels(plan)[0].startswith("f16::k_grouped<")
+    ac.adaptcore_grouped_matmul(plan, cnt.data_ptr(), Ad.data_ptr(), K, Bd.data_ptr(), N, K * N, Cd.data_ptr(), N, 0)
+    t.cuda.synchronize()
+    got = gemm_ref.decode(Cd.cpu().numpy().view(np.uint16).reshape(rows, N), fmt="fp16")
+    C_ref, D, cov = grouped_ref.grouped_gemm(A, B, counts, rows, N, K, K, N, K * N, fmt="fp16")
+    got = np.where(np.abs(got - C_ref) <= 2.0 ** -25, C_ref, got)
+    assert gemm_ref.err_metric(got[cov], C_ref[cov], D[cov]) <= gemm_ref.TOL["fp16"]
+    assert not got[~cov].any()
+    # batched: contiguous batches of 80 rows
+    batch, M = 5, 80
+    plan = ac.adaptcore_batched_plan(batch, M, N, K, F16)
+    Cd.zero_()
+    ac.adaptcore_batched_matmul(plan, Ad.data_ptr(), K, M * K, Bd.data_ptr(), N, K * N, Cd.data_ptr(), N, M * N, 0)
+    t.cuda.synchronize()
+    got = gemm_ref.decode(Cd.cpu().numpy().view(np.uint16)[:batch * M * N].reshape(batch, M, N), fmt="fp16")
+    C_ref, D = grouped_ref.batched_gemm(A, B, batch, M, N, K, K, N, M * K, K * N, fmt="fp16")
+    got = np.where(np.abs(got - C_ref) <= 2.0 ** -25, C_ref, got)
+    assert gemm_ref.err_metric(got.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N)) <= gemm_ref.TOL["fp16"]

@@ -21,6 +21,7 @@ from gpu_util import all_candidates, check, forced_plan, run, torch
 pytestmark = pytest.mark.gpu
 
 F32, BF16 = ac.AC_BF16_F32OUT, ac.AC_BF16_BF16OUT
+F16F32, F16F16 = ac.AC_F16_F32OUT, ac.AC_F16_F16OUT
 
 
 def note(*a):
@@ -216,3 +217,43 @@ def test_persistent_tile_configurations(shape, dtype):
         if key is not None:
             vt, ok2 = run(forced_plan(M, N, K, dtype, key), A, B, M, N, K, dtype)
             assert ok2 and np.array_equal(vt, vals), "persistent differs from the tile kernel %s" % c
+
+
+
+# ---- fp16 inputs (the same kernels built for the fp16 MFMA instructions)
+
+SMALL_F16 = [(1, 1, 1), (7, 5, 3), (17, 33, 65), (129, 255, 257), (200, 300, 1000), (255, 64, 1),
+             (3, 1000, 100), (500, 7, 300), (300, 600, 70), (1000, 20, 33)]
+
+
+@pytest.mark.parametrize("dtype", [F16F32, F16F16], ids=["f16_f32out", "f16_f16out"])
+@pytest.mark.parametrize("shape", SMALL_F16, ids=lambda s: "x".join(map(str, s)))
+def test_fp16_every_configuration(shape, dtype):
+    M, N, K = shape
+    A, B = gen.operands(M, N, K, seed=M * 5 + N * 3 + K, dist="uniform_f16")
+    ref = gemm_ref.gemm(A, B, fmt="fp16")
+    cands = all_candidates(M, N, K, dtype)
+    assert cands
+    note("fp16 shape", shape, "dtype", dtype, "configurations", len(cands))
+    for c in cands:
+        plan = forced_plan(M, N, K, dtype, c["variant_key"])
+        assert ac.adaptcore_plan_kernels(plan)[0].startswith("f16::")
+        vals, ok = run(plan, A, B, M, N, K, dtype)
+        check(vals, ok, A, B, dtype, ref=ref, label="%s %s" % (shape, c))
+
+
+@pytest.mark.parametrize("dtype", [F16F32, F16F16], ids=["f16_f32out", "f16_f16out"])
+def test_fp16_default_plans_and_persistent(dtype):
+    """Default plans of larger shapes and every persistent configuration of
+    one shape with more tiles than workgroups, fp16 inputs."""
+    for (M, N, K) in [(2100, 3000, 200), (640, 1000, 4096), (4, 4096, 4096)]:
+        A, B = gen.operands(M, N, K, seed=M + N + K, dist="uniform_f16")
+        ref = gemm_ref.gemm(A, B, fmt="fp16")
+        keys = [ac.adaptcore_plan_info(ac.adaptcore_plan(M, N, K, dtype))["variant_key"]]
+        if (M, N, K) == (2100, 3000, 200):
+            keys += [c["variant_key"] for c in all_candidates(M, N, K, dtype) if c["family_name"] == "persist"]
+        for k in keys:
+            plan = forced_plan(M, N, K, dtype, k)
+            note("fp16", (M, N, K), ac.adaptcore_plan_kernels(plan))
+            vals, ok = run(plan, A, B, M, N, K, dtype)
+            check(vals, ok, A, B, dtype, ref=ref, label="%s %s" % ((M, N, K), hex(k)))

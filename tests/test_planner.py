@@ -214,3 +214,19 @@ def test_profile_validation_and_cu_count_effect():
     finally:
         ac.adaptcore_set_hw(hw)
     assert ac.adaptcore_get_hw().n_cu == hw.n_cu
+
+
+def test_fp16_plans():
+    """fp16 inputs plan like bf16 (same model, same configurations), under a
+    different key, with the kernels of the fp16 build."""
+    for s in [(512, 512, 512), (3, 4096, 4096), (20000, 30000, 100), (7, 5, 3)]:
+        for dt16, dtb in [(ac.AC_F16_F32OUT, ac.AC_BF16_F32OUT), (ac.AC_F16_F16OUT, ac.AC_BF16_BF16OUT)]:
+            h16, hb = ac.adaptcore_plan(*s, dt16), ac.adaptcore_plan(*s, dtb)
+            d16, db = ac.adaptcore_plan_info(h16), ac.adaptcore_plan_info(hb)
+            assert h16 != hb and d16["shape_key"] != db["shape_key"]
+            assert (d16["family"], d16["tile_m"], d16["tile_n"], d16["pk"]) == (db["family"], db["tile_m"], db["tile_n"], db["pk"])
+            k16, kb = ac.adaptcore_plan_kernels(h16), ac.adaptcore_plan_kernels(hb)
+            assert k16 == ["f16::" + k for k in kb], (k16, kb)
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_plan(4, 4, 4, 4)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED

@@ -40,6 +40,16 @@ def bf16_bits(x):
     return out
 
 
+def f16_bits(x):
+    """fp32 array -> uint16 IEEE fp16 bit patterns, round to nearest, ties to even."""
+    return np.ascontiguousarray(x, dtype=np.float32).astype(np.float16).view(U16)
+
+
+def uniform_f16(rows, cols, seed, lo=-1.0, hi=1.0):
+    rng = np.random.default_rng(seed)
+    return f16_bits(rng.uniform(lo, hi, size=(rows, cols)).astype(np.float32))
+
+
 def uniform_bf16(rows, cols, seed, lo=-1.0, hi=1.0):
     rng = np.random.default_rng(seed)
     return bf16_bits(rng.uniform(lo, hi, size=(rows, cols)).astype(np.float32))
@@ -56,7 +66,10 @@ def int_bf16(rows, cols, seed, lim=4):
 
 
 def operands(M, N, K, seed, dist="uniform"):
-    """A (M x K) and B (K x N) bf16 bit patterns for one shape."""
+    """A (M x K) and B (K x N) bf16 bit patterns for one shape ("uniform_f16":
+    fp16 bit patterns of the same distribution)."""
+    if dist == "uniform_f16":
+        return uniform_f16(M, K, (seed, 0)), uniform_f16(K, N, (seed, 1))
     if dist == "uniform":
         return uniform_bf16(M, K, (seed, 0)), uniform_bf16(K, N, (seed, 1))
     if dist == "normal":  # normal(0, 1/sqrt(K)), sigma read as the std
