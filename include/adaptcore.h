@@ -198,6 +198,25 @@ const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, 
 adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
                                   int64_t ldb, void* C, int64_t ldc, void* stream);
 
+/* ---- AddMM ------------------------------------------------------------------
+ * AddMM is one of the dense operators the paper replaces in its end-to-end
+ * models beside MatMul (Section 6.5; operator scope, Section 7). It runs a
+ * plain plan with an epilogue applied to every element of C at the final
+ * store, in fp32, before the rounding to C's type:
+ *
+ *   C[i][j] = alpha * (A * B)[i][j] + beta * C_old[i][j] + bias[j]
+ *
+ * C_old is C's content before the call (read only when beta != 0, so C may
+ * hold anything when beta == 0); bias is a device array of N fp32 values
+ * (NULL: no bias term). Split-K and stream-K plans apply the epilogue once,
+ * in the kernel that writes the final value. Arguments, validation, workspace
+ * and stream semantics are those of adaptcore_matmul; in addition alpha and
+ * beta must be finite and bias aligned to 4 bytes (AC_ERR_INVALID_VALUE).
+ * K == 0 yields C = beta * C_old + bias. A, B and bias must not overlap C. */
+adaptcore_status adaptcore_addmm(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
+                                 int64_t ldb, void* C, int64_t ldc, float alpha, float beta, const float* bias,
+                                 void* stream);
+
 /* ---- Grouped product (GroupMM) ---------------------------------------------
  * The paper replaces the grouped products of its end-to-end models (GroupMM,
  * Section 6.5; operator scope, Section 7) as well as plain ones, and names

@@ -1,0 +1,55 @@
+"""AddMM oracle -- TEST INFRASTRUCTURE ONLY.
+
+Only tests, the smoke check and the benchmark's CPU-baseline leg may import
+this module; it shares no code with the GPU library.
+
+AddMM is one of the dense operators the paper replaces in its end-to-end
+models next to MatMul (Section 6.5; operator scope, Section 7). The paper
+names the operator but does not write it out; it is read here with its usual
+meaning, a scaled product plus a scaled input plus a bias row broadcast over
+the rows:
+
+    C[i][j] = alpha * sum_k A[i][k] * B[k][j] + beta * C_old[i][j] + bias[j]
+
+with the product taken from the plain-product oracle (gemm_ref) in fp64.
+When beta == 0 the input C_old takes no part at all (it may hold NaN or
+garbage, as with the BLAS convention); bias None means no bias term.
+
+The acceptance scale of an entry is the sum of the magnitudes of its terms,
+
+    D[i][j] = |alpha| * sum_k |A[i][k] B[k][j]| + |beta| |C_old[i][j]| + |bias[j]|,
+
+so that the GPU's fp32 epilogue rounding and the final rounding to a 16-bit
+output are measured against the same relative bars as a plain product.
+
+Parity pins: tests/test_oracle_addmm.py (exact rational brute force of C and
+D on tiny inputs with mixed-sign alpha and beta, reduction to the plain
+product, beta == 0 ignoring a NaN C_old, K == 0, and a mutation test).
+"""
+import numpy as np
+
+from . import gemm_ref
+
+
+def addmm(A, B, C_old, alpha, beta, bias=None, M=None, N=None, K=None, lda=None, ldb=None, fmt="bf16",
+          lib=None):
+    """(C_ref, D) of AddMM in fp64, both M x N.
+
+    A, B: uint16 bit patterns as for gemm_ref.gemm; C_old: M x N values (the
+    previous content of C, already decoded to numbers); bias: N values or
+    None.
+    """
+    P, Dp = gemm_ref.gemm(A, B, M=M, N=N, K=K, lda=lda, ldb=ldb, fmt=fmt, lib=lib)
+    alpha = float(alpha)
+    beta = float(beta)
+    C = alpha * P
+    D = abs(alpha) * Dp
+    if beta != 0.0:
+        Co = np.asarray(C_old, np.float64).reshape(C.shape)
+        C = C + beta * Co
+        D = D + abs(beta) * np.abs(Co)
+    if bias is not None:
+        b = np.asarray(bias, np.float64).reshape(1, C.shape[1])
+        C = C + b
+        D = D + np.abs(b)
+    return C, D

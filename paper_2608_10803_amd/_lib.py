@@ -128,6 +128,8 @@ def lib():
         L.adaptcore_plan_variant.restype = p
         L.adaptcore_matmul.argtypes = [p, p, i64, p, i64, p, i64, p]
         L.adaptcore_matmul.restype = i32
+        L.adaptcore_addmm.argtypes = [p, p, i64, p, i64, p, i64, ctypes.c_float, ctypes.c_float, p, p]
+        L.adaptcore_addmm.restype = i32
         L.adaptcore_grouped_plan.argtypes = [i64, i64, i64, i64, i32, u32]
         L.adaptcore_grouped_plan.restype = p
         L.adaptcore_grouped_plan_variant.argtypes = [i64, i64, i64, i64, i32, u32, u64]
@@ -211,6 +213,12 @@ def adaptcore_plan_variant(M, N, K, dtype, layouts, variant_key):
 def adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream=0):
     """C = A * B on `stream`; A, B, C are device addresses (ints)."""
     return _check(lib().adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream))
+
+
+def adaptcore_addmm(plan, A, lda, B, ldb, C, ldc, alpha=1.0, beta=0.0, bias=0, stream=0):
+    """C = alpha * A * B + beta * C + bias on `stream`; A, B, C, bias are
+    device addresses (ints), bias = 0 for none."""
+    return _check(lib().adaptcore_addmm(plan, A, lda, B, ldb, C, ldc, alpha, beta, bias, stream))
 
 
 def adaptcore_grouped_plan(rows, groups, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):
@@ -323,12 +331,8 @@ def adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain):
     return lib().adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain)
 
 
-def matmul_tensors(A, B, C, stream=None, plan=None):
-    """C = A @ B for torch tensors on the GPU (2-D, row-major rows: stride(1)
-    == 1). A and B are both torch.bfloat16 or both torch.float16, C
-    torch.float32 or the input type.
-    Marshals pointers and leading dimensions; all arithmetic runs in the
-    library's kernels."""
+def _marshal_tensors(A, B, C):
+    """(M, N, K, dtype code) of a tensor product, after the checks."""
     import torch
     M, K = A.shape
     K2, N = B.shape
@@ -346,9 +350,39 @@ def matmul_tensors(A, B, C, stream=None, plan=None):
     for t in (A, B, C):
         if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1) or not t.is_cuda:
             raise ValueError("operands must be 2-D GPU tensors with unit column stride")
+    return M, N, K, dt
+
+
+def matmul_tensors(A, B, C, stream=None, plan=None):
+    """C = A @ B for torch tensors on the GPU (2-D, row-major rows: stride(1)
+    == 1). A and B are both torch.bfloat16 or both torch.float16, C
+    torch.float32 or the input type.
+    Marshals pointers and leading dimensions; all arithmetic runs in the
+    library's kernels."""
+    import torch
+    M, N, K, dt = _marshal_tensors(A, B, C)
     if plan is None:
         plan = adaptcore_plan(M, N, K, dt, AC_LAYOUT_ROW_ROW)
     s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
     adaptcore_matmul(plan, A.data_ptr(), max(A.stride(0), 1), B.data_ptr(), max(B.stride(0), 1),
                      C.data_ptr(), max(C.stride(0), 1), s)
+    return C
+
+
+def addmm_tensors(A, B, C, alpha=1.0, beta=0.0, bias=None, stream=None, plan=None):
+    """C = alpha * A @ B + beta * C + bias in place, for torch tensors laid out
+    as in matmul_tensors; bias is None or a contiguous float32 GPU tensor of
+    N elements."""
+    import torch
+    M, N, K, dt = _marshal_tensors(A, B, C)
+    bp = 0
+    if bias is not None:
+        if bias.dtype != torch.float32 or bias.numel() != N or not bias.is_cuda or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous float32 GPU tensor of N elements")
+        bp = bias.data_ptr()
+    if plan is None:
+        plan = adaptcore_plan(M, N, K, dt, AC_LAYOUT_ROW_ROW)
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    adaptcore_addmm(plan, A.data_ptr(), max(A.stride(0), 1), B.data_ptr(), max(B.stride(0), 1),
+                    C.data_ptr(), max(C.stride(0), 1), float(alpha), float(beta), bp, s)
     return C

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <chrono>
 #include <cstring>
@@ -303,8 +304,13 @@ adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes) {
   return get_workspace(static_cast<hipStream_t>(stream), bytes, &w);
 }
 
-adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
-                                  void* C, int64_t ldc, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// One call of a plain plan; epi != 0 selects the AddMM epilogue.
+adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
+                            void* C, int64_t ldc, void* stream, int epi, float alpha, float beta, const float* bias) {
   if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
   const ac::Plan& p = plan->p;
   if (p.family == ac::FAM_GROUPED)
@@ -338,6 +344,10 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   g.ldb = ldb;
   g.ldc = ldc;
   g.ldw = (N + 7) / 8 * 8;
+  g.epi = epi;
+  g.alpha = alpha;
+  g.beta = beta;
+  g.bias = bias;
   g.pk = p.family == ac::FAM_STREAMK ? 1 : p.pk;
   g.kper = p.kper;
   g.tiles_m = p.pm;
@@ -357,6 +367,22 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add((uint64_t)p.n_launch, std::memory_order_relaxed);
   return AC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
+                                  void* C, int64_t ldc, void* stream) {
+  return run_matmul(plan, A, lda, B, ldb, C, ldc, stream, 0, 1.0f, 0.0f, nullptr);
+}
+
+adaptcore_status adaptcore_addmm(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
+                                 void* C, int64_t ldc, float alpha, float beta, const float* bias, void* stream) {
+  if (!std::isfinite(alpha) || !std::isfinite(beta)) return fail(AC_ERR_INVALID_VALUE, "alpha and beta must be finite");
+  if (((uintptr_t)bias & 3)) return fail(AC_ERR_INVALID_VALUE, "bias not aligned to 4 bytes");
+  return run_matmul(plan, A, lda, B, ldb, C, ldc, stream, 1, alpha, beta, bias);
 }
 
 const adaptcore_plan_t* adaptcore_grouped_plan(int64_t rows, int64_t groups, int64_t N, int64_t K, int32_t dtype,

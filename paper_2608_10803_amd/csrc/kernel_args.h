@@ -45,6 +45,12 @@ struct GemmArgs {
   int sk_tiles;      // stream-K: tiles handled by the stream-K phase
   int ws_pk;         // stream-K: partial slots per split tile
   int grid;          // stream-K: persistent workgroups
+  // AddMM epilogue (epi != 0): C = alpha * (A B) + beta * C_old + bias[col],
+  // applied in fp32 where the final C is written; C_old is read only when
+  // beta != 0. Partials of split K and stream-K stay raw sums.
+  float alpha, beta;
+  const float* bias;  // N values or null
+  int epi;
 };
 
 // Arguments of the grouped kernel. With counts: group g owns rows

@@ -148,6 +148,30 @@ __device__ __forceinline__ void store_c(void* C, int64_t idx, float v) {
     static_cast<float*>(C)[idx] = v;
 }
 
+// ---- AddMM epilogue on outputs of one row (uniform test of g.epi; C_old is
+// read only where an output exists and beta != 0)
+template <bool OBF>
+__device__ __forceinline__ float c_old(const GemmArgs& g, int64_t row, int64_t col) {
+  if constexpr (OBF)
+    return from16(static_cast<const uint16_t*>(g.C)[row * g.ldc + col]);
+  else
+    return static_cast<const float*>(g.C)[row * g.ldc + col];
+}
+template <bool OBF, int NV>
+__device__ __forceinline__ void epi_apply(const GemmArgs& g, float (&v)[NV], int64_t row, int64_t col,
+                                          int64_t valid) {
+  if (!g.epi) return;
+#pragma unroll
+  for (int e = 0; e < NV; ++e) {
+    if (e < valid) {
+      float x = g.alpha * v[e];
+      if (g.bias) x += g.bias[col + e];
+      if (g.beta != 0.f) x += g.beta * c_old<OBF>(g, row, col + e);
+      v[e] = x;
+    }
+  }
+}
+
 // Eight consecutive outputs of one row; `valid` of them exist.
 template <bool OBF>
 __device__ __forceinline__ void store_c8(void* C, int64_t idx, const float (&v)[8], int64_t valid) {
@@ -171,6 +195,23 @@ __device__ __forceinline__ void store_c8(void* C, int64_t idx, const float (&v)[
       for (int j = 0; j < valid; ++j) p[j] = v[j];
     }
   }
+}
+
+// One / eight final outputs of C at (row, col): the epilogue, then the store.
+template <bool OBF>
+__device__ __forceinline__ void store_out(const GemmArgs& g, int64_t row, int64_t col, float v) {
+  float w[1] = {v};
+  epi_apply<OBF, 1>(g, w, row, col, 1);
+  store_c<OBF>(g.C, row * g.ldc + col, w[0]);
+}
+template <bool OBF>
+__device__ __forceinline__ void store_out8(const GemmArgs& g, int64_t row, int64_t col, const float (&v)[8],
+                                           int64_t valid) {
+  float w[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) w[e] = v[e];
+  epi_apply<OBF, 8>(g, w, row, col, valid);
+  store_c8<OBF>(g.C, row * g.ldc + col, w, valid);
 }
 
 // LDS rows are 16-byte chunks; the chunk index is XORed with low row bits so
@@ -572,7 +613,7 @@ template <int BM, int BN, int MS>
 __device__ __forceinline__ void store_acc_f32(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                             [TileShape<BM, BN, MS>::TN],
                                               float* dst, int64_t ld, int64_t m0, int64_t n0, int64_t rmax,
-                                              int64_t cmax) {
+                                              int64_t cmax, const GemmArgs* ep = nullptr) {
   typedef TileShape<BM, BN, MS> S;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wr = wave / S::WC, wc = wave % S::WC;
@@ -587,13 +628,15 @@ __device__ __forceinline__ void store_acc_f32(const typename AccOf<MS>::T (&acc)
         // elements 4q .. 4q+3: four consecutive columns of the lane's row
         const int64_t col = n0 + wc * S::WTN + j * MS + acc_col<MS>(4 * q, lane);
         float* d = dst + row * ld + col;
+        float w[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (ep != nullptr && col < cmax) epi_apply<false, 4>(*ep, w, row, col, cmax - col);
         if (col + 4 <= cmax) {
-          const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          const f32x4 v = {w[0], w[1], w[2], w[3]};
           __builtin_memcpy(d, &v, 16);
         } else {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (col + e < cmax) d[e] = acc[i][j][4 * q + e];
+            if (col + e < cmax) d[e] = w[e];
         }
       }
   }
@@ -601,7 +644,7 @@ __device__ __forceinline__ void store_acc_f32(const typename AccOf<MS>::T (&acc)
 
 // bf16 output through LDS: the tile is converted into LDS row-major (rows
 // padded to BN + 4 elements), then written with 16-byte row segments.
-template <int BM, int BN, int MS>
+template <int BM, int BN, int MS, bool EPI>
 __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                              [TileShape<BM, BN, MS>::TN],
                                                const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
@@ -620,8 +663,14 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
       uint16_t* base = ct + (wr * S::WTM + i * MS + (lane % MS)) * S::CT_LD + wc * S::WTN + j * MS;
 #pragma unroll
       for (int q = 0; q < S::NA / 4; ++q) {
-        const uint32_t lo = (uint32_t)to16(acc[i][j][4 * q]) | ((uint32_t)to16(acc[i][j][4 * q + 1]) << 16);
-        const uint32_t hi = (uint32_t)to16(acc[i][j][4 * q + 2]) | ((uint32_t)to16(acc[i][j][4 * q + 3]) << 16);
+        float w[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (EPI && g.epi) {
+          const int64_t row = m0 + wr * S::WTM + i * MS + (lane % MS);
+          const int64_t col = n0 + wc * S::WTN + j * MS + acc_col<MS>(4 * q, lane);
+          if (row < g.M && col < g.N) epi_apply<true, 4>(g, w, row, col, g.N - col);
+        }
+        const uint32_t lo = (uint32_t)to16(w[0]) | ((uint32_t)to16(w[1]) << 16);
+        const uint32_t hi = (uint32_t)to16(w[2]) | ((uint32_t)to16(w[3]) << 16);
         const uint64_t v = (uint64_t)lo | ((uint64_t)hi << 32);
         *reinterpret_cast<uint64_t*>(base + acc_col<MS>(4 * q, lane)) = v;
       }
@@ -648,22 +697,22 @@ __device__ __forceinline__ void store_acc_bf16(const typename AccOf<MS>::T (&acc
   }
 }
 
-template <int BM, int BN, int MS, bool OBF>
+template <int BM, int BN, int MS, bool OBF, bool EPI = false>
 __device__ __forceinline__ void store_tile_c(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                            [TileShape<BM, BN, MS>::TN],
                                              const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
   if constexpr (OBF)
-    store_acc_bf16<BM, BN, MS>(acc, g, m0, n0, smem);
+    store_acc_bf16<BM, BN, MS, EPI>(acc, g, m0, n0, smem);
   else
-    store_acc_f32<BM, BN, MS>(acc, static_cast<float*>(g.C), g.ldc, m0, n0, g.M, g.N);
+    store_acc_f32<BM, BN, MS>(acc, static_cast<float*>(g.C), g.ldc, m0, n0, g.M, g.N, EPI ? &g : nullptr);
 }
 
 // Output of the tile kernel: C in fp32, C in bf16, or (P_k > 1) the fp32
 // partial of the workgroup's K partition.
 enum TileOut : int { OUT_F32 = 0, OUT_BF16 = 1, OUT_PARTIAL = 2 };
 
-template <int BM, int BN, int MS, int OUT, int DEPTH>
-__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
+template <int BM, int BN, int MS, int OUT, int DEPTH, bool EPI>
+__device__ __forceinline__ void tile_kernel(const GemmArgs& g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
@@ -690,7 +739,18 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
   if constexpr (OUT == OUT_PARTIAL)  // this partition's fp32 partial, row-major slice `split`
     store_acc_f32<BM, BN, MS>(acc, g.ws + (size_t)split * (size_t)g.M * (size_t)g.ldw, g.ldw, m0, n0, g.M, g.N);
   else
-    store_tile_c<BM, BN, MS, OUT == OUT_BF16>(acc, g, m0, n0, smem);
+    store_tile_c<BM, BN, MS, OUT == OUT_BF16, EPI>(acc, g, m0, n0, smem);
+}
+
+// The tile kernel, and its form with the AddMM epilogue (a kernel of its own,
+// so that the epilogue's registers never weigh on the plain product).
+template <int BM, int BN, int MS, int OUT, int DEPTH>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
+  tile_kernel<BM, BN, MS, OUT, DEPTH, false>(g);
+}
+template <int BM, int BN, int MS, int OUT, int DEPTH>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_addmm(GemmArgs g) {
+  tile_kernel<BM, BN, MS, OUT, DEPTH, true>(g);
 }
 
 // ------------------------------------------------- persistent tile kernel
@@ -707,7 +767,7 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile(GemmArgs g) {
 constexpr int32_t OOB_OFF = (int32_t)0x80000000u;  // past every tile's range
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;      // raw buffer, 32-bit data
 
-template <int BM, int BN, int MS>
+template <int BM, int BN, int MS, bool EPI>
 __device__ __forceinline__ void store_acc_bf16_fixed(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
                                                                                    [TileShape<BM, BN, MS>::TN],
                                                      const GemmArgs& g, int64_t m0, int64_t n0, char* smem) {
@@ -723,8 +783,14 @@ __device__ __forceinline__ void store_acc_bf16_fixed(const typename AccOf<MS>::T
       uint16_t* base = ct + (wr * S::WTM + i * MS + (lane % MS)) * S::CT_LD + wc * S::WTN + j * MS;
 #pragma unroll
       for (int q = 0; q < S::NA / 4; ++q) {
-        const uint32_t lo = (uint32_t)to16(acc[i][j][4 * q]) | ((uint32_t)to16(acc[i][j][4 * q + 1]) << 16);
-        const uint32_t hi = (uint32_t)to16(acc[i][j][4 * q + 2]) | ((uint32_t)to16(acc[i][j][4 * q + 3]) << 16);
+        float w[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        if (EPI && g.epi) {
+          const int64_t row = m0 + wr * S::WTM + i * MS + (lane % MS);
+          const int64_t col = n0 + wc * S::WTN + j * MS + acc_col<MS>(4 * q, lane);
+          if (row < g.M && col < g.N) epi_apply<true, 4>(g, w, row, col, g.N - col);
+        }
+        const uint32_t lo = (uint32_t)to16(w[0]) | ((uint32_t)to16(w[1]) << 16);
+        const uint32_t hi = (uint32_t)to16(w[2]) | ((uint32_t)to16(w[3]) << 16);
         *reinterpret_cast<uint64_t*>(base + acc_col<MS>(4 * q, lane)) = (uint64_t)lo | ((uint64_t)hi << 32);
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -776,8 +842,8 @@ __device__ __forceinline__ void store_acc_bf16_fixed(const typename AccOf<MS>::T
 // at the end of the iteration: its memory latency is spent under the stores
 // of C. Requires K >= 8 and N >= 8 (the planner offers it only then) and a
 // row pitch of C below 2^23 bytes (the launcher checks it).
-template <int BM, int BN, int MS, bool OBF>
-__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g) {
+template <int BM, int BN, int MS, bool OBF, bool EPI>
+__device__ __forceinline__ void persist_kernel(const GemmArgs& g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
@@ -868,9 +934,9 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g)
     // registers live than those tiles afford: spills, whose reloads wait for
     // every memory operation, cost more than the overlap gains).
     if constexpr (OBF && !(BM == 256 && BN == 256))
-      store_acc_bf16_fixed<BM, BN, MS>(acc, g, m0, n0, smem);
+      store_acc_bf16_fixed<BM, BN, MS, EPI>(acc, g, m0, n0, smem);
     else
-      store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
+      store_tile_c<BM, BN, MS, OBF, EPI>(acc, g, m0, n0, smem);
     if (!more) break;
     __syncthreads();  // every wave is done with LDS (last MFMAs, epilogue reads)
     n_edge = n1 + BN > g.N;
@@ -880,6 +946,15 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g)
     m0 = m1;
     n0 = n1;
   }
+}
+
+template <int BM, int BN, int MS, bool OBF>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp(GemmArgs g) {
+  persist_kernel<BM, BN, MS, OBF, false>(g);
+}
+template <int BM, int BN, int MS, bool OBF>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_pp_addmm(GemmArgs g) {
+  persist_kernel<BM, BN, MS, OBF, true>(g);
 }
 
 // --------------------------------------------------------- grouped kernel
@@ -1029,8 +1104,8 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a
 // tile's slot (workgroup - first workgroup of the tile) as a row-major fp32
 // tile, summed later by k_sk_fixup. The remaining tiles are processed whole,
 // data-parallel, by the grid.
-template <int BM, int BN, int MS, bool OBF>
-__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g) {
+template <int BM, int BN, int MS, bool OBF, bool EPI>
+__device__ __forceinline__ void streamk_kernel(const GemmArgs& g) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
@@ -1060,7 +1135,7 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g)
     const int first_wg = (int)(t0 / g.iters_per_wg);
     const int last_wg = (int)min((int64_t)g.grid - 1, (t0 + ipt - 1) / g.iters_per_wg);
     if (first_wg == last_wg) {
-      store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
+      store_tile_c<BM, BN, MS, OBF, EPI>(acc, g, m0, n0, smem);
     } else {
       float* slot = g.ws + ((size_t)tile * g.ws_pk + (blockIdx.x - first_wg)) * tile_floats;
       store_acc_f32<BM, BN, MS>(acc, slot, BN, 0, 0, BM, BN);
@@ -1079,8 +1154,17 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g)
       for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
     __syncthreads();
     tile_mainloop<BM, BN, MS, streamk_depth(BM, BN)>(g, m0, n0, 0, ipt, acc, smem);
-    store_tile_c<BM, BN, MS, OBF>(acc, g, m0, n0, smem);
+    store_tile_c<BM, BN, MS, OBF, EPI>(acc, g, m0, n0, smem);
   }
+}
+
+template <int BM, int BN, int MS, bool OBF>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk(GemmArgs g) {
+  streamk_kernel<BM, BN, MS, OBF, false>(g);
+}
+template <int BM, int BN, int MS, bool OBF>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_streamk_addmm(GemmArgs g) {
+  streamk_kernel<BM, BN, MS, OBF, true>(g);
 }
 
 // Sums the pieces of every split stream-K tile in workgroup order and writes
@@ -1112,7 +1196,7 @@ __global__ __launch_bounds__(256) void k_sk_fixup(GemmArgs g, int BM, int BN) {
       s1 += *reinterpret_cast<const f32x4*>(src + p * tile_floats + 4);
     }
     const float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
-    store_c8<OBF>(g.C, gr * g.ldc + gc, v, g.N - gc);
+    store_out8<OBF>(g, gr, gc, v, g.N - gc);
   }
 }
 
@@ -1161,7 +1245,7 @@ __global__ __launch_bounds__(256) void k_reduce(GemmArgs g, int lg) {
   }
   if (!live || j != 0) return;
   const float v[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
-  store_c8<OBF>(g.C, row * g.ldc + c0, v, g.N - c0);
+  store_out8<OBF>(g, row, c0, v, g.N - c0);
 }
 
 // -------------------------------------------------------- skinny-M kernel
@@ -1292,7 +1376,7 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) o[j] = acc[mt][j][r];
         if (g.pk == 1)
-          store_c8<OBF>(g.C, row * g.ldc + col0, o, nvalid);
+          store_out8<OBF>(g, row, col0, o, nvalid);
         else
           store_c8<false>(g.ws + (size_t)split * (size_t)M * (size_t)g.ldw, row * g.ldw + col0, o, nvalid);
       }
@@ -1413,7 +1497,7 @@ __global__ __launch_bounds__(256) void k_skinny_n(GemmArgs g) {
         const int64_t row = rbase + rb * 16 + r;
         if (row < M && col < N) {
           if (g.pk == 1)
-            store_c<OBF>(g.C, row * g.ldc + col, acc[rb][nt][r]);
+            store_out<OBF>(g, row, col, acc[rb][nt][r]);
           else
             part[row * g.ldw + col] = acc[rb][nt][r];
         }
@@ -1475,7 +1559,7 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[j] = __builtin_fmaf(a, b[k][j], acc[j]);
       }
-      if (rb + r < rend) store_c8<OBF>(g.C, (rb + r) * g.ldc + c0, acc, N - c0);
+      if (rb + r < rend) store_out8<OBF>(g, rb + r, c0, acc, N - c0);
     }
   }
 }
@@ -1608,12 +1692,17 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int c = (wave & 1) * 32 + 8 * q + 4 * (lane >> 5);
+      float w[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+      if constexpr (OUT != OUT_PARTIAL) {
+        const int64_t gr = (int64_t)tm * 64 + r, gc = (int64_t)tn * 64 + c;
+        if (g.epi && gr < M && gc < N) epi_apply<OUT == OUT_BF16, 4>(g, w, gr, gc, N - gc);
+      }
       if constexpr (OUT == OUT_BF16) {
-        const uint32_t lo = (uint32_t)to16(acc[4 * q]) | ((uint32_t)to16(acc[4 * q + 1]) << 16);
-        const uint32_t hi = (uint32_t)to16(acc[4 * q + 2]) | ((uint32_t)to16(acc[4 * q + 3]) << 16);
+        const uint32_t lo = (uint32_t)to16(w[0]) | ((uint32_t)to16(w[1]) << 16);
+        const uint32_t hi = (uint32_t)to16(w[2]) | ((uint32_t)to16(w[3]) << 16);
         *reinterpret_cast<uint64_t*>(ct + r * LD + c) = (uint64_t)lo | ((uint64_t)hi << 32);
       } else {
-        const f32x4 v = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+        const f32x4 v = {w[0], w[1], w[2], w[3]};
         *reinterpret_cast<f32x4*>(ct + r * LD + c) = v;
       }
     }
@@ -1645,7 +1734,9 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int64_t col = n0 + 8 * q + 4 * (lane >> 5);
-    const float v[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+    float v[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+    if constexpr (OUT != OUT_PARTIAL)
+      if (g.epi && col < N) epi_apply<OUT == OUT_BF16, 4>(g, v, row, col, N - col);
     if (col + 4 <= N) {
       if constexpr (OUT == OUT_PARTIAL) {
         __builtin_memcpy(part + row * g.ldw + col, v, 16);
@@ -1711,11 +1802,22 @@ hipError_t launch_reduce(const GemmArgs& g, hipStream_t st, bool obf) {
   return hipGetLastError();
 }
 
+// whole-K tiles with the AddMM epilogue
+template <int BM, int BN, int MS, int D>
+void launch_tile_addmm(dim3 grid, dim3 block, const GemmArgs& g, hipStream_t st, bool obf) {
+  if (obf)
+    hipLaunchKernelGGL((k_tile_addmm<BM, BN, MS, OUT_BF16, D>), grid, block, 0, st, g);
+  else
+    hipLaunchKernelGGL((k_tile_addmm<BM, BN, MS, OUT_F32, D>), grid, block, 0, st, g);
+}
+
 template <int BM, int BN, int MS, int D>
 hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, p.grid_y), block(TileShape<BM, BN, MS>::NT);
   if (p.pk > 1)
     hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_PARTIAL, D>), grid, block, 0, st, g);
+  else if (g.epi)
+    launch_tile_addmm<BM, BN, MS, D>(grid, block, g, st, obf);
   else if (obf)
     hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_BF16, D>), grid, block, 0, st, g);
   else
@@ -1727,7 +1829,11 @@ hipError_t launch_tile(const Plan& p, const GemmArgs& g, hipStream_t st, bool ob
 template <int BM, int BN, int MS>
 hipError_t launch_streamk(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, 1), block(TileShape<BM, BN, MS>::NT), fblock(256);
-  if (obf)
+  if (g.epi && obf)
+    hipLaunchKernelGGL((k_streamk_addmm<BM, BN, MS, true>), grid, block, 0, st, g);
+  else if (g.epi)
+    hipLaunchKernelGGL((k_streamk_addmm<BM, BN, MS, false>), grid, block, 0, st, g);
+  else if (obf)
     hipLaunchKernelGGL((k_streamk<BM, BN, MS, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_streamk<BM, BN, MS, false>), grid, block, 0, st, g);
@@ -1794,14 +1900,20 @@ hipError_t launch_persist(const Plan& p, const GemmArgs& g, hipStream_t st, bool
   if (g.ldc * (obf ? 2 : 4) >= (1LL << 23)) {
     static_assert(kTileCfg[0].depth == 1, "the persistent kernels are the depth-1 tile kernels");
     const dim3 grid(p.pm * p.pn), block(TileShape<BM, BN, MS>::NT);
-    if (obf)
+    if (g.epi)
+      launch_tile_addmm<BM, BN, MS, 1>(grid, block, g, st, obf);
+    else if (obf)
       hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_BF16, 1>), grid, block, 0, st, g);
     else
       hipLaunchKernelGGL((k_tile<BM, BN, MS, OUT_F32, 1>), grid, block, 0, st, g);
     return hipGetLastError();
   }
   const dim3 grid(p.grid_x), block(TileShape<BM, BN, MS>::NT);
-  if (obf)
+  if (g.epi && obf)
+    hipLaunchKernelGGL((k_tile_pp_addmm<BM, BN, MS, true>), grid, block, 0, st, g);
+  else if (g.epi)
+    hipLaunchKernelGGL((k_tile_pp_addmm<BM, BN, MS, false>), grid, block, 0, st, g);
+  else if (obf)
     hipLaunchKernelGGL((k_tile_pp<BM, BN, MS, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_tile_pp<BM, BN, MS, false>), grid, block, 0, st, g);

@@ -56,6 +56,16 @@ class Out:
             self.dev = t.from_numpy(self.host.view(np.int16).copy()).to("cuda")
             self.addr = self.dev.data_ptr() + 2 * ldc
 
+    def fill(self, vals):
+        """Sets the M x N interior (fp32 values, or 16-bit bit patterns) and
+        keeps the canaries around it."""
+        host = self.host.copy()
+        w = host.reshape(self.M + 2, self.ldc)
+        w[1:self.M + 1, :self.N] = vals
+        t = torch()
+        src = host if fp32_out(self.dtype) else host.view(np.int16)
+        self.dev.copy_(t.from_numpy(src.copy()).to("cuda"))
+
     def read(self):
         """(values as fp64 M x N, canaries intact?)"""
         raw = self.dev.cpu().numpy()
@@ -86,6 +96,30 @@ def run(plan, A, B, M, N, K, dtype, lda=None, ldb=None, ldc=None, a_off=0, b_off
     t.cuda.synchronize()
     vals, ok = out.read()
     del Ad, Bd
+    return vals, ok
+
+
+def run_addmm(plan, A, B, M, N, K, dtype, c_old, alpha, beta, bias=None, lda=None, ldb=None, ldc=None,
+              a_off=0, b_off=0, stream=0):
+    """One adaptcore_addmm through the C ABI with C holding c_old (fp32
+    values or 16-bit patterns) before the call; bias is None or N fp32
+    values. Returns (C values, canaries ok)."""
+    t = torch()
+    lda = max(K, 1) if lda is None else lda
+    ldb = max(N, 1) if ldb is None else ldb
+    ldc = max(N, 1) if ldc is None else ldc
+    Ad, a = to_device(A, lda, a_off)
+    Bd, b = to_device(B, ldb, b_off)
+    out = Out(M, N, ldc, dtype)
+    out.fill(c_old)
+    bd = None
+    if bias is not None:
+        bd = t.from_numpy(np.ascontiguousarray(bias, np.float32)).to("cuda")
+    ac.adaptcore_addmm(plan, a, lda, b, ldb, out.addr, ldc, alpha, beta, bd.data_ptr() if bd is not None else 0,
+                       stream)
+    t.cuda.synchronize()
+    vals, ok = out.read()
+    del Ad, Bd, bd
     return vals, ok
 
 

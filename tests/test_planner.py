@@ -159,6 +159,30 @@ def test_argument_validation():
         ac.adaptcore_matmul(0, 0x1000, 16, 0x2000, 32, 0x3000, 32)
 
 
+def test_addmm_argument_validation():
+    h = ac.adaptcore_plan(64, 32, 16)
+    good = (0x1000, 16, 0x2000, 32, 0x3000, 32)
+    # non-finite scalars and a misaligned bias are rejected before any GPU work
+    for alpha, beta, bias in [(float("nan"), 1.0, 0), (1.0, float("inf"), 0), (1.0, 1.0, 0x4002)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_addmm(h, *good, alpha, beta, bias)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    # the plain product's checks apply unchanged
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_addmm(h, 0x1000, 15, 0x2000, 32, 0x3000, 32, 1.0, 1.0, 0)
+    assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_addmm(h, 0x1000, 1 << 23, 0x2000, 32, 0x3000, 32, 1.0, 1.0, 0)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    # grouped and batched plans only run through their own entry points
+    for hp in (ac.adaptcore_grouped_plan(64, 4, 32, 16), ac.adaptcore_batched_plan(4, 16, 32, 16)):
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_addmm(hp, *good, 1.0, 0.0, 0)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    # an empty output launches nothing and succeeds anywhere
+    ac.adaptcore_addmm(ac.adaptcore_plan(0, 5, 7), 0, 7, 0x2000, 5, 0x3000, 5, 2.0, 0.5, 0x4000)
+
+
 def test_candidates_are_legal_and_keys_round_trip():
     hw = ac.adaptcore_get_hw()
     for s in [(1, 4096, 4096), (17, 300, 65536), (512, 512, 512), (3000, 5, 700), (64, 64, 65536),

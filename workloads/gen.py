@@ -65,6 +65,12 @@ def int_bf16(rows, cols, seed, lim=4):
     return bf16_bits(rng.integers(-lim, lim + 1, size=(rows, cols)).astype(np.float32))
 
 
+def uniform_f32(rows, cols, seed, lo=-1.0, hi=1.0):
+    """fp32 values (an AddMM input C or bias row)."""
+    rng = np.random.default_rng(seed)
+    return rng.uniform(lo, hi, size=(rows, cols)).astype(np.float32)
+
+
 def operands(M, N, K, seed, dist="uniform"):
     """A (M x K) and B (K x N) bf16 bit patterns for one shape ("uniform_f16":
     fp16 bit patterns of the same distribution)."""
