@@ -28,6 +28,11 @@ each call bracketed by its own events: includes the event overhead), a
 secondary fraction against max(t_floor, measured empty-kernel launch floor),
 plan-miss and cached-lookup costs, the roofline of the dominant kernel, and
 the oracle timed on the host cores (cpu_baseline).
+
+Other workloads (one JSON line each): single, skinny, splitk, mfma (fixed
+shape sets, same timing); moe (the routed grouped product against per-expert
+calls); ablation (the paper's module-ablation and CU-scaling shapes);
+layouts (row-major against column-major operands, i.e. the prologue copy).
 """
 import argparse
 import hashlib
@@ -286,10 +291,14 @@ def time_plan(ac, torch, plan, M, N, K, dtype, copies=8, target_s=250e-6, steps=
     B = torch.empty(nb * K * N, dtype=torch.bfloat16, device=dev).uniform_(-1, 1)
     C = torch.empty(nc * M * N, dtype=torch.float32 if cb == 4 else torch.bfloat16, device=dev)
     cs = torch.cuda.Stream()
-    ac.adaptcore_reserve_workspace(cs.cuda_stream, max(ac.adaptcore_plan_info(plan)["workspace_bytes"], 1))
+    info = ac.adaptcore_plan_info(plan)
+    ac.adaptcore_reserve_workspace(cs.cuda_stream, max(info["workspace_bytes"], 1))
+    # column-major operands are stored K x M (A) and N x K (B)
+    lda = M if info["layouts"] & ac.AC_LAYOUT_A_COL else K
+    ldb = K if info["layouts"] & ac.AC_LAYOUT_B_COL else N
 
     def call(r):
-        ac.adaptcore_matmul(plan, A.data_ptr() + (r % na) * fa, K, B.data_ptr() + (r % nb) * fb, N,
+        ac.adaptcore_matmul(plan, A.data_ptr() + (r % na) * fa, lda, B.data_ptr() + (r % nb) * fb, ldb,
                             C.data_ptr() + (r % nc) * fc, N, cs.cuda_stream)
     for r in range(3):
         call(r)
@@ -417,12 +426,46 @@ def ablation_main(args):
     print(json.dumps(line), flush=True)
 
 
+def layouts_main(args):
+    """Column-major operands: each shape planned and timed with row-major A
+    and B and with each transposed layout (the prologue copies the
+    column-major operand into the workspace, then the row-major plan runs);
+    the extra time over row-major is the prologue's, reported with the rate
+    at which it moves the copied bytes (read + write)."""
+    import torch
+    import paper_2608_10803_amd as ac
+    bf = ac.AC_BF16_BF16OUT
+    rows = []
+    for (M, N, K) in [(4096, 4096, 4096), (2048, 14336, 4096), (8192, 8192, 1024), (16, 4096, 14336),
+                      (512, 512, 512)]:
+        t0 = None
+        for lay in (0, 1, 2, 3):
+            plan = ac.adaptcore_plan(M, N, K, bf, lay)
+            t = time_plan(ac, torch, plan, M, N, K, bf)
+            if lay == 0:
+                t0 = t
+            moved = 4 * ((M * K if lay & 1 else 0) + (K * N if lay & 2 else 0))
+            r = {"shape": [M, N, K], "layouts": lay, "us": round(t * 1e6, 2), "vs_row_major": round(t / t0, 3),
+                 "predicted_us": round(ac.adaptcore_plan_info(plan)["predicted_s"] * 1e6, 2),
+                 "kernels": ac.adaptcore_plan_kernels(plan)}
+            if lay:
+                r["prologue_us"] = round((t - t0) * 1e6, 2)
+                r["prologue_gbps"] = round(moved / max(t - t0, 1e-9) / 1e9, 1)
+            rows.append(r)
+            print("layouts", r, file=sys.stderr, flush=True)
+    line = {"metric": "time per call by operand layout (prologue copy of column-major operands)", "value": None,
+            "unit": "us", "n_gpus": 1, "dtype": "bf16", "data": "synthetic", "higher_is_better": False,
+            "config": {"workload": "5 shapes x 4 layouts, bf16 output"}, "rows": rows}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe", "ablation", "mfma"])
+    ap.add_argument("--workload", default="sweep", choices=["sweep", "single", "skinny", "splitk", "moe", "ablation", "mfma",
+                                                           "layouts"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-isolated", action="store_true")
     ap.add_argument("--per-shape", default=None, help="write per-shape results to this JSON file")
@@ -450,6 +493,8 @@ def main():
         return moe_main(args)
     if args.workload == "ablation":
         return ablation_main(args)
+    if args.workload == "layouts":
+        return layouts_main(args)
     dev = torch.device("cuda")
     if args.copy_ref:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)

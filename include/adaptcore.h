@@ -55,8 +55,16 @@ typedef enum {
   AC_F16_F16OUT = 3    /* fp16 inputs, C is fp16, rounded to nearest even */
 } adaptcore_dtype;
 
-/* Operand layouts. This build provides row-major A and row-major B. */
-enum { AC_LAYOUT_ROW_ROW = 0 };
+/* Operand layouts of plain products (adaptcore_plan, adaptcore_matmul,
+ * adaptcore_addmm), a bit set: AC_LAYOUT_A_COL = A stored column-major
+ * (element (i, k) at A[i + k * lda], lda >= M), AC_LAYOUT_B_COL = B stored
+ * column-major (element (k, j) at B[k + j * ldb], ldb >= K); clear bits mean
+ * row-major (A[i * lda + k], lda >= K; B[k * ldb + j], ldb >= N). The matrix
+ * C is always row-major. A column-major operand is copied into a row-major
+ * copy in the plan's workspace by a prologue kernel before the main kernel
+ * (the copy prologue of the paper's padding module, priced as T_pro in
+ * Eq. 7). Grouped and batched products take row-major operands only. */
+enum { AC_LAYOUT_ROW_ROW = 0, AC_LAYOUT_A_COL = 1, AC_LAYOUT_B_COL = 2, AC_LAYOUT_COL_COL = 3 };
 
 /* Templates of the 2D tiling taxonomy (Section 4.2). */
 typedef enum {
@@ -97,7 +105,8 @@ typedef struct {
   int32_t swizzle;      /* 1 = XCD-aware grouped tile order (ShuffleK analogue) */
   int32_t n_candidates; /* legal candidates the model compared */
   double predicted_s;   /* model latency of the selected configuration, seconds */
-  int64_t workspace_bytes; /* fp32 partial tiles + counters needed per stream */
+  int64_t workspace_bytes; /* per stream: fp32 partials, then row-major copies of column-major
+                              operands */
   int64_t groups;       /* grouped plans: number of groups (M is the row capacity); batched
                            plans: batch count (M, N, K of every batch); else 0 */
 } adaptcore_plan_desc_t;
@@ -186,11 +195,14 @@ const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, 
 
 /* Runs a plan: C = A * B, asynchronously on `stream` (a hipStream_t; NULL is
  * the null stream). Validates the leading dimensions against the plan's
- * shape (lda >= K, ldb >= N, ldc >= N, all >= 1: AC_ERR_INVALID_VALUE;
- * lda or ldb >= AC_MAX_LD: AC_ERR_UNSUPPORTED) and the pointer alignment
- * (A, B: 2 bytes; C: its element size). M == 0 or N == 0: nothing is
- * launched. K == 0: C is set to zero.
- * Split-K plans use a workspace owned by the library for this (device,
+ * shape and layouts (row-major A: lda >= K, column-major A: lda >= M;
+ * row-major B: ldb >= N, column-major B: ldb >= K; ldc >= N; all >= 1:
+ * AC_ERR_INVALID_VALUE; a row-major lda or ldb >= AC_MAX_LD, or K or N of a
+ * copied operand with its row padded to 8 reaching AC_MAX_LD:
+ * AC_ERR_UNSUPPORTED) and the pointer alignment (A, B: 2 bytes; C: its
+ * element size). M == 0 or N == 0: nothing is launched. K == 0: C is set to
+ * zero.
+ * Split-K plans and plans with a column-major operand use a workspace owned by the library for this (device,
  * stream); it is allocated on the stream's first use (outside any stream
  * capture: under capture a missing workspace gives AC_ERR_NOT_INITIALIZED)
  * and grows monotonically. Concurrent calls on ONE stream are ordered by the

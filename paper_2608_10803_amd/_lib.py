@@ -26,6 +26,9 @@ AC_BF16_BF16OUT = 1
 AC_F16_F32OUT = 2
 AC_F16_F16OUT = 3
 AC_LAYOUT_ROW_ROW = 0
+AC_LAYOUT_A_COL = 1  # A stored column-major (lda >= M)
+AC_LAYOUT_B_COL = 2  # B stored column-major (ldb >= K)
+AC_LAYOUT_COL_COL = 3
 (AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
  AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED) = range(9)
 
@@ -331,8 +334,26 @@ def adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain):
     return lib().adaptcore_schedule(kind, Q, L, t_m, t_p, t_drain)
 
 
+def _operand(t, rows, cols):
+    """(column-major?, leading dimension) of a 2-D operand view: rows
+    contiguous (stride(1) == 1) or columns contiguous (stride(0) == 1)."""
+    if t.dim() != 2 or not t.is_cuda:
+        raise ValueError("operands must be 2-D GPU tensors")
+    if cols <= 1 or t.stride(1) == 1:
+        col, ld, need = False, (t.stride(0) if rows > 1 else cols), cols
+    elif rows <= 1 or t.stride(0) == 1:
+        col, ld, need = True, (t.stride(1) if cols > 1 else rows), rows
+    else:
+        raise ValueError("operands must have contiguous rows or contiguous columns")
+    if ld < need:
+        raise ValueError("overlapping operand view")
+    return col, max(ld, 1)
+
+
 def _marshal_tensors(A, B, C):
-    """(M, N, K, dtype code) of a tensor product, after the checks."""
+    """(M, N, K, dtype code, layouts, lda, ldb, ldc) of a tensor product,
+    after the checks. A and B may be transposed views (contiguous columns);
+    C must have contiguous rows."""
     import torch
     M, K = A.shape
     K2, N = B.shape
@@ -347,25 +368,27 @@ def _marshal_tensors(A, B, C):
         dt = AC_F16_F16OUT if f16 else AC_BF16_BF16OUT
     else:
         raise TypeError("C must be float32 or the input type")
-    for t in (A, B, C):
-        if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1) or not t.is_cuda:
-            raise ValueError("operands must be 2-D GPU tensors with unit column stride")
-    return M, N, K, dt
+    a_col, lda = _operand(A, M, K)
+    b_col, ldb = _operand(B, K, N)
+    if C.dim() != 2 or not C.is_cuda or (N > 1 and C.stride(1) != 1):
+        raise ValueError("C must be a 2-D GPU tensor with contiguous rows")
+    layouts = (AC_LAYOUT_A_COL if a_col else 0) | (AC_LAYOUT_B_COL if b_col else 0)
+    return M, N, K, dt, layouts, lda, ldb, max(C.stride(0), N, 1)
 
 
 def matmul_tensors(A, B, C, stream=None, plan=None):
-    """C = A @ B for torch tensors on the GPU (2-D, row-major rows: stride(1)
-    == 1). A and B are both torch.bfloat16 or both torch.float16, C
-    torch.float32 or the input type.
+    """C = A @ B for torch tensors on the GPU: 2-D, A and B with contiguous
+    rows or contiguous columns (a transposed view selects the column-major
+    layout), C with contiguous rows. A and B are both torch.bfloat16 or both
+    torch.float16, C torch.float32 or the input type.
     Marshals pointers and leading dimensions; all arithmetic runs in the
     library's kernels."""
     import torch
-    M, N, K, dt = _marshal_tensors(A, B, C)
+    M, N, K, dt, layouts, lda, ldb, ldc = _marshal_tensors(A, B, C)
     if plan is None:
-        plan = adaptcore_plan(M, N, K, dt, AC_LAYOUT_ROW_ROW)
+        plan = adaptcore_plan(M, N, K, dt, layouts)
     s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
-    adaptcore_matmul(plan, A.data_ptr(), max(A.stride(0), 1), B.data_ptr(), max(B.stride(0), 1),
-                     C.data_ptr(), max(C.stride(0), 1), s)
+    adaptcore_matmul(plan, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, s)
     return C
 
 
@@ -374,15 +397,14 @@ def addmm_tensors(A, B, C, alpha=1.0, beta=0.0, bias=None, stream=None, plan=Non
     as in matmul_tensors; bias is None or a contiguous float32 GPU tensor of
     N elements."""
     import torch
-    M, N, K, dt = _marshal_tensors(A, B, C)
+    M, N, K, dt, layouts, lda, ldb, ldc = _marshal_tensors(A, B, C)
     bp = 0
     if bias is not None:
         if bias.dtype != torch.float32 or bias.numel() != N or not bias.is_cuda or not bias.is_contiguous():
             raise ValueError("bias must be a contiguous float32 GPU tensor of N elements")
         bp = bias.data_ptr()
     if plan is None:
-        plan = adaptcore_plan(M, N, K, dt, AC_LAYOUT_ROW_ROW)
+        plan = adaptcore_plan(M, N, K, dt, layouts)
     s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
-    adaptcore_addmm(plan, A.data_ptr(), max(A.stride(0), 1), B.data_ptr(), max(B.stride(0), 1),
-                    C.data_ptr(), max(C.stride(0), 1), float(alpha), float(beta), bp, s)
+    adaptcore_addmm(plan, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, float(alpha), float(beta), bp, s)
     return C

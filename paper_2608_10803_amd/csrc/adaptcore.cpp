@@ -128,11 +128,18 @@ bool valid_args(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts
     *st = fail(AC_ERR_UNSUPPORTED, "dtype not provided by this build (bf16 or fp16 inputs, fp32 or 16-bit output)");
     return false;
   }
-  if (layouts != AC_LAYOUT_ROW_ROW) {
-    *st = fail(AC_ERR_UNSUPPORTED, "layout not provided by this build (row-major A and B)");
+  if (layouts > AC_LAYOUT_COL_COL) {
+    *st = fail(AC_ERR_UNSUPPORTED, "unknown layout bits");
     return false;
   }
   return true;
+}
+
+// Grouped and batched products read their operands row-major.
+bool row_major_only(uint32_t layouts) {
+  if (layouts == AC_LAYOUT_ROW_ROW) return true;
+  fail(AC_ERR_UNSUPPORTED, "grouped and batched products take row-major A and B only");
+  return false;
 }
 
 adaptcore_plan_s* plan_miss(const ac::Shape& s) {
@@ -319,11 +326,15 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
     return fail(AC_ERR_INVALID_VALUE, "batched plan: run it with adaptcore_batched_matmul");
   const int64_t M = p.s.M, N = p.s.N, K = p.s.K;
   if (M == 0 || N == 0) return AC_OK;
-  if (lda < std::max<int64_t>(1, K) || ldb < std::max<int64_t>(1, N) || ldc < std::max<int64_t>(1, N))
-    return fail(AC_ERR_INVALID_VALUE, "leading dimension smaller than the row length");
-  // the kernels address A and B tiles with 32-bit byte offsets from a row base
-  if (lda >= AC_MAX_LD || ldb >= AC_MAX_LD)
-    return fail(AC_ERR_UNSUPPORTED, "lda and ldb must be below 2^23 elements");
+  const bool a_col = (p.s.layouts & AC_LAYOUT_A_COL) != 0, b_col = (p.s.layouts & AC_LAYOUT_B_COL) != 0;
+  if (lda < std::max<int64_t>(1, a_col ? M : K) || ldb < std::max<int64_t>(1, b_col ? K : N) ||
+      ldc < std::max<int64_t>(1, N))
+    return fail(AC_ERR_INVALID_VALUE, "leading dimension smaller than the stored row or column");
+  // the kernels address A and B tiles with 32-bit byte offsets from a row
+  // base (of the caller's operand, or of the row-major copy of a column-major
+  // one, whose rows are padded to a multiple of 8)
+  if ((a_col ? (K + 7) / 8 * 8 : lda) >= AC_MAX_LD || (b_col ? (N + 7) / 8 * 8 : ldb) >= AC_MAX_LD)
+    return fail(AC_ERR_UNSUPPORTED, "row pitch of A or B must be below 2^23 elements");
   if (!C || (K > 0 && (!A || !B))) return fail(AC_ERR_INVALID_VALUE, "null matrix pointer");
   const int cbytes = ac::dtype_out_bytes(p.s.dtype);
   if (((uintptr_t)A & 1) || ((uintptr_t)B & 1) || ((uintptr_t)C & (cbytes - 1)))
@@ -362,6 +373,22 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
     st = get_workspace(s, p.ws_bytes, &w);
     if (st != AC_OK) return st;
     g.ws = reinterpret_cast<float*>(w.ptr);
+    // prologue: row-major copies of column-major operands (A: M x K, B: K x N)
+    char* base = static_cast<char*>(w.ptr);
+    if (p.ws_a_off >= 0) {
+      uint16_t* a2 = reinterpret_cast<uint16_t*>(base + p.ws_a_off);
+      const hipError_t e = ac::launch_transpose16(g.A, lda, K, M, a2, (K + 7) / 8 * 8, s);
+      if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+      g.A = a2;
+      g.lda = (K + 7) / 8 * 8;
+    }
+    if (p.ws_b_off >= 0) {
+      uint16_t* b2 = reinterpret_cast<uint16_t*>(base + p.ws_b_off);
+      const hipError_t e = ac::launch_transpose16(g.B, ldb, N, K, b2, (N + 7) / 8 * 8, s);
+      if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+      g.B = b2;
+      g.ldb = (N + 7) / 8 * 8;
+    }
   }
   const hipError_t e = ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(p, g, s) : ac::launch_plan(p, g, s);
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
@@ -389,6 +416,7 @@ const adaptcore_plan_t* adaptcore_grouped_plan(int64_t rows, int64_t groups, int
                                                uint32_t layouts) {
   adaptcore_status st;
   if (!valid_args(rows, N, K, dtype, layouts, &st)) return nullptr;
+  if (!row_major_only(layouts)) return nullptr;
   if (groups < 0 || groups > (1LL << 20)) {
     fail(AC_ERR_INVALID_VALUE, "groups must be in [0, 2^20]");
     return nullptr;
@@ -423,6 +451,7 @@ const adaptcore_plan_t* adaptcore_grouped_plan_variant(int64_t rows, int64_t gro
                                                        int32_t dtype, uint32_t layouts, uint64_t variant_key) {
   adaptcore_status st;
   if (!valid_args(rows, N, K, dtype, layouts, &st)) return nullptr;
+  if (!row_major_only(layouts)) return nullptr;
   if (groups < 0 || groups > (1LL << 20)) {
     fail(AC_ERR_INVALID_VALUE, "groups must be in [0, 2^20]");
     return nullptr;
@@ -498,6 +527,7 @@ const adaptcore_plan_t* adaptcore_batched_plan(int64_t batch, int64_t M, int64_t
                                                uint32_t layouts) {
   adaptcore_status st;
   if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  if (!row_major_only(layouts)) return nullptr;
   if (batch < 0 || batch > (1LL << 24)) {
     fail(AC_ERR_INVALID_VALUE, "batch must be in [0, 2^24]");
     return nullptr;
@@ -532,6 +562,7 @@ const adaptcore_plan_t* adaptcore_batched_plan_variant(int64_t batch, int64_t M,
                                                        int32_t dtype, uint32_t layouts, uint64_t variant_key) {
   adaptcore_status st;
   if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  if (!row_major_only(layouts)) return nullptr;
   if (batch < 0 || batch > (1LL << 24)) {
     fail(AC_ERR_INVALID_VALUE, "batch must be in [0, 2^24]");
     return nullptr;

@@ -1761,6 +1761,69 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
   }
 }
 
+// ------------------------------------------------------ layout prologue
+#if !AC_INPUT_F16
+// The row-major copy of a column-major operand: dst (cols x rows, pitch
+// ld_dst) = transpose of src (rows x cols, pitch ld_src). 64 x 64 tiles go
+// through LDS: a thread reads runs of 8 elements of a source row with one
+// 16-byte load (any 2-byte alignment; element loads at the end of a row),
+// eight threads cover a 128-byte run of a row; a thread writes one 16-byte
+// aligned run of 8 elements of a copy row (ld_dst is a multiple of 8 and dst
+// is 16-byte aligned); elements past `rows` in the last run of a copy row
+// are written as zero (the row pad). A grid-stride loop over the tiles.
+constexpr int TR_T = 64;
+__global__ __launch_bounds__(256) void k_transpose16(const uint16_t* __restrict__ src, int64_t ld_src,
+                                                      uint16_t* __restrict__ dst, int64_t ld_dst, int64_t rows,
+                                                      int64_t cols, int64_t tiles_c, int64_t tiles) {
+  // rows of 66 elements (132 bytes): 4-byte aligned runs, and the column
+  // reads of the write phase spread over the banks
+  __shared__ uint32_t t32[TR_T * (TR_T + 2) / 2];
+  const int tid = threadIdx.x;
+  for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const int64_t r0 = (tile / tiles_c) * TR_T, c0 = (tile % tiles_c) * TR_T;
+    __syncthreads();  // the previous tile's reads of t are done
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int e = tid + 256 * j;
+      const int r = e >> 3, v8 = (e & 7) * 8;  // source row r0 + r, elements c0 + v8 .. + 7
+      const int64_t gr = r0 + r, gc = c0 + v8;
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (gr < rows && gc < cols) {
+        const uint16_t* p = src + gr * ld_src + gc;
+        if (gc + 8 <= cols) {
+          w = load16(p);
+        } else {
+#pragma unroll
+          for (int x = 0; x < 8; ++x)
+            if (gc + x < cols) w[x >> 1] |= (uint32_t)p[x] << (16 * (x & 1));
+        }
+      }
+      uint32_t* d = t32 + (r * (TR_T + 2) + v8) / 2;
+#pragma unroll
+      for (int x = 0; x < 4; ++x) d[x] = w[x];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int e = tid + 256 * j;
+      const int cc = e >> 3, q = e & 7;  // copy row c0 + cc, elements r0 + 8q .. r0 + 8q + 7
+      const int64_t drow = c0 + cc, dcol = r0 + 8 * q;
+      if (drow >= cols || dcol >= rows) continue;
+      // element (row, cc) of the tile is half (cc & 1) of word (row * 66 + cc) / 2
+      const int sh = 16 * (cc & 1);
+      u32x4 w;
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const uint32_t lo = (t32[((8 * q + 2 * x) * (TR_T + 2) + cc) >> 1] >> sh) & 0xFFFFu;
+        const uint32_t hi = (t32[((8 * q + 2 * x + 1) * (TR_T + 2) + cc) >> 1] >> sh) & 0xFFFFu;
+        w[x] = lo | (hi << 16);
+      }
+      *reinterpret_cast<u32x4*>(dst + drow * ld_dst + dcol) = w;
+    }
+  }
+}
+#endif
+
 #if AC_INPUT_F16
 }  // namespace f16
 #endif
@@ -2118,6 +2181,19 @@ hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st
     return hipErrorInvalidValue;
   return kGroupedFns[p.cfg](p, a, st, dtype_out16(p.s.dtype));
 }
+
+#if !AC_INPUT_F16
+hipError_t launch_transpose16(const uint16_t* src, int64_t ld_src, int64_t rows, int64_t cols, uint16_t* dst,
+                              int64_t ld_dst, hipStream_t st) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (ld_src < cols || ld_dst < rows || (ld_dst & 7) != 0 || ((uintptr_t)dst & 15) != 0) return hipErrorInvalidValue;
+  const int64_t tiles_c = (cols + TR_T - 1) / TR_T;
+  const int64_t tiles = (rows + TR_T - 1) / TR_T * tiles_c;
+  const dim3 grid((unsigned)(tiles < 4096 ? tiles : 4096)), block(256);
+  hipLaunchKernelGGL(k_transpose16, grid, block, 0, st, src, ld_src, dst, ld_dst, rows, cols, tiles_c, tiles);
+  return hipGetLastError();
+}
+#endif
 
 void query_occupancy() {
   for (int i = 0; i < N_TILE_CFG; ++i) set_runtime_occupancy(FAM_TILE, i, kTileOcc[i]());

@@ -489,11 +489,33 @@ bool build_streamk(const Ctx& c, int cfg, Plan* p, Work* w) {
 
 const int kSplits[] = {2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32, 40, 48, 64, 80, 96, 128, 160, 192, 256, 384, 512, 768, 1024};
 
+// Prologue of a plan with column-major operands: each one is copied into a
+// row-major copy in the workspace (after the partials) by a transposing
+// kernel, read and written once at the HBM rate: T_pro of Eq. 7, the same for
+// every configuration of the shape. Rows of the copies are padded to a
+// multiple of 8 elements (16-byte aligned rows for the main kernels).
+void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
+  p->ws_a_off = p->ws_b_off = -1;
+  p->t_pro = 0;
+  if (s.M == 0 || s.N == 0 || s.K == 0) return;
+  auto copy = [&](int64_t rows, int64_t cols, int64_t* off) {
+    *off = (p->ws_bytes + 255) / 256 * 256;
+    p->ws_bytes = *off + rows * ldw8(cols) * 2;
+    p->t_pro += hw.t_launch + 4.0 * (double)rows * (double)cols / (hw.hbm_bw * hw.hbm_eta);
+    p->n_launch += 1;
+  };
+  if (s.layouts & AC_LAYOUT_A_COL) copy(s.M, s.K, &p->ws_a_off);
+  if (s.layouts & AC_LAYOUT_B_COL) copy(s.K, s.N, &p->ws_b_off);
+  p->predicted += p->t_pro;
+}
+
 bool finish(const Ctx& c, Plan* p, const Work& w) {
   p->s = c.s;
   p->predicted = model_time(c.s, w, c.hw, c.compulsory);
   p->variant_key = make_variant_key(p->family, p->cfg, p->swizzle, p->pk, c.s.dtype, (int)c.s.layouts);
-  return p->ws_bytes <= ((int64_t)2 << 30);  // workspace cap
+  if (p->ws_bytes > ((int64_t)2 << 30)) return false;  // cap of the partials
+  add_prologue(c.s, c.hw, p);
+  return true;
 }
 
 // The grouped kernel for one tile configuration. Launch: an upper bound of
@@ -924,13 +946,18 @@ static std::string kernel_names_fmt(const Plan& p);
 std::string kernel_names(const Plan& p) {
   // the fp16-input kernels live in the nested namespace f16
   std::string r = kernel_names_fmt(p);
-  if (!dtype_f16_input(p.s.dtype) || r.empty()) return r;
-  std::string out = "f16::";
-  for (char ch : r) {
-    out += ch;
-    if (ch == ';') out += "f16::";
+  if (dtype_f16_input(p.s.dtype) && !r.empty()) {
+    std::string out = "f16::";
+    for (char ch : r) {
+      out += ch;
+      if (ch == ';') out += "f16::";
+    }
+    r = out;
   }
-  return out;
+  // the layout prologue (one copy kernel per column-major operand) runs first
+  if (p.ws_b_off >= 0) r = "k_transpose16;" + r;
+  if (p.ws_a_off >= 0) r = "k_transpose16;" + r;
+  return r;
 }
 
 static std::string kernel_names_fmt(const Plan& p) {

@@ -33,7 +33,11 @@ struct Plan {
   int sk_tiles = 0;      // stream-K
   int ws_pk = 0;         // stream-K: partial slots per split tile
   int n_launch = 1;      // kernels per call (split K and stream-K add a reduction)
-  int64_t ws_bytes = 0;  // fp32 partials
+  int64_t ws_bytes = 0;  // fp32 partials, then the row-major copies of transposed operands
+  // Prologue (Eq. 7's T_pro): byte offsets in the workspace of the row-major
+  // copies of a column-major A (M x ld8(K)) and B (K x ld8(N)); -1: none.
+  int64_t ws_a_off = -1, ws_b_off = -1;
+  double t_pro = 0;      // its model time, included in `predicted`
   int n_candidates = 0;
   double predicted = 0;
   int64_t groups = 0;    // grouped product: groups (s.M is then the row capacity);

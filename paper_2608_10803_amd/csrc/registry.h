@@ -12,6 +12,11 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 // Reads the device's occupancy of every kernel into the planner.
 void query_occupancy();
+// Layout prologue: dst (cols x rows, row pitch ld_dst, a multiple of 8, dst
+// 16-byte aligned) = transpose of the 16-bit matrix src (rows x cols, row
+// pitch ld_src >= cols); the pad of each dst row is written with zeros.
+hipError_t launch_transpose16(const uint16_t* src, int64_t ld_src, int64_t rows, int64_t cols, uint16_t* dst,
+                              int64_t ld_dst, hipStream_t st);
 // the same kernels for fp16 inputs (dtypes 2 and 3)
 namespace f16 {
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);

@@ -145,7 +145,7 @@ def check(vals, ok, A, B, dtype, ref=None, label=""):
     return err
 
 
-def all_candidates(M, N, K, dtype):
+def all_candidates(M, N, K, dtype, layouts=0):
     """Every legal configuration of a shape, including stream-K and the
     configurations outside the taxonomy's template."""
     hw = ac.adaptcore_get_hw()
@@ -154,11 +154,11 @@ def all_candidates(M, N, K, dtype):
     h2.enable_streamk = 1
     ac.adaptcore_set_hw(h2)
     try:
-        return ac.adaptcore_candidates(M, N, K, dtype, 0)
+        return ac.adaptcore_candidates(M, N, K, dtype, layouts)
     finally:
         ac.adaptcore_set_hw(hw)
 
 
-def forced_plan(M, N, K, dtype, key):
+def forced_plan(M, N, K, dtype, key, layouts=0):
     """Plan for a configuration key (valid until the next profile change)."""
-    return ac.adaptcore_plan_variant(M, N, K, dtype, 0, key)
+    return ac.adaptcore_plan_variant(M, N, K, dtype, layouts, key)

@@ -139,7 +139,7 @@ def test_argument_validation():
         ac.adaptcore_plan(4, 4, 4, 7)
     assert e.value.status == ac.AC_ERR_UNSUPPORTED
     with pytest.raises(ac.AdaptCoreError):
-        ac.adaptcore_plan(4, 4, 4, ac.AC_BF16_F32OUT, 3)
+        ac.adaptcore_plan(4, 4, 4, ac.AC_BF16_F32OUT, 4)
     h = ac.adaptcore_plan(64, 32, 16)
     # leading dimensions shorter than the rows are rejected before any GPU work
     for args in [(0x1000, 15, 0x2000, 32, 0x3000, 32), (0x1000, 16, 0x2000, 31, 0x3000, 32),
@@ -181,6 +181,54 @@ def test_addmm_argument_validation():
         assert e.value.status == ac.AC_ERR_INVALID_VALUE
     # an empty output launches nothing and succeeds anywhere
     ac.adaptcore_addmm(ac.adaptcore_plan(0, 5, 7), 0, 7, 0x2000, 5, 0x3000, 5, 2.0, 0.5, 0x4000)
+
+
+def test_layout_plans():
+    """Column-major operands: a prologue copy per operand in the workspace
+    (after the partials, 256-byte aligned, rows padded to 8), priced in the
+    prediction; the configuration choice is the row-major one's."""
+    for (M, N, K) in [(2100, 3000, 200), (640, 1000, 4096), (4, 4096, 4096), (37, 91, 333)]:
+        d0 = ac.adaptcore_plan_info(ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, 0))
+        for layouts in (1, 2, 3):
+            h = ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, layouts)
+            d = ac.adaptcore_plan_info(h)
+            assert d["layouts"] == layouts and (d["variant_key"] >> 52) & 3 == layouts
+            assert d["variant_key"] & ~(3 << 52) == d0["variant_key"]
+            copies = 0
+            ws = d0["workspace_bytes"]
+            if layouts & 1:
+                ws = -(-ws // 256) * 256 + M * (-(-K // 8) * 8) * 2
+                copies += 1
+            if layouts & 2:
+                ws = -(-ws // 256) * 256 + K * (-(-N // 8) * 8) * 2
+                copies += 1
+            assert d["workspace_bytes"] == ws
+            assert d["predicted_s"] > d0["predicted_s"]
+            names = ac.adaptcore_plan_kernels(h)
+            assert names[:copies] == ["k_transpose16"] * copies
+            assert names[copies:] == ac.adaptcore_plan_kernels(ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, 0))
+    # K == 0: nothing to copy
+    d = ac.adaptcore_plan_info(ac.adaptcore_plan(30, 40, 0, ac.AC_BF16_F32OUT, 3))
+    assert d["workspace_bytes"] == 0
+    # leading dimensions follow the stored orientation
+    h = ac.adaptcore_plan(64, 32, 16, ac.AC_BF16_BF16OUT, 3)
+    for args in [(0x1000, 63, 0x2000, 16, 0x3000, 32), (0x1000, 64, 0x2000, 15, 0x3000, 32)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_matmul(h, *args)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    # the row pitch of a copy must stay below 2^23 like any operand's
+    big = ac.adaptcore_plan(2, 2, (1 << 23) - 3, ac.AC_BF16_F32OUT, 1)
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_matmul(big, 0x1000, 2, 0x2000, 2, 0x3000, 2)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    # unknown bits, and grouped and batched products, are refused
+    with pytest.raises(ac.AdaptCoreError) as e:
+        ac.adaptcore_plan(4, 4, 4, ac.AC_BF16_F32OUT, 4)
+    assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    for f, args in [(ac.adaptcore_grouped_plan, (64, 4, 32, 16)), (ac.adaptcore_batched_plan, (4, 16, 32, 16))]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            f(*args, ac.AC_BF16_F32OUT, 1)
+        assert e.value.status == ac.AC_ERR_UNSUPPORTED
 
 
 def test_candidates_are_legal_and_keys_round_trip():
