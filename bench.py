@@ -431,7 +431,8 @@ def layouts_main(args):
     and B and with each transposed layout (the prologue copies the
     column-major operand into the workspace, then the row-major plan runs);
     the extra time over row-major is the prologue's, reported with the rate
-    at which it moves the copied bytes (read + write)."""
+    at which it moves the copied bytes (read + write). A column-major B under
+    the small-M kernel is read in place (no copy)."""
     import torch
     import paper_2608_10803_amd as ac
     bf = ac.AC_BF16_BF16OUT
@@ -444,11 +445,12 @@ def layouts_main(args):
             t = time_plan(ac, torch, plan, M, N, K, bf)
             if lay == 0:
                 t0 = t
-            moved = 4 * ((M * K if lay & 1 else 0) + (K * N if lay & 2 else 0))
+            names = ac.adaptcore_plan_kernels(plan)
+            b_in_place = any(n.startswith("k_skinny_m_bt<") for n in names)
+            moved = 4 * ((M * K if lay & 1 else 0) + (K * N if lay & 2 and not b_in_place else 0))
             r = {"shape": [M, N, K], "layouts": lay, "us": round(t * 1e6, 2), "vs_row_major": round(t / t0, 3),
-                 "predicted_us": round(ac.adaptcore_plan_info(plan)["predicted_s"] * 1e6, 2),
-                 "kernels": ac.adaptcore_plan_kernels(plan)}
-            if lay:
+                 "predicted_us": round(ac.adaptcore_plan_info(plan)["predicted_s"] * 1e6, 2), "kernels": names}
+            if moved:
                 r["prologue_us"] = round((t - t0) * 1e6, 2)
                 r["prologue_gbps"] = round(moved / max(t - t0, 1e-9) / 1e9, 1)
             rows.append(r)

@@ -63,7 +63,8 @@ typedef enum {
  * C is always row-major. A column-major operand is copied into a row-major
  * copy in the plan's workspace by a prologue kernel before the main kernel
  * (the copy prologue of the paper's padding module, priced as T_pro in
- * Eq. 7). Grouped and batched products take row-major operands only. */
+ * Eq. 7), except a column-major B under the small-M kernel, which reads it
+ * in place. Grouped and batched products take row-major operands only. */
 enum { AC_LAYOUT_ROW_ROW = 0, AC_LAYOUT_A_COL = 1, AC_LAYOUT_B_COL = 2, AC_LAYOUT_COL_COL = 3 };
 
 /* Templates of the 2D tiling taxonomy (Section 4.2). */

@@ -1256,8 +1256,12 @@ __global__ __launch_bounds__(256) void k_reduce(GemmArgs g, int lg) {
 // {base + 8c + j}. A fragments (16 rows x 32 k) come straight from global
 // memory (A is small and stays in cache). WKW waves of a workgroup split the
 // workgroup's k-range and are reduced through LDS in wave order.
-template <int MT, int WKW, bool OBF>
-__global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
+// BT: B stored column-major (element (k, j) at B[j * ldb + k]). A column's 8
+// consecutive k are then contiguous, which is the MFMA's B fragment: each of
+// the 8 columns is one 16-byte load (like an A fragment) and no register
+// transpose is needed.
+template <int MT, int WKW, bool OBF, bool BT>
+__device__ __forceinline__ void skinny_m_kernel(const GemmArgs& g) {
   constexpr int WNW = 4 / WKW;
   constexpr int NB = 128 * WNW;
   constexpr int U = 2;
@@ -1287,8 +1291,8 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
   // past the row end) and the leading extra columns are dropped afterwards;
   // B rows past K are clamped and dropped; A vectors of the K tail end at the
   // row end. K < 8 or N < 8 take element loads instead.
-  const bool small = K < 8 || N < 8;
-  const int64_t cst = small ? col0 : min(col0, N - 8);
+  const bool small = BT ? K < 8 : (K < 8 || N < 8);
+  const int64_t cst = (small || BT) ? col0 : min(col0, N - 8);
   const int cs = small ? 0 : (int)min(col0 - cst, (int64_t)8);
   for (int kb = kb0 + wk; kb < kb1; kb += WKW * U) {
     u32x4 rb[U][8];
@@ -1303,11 +1307,28 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
       const bool on = kbu < kb1;  // uniform over the wave
       edge = edge || !on || (k_tail && kbu == kb_total - 1);
       past[u] = 0;
-      if (!small) {
+      if (BT) {
+        // column j of the lane: col0 + j, clamped into the matrix (columns
+        // past N compute values that are never stored)
+        const int64_t st = small ? k : min(k, K - 8);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          rb[u][i] = load16(g.B + min(k + i, K - 1) * ldb + cst);
-          past[u] |= (uint32_t)(!on || k + i >= K) << i;
+        for (int j = 0; j < 8; ++j) {
+          const uint16_t* bc = g.B + min(col0 + j, N - 1) * ldb;
+          if (!small) {
+            rb[u][j] = load16(bc + st);
+          } else {
+            const u32x4 v = load_row8_small(bc, k, K);
+            rb[u][j] = on ? v : u32x4{0u, 0u, 0u, 0u};
+          }
+        }
+      }
+      if (!small) {
+        if (!BT) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            rb[u][i] = load16(g.B + min(k + i, K - 1) * ldb + cst);
+            past[u] |= (uint32_t)(!on || k + i >= K) << i;
+          }
         }
         const int64_t st = min(k, K - 8);
         sa[u] = on ? (int)min(k - st, (int64_t)8) : 8;
@@ -1318,10 +1339,12 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
         }
       } else {
         sa[u] = 0;
+        if (!BT) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const u32x4 v = load_row8_small(g.B + min(k + i, K - 1) * ldb, col0, N);
-          rb[u][i] = (on && k + i < K) ? v : u32x4{0u, 0u, 0u, 0u};
+          for (int i = 0; i < 8; ++i) {
+            const u32x4 v = load_row8_small(g.B + min(k + i, K - 1) * ldb, col0, N);
+            rb[u][i] = (on && k + i < K) ? v : u32x4{0u, 0u, 0u, 0u};
+          }
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
@@ -1335,12 +1358,18 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
     for (int u = 0; u < U; ++u) {
       if (edge && !small) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) rb[u][i] = shift_down(rb[u][i], ((past[u] >> i) & 1) ? 8 : cs);
+        for (int i = 0; i < 8; ++i)
+          rb[u][i] = shift_down(rb[u][i], BT ? sa[u] : (((past[u] >> i) & 1) ? 8 : cs));
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) fa[u][mt] = shift_down(fa[u][mt], sa[u]);
       }
       u32x4 col[8];
-      transpose8x8(rb[u], col);
+      if constexpr (BT) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) col[j] = rb[u][j];
+      } else {
+        transpose8x8(rb[u], col);
+      }
 #pragma unroll
       for (int j = 0; j < 8; ++j)
 #pragma unroll
@@ -1381,6 +1410,15 @@ __global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
           store_c8<false>(g.ws + (size_t)split * (size_t)M * (size_t)g.ldw, row * g.ldw + col0, o, nvalid);
       }
     }
+}
+
+template <int MT, int WKW, bool OBF>
+__global__ __launch_bounds__(256) void k_skinny_m(GemmArgs g) {
+  skinny_m_kernel<MT, WKW, OBF, false>(g);
+}
+template <int MT, int WKW, bool OBF>
+__global__ __launch_bounds__(256) void k_skinny_m_bt(GemmArgs g) {
+  skinny_m_kernel<MT, WKW, OBF, true>(g);
 }
 
 // -------------------------------------------------------- skinny-N kernel
@@ -1913,7 +1951,13 @@ hipError_t launch_streamk(const Plan& p, const GemmArgs& g, hipStream_t st, bool
 template <int MT, int WKW>
 hipError_t launch_skinny_m(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, p.grid_y), block(256);
-  if (obf)
+  // a column-major B without a prologue copy is read in place
+  const bool bt = (p.s.layouts & AC_LAYOUT_B_COL) && p.ws_b_off < 0;
+  if (bt && obf)
+    hipLaunchKernelGGL((k_skinny_m_bt<MT, WKW, true>), grid, block, 0, st, g);
+  else if (bt)
+    hipLaunchKernelGGL((k_skinny_m_bt<MT, WKW, false>), grid, block, 0, st, g);
+  else if (obf)
     hipLaunchKernelGGL((k_skinny_m<MT, WKW, true>), grid, block, 0, st, g);
   else
     hipLaunchKernelGGL((k_skinny_m<MT, WKW, false>), grid, block, 0, st, g);

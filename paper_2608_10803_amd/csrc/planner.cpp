@@ -492,8 +492,9 @@ const int kSplits[] = {2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32, 40, 48, 64, 80,
 // Prologue of a plan with column-major operands: each one is copied into a
 // row-major copy in the workspace (after the partials) by a transposing
 // kernel, read and written once at the HBM rate: T_pro of Eq. 7, the same for
-// every configuration of the shape. Rows of the copies are padded to a
-// multiple of 8 elements (16-byte aligned rows for the main kernels).
+// every configuration of the shape except the small-M kernel, which reads a
+// column-major B in place. Rows of the copies are padded to a multiple of 8
+// elements (16-byte aligned rows for the main kernels).
 void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
   p->ws_a_off = p->ws_b_off = -1;
   p->t_pro = 0;
@@ -505,7 +506,9 @@ void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
     p->n_launch += 1;
   };
   if (s.layouts & AC_LAYOUT_A_COL) copy(s.M, s.K, &p->ws_a_off);
-  if (s.layouts & AC_LAYOUT_B_COL) copy(s.K, s.N, &p->ws_b_off);
+  // the small-M kernel reads a column-major B in place (its MFMA fragments
+  // are runs of k), so only the other families copy B
+  if ((s.layouts & AC_LAYOUT_B_COL) && p->family != FAM_SKINNY_M) copy(s.K, s.N, &p->ws_b_off);
   p->predicted += p->t_pro;
 }
 
@@ -981,7 +984,8 @@ static std::string kernel_names_fmt(const Plan& p) {
     }
     case FAM_SKINNY_M: {
       const SkinnyMCfg& k = kSkinnyMCfg[p.cfg];
-      std::snprintf(buf, sizeof buf, "k_skinny_m<%d, %d, %s>", k.mt, k.wkw, b);
+      const bool bt = (p.s.layouts & AC_LAYOUT_B_COL) && p.ws_b_off < 0;
+      std::snprintf(buf, sizeof buf, "k_skinny_m%s<%d, %d, %s>", bt ? "_bt" : "", k.mt, k.wkw, b);
       std::string r(buf);
       if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
       return r;

@@ -186,27 +186,38 @@ def test_addmm_argument_validation():
 def test_layout_plans():
     """Column-major operands: a prologue copy per operand in the workspace
     (after the partials, 256-byte aligned, rows padded to 8), priced in the
-    prediction; the configuration choice is the row-major one's."""
+    prediction -- except a column-major B under the small-M kernel, which
+    reads it in place. Every forced configuration keeps the row-major
+    configuration's kernels after the copies."""
     for (M, N, K) in [(2100, 3000, 200), (640, 1000, 4096), (4, 4096, 4096), (37, 91, 333)]:
-        d0 = ac.adaptcore_plan_info(ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, 0))
         for layouts in (1, 2, 3):
-            h = ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, layouts)
-            d = ac.adaptcore_plan_info(h)
-            assert d["layouts"] == layouts and (d["variant_key"] >> 52) & 3 == layouts
-            assert d["variant_key"] & ~(3 << 52) == d0["variant_key"]
-            copies = 0
-            ws = d0["workspace_bytes"]
-            if layouts & 1:
-                ws = -(-ws // 256) * 256 + M * (-(-K // 8) * 8) * 2
-                copies += 1
-            if layouts & 2:
-                ws = -(-ws // 256) * 256 + K * (-(-N // 8) * 8) * 2
-                copies += 1
-            assert d["workspace_bytes"] == ws
-            assert d["predicted_s"] > d0["predicted_s"]
-            names = ac.adaptcore_plan_kernels(h)
-            assert names[:copies] == ["k_transpose16"] * copies
-            assert names[copies:] == ac.adaptcore_plan_kernels(ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, 0))
+            for c in ac.adaptcore_candidates(M, N, K, ac.AC_BF16_BF16OUT, layouts):
+                key = c["variant_key"]
+                assert (key >> 52) & 3 == layouts
+                h = ac.adaptcore_plan_variant(M, N, K, ac.AC_BF16_BF16OUT, layouts, key)
+                h0 = ac.adaptcore_plan_variant(M, N, K, ac.AC_BF16_BF16OUT, 0, key & ~(3 << 52))
+                d, d0 = ac.adaptcore_plan_info(h), ac.adaptcore_plan_info(h0)
+                assert d["layouts"] == layouts
+                skinny = d["family"] == ac.AC_FAMILY_SKINNY_M
+                ws, copies = d0["workspace_bytes"], 0
+                if layouts & 1:
+                    ws = -(-ws // 256) * 256 + M * (-(-K // 8) * 8) * 2
+                    copies += 1
+                if layouts & 2 and not skinny:
+                    ws = -(-ws // 256) * 256 + K * (-(-N // 8) * 8) * 2
+                    copies += 1
+                assert d["workspace_bytes"] == ws, (layouts, c)
+                assert (d["predicted_s"] > d0["predicted_s"]) == (copies > 0)
+                names = ac.adaptcore_plan_kernels(h)
+                assert names[:copies] == ["k_transpose16"] * copies
+                rest = ac.adaptcore_plan_kernels(h0)
+                if layouts & 2 and skinny:
+                    rest = [n.replace("k_skinny_m<", "k_skinny_m_bt<") for n in rest]
+                assert names[copies:] == rest, (names, rest)
+        # the decode shape with B column-major picks the in-place small-M kernel
+        if (M, N, K) == (4, 4096, 4096):
+            names = ac.adaptcore_plan_kernels(ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, 2))
+            assert names[0].startswith("k_skinny_m_bt<"), names
     # K == 0: nothing to copy
     d = ac.adaptcore_plan_info(ac.adaptcore_plan(30, 40, 0, ac.AC_BF16_F32OUT, 3))
     assert d["workspace_bytes"] == 0
