@@ -164,6 +164,16 @@ typedef struct {
    * load phase for the fixed cost. Each value must lie in [0, 1) seconds. */
   double cfg_iter[AC_N_CFG];
   double cfg_wg[AC_N_CFG];
+  /* Per kernel configuration: achieved fraction of the streaming HBM rate
+   * (hbm_bw * hbm_eta) for the bytes the configuration writes (C or fp32
+   * partials) -- the per-variant efficiency of Eq. 8 applied to the output
+   * traffic. 0 = not calibrated (read as 1); each value in [0, 1]. */
+  double cfg_wr[AC_N_CFG];
+  /* Time factor of the main kernel of a tile-family plan with the XCD-aware
+   * tile order (swizzle = 1) against the plain order: the order changes
+   * which tiles share an XCD's L2, and so the traffic efficiency (Eq. 8's
+   * eta) of both re-reads and output writes. In (0, 1]; 1 = no effect. */
+  double swizzle_gain;
 } adaptcore_hw_t;
 
 /* Index of a kernel configuration in adaptcore_hw_t::cfg_iter / cfg_wg, or -1. */

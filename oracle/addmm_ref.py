@@ -24,7 +24,8 @@ output are measured against the same relative bars as a plain product.
 
 Parity pins: tests/test_oracle_addmm.py (exact rational brute force of C and
 D on tiny inputs with mixed-sign alpha and beta, reduction to the plain
-product, beta == 0 ignoring a NaN C_old, K == 0, and a mutation test).
+product, beta == 0 ignoring a NaN C_old, K == 0, sampled entries equal to
+the full result, and a mutation test).
 """
 import numpy as np
 
@@ -50,6 +51,27 @@ def addmm(A, B, C_old, alpha, beta, bias=None, M=None, N=None, K=None, lda=None,
         D = D + abs(beta) * np.abs(Co)
     if bias is not None:
         b = np.asarray(bias, np.float64).reshape(1, C.shape[1])
+        C = C + b
+        D = D + np.abs(b)
+    return C, D
+
+
+def addmm_entries(A, B, I, J, c_old, alpha, beta, bias, M=None, N=None, K=None, lda=None, ldb=None, fmt="bf16",
+                  lib=None):
+    """Entries (I[t], J[t]) of AddMM, each from its A row and B column (the
+    plain oracle's gemm_entries); c_old[t] is C_old at that entry and
+    bias[t] the bias of its column (None: no bias)."""
+    P, Dp = gemm_ref.gemm_entries(A, B, I, J, M=M, N=N, K=K, lda=lda, ldb=ldb, fmt=fmt, lib=lib)
+    alpha = float(alpha)
+    beta = float(beta)
+    C = alpha * P
+    D = abs(alpha) * Dp
+    if beta != 0.0:
+        Co = np.asarray(c_old, np.float64).reshape(C.shape)
+        C = C + beta * Co
+        D = D + abs(beta) * np.abs(Co)
+    if bias is not None:
+        b = np.asarray(bias, np.float64).reshape(C.shape)
         C = C + b
         D = D + np.abs(b)
     return C, D

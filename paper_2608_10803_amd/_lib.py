@@ -86,13 +86,14 @@ class Hw(ctypes.Structure):
                 ("t_mem_latency", ctypes.c_double), ("t_wg", ctypes.c_double), ("mfma_eta", ctypes.c_double),
                 ("lds_bw_cu", ctypes.c_double), ("unaligned_eta", ctypes.c_double), ("l2_hit", ctypes.c_double),
                 ("search_open", ctypes.c_int32), ("enable_streamk", ctypes.c_int32),
-                ("cfg_iter", ctypes.c_double * AC_N_CFG), ("cfg_wg", ctypes.c_double * AC_N_CFG)]
+                ("cfg_iter", ctypes.c_double * AC_N_CFG), ("cfg_wg", ctypes.c_double * AC_N_CFG),
+                ("cfg_wr", ctypes.c_double * AC_N_CFG), ("swizzle_gain", ctypes.c_double)]
 
     def as_dict(self):
         d = {}
         for f, _ in self._fields_:
             v = getattr(self, f)
-            d[f] = list(v) if f in ("cfg_iter", "cfg_wg") else v
+            d[f] = list(v) if f in ("cfg_iter", "cfg_wg", "cfg_wr") else v
         return d
 
     def copy(self):

@@ -33,8 +33,8 @@ from . import _lib as ac
 # workgroup costs (cfg_iter, cfg_wg).
 # The launch cost is not fitted: it is the measured per-kernel floor of
 # back-to-back launches, and the fixed part of each configuration is in cfg_wg.
-FIT_FIELDS = ["t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit"]
-BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.99)}
+FIT_FIELDS = ["t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit", "swizzle_gain"]
+BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.99), "swizzle_gain": (0.5, 1.0)}
 N_CFG = ac.AC_N_CFG
 
 
@@ -51,7 +51,23 @@ def sample_shapes(n_sweep=200, seed=11):
 
     order = sorted(range(len(sw)), key=lambda i: floor(sw[i]))
     pick = [sw[order[int(j)]] for j in np.linspace(0, len(sw) - 1, n_sweep)]
-    return pick + gen.skinny_m() + gen.small_mn_large_k()
+    return pick + gen.skinny_m() + gen.small_mn_large_k() + write_bound_shapes()
+
+
+def write_bound_shapes(n=40, seed=12):
+    """Shapes whose traffic is mostly the output (large M x N, small K), drawn
+    on their own (not from the sweep): M, N log-uniform in [2048, 100000], K
+    log-uniform in [8, 400], kept when C is at least half of the bytes and
+    at most 4 GiB. They fix the per-configuration write efficiency."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        M, N = (int(round(math.exp(rng.uniform(math.log(2048), math.log(100000))))) for _ in range(2))
+        K = int(round(math.exp(rng.uniform(math.log(8), math.log(400)))))
+        c = 2.0 * M * N
+        if c >= 0.5 * (2.0 * M * K + 2.0 * K * N + c) and c <= 4 * 2 ** 30:
+            out.append((M, N, K))
+    return out
 
 
 def _open_profile():
@@ -198,7 +214,8 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print):
     """Fit the profile: minimise the squared log error of the model over all
     measured configurations. Alternates a Nelder-Mead search over the global
     constants (launch, latency, bandwidth, cache hit rate) with one over the
-    two costs of each kernel configuration on that configuration's records."""
+    three constants of each kernel configuration (iteration cost, workgroup
+    cost, write efficiency) on that configuration's records."""
     from scipy.optimize import minimize
     hw0 = (hw0 or ac.adaptcore_get_hw()).copy()
     meas = _by_shape(recs)
@@ -233,23 +250,29 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print):
             keys = by_cfg[idx]
             sub = {sk: mt for sk, mt in meas.items() if any(k in keys for k in mt)}
 
-            def loss_cfg(x):
-                h = cur.copy()
+            def put(h, x):
                 h.cfg_iter[idx] = math.exp(min(max(x[0], -30.0), -7.0))
                 h.cfg_wg[idx] = math.exp(min(max(x[1], -30.0), -7.0))
+                h.cfg_wr[idx] = math.exp(min(max(x[2], math.log(0.05)), 0.0))
+
+            def loss_cfg(x):
+                h = cur.copy()
+                put(h, x)
                 e = _log_errors(h, sub, keys)
                 return float(np.mean(np.square(e))) if len(e) else 0.0
             if not len(_log_errors(cur, sub, keys)):
                 continue  # none of this configuration's records is a candidate now
+            # (an uncalibrated efficiency starts inside its range: Nelder-Mead's
+            # first simplex is too small around 0 to leave the bound at 1)
+            wr0 = math.log(cur.cfg_wr[idx]) if cur.cfg_wr[idx] > 0 else math.log(0.7)
             if cur.cfg_iter[idx] > 0:
-                x0 = np.array([math.log(cur.cfg_iter[idx]), math.log(max(cur.cfg_wg[idx], 1e-9))])
+                x0 = np.array([math.log(cur.cfg_iter[idx]), math.log(max(cur.cfg_wg[idx], 1e-9)), wr0])
             else:  # coarse grid for the first start
-                grid = [(a, b) for a in np.log(np.logspace(-9, -5, 17)) for b in np.log([1e-8, 1e-7, 3e-7, 1e-6])]
+                grid = [(a, b, wr0) for a in np.log(np.logspace(-9, -5, 17)) for b in np.log([1e-8, 1e-7, 3e-7, 1e-6])]
                 x0 = np.array(min(grid, key=lambda g: loss_cfg(g)))
-            r2 = minimize(loss_cfg, x0, method="Nelder-Mead", options={"maxiter": 200, "xatol": 1e-3, "fatol": 1e-6})
+            r2 = minimize(loss_cfg, x0, method="Nelder-Mead", options={"maxiter": 300, "xatol": 1e-3, "fatol": 1e-6})
             evals += r2.nfev
-            cur.cfg_iter[idx] = math.exp(min(max(r2.x[0], -30.0), -7.0))
-            cur.cfg_wg[idx] = math.exp(min(max(r2.x[1], -30.0), -7.0))
+            put(cur, r2.x)
         log("fit round %d: loss %.4f" % (rnd, loss_all(cur)))
     l1 = loss_all(cur)
     log("fit: loss %.4f -> %.4f (%d evaluations)" % (l0, l1, evals))
@@ -262,11 +285,14 @@ def emit_cpp(profile):
     p = profile
     lines = ["  h.t_launch = %.4g;" % p["t_launch"], "  h.t_mem_latency = %.4g;" % p["t_mem_latency"],
              "  h.hbm_eta = %.4g;" % p["hbm_eta"], "  h.l2_bw_cu = %.4g;" % p["l2_bw_cu"],
-             "  h.unaligned_eta = %.4g;" % p["unaligned_eta"], "  h.l2_hit = %.4g;" % p["l2_hit"]]
+             "  h.unaligned_eta = %.4g;" % p["unaligned_eta"], "  h.l2_hit = %.4g;" % p["l2_hit"],
+             "  h.swizzle_gain = %.4g;" % p.get("swizzle_gain", 1.0)]
     it = ", ".join("%.4g" % v for v in p["cfg_iter"])
     wg = ", ".join("%.4g" % v for v in p["cfg_wg"])
+    wr = ", ".join("%.4g" % v for v in p.get("cfg_wr", [0.0] * len(p["cfg_wg"])))
     lines.append("  static const double kIter[AC_N_CFG] = {%s};" % it)
     lines.append("  static const double kWg[AC_N_CFG] = {%s};" % wg)
+    lines.append("  static const double kWr[AC_N_CFG] = {%s};" % wr)
     return "\n".join(lines)
 
 

@@ -718,10 +718,11 @@ adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw) {
   if (hw->n_cu <= 0 || hw->lds_bytes <= 0 || hw->s_acc_bytes <= 0 || !(hw->clock_hz > 0) || !(hw->hbm_bw > 0) ||
       !(hw->hbm_eta > 0) || !(hw->l2_bw_cu > 0) || !(hw->mfma_eta > 0) || !(hw->lds_bw_cu > 0) ||
       !(hw->unaligned_eta > 0) || hw->l2_hit < 0 || hw->l2_hit > 1 || hw->t_launch < 0 || hw->t_mem_latency < 0 ||
-      hw->t_wg < 0)
+      hw->t_wg < 0 || !(hw->swizzle_gain > 0 && hw->swizzle_gain <= 1))
     return fail(AC_ERR_INVALID_VALUE, "profile field out of range");
   for (int i = 0; i < AC_N_CFG; ++i)
-    if (!(hw->cfg_iter[i] >= 0 && hw->cfg_iter[i] < 1) || !(hw->cfg_wg[i] >= 0 && hw->cfg_wg[i] < 1))
+    if (!(hw->cfg_iter[i] >= 0 && hw->cfg_iter[i] < 1) || !(hw->cfg_wg[i] >= 0 && hw->cfg_wg[i] < 1) ||
+        !(hw->cfg_wr[i] >= 0 && hw->cfg_wr[i] <= 1))
       return fail(AC_ERR_INVALID_VALUE, "calibrated configuration cost out of range");
   adaptcore_cache_clear();
   std::lock_guard<std::mutex> lk(g_mu);

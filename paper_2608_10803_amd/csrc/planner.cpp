@@ -75,6 +75,7 @@ struct Work {
   double prefetch = 1;   // main-loop iterations of loads in flight
   double total_read = 0; // sum over workgroups of bytes read (Eq. 1 analogue)
   bool unaligned = false;
+  bool swizzle = false;  // XCD-aware tile order (tile-family kernels)
 };
 
 // Eq. 8 with shared bandwidth: per-workgroup share of HBM (compulsory
@@ -86,6 +87,8 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
   const double slots = (double)hw.n_cu * std::max(1, w.occ);
   const double eta = hw.hbm_eta * (w.unaligned ? hw.unaligned_eta : 1.0);
   const double agg_hbm = hw.hbm_bw * eta;
+  // per-configuration efficiency of the output writes (calibrated; 1 if not)
+  const double wr = (w.idx >= 0 && hw.cfg_wr[w.idx] > 0) ? hw.cfg_wr[w.idx] : 1.0;
   // fraction of loaded bytes that come from HBM (the rest hits L2 / MALL)
   double hbm_frac = 1.0;
   if (w.total_read > compulsory && w.total_read > 0) {
@@ -111,7 +114,7 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
     const double twg = cal ? hw.cfg_wg[w.idx] : hw.t_wg;
     const double lat = cal ? 0.0 : hw.t_mem_latency;
     const double t_fill = lat + tM + tP;  // first slice: load latency, load, compute
-    const double t_drain = w.out_unit / bw_hbm;
+    const double t_drain = w.out_unit / (bw_hbm * wr);
     const double t_setup = (w.setup > 0 ? lat + w.setup / bw_l2 : 0.0) + w.extra_lat * hw.t_mem_latency;
     const double L = std::max(0.0, w.L);
     if (L == 0) return twg + t_setup + t_drain;
@@ -122,15 +125,16 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
   double t_main = full * unit_time(slots);
   if (rem > 0) t_main += unit_time(rem);
   // aggregate HBM roof over the whole launch
-  const double hbm_bytes =
-      compulsory + (w.total_read - std::min(w.total_read, compulsory)) * (1.0 - hw.l2_hit) + w.total_write;
-  t_main = std::max(t_main, hbm_bytes / agg_hbm);
+  const double hbm_read = compulsory + (w.total_read - std::min(w.total_read, compulsory)) * (1.0 - hw.l2_hit);
+  t_main = std::max(t_main, hbm_read / agg_hbm + w.total_write / (agg_hbm * wr));
+  // the XCD-aware tile order's calibrated effect on the main kernel
+  if (w.swizzle) t_main *= hw.swizzle_gain;
   // cross-workgroup reduction (Eq. 11) as a second kernel: one more launch, the
   // partials read back and the output written once
   double t_epi = 0;
   if (w.epi > 0) t_epi = hw.t_launch + hw.t_mem_latency + (w.epi + w.epi_out) / (hw.hbm_bw * hw.hbm_eta);
   (void)s;
-  return hw.t_launch + t_main + t_epi;  // Eq. 7 (T_pro = 0)
+  return hw.t_launch + t_main + t_epi;  // Eq. 7 (T_pro: added for column-major operands, add_prologue)
 }
 
 struct Ctx {
@@ -191,6 +195,7 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
   w->prefetch = t.depth;
   w->total_read = (double)tm * tn * (bm_e + bn_e) * (double)s.K * 2;
   w->unaligned = c.unaligned;
+  w->swizzle = swizzle != 0;
   return true;
 }
 
@@ -586,19 +591,22 @@ adaptcore_hw_t default_hw() {
   h.t_wg = 0.2e-6;
   h.search_open = 0;
   h.enable_streamk = 0;
-  // Constants fitted to per-configuration timings of 150 shapes of the
+  // Constants fitted to per-configuration timings of shapes of the
   // dynamic-shape, decode-style and small-MN large-K workloads on one MI355X
   // (squared log error of the model over every measured configuration). The
-  // launch cost is the measured per-kernel floor of back-to-back launches.
+  // launch cost is the measured per-kernel floor of back-to-back launches;
+  // the XCD-order factor is the measured geomean time ratio of the swizzled
+  // to the plain variant of a tile configuration (2,240 measured pairs).
   h.t_launch = 1.9e-06;
   h.t_mem_latency = 1.413e-06;
   h.hbm_eta = 1;
   h.l2_bw_cu = 2.928e+10;
   h.unaligned_eta = 1;
   h.l2_hit = 5.38e-33;
+  h.swizzle_gain = 0.935;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
-  // 20-21, stream-K 22-29, direct 30-32; 0 = analytic estimate, no timing
-  // data)
+  // 20-21, stream-K 22-29, direct 30-32, persistent 33-43; 0 = analytic
+  // estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
       2.853e-06, 2.085e-06, 1.938e-06, 3.052e-07, 5.513e-07, 2.327e-07, 5.38e-07, 3.959e-07,
       1.119e-06, 2.57e-08, 9.358e-14, 1.231e-06, 1.259e-06, 1.399e-06, 1.399e-06, 1.761e-06,
@@ -617,9 +625,12 @@ adaptcore_hw_t default_hw() {
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
+  // achieved fraction of the streaming rate for the output writes (0: 1)
+  static const double kWr[AC_N_CFG] = {0};
   for (int i = 0; i < AC_N_CFG; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];
+    h.cfg_wr[i] = kWr[i];
   }
   return h;
 }

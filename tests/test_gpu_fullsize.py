@@ -16,6 +16,7 @@ import numpy as np
 import pytest
 
 import paper_2608_10803_amd as ac
+from oracle import addmm_ref
 from oracle import gemm_ref
 from workloads import gen
 
@@ -164,3 +165,81 @@ def test_moe_stream_full_size():
             ac.adaptcore_matmul(plan, arena.A.data_ptr(), K, arena.B.data_ptr(), N, arena.C.data_ptr(), N, 0)
             continue
         check_shape(arena, M, N, K, BF16, 5000 + i, "moe #%d" % i)
+
+
+# the shapes of the benchmark's layouts workload
+LAYOUT_SHAPES = [(4096, 4096, 4096), (2048, 14336, 4096), (8192, 8192, 1024), (16, 4096, 14336), (512, 512, 512)]
+
+
+def _sampled(t, Alog, Blog, M, N, K, seed):
+    """Sampled entries and the raw bf16 A rows and B columns they need,
+    read through the logical (possibly transposed) views."""
+    I, J = sample_entries(M, N, seed)
+    ui, inv_i = np.unique(I, return_inverse=True)
+    uj, inv_j = np.unique(J, return_inverse=True)
+    Ar = Alog[t.from_numpy(ui).cuda()].contiguous().view(t.int16).cpu().numpy().view(np.uint16)
+    Bc = Blog[:, t.from_numpy(uj).cuda()].contiguous().view(t.int16).cpu().numpy().view(np.uint16)
+    return I, J, Ar, Bc, inv_i, inv_j, len(ui), len(uj)
+
+
+def test_layouts_full_size():
+    """The benchmark's layouts workload: each shape with A, B or both stored
+    column-major, the planner's own plan, bf16 output, sampled entries."""
+    t = _torch()
+    g = t.Generator(device="cuda")
+    g.manual_seed(6)
+    for si, (M, N, K) in enumerate(LAYOUT_SHAPES):
+        A = t.empty(M * K, dtype=t.bfloat16, device="cuda").uniform_(-1, 1, generator=g)
+        B = t.empty(K * N, dtype=t.bfloat16, device="cuda").uniform_(-1, 1, generator=g)
+        C = t.empty(M, N, dtype=t.bfloat16, device="cuda")
+        for lay in (ac.AC_LAYOUT_A_COL, ac.AC_LAYOUT_B_COL, ac.AC_LAYOUT_COL_COL):
+            a_col, b_col = bool(lay & 1), bool(lay & 2)
+            _progress("layouts %d %s" % (lay, (M, N, K)))
+            Alog = A.view(K, M).t() if a_col else A.view(M, K)
+            Blog = B.view(N, K).t() if b_col else B.view(K, N)
+            plan = ac.adaptcore_plan(M, N, K, BF16, lay)
+            C.fill_(float("nan"))
+            ac.adaptcore_matmul(plan, A.data_ptr(), M if a_col else K, B.data_ptr(), K if b_col else N,
+                                C.data_ptr(), N, 0)
+            t.cuda.synchronize()
+            I, J, Ar, Bc, ii, jj, nu, nv = _sampled(t, Alog, Blog, M, N, K, 7000 + 10 * si + lay)
+            got = C[t.from_numpy(I).cuda(), t.from_numpy(J).cuda()]
+            vals = gemm_ref.decode(got.view(t.int16).cpu().numpy().view(np.uint16))
+            C_ref, D = gemm_ref.gemm_entries(Ar, Bc, ii, jj, M=nu, N=nv, K=K)
+            err = gemm_ref.err_metric(vals, C_ref, D)
+            assert err <= tol(BF16), ((M, N, K), lay, err, ac.adaptcore_plan_kernels(plan))
+
+
+def test_addmm_full_size():
+    """AddMM (alpha, beta, bias) at full size with fp32 and bf16 output, row-
+    and column-major B, the planner's own plan, sampled entries."""
+    t = _torch()
+    g = t.Generator(device="cuda")
+    g.manual_seed(8)
+    for si, (M, N, K) in enumerate([(2048, 14336, 4096), (16, 4096, 14336), (8192, 8192, 1024)]):
+        A = t.empty(M * K, dtype=t.bfloat16, device="cuda").uniform_(-1, 1, generator=g)
+        B = t.empty(K * N, dtype=t.bfloat16, device="cuda").uniform_(-1, 1, generator=g)
+        bias = t.empty(N, dtype=t.float32, device="cuda").uniform_(-1, 1, generator=g)
+        for dtype in (F32, BF16):
+            for lay in (0, ac.AC_LAYOUT_B_COL):
+                _progress("addmm %s dtype %d layouts %d" % ((M, N, K), dtype, lay))
+                C = t.empty(M, N, dtype=t.float32 if dtype == F32 else t.bfloat16, device="cuda")
+                C.uniform_(-2, 2, generator=g)
+                I, J = sample_entries(M, N, 8000 + si)
+                Ii, Jj = t.from_numpy(I).cuda(), t.from_numpy(J).cuda()
+                old = C[Ii, Jj].float().cpu().numpy().astype(np.float64)
+                Blog = B.view(N, K).t() if lay else B.view(K, N)
+                plan = ac.adaptcore_plan(M, N, K, dtype, lay)
+                ac.adaptcore_addmm(plan, A.data_ptr(), K, B.data_ptr(), K if lay else N, C.data_ptr(), N,
+                                   0.75, -1.25, bias.data_ptr(), 0)
+                t.cuda.synchronize()
+                got = C[Ii, Jj]
+                if dtype == F32:
+                    vals = got.cpu().numpy().astype(np.float64)
+                else:
+                    vals = gemm_ref.decode(got.view(t.int16).cpu().numpy().view(np.uint16))
+                _, _, Ar, Bc, ii, jj, nu, nv = _sampled(t, A.view(M, K), Blog, M, N, K, 8000 + si)
+                b = bias[Jj].cpu().numpy().astype(np.float64)
+                C_ref, D = addmm_ref.addmm_entries(Ar, Bc, ii, jj, old, 0.75, -1.25, b, M=nu, N=nv, K=K)
+                err = gemm_ref.err_metric(vals, C_ref, D)
+                assert err <= tol(dtype), ((M, N, K), dtype, lay, err, ac.adaptcore_plan_kernels(plan))

@@ -134,6 +134,18 @@ def test_fp16_inputs():
     assert np.allclose(D, 0.5 * Dp + 1.5 * np.abs(C_old), rtol=1e-15, atol=0)
 
 
+def test_entries_match_full_result():
+    A, B, C_old, alpha, beta, bias = _case(11)
+    C, D = addmm_ref.addmm(A, B, C_old, alpha, beta, bias)
+    rng = np.random.default_rng(12)
+    I = rng.integers(0, A.shape[0], 15)
+    J = rng.integers(0, B.shape[1], 15)
+    Ce, De = addmm_ref.addmm_entries(A, B, I, J, C_old[I, J], alpha, beta, bias[J])
+    assert np.array_equal(Ce, C[I, J]) and np.array_equal(De, D[I, J])
+    Ce, De = addmm_ref.addmm_entries(A, B, I, J, np.full(15, np.nan), alpha, 0.0, None)
+    assert np.all(np.isfinite(Ce))
+
+
 MUTATIONS = [
     ("bias dropped", "        C = C + b\n", "        C = C\n"),
     ("beta sign", "C = C + beta * Co", "C = C - beta * Co"),
