@@ -66,6 +66,8 @@ typedef enum {
  * Eq. 7), except a column-major B under the small-M kernel, which reads it
  * in place. Grouped and batched products take row-major operands only. */
 enum { AC_LAYOUT_ROW_ROW = 0, AC_LAYOUT_A_COL = 1, AC_LAYOUT_B_COL = 2, AC_LAYOUT_COL_COL = 3 };
+/* The same bits named per operand (A_ROWMAJOR | B_COLMAJOR, ...). */
+enum { AC_A_ROWMAJOR = 0, AC_A_COLMAJOR = AC_LAYOUT_A_COL, AC_B_ROWMAJOR = 0, AC_B_COLMAJOR = AC_LAYOUT_B_COL };
 
 /* Templates of the 2D tiling taxonomy (Section 4.2). */
 typedef enum {
