@@ -322,6 +322,18 @@ adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const vo
                                           const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
                                           int64_t stride_c, void* stream);
 
+/* The batched product with the AddMM epilogue of adaptcore_addmm (the
+ * epilogues the paper's BatchMM and AddMM operators need, Section 6.5): for
+ * every batch b, C_b = alpha * A_b * B_b + beta * C_b,old + bias, in fp32
+ * before the rounding to C's type, C_b,old read only when beta != 0, bias a
+ * device array of N fp32 values shared by all batches (NULL: none).
+ * Arguments and validation as adaptcore_batched_matmul, plus finite alpha
+ * and beta and a 4-byte-aligned bias (AC_ERR_INVALID_VALUE). K == 0 yields
+ * C_b = beta * C_b,old + bias. */
+adaptcore_status adaptcore_batched_addmm(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
+                                         const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
+                                         int64_t stride_c, float alpha, float beta, const float* bias, void* stream);
+
 /* Allocates (if needed) the workspace of `stream` for plans needing up to
  * `bytes`, so that later calls, also under capture, do not allocate. */
 adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes);

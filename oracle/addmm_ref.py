@@ -22,14 +22,20 @@ The acceptance scale of an entry is the sum of the magnitudes of its terms,
 so that the GPU's fp32 epilogue rounding and the final rounding to a 16-bit
 output are measured against the same relative bars as a plain product.
 
+The batched form (BatchMM with the same epilogue) applies it to every batch
+of the strided batched product (grouped_ref.batched_gemm), with one bias row
+shared by all batches.
+
 Parity pins: tests/test_oracle_addmm.py (exact rational brute force of C and
 D on tiny inputs with mixed-sign alpha and beta, reduction to the plain
 product, beta == 0 ignoring a NaN C_old, K == 0, sampled entries equal to
-the full result, and a mutation test).
+the full result, every batch of the batched form equal to the single form on
+that batch's matrices, and a mutation test).
 """
 import numpy as np
 
 from . import gemm_ref
+from . import grouped_ref
 
 
 def addmm(A, B, C_old, alpha, beta, bias=None, M=None, N=None, K=None, lda=None, ldb=None, fmt="bf16",
@@ -72,6 +78,26 @@ def addmm_entries(A, B, I, J, c_old, alpha, beta, bias, M=None, N=None, K=None, 
         D = D + abs(beta) * np.abs(Co)
     if bias is not None:
         b = np.asarray(bias, np.float64).reshape(C.shape)
+        C = C + b
+        D = D + np.abs(b)
+    return C, D
+
+
+def batched_addmm(A, B, C_old, batch, M, N, K, lda, ldb, stride_a, stride_b, alpha, beta, bias=None, fmt="bf16",
+                  lib=None):
+    """(C_ref, D) of shape (batch, M, N): the epilogue above applied to every
+    batch of the strided batched product; C_old has shape (batch, M, N)."""
+    P, Dp = grouped_ref.batched_gemm(A, B, batch, M, N, K, lda, ldb, stride_a, stride_b, fmt=fmt, lib=lib)
+    alpha = float(alpha)
+    beta = float(beta)
+    C = alpha * P
+    D = abs(alpha) * Dp
+    if beta != 0.0:
+        Co = np.asarray(C_old, np.float64).reshape(C.shape)
+        C = C + beta * Co
+        D = D + abs(beta) * np.abs(Co)
+    if bias is not None:
+        b = np.asarray(bias, np.float64).reshape(1, 1, N)
         C = C + b
         D = D + np.abs(b)
     return C, D

@@ -147,6 +147,9 @@ def lib():
         L.adaptcore_batched_plan_variant.restype = p
         L.adaptcore_batched_matmul.argtypes = [p, p, i64, i64, p, i64, i64, p, i64, i64, p]
         L.adaptcore_batched_matmul.restype = i32
+        L.adaptcore_batched_addmm.argtypes = [p, p, i64, i64, p, i64, i64, p, i64, i64, ctypes.c_float,
+                                              ctypes.c_float, p, p]
+        L.adaptcore_batched_addmm.restype = i32
         L.adaptcore_reserve_workspace.argtypes = [p, i64]
         L.adaptcore_reserve_workspace.restype = i32
         L.adaptcore_plan_info.argtypes = [p, ctypes.POINTER(PlanDesc)]
@@ -264,6 +267,14 @@ def adaptcore_batched_plan_variant(batch, M, N, K, dtype, layouts, variant_key):
 def adaptcore_batched_matmul(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, stream=0):
     """Strided batched product on `stream`; A, B, C are device addresses."""
     return _check(lib().adaptcore_batched_matmul(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, stream))
+
+
+def adaptcore_batched_addmm(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, alpha=1.0, beta=0.0, bias=0,
+                            stream=0):
+    """C_b = alpha * A_b B_b + beta * C_b + bias for every batch b on `stream`;
+    A, B, C, bias are device addresses (bias = 0 for none)."""
+    return _check(lib().adaptcore_batched_addmm(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, alpha,
+                                                beta, bias, stream))
 
 
 def adaptcore_reserve_workspace(stream, nbytes):

@@ -585,9 +585,14 @@ const adaptcore_plan_t* adaptcore_batched_plan_variant(int64_t batch, int64_t M,
   return pp;
 }
 
-adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
-                                          const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
-                                          int64_t stride_c, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// One call of a batched plan; epi != 0 selects the AddMM epilogue.
+adaptcore_status run_batched(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
+                             const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc, int64_t stride_c,
+                             void* stream, int epi, float alpha, float beta, const float* bias) {
   if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
   const ac::Plan& p = plan->p;
   if (p.family != ac::FAM_BATCHED)
@@ -626,6 +631,10 @@ adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const vo
   a.g.tiles_m = p.pm;
   a.g.tiles_n = p.pn;
   a.g.swizzle = p.swizzle;
+  a.g.epi = epi;
+  a.g.alpha = alpha;
+  a.g.beta = beta;
+  a.g.bias = bias;
   a.counts = nullptr;
   a.rows = M;
   a.stride_a = stride_a;
@@ -639,6 +648,24 @@ adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const vo
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add(1, std::memory_order_relaxed);
   return AC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+adaptcore_status adaptcore_batched_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
+                                          const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
+                                          int64_t stride_c, void* stream) {
+  return run_batched(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, stream, 0, 1.0f, 0.0f, nullptr);
+}
+
+adaptcore_status adaptcore_batched_addmm(const adaptcore_plan_t* plan, const void* A, int64_t lda, int64_t stride_a,
+                                         const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc,
+                                         int64_t stride_c, float alpha, float beta, const float* bias, void* stream) {
+  if (!std::isfinite(alpha) || !std::isfinite(beta)) return fail(AC_ERR_INVALID_VALUE, "alpha and beta must be finite");
+  if (((uintptr_t)bias & 3)) return fail(AC_ERR_INVALID_VALUE, "bias not aligned to 4 bytes");
+  return run_batched(plan, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, stream, 1, alpha, beta, bias);
 }
 
 adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out) {

@@ -1039,8 +1039,8 @@ __device__ __forceinline__ bool group_of_slot(const GroupArgs& a, const GroupChu
   return false;
 }
 
-template <int BM, int BN, int MS, int OUT, int DEPTH>
-__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a) {
+template <int BM, int BN, int MS, int OUT, int DEPTH, bool EPI>
+__device__ __forceinline__ void grouped_kernel(const GroupArgs& a) {
   typedef TileShape<BM, BN, MS> S;
   typedef typename AccOf<MS>::T Acc;
   __shared__ __attribute__((aligned(16))) char smem[S::SMEM];
@@ -1093,7 +1093,18 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a
     for (int j = 0; j < S::TN; ++j) acc[i][j] = Acc{};
 
   tile_mainloop<BM, BN, MS, DEPTH>(g, m0, n0, 0, kt_total, acc, smem);
-  store_tile_c<BM, BN, MS, OUT == OUT_BF16>(acc, g, m0, n0, smem);
+  store_tile_c<BM, BN, MS, OUT == OUT_BF16, EPI>(acc, g, m0, n0, smem);
+}
+
+// The grouped kernel, and its form with the AddMM epilogue (C_old and the
+// bias row relative to each group's C).
+template <int BM, int BN, int MS, int OUT, int DEPTH>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped(GroupArgs a) {
+  grouped_kernel<BM, BN, MS, OUT, DEPTH, false>(a);
+}
+template <int BM, int BN, int MS, int OUT, int DEPTH>
+__global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_grouped_addmm(GroupArgs a) {
+  grouped_kernel<BM, BN, MS, OUT, DEPTH, true>(a);
 }
 
 // --------------------------------------------------------- stream-K kernel
@@ -2030,7 +2041,11 @@ hipError_t launch_persist(const Plan& p, const GemmArgs& g, hipStream_t st, bool
 template <int BM, int BN, int MS, int D>
 hipError_t launch_grouped(const Plan& p, const GroupArgs& a, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x), block(TileShape<BM, BN, MS>::NT);
-  if (obf)
+  if (a.g.epi && obf)
+    hipLaunchKernelGGL((k_grouped_addmm<BM, BN, MS, OUT_BF16, D>), grid, block, 0, st, a);
+  else if (a.g.epi)
+    hipLaunchKernelGGL((k_grouped_addmm<BM, BN, MS, OUT_F32, D>), grid, block, 0, st, a);
+  else if (obf)
     hipLaunchKernelGGL((k_grouped<BM, BN, MS, OUT_BF16, D>), grid, block, 0, st, a);
   else
     hipLaunchKernelGGL((k_grouped<BM, BN, MS, OUT_F32, D>), grid, block, 0, st, a);

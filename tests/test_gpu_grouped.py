@@ -15,7 +15,7 @@ import numpy as np
 import pytest
 
 import paper_2608_10803_amd as ac
-from oracle import gemm_ref, grouped_ref
+from oracle import addmm_ref, gemm_ref, grouped_ref
 from workloads import gen
 
 from gpu_util import BF16_CANARY, F32_CANARY, Out, to_device, tol, torch
@@ -256,22 +256,38 @@ def batched_case(batch, M, N, K, lda, ldb, ldc, stride_a, stride_b, stride_c, se
     return A, B
 
 
-def run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, stride_a, stride_b, stride_c, dtype):
-    """One adaptcore_batched_matmul; returns (values (batch, M, N), every
-    element outside the C matrices still holds its canary)."""
+def run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, stride_a, stride_b, stride_c, dtype, addmm=None):
+    """One adaptcore_batched_matmul (or, with addmm = (c_old, alpha, beta,
+    bias), adaptcore_batched_addmm with C holding c_old: (batch, M, N) fp32
+    values or 16-bit patterns); returns (values (batch, M, N), every element
+    outside the C matrices still holds its canary)."""
     t = torch()
     n = (batch - 1) * stride_c + (M - 1) * ldc + N + 2 * ldc
     if dtype == F32:
         host = np.full(n, F32_CANARY, np.float32)
+    else:
+        host = np.full(n, BF16_CANARY, np.uint16)
+    if addmm is not None:
+        for b in range(batch):
+            for i in range(M):
+                o = ldc + b * stride_c + i * ldc
+                host[o:o + N] = addmm[0][b, i]
+    if dtype == F32:
         dev = t.from_numpy(host.copy()).to("cuda")
         addr = dev.data_ptr() + 4 * ldc
     else:
-        host = np.full(n, BF16_CANARY, np.uint16)
         dev = t.from_numpy(host.view(np.int16).copy()).to("cuda")
         addr = dev.data_ptr() + 2 * ldc
     Ad = t.from_numpy(A.view(np.int16)).to("cuda")
     Bd = t.from_numpy(B.view(np.int16)).to("cuda")
-    ac.adaptcore_batched_matmul(plan, Ad.data_ptr(), lda, stride_a, Bd.data_ptr(), ldb, stride_b, addr, ldc, stride_c, 0)
+    if addmm is None:
+        ac.adaptcore_batched_matmul(plan, Ad.data_ptr(), lda, stride_a, Bd.data_ptr(), ldb, stride_b, addr, ldc,
+                                    stride_c, 0)
+    else:
+        _, alpha, beta, bias = addmm
+        bd = t.from_numpy(np.ascontiguousarray(bias, np.float32)).to("cuda") if bias is not None else None
+        ac.adaptcore_batched_addmm(plan, Ad.data_ptr(), lda, stride_a, Bd.data_ptr(), ldb, stride_b, addr, ldc,
+                                   stride_c, alpha, beta, bd.data_ptr() if bd is not None else 0, 0)
     t.cuda.synchronize()
     raw = dev.cpu().numpy()
     raw = raw if dtype == F32 else raw.view(np.uint16)
@@ -339,6 +355,38 @@ def test_batched_default_plans(case):
         assert ok
         err = gemm_ref.err_metric(vals.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N))
         assert err <= tol(dtype), (case, dtype, err)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+def test_batched_addmm_every_configuration(dtype):
+    """The batched product with the AddMM epilogue (alpha, beta, a bias row
+    shared by the batches) on every batched configuration, padded leading
+    dimensions and gaps between the matrices; then beta = 0 with NaN in C."""
+    batch, M, N, K = 4, 70, 300, 197
+    lda, ldb, ldc = K + 3, N + 5, N + 7
+    sa, sb, sc = M * lda + 11, K * ldb + 13, M * ldc + 17
+    A, B = batched_case(batch, M, N, K, lda, ldb, ldc, sa, sb, sc, seed=41)
+    if dtype == F32:
+        stored = gen.uniform_f32(batch * M, N, 42, -2.0, 2.0).reshape(batch, M, N)
+        old = stored.astype(np.float64)
+    else:
+        stored = gen.uniform_bf16(batch * M, N, 42, -2.0, 2.0).reshape(batch, M, N)
+        old = gemm_ref.decode(stored.reshape(-1, N)).reshape(batch, M, N)
+    bias = gen.uniform_f32(1, N, 43).reshape(-1)
+    C_ref, D = addmm_ref.batched_addmm(A, B, old, batch, M, N, K, lda, ldb, sa, sb, -0.75, 1.5, bias)
+    for key in batched_keys(batch, M, N, K, dtype):
+        plan = ac.adaptcore_batched_plan_variant(batch, M, N, K, dtype, 0, key)
+        vals, ok = run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, sa, sb, sc, dtype,
+                               addmm=(stored, -0.75, 1.5, bias))
+        assert ok, "write outside the C matrices %s" % hex(key)
+        err = gemm_ref.err_metric(vals.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N))
+        assert err <= tol(dtype), "err %.3g %s" % (err, hex(key))
+    nan = np.full_like(stored, np.nan) if dtype == F32 else np.full_like(stored, 0x7FC0)
+    C_ref, D = addmm_ref.batched_addmm(A, B, None, batch, M, N, K, lda, ldb, sa, sb, 2.0, 0.0, bias)
+    plan = ac.adaptcore_batched_plan(batch, M, N, K, dtype)
+    vals, ok = run_batched(plan, A, B, batch, M, N, K, lda, ldb, ldc, sa, sb, sc, dtype, addmm=(nan, 2.0, 0.0, bias))
+    err = gemm_ref.err_metric(vals.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N))
+    assert ok and err <= tol(dtype), err
 
 
 def test_batched_k_zero():

@@ -181,6 +181,15 @@ def test_batched_argument_validation():
     with pytest.raises(ac.AdaptCoreError) as e:
         ac.adaptcore_batched_matmul(hb, 0x1000, 1 << 23, 128, 0x2000, 32, 256, 0x3000, 32, 512)
     assert e.value.status == ac.AC_ERR_UNSUPPORTED
+    # the AddMM form: the same checks, plus finite scalars and an aligned bias
+    for alpha, beta, bias in [(float("nan"), 1.0, 0), (1.0, float("-inf"), 0), (1.0, 1.0, 0x5001)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_batched_addmm(hb, *ok, alpha, beta, bias)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    for args in bad:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_batched_addmm(hb, *args, 1.0, 0.0, 0)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE, args
     # the smallest stride that keeps the C matrices apart is accepted before any GPU work is needed
     for h in (ac.adaptcore_batched_plan(0, 16, 32, 8), ac.adaptcore_batched_plan(3, 0, 32, 8)):
         ac.adaptcore_batched_matmul(h, 0x1000, 8, 128, 0x2000, 32, 256, 0x3000, 32, 15 * 32 + 32)

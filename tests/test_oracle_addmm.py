@@ -110,7 +110,28 @@ def pin_k_zero(ar):
     return True
 
 
-PINS = [pin_brute_force, pin_no_bias, pin_plain_product, pin_beta_zero_ignores_c_old, pin_k_zero]
+def pin_batched_is_per_batch(ar):
+    """Every batch of the batched form equals the single form on that batch's
+    matrices (padded rows, gaps between the matrices, a different C_old per
+    batch, one bias), bit for bit."""
+    batch, M, N, K = 3, 4, 6, 5
+    lda, ldb, sa, sb = K + 2, N + 1, M * (K + 2) + 3, K * (N + 1) + 7
+    A = gen.uniform_bf16(1, (batch - 1) * sa + M * lda, 350).reshape(-1)
+    B = gen.uniform_bf16(1, (batch - 1) * sb + K * ldb, 351).reshape(-1)
+    C_old = gen.uniform_f32(batch * M, N, 352).astype(np.float64).reshape(batch, M, N)
+    bias = gen.uniform_f32(1, N, 353).reshape(-1).astype(np.float64)
+    C, D = ar.batched_addmm(A, B, C_old, batch, M, N, K, lda, ldb, sa, sb, -1.5, 0.5, bias)
+    for b in range(batch):
+        Ab = A[b * sa:b * sa + M * lda].reshape(M, lda)[:, :K]
+        Bb = B[b * sb:b * sb + K * ldb].reshape(K, ldb)[:, :N]
+        Cb, Db = ar.addmm(np.ascontiguousarray(Ab), np.ascontiguousarray(Bb), C_old[b], -1.5, 0.5, bias)
+        if not (np.array_equal(C[b], Cb) and np.array_equal(D[b], Db)):
+            return False
+    return True
+
+
+PINS = [pin_brute_force, pin_no_bias, pin_plain_product, pin_beta_zero_ignores_c_old, pin_k_zero,
+        pin_batched_is_per_batch]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -155,6 +176,9 @@ MUTATIONS = [
     ("bias along the rows", "reshape(1, C.shape[1])", "reshape(C.shape[0], 1)"),
     ("alpha applied to C_old", "C = C + beta * Co", "C = C + alpha * beta * Co"),
     ("bias magnitude missing from D", "D = D + np.abs(b)", "D = D"),
+    ("batched A read with the B stride", "batched_gemm(A, B, batch, M, N, K, lda, ldb, stride_a, stride_b",
+     "batched_gemm(A, B, batch, M, N, K, lda, ldb, stride_b, stride_b"),
+    ("batched bias along the rows", "reshape(1, 1, N)", "reshape(1, N, 1)"),
 ]
 
 
@@ -169,6 +193,8 @@ def test_mutations_are_caught(name, old, new):
         # the mutated module imports the real plain-product oracle
         with open(os.path.join(pkg, "gemm_ref.py"), "w") as f:
             f.write("from oracle.gemm_ref import *  # noqa\n")
+        with open(os.path.join(pkg, "grouped_ref.py"), "w") as f:
+            f.write("from oracle.grouped_ref import *  # noqa\n")
         path = os.path.join(pkg, "addmm_ref.py")
         with open(path, "w") as f:
             f.write(src.replace(old, new))
