@@ -289,6 +289,21 @@ adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const in
                                           int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
                                           int64_t ldc, void* stream);
 
+/* The grouped product with the AddMM epilogue of adaptcore_addmm (GroupMM
+ * and AddMM, Section 6.5): the covered rows r of group g get
+ * C[r] = alpha * (A[r] * B_g) + beta * C_old[r] + bias_g, in fp32 before the
+ * rounding to C's type, C_old read only when beta != 0; bias_g is the row of
+ * N fp32 values at bias + g * stride_bias (stride_bias = 0 shares one row;
+ * bias NULL: none). Arguments and validation as adaptcore_grouped_matmul,
+ * plus finite alpha and beta, a 4-byte-aligned bias and 0 <= stride_bias <
+ * 2^40 (AC_ERR_INVALID_VALUE); the caller guarantees that bias holds
+ * (groups - 1) * stride_bias + N values. Rows no group covers keep their
+ * contents. */
+adaptcore_status adaptcore_grouped_addmm(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
+                                         int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
+                                         int64_t ldc, float alpha, float beta, const float* bias, int64_t stride_bias,
+                                         void* stream);
+
 /* ---- Batched product (BatchMM) ---------------------------------------------
  * The other batched operator the paper replaces in its end-to-end models
  * (BatchMM, Section 6.5; operator scope, Section 7), in the strided form:

@@ -24,13 +24,16 @@ output are measured against the same relative bars as a plain product.
 
 The batched form (BatchMM with the same epilogue) applies it to every batch
 of the strided batched product (grouped_ref.batched_gemm), with one bias row
-shared by all batches.
+shared by all batches; the grouped form (GroupMM with the same epilogue)
+applies it to the covered rows of the grouped product (grouped_ref), group g
+adding its own bias row, stored stride_bias values after group g-1's.
 
 Parity pins: tests/test_oracle_addmm.py (exact rational brute force of C and
 D on tiny inputs with mixed-sign alpha and beta, reduction to the plain
 product, beta == 0 ignoring a NaN C_old, K == 0, sampled entries equal to
 the full result, every batch of the batched form equal to the single form on
-that batch's matrices, and a mutation test).
+that batch's matrices, every group of the grouped form equal to the single
+form on that group's rows and bias row, and a mutation test).
 """
 import numpy as np
 
@@ -101,3 +104,27 @@ def batched_addmm(A, B, C_old, batch, M, N, K, lda, ldb, stride_a, stride_b, alp
         C = C + b
         D = D + np.abs(b)
     return C, D
+
+
+def grouped_addmm(A, B, counts, rows, N, K, lda, ldb, stride_b, C_old, alpha, beta, bias=None, stride_bias=0,
+                  fmt="bf16", lib=None):
+    """(C_ref, D, covered) of the grouped form, C_ref and D of shape (rows, N)
+    (uncovered rows 0); C_old has shape (rows, N); bias is a flat array with
+    group g's row at g * stride_bias."""
+    P, Dp, covered = grouped_ref.grouped_gemm(A, B, counts, rows, N, K, lda, ldb, stride_b, fmt=fmt, lib=lib)
+    alpha = float(alpha)
+    beta = float(beta)
+    C = alpha * P
+    D = abs(alpha) * Dp
+    if beta != 0.0:
+        Co = np.where(covered[:, None], np.asarray(C_old, np.float64).reshape(rows, N), 0.0)
+        C = C + beta * Co
+        D = D + abs(beta) * np.abs(Co)
+    if bias is not None:
+        bias = np.asarray(bias, np.float64).reshape(-1)
+        for g, (s, e) in enumerate(grouped_ref.group_rows(counts, rows)):
+            if e > s:
+                b = bias[g * stride_bias:g * stride_bias + N].reshape(1, N)
+                C[s:e] = C[s:e] + b
+                D[s:e] = D[s:e] + np.abs(b)
+    return C, D, covered

@@ -150,6 +150,9 @@ def lib():
         L.adaptcore_batched_addmm.argtypes = [p, p, i64, i64, p, i64, i64, p, i64, i64, ctypes.c_float,
                                               ctypes.c_float, p, p]
         L.adaptcore_batched_addmm.restype = i32
+        L.adaptcore_grouped_addmm.argtypes = [p, p, p, i64, p, i64, i64, p, i64, ctypes.c_float, ctypes.c_float, p,
+                                              i64, p]
+        L.adaptcore_grouped_addmm.restype = i32
         L.adaptcore_reserve_workspace.argtypes = [p, i64]
         L.adaptcore_reserve_workspace.restype = i32
         L.adaptcore_plan_info.argtypes = [p, ctypes.POINTER(PlanDesc)]
@@ -247,6 +250,14 @@ def adaptcore_grouped_plan_variant(rows, groups, N, K, dtype, layouts, variant_k
 def adaptcore_grouped_matmul(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream=0):
     """Grouped product on `stream`; counts, A, B, C are device addresses."""
     return _check(lib().adaptcore_grouped_matmul(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream))
+
+
+def adaptcore_grouped_addmm(plan, counts, A, lda, B, ldb, stride_b, C, ldc, alpha=1.0, beta=0.0, bias=0,
+                            stride_bias=0, stream=0):
+    """Grouped product with the AddMM epilogue on `stream` (bias row of group
+    g at bias + g * stride_bias floats; bias = 0 for none)."""
+    return _check(lib().adaptcore_grouped_addmm(plan, counts, A, lda, B, ldb, stride_b, C, ldc, alpha, beta, bias,
+                                                stride_bias, stream))
 
 
 def adaptcore_batched_plan(batch, M, N, K, dtype=AC_BF16_BF16OUT, layouts=AC_LAYOUT_ROW_ROW):

@@ -474,9 +474,15 @@ const adaptcore_plan_t* adaptcore_grouped_plan_variant(int64_t rows, int64_t gro
   return pp;
 }
 
-adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
-                                          int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
-                                          int64_t ldc, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// One call of a grouped plan; epi != 0 selects the AddMM epilogue (bias rows
+// stride_bias apart, one per group).
+adaptcore_status run_grouped(const adaptcore_plan_t* plan, const int32_t* counts, const void* A, int64_t lda,
+                             const void* B, int64_t ldb, int64_t stride_b, void* C, int64_t ldc, void* stream,
+                             int epi, float alpha, float beta, const float* bias, int64_t stride_bias) {
   if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
   const ac::Plan& p = plan->p;
   if (p.family != ac::FAM_GROUPED)
@@ -511,9 +517,14 @@ adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const in
   a.g.tiles_m = p.pm;
   a.g.tiles_n = p.pn;
   a.g.swizzle = p.swizzle;
+  a.g.epi = epi;
+  a.g.alpha = alpha;
+  a.g.beta = beta;
+  a.g.bias = bias;
   a.counts = counts;
   a.rows = rows;
   a.stride_b = stride_b;
+  a.stride_bias = stride_bias;
   a.groups = (int)p.groups;
   a.slots = p.pm;
   const hipError_t e = ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_grouped_plan(p, a, static_cast<hipStream_t>(stream))
@@ -521,6 +532,27 @@ adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const in
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add(1, std::memory_order_relaxed);
   return AC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+adaptcore_status adaptcore_grouped_matmul(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
+                                          int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
+                                          int64_t ldc, void* stream) {
+  return run_grouped(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream, 0, 1.0f, 0.0f, nullptr, 0);
+}
+
+adaptcore_status adaptcore_grouped_addmm(const adaptcore_plan_t* plan, const int32_t* counts, const void* A,
+                                         int64_t lda, const void* B, int64_t ldb, int64_t stride_b, void* C,
+                                         int64_t ldc, float alpha, float beta, const float* bias, int64_t stride_bias,
+                                         void* stream) {
+  if (!std::isfinite(alpha) || !std::isfinite(beta)) return fail(AC_ERR_INVALID_VALUE, "alpha and beta must be finite");
+  if (((uintptr_t)bias & 3)) return fail(AC_ERR_INVALID_VALUE, "bias not aligned to 4 bytes");
+  if (stride_bias < 0 || stride_bias >= (1LL << 40))
+    return fail(AC_ERR_INVALID_VALUE, "stride_bias must be in [0, 2^40)");
+  return run_grouped(plan, counts, A, lda, B, ldb, stride_b, C, ldc, stream, 1, alpha, beta, bias, stride_bias);
 }
 
 const adaptcore_plan_t* adaptcore_batched_plan(int64_t batch, int64_t M, int64_t N, int64_t K, int32_t dtype,

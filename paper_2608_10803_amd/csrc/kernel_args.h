@@ -66,6 +66,7 @@ struct GroupArgs {
   int64_t stride_a;       // strided batch: elements between two A matrices (else 0)
   int64_t stride_b;       // elements between the B matrices of two groups
   int64_t stride_c;       // strided batch: elements between two C matrices (else 0)
+  int64_t stride_bias;    // AddMM epilogue: fp32 values between the bias rows of two groups
   int groups;
   int slots;              // row-tile slots launched (an upper bound of the tiles along M)
   int tiles_per_group;    // strided batch: row tiles of every group

@@ -1082,6 +1082,7 @@ __device__ __forceinline__ void grouped_kernel(const GroupArgs& a) {
   g.A += row0 * g.lda + (int64_t)grp * a.stride_a;
   g.B += (int64_t)grp * a.stride_b;
   g.C = static_cast<char*>(g.C) + (row0 * g.ldc + (int64_t)grp * a.stride_c) * (OUT == OUT_BF16 ? 2 : 4);
+  if (EPI && g.bias != nullptr) g.bias += (int64_t)grp * a.stride_bias;
   g.M = rows_g;
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int kt_total = (int)((g.K + S::BK - 1) / S::BK);

@@ -99,6 +99,24 @@ class Case:
         return vals, ok, canary_rows
 
 
+    def run_addmm(self, plan, dtype, ldc, stored, alpha, beta, bias, stride_bias):
+        """adaptcore_grouped_addmm with C holding `stored` (rows x N fp32
+        values or 16-bit patterns); returns (values, canaries around C ok)."""
+        t = torch()
+        Ad, a = to_device(self.A, self.lda, 0)
+        Bd = t.from_numpy(self.B.view(np.int16)).to("cuda")
+        cnt = t.from_numpy(self.counts).to("cuda")
+        bd = t.from_numpy(np.ascontiguousarray(bias, np.float32)).to("cuda")
+        out = Out(self.rows, self.N, ldc, dtype)
+        out.fill(stored)
+        ac.adaptcore_grouped_addmm(plan, cnt.data_ptr(), a, self.lda, Bd.data_ptr(), self.ldb, self.stride_b,
+                                   out.addr, ldc, alpha, beta, bd.data_ptr(), stride_bias, 0)
+        t.cuda.synchronize()
+        vals, ok = out.read()
+        del Ad, Bd, cnt, bd
+        return vals, ok
+
+
 def check(case, vals, ok, canary_rows, dtype, ref, label):
     C_ref, D, cov = ref
     assert ok, "write outside C %s" % label
@@ -126,6 +144,35 @@ def test_every_grouped_configuration(dtype):
         note("grouped", label)
         vals, ok, canary = case.run(plan, dtype, ldc=c["N"] + 7)
         check(case, vals, ok, canary, dtype, ref, label)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+def test_grouped_addmm_every_configuration(dtype):
+    """The grouped product with the AddMM epilogue (a bias row per group) on
+    every grouped configuration of the ragged case; rows no group covers
+    keep their previous contents."""
+    c = RAGGED
+    rows, N, K, G = c["rows"], c["N"], c["K"], len(c["counts"])
+    case = Case(c["counts"], rows, N, K, lda=K + 5, ldb=N + 3, stride_b=K * (N + 3) + 11, seed=12)
+    if dtype == F32:
+        stored = gen.uniform_f32(rows, N, 44, -2.0, 2.0)
+        old = stored.astype(np.float64)
+    else:
+        stored = gen.uniform_bf16(rows, N, 44, -2.0, 2.0)
+        old = gemm_ref.decode(stored)
+    sbias = N + 9
+    bias = gen.uniform_f32(1, (G - 1) * sbias + N, 45).reshape(-1)
+    Apad = np.zeros((rows, K + 5), np.uint16)
+    Apad[:, :K] = case.A
+    C_ref, D, cov = addmm_ref.grouped_addmm(Apad, case.B, case.counts, rows, N, K, K + 5, N + 3, case.stride_b, old,
+                                            1.25, -0.5, bias, sbias)
+    for key in grouped_keys(rows, G, N, K, dtype):
+        plan = ac.adaptcore_grouped_plan_variant(rows, G, N, K, dtype, 0, key)
+        vals, ok = case.run_addmm(plan, dtype, N + 7, stored, 1.25, -0.5, bias, sbias)
+        assert ok, "write outside C %s" % hex(key)
+        assert np.array_equal(vals[~cov], old[~cov]), "an uncovered row changed %s" % hex(key)
+        err = gemm_ref.err_metric(vals[cov], C_ref[cov], D[cov])
+        assert err <= tol(dtype), "err %.3g %s" % (err, hex(key))
 
 
 SHAPES = [

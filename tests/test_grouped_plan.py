@@ -113,6 +113,15 @@ def test_argument_validation():
         with pytest.raises(ac.AdaptCoreError) as e:
             ac.adaptcore_grouped_matmul(hg, *args)
         assert e.value.status == ac.AC_ERR_INVALID_VALUE, args
+    # the AddMM form: the same checks, plus finite scalars, an aligned bias and its stride
+    for extra in [(float("nan"), 1.0, 0, 0), (1.0, 1.0, 0x5002, 0), (1.0, 1.0, 0x5000, -1), (1.0, 1.0, 0x5000, 1 << 40)]:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_grouped_addmm(hg, *good, *extra)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE, extra
+    for args in bad:
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_grouped_addmm(hg, *args, 1.0, 0.0, 0, 0)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE, args
     for args in [(0x4000, 0x1000, 1 << 23, 0x2000, 32, 512, 0x3000, 32),
                  (0x4000, 0x1000, 16, 0x2000, 1 << 23, 512, 0x3000, 32)]:
         with pytest.raises(ac.AdaptCoreError) as e:

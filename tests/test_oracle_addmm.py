@@ -130,8 +130,33 @@ def pin_batched_is_per_batch(ar):
     return True
 
 
+def pin_grouped_is_per_group(ar):
+    """Every group of the grouped form equals the single form on that group's
+    rows with its own bias row (empty and truncated groups included), bit
+    for bit; uncovered rows stay 0."""
+    counts, rows, N, K = [3, 0, 4, -2, 9], 12, 6, 5
+    stride_b, stride_bias = K * N + 3, N + 2
+    A = gen.uniform_bf16(rows, K, 360)
+    mats = [gen.uniform_bf16(K, N, 361 + g) for g in range(len(counts))]
+    B = np.zeros(stride_b * (len(counts) - 1) + K * N, np.uint16)
+    for g, m in enumerate(mats):
+        B[g * stride_b:g * stride_b + K * N] = m.reshape(-1)
+    C_old = gen.uniform_f32(rows, N, 366).astype(np.float64)
+    bias = gen.uniform_f32(1, stride_bias * (len(counts) - 1) + N, 367).reshape(-1).astype(np.float64)
+    C, D, cov = ar.grouped_addmm(A, B, counts, rows, N, K, K, N, stride_b, C_old, 0.5, -2.0, bias, stride_bias)
+    bounds = [(0, 3), (3, 3), (3, 7), (7, 7), (7, 12)]  # the last group is cut at the capacity
+    for g, (s, e) in enumerate(bounds):
+        if e <= s:
+            continue
+        Cg, Dg = ar.addmm(np.ascontiguousarray(A[s:e]), mats[g], C_old[s:e], 0.5, -2.0,
+                          bias[g * stride_bias:g * stride_bias + N])
+        if not (np.array_equal(C[s:e], Cg) and np.array_equal(D[s:e], Dg)):
+            return False
+    return bool(cov.all()) and len(cov) == rows
+
+
 PINS = [pin_brute_force, pin_no_bias, pin_plain_product, pin_beta_zero_ignores_c_old, pin_k_zero,
-        pin_batched_is_per_batch]
+        pin_batched_is_per_batch, pin_grouped_is_per_group]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -179,6 +204,8 @@ MUTATIONS = [
     ("batched A read with the B stride", "batched_gemm(A, B, batch, M, N, K, lda, ldb, stride_a, stride_b",
      "batched_gemm(A, B, batch, M, N, K, lda, ldb, stride_b, stride_b"),
     ("batched bias along the rows", "reshape(1, 1, N)", "reshape(1, N, 1)"),
+    ("grouped bias of the previous group", "b = bias[g * stride_bias:g * stride_bias + N]",
+     "b = bias[max(g - 1, 0) * stride_bias:max(g - 1, 0) * stride_bias + N]"),
 ]
 
 
