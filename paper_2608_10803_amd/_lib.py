@@ -432,3 +432,82 @@ def addmm_tensors(A, B, C, alpha=1.0, beta=0.0, bias=None, stream=None, plan=Non
     s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
     adaptcore_addmm(plan, A.data_ptr(), lda, B.data_ptr(), ldb, C.data_ptr(), ldc, float(alpha), float(beta), bp, s)
     return C
+
+
+def _dtype_code(A, B, C):
+    import torch
+    if A.dtype != B.dtype or A.dtype not in (torch.bfloat16, torch.float16):
+        raise TypeError("A and B must both be bfloat16 or both float16")
+    f16 = A.dtype == torch.float16
+    if C.dtype == torch.float32:
+        return AC_F16_F32OUT if f16 else AC_BF16_F32OUT
+    if C.dtype == A.dtype:
+        return AC_F16_F16OUT if f16 else AC_BF16_BF16OUT
+    raise TypeError("C must be float32 or the input type")
+
+
+def _rows_contiguous(t, name):
+    if not t.is_cuda or (t.shape[-1] > 1 and t.stride(-1) != 1):
+        raise ValueError("%s must be a GPU tensor with contiguous rows" % name)
+
+
+def bmm_tensors(A, B, C, alpha=None, beta=0.0, bias=None, stream=None, plan=None):
+    """C[b] = A[b] @ B[b] for 3-D torch tensors on the GPU (batch x M x K,
+    batch x K x N, batch x M x N; contiguous rows, any batch stride, B may be
+    broadcast with batch stride 0). With alpha given: C[b] = alpha * A[b] @
+    B[b] + beta * C[b] + bias (bias None or N float32 values), in place.
+    Marshals pointers, leading dimensions and strides only."""
+    import torch
+    batch, M, K = A.shape
+    batch2, K2, N = B.shape
+    if batch2 != batch or K2 != K or tuple(C.shape) != (batch, M, N):
+        raise ValueError("shape mismatch")
+    dt = _dtype_code(A, B, C)
+    for t, n in ((A, "A"), (B, "B"), (C, "C")):
+        _rows_contiguous(t, n)
+    lda, ldb, ldc = max(A.stride(1), K, 1), max(B.stride(1), N, 1), max(C.stride(1), N, 1)
+    if plan is None:
+        plan = adaptcore_batched_plan(batch, M, N, K, dt)
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    if alpha is None:
+        adaptcore_batched_matmul(plan, A.data_ptr(), lda, A.stride(0), B.data_ptr(), ldb, B.stride(0), C.data_ptr(),
+                                 ldc, C.stride(0), s)
+    else:
+        bp = 0
+        if bias is not None:
+            if bias.dtype != torch.float32 or bias.numel() != N or not bias.is_cuda or not bias.is_contiguous():
+                raise ValueError("bias must be a contiguous float32 GPU tensor of N elements")
+            bp = bias.data_ptr()
+        adaptcore_batched_addmm(plan, A.data_ptr(), lda, A.stride(0), B.data_ptr(), ldb, B.stride(0), C.data_ptr(),
+                                ldc, C.stride(0), float(alpha), float(beta), bp, s)
+    return C
+
+
+def grouped_mm_tensors(A, B, counts, C, stream=None, plan=None):
+    """The grouped product for torch tensors on the GPU: A (rows x K) holds
+    the groups' rows one after another, B (groups x K x N, or K x N shared
+    by all groups), counts an int32 GPU tensor of `groups` row counts (read by
+    the kernel, never by the host), C (rows x N). Contiguous rows required.
+    Marshals pointers, leading dimensions and strides only."""
+    import torch
+    rows, K = A.shape
+    if B.dim() == 2:
+        groups, stride_b = counts.numel(), 0
+        K2, N = B.shape
+        ldb = max(B.stride(0), N, 1)
+    else:
+        groups, K2, N = B.shape
+        stride_b, ldb = B.stride(0), max(B.stride(1), N, 1)
+    if K2 != K or tuple(C.shape) != (rows, N) or counts.numel() != groups:
+        raise ValueError("shape mismatch")
+    if counts.dtype != torch.int32 or not counts.is_cuda or not counts.is_contiguous():
+        raise ValueError("counts must be a contiguous int32 GPU tensor")
+    dt = _dtype_code(A, B, C)
+    for t, n in ((A, "A"), (B, "B"), (C, "C")):
+        _rows_contiguous(t, n)
+    if plan is None:
+        plan = adaptcore_grouped_plan(rows, groups, N, K, dt)
+    s = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+    adaptcore_grouped_matmul(plan, counts.data_ptr(), A.data_ptr(), max(A.stride(0), K, 1), B.data_ptr(), ldb,
+                             stride_b, C.data_ptr(), max(C.stride(0), N, 1), s)
+    return C

@@ -477,3 +477,56 @@ def test_fp16_grouped_and_batched():
     C_ref, D = grouped_ref.batched_gemm(A, B, batch, M, N, K, K, N, M * K, K * N, fmt="fp16")
     got = np.where(np.abs(got - C_ref) <= 2.0 ** -25, C_ref, got)
     assert gemm_ref.err_metric(got.reshape(-1, N), C_ref.reshape(-1, N), D.reshape(-1, N)) <= gemm_ref.TOL["fp16"]
+
+
+def test_tensor_bindings():
+    """bmm_tensors (plain, with the AddMM epilogue, and with B broadcast over
+    the batch) and grouped_mm_tensors (per-group and shared B) against the
+    batched and grouped oracles."""
+    t = torch()
+    batch, M, N, K = 3, 50, 70, 90
+    A = gen.uniform_bf16(batch * M, K, 71)
+    B = gen.uniform_bf16(batch * K, N, 72)
+    Ad = t.from_numpy(A.view(np.int16)).cuda().view(t.bfloat16).view(batch, M, K)
+    Bd = t.from_numpy(B.view(np.int16)).cuda().view(t.bfloat16).view(batch, K, N)
+    C = t.empty(batch, M, N, dtype=t.float32, device="cuda")
+    ac.bmm_tensors(Ad, Bd, C)
+    t.cuda.synchronize()
+    C_ref, D = grouped_ref.batched_gemm(A.reshape(-1), B.reshape(-1), batch, M, N, K, K, N, M * K, K * N)
+    err = gemm_ref.err_metric(C.cpu().numpy().reshape(-1, N).astype(np.float64), C_ref.reshape(-1, N),
+                              D.reshape(-1, N))
+    assert err <= tol(F32), err
+    # AddMM epilogue on the same operands
+    old = gen.uniform_f32(batch * M, N, 73).reshape(batch, M, N)
+    bias = gen.uniform_f32(1, N, 74).reshape(-1)
+    C = t.from_numpy(old.copy()).cuda()
+    ac.bmm_tensors(Ad, Bd, C, alpha=0.5, beta=-1.0, bias=t.from_numpy(bias).cuda())
+    t.cuda.synchronize()
+    R, DR = addmm_ref.batched_addmm(A.reshape(-1), B.reshape(-1), old.astype(np.float64), batch, M, N, K, K, N, M * K,
+                                    K * N, 0.5, -1.0, bias)
+    err = gemm_ref.err_metric(C.cpu().numpy().reshape(-1, N).astype(np.float64), R.reshape(-1, N), DR.reshape(-1, N))
+    assert err <= tol(F32), err
+    # B broadcast over the batch (batch stride 0)
+    Bb = Bd[0:1].expand(batch, K, N)
+    C = t.empty(batch, M, N, dtype=t.float32, device="cuda")
+    ac.bmm_tensors(Ad, Bb, C)
+    t.cuda.synchronize()
+    C_ref, D = grouped_ref.batched_gemm(A.reshape(-1), B.reshape(-1), batch, M, N, K, K, N, M * K, 0)
+    err = gemm_ref.err_metric(C.cpu().numpy().reshape(-1, N).astype(np.float64), C_ref.reshape(-1, N),
+                              D.reshape(-1, N))
+    assert err <= tol(F32), err
+    # grouped: 3 groups over 140 rows (the last 10 rows uncovered)
+    counts = np.array([60, 0, 70], np.int32)
+    rows = 140
+    Ag = gen.uniform_bf16(rows, K, 75)
+    Agd = t.from_numpy(Ag.view(np.int16)).cuda().view(t.bfloat16)
+    cnt = t.from_numpy(counts).cuda()
+    for shared in (False, True):
+        Bg = Bd[0] if shared else Bd
+        Cg = t.zeros(rows, N, dtype=t.float32, device="cuda")
+        ac.grouped_mm_tensors(Agd, Bg, cnt, Cg)
+        t.cuda.synchronize()
+        R, DR, cov = grouped_ref.grouped_gemm(Ag, B.reshape(-1), counts, rows, N, K, K, N, 0 if shared else K * N)
+        got = Cg.cpu().numpy().astype(np.float64)
+        err = gemm_ref.err_metric(got[cov], R[cov], DR[cov])
+        assert err <= tol(F32) and not got[~cov].any(), (shared, err)
