@@ -20,7 +20,7 @@ from oracle import gemm_ref
 from oracle import layout_ref
 from workloads import gen
 
-from gpu_util import all_candidates, check, fmt_of, forced_plan, fp32_out, run, run_addmm, torch
+from gpu_util import all_candidates, check, fmt_of, forced_plan, run, run_addmm, torch
 
 pytestmark = pytest.mark.gpu
 

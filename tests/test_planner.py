@@ -11,7 +11,6 @@ import os
 import random
 import re
 import threading
-from fractions import Fraction
 
 import pytest
 
