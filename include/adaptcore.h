@@ -2,7 +2,8 @@
  * adaptcore.h -- C ABI of the adaptive dynamic-shape GEMM library for AMD
  * Instinct MI355X (gfx950).
  *
- * The library computes C = A * B for dense matrices of arbitrary (M, N, K),
+ * The library computes C = A * B for dense matrices of arbitrary (M, N, K)
+ * (also with an AddMM epilogue, and as grouped and strided batched products),
  * following "Adaptive Matrix Multiplication for Dynamic Shapes on Ascend
  * NPUs" (AdaptCore), re-designed for gfx950:
  *   - a shape is mapped to a template of the 2D tiling taxonomy (Section 4.2:
@@ -17,7 +18,8 @@
  *   - All functions are extern "C", never throw, and report failure through
  *     the return code (or NULL); adaptcore_last_error() then returns a
  *     thread-local message describing the last failure of the calling thread.
- *   - Matrices are dense, row-major, with leading dimensions in ELEMENTS.
+ *   - Matrices are dense and row-major (plain products may declare A or B
+ *     column-major, AC_LAYOUT_*), with leading dimensions in ELEMENTS.
  *     A is M x K (lda >= max(1, K)), B is K x N (ldb >= max(1, N)),
  *     C is M x N (ldc >= max(1, N)). Inputs are bf16 or fp16 (raw 16-bit
  *     storage); accumulation is always fp32; C is fp32 or 16-bit in the
@@ -54,6 +56,8 @@ typedef enum {
   AC_F16_F32OUT = 2,   /* fp16 inputs, C is fp32 */
   AC_F16_F16OUT = 3    /* fp16 inputs, C is fp16, rounded to nearest even */
 } adaptcore_dtype;
+/* The fp16 codes under their longer names. */
+enum { AC_FP16_F32OUT = AC_F16_F32OUT, AC_FP16_FP16OUT = AC_F16_F16OUT };
 
 /* Operand layouts of plain products (adaptcore_plan, adaptcore_matmul,
  * adaptcore_addmm), a bit set: AC_LAYOUT_A_COL = A stored column-major

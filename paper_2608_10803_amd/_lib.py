@@ -25,6 +25,7 @@ AC_BF16_F32OUT = 0
 AC_BF16_BF16OUT = 1
 AC_F16_F32OUT = 2
 AC_F16_F16OUT = 3
+AC_FP16_F32OUT, AC_FP16_FP16OUT = AC_F16_F32OUT, AC_F16_F16OUT
 AC_LAYOUT_ROW_ROW = 0
 AC_LAYOUT_A_COL = 1  # A stored column-major (lda >= M)
 AC_LAYOUT_B_COL = 2  # B stored column-major (ldb >= K)
