@@ -16,7 +16,7 @@ import paper_2608_10803_amd as ac
 from oracle import addmm_ref, gemm_ref, grouped_ref, layout_ref
 from workloads import gen
 
-from gpu_util import tol, torch
+from gpu_util import all_candidates, forced_plan, tol, torch
 
 pytestmark = pytest.mark.gpu
 
@@ -122,3 +122,31 @@ def test_graph_replays_match_the_oracle():
         R, D = bref
         got = Cb.cpu().numpy().astype(np.float64)
         assert gemm_ref.err_metric(got, R.reshape(-1, N), D.reshape(-1, N)) <= tol(F32), replay
+
+
+def test_capture_without_workspace_is_an_error():
+    """A split-K plan whose workspace (512 MiB) is larger than any other test
+    reserves, captured on a stream: the call refuses to allocate under
+    capture and reports AC_ERR_NOT_INITIALIZED (the operands are real
+    buffers of the full size all the same)."""
+    t = torch()
+    ac.adaptcore_init()
+    s = t.cuda.Stream()
+    M, N, K = 2048, 2048, 131072
+    keys = [c["variant_key"] for c in all_candidates(M, N, K, F32)
+            if c["family_name"] == "tile" and c["pk"] == 32 and c["tile_m"] == 256 and c["tile_n"] == 256]
+    assert keys
+    plan = forced_plan(M, N, K, F32, keys[0])
+    assert ac.adaptcore_plan_info(plan)["workspace_bytes"] >= 512 << 20
+    Ad = t.empty(M * K, dtype=t.bfloat16, device="cuda")
+    Bd = t.empty(K * N, dtype=t.bfloat16, device="cuda")
+    C = t.empty(M, N, dtype=t.float32, device="cuda")
+    g = t.cuda.CUDAGraph()
+    status = None
+    with t.cuda.graph(g, stream=s):
+        try:
+            ac.adaptcore_matmul(plan, Ad.data_ptr(), K, Bd.data_ptr(), N, C.data_ptr(), N, s.cuda_stream)
+        except ac.AdaptCoreError as e:
+            status = e.status
+        C.fill_(0.0)  # something to capture
+    assert status == ac.AC_ERR_NOT_INITIALIZED
