@@ -51,7 +51,7 @@ def sample_shapes(n_sweep=200, seed=11):
 
     order = sorted(range(len(sw)), key=lambda i: floor(sw[i]))
     pick = [sw[order[int(j)]] for j in np.linspace(0, len(sw) - 1, n_sweep)]
-    return pick + gen.skinny_m() + gen.small_mn_large_k() + write_bound_shapes()
+    return pick + gen.skinny_m() + gen.small_mn_large_k() + write_bound_shapes() + split_k_shapes()
 
 
 def write_bound_shapes(n=40, seed=12):
@@ -66,6 +66,23 @@ def write_bound_shapes(n=40, seed=12):
         K = int(round(math.exp(rng.uniform(math.log(8), math.log(400)))))
         c = 2.0 * M * N
         if c >= 0.5 * (2.0 * M * K + 2.0 * K * N + c) and c <= 4 * 2 ** 30:
+            out.append((M, N, K))
+    return out
+
+
+def split_k_shapes(n=40, seed=13):
+    """Shapes with few output tiles and a long K (the split-K regime of the
+    MultiCoreSplitK class), drawn on their own (not from the sweep): M, N
+    log-uniform in [1, 4096], K log-uniform in [2048, 100000], kept when
+    the output has fewer than 64 tiles of 32 x 32 and M*N*K <= 2^37. They
+    fix how the split kernels' cost changes with the number of workgroups
+    that share a CU."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        M, N = (int(round(math.exp(rng.uniform(0.0, math.log(4096))))) for _ in range(2))
+        K = int(round(math.exp(rng.uniform(math.log(2048), math.log(100000)))))
+        if -(-M // 32) * -(-N // 32) < 64 and M * N * K <= 2 ** 37:
             out.append((M, N, K))
     return out
 
