@@ -87,11 +87,13 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "sweep_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_10803_amd", "csrc", "kernels.hip")
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, dispatches=None):
     """HBM bytes per launch of `kernel` from the committed counter summary
     (FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what the counters read
-    for a 1 GiB copy), or None if the kernel is not in it or the kernel
-    source has changed since the counters were taken."""
+    for a 1 GiB copy), or None if the kernel is not in it, the kernel source
+    has changed since the counters were taken, or (given `dispatches`, the
+    kernel's launches in one pass of this run) the counters covered a
+    different set of launches, i.e. the planner now sends other shapes to it."""
     try:
         text = open(TRAFFIC_SUMMARY).read()
     except OSError:
@@ -105,6 +107,8 @@ def measured_traffic(kernel):
     for l in text.splitlines():
         cells = [c.strip().strip("`") for c in l.strip().strip("|").split("|")]
         if len(cells) >= 4 and cells[0] == kernel:
+            if dispatches is not None and int(cells[1]) != dispatches:
+                return None
             return (float(cells[2]) * ff + float(cells[3]) * fw) * 1024.0
     return None
 
@@ -688,7 +692,7 @@ def main():
     else:
         roofline = {"bound": "hbm", "achieved": round(dom["B"] / dom["t"] / 1e9, 1), "peak": 8000.0, "unit": "GB/s"}
         roofline["frac"] = round(roofline["achieved"] / 8000.0, 4)
-    traffic = measured_traffic(dom_name)
+    traffic = measured_traffic(dom_name, dom["n"])
     roofline.update({"traffic": round(traffic) if traffic else None,
                      "traffic_vs_algorithmic": round(traffic / (dom["B"] / dom["n"]), 3) if traffic else None,
                      "kernel": dom_name, "shapes": dom["shapes"],

@@ -593,14 +593,16 @@ adaptcore_hw_t default_hw() {
   h.enable_streamk = 0;
   // Constants fitted to per-configuration timings of shapes of the
   // dynamic-shape, decode-style and small-MN large-K workloads on one MI355X
-  // (squared log error of the model over every measured configuration). The
+  // (squared log error of the model over every measured configuration),
+  // evaluated with the workgroups-per-CU that the device reports for each
+  // kernel, which is what the planner uses at run time. The
   // launch cost is the measured per-kernel floor of back-to-back launches;
   // the XCD-order factor is the measured geomean time ratio of the swizzled
   // to the plain variant of a tile configuration (2,240 measured pairs).
   h.t_launch = 1.9e-06;
   h.t_mem_latency = 1.413e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 2.928e+10;
+  h.l2_bw_cu = 2.929e+10;
   h.unaligned_eta = 1;
   h.l2_hit = 5.38e-33;
   h.swizzle_gain = 0.935;
@@ -608,25 +610,33 @@ adaptcore_hw_t default_hw() {
   // 20-21, stream-K 22-29, direct 30-32, persistent 33-43; 0 = analytic
   // estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
-      2.853e-06, 2.085e-06, 1.938e-06, 3.052e-07, 5.513e-07, 2.327e-07, 5.38e-07, 3.959e-07,
-      1.119e-06, 2.57e-08, 9.358e-14, 1.231e-06, 1.259e-06, 1.399e-06, 1.399e-06, 1.761e-06,
-      1.964e-06, 6.729e-07, 6.937e-07, 8.013e-07, 2.712e-07, 2.062e-07, 4.752e-06, 2.484e-06,
-      3.088e-06, 1.534e-06, 1.002e-06, 1.065e-06, 0, 0, 9.358e-14, 9.358e-14,
-      3.967e-11, 2.943e-06, 2.043e-06, 0, 4.402e-07, 1.36e-07, 1.521e-07, 0,
+      2.914e-06, 2.083e-06, 1.999e-06, 9.358e-14, 1.874e-07, 9.358e-14, 5.407e-07, 3.958e-07,
+      1.119e-06, 9.358e-14, 9.358e-14, 1.258e-06, 1.297e-06, 1.372e-06, 1.402e-06, 1.945e-06,
+      2.035e-06, 6.562e-07, 5.774e-07, 7.79e-07, 2.24e-07, 1.964e-08, 4.516e-06, 2.397e-06,
+      3.032e-06, 9.358e-14, 8.328e-07, 9.315e-07, 5.998e-07, 4.265e-07, 2.493e-08, 9.358e-14,
+      9.358e-14, 2.932e-06, 2.063e-06, 0, 9.358e-14, 9.358e-14, 7.86e-07, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      2.31e-06, 1.15e-06, 3.06e-06, 2.529e-06, 1.161e-07, 7.499e-07, 3.608e-07, 3.72e-08,
-      1.987e-06, 1.794e-06, 2.042e-06, 7.819e-07, 1.181e-06, 2.927e-06, 4.094e-06, 6.485e-06,
-      7.368e-06, 7.191e-07, 1.131e-06, 1.954e-06, 9.492e-07, 1.392e-06, 2.626e-06, 1.239e-06,
-      8.657e-06, 9.358e-14, 1.078e-06, 2.487e-06, 0, 0, 9.358e-14, 3.788e-07,
-      1.919e-07, 9.099e-06, 5.193e-06, 0, 3.237e-06, 2.595e-06, 2.819e-06, 0,
+      1.949e-06, 1.152e-06, 2.724e-06, 2.698e-06, 6.777e-07, 1.342e-06, 1.78e-07, 9.358e-14,
+      1.945e-06, 1.677e-06, 1.82e-06, 1.005e-06, 1.334e-06, 2.89e-06, 3.685e-06, 7.394e-06,
+      1e-05, 2.616e-07, 4.436e-08, 1.596e-06, 1.15e-06, 1.738e-06, 9.358e-14, 9.358e-14,
+      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 3.68e-06, 8.584e-06, 9.358e-14, 3.857e-07,
+      9.358e-14, 9.358e-14, 7.945e-07, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   // achieved fraction of the streaming rate for the output writes (0: 1)
-  static const double kWr[AC_N_CFG] = {0};
+  static const double kWr[AC_N_CFG] = {
+      0.8769, 1, 1, 1, 0.8662, 1, 1, 1,
+      1, 1, 1, 1, 1, 1, 1, 1,
+      1, 0.1506, 0.1648, 0.4695, 1, 1, 0.7675, 0.7711,
+      0.4256, 0.6809, 0.5186, 0.7474, 0.2449, 0.3769, 1, 0.696,
+      0.2869, 0.5725, 0.5876, 0, 0.5354, 0.5246, 0.6132, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0};
   for (int i = 0; i < AC_N_CFG; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];

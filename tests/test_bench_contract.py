@@ -29,6 +29,8 @@ def test_traffic_summary_parses_when_source_matches(tmp_path, monkeypatch):
     got = bench.measured_traffic(kernel)
     assert got is not None and abs(got - want) <= 1e-6 * want
     assert bench.measured_traffic("k_not_a_kernel<1>") is None
+    assert bench.measured_traffic(kernel, int(cells[1])) == got
+    assert bench.measured_traffic(kernel, int(cells[1]) + 1) is None
 
 
 def test_traffic_summary_ignored_after_source_change(tmp_path, monkeypatch):
