@@ -12,7 +12,8 @@
  *     selects the tile and the optimisation modules (Table 2) among the legal
  *     candidates (Eq. 6);
  *   - the selected configuration is cached under a 64-bit key of the shape
- *     (Section 3.1, online phase), so a repeated shape dispatches in O(1).
+ *     (Section 3.2, online phase: the TilingKey lookup), so a repeated shape
+ *     dispatches in O(1).
  *
  * Conventions for every entry point:
  *   - All functions are extern "C", never throw, and report failure through
@@ -190,20 +191,48 @@ int32_t adaptcore_config_index(int32_t family, int32_t cfg);
  * when no device is present. */
 adaptcore_status adaptcore_init(void);
 
-/* Returns the cached plan for (M, N, K, dtype, layouts), planning it on the
- * first request (taxonomy, candidate enumeration, latency model, arg-min).
- * The same arguments always return the same pointer until
- * adaptcore_cache_clear(). M, N, K >= 0 and < 2^31. NULL on invalid or
- * unsupported arguments (see adaptcore_last_error). Host-only: no GPU work,
- * safe from many threads at once. */
+/* The problem statement of Section 5.1: given an input shape s = (M, N, K),
+ * choose the configuration x* = argmin over the legal candidates S(b(s)) of
+ * the modelled latency T(s; theta(s), x) (Eq. 6), where b(s) is the template
+ * the taxonomy of Section 4.2 assigns to s. Section 3.2 (online phase): the
+ * shape is packed into a 64-bit key and looked up in the plan cache; only a
+ * miss runs the offline steps (taxonomy, candidate enumeration, latency
+ * model of Eqs. 7-14, arg-min with ties to the smaller VariantKey).
+ *
+ * Returns the cached plan for (M, N, K, dtype, layouts): dtype one of
+ * adaptcore_dtype, layouts a set of AC_LAYOUT_* bits. The same arguments
+ * always return the same pointer until adaptcore_cache_clear(); the plan is
+ * owned by the library (never freed by the caller). M, N, K >= 0 and < 2^31.
+ * NULL on invalid or unsupported arguments (see adaptcore_last_error /
+ * adaptcore_last_status). Host-only: no GPU work beyond reading the
+ * device's kernel occupancies once; safe from many threads at once. While
+ * adaptcore_set_override holds a key on the calling thread, the call
+ * returns that configuration instead (adaptcore_plan_variant) and leaves
+ * the cache untouched. */
 const adaptcore_plan_t* adaptcore_plan(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts);
 
 /* Like adaptcore_plan, but with the configuration forced to `variant_key`
- * (one of the keys listed by adaptcore_candidates). For tests and the
- * exhaustive model-accuracy experiment. NULL if the key is not legal for the
- * shape. */
+ * (one of the keys listed by adaptcore_candidates): one point x of the
+ * candidate set S(b(s)) of Eq. 6 instead of the arg-min. For tests and the
+ * exhaustive model-accuracy experiment of Section 6.6. The plan is owned by
+ * the library (a map of its own, not the shape cache). NULL if the key is
+ * not legal for the shape (AC_ERR_INVALID_VALUE). */
 const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, int32_t dtype,
                                                uint32_t layouts, uint64_t variant_key);
+
+/* Forces the configuration of every later adaptcore_plan call made by the
+ * CALLING THREAD to `variant_key_or_0` (0 restores the model's choice): the
+ * override hook of the exhaustive search of Section 6.6, which times every
+ * legal configuration of a shape through the unchanged adaptcore_plan /
+ * adaptcore_matmul path. The setting is thread-local; other threads and the
+ * shape cache are not affected. With an override set, adaptcore_plan returns
+ * adaptcore_plan_variant(M, N, K, dtype, layouts, key), i.e. NULL with
+ * AC_ERR_INVALID_VALUE for shapes the key is not legal for (a key also
+ * fixes dtype and layouts). Always AC_OK. For tests and timing only. */
+adaptcore_status adaptcore_set_override(uint64_t variant_key_or_0);
+
+/* The calling thread's override key (0 = none). */
+uint64_t adaptcore_get_override(void);
 
 /* Largest leading dimension (exclusive, in elements) of A and B accepted by
  * adaptcore_matmul: the kernels address operand tiles with 32-bit byte
@@ -211,7 +240,11 @@ const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, 
 #define AC_MAX_LD (1LL << 23)
 
 /* Runs a plan: C = A * B, asynchronously on `stream` (a hipStream_t; NULL is
- * the null stream). Validates the leading dimensions against the plan's
+ * the null stream). This is the online execution of Section 3.2: the cached
+ * configuration's kernels are launched by its VariantKey (the registry of
+ * compiled templates, Section 4.2 and Table 2); every template computes the
+ * same mathematical product C[i][j] = sum_k A[i][k] * B[k][j] (Section 4.1),
+ * in fp32, with only the fp32 summation order differing between them. Validates the leading dimensions against the plan's
  * shape and layouts (row-major A: lda >= K, column-major A: lda >= M;
  * row-major B: ldb >= N, column-major B: ldb >= K; ldc >= N; all >= 1:
  * AC_ERR_INVALID_VALUE; a row-major lda or ldb >= AC_MAX_LD, or K or N of a
@@ -222,8 +255,14 @@ const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, 
  * Split-K plans and plans with a column-major operand use a workspace owned by the library for this (device,
  * stream); it is allocated on the stream's first use (outside any stream
  * capture: under capture a missing workspace gives AC_ERR_NOT_INITIALIZED)
- * and grows monotonically. Concurrent calls on ONE stream are ordered by the
- * stream; calls on different streams use different workspaces. */
+ * and grows monotonically: a larger buffer replaces it for later calls, and
+ * the replaced one is kept (never freed) until the process ends, so graphs
+ * captured earlier and calls already enqueued keep valid memory. Concurrent
+ * calls on ONE stream are ordered by the stream; calls on different streams
+ * use different workspaces. Errors: AC_ERR_OUT_OF_MEMORY (workspace),
+ * AC_ERR_LAUNCH (the runtime rejected a kernel), AC_ERR_NOT_INITIALIZED (no
+ * device, or a missing workspace under capture); nothing is launched then
+ * except kernels of the same call that were already enqueued. */
 adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
                                   int64_t ldb, void* C, int64_t ldc, void* stream);
 
@@ -354,10 +393,16 @@ adaptcore_status adaptcore_batched_addmm(const adaptcore_plan_t* plan, const voi
                                          int64_t stride_c, float alpha, float beta, const float* bias, void* stream);
 
 /* Allocates (if needed) the workspace of `stream` for plans needing up to
- * `bytes`, so that later calls, also under capture, do not allocate. */
+ * `bytes`, so that later calls, also under capture, do not allocate. A
+ * workspace that grows keeps its previous buffer alive (see
+ * adaptcore_matmul). */
 adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes);
 
-/* Fills *out with the description of a plan. */
+/* Fills *out with the description of a plan: the template of the taxonomy
+ * (Section 4.2), the selected configuration x* (Eq. 6) as its VariantKey,
+ * the tiling (m1, n1, k1) and task counts P_m, P_n, P_k of Table 1, the
+ * launch grid, the latency the model of Eqs. 7-14 predicts and the workspace
+ * size. AC_ERR_INVALID_VALUE for a null argument. */
 adaptcore_status adaptcore_plan_info(const adaptcore_plan_t* plan, adaptcore_plan_desc_t* out);
 
 /* Writes the kernels one call of the plan launches, in launch order, as
@@ -372,7 +417,9 @@ adaptcore_status adaptcore_plan_kernels(const adaptcore_plan_t* plan, char* buf,
 int64_t adaptcore_candidates(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts,
                              adaptcore_candidate_t* out, int64_t cap);
 
-/* Planner profile. set() drops every cached plan (they depend on it). */
+/* Planner profile. set() drops every cached plan (they depend on it) by
+ * calling adaptcore_cache_clear: plans returned earlier become invalid, so
+ * call it only when no other thread uses the library. */
 adaptcore_status adaptcore_get_hw(adaptcore_hw_t* out);
 adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw);
 

@@ -132,6 +132,10 @@ def lib():
         L.adaptcore_plan.restype = p
         L.adaptcore_plan_variant.argtypes = [i64, i64, i64, i32, u32, u64]
         L.adaptcore_plan_variant.restype = p
+        L.adaptcore_set_override.argtypes = [u64]
+        L.adaptcore_set_override.restype = i32
+        L.adaptcore_get_override.argtypes = []
+        L.adaptcore_get_override.restype = u64
         L.adaptcore_matmul.argtypes = [p, p, i64, p, i64, p, i64, p]
         L.adaptcore_matmul.restype = i32
         L.adaptcore_addmm.argtypes = [p, p, i64, p, i64, p, i64, ctypes.c_float, ctypes.c_float, p, p]
@@ -220,6 +224,15 @@ def adaptcore_plan_variant(M, N, K, dtype, layouts, variant_key):
     if not h:
         raise AdaptCoreError(adaptcore_last_status(), last_error())
     return h
+
+
+def adaptcore_set_override(variant_key_or_0):
+    """Force the configuration of this thread's later adaptcore_plan calls (0 = none)."""
+    return _check(lib().adaptcore_set_override(variant_key_or_0))
+
+
+def adaptcore_get_override():
+    return lib().adaptcore_get_override()
 
 
 def adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream=0):

@@ -1,6 +1,6 @@
 """Build libadaptcore.so (gfx950) in-tree with hipcc.
 
-    python -m paper_2608_10803_amd.build [--if-stale]
+    python -m paper_2608_10803_amd.build [--if-stale] [--incremental]
 
 Every source is compiled to an object under _build/ (in parallel) and linked
 into paper_2608_10803_amd/libadaptcore.so. Device code is compiled with
@@ -44,6 +44,17 @@ def stale():
     return any(os.path.getmtime(f) > t for f in _inputs())
 
 
+def _obj_stale(unit):
+    src, name, _ = unit
+    obj = os.path.join(BUILD, name)
+    if not os.path.exists(obj):
+        return True
+    t = os.path.getmtime(obj)
+    deps = [os.path.join(CSRC, src)] + [os.path.join(CSRC, h) for h in HEADERS]
+    deps.append(os.path.join(ROOT, "include", "adaptcore.h"))
+    return any(os.path.getmtime(f) > t for f in deps)
+
+
 def _compile(unit):
     src, name, extra = unit
     obj = os.path.join(BUILD, name)
@@ -56,15 +67,17 @@ def _compile(unit):
     return obj, err
 
 
-def build(verbose=False):
+def build(verbose=False, incremental=False):
+    """Compiles every unit (incremental=True: only units whose object is older
+    than its source or a header) and links the library."""
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(len(UNITS)) as ex:
-        results = list(ex.map(_compile, UNITS))
-    objs = []
-    for obj, err in results:
-        objs.append(obj)
+    todo = [u for u in UNITS if not incremental or _obj_stale(u)]
+    with cf.ThreadPoolExecutor(max(1, len(todo))) as ex:
+        results = list(ex.map(_compile, todo))
+    for _, err in results:
         if verbose and err.strip():
             print(err, file=sys.stderr)
+    objs = [os.path.join(BUILD, name) for _, name, _ in UNITS]
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -78,4 +91,4 @@ if __name__ == "__main__":
     if "--if-stale" in sys.argv and not stale():
         print(LIB, "(up to date)")
     else:
-        print(build(verbose=True))
+        print(build(verbose=True, incremental="--incremental" in sys.argv))

@@ -1,5 +1,5 @@
-// C ABI: validation, the plan cache (O(1) online dispatch, Section 3.1),
-// per-stream workspaces and the launch.
+// C ABI: validation, the plan cache (O(1) online dispatch of the online
+// phase, Section 3.2), per-stream workspaces and the launch.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -25,6 +25,11 @@ namespace {
 
 thread_local std::string t_err;
 thread_local adaptcore_status t_status = AC_OK;
+// adaptcore_set_override: VariantKey forced on this thread's adaptcore_plan
+// calls (0 = none).
+thread_local uint64_t t_override = 0;
+
+void init_for_planning();
 
 adaptcore_status fail(adaptcore_status st, const std::string& msg) {
   t_err = msg;
@@ -169,6 +174,7 @@ inline const adaptcore_plan_s* lookup(int64_t M, int64_t N, int64_t K, int32_t d
       return p;
     }
   }
+  init_for_planning();
   std::lock_guard<std::mutex> lk(g_mu);
   if (exact) {
     if (adaptcore_plan_s* p = table_find(g_tab.load(std::memory_order_acquire), key + 1)) {
@@ -201,6 +207,7 @@ struct Workspace {
 };
 std::mutex g_ws_mu;
 std::map<std::pair<int, void*>, Workspace> g_ws;
+std::vector<char*> g_ws_retired;  // replaced workspaces, kept until the process ends
 std::once_flag g_init_once;
 adaptcore_status g_init_status = AC_ERR_NOT_INITIALIZED;
 std::string g_init_msg;
@@ -238,6 +245,12 @@ adaptcore_status ensure_init() {
   return AC_OK;
 }
 
+// Every planning path runs this first (outside g_mu), so a plan is priced
+// with the occupancies the device reports for the compiled kernels whatever
+// the order of the caller's first calls; host API queries only, no launch.
+// Without a device the planner keeps its table of workgroups per CU.
+void init_for_planning() { std::call_once(g_init_once, [] { g_init_status = do_init(); }); }
+
 // Workspace of (current device, stream) with at least `need` bytes; allocates
 // outside stream capture only. Partials are fully rewritten by every call that
 // uses them, so a workspace needs no initialisation.
@@ -255,14 +268,13 @@ adaptcore_status get_workspace(hipStream_t stream, int64_t need, Workspace* out)
     return fail(AC_ERR_NOT_INITIALIZED,
                 "split-K workspace missing for this stream under capture: call adaptcore_reserve_workspace first");
   const int64_t grow = std::max<int64_t>(std::max<int64_t>(need, 1 << 20), w.bytes + w.bytes / 2);
-  if (w.ptr) {
-    (void)hipStreamSynchronize(stream);  // kernels in flight may still use the old buffer
-    (void)hipFree(w.ptr);
-    w.ptr = nullptr;
-    w.bytes = 0;
-  }
   void* p = nullptr;
   if (hipMalloc(&p, (size_t)grow) != hipSuccess) return fail(AC_ERR_OUT_OF_MEMORY, "workspace allocation failed");
+  // The replaced buffer is never freed: a graph captured earlier on this
+  // stream, or another thread that took the pointer and has not launched
+  // yet, may still use it. With growth by at least 1.5x the retired buffers
+  // of a stream add up to at most twice its current workspace.
+  if (w.ptr) g_ws_retired.push_back(w.ptr);
   w.ptr = static_cast<char*>(p);
   w.bytes = grow;
   *out = w;
@@ -278,14 +290,23 @@ adaptcore_status adaptcore_init(void) { return ensure_init(); }
 const adaptcore_plan_t* adaptcore_plan(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts) {
   adaptcore_status st;
   if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
+  if (t_override != 0) return adaptcore_plan_variant(M, N, K, dtype, layouts, t_override);
   return lookup(M, N, K, dtype, layouts);
 }
+
+adaptcore_status adaptcore_set_override(uint64_t variant_key_or_0) {
+  t_override = variant_key_or_0;
+  return AC_OK;
+}
+
+uint64_t adaptcore_get_override(void) { return t_override; }
 
 const adaptcore_plan_t* adaptcore_plan_variant(int64_t M, int64_t N, int64_t K, int32_t dtype, uint32_t layouts,
                                                uint64_t variant_key) {
   adaptcore_status st;
   if (!valid_args(M, N, K, dtype, layouts, &st)) return nullptr;
   const auto tk = std::make_tuple(M, N, K, (int)dtype, layouts);
+  init_for_planning();
   std::lock_guard<std::mutex> lk(g_mu);
   auto it = g_forced.find(std::make_pair(tk, variant_key));
   if (it != g_forced.end()) return it->second;
@@ -423,6 +444,7 @@ const adaptcore_plan_t* adaptcore_grouped_plan(int64_t rows, int64_t groups, int
   }
   st_lookups.fetch_add(1, std::memory_order_relaxed);
   const GroupKey k = std::make_tuple(rows, groups, N, K, (int)dtype, layouts);
+  init_for_planning();
   std::lock_guard<std::mutex> lk(g_mu);
   auto it = g_grouped.find(k);
   if (it != g_grouped.end()) {
@@ -457,6 +479,7 @@ const adaptcore_plan_t* adaptcore_grouped_plan_variant(int64_t rows, int64_t gro
     return nullptr;
   }
   const GroupKey k = std::make_tuple(rows, groups, N, K, (int)dtype, layouts);
+  init_for_planning();
   std::lock_guard<std::mutex> lk(g_mu);
   auto it = g_grouped_forced.find(std::make_pair(k, variant_key));
   if (it != g_grouped_forced.end()) return it->second;
@@ -566,6 +589,7 @@ const adaptcore_plan_t* adaptcore_batched_plan(int64_t batch, int64_t M, int64_t
   }
   st_lookups.fetch_add(1, std::memory_order_relaxed);
   const GroupKey k = std::make_tuple(M, batch, N, K, (int)dtype, layouts);
+  init_for_planning();
   std::lock_guard<std::mutex> lk(g_mu);
   auto it = g_batched.find(k);
   if (it != g_batched.end()) {
@@ -600,6 +624,7 @@ const adaptcore_plan_t* adaptcore_batched_plan_variant(int64_t batch, int64_t M,
     return nullptr;
   }
   const GroupKey k = std::make_tuple(M, batch, N, K, (int)dtype, layouts);
+  init_for_planning();
   std::lock_guard<std::mutex> lk(g_mu);
   auto it = g_batched_forced.find(std::make_pair(k, variant_key));
   if (it != g_batched_forced.end()) return it->second;
@@ -742,6 +767,7 @@ int64_t adaptcore_candidates(int64_t M, int64_t N, int64_t K, int32_t dtype, uin
   adaptcore_status st;
   if (!valid_args(M, N, K, dtype, layouts, &st)) return st;
   adaptcore_hw_t hw;
+  init_for_planning();
   {
     std::lock_guard<std::mutex> lk(g_mu);
     hw = g_hw;
@@ -783,6 +809,7 @@ adaptcore_status adaptcore_set_hw(const adaptcore_hw_t* hw) {
     if (!(hw->cfg_iter[i] >= 0 && hw->cfg_iter[i] < 1) || !(hw->cfg_wg[i] >= 0 && hw->cfg_wg[i] < 1) ||
         !(hw->cfg_wr[i] >= 0 && hw->cfg_wr[i] <= 1))
       return fail(AC_ERR_INVALID_VALUE, "calibrated configuration cost out of range");
+  init_for_planning();  // the device's CU count must not replace the caller's profile later
   adaptcore_cache_clear();
   std::lock_guard<std::mutex> lk(g_mu);
   g_hw = *hw;

@@ -312,3 +312,41 @@ def test_fp16_plans():
     with pytest.raises(ac.AdaptCoreError) as e:
         ac.adaptcore_plan(4, 4, 4, 4)
     assert e.value.status == ac.AC_ERR_UNSUPPORTED
+
+
+def test_set_override_is_thread_local_and_leaves_the_cache():
+    """adaptcore_set_override forces the configuration of the calling
+    thread's adaptcore_plan calls (the exhaustive-search hook, Section 6.6):
+    each legal key of a shape comes back through adaptcore_plan, other
+    threads still get the model's choice, the shape cache gains no entry and
+    its plan is unchanged, an illegal key gives NULL, and 0 restores."""
+    s = (700, 900, 3000)
+    chosen = ac.adaptcore_plan(*s)
+    chosen_key = ac.adaptcore_plan_info(chosen)["variant_key"]
+    cands = ac.adaptcore_candidates(*s)
+    others = [c["variant_key"] for c in cands if c["variant_key"] != chosen_key][:6]
+    assert others
+    entries = ac.adaptcore_stats()["entries"]
+    seen_other_thread = []
+    try:
+        for k in others:
+            ac.adaptcore_set_override(k)
+            assert ac.adaptcore_get_override() == k
+            h = ac.adaptcore_plan(*s)
+            assert ac.adaptcore_plan_info(h)["variant_key"] == k
+            assert h == ac.adaptcore_plan_variant(*s, ac.AC_BF16_BF16OUT, 0, k)
+            t = threading.Thread(target=lambda: seen_other_thread.append(
+                (ac.adaptcore_get_override(), ac.adaptcore_plan(*s))))
+            t.start()
+            t.join()
+        # a key of another dtype is not legal for a bf16-output shape
+        ac.adaptcore_set_override(others[0] & ~(0xF << 48) | (ac.AC_BF16_F32OUT << 48))
+        with pytest.raises(ac.AdaptCoreError) as e:
+            ac.adaptcore_plan(*s)
+        assert e.value.status == ac.AC_ERR_INVALID_VALUE
+    finally:
+        ac.adaptcore_set_override(0)
+    assert ac.adaptcore_get_override() == 0
+    assert all(o == 0 and h == chosen for o, h in seen_other_thread)
+    assert ac.adaptcore_plan(*s) == chosen
+    assert ac.adaptcore_stats()["entries"] == entries
