@@ -62,13 +62,37 @@ class Arena:
         self.B[:K * N].normal_(0.0, s, generator=self.g)
 
 
-def sample_entries(M, N, seed, tile=256):
+def _tile_edges(L, tile, rng, most=12):
+    """First and last index of up to `most` tiles of size `tile` along a
+    dimension of L (always the last, possibly ragged, tile), in random order."""
+    nt = (L + tile - 1) // tile
+    ts = sorted(set(np.linspace(0, nt - 1, min(nt, most)).astype(np.int64).tolist()) | {nt - 1})
+    idx = []
+    for t in ts:
+        idx += [t * tile, min((t + 1) * tile, L) - 1]
+    return list(rng.permutation(np.array(idx, np.int64)))
+
+
+def sample_entries(M, N, seed, tile_m=256, tile_n=256):
+    """The four corners, the first and last row / column of tiles of the
+    plan's own tiling (the last, ragged tile always) paired with random
+    columns / rows, and N_RANDOM random entries."""
     rng = np.random.default_rng(seed)
-    I = [0, M - 1, 0, M - 1, (M - 1) // tile * tile, M - 1, max(M - 1 - tile // 2, 0)]
-    J = [0, N - 1, N - 1, 0, N - 1, (N - 1) // tile * tile, max(N - 1 - tile // 2, 0)]
+    I = [0, M - 1, 0, M - 1]
+    J = [0, N - 1, N - 1, 0]
+    ei = _tile_edges(M, max(tile_m, 1), rng)
+    ej = _tile_edges(N, max(tile_n, 1), rng)
+    I += ei + list(rng.integers(0, M, len(ej)))
+    J += list(rng.integers(0, N, len(ei))) + ej
     I += list(rng.integers(0, M, N_RANDOM))
     J += list(rng.integers(0, N, N_RANDOM))
     return np.array(I, np.int64), np.array(J, np.int64)
+
+
+def assert_covered(t, C, label):
+    """C was filled with NaN before the call and the inputs are finite: every
+    entry must have been written."""
+    assert not bool(t.isnan(C).any()), "%s: entries of C left unwritten" % (label,)
 
 
 def check_shape(arena, M, N, K, dtype, seed, label):
@@ -81,7 +105,9 @@ def check_shape(arena, M, N, K, dtype, seed, label):
     ac.adaptcore_matmul(plan, arena.A.data_ptr(), max(K, 1), arena.B.data_ptr(), max(N, 1),
                         arena.C.data_ptr(), max(N, 1), 0)
     t.cuda.synchronize()
-    I, J = sample_entries(M, N, seed)
+    d = ac.adaptcore_plan_info(plan)
+    assert_covered(t, C, "%s %s" % (label, (M, N, K)))
+    I, J = sample_entries(M, N, seed, d["tile_m"], d["tile_n"])
     got = C[t.from_numpy(I).cuda(), t.from_numpy(J).cuda()]
     if dtype == F32:
         vals = got.cpu().numpy().astype(np.float64)
@@ -94,7 +120,6 @@ def check_shape(arena, M, N, K, dtype, seed, label):
     Bc = B[:, t.from_numpy(uj).cuda()].contiguous().view(t.int16).cpu().numpy().view(np.uint16)
     C_ref, D = gemm_ref.gemm_entries(Ar, Bc, inv_i, inv_j, M=len(ui), N=len(uj), K=K)
     err = gemm_ref.err_metric(vals, C_ref, D)
-    d = ac.adaptcore_plan_info(plan)
     assert err <= tol(dtype), "%s %s err %.3g (%s %dx%d pk %d)" % (
         label, (M, N, K), err, d["family_name"], d["tile_m"], d["tile_n"], d["pk"])
     return err, d["family_name"]
@@ -171,10 +196,11 @@ def test_moe_stream_full_size():
 LAYOUT_SHAPES = [(4096, 4096, 4096), (2048, 14336, 4096), (8192, 8192, 1024), (16, 4096, 14336), (512, 512, 512)]
 
 
-def _sampled(t, Alog, Blog, M, N, K, seed):
+def _sampled(t, Alog, Blog, M, N, K, seed, plan=None):
     """Sampled entries and the raw bf16 A rows and B columns they need,
     read through the logical (possibly transposed) views."""
-    I, J = sample_entries(M, N, seed)
+    d = ac.adaptcore_plan_info(plan) if plan is not None else {"tile_m": 256, "tile_n": 256}
+    I, J = sample_entries(M, N, seed, d["tile_m"], d["tile_n"])
     ui, inv_i = np.unique(I, return_inverse=True)
     uj, inv_j = np.unique(J, return_inverse=True)
     Ar = Alog[t.from_numpy(ui).cuda()].contiguous().view(t.int16).cpu().numpy().view(np.uint16)
@@ -202,7 +228,8 @@ def test_layouts_full_size():
             ac.adaptcore_matmul(plan, A.data_ptr(), M if a_col else K, B.data_ptr(), K if b_col else N,
                                 C.data_ptr(), N, 0)
             t.cuda.synchronize()
-            I, J, Ar, Bc, ii, jj, nu, nv = _sampled(t, Alog, Blog, M, N, K, 7000 + 10 * si + lay)
+            assert_covered(t, C, "layouts %d %s" % (lay, (M, N, K)))
+            I, J, Ar, Bc, ii, jj, nu, nv = _sampled(t, Alog, Blog, M, N, K, 7000 + 10 * si + lay, plan)
             got = C[t.from_numpy(I).cuda(), t.from_numpy(J).cuda()]
             vals = gemm_ref.decode(got.view(t.int16).cpu().numpy().view(np.uint16))
             C_ref, D = gemm_ref.gemm_entries(Ar, Bc, ii, jj, M=nu, N=nv, K=K)
@@ -225,11 +252,12 @@ def test_addmm_full_size():
                 _progress("addmm %s dtype %d layouts %d" % ((M, N, K), dtype, lay))
                 C = t.empty(M, N, dtype=t.float32 if dtype == F32 else t.bfloat16, device="cuda")
                 C.uniform_(-2, 2, generator=g)
-                I, J = sample_entries(M, N, 8000 + si)
+                plan = ac.adaptcore_plan(M, N, K, dtype, lay)
+                d = ac.adaptcore_plan_info(plan)
+                I, J = sample_entries(M, N, 8000 + si, d["tile_m"], d["tile_n"])
                 Ii, Jj = t.from_numpy(I).cuda(), t.from_numpy(J).cuda()
                 old = C[Ii, Jj].float().cpu().numpy().astype(np.float64)
                 Blog = B.view(N, K).t() if lay else B.view(K, N)
-                plan = ac.adaptcore_plan(M, N, K, dtype, lay)
                 ac.adaptcore_addmm(plan, A.data_ptr(), K, B.data_ptr(), K if lay else N, C.data_ptr(), N,
                                    0.75, -1.25, bias.data_ptr(), 0)
                 t.cuda.synchronize()
@@ -238,7 +266,7 @@ def test_addmm_full_size():
                     vals = got.cpu().numpy().astype(np.float64)
                 else:
                     vals = gemm_ref.decode(got.view(t.int16).cpu().numpy().view(np.uint16))
-                _, _, Ar, Bc, ii, jj, nu, nv = _sampled(t, A.view(M, K), Blog, M, N, K, 8000 + si)
+                _, _, Ar, Bc, ii, jj, nu, nv = _sampled(t, A.view(M, K), Blog, M, N, K, 8000 + si, plan)
                 b = bias[Jj].cpu().numpy().astype(np.float64)
                 C_ref, D = addmm_ref.addmm_entries(Ar, Bc, ii, jj, old, 0.75, -1.25, b, M=nu, N=nv, K=K)
                 err = gemm_ref.err_metric(vals, C_ref, D)

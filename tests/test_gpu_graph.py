@@ -150,3 +150,54 @@ def test_capture_without_workspace_is_an_error():
             status = e.status
         C.fill_(0.0)  # something to capture
     assert status == ac.AC_ERR_NOT_INITIALIZED
+
+
+def test_workspace_growth_after_capture_keeps_the_captured_buffer():
+    """A split-K call captured on a stream with a small reserved workspace,
+    then an eager call on the same stream whose plan needs a larger one (the
+    workspace grows), then new device allocations filled with a pattern, then
+    replays of the graph: the captured call keeps using its buffer, which the
+    growth retired but did not free. Every replay matches the oracle, and
+    the buffers allocated after the growth keep their pattern."""
+    t = torch()
+    ac.adaptcore_init()
+    s = t.cuda.Stream()
+    M, N, K = 64, 64, 20000
+    small = ac.adaptcore_plan(M, N, K, F32)
+    ws_small = ac.adaptcore_plan_info(small)["workspace_bytes"]
+    assert ac.adaptcore_plan_info(small)["pk"] > 1 and ws_small > 0
+    ac.adaptcore_reserve_workspace(s.cuda_stream, ws_small)
+    A, B = gen.operands(M, N, K, seed=21)
+    Ad, Bd = _dev(A), _dev(B)
+    C = t.empty(M, N, dtype=t.float32, device="cuda")
+    g = t.cuda.CUDAGraph()
+    with t.cuda.graph(g, stream=s):
+        ac.adaptcore_matmul(small, Ad.data_ptr(), K, Bd.data_ptr(), N, C.data_ptr(), N, s.cuda_stream)
+    # an eager split-K call that needs a workspace larger than the reserved one
+    M2, N2, K2 = 512, 512, 65536
+    keys = [c["variant_key"] for c in all_candidates(M2, N2, K2, F32)
+            if c["family_name"] == "tile" and c["pk"] >= 16]
+    assert keys
+    big = forced_plan(M2, N2, K2, F32, keys[0])
+    assert ac.adaptcore_plan_info(big)["workspace_bytes"] > 4 * max(ws_small, 1 << 20)
+    A2, B2 = gen.operands(M2, N2, 512, seed=22)  # K2 rows built from a tiled 512-deep slice
+    A2 = np.tile(A2, (1, K2 // 512))
+    B2 = np.tile(B2, (K2 // 512, 1))
+    A2d, B2d = _dev(A2), _dev(B2)
+    C2 = t.empty(M2, N2, dtype=t.float32, device="cuda")
+    with t.cuda.stream(s):
+        ac.adaptcore_matmul(big, A2d.data_ptr(), K2, B2d.data_ptr(), N2, C2.data_ptr(), N2, s.cuda_stream)
+    s.synchronize()
+    rows = np.arange(0, M2, 37)
+    R2, D2 = gemm_ref.gemm(A2[rows], B2)
+    assert gemm_ref.err_metric(C2.cpu().numpy().astype(np.float64)[rows], R2, D2) <= tol(F32)
+    # allocations made after the growth: a freed buffer would be handed out here
+    fillers = [t.full((max(ws_small, 1 << 20) // 4 + 64,), 7.0, device="cuda") for _ in range(4)]
+    ref = gemm_ref.gemm(A, B)
+    for replay in range(3):
+        C.fill_(float("nan"))
+        t.cuda.synchronize()
+        g.replay()
+        t.cuda.synchronize()
+        assert gemm_ref.err_metric(C.cpu().numpy().astype(np.float64), *ref) <= tol(F32), replay
+        assert all(bool((f == 7.0).all()) for f in fillers), replay

@@ -257,3 +257,26 @@ def test_fp16_default_plans_and_persistent(dtype):
             note("fp16", (M, N, K), ac.adaptcore_plan_kernels(plan))
             vals, ok = run(plan, A, B, M, N, K, dtype)
             check(vals, ok, A, B, dtype, ref=ref, label="%s %s" % ((M, N, K), hex(k)))
+
+
+def test_plan_before_init_equals_plan_after_init():
+    """The planner prices candidates with the occupancies the device reports
+    whatever the order of the first calls: in a fresh process, plans made
+    before adaptcore_init equal those made after it (cache cleared)."""
+    import json
+    import subprocess
+    import sys
+    code = r'''
+import json, paper_2608_10803_amd as ac
+shapes = [(64, 64, 20000), (3000, 5, 700), (33, 4096, 4096), (700, 900, 3000), (16, 16, 16), (2048, 2048, 2048)]
+first = [ac.adaptcore_plan_info(ac.adaptcore_plan(*s, 0))["variant_key"] for s in shapes]
+ac.adaptcore_init()
+ac.adaptcore_cache_clear()
+second = [ac.adaptcore_plan_info(ac.adaptcore_plan(*s, 0))["variant_key"] for s in shapes]
+print(json.dumps([first, second]))
+'''
+    root = __import__("os").path.dirname(__import__("os").path.dirname(__import__("os").path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr[-2000:]
+    first, second = json.loads(out.stdout.strip().splitlines()[-1])
+    assert first == second
