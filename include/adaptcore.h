@@ -266,6 +266,28 @@ uint64_t adaptcore_get_override(void);
 adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
                                   int64_t ldb, void* C, int64_t ldc, void* stream);
 
+/* ---- No-allocation variant ---------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc. It runs a
+ * plain plan exactly as adaptcore_matmul does (same kernels, same results
+ * bit for bit), but the workspace (split-K partials, stream-K pieces,
+ * row-major copies of column-major operands) is a fixed array of device
+ * memory compiled into the library, adaptcore_noalloc_scratch_bytes() bytes
+ * (64 MiB) on every GPU the library runs on, held until the process ends.
+ * No call of this entry point allocates or frees device memory. The
+ * caller still passes A, B and C; arguments and checks are those of
+ * adaptcore_matmul, and a plan whose workspace_bytes exceed the array gives
+ * AC_ERR_UNSUPPORTED (nothing launched). Every call on one GPU shares that
+ * GPU's array, and the array keeps the last call's contents: no part of it
+ * needs clearing (every byte a call reads was written earlier in the same
+ * call), but calls that overlap in time on one GPU (different streams, or
+ * the same graph replayed concurrently) race on it -- order them. */
+adaptcore_status adaptcore_matmul_noalloc(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
+                                          int64_t ldb, void* C, int64_t ldc, void* stream);
+
+/* Size in bytes of the per-GPU array used by adaptcore_matmul_noalloc. */
+int64_t adaptcore_noalloc_scratch_bytes(void);
+
 /* ---- AddMM ------------------------------------------------------------------
  * AddMM is one of the dense operators the paper replaces in its end-to-end
  * models beside MatMul (Section 6.5; operator scope, Section 7). It runs a

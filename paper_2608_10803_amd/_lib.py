@@ -138,6 +138,10 @@ def lib():
         L.adaptcore_get_override.restype = u64
         L.adaptcore_matmul.argtypes = [p, p, i64, p, i64, p, i64, p]
         L.adaptcore_matmul.restype = i32
+        L.adaptcore_matmul_noalloc.argtypes = [p, p, i64, p, i64, p, i64, p]
+        L.adaptcore_matmul_noalloc.restype = i32
+        L.adaptcore_noalloc_scratch_bytes.argtypes = []
+        L.adaptcore_noalloc_scratch_bytes.restype = i64
         L.adaptcore_addmm.argtypes = [p, p, i64, p, i64, p, i64, ctypes.c_float, ctypes.c_float, p, p]
         L.adaptcore_addmm.restype = i32
         L.adaptcore_grouped_plan.argtypes = [i64, i64, i64, i64, i32, u32]
@@ -238,6 +242,16 @@ def adaptcore_get_override():
 def adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream=0):
     """C = A * B on `stream`; A, B, C are device addresses (ints)."""
     return _check(lib().adaptcore_matmul(plan, A, lda, B, ldb, C, ldc, stream))
+
+
+def adaptcore_matmul_noalloc(plan, A, lda, B, ldb, C, ldc, stream=0):
+    """adaptcore_matmul with the library's fixed device scratch as workspace
+    (allocates nothing)."""
+    return _check(lib().adaptcore_matmul_noalloc(plan, A, lda, B, ldb, C, ldc, stream))
+
+
+def adaptcore_noalloc_scratch_bytes():
+    return lib().adaptcore_noalloc_scratch_bytes()
 
 
 def adaptcore_addmm(plan, A, lda, B, ldb, C, ldc, alpha=1.0, beta=0.0, bias=0, stream=0):

@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "adaptcore.h"
+#include "noalloc.h"
 #include "planner.h"
 #include "registry.h"
 
@@ -232,6 +233,11 @@ adaptcore_status do_init() {
     return AC_ERR_UNSUPPORTED;
   }
   ac::query_occupancy();
+  // Resolve the no-allocation entry point's scratch array on this device
+  // now; a failure is reported by that entry point (it tries again), the
+  // rest of the library does not depend on it.
+  void* scratch = nullptr;
+  (void)ac::noalloc_scratch(dev, &scratch);
   std::lock_guard<std::mutex> lk(g_mu);
   if (g_hw.n_cu != prop.multiProcessorCount) {
     g_hw.n_cu = prop.multiProcessorCount;
@@ -336,9 +342,12 @@ adaptcore_status adaptcore_reserve_workspace(void* stream, int64_t bytes) {
 
 namespace {
 
-// One call of a plain plan; epi != 0 selects the AddMM epilogue.
+// One call of a plain plan; epi != 0 selects the AddMM epilogue. With
+// `fixed` the workspace is the device scratch array of
+// adaptcore_matmul_noalloc (nothing is allocated).
 adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
-                            void* C, int64_t ldc, void* stream, int epi, float alpha, float beta, const float* bias) {
+                            void* C, int64_t ldc, void* stream, int epi, float alpha, float beta, const float* bias,
+                            bool fixed = false) {
   if (!plan) return fail(AC_ERR_INVALID_VALUE, "null plan");
   const ac::Plan& p = plan->p;
   if (p.family == ac::FAM_GROUPED)
@@ -391,8 +400,21 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   g.grid = p.grid_x;
   if (p.ws_bytes > 0) {
     Workspace w;
-    st = get_workspace(s, p.ws_bytes, &w);
-    if (st != AC_OK) return st;
+    if (fixed) {
+      if (p.ws_bytes > ac::NOALLOC_SCRATCH_BYTES)
+        return fail(AC_ERR_UNSUPPORTED, "the plan's workspace (" + std::to_string(p.ws_bytes) +
+                                            " bytes) exceeds the no-allocation scratch of " +
+                                            std::to_string(ac::NOALLOC_SCRATCH_BYTES) + " bytes");
+      int dev = 0;
+      void* ptr = nullptr;
+      if (hipGetDevice(&dev) != hipSuccess || ac::noalloc_scratch(dev, &ptr) != hipSuccess)
+        return fail(AC_ERR_NOT_INITIALIZED, "the device scratch array is not addressable on this device");
+      w.ptr = static_cast<char*>(ptr);
+      w.bytes = ac::NOALLOC_SCRATCH_BYTES;
+    } else {
+      st = get_workspace(s, p.ws_bytes, &w);
+      if (st != AC_OK) return st;
+    }
     g.ws = reinterpret_cast<float*>(w.ptr);
     // prologue: row-major copies of column-major operands (A: M x K, B: K x N)
     char* base = static_cast<char*>(w.ptr);
@@ -425,6 +447,13 @@ adaptcore_status adaptcore_matmul(const adaptcore_plan_t* plan, const void* A, i
                                   void* C, int64_t ldc, void* stream) {
   return run_matmul(plan, A, lda, B, ldb, C, ldc, stream, 0, 1.0f, 0.0f, nullptr);
 }
+
+adaptcore_status adaptcore_matmul_noalloc(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B,
+                                          int64_t ldb, void* C, int64_t ldc, void* stream) {
+  return run_matmul(plan, A, lda, B, ldb, C, ldc, stream, 0, 1.0f, 0.0f, nullptr, true);
+}
+
+int64_t adaptcore_noalloc_scratch_bytes(void) { return ac::NOALLOC_SCRATCH_BYTES; }
 
 adaptcore_status adaptcore_addmm(const adaptcore_plan_t* plan, const void* A, int64_t lda, const void* B, int64_t ldb,
                                  void* C, int64_t ldc, float alpha, float beta, const float* bias, void* stream) {
