@@ -93,7 +93,11 @@ typedef enum {
   AC_FAMILY_GROUPED = 6,  /* the tile kernel over the groups of a grouped product */
   AC_FAMILY_PERSIST = 7,  /* persistent tile kernel: the next tile's first k-block is fetched
                              before the current tile's epilogue (K >= 8, N >= 8) */
-  AC_FAMILY_BATCHED = 8   /* the grouped kernel over a strided batch of equal shapes */
+  AC_FAMILY_BATCHED = 8,  /* the grouped kernel over a strided batch of equal shapes */
+  AC_FAMILY_DL = 9        /* tile kernel with operand tiles loaded straight into LDS through 2-3
+                             stages (Multi-Buffer); needs K, N multiples of 8 and, at run time,
+                             16-byte aligned rows of A and B (else the same tiling runs on
+                             AC_FAMILY_TILE) */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */

@@ -22,7 +22,8 @@ enum Family : int {
   FAM_GROUPED = 6,   // the tile kernel over the groups of a grouped product
   FAM_PERSIST = 7,   // persistent tile kernel, next tile's first block fetched before the epilogue
   FAM_BATCHED = 8,   // the grouped kernel over a strided batch (every group the same shape)
-  FAM_COUNT = 9
+  FAM_DL = 9,        // tile kernel with operand tiles loaded straight into LDS (multi-stage)
+  FAM_COUNT = 10
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N

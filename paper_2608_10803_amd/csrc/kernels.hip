@@ -41,14 +41,7 @@ namespace ac {
 namespace f16 {
 #endif
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-#if AC_INPUT_F16
-typedef _Float16 in16x8 __attribute__((ext_vector_type(8)));
-#else
-typedef __bf16 in16x8 __attribute__((ext_vector_type(8)));
-#endif
+#include "device_common.h"
 
 // ---------------------------------------------------------------- helpers
 
@@ -114,64 +107,6 @@ __device__ __forceinline__ void transpose8x8(const u32x4 (&r)[8], u32x4 (&c)[8])
   }
 }
 
-#if AC_INPUT_F16
-__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
-                                                0, 0);
-}
-__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
-                                                0, 0);
-}
-// fp32 -> the 16-bit output format, round to nearest even; NaN stays NaN
-__device__ __forceinline__ uint16_t to16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
-// the value of a 16-bit input element (low 16 bits of h)
-__device__ __forceinline__ float from16(uint32_t h) { return (float)__builtin_bit_cast(_Float16, (uint16_t)h); }
-#else
-__device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
-                                                 0, 0);
-}
-__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(in16x8, a), __builtin_bit_cast(in16x8, b), c, 0,
-                                                 0, 0);
-}
-__device__ __forceinline__ uint16_t to16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
-__device__ __forceinline__ float from16(uint32_t h) { return __uint_as_float(h << 16); }
-#endif
-
-template <bool OBF>
-__device__ __forceinline__ void store_c(void* C, int64_t idx, float v) {
-  if constexpr (OBF)
-    static_cast<uint16_t*>(C)[idx] = to16(v);
-  else
-    static_cast<float*>(C)[idx] = v;
-}
-
-// ---- AddMM epilogue on outputs of one row (uniform test of g.epi; C_old is
-// read only where an output exists and beta != 0)
-template <bool OBF>
-__device__ __forceinline__ float c_old(const GemmArgs& g, int64_t row, int64_t col) {
-  if constexpr (OBF)
-    return from16(static_cast<const uint16_t*>(g.C)[row * g.ldc + col]);
-  else
-    return static_cast<const float*>(g.C)[row * g.ldc + col];
-}
-template <bool OBF, int NV>
-__device__ __forceinline__ void epi_apply(const GemmArgs& g, float (&v)[NV], int64_t row, int64_t col,
-                                          int64_t valid) {
-  if (!g.epi) return;
-#pragma unroll
-  for (int e = 0; e < NV; ++e) {
-    if (e < valid) {
-      float x = g.alpha * v[e];
-      if (g.bias) x += g.bias[col + e];
-      if (g.beta != 0.f) x += g.beta * c_old<OBF>(g, row, col + e);
-      v[e] = x;
-    }
-  }
-}
-
 // Eight consecutive outputs of one row; `valid` of them exist.
 template <bool OBF>
 __device__ __forceinline__ void store_c8(void* C, int64_t idx, const float (&v)[8], int64_t valid) {
@@ -217,31 +152,6 @@ __device__ __forceinline__ void store_out8(const GemmArgs& g, int64_t row, int64
 // LDS rows are 16-byte chunks; the chunk index is XORed with low row bits so
 // that the lanes reading consecutive rows at one chunk hit distinct banks.
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row & 7) ^ ((row >> 3) & 1)); }
-
-// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2):
-// give every XCD a contiguous range of tile ids, so neighbouring tiles share an L2.
-__device__ __forceinline__ int xcd_remap(int b, int n) {
-  const int q = n >> 3, r = n & 7, x = b & 7, i = b >> 3;
-  return x * q + min(x, r) + i;
-}
-
-// Tile id -> (tile_m, tile_n). Grouped order: 8 tile rows per group, column
-// by column inside a group, so consecutive ids reuse A rows and B columns.
-__device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int grouped, int& tm, int& tn) {
-  if (!grouped) {
-    tm = t / tiles_n;
-    tn = t - tm * tiles_n;
-    return;
-  }
-  const int G = 8;
-  const int per_group = G * tiles_n;
-  const int grp = t / per_group;
-  const int first = grp * G;
-  const int gsz = min(tiles_m - first, G);
-  const int in = t - grp * per_group;
-  tm = first + in % gsz;
-  tn = in / gsz;
-}
 
 // ------------------------------------------------------------ tile kernel
 
@@ -764,8 +674,6 @@ __global__ __launch_bounds__(64 * tile_waves(BM, BN)) void k_tile_addmm(GemmArgs
 // (N not a multiple of 8) adds element stores. Requires the tile's span of C
 // below 2^31 bytes (the launcher checks ldc). bf16 output only; fp32 output
 // keeps the conditional register-to-memory stores.
-constexpr int32_t OOB_OFF = (int32_t)0x80000000u;  // past every tile's range
-constexpr uint32_t RSRC_WORD3 = 0x00020000u;      // raw buffer, 32-bit data
 
 template <int BM, int BN, int MS, bool EPI>
 __device__ __forceinline__ void store_acc_bf16_fixed(const typename AccOf<MS>::T (&acc)[TileShape<BM, BN, MS>::TM]
@@ -2147,6 +2055,14 @@ constexpr bool tiles_match() {
   return true;
 }
 static_assert(tiles_match(), "tile kernels must follow kTileCfg");
+constexpr bool dl_siblings_match() {
+  for (int i = 0; i < N_DL_CFG; ++i) {
+    const TileCfg& t = kTileCfg[kDlCfg[i].sibling];
+    if (t.bm != kDlCfg[i].bm || t.bn != kDlCfg[i].bn || t.ms != 32) return false;
+  }
+  return true;
+}
+static_assert(dl_siblings_match(), "a direct-to-LDS configuration falls back to the tile kernel of its tiling");
 static_assert(sizeof(kSkinnyMFns) / sizeof(kSkinnyMFns[0]) == N_SKINNY_M_CFG, "skinny-M table");
 static_assert(sizeof(kSkinnyNFns) / sizeof(kSkinnyNFns[0]) == N_SKINNY_N_CFG, "skinny-N table");
 
@@ -2231,6 +2147,15 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
     case FAM_PERSIST:
       if (p.cfg < 0 || p.cfg >= N_TILE_CFG || !kPersistFns[p.cfg] || g.K < 8 || g.N < 8) return hipErrorInvalidValue;
       return kPersistFns[p.cfg](p, g, st, obf);
+    case FAM_DL: {
+      if (p.cfg < 0 || p.cfg >= N_DL_CFG) return hipErrorInvalidValue;
+      // operands without 16-byte aligned rows: the same tiling (grid, split
+      // count, k granule, partial layout) on the register-staged tile kernel
+      if (!ac::dl_operands_aligned(g)) return kTileFns[kDlCfg[p.cfg].sibling](p, g, st, obf);
+      const hipError_t e = (launch_dl_main)(p, g, st);  // this format's kernels (no argument-dependent lookup)
+      if (e != hipSuccess || p.pk == 1) return e;
+      return launch_reduce(g, st, obf);
+    }
   }
   return hipErrorInvalidValue;
 }
@@ -2266,6 +2191,7 @@ void query_occupancy() {
     if (kGroupedOcc[i]) set_runtime_occupancy(FAM_GROUPED, i, kGroupedOcc[i]());
   for (int i = 0; i < N_TILE_CFG; ++i)
     if (kPersistOcc[i]) set_runtime_occupancy(FAM_PERSIST, i, kPersistOcc[i]());
+  query_occupancy_dl();
 }
 
 #if AC_INPUT_F16

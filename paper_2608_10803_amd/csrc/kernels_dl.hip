@@ -1,0 +1,503 @@
+// gfx950 macro-tile kernels whose operand tiles travel from global memory
+// straight into LDS (buffer_load ... lds: no staging registers, no register
+// transposes) through S LDS stages, so that S - 1 k-blocks of loads are in
+// flight while one is multiplied out (the Multi-Buffer module of Table 2;
+// the schedule of Eq. 13 with a deeper pipeline).
+//
+//   A tile  BM x 64 k, row-major as in memory, 16-byte chunks XOR-swizzled
+//           per row; MFMA fragments read with ds_read_b128.
+//   B tile  64 k x BN, row-major as in memory (chunks swizzled per k-row);
+//           MFMA fragments read with the LDS transpose read
+//           ds_read_b64_tr_b16, which hands each lane four consecutive k of
+//           one column: the k-contiguous operand the MFMA needs, without the
+//           v_perm transposes of the register-staged kernel.
+//   C       4 waves in a 2 x 2 grid, each a (BM/2) x (BN/2) quadrant of
+//           32 x 32 x 16 MFMAs; fp32 accumulation in the accumulation
+//           registers; bf16 output converted through a per-wave LDS slab and
+//           written as whole 16-byte row segments.
+//
+// The swizzle of a stage is applied on the global side: a wave-wide LDS load
+// writes 1024 contiguous bytes (lane l to bytes 16l .. 16l+15), so each lane
+// fetches the global chunk that belongs at its slot.
+//
+// Operands must be row-major with 16-byte aligned rows (A and B base
+// addresses 16-byte aligned, lda and ldb multiples of 8 below 2^22) and K, N
+// multiples of 8; the launcher of the plan checks this and otherwise runs
+// the same tiling on the register-staged tile kernel. Chunks outside the
+// matrices (rows past M, columns past N, k past K) are read as zeros through
+// out-of-range buffer offsets, so edge tiles take the same path.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "kernel_args.h"
+#include "registry.h"
+
+#ifndef AC_INPUT_F16
+#define AC_INPUT_F16 0
+#endif
+
+namespace ac {
+#if AC_INPUT_F16
+namespace f16 {
+#endif
+
+#include "device_common.h"
+
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_void;
+// the transpose read moves 16-bit patterns; its bf16 form serves fp16 too
+typedef __bf16 tr16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) tr16x4 lds_tr16x4;
+
+enum DlOut : int { DL_F32 = 0, DL_BF16 = 1, DL_PARTIAL = 2 };
+
+template <int BM, int BN, int BK_, int S_>
+struct Dl {
+  static constexpr int BN_ = BN, BK = BK_, S = S_, NT = 256;
+  static constexpr int WTM = BM / 2, WTN = BN / 2;  // wave quadrant
+  static constexpr int TM = WTM / 32, TN = WTN / 32;
+  static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BK * BN * 2;
+  static constexpr int A_LPR = BK / 8;        // 16-byte chunks of an A row
+  static constexpr int A_RPI = 64 / A_LPR;    // A rows per wave-wide load
+  static constexpr int B_LPR = BN / 8;        // 16-byte chunks of a B row
+  static constexpr int B_RPI = 64 / B_LPR;    // B rows per wave-wide load
+  static constexpr int NIA = A_BYTES / 4096;  // wave-wide loads per wave and A stage
+  static constexpr int NIB = B_BYTES / 4096;
+  static constexpr int LOADS = NIA + NIB;
+  static constexpr int CT_LD = WTN + 4;       // padded row of the bf16 output slab
+  static_assert(BM % 64 == 0 && BN >= 128 && BN <= 512 && (BK == 32 || BK == 64), "tile");
+  static_assert(3 * LOADS <= 63, "vmcnt range");
+  // the bf16 epilogue's per-wave slab of 32 output rows goes into one stage
+  // buffer per wave: A0, A1, B0, B1 if both kinds are large enough, else
+  // the first four of the kind that is
+  static constexpr int SLAB = 32 * CT_LD * 2;
+  static constexpr int SLAB_KIND = (SLAB <= A_BYTES && SLAB <= B_BYTES) ? 0 : (SLAB <= B_BYTES && S >= 4) ? 1 : 2;
+  static_assert(SLAB_KIND != 2 || (SLAB <= A_BYTES && S >= 4), "output slab fits a stage buffer");
+};
+
+// A stage: chunk c (8 k) of row r sits at slot c ^ swz_a(r) of the row's
+// slots (8 for 64-deep, 4 for 32-deep blocks): the lanes that read 8 or 16
+// consecutive rows at one chunk fall on distinct banks, for 32 as for 64
+// banks.
+template <int BK>
+__device__ __forceinline__ int swz_a(int r) {
+  if constexpr (BK == 64)
+    return (r & 7) ^ ((r >> 3) & 1);
+  else
+    return ((r >> 1) & 3) ^ ((r >> 3) & 1);
+}
+// B stage: chunk c of k-row r sits at slot c ^ f(r & 3), f = 0, 6, 12, 10.
+// One transpose read covers 4 consecutive k-rows and 2 (16 lanes) or 4 (32
+// lanes) consecutive chunks; f keeps those on distinct banks for both 32
+// and 64 banks.
+__device__ __forceinline__ int swz_b(int r) { return (0xAC60 >> (4 * (r & 3))) & 15; }
+
+// s_waitcnt immediate for vmcnt(n) alone (expcnt 7 and lgkmcnt 15 do not
+// wait; vmcnt bits 3:0 and 15:14)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Workgroup barrier of the pipeline: this wave waits until at most `ahead`
+// (0 .. 3) later stages of its own loads are in flight and its LDS reads
+// are done, then all waves meet. After it every wave's loads of the stage
+// about to be read have landed and no wave still reads the stage about to be
+// reloaded. (__syncthreads would add a workgroup fence, which waits for ALL
+// loads into LDS, the prefetched stages included.) The empty asm with a
+// memory clobber keeps the compiler from moving LDS accesses across it.
+template <int LOADS>
+__device__ __forceinline__ void stage_barrier(int ahead) {
+  if (ahead <= 0)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  else if (ahead == 1)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(LOADS));
+  else if (ahead == 2)
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));
+  else
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LOADS));
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Per-tile addressing of a workgroup's loads: the byte offset of every
+// 16-byte chunk this lane loads (OOB_OFF for rows past M and columns past
+// N), and the k of that chunk within the block for the K tail.
+template <class G>
+struct DlTile {
+  const char* a;  // A + m0 * lda
+  const char* b;  // B + n0
+  int64_t ldb2;
+  int64_t K;
+  int32_t a_off[G::NIA], b_off[G::NIB];
+  int32_t a_k[G::NIA], b_k[G::NIB];
+
+  __device__ __forceinline__ void init(const GemmArgs& g, int64_t m0, int64_t n0) {
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    a = reinterpret_cast<const char*>(g.A + m0 * g.lda);
+    b = reinterpret_cast<const char*>(g.B + n0);
+    ldb2 = g.ldb * 2;
+    K = g.K;
+    const int64_t rows = g.M - m0, cols = g.N - n0;
+#pragma unroll
+    for (int q = 0; q < G::NIA; ++q) {
+      const int u = w * G::NIA + q;            // 1024-byte block of the stage: A_RPI rows
+      const int row = u * G::A_RPI + lane / G::A_LPR;
+      const int c = (lane % G::A_LPR) ^ swz_a<G::BK>(row);  // the chunk this slot holds
+      a_off[q] = row < rows ? (int32_t)(row * g.lda * 2) + c * 16 : OOB_OFF;
+      a_k[q] = c * 8;
+    }
+#pragma unroll
+    for (int q = 0; q < G::NIB; ++q) {
+      const int u = w * G::NIB + q;
+      const int kr = u * G::B_RPI + lane / G::B_LPR;
+      const int c = (lane % G::B_LPR) ^ swz_b(kr);
+      b_off[q] = c * 8 < cols ? (int32_t)(kr * g.ldb * 2) + c * 16 : OOB_OFF;
+      b_k[q] = kr;
+    }
+  }
+};
+
+// This wave's share of the loads of one k-block (starting at k0) into one
+// stage: NIA loads of A, then NIB loads of B, issued one at a time so that
+// they can be spread between MFMAs. A block past K (the pipeline's tail)
+// loads nothing: every offset is out of range, the stage gets zeros that no
+// step reads.
+template <class G>
+struct StageLoads {
+  __amdgpu_buffer_rsrc_t ra, rb;
+  char* sA;
+  char* sB;
+  int krem;
+  bool full;
+  __device__ __forceinline__ void init(char* a_stage, char* b_stage, const DlTile<G>& t, int64_t k0) {
+    const int64_t kleft = t.K - k0;
+    krem = kleft < G::BK ? (int)(kleft > 0 ? kleft : 0) : G::BK;  // k in this block (uniform)
+    full = krem == G::BK;  // only a K tail needs the per-chunk test
+    ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(t.a) + k0 * 2, (short)0, (int)0x7FFFFFF0,
+                                           (int)RSRC_WORD3);
+    rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(t.b) + k0 * t.ldb2, (short)0, (int)0x7FFFFFF0,
+                                           (int)RSRC_WORD3);
+    sA = a_stage;
+    sB = b_stage;
+  }
+  // load q of this wave (0 .. NIA + NIB - 1; a compile-time index)
+  __device__ __forceinline__ void issue(const DlTile<G>& t, int q) const {
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (q < G::NIA) {
+      const int32_t off = full || t.a_k[q] < krem ? t.a_off[q] : OOB_OFF;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(sA + (w * G::NIA + q) * 1024), 16, off, 0, 0, 0);
+    } else {
+      const int qb = q - G::NIA;
+      const int32_t off = full || t.b_k[qb] < krem ? t.b_off[qb] : OOB_OFF;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(sB + (w * G::NIB + qb) * 1024), 16, off, 0, 0, 0);
+    }
+  }
+};
+
+template <class G>
+__device__ __forceinline__ void issue_stage(char* sA, char* sB, const DlTile<G>& t, int64_t k0) {
+  StageLoads<G> L;
+  L.init(sA, sB, t, k0);
+#pragma unroll
+  for (int q = 0; q < G::LOADS; ++q) L.issue(t, q);
+}
+
+// Fragments of one k-step (16 k) of a stage: TM A fragments (ds_read_b128
+// of a swizzled row chunk) and TN B fragments (two transpose reads each).
+template <class G>
+struct Frags {
+  u32x4 a[G::TM], b[G::TN];
+};
+
+template <class G>
+__device__ __forceinline__ void read_frags(const char* sA, const char* sB, int ks, int wr, int wc, Frags<G>& f) {
+  const int lane = threadIdx.x & 63;
+  const int l32 = lane & 31, hi = lane >> 5, i16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < G::TM; ++i) {
+    const int row = wr * G::WTM + 32 * i + l32;
+    const int ch = 2 * ks + hi;  // 8 consecutive k of the lane's k-group
+    f.a[i] = *reinterpret_cast<const u32x4*>(sA + row * (G::BK * 2) + ((ch ^ swz_a<G::BK>(row)) << 4));
+  }
+  // the transpose read of a 16-lane group covers 4 k-rows x 16 columns: lane
+  // i16 addresses k-row i16 >> 2 and columns 4 * (i16 & 3) .. +3 and receives
+  // column i16 of the 4 rows; groups 0 / 1 take columns 0-15 / 16-31 of the
+  // fragment at the lane's k-group 0, groups 2 / 3 the same at k-group 1
+  const int kr0 = 8 * (g >> 1) + (i16 >> 2);
+  const int sw = swz_b(kr0);  // every k-row the lane reads is kr0 mod 4
+#pragma unroll
+  for (int j = 0; j < G::TN; ++j) {
+    const int col = wc * G::WTN + 32 * j + 16 * (g & 1) + (i16 & 3) * 4;
+    const int cb = ((col >> 3) ^ sw) * 16 + (col & 7) * 2;
+    uint32_t v[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int kr = 16 * ks + 4 * h + kr0;
+      const tr16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_tr16x4*)(sB + kr * (G::BN_ * 2) + cb));
+      const uint64_t bits = __builtin_bit_cast(uint64_t, r);
+      v[2 * h] = (uint32_t)bits;
+      v[2 * h + 1] = (uint32_t)(bits >> 32);
+    }
+    f.b[j] = u32x4{v[0], v[1], v[2], v[3]};
+  }
+}
+
+// Multiplies out one stage: BK / 16 k-steps, TM x TN MFMAs each, while the
+// next stage's loads go out. The reads of step ks + 1 are issued before the
+// MFMAs of step ks (two fragment sets), so their latency runs under those
+// MFMAs; the next stage's global loads are spread one per MFMA over the
+// steps instead of leaving in one burst (a burst fills the load queue, and
+// a wave stalled on a full queue issues no MFMAs). The scheduling barriers
+// keep the compiler to this order.
+template <class G>
+__device__ __forceinline__ void compute_stage(const char* sA, const char* sB, f32x16 (&acc)[G::TM][G::TN],
+                                              int wr, int wc, const StageLoads<G>& nxt, const DlTile<G>& t) {
+  constexpr int KS = G::BK / 16, NMF = G::TM * G::TN;
+  // next-stage loads per k-step: with two stages the loads must land
+  // within this stage, so they all go out as early as possible (one per
+  // MFMA from the first step on); with more stages they are spread evenly
+  constexpr int LPS = G::S == 2 ? NMF : (G::LOADS + KS - 1) / KS;
+  static_assert(G::S > 2 || G::LOADS <= KS * NMF, "one load per MFMA at most");
+  Frags<G> f[2];
+  read_frags<G>(sA, sB, 0, wr, wc, f[0]);
+  __builtin_amdgcn_sched_barrier(0);  // step 0's reads first: its MFMAs wait for those only
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    Frags<G>& cur = f[ks & 1];
+    if (ks + 1 < KS) read_frags<G>(sA, sB, ks + 1, wr, wc, f[(ks + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < G::TN; ++j) acc[i][j] = mfma32(cur.b[j], cur.a[i], acc[i][j]);  // C^T: a lane holds a row of C
+#pragma unroll
+    for (int q = ks * LPS; q < (ks + 1) * LPS && q < G::LOADS; ++q) nxt.issue(t, q);
+#pragma unroll
+    for (int m = 0; m < NMF; ++m) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      if (m < LPS && ks * LPS + m < G::LOADS) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one load
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int BM, int BN, int BK, int S, int OUT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dl(GemmArgs g) {
+  typedef Dl<BM, BN, BK, S> G;
+  __shared__ __attribute__((aligned(1024))) char lA0[G::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lA1[G::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lA2[G::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lA3[G::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lA4[G::A_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lB0[G::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lB1[G::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lB2[G::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lB3[G::B_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lB4[G::B_BYTES];
+  static_assert(S >= 2 && S <= 5, "stages");
+
+  const int ntiles = g.tiles_m * g.tiles_n;
+  int tile = blockIdx.x;
+  if (g.swizzle) tile = xcd_remap(tile, ntiles);
+  int tm, tn;
+  tile_coords(tile, g.tiles_m, g.tiles_n, g.swizzle, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  // this workgroup's K partition: kper blocks of the plan's 64-deep granule,
+  // a whole number of this kernel's k-blocks
+  const int split = blockIdx.y;
+  const int64_t kbeg = min((int64_t)split * g.kper * 64, g.K);
+  const int64_t kend = min(kbeg + (int64_t)g.kper * 64, g.K);
+  const int nk = (int)((kend - kbeg + G::BK - 1) / G::BK);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+
+  DlTile<G> t;
+  t.init(g, m0, n0);
+
+  f32x16 acc[G::TM][G::TN];
+#pragma unroll
+  for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j) acc[i][j] = f32x16{};
+
+  // Stage I holds k-blocks I, I + S, I + 2S, ... of the partition. The
+  // stage buffers are distinct variables so that the compiler's wait
+  // before a read of one stage does not include the loads into the others.
+  auto stA = [&](auto ic) -> char* {
+    constexpr int I = decltype(ic)::value;
+    return I == 0 ? lA0 : I == 1 ? lA1 : I == 2 ? lA2 : I == 3 ? lA3 : lA4;
+  };
+  auto stB = [&](auto ic) -> char* {
+    constexpr int I = decltype(ic)::value;
+    return I == 0 ? lB0 : I == 1 ? lB1 : I == 2 ? lB2 : I == 3 ? lB3 : lB4;
+  };
+  // Every step issues one stage of loads (past the partition's last block:
+  // out-of-range loads), so at step kb exactly S - 2 stages of this wave's
+  // loads were issued after those of block kb.
+  const int64_t kstop = kbeg + (int64_t)nk * G::BK;  // the partition's end, rounded up to a block
+  auto kpos = [&](int b) { const int64_t k = kbeg + (int64_t)b * G::BK; return k < kstop ? k : t.K; };
+  if (nk > 0) {
+    issue_stage<G>(lA0, lB0, t, kpos(0));
+    if constexpr (S > 2) issue_stage<G>(lA1, lB1, t, kpos(1));
+    if constexpr (S > 3) issue_stage<G>(lA2, lB2, t, kpos(2));
+    if constexpr (S > 4) issue_stage<G>(lA3, lB3, t, kpos(3));
+  }
+
+  auto step = [&](auto ic, int kb) {
+    constexpr int I = decltype(ic)::value;
+    constexpr int NX = (I + S - 1) % S;  // stage that receives block kb + S - 1
+    stage_barrier<G::LOADS>(S - 2);
+    StageLoads<G> nxt;
+    nxt.init(stA(std::integral_constant<int, NX>{}), stB(std::integral_constant<int, NX>{}), t, kpos(kb + S - 1));
+    compute_stage<G>(stA(ic), stB(ic), acc, wr, wc, nxt, t);
+  };
+  // whole groups of S blocks, then the remaining 0 .. S-1 blocks
+  int kb = 0;
+  for (; kb + S <= nk; kb += S) {
+    step(std::integral_constant<int, 0>{}, kb);
+    step(std::integral_constant<int, 1>{}, kb + 1);
+    if constexpr (S > 2) step(std::integral_constant<int, 2>{}, kb + 2);
+    if constexpr (S > 3) step(std::integral_constant<int, 3>{}, kb + 3);
+    if constexpr (S > 4) step(std::integral_constant<int, 4>{}, kb + 4);
+  }
+  if (kb < nk) step(std::integral_constant<int, 0>{}, kb);
+  if (kb + 1 < nk) step(std::integral_constant<int, 1>{}, kb + 1);
+  if constexpr (S > 3)
+    if (kb + 2 < nk) step(std::integral_constant<int, 2>{}, kb + 2);
+  if constexpr (S > 4)
+    if (kb + 3 < nk) step(std::integral_constant<int, 3>{}, kb + 3);
+
+  // ---- epilogue
+  const int64_t rbase = m0 + wr * G::WTM, cbase = n0 + wc * G::WTN;
+  if constexpr (OUT == DL_BF16) {
+    stage_barrier<G::LOADS>(0);  // every wave's last reads of the stages are done
+    // the wave's slab: 32 rows x WTN bf16 in one of the stage buffers
+    char* slab;
+    if constexpr (G::SLAB_KIND == 0)
+      slab = wave == 0 ? lA0 : wave == 1 ? lA1 : wave == 2 ? lB0 : lB1;
+    else if constexpr (G::SLAB_KIND == 1)
+      slab = wave == 0 ? lB0 : wave == 1 ? lB1 : wave == 2 ? lB2 : lB3;
+    else
+      slab = wave == 0 ? lA0 : wave == 1 ? lA1 : wave == 2 ? lA2 : lA3;
+    uint16_t* ct = reinterpret_cast<uint16_t*>(slab);
+    uint16_t* C = static_cast<uint16_t*>(g.C);
+    constexpr int GPR = G::WTN / 8;  // 16-byte groups per slab row
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i) {
+      const int64_t row = rbase + 32 * i + (lane & 31);
+#pragma unroll
+      for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = 32 * j + (q << 3) + ((lane >> 5) << 2);  // acc elements 4q .. 4q+3: four columns
+          float w[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          if (g.epi && row < g.M && cbase + c < g.N) epi_apply<true, 4>(g, w, row, cbase + c, g.N - cbase - c);
+          const uint32_t lo = (uint32_t)to16(w[0]) | ((uint32_t)to16(w[1]) << 16);
+          const uint32_t hi = (uint32_t)to16(w[2]) | ((uint32_t)to16(w[3]) << 16);
+          *reinterpret_cast<uint64_t*>(ct + (lane & 31) * G::CT_LD + c) = (uint64_t)lo | ((uint64_t)hi << 32);
+        }
+      // the slab back as 16-byte row segments (the same wave: LDS is in order)
+#pragma unroll
+      for (int v = 0; v < 32 * GPR / 64; ++v) {
+        const int u = lane + 64 * v, r = u / GPR, grp = u % GPR;
+        const uint16_t* src = ct + r * G::CT_LD + grp * 8;
+        const uint64_t a = *reinterpret_cast<const uint64_t*>(src);
+        const uint64_t b = *reinterpret_cast<const uint64_t*>(src + 4);
+        const int64_t gr = rbase + 32 * i + r, gc = cbase + grp * 8;
+        if (gr < g.M && gc < g.N) {  // N is a multiple of 8: the group is whole
+          const uint64_t vv[2] = {a, b};
+          __builtin_memcpy(C + gr * g.ldc + gc, vv, 16);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // slab by slab: bounded live registers
+    }
+  } else {
+    float* dst = OUT == DL_PARTIAL ? g.ws + (size_t)split * (size_t)g.M * (size_t)g.ldw : static_cast<float*>(g.C);
+    const int64_t ld = OUT == DL_PARTIAL ? g.ldw : g.ldc;
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i) {
+      const int64_t row = rbase + 32 * i + (lane & 31);
+      if (row >= g.M) continue;
+#pragma unroll
+      for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t col = cbase + 32 * j + (q << 3) + ((lane >> 5) << 2);
+          if (col >= g.N) continue;  // N is a multiple of 8: four columns are whole
+          float w[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          if (OUT == DL_F32 && g.epi) epi_apply<false, 4>(g, w, row, col, g.N - col);
+          const f32x4 vv = {w[0], w[1], w[2], w[3]};
+          __builtin_memcpy(dst + row * ld + col, &vv, 16);
+        }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+template <int BM, int BN, int BK, int S>
+hipError_t launch_dl(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
+  const dim3 grid(p.grid_x, p.grid_y), block(256);
+  if (p.pk > 1)
+    hipLaunchKernelGGL((k_dl<BM, BN, BK, S, DL_PARTIAL>), grid, block, 0, st, g);
+  else if (obf)
+    hipLaunchKernelGGL((k_dl<BM, BN, BK, S, DL_BF16>), grid, block, 0, st, g);
+  else
+    hipLaunchKernelGGL((k_dl<BM, BN, BK, S, DL_F32>), grid, block, 0, st, g);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int S>
+int occ_dl() {
+  int o = 1 << 20;
+  const void* ks[3] = {reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_F32>),
+                       reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_BF16>),
+                       reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_PARTIAL>)};
+  for (const void* k : ks) {
+    int a = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, k, 256, 0) != hipSuccess) a = 0;
+    o = a < o ? a : o;
+  }
+  return o;
+}
+
+typedef hipError_t (*DlLaunchFn)(const Plan&, const GemmArgs&, hipStream_t, bool);
+typedef int (*DlOccFn)();
+#define DL_CFGS(X) X(256, 256, 64, 2), X(256, 128, 64, 3), X(128, 256, 64, 3), X(128, 128, 64, 3), X(256, 256, 32, 4), \
+    X(256, 256, 32, 5), X(256, 128, 32, 4), X(128, 256, 32, 4)
+#define DL_L(a, b, c, d) &launch_dl<a, b, c, d>
+#define DL_O(a, b, c, d) &occ_dl<a, b, c, d>
+#define DL_C(a, b, c, d) {a, b, c, d}
+const DlLaunchFn kDlFns[] = {DL_CFGS(DL_L)};
+const DlOccFn kDlOcc[] = {DL_CFGS(DL_O)};
+constexpr int kDlCheck[][4] = {DL_CFGS(DL_C)};
+constexpr bool dl_match() {
+  for (int i = 0; i < N_DL_CFG; ++i)
+    if (kDlCheck[i][0] != kDlCfg[i].bm || kDlCheck[i][1] != kDlCfg[i].bn || kDlCheck[i][2] != kDlCfg[i].bk ||
+        kDlCheck[i][3] != kDlCfg[i].stages)
+      return false;
+  return true;
+}
+static_assert(sizeof(kDlFns) / sizeof(kDlFns[0]) == N_DL_CFG && dl_match(), "kernels must follow kDlCfg");
+
+}  // namespace
+
+hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st) {
+  if (p.family != FAM_DL || p.cfg < 0 || p.cfg >= N_DL_CFG || !ac::dl_operands_aligned(g)) return hipErrorInvalidValue;
+  return kDlFns[p.cfg](p, g, st, dtype_out16(p.s.dtype));
+}
+
+void query_occupancy_dl() {
+  for (int i = 0; i < N_DL_CFG; ++i) set_runtime_occupancy(FAM_DL, i, kDlOcc[i]());
+}
+
+#if AC_INPUT_F16
+}  // namespace f16
+#else
+bool dl_operands_aligned(const GemmArgs& g) {
+  return ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.B)) & 15) == 0 && (g.lda & 7) == 0 &&
+         (g.ldb & 7) == 0 && (g.K & 7) == 0 && (g.N & 7) == 0 && g.lda < DL_MAX_LD && g.ldb < DL_MAX_LD;
+}
+#endif
+}  // namespace ac

@@ -36,6 +36,8 @@ int table_occ(int family, int cfg) {
       return kSmallKCfg[cfg].occ;
     case FAM_DIRECT:
       return kDirectCfg[cfg].occ;
+    case FAM_DL:
+      return 1;
   }
   return 1;
 }
@@ -50,7 +52,8 @@ constexpr int IDX_SMALLK = IDX_SKINNY_N + N_SKINNY_N_CFG;
 constexpr int IDX_STREAMK = IDX_SMALLK + N_SMALLK_CFG;
 constexpr int IDX_DIRECT = IDX_STREAMK + N_STREAMK_CFG;
 constexpr int IDX_PERSIST = IDX_DIRECT + N_DIRECT_CFG;
-static_assert(IDX_PERSIST + N_TILE_CFG <= AC_N_CFG, "calibrated cost tables");
+constexpr int IDX_DL = IDX_PERSIST + N_TILE_CFG;
+static_assert(IDX_DL + N_DL_CFG <= AC_N_CFG, "calibrated cost tables");
 
 // Tiles the taxonomy uses for its spatial predicate: the menu entries whose
 // accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
@@ -220,6 +223,32 @@ bool build_persist(const Ctx& c, int cfg, int swizzle, Plan* p, Work* w) {
   w->idx = IDX_PERSIST + cfg;
   w->L = (double)per * (double)p->kper;
   w->out_unit *= (double)per;
+  return true;
+}
+
+// Direct-to-LDS tile kernel: the tile kernel's tiling and split counts with
+// stages - 1 k-blocks of loads in flight (Eq. 13 with a deeper pipeline) and
+// no register staging. Offered where every 16-byte chunk of a row lies
+// wholly inside or outside the matrix (K and N multiples of 8); the caller's
+// pointers and leading dimensions are checked at launch, which runs the
+// register-staged sibling of the same tiling when they are not aligned.
+bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w) {
+  if (cfg < 0 || cfg >= N_DL_CFG) return false;
+  const DlCfg& d = kDlCfg[cfg];
+  const Shape& s = c.s;
+  if ((s.K % 8) != 0 || (s.N % 8) != 0 || s.K < 1) return false;
+  if (dl_lds_bytes(d) > c.hw.lds_bytes) return false;
+  if (!build_tile(c, d.sibling, pk_req, swizzle, p, w)) return false;
+  p->family = FAM_DL;
+  p->cfg = cfg;
+  w->occ = occupancy(FAM_DL, cfg);
+  w->idx = IDX_DL + cfg;
+  // LDS traffic per iteration (one TILE_BK of k): the stage written once by
+  // the loads, A read once per column half and B once per row half (4 waves
+  // in 2 x 2); the pipeline holds (stages - 1) * bk of k in flight
+  w->lds_it = (double)(d.bm + d.bn) * TILE_BK * 2 * 3;
+  w->prefetch = (double)(d.stages - 1) * d.bk / TILE_BK;
+  w->unaligned = false;
   return true;
 }
 
@@ -720,6 +749,29 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
       if (build_persist(c, cfg, sw, &p, &w)) add(p, w);
     }
   }
+  // direct-to-LDS tile kernels: in the class-fixed search only once their
+  // costs are calibrated
+  for (int cfg = 0; cfg < N_DL_CFG; ++cfg) {
+    const int idx = IDX_DL + cfg;
+    if (!c.hw.search_open && !(c.hw.cfg_iter[idx] > 0 && c.hw.cfg_wg[idx] > 0)) continue;
+    const DlCfg& d = kDlCfg[cfg];
+    if (d.bm > 2 * s.M || d.bn > 2 * s.N) continue;
+    for (int sw = 0; sw < 2; ++sw) {
+      const int64_t ntiles = cdiv(s.M, d.bm) * cdiv(s.N, d.bn);
+      if (sw == 1 && ntiles < 16) continue;
+      {
+        Plan p;
+        Work w;
+        if (build_dl(c, cfg, 1, sw, &p, &w)) add(p, w);
+      }
+      for (int pk : kSplits) {
+        if ((int64_t)pk * ntiles > 8LL * c.hw.n_cu) break;
+        Plan p;
+        Work w;
+        if (build_dl(c, cfg, pk, sw, &p, &w)) add(p, w);
+      }
+    }
+  }
   for (int cfg = 0; cfg < N_SKINNY_M_CFG; ++cfg) {
     const int64_t cb = cdiv(s.N, skinny_m_cols(kSkinnyMCfg[cfg]));
     {
@@ -844,6 +896,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
       break;
     case FAM_PERSIST:
       ok = pk == 1 && build_persist(c, cfg, sw, &p, &w);
+      break;
+    case FAM_DL:
+      ok = cfg < N_DL_CFG && pk >= 1 && build_dl(c, cfg, pk, sw, &p, &w);
       break;
   }
   if (!ok || !finish(c, &p, w)) return false;
@@ -1038,6 +1093,13 @@ static std::string kernel_names_fmt(const Plan& p) {
       if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
       return r;
     }
+    case FAM_DL: {
+      const DlCfg& d = kDlCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "k_dl<%d, %d, %d, %d, %d>", d.bm, d.bn, d.bk, d.stages, p.pk > 1 ? 2 : obf);
+      std::string r(buf);
+      if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
+      return r;
+    }
   }
   return "";
 }
@@ -1058,6 +1120,8 @@ int config_index(int family, int cfg) {
       return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
     case FAM_PERSIST:
       return cfg >= 0 && cfg < N_TILE_CFG && kPersistCfg[cfg] ? IDX_PERSIST + cfg : -1;
+    case FAM_DL:
+      return cfg >= 0 && cfg < N_DL_CFG ? IDX_DL + cfg : -1;
     case FAM_BATCHED:
     case FAM_GROUPED:  // the tile kernel's costs
       return cfg >= 0 && cfg < N_TILE_CFG && kGroupedCfg[cfg] ? IDX_TILE + cfg : -1;

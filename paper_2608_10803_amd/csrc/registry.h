@@ -8,6 +8,14 @@
 namespace ac {
 // bf16 inputs (dtypes 0 and 1)
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
+// Direct-to-LDS tile kernels (kernels_dl.hip): whether the operands meet
+// their alignment (16-byte aligned rows of A and B, K and N multiples of 8,
+// lda and ldb below DL_MAX_LD; the same for both input formats), and the
+// main kernel of a FAM_DL plan (the split-K reduction is launched by
+// launch_plan).
+bool dl_operands_aligned(const GemmArgs& g);
+hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
+void query_occupancy_dl();
 // Launch of a grouped or batched plan (families FAM_GROUPED, FAM_BATCHED).
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 // Reads the device's occupancy of every kernel into the planner.
@@ -20,6 +28,8 @@ hipError_t launch_transpose16(const uint16_t* src, int64_t ld_src, int64_t rows,
 // the same kernels for fp16 inputs (dtypes 2 and 3)
 namespace f16 {
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
+hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
+void query_occupancy_dl();
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 void query_occupancy();
 }  // namespace f16

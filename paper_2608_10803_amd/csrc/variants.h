@@ -77,6 +77,22 @@ constexpr DirectCfg kDirectCfg[] = {{1, 4}, {4, 4}, {16, 1}};
 constexpr int N_DIRECT_CFG = sizeof(kDirectCfg) / sizeof(kDirectCfg[0]);
 inline int direct_tile(const DirectCfg& c) { return c.wk == 1 ? 64 : 32; }
 
+// Direct-to-LDS tile configurations (family FAM_DL): BM x BN output tile, 4
+// waves in a 2 x 2 grid, k-blocks of bk (32 or 64; splits stay in units of
+// TILE_BK), `stages` LDS stages (stages - 1 k-blocks of loads in flight);
+// one workgroup per CU. `sibling` is the register-staged tile configuration
+// of the same tiling, which runs the plan when the caller's operands are not
+// 16-byte aligned row by row.
+struct DlCfg {
+  int bm, bn, bk, stages, sibling;
+};
+constexpr DlCfg kDlCfg[] = {{256, 256, 64, 2, 0}, {256, 128, 64, 3, 1}, {128, 256, 64, 3, 2}, {128, 128, 64, 3, 3},
+                            {256, 256, 32, 4, 0}, {256, 256, 32, 5, 0}, {256, 128, 32, 4, 1}, {128, 256, 32, 4, 2}};
+constexpr int N_DL_CFG = sizeof(kDlCfg) / sizeof(kDlCfg[0]);
+// leading dimensions of A and B the direct-to-LDS kernels address (elements)
+constexpr int64_t DL_MAX_LD = 1LL << 22;
+inline int dl_lds_bytes(const DlCfg& d) { return d.stages * (d.bm + d.bn) * d.bk * 2; }
+
 // 64-bit key of a configuration:
 //   bits  0- 3 family, 4-11 config index, 12 swizzle, 16-35 P_k (or the
 //   stream-K grid), 36-47 reserved, 48-51 dtype, 52-53 layouts.

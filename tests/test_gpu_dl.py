@@ -1,0 +1,134 @@
+"""GPU parity of the direct-to-LDS tile kernels (family dl).
+
+Every dl configuration of each shape (tile, split count, tile order) runs
+through the C ABI and is checked against the fp64 oracle at the output
+type's tolerance and, bit for bit, against the register-staged tile kernel
+of the same tiling and split count: both multiply the same fragments in the
+same k order, so any difference is a loading, swizzle or transpose-read
+error. The shapes cover K tails (K not a multiple of the 64-deep k-block,
+down to K = 8), ragged M and N edges, partial last stage groups and split
+K. Operands that break the kernels' alignment (an odd leading dimension, a
+2-byte offset pointer) must run the sibling tile kernel instead, and the
+AddMM epilogue and fp16 inputs take the same path.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2608_10803_amd as ac
+from oracle import addmm_ref, gemm_ref
+from workloads import gen
+
+from gpu_util import all_candidates, check, forced_plan, run, run_addmm, tol, torch
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16 = ac.AC_BF16_F32OUT, ac.AC_BF16_BF16OUT
+F16F32, F16F16 = ac.AC_F16_F32OUT, ac.AC_F16_F16OUT
+DL_SIBLING = [0, 1, 2, 3, 0, 0, 1, 2]  # variants.h kDlCfg[i].sibling
+
+
+def note(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    torch()
+    ac.adaptcore_init()
+    yield
+
+
+def dl_candidates(M, N, K, dtype):
+    return [c for c in all_candidates(M, N, K, dtype) if c["family_name"] == "dl"]
+
+
+def sibling_key(key):
+    """The tile-family key of a dl key: same tiling, split count, tile order."""
+    cfg = (key >> 4) & 0xFF
+    return (key & ~0xFFF) | (key & (1 << 12)) | (DL_SIBLING[cfg] << 4) | ac.AC_FAMILY_TILE
+
+
+SHAPES = [(300, 264, 200), (513, 640, 1000), (257, 136, 136), (1024, 1024, 1024), (96, 4096, 8192),
+          (2048, 512, 64), (300, 256, 8), (130, 392, 4104), (700, 128, 520)]
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_every_dl_configuration_against_oracle_and_sibling(shape, dtype):
+    M, N, K = shape
+    A, B = gen.operands(M, N, K, seed=3 * M + 5 * N + K)
+    ref = gemm_ref.gemm(A, B)
+    cands = dl_candidates(M, N, K, dtype)
+    assert cands, shape
+    note("dl", shape, dtype, len(cands), "configurations")
+    for c in cands:
+        key = c["variant_key"]
+        vals, ok = run(forced_plan(M, N, K, dtype, key), A, B, M, N, K, dtype)
+        check(vals, ok, A, B, dtype, ref=ref, label="%s %s" % (shape, c))
+        sib, ok2 = run(forced_plan(M, N, K, dtype, sibling_key(key)), A, B, M, N, K, dtype)
+        assert ok2
+        assert np.array_equal(vals.view(np.uint64), sib.view(np.uint64)), ("differs from the tile kernel", shape, c)
+
+
+def test_integer_inputs_exact_for_every_dl_configuration():
+    """Integer inputs: every partial sum exact in fp32, so every split gives
+    the exact integer product."""
+    M, N, K = 200, 392, 5000
+    A, B = gen.operands(M, N, K, seed=13, dist="int")
+    exact = (np.rint(gemm_ref.decode(A)).astype(np.int64) @ np.rint(gemm_ref.decode(B)).astype(np.int64))
+    for c in dl_candidates(M, N, K, F32):
+        vals, ok = run(forced_plan(M, N, K, F32, c["variant_key"]), A, B, M, N, K, F32)
+        assert ok and np.array_equal(vals, exact.astype(np.float64)), c
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+def test_unaligned_operands_run_the_sibling(dtype):
+    """A leading dimension that is not a multiple of 8, or an A / B pointer
+    2 bytes off a 16-byte boundary, runs the register-staged tile kernel of
+    the same tiling: the same bits as that kernel called directly."""
+    M, N, K = 300, 264, 520
+    A, B = gen.operands(M, N, K, seed=17)
+    ref = gemm_ref.gemm(A, B)
+    for c in dl_candidates(M, N, K, dtype):
+        key = c["variant_key"]
+        dl, sib = forced_plan(M, N, K, dtype, key), forced_plan(M, N, K, dtype, sibling_key(key))
+        for kw in [dict(lda=K + 3), dict(ldb=N + 4), dict(a_off=1), dict(b_off=3), dict(lda=K + 8, ldb=N + 16)]:
+            v1, ok1 = run(dl, A, B, M, N, K, dtype, **kw)
+            v2, ok2 = run(sib, A, B, M, N, K, dtype, **kw)
+            check(v1, ok1, A, B, dtype, ref=ref, label="%s %s" % (kw, c))
+            assert ok2 and np.array_equal(v1.view(np.uint64), v2.view(np.uint64)), (kw, c)
+
+
+@pytest.mark.parametrize("dtype", [F16F32, F16F16], ids=["f32out", "f16out"])
+def test_fp16_dl_configurations(dtype):
+    M, N, K = 300, 264, 1000
+    A, B = gen.operands(M, N, K, seed=19, dist="uniform_f16")
+    ref = gemm_ref.gemm(A, B, fmt="fp16")
+    cands = dl_candidates(M, N, K, dtype)
+    assert cands
+    for c in cands:
+        vals, ok = run(forced_plan(M, N, K, dtype, c["variant_key"]), A, B, M, N, K, dtype)
+        check(vals, ok, A, B, dtype, ref=ref, label=str(c))
+        sib, _ = run(forced_plan(M, N, K, dtype, sibling_key(c["variant_key"])), A, B, M, N, K, dtype)
+        assert np.array_equal(vals.view(np.uint64), sib.view(np.uint64)), c
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+def test_addmm_through_dl_plans(dtype):
+    M, N, K = 260, 392, 704
+    A, B = gen.operands(M, N, K, seed=23)
+    old32 = gen.uniform_f32(M, N, 24)
+    old = old32 if dtype == F32 else gen.bf16_bits(old32)
+    old_vals = old32.astype(np.float64) if dtype == F32 else gemm_ref.decode(old)
+    bias = gen.uniform_f32(1, N, 25).reshape(-1)
+    R, D = addmm_ref.addmm(A, B, old_vals, -1.25, 0.5, bias)
+    for c in dl_candidates(M, N, K, dtype):
+        if c["pk"] != 1:
+            continue
+        vals, ok = run_addmm(forced_plan(M, N, K, dtype, c["variant_key"]), A, B, M, N, K, dtype, old, -1.25, 0.5,
+                             bias)
+        assert ok, c
+        err = gemm_ref.err_metric(vals, R, D)
+        assert err <= tol(dtype), (c, err)
