@@ -398,6 +398,25 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   g.sk_tiles = p.sk_tiles;
   g.ws_pk = p.ws_pk;
   g.grid = p.grid_x;
+  g.kB = K;
+  g.nB = N;
+  // Direct-to-LDS plans: operands the plan does not copy must have 16-byte
+  // aligned rows of whole chunks; otherwise the register-staged sibling of
+  // the same tiling runs on the operands as given (no padding copies).
+  ac::Plan sib;
+  const ac::Plan* run = &p;
+  bool dl = p.family == ac::FAM_DL;
+  if (dl) {
+    const bool a_ok = a_col || p.ws_a_off >= 0 || ac::dl_a_aligned(A, lda, K);
+    const bool b_ok = b_col || p.ws_b_off >= 0 || ac::dl_b_aligned(B, ldb, N);
+    if (!(a_ok && b_ok)) {
+      sib = p;
+      sib.family = ac::FAM_TILE;
+      sib.cfg = ac::kDlCfg[p.cfg].sibling;
+      run = &sib;
+      dl = false;
+    }
+  }
   if (p.ws_bytes > 0) {
     Workspace w;
     if (fixed) {
@@ -418,22 +437,33 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
     g.ws = reinterpret_cast<float*>(w.ptr);
     // prologue: row-major copies of column-major operands (A: M x K, B: K x N)
     char* base = static_cast<char*>(w.ptr);
-    if (p.ws_a_off >= 0) {
+    // prologue: row-major copies of column-major operands, and zero-padded
+    // copies of unaligned row-major operands for direct-to-LDS plans (rows
+    // of K and N rounded up to 8)
+    const int64_t K8 = (K + 7) / 8 * 8, N8 = (N + 7) / 8 * 8;
+    if (p.ws_a_off >= 0 && (a_col || dl)) {
       uint16_t* a2 = reinterpret_cast<uint16_t*>(base + p.ws_a_off);
-      const hipError_t e = ac::launch_transpose16(g.A, lda, K, M, a2, (K + 7) / 8 * 8, s);
+      const hipError_t e = a_col ? ac::launch_transpose16(g.A, lda, K, M, a2, K8, s)
+                                 : ac::launch_pad16(g.A, lda, M, K, a2, K8, s);
       if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
       g.A = a2;
-      g.lda = (K + 7) / 8 * 8;
+      g.lda = K8;
     }
-    if (p.ws_b_off >= 0) {
+    if (p.ws_b_off >= 0 && (b_col || dl)) {
       uint16_t* b2 = reinterpret_cast<uint16_t*>(base + p.ws_b_off);
-      const hipError_t e = ac::launch_transpose16(g.B, ldb, N, K, b2, (N + 7) / 8 * 8, s);
+      const hipError_t e = b_col ? ac::launch_transpose16(g.B, ldb, N, K, b2, N8, s)
+                                 : ac::launch_pad16(g.B, ldb, K, N, b2, N8, s);
       if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
       g.B = b2;
-      g.ldb = (N + 7) / 8 * 8;
+      g.ldb = N8;
+      if (dl) g.nB = N8;
     }
+    // the direct-to-LDS loop runs over whole 8-element chunks of A's rows
+    // (zeros past K in a copy); B's rows stay K
+    if (dl) g.K = K8;
   }
-  const hipError_t e = ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(p, g, s) : ac::launch_plan(p, g, s);
+  const hipError_t e =
+      ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(*run, g, s) : ac::launch_plan(*run, g, s);
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
   st_launches.fetch_add((uint64_t)p.n_launch, std::memory_order_relaxed);
   return AC_OK;

@@ -52,6 +52,11 @@ struct GemmArgs {
   float alpha, beta;
   const float* bias;  // N values or null
   int epi;
+  // Direct-to-LDS kernels: the rows of B (its real K) and the columns of B
+  // that may be loaded (N, or N rounded up to 8 when B is a zero-padded
+  // copy). K is then the k the loop runs over: rounded up to 8 when A is a
+  // zero-padded copy. Other kernels ignore both.
+  int64_t kB, nB;
 };
 
 // Arguments of the grouped kernel. With counts: group g owns rows

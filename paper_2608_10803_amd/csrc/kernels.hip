@@ -2149,9 +2149,9 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       return kPersistFns[p.cfg](p, g, st, obf);
     case FAM_DL: {
       if (p.cfg < 0 || p.cfg >= N_DL_CFG) return hipErrorInvalidValue;
-      // operands without 16-byte aligned rows: the same tiling (grid, split
-      // count, k granule, partial layout) on the register-staged tile kernel
-      if (!ac::dl_operands_aligned(g)) return kTileFns[kDlCfg[p.cfg].sibling](p, g, st, obf);
+      // the caller (adaptcore_matmul) runs the register-staged sibling when
+      // the operands are not aligned for these kernels
+      if (!ac::dl_operands_aligned(g)) return hipErrorInvalidValue;
       const hipError_t e = (launch_dl_main)(p, g, st);  // this format's kernels (no argument-dependent lookup)
       if (e != hipSuccess || p.pk == 1) return e;
       return launch_reduce(g, st, obf);

@@ -127,7 +127,7 @@ struct DlTile {
   const char* a;  // A + m0 * lda
   const char* b;  // B + n0
   int64_t ldb2;
-  int64_t K;
+  int64_t K, kB;  // k of the loop (A's columns), rows of B
   int32_t a_off[G::NIA], b_off[G::NIB];
   int32_t a_k[G::NIA], b_k[G::NIB];
 
@@ -138,7 +138,8 @@ struct DlTile {
     b = reinterpret_cast<const char*>(g.B + n0);
     ldb2 = g.ldb * 2;
     K = g.K;
-    const int64_t rows = g.M - m0, cols = g.N - n0;
+    kB = g.kB;
+    const int64_t rows = g.M - m0, cols = g.nB - n0;
 #pragma unroll
     for (int q = 0; q < G::NIA; ++q) {
       const int u = w * G::NIA + q;            // 1024-byte block of the stage: A_RPI rows
@@ -168,12 +169,14 @@ struct StageLoads {
   __amdgpu_buffer_rsrc_t ra, rb;
   char* sA;
   char* sB;
-  int krem;
-  bool full;
+  int krem, kremB;
+  bool full, fullB;
   __device__ __forceinline__ void init(char* a_stage, char* b_stage, const DlTile<G>& t, int64_t k0) {
-    const int64_t kleft = t.K - k0;
-    krem = kleft < G::BK ? (int)(kleft > 0 ? kleft : 0) : G::BK;  // k in this block (uniform)
+    const int64_t kleft = t.K - k0, kleftB = t.kB - k0;
+    krem = kleft < G::BK ? (int)(kleft > 0 ? kleft : 0) : G::BK;  // k of A in this block (uniform)
+    kremB = kleftB < G::BK ? (int)(kleftB > 0 ? kleftB : 0) : G::BK;  // rows of B in this block
     full = krem == G::BK;  // only a K tail needs the per-chunk test
+    fullB = kremB == G::BK;
     ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(t.a) + k0 * 2, (short)0, (int)0x7FFFFFF0,
                                            (int)RSRC_WORD3);
     rb = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(t.b) + k0 * t.ldb2, (short)0, (int)0x7FFFFFF0,
@@ -189,7 +192,7 @@ struct StageLoads {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(sA + (w * G::NIA + q) * 1024), 16, off, 0, 0, 0);
     } else {
       const int qb = q - G::NIA;
-      const int32_t off = full || t.b_k[qb] < krem ? t.b_off[qb] : OOB_OFF;
+      const int32_t off = fullB || t.b_k[qb] < kremB ? t.b_off[qb] : OOB_OFF;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(sB + (w * G::NIB + qb) * 1024), 16, off, 0, 0, 0);
     }
   }
@@ -406,9 +409,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const uint64_t a = *reinterpret_cast<const uint64_t*>(src);
         const uint64_t b = *reinterpret_cast<const uint64_t*>(src + 4);
         const int64_t gr = rbase + 32 * i + r, gc = cbase + grp * 8;
-        if (gr < g.M && gc < g.N) {  // N is a multiple of 8: the group is whole
+        if (gr < g.M && gc + 8 <= g.N) {
           const uint64_t vv[2] = {a, b};
           __builtin_memcpy(C + gr * g.ldc + gc, vv, 16);
+        } else if (gr < g.M && gc < g.N) {  // the last, partial group of a row
+          const uint16_t* e = src;
+          for (int j = 0; j < (int)(g.N - gc); ++j) C[gr * g.ldc + gc + j] = e[j];
         }
       }
       __builtin_amdgcn_sched_barrier(0);  // slab by slab: bounded live registers
@@ -425,11 +431,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int64_t col = cbase + 32 * j + (q << 3) + ((lane >> 5) << 2);
-          if (col >= g.N) continue;  // N is a multiple of 8: four columns are whole
+          if (col >= g.N) continue;
           float w[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
           if (OUT == DL_F32 && g.epi) epi_apply<false, 4>(g, w, row, col, g.N - col);
-          const f32x4 vv = {w[0], w[1], w[2], w[3]};
-          __builtin_memcpy(dst + row * ld + col, &vv, 16);
+          if (col + 4 <= g.N) {
+            const f32x4 vv = {w[0], w[1], w[2], w[3]};
+            __builtin_memcpy(dst + row * ld + col, &vv, 16);
+          } else {
+            for (int e = 0; e < (int)(g.N - col); ++e) dst[row * ld + col + e] = w[e];
+          }
         }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -495,9 +505,48 @@ void query_occupancy_dl() {
 #if AC_INPUT_F16
 }  // namespace f16
 #else
-bool dl_operands_aligned(const GemmArgs& g) {
-  return ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.B)) & 15) == 0 && (g.lda & 7) == 0 &&
-         (g.ldb & 7) == 0 && (g.K & 7) == 0 && (g.N & 7) == 0 && g.lda < DL_MAX_LD && g.ldb < DL_MAX_LD;
+bool dl_a_aligned(const void* A, int64_t lda, int64_t K) {
+  return (reinterpret_cast<uintptr_t>(A) & 15) == 0 && (lda & 7) == 0 && (K & 7) == 0 && lda < DL_MAX_LD;
+}
+bool dl_b_aligned(const void* B, int64_t ldb, int64_t nB) {
+  return (reinterpret_cast<uintptr_t>(B) & 15) == 0 && (ldb & 7) == 0 && (nB & 7) == 0 && ldb < DL_MAX_LD;
+}
+bool dl_operands_aligned(const GemmArgs& g) { return dl_a_aligned(g.A, g.lda, g.K) && dl_b_aligned(g.B, g.ldb, g.nB); }
+
+// ---- padding prologue (the Padding module of Table 2)
+// dst (rows x ld_dst, ld_dst = cols rounded up to 8, 16-byte aligned) =
+// src (rows x cols, row pitch ld_src, any 2-byte alignment), zeros in the pad
+// columns: every row of the copy is a whole number of aligned 16-byte
+// chunks. A thread moves one 16-byte group; x: groups of a row, y: rows.
+__global__ __launch_bounds__(256) void k_pad16(const uint16_t* __restrict__ src, int64_t ld_src,
+                                               uint16_t* __restrict__ dst, int64_t ld_dst, int64_t rows,
+                                               int64_t cols) {
+  const int64_t c = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (c >= ld_dst) return;
+  for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+    const uint16_t* s = src + r * ld_src + c;
+    u32x4 v;
+    if (c + 8 <= cols) {
+      __builtin_memcpy(&v, s, 16);  // unaligned 16-byte load (gfx950 unaligned mode)
+    } else {
+      uint32_t h[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[e] = c + e < cols ? s[e] : 0u;
+      v = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+    }
+    __builtin_memcpy(dst + r * ld_dst + c, &v, 16);
+  }
+}
+
+hipError_t launch_pad16(const uint16_t* src, int64_t ld_src, int64_t rows, int64_t cols, uint16_t* dst,
+                        int64_t ld_dst, hipStream_t st) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (ld_src < cols || ld_dst < cols || (ld_dst & 7) != 0 || ((uintptr_t)dst & 15) != 0) return hipErrorInvalidValue;
+  const int64_t gx = (ld_dst / 8 + 255) / 256;
+  if (gx > (1LL << 31) - 1) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)gx, (unsigned)(rows < 4096 ? rows : 4096)), block(256);
+  hipLaunchKernelGGL(k_pad16, grid, block, 0, st, src, ld_src, dst, ld_dst, rows, cols);
+  return hipGetLastError();
 }
 #endif
 }  // namespace ac

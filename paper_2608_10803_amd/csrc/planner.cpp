@@ -228,15 +228,18 @@ bool build_persist(const Ctx& c, int cfg, int swizzle, Plan* p, Work* w) {
 
 // Direct-to-LDS tile kernel: the tile kernel's tiling and split counts with
 // stages - 1 k-blocks of loads in flight (Eq. 13 with a deeper pipeline) and
-// no register staging. Offered where every 16-byte chunk of a row lies
-// wholly inside or outside the matrix (K and N multiples of 8); the caller's
-// pointers and leading dimensions are checked at launch, which runs the
-// register-staged sibling of the same tiling when they are not aligned.
+// no register staging. Its operands need 16-byte aligned rows whose 16-byte
+// chunks lie wholly inside or outside the matrix: a row-major A with K not a
+// multiple of 8, or a row-major B with N not a multiple of 8, is first copied
+// into a zero-padded form (the Padding module of Table 2, priced as T_pro by
+// add_prologue). The caller's pointers and leading dimensions are checked at
+// launch, which runs the register-staged sibling of the same tiling on the
+// original operands when an operand that is not copied is not aligned.
 bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w) {
   if (cfg < 0 || cfg >= N_DL_CFG) return false;
   const DlCfg& d = kDlCfg[cfg];
   const Shape& s = c.s;
-  if ((s.K % 8) != 0 || (s.N % 8) != 0 || s.K < 1) return false;
+  if (s.K < 1) return false;
   if (dl_lds_bytes(d) > c.hw.lds_bytes) return false;
   if (!build_tile(c, d.sibling, pk_req, swizzle, p, w)) return false;
   p->family = FAM_DL;
@@ -540,9 +543,13 @@ void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
     p->n_launch += 1;
   };
   if (s.layouts & AC_LAYOUT_A_COL) copy(s.M, s.K, &p->ws_a_off);
+  // the padding prologue of the direct-to-LDS kernels: a row-major operand
+  // whose rows are not whole 16-byte chunks is copied zero-padded
+  else if (p->family == FAM_DL && (s.K % 8) != 0) copy(s.M, s.K, &p->ws_a_off);
   // the small-M kernel reads a column-major B in place (its MFMA fragments
   // are runs of k), so only the other families copy B
   if ((s.layouts & AC_LAYOUT_B_COL) && p->family != FAM_SKINNY_M) copy(s.K, s.N, &p->ws_b_off);
+  else if (!(s.layouts & AC_LAYOUT_B_COL) && p->family == FAM_DL && (s.N % 8) != 0) copy(s.K, s.N, &p->ws_b_off);
   p->predicted += p->t_pro;
 }
 
@@ -1033,9 +1040,10 @@ std::string kernel_names(const Plan& p) {
     }
     r = out;
   }
-  // the layout prologue (one copy kernel per column-major operand) runs first
-  if (p.ws_b_off >= 0) r = "k_transpose16;" + r;
-  if (p.ws_a_off >= 0) r = "k_transpose16;" + r;
+  // the prologue (one copy kernel per copied operand: a transpose for a
+  // column-major operand, the padding copy otherwise) runs first
+  if (p.ws_b_off >= 0) r = std::string((p.s.layouts & AC_LAYOUT_B_COL) ? "k_transpose16;" : "k_pad16;") + r;
+  if (p.ws_a_off >= 0) r = std::string((p.s.layouts & AC_LAYOUT_A_COL) ? "k_transpose16;" : "k_pad16;") + r;
   return r;
 }
 

@@ -14,6 +14,15 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
 // main kernel of a FAM_DL plan (the split-K reduction is launched by
 // launch_plan).
 bool dl_operands_aligned(const GemmArgs& g);
+// The same test per operand (A: 16-byte aligned rows of K, K a multiple of
+// 8; B: 16-byte aligned rows, nB a multiple of 8; lda, ldb below DL_MAX_LD).
+bool dl_a_aligned(const void* A, int64_t lda, int64_t K);
+bool dl_b_aligned(const void* B, int64_t ldb, int64_t nB);
+// Padding prologue: dst (rows x ld_dst, ld_dst a multiple of 8 >= cols, dst
+// 16-byte aligned) = src (rows x cols, row pitch ld_src) with zeros in the
+// pad columns.
+hipError_t launch_pad16(const uint16_t* src, int64_t ld_src, int64_t rows, int64_t cols, uint16_t* dst,
+                        int64_t ld_dst, hipStream_t st);
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
 void query_occupancy_dl();
 // Launch of a grouped or batched plan (families FAM_GROUPED, FAM_BATCHED).

@@ -7,9 +7,11 @@ of the same tiling and split count: both multiply the same fragments in the
 same k order, so any difference is a loading, swizzle or transpose-read
 error. The shapes cover K tails (K not a multiple of the 64-deep k-block,
 down to K = 8), ragged M and N edges, partial last stage groups and split
-K. Operands that break the kernels' alignment (an odd leading dimension, a
-2-byte offset pointer) must run the sibling tile kernel instead, and the
-AddMM epilogue and fp16 inputs take the same path.
+K, and K or N not a multiple of 8, where the plan first copies A or B into
+a zero-padded form (the padding prologue). Operands that break the kernels'
+alignment (an odd leading dimension, a 2-byte offset pointer) must run the
+sibling tile kernel instead, and the AddMM epilogue, fp16 inputs and
+column-major operands (their transposed copies) take the same path.
 """
 import sys
 
@@ -17,7 +19,7 @@ import numpy as np
 import pytest
 
 import paper_2608_10803_amd as ac
-from oracle import addmm_ref, gemm_ref
+from oracle import addmm_ref, gemm_ref, layout_ref
 from workloads import gen
 
 from gpu_util import all_candidates, check, forced_plan, run, run_addmm, tol, torch
@@ -51,7 +53,9 @@ def sibling_key(key):
 
 
 SHAPES = [(300, 264, 200), (513, 640, 1000), (257, 136, 136), (1024, 1024, 1024), (96, 4096, 8192),
-          (2048, 512, 64), (300, 256, 8), (130, 392, 4104), (700, 128, 520)]
+          (2048, 512, 64), (300, 256, 8), (130, 392, 4104), (700, 128, 520),
+          # K and / or N not a multiple of 8: the padding prologue copies A / B
+          (300, 263, 517), (257, 136, 133), (130, 391, 4100), (129, 255, 5), (640, 1000, 70)]
 
 
 @pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
@@ -132,3 +136,46 @@ def test_addmm_through_dl_plans(dtype):
         assert ok, c
         err = gemm_ref.err_metric(vals, R, D)
         assert err <= tol(dtype), (c, err)
+
+
+@pytest.mark.parametrize("layouts", [ac.AC_LAYOUT_A_COL, ac.AC_LAYOUT_B_COL, ac.AC_LAYOUT_COL_COL],
+                         ids=["acol", "bcol", "colcol"])
+def test_dl_column_major_operands(layouts):
+    """Column-major A and / or B: the transposed copies are zero-padded
+    row-major operands for the direct-to-LDS kernels; every dl configuration
+    against the oracle and bit for bit against the sibling with the same
+    layouts."""
+    t = torch()
+    M, N, K = 260, 391, 517
+    a_col, b_col = bool(layouts & 1), bool(layouts & 2)
+    A, B = gen.operands(M, N, K, seed=29)
+    As = np.ascontiguousarray(A.T) if a_col else A
+    Bs = np.ascontiguousarray(B.T) if b_col else B
+    lda, ldb = (M if a_col else K), (K if b_col else N)
+    R, D = layout_ref.gemm_layout(As.reshape(-1), Bs.reshape(-1), M, N, K, lda, ldb, layouts)
+    cands = [c for c in all_candidates(M, N, K, F32, layouts) if c["family_name"] == "dl"]
+    assert cands
+    Ad = t.from_numpy(As.view(np.int16)).cuda()
+    Bd = t.from_numpy(Bs.view(np.int16)).cuda()
+    outs = []
+    for key in [c["variant_key"] for c in cands[:16]]:
+        for k in (key, sibling_key(key)):
+            plan = ac.adaptcore_plan_variant(M, N, K, F32, layouts, k)
+            C = t.full((M, N), float("nan"), dtype=t.float32, device="cuda")
+            ac.adaptcore_matmul(plan, Ad.data_ptr(), lda, Bd.data_ptr(), ldb, C.data_ptr(), N, 0)
+            t.cuda.synchronize()
+            outs.append(C.cpu().numpy().astype(np.float64))
+        assert gemm_ref.err_metric(outs[-2], R, D) <= tol(F32), hex(key)
+        assert np.array_equal(outs[-2].view(np.uint64), outs[-1].view(np.uint64)), hex(key)
+
+
+def test_padding_prologue_in_the_plan():
+    """A dl plan of a shape with K and N not multiples of 8 lists the two
+    padding copies before its kernel and reserves their workspace."""
+    M, N, K = 300, 263, 517
+    c = dl_candidates(M, N, K, BF16)[0]
+    plan = forced_plan(M, N, K, BF16, c["variant_key"])
+    names = ac.adaptcore_plan_kernels(plan)
+    assert names[:2] == ["k_pad16", "k_pad16"] and names[2].startswith("k_dl<"), names
+    d = ac.adaptcore_plan_info(plan)
+    assert d["workspace_bytes"] >= 2 * (M * 520 + K * 264)

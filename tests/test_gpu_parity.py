@@ -237,7 +237,10 @@ def test_fp16_every_configuration(shape, dtype):
     note("fp16 shape", shape, "dtype", dtype, "configurations", len(cands))
     for c in cands:
         plan = forced_plan(M, N, K, dtype, c["variant_key"])
-        assert ac.adaptcore_plan_kernels(plan)[0].startswith("f16::")
+        # the kernels of the fp16 build (the prologue copies move 16-bit
+        # patterns and are shared by both formats)
+        names = ac.adaptcore_plan_kernels(plan)
+        assert all(k.startswith("f16::") for k in names if k not in ("k_pad16", "k_transpose16")), names
         vals, ok = run(plan, A, B, M, N, K, dtype)
         check(vals, ok, A, B, dtype, ref=ref, label="%s %s" % (shape, c))
 
