@@ -187,7 +187,9 @@ typedef struct {
   double swizzle_gain;
 } adaptcore_hw_t;
 
-/* Index of a kernel configuration in adaptcore_hw_t::cfg_iter / cfg_wg, or -1. */
+/* Index of a kernel configuration in adaptcore_hw_t::cfg_iter / cfg_wg, or -1
+ * (for AC_FAMILY_DL, cfg | 0x100 names the configuration's register-load
+ * form, VariantKey bit 13, which has a slot of its own). */
 int32_t adaptcore_config_index(int32_t family, int32_t cfg);
 
 /* Optional: bind the library to the current HIP device and read its CU count.

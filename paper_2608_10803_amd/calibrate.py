@@ -15,8 +15,13 @@ are obtained by profiling. This module
     for the open search.
 
     python -m paper_2608_10803_amd.calibrate measure OUT.json   (GPU)
-    python -m paper_2608_10803_amd.calibrate fit RECORDS.json   (CPU)
+    python -m paper_2608_10803_amd.calibrate fit RECORDS.json   (after init on
+        the GPU machine, so that the planner prices with the device's occupancies)
     python -m paper_2608_10803_amd.calibrate emit FIT.json      (C++ defaults)
+
+`fit` holds half of the measured shapes out: the profile is fitted on a
+seeded half (split_shapes) and its ranking is reported on both halves, so
+the held-out figures are not in-sample.
 """
 import json
 import math
@@ -51,7 +56,33 @@ def sample_shapes(n_sweep=200, seed=11):
 
     order = sorted(range(len(sw)), key=lambda i: floor(sw[i]))
     pick = [sw[order[int(j)]] for j in np.linspace(0, len(sw) - 1, n_sweep)]
-    return pick + gen.skinny_m() + gen.small_mn_large_k() + write_bound_shapes() + split_k_shapes()
+    return (pick + gen.skinny_m() + gen.small_mn_large_k() + write_bound_shapes() + split_k_shapes() +
+            compute_bound_shapes())
+
+
+def compute_bound_shapes(n=30, seed=14):
+    """Shapes whose roofline floor is the MFMA one, drawn on their own: M, N,
+    K log-uniform in [512, 16384], kept when the arithmetic intensity with
+    bf16 output is at least 312.5 FLOP/B and M*N*K <= 2^37. They fix the
+    main-loop costs of the large tiles."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        M, N, K = (int(round(math.exp(rng.uniform(math.log(512), math.log(16384))))) for _ in range(3))
+        F = 2.0 * M * N * K
+        Bb = 2.0 * M * K + 2.0 * K * N + 2.0 * M * N
+        if F / Bb >= 312.5 and M * N * K <= 2 ** 37:
+            out.append((M, N, K))
+    return out
+
+
+def split_shapes(shape_keys, seed=15):
+    """A seeded split of the measured shapes into a fitting half and a
+    held-out half (every shape lands in exactly one)."""
+    keys = sorted(shape_keys)
+    perm = np.random.default_rng(seed).permutation(len(keys))
+    train = {keys[i] for i in perm[: len(keys) // 2]}
+    return train, set(keys) - train
 
 
 def write_bound_shapes(n=40, seed=12):
@@ -107,7 +138,7 @@ def warm_up(A, B, C, stream, seconds=2.0):
         torch.cuda.synchronize()
 
 
-def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=80, log=print):
+def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=print):
     """Time every legal configuration of each shape (GPU). Writes a JSON list
     of records {M, N, K, key, family, cfg fields, t}."""
     import torch
@@ -131,8 +162,12 @@ def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=80, log=p
     t0 = time.time()
     for si, (M, N, K) in enumerate(shapes):
         cands = ac.adaptcore_candidates(M, N, K, dtype, 0)
-        if len(cands) > max_cands:  # keep the model's best and a spread of the rest
-            idx = sorted(set(list(range(20)) + list(np.linspace(20, len(cands) - 1, max_cands - 20).astype(int))))
+        if len(cands) > max_cands:
+            # the model's best, every direct-to-LDS and persistent configuration
+            # with at most 4 splits, and a spread of the rest
+            must = [i for i, c in enumerate(cands) if c["family_name"] in ("dl", "persist") and c["pk"] <= 4]
+            rest = max(max_cands - 20 - len(must), 10)
+            idx = sorted(set(list(range(20)) + must + list(np.linspace(20, len(cands) - 1, rest).astype(int))))
             cands = [cands[i] for i in idx]
         fa, fb, fc = 2 * M * K, 2 * K * N, cb * M * N
         for c in cands:
@@ -210,8 +245,13 @@ def evaluate(recs, hw, open_search=False):
 
 
 def config_of(key):
-    """Index of the calibrated cost slot of a variant key."""
-    return ac.adaptcore_config_index(int(key) & 0xF, (int(key) >> 4) & 0xFF)
+    """Index of the calibrated cost slot of a variant key (the register-load
+    form of a direct-to-LDS configuration, key bit 13, has its own)."""
+    key = int(key)
+    cfg = (key >> 4) & 0xFF
+    if (key & 0xF) == ac.AC_FAMILY_DL and (key >> 13) & 1:
+        cfg |= 0x100
+    return ac.adaptcore_config_index(key & 0xF, cfg)
 
 
 def _log_errors(hw, meas, keys_filter=None):
@@ -290,6 +330,7 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print):
             r2 = minimize(loss_cfg, x0, method="Nelder-Mead", options={"maxiter": 300, "xatol": 1e-3, "fatol": 1e-6})
             evals += r2.nfev
             put(cur, r2.x)
+            log("  round %d configuration %d: loss %.4f" % (rnd, idx, r2.fun))
         log("fit round %d: loss %.4f" % (rnd, loss_all(cur)))
     l1 = loss_all(cur)
     log("fit: loss %.4f -> %.4f (%d evaluations)" % (l0, l1, evals))
@@ -319,12 +360,30 @@ def main(argv):
     elif len(argv) >= 2 and argv[0] == "fit":
         with open(argv[1]) as f:
             recs = json.load(f)
+        ac.adaptcore_init()  # the device's occupancies, as the planner uses them at run time
         hw0 = ac.adaptcore_get_hw()
-        before = {"class": evaluate(recs, hw0, False), "open": evaluate(recs, hw0, True)}
-        h, stats = fit(recs, hw0, log=lambda m: print(m, file=sys.stderr))
-        after = {"class": evaluate(recs, h, False), "open": evaluate(recs, h, True)}
+        train_keys, test_keys = split_shapes({(r["M"], r["N"], r["K"], r["dtype"]) for r in recs})
+        train = [r for r in recs if (r["M"], r["N"], r["K"], r["dtype"]) in train_keys]
+        test = [r for r in recs if (r["M"], r["N"], r["K"], r["dtype"]) in test_keys]
+        sk = set(split_k_shapes())
+        cb = set(compute_bound_shapes())
+        wb = set(write_bound_shapes())
+
+        def report(h):
+            out = {}
+            for name, rr in (("train", train), ("held_out", test)):
+                out[name] = {"class": evaluate(rr, h, False), "open": evaluate(rr, h, True)}
+                for tag, st in (("split_k", sk), ("compute_bound", cb), ("write_bound", wb)):
+                    sub = [r for r in rr if (r["M"], r["N"], r["K"]) in st]
+                    if sub:
+                        out[name][tag] = evaluate(sub, h, False)
+            return out
+        before = report(hw0)
+        h, stats = fit(train, hw0, log=lambda m: print(m, file=sys.stderr))
+        after = report(h)
         out = {"profile": h.as_dict(), "fit": stats, "before": before, "after": after,
-               "records": len(recs), "shapes": len(_by_shape(recs))}
+               "records": len(recs), "shapes": len(_by_shape(recs)), "train_shapes": len(train_keys),
+               "held_out_shapes": len(test_keys)}
         print(json.dumps(out, indent=1))
     elif len(argv) >= 2 and argv[0] == "emit":
         with open(argv[1]) as f:

@@ -406,7 +406,7 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   ac::Plan sib;
   const ac::Plan* run = &p;
   bool dl = p.family == ac::FAM_DL;
-  if (dl) {
+  if (dl && !p.unal) {  // (the register-load form takes any alignment)
     const bool a_ok = a_col || p.ws_a_off >= 0 || ac::dl_a_aligned(A, lda, K);
     const bool b_ok = b_col || p.ws_b_off >= 0 || ac::dl_b_aligned(B, ldb, N);
     if (!(a_ok && b_ok)) {
@@ -459,8 +459,9 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
       if (dl) g.nB = N8;
     }
     // the direct-to-LDS loop runs over whole 8-element chunks of A's rows
-    // (zeros past K in a copy); B's rows stay K
-    if (dl) g.K = K8;
+    // (zeros past K in a copy); B's rows stay K. The register-load form
+    // reads the operands as given and zero-fills past K itself.
+    if (dl && !p.unal) g.K = K8;
   }
   const hipError_t e =
       ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(*run, g, s) : ac::launch_plan(*run, g, s);

@@ -45,56 +45,6 @@ namespace f16 {
 
 // ---------------------------------------------------------------- helpers
 
-// 16-byte load from a 2-byte aligned address. gfx950 runs in unaligned
-// access mode, and the compiler emits one dwordx4 load for this copy.
-__device__ __forceinline__ u32x4 load16(const uint16_t* p) {
-  u32x4 v;
-  __builtin_memcpy(&v, p, 16);
-  return v;
-}
-
-// Drops the first s (0..8) 16-bit elements of v, shifting the rest down and
-// filling with zeros. Branch-free (selects only).
-__device__ __forceinline__ u32x4 shift_down(u32x4 v, int s) {
-  const uint64_t lo = (uint64_t)v[0] | ((uint64_t)v[1] << 32);
-  const uint64_t hi = (uint64_t)v[2] | ((uint64_t)v[3] << 32);
-  const int sb = s * 16;  // 0 .. 128
-  const int s1 = sb & 63;
-  const uint64_t lo_a = (lo >> s1) | (s1 ? (hi << (64 - s1)) : 0ull);  // sb < 64
-  const uint64_t hi_a = hi >> s1;
-  const uint64_t lo_b = hi >> s1;                                       // 64 <= sb < 128
-  const uint64_t nlo = sb < 64 ? lo_a : (sb < 128 ? lo_b : 0ull);
-  const uint64_t nhi = sb < 64 ? hi_a : 0ull;
-  return u32x4{(uint32_t)nlo, (uint32_t)(nlo >> 32), (uint32_t)nhi, (uint32_t)(nhi >> 32)};
-}
-
-// Elements e .. e+7 of a row of `len` >= 8 elements; those at index >= len
-// read as zero. The 16-byte load ends at the row end at the latest, so it
-// never leaves the row, and no lane branches (no waits inside branches).
-__device__ __forceinline__ u32x4 load_row8(const uint16_t* row, int64_t e, int64_t len) {
-  const int64_t start = min(e, len - 8);
-  const int s = (int)min<int64_t>(e - start, 8);
-  return shift_down(load16(row + start), s);
-}
-
-// The same for rows of fewer than 8 elements: eight 2-byte loads at clamped
-// indices, then selects.
-__device__ __forceinline__ u32x4 load_row8_small(const uint16_t* row, int64_t e, int64_t len) {
-  uint32_t h[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int64_t idx = e + i;
-    const uint32_t v = row[min(max(idx, (int64_t)0), len - 1)];
-    h[i] = idx < len ? v : 0u;
-  }
-  return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
-}
-
-// Elements e .. e+7 of a row of `len` >= 1 elements, zeros past the end.
-__device__ __forceinline__ u32x4 load_row(const uint16_t* row, int64_t e, int64_t len) {
-  return len >= 8 ? load_row8(row, e, len) : load_row8_small(row, e, len);
-}
-
 // Transpose an 8 x 8 block of 16-bit values: r[i] holds row i (8 columns),
 // c[j] receives column j (8 rows), row 2e in the low half of dword e.
 __device__ __forceinline__ void transpose8x8(const u32x4 (&r)[8], u32x4 (&c)[8]) {
@@ -2149,9 +2099,9 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       return kPersistFns[p.cfg](p, g, st, obf);
     case FAM_DL: {
       if (p.cfg < 0 || p.cfg >= N_DL_CFG) return hipErrorInvalidValue;
-      // the caller (adaptcore_matmul) runs the register-staged sibling when
-      // the operands are not aligned for these kernels
-      if (!ac::dl_operands_aligned(g)) return hipErrorInvalidValue;
+      // launch_dl_main checks the operands against the plan's form: aligned
+      // rows for the direct loads (the caller runs the register-staged
+      // sibling otherwise), any alignment for the register-load form
       const hipError_t e = (launch_dl_main)(p, g, st);  // this format's kernels (no argument-dependent lookup)
       if (e != hipSuccess || p.pk == 1) return e;
       return launch_reduce(g, st, obf);

@@ -68,6 +68,11 @@ struct Dl {
   static constexpr int NIB = B_BYTES / 4096;
   static constexpr int LOADS = NIA + NIB;
   static constexpr int CT_LD = WTN + 4;       // padded row of the bf16 output slab
+  // workgroups per CU the configuration is built for: two when two fit the
+  // LDS and the register file (two waves per SIMD, at most 256 registers
+  // each): one workgroup's epilogue stores then overlap the other's loads
+  // and MFMAs
+  static constexpr int WPE = (S * (BM + BN) * BK * 2 <= 80 * 1024 && BM * BN <= 256 * 128) ? 2 : 1;
   static_assert(BM % 64 == 0 && BN >= 128 && BN <= 512 && (BK == 32 || BK == 64), "tile");
   static_assert(3 * LOADS <= 63, "vmcnt range");
   // the bf16 epilogue's per-wave slab of 32 output rows goes into one stage
@@ -206,6 +211,99 @@ __device__ __forceinline__ void issue_stage(char* sA, char* sB, const DlTile<G>&
   for (int q = 0; q < G::LOADS; ++q) L.issue(t, q);
 }
 
+// ---- loads through registers (any alignment, K >= 8 and N >= 8)
+// The same chunks into the same LDS slots as the direct loads, fetched with
+// 16-byte loads at any 2-byte address: a chunk that crosses the end of a
+// row is loaded as the 16 bytes ending at the row end and shifted down in
+// registers, with zeros past K (A columns, B rows) and past N (B columns).
+// Rows past M re-read row M - 1 (their outputs are never stored).
+template <class G>
+struct DlTileU {
+  const uint16_t* a;  // A + m0 * lda
+  const uint16_t* B;
+  int64_t ldb, K, N;
+  uint32_t a_row[G::NIA];  // bytes: clamped row * lda * 2
+  int32_t a_c[G::NIA];     // k of the chunk within the block
+  int32_t b_kr[G::NIB];    // k-row of the chunk within the block
+  uint32_t b_col[G::NIB];  // bytes: first column loaded (<= N - 8)
+  int32_t b_cs[G::NIB];    // elements dropped at the N edge (0 .. 8)
+
+  __device__ __forceinline__ void init(const GemmArgs& g, int64_t m0, int64_t n0) {
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    a = g.A + m0 * g.lda;
+    B = g.B;
+    ldb = g.ldb;
+    K = g.K;
+    N = g.N;
+#pragma unroll
+    for (int q = 0; q < G::NIA; ++q) {
+      const int u = w * G::NIA + q;
+      const int row = u * G::A_RPI + lane / G::A_LPR;
+      const int c = (lane % G::A_LPR) ^ swz_a<G::BK>(row);
+      a_row[q] = (uint32_t)((min(m0 + row, g.M - 1) - m0) * g.lda * 2);
+      a_c[q] = c * 8;
+    }
+#pragma unroll
+    for (int q = 0; q < G::NIB; ++q) {
+      const int u = w * G::NIB + q;
+      const int kr = u * G::B_RPI + lane / G::B_LPR;
+      const int c = (lane % G::B_LPR) ^ swz_b(kr);
+      const int64_t gn = n0 + c * 8, st = min(gn, g.N - 8);
+      b_kr[q] = kr;
+      b_col[q] = (uint32_t)(st * 2);
+      b_cs[q] = (int32_t)min(gn - st, (int64_t)8);
+    }
+  }
+};
+
+template <class G>
+struct RegLoads {
+  u32x4 va[G::NIA], vb[G::NIB];
+  uint32_t sha, shb;  // per chunk 4 bits: elements to drop (8 = all)
+  const uint16_t* a0;  // A tile base at this block's k (elements: the chunk's start added per lane)
+  const uint16_t* b0;  // B + min(k0, K - 1) * ldb
+  int64_t k0, kb0;
+  char* sA;
+  char* sB;
+  __device__ __forceinline__ void init(char* a_stage, char* b_stage, const DlTileU<G>& t, int64_t k) {
+    k0 = k;
+    kb0 = min(k, t.K - 1);
+    b0 = t.B + kb0 * t.ldb;
+    sA = a_stage;
+    sB = b_stage;
+    sha = shb = 0;
+  }
+  // global load q into registers (0 .. NIA + NIB - 1, a compile-time index)
+  __device__ __forceinline__ void issue(const DlTileU<G>& t, int q) {
+    if (q < G::NIA) {
+      const int64_t e = k0 + t.a_c[q], st = min(e, t.K - 8);
+      const uint32_t s = (uint32_t)min(e - st, (int64_t)8);
+      va[q] = load16(reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(t.a) + t.a_row[q] + st * 2));
+      sha |= s << (4 * q);
+    } else {
+      const int qb = q - G::NIA;
+      const int64_t r = k0 + t.b_kr[qb];
+      const int64_t rr = min(r, t.K - 1) - kb0;  // >= 0
+      vb[qb] = load16(reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(b0) +
+                                                         (uint32_t)(rr * t.ldb * 2) + t.b_col[qb]));
+      const uint32_t s = r >= t.K ? 8u : (uint32_t)t.b_cs[qb];
+      shb |= s << (4 * qb);
+    }
+  }
+  // the shifted chunks into their LDS slots (after the loads landed)
+  __device__ __forceinline__ void finish() {
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int q = 0; q < G::NIA; ++q)
+      *reinterpret_cast<u32x4*>(sA + (w * G::NIA + q) * 1024 + lane * 16) = shift_down(va[q], (sha >> (4 * q)) & 15);
+#pragma unroll
+    for (int q = 0; q < G::NIB; ++q)
+      *reinterpret_cast<u32x4*>(sB + (w * G::NIB + q) * 1024 + lane * 16) = shift_down(vb[q], (shb >> (4 * q)) & 15);
+  }
+};
+
 // Fragments of one k-step (16 k) of a stage: TM A fragments (ds_read_b128
 // of a swizzled row chunk) and TN B fragments (two transpose reads each).
 template <class G>
@@ -253,9 +351,9 @@ __device__ __forceinline__ void read_frags(const char* sA, const char* sB, int k
 // steps instead of leaving in one burst (a burst fills the load queue, and
 // a wave stalled on a full queue issues no MFMAs). The scheduling barriers
 // keep the compiler to this order.
-template <class G>
+template <class G, class Loads, class Tile>
 __device__ __forceinline__ void compute_stage(const char* sA, const char* sB, f32x16 (&acc)[G::TM][G::TN],
-                                              int wr, int wc, const StageLoads<G>& nxt, const DlTile<G>& t) {
+                                              int wr, int wc, Loads& nxt, const Tile& t) {
   constexpr int KS = G::BK / 16, NMF = G::TM * G::TN;
   // next-stage loads per k-step: with two stages the loads must land
   // within this stage, so they all go out as early as possible (one per
@@ -283,11 +381,14 @@ __device__ __forceinline__ void compute_stage(const char* sA, const char* sB, f3
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+  if constexpr (std::is_same<Loads, RegLoads<G>>::value) nxt.finish();  // registers -> the next stage
 }
 
-template <int BM, int BN, int BK, int S, int OUT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_dl(GemmArgs g) {
+template <int BM, int BN, int BK, int S, int OUT, bool RG>
+__device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
   typedef Dl<BM, BN, BK, S> G;
+  typedef typename std::conditional<RG, DlTileU<G>, DlTile<G>>::type Tile;
+  typedef typename std::conditional<RG, RegLoads<G>, StageLoads<G>>::type Loads;
   __shared__ __attribute__((aligned(1024))) char lA0[G::A_BYTES];
   __shared__ __attribute__((aligned(1024))) char lA1[G::A_BYTES];
   __shared__ __attribute__((aligned(1024))) char lA2[G::A_BYTES];
@@ -316,7 +417,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wr = wave >> 1, wc = wave & 1;
 
-  DlTile<G> t;
+  Tile t;
   t.init(g, m0, n0);
 
   f32x16 acc[G::TM][G::TN];
@@ -341,18 +442,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // loads were issued after those of block kb.
   const int64_t kstop = kbeg + (int64_t)nk * G::BK;  // the partition's end, rounded up to a block
   auto kpos = [&](int b) { const int64_t k = kbeg + (int64_t)b * G::BK; return k < kstop ? k : t.K; };
+  auto prologue = [&](char* a_st, char* b_st, int64_t k) {
+    Loads L;
+    L.init(a_st, b_st, t, k);
+#pragma unroll
+    for (int q = 0; q < G::LOADS; ++q) L.issue(t, q);
+    if constexpr (RG) L.finish();
+  };
   if (nk > 0) {
-    issue_stage<G>(lA0, lB0, t, kpos(0));
-    if constexpr (S > 2) issue_stage<G>(lA1, lB1, t, kpos(1));
-    if constexpr (S > 3) issue_stage<G>(lA2, lB2, t, kpos(2));
-    if constexpr (S > 4) issue_stage<G>(lA3, lB3, t, kpos(3));
+    prologue(lA0, lB0, kpos(0));
+    if constexpr (S > 2) prologue(lA1, lB1, kpos(1));
+    if constexpr (S > 3) prologue(lA2, lB2, kpos(2));
+    if constexpr (S > 4) prologue(lA3, lB3, kpos(3));
   }
 
   auto step = [&](auto ic, int kb) {
     constexpr int I = decltype(ic)::value;
     constexpr int NX = (I + S - 1) % S;  // stage that receives block kb + S - 1
-    stage_barrier<G::LOADS>(S - 2);
-    StageLoads<G> nxt;
+    stage_barrier<G::LOADS>(RG ? 0 : S - 2);
+    Loads nxt;
     nxt.init(stA(std::integral_constant<int, NX>{}), stB(std::integral_constant<int, NX>{}), t, kpos(kb + S - 1));
     compute_stage<G>(stA(ic), stB(ic), acc, wr, wc, nxt, t);
   };
@@ -446,10 +554,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
 }
 
+// the kernels: operand tiles loaded straight into LDS (k_dl), or through
+// registers at any alignment (k_dlu)
+template <int BM, int BN, int BK, int S, int OUT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Dl<BM, BN, BK, S>::WPE, Dl<BM, BN, BK, S>::WPE)))
+void k_dl(GemmArgs g) {
+  dl_kernel<BM, BN, BK, S, OUT, false>(g);
+}
+template <int BM, int BN, int BK, int S, int OUT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Dl<BM, BN, BK, S>::WPE, Dl<BM, BN, BK, S>::WPE)))
+void k_dlu(GemmArgs g) {
+  dl_kernel<BM, BN, BK, S, OUT, true>(g);
+}
+
 template <int BM, int BN, int BK, int S>
 hipError_t launch_dl(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
   const dim3 grid(p.grid_x, p.grid_y), block(256);
-  if (p.pk > 1)
+  if (p.unal) {
+    if constexpr (dl_has_unal(BM, BN, BK, S)) {
+      if (p.pk > 1)
+        hipLaunchKernelGGL((k_dlu<BM, BN, BK, S, DL_PARTIAL>), grid, block, 0, st, g);
+      else if (obf)
+        hipLaunchKernelGGL((k_dlu<BM, BN, BK, S, DL_BF16>), grid, block, 0, st, g);
+      else
+        hipLaunchKernelGGL((k_dlu<BM, BN, BK, S, DL_F32>), grid, block, 0, st, g);
+    } else {
+      return hipErrorInvalidValue;
+    }
+  } else if (p.pk > 1)
     hipLaunchKernelGGL((k_dl<BM, BN, BK, S, DL_PARTIAL>), grid, block, 0, st, g);
   else if (obf)
     hipLaunchKernelGGL((k_dl<BM, BN, BK, S, DL_BF16>), grid, block, 0, st, g);
@@ -461,10 +593,16 @@ hipError_t launch_dl(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf)
 template <int BM, int BN, int BK, int S>
 int occ_dl() {
   int o = 1 << 20;
-  const void* ks[3] = {reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_F32>),
+  const void* ks[6] = {reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_F32>),
                        reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_BF16>),
-                       reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_PARTIAL>)};
+                       reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_PARTIAL>), nullptr, nullptr, nullptr};
+  if constexpr (dl_has_unal(BM, BN, BK, S)) {  // the register-load form shares the configuration's cost slot
+    ks[3] = reinterpret_cast<const void*>(k_dlu<BM, BN, BK, S, DL_F32>);
+    ks[4] = reinterpret_cast<const void*>(k_dlu<BM, BN, BK, S, DL_BF16>);
+    ks[5] = reinterpret_cast<const void*>(k_dlu<BM, BN, BK, S, DL_PARTIAL>);
+  }
   for (const void* k : ks) {
+    if (!k) continue;
     int a = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&a, k, 256, 0) != hipSuccess) a = 0;
     o = a < o ? a : o;
@@ -475,7 +613,8 @@ int occ_dl() {
 typedef hipError_t (*DlLaunchFn)(const Plan&, const GemmArgs&, hipStream_t, bool);
 typedef int (*DlOccFn)();
 #define DL_CFGS(X) X(256, 256, 64, 2), X(256, 128, 64, 3), X(128, 256, 64, 3), X(128, 128, 64, 3), X(256, 256, 32, 4), \
-    X(256, 256, 32, 5), X(256, 128, 32, 4), X(128, 256, 32, 4)
+    X(256, 256, 32, 5), X(256, 128, 32, 4), X(128, 256, 32, 4), X(256, 128, 32, 2), X(128, 128, 64, 2),       \
+    X(128, 128, 32, 2)
 #define DL_L(a, b, c, d) &launch_dl<a, b, c, d>
 #define DL_O(a, b, c, d) &occ_dl<a, b, c, d>
 #define DL_C(a, b, c, d) {a, b, c, d}
@@ -490,11 +629,21 @@ constexpr bool dl_match() {
   return true;
 }
 static_assert(sizeof(kDlFns) / sizeof(kDlFns[0]) == N_DL_CFG && dl_match(), "kernels must follow kDlCfg");
+#define DL_W(a, b, c, d) Dl<a, b, c, d>::WPE
+constexpr int kDlWpe[] = {DL_CFGS(DL_W)};
+constexpr bool dl_occ_match() {
+  for (int i = 0; i < N_DL_CFG; ++i)
+    if (kDlWpe[i] != kDlCfg[i].occ) return false;
+  return true;
+}
+static_assert(dl_occ_match(), "the table's workgroups per CU must be those the kernels are built for");
 
 }  // namespace
 
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st) {
-  if (p.family != FAM_DL || p.cfg < 0 || p.cfg >= N_DL_CFG || !ac::dl_operands_aligned(g)) return hipErrorInvalidValue;
+  if (p.family != FAM_DL || p.cfg < 0 || p.cfg >= N_DL_CFG) return hipErrorInvalidValue;
+  // the register-load form takes any alignment (K >= 8, N >= 8; two stages)
+  if (p.unal ? (!kDlCfg[p.cfg].unal || g.K < 8 || g.N < 8) : !ac::dl_operands_aligned(g)) return hipErrorInvalidValue;
   return kDlFns[p.cfg](p, g, st, dtype_out16(p.s.dtype));
 }
 

@@ -37,7 +37,7 @@ int table_occ(int family, int cfg) {
     case FAM_DIRECT:
       return kDirectCfg[cfg].occ;
     case FAM_DL:
-      return 1;
+      return kDlCfg[cfg].occ;
   }
   return 1;
 }
@@ -53,7 +53,19 @@ constexpr int IDX_STREAMK = IDX_SMALLK + N_SMALLK_CFG;
 constexpr int IDX_DIRECT = IDX_STREAMK + N_STREAMK_CFG;
 constexpr int IDX_PERSIST = IDX_DIRECT + N_DIRECT_CFG;
 constexpr int IDX_DL = IDX_PERSIST + N_TILE_CFG;
-static_assert(IDX_DL + N_DL_CFG <= AC_N_CFG, "calibrated cost tables");
+constexpr int IDX_DLU = IDX_DL + N_DL_CFG;  // the register-load forms, in configuration order
+constexpr int n_dl_unal() {
+  int n = 0;
+  for (const DlCfg& d : kDlCfg) n += d.unal != 0;
+  return n;
+}
+static_assert(IDX_DLU + n_dl_unal() <= AC_N_CFG, "calibrated cost tables");
+// cost slot of the register-load form of a direct-to-LDS configuration
+int dlu_index(int cfg) {
+  int n = 0;
+  for (int i = 0; i < cfg; ++i) n += kDlCfg[i].unal != 0;
+  return IDX_DLU + n;
+}
 
 // Tiles the taxonomy uses for its spatial predicate: the menu entries whose
 // accumulation tile keeps the MFMA pipeline efficient (>= 128 x 128), largest
@@ -121,7 +133,14 @@ double model_time(const Shape& s, const Work& w, const adaptcore_hw_t& hw, doubl
     const double t_setup = (w.setup > 0 ? lat + w.setup / bw_l2 : 0.0) + w.extra_lat * hw.t_mem_latency;
     const double L = std::max(0.0, w.L);
     if (L == 0) return twg + t_setup + t_drain;
-    return twg + t_setup + t_fill + (L - 1) * std::max(tM, tP) + t_drain;  // Eq. 13
+    const double t_loop = t_fill + (L - 1) * std::max(tM, tP);  // Eq. 13
+    // With r >= 2 workgroups resident on a CU their phases drift apart: one
+    // writes its output while another runs its main loop (the overlap that
+    // Eq. 14's preloading gives consecutive tiles, here between co-resident
+    // ones), so of the two phases only the longer one and a 1/r share of the
+    // shorter one remain on the critical path. r = 1 is Eq. 13's sum.
+    const double r = std::min(per_cu, (double)std::max(1, w.occ));
+    return twg + t_setup + std::max(t_loop, t_drain) + std::min(t_loop, t_drain) / r;
   };
   const int64_t full = (int64_t)(w.units / slots);
   const double rem = (double)w.units - full * slots;
@@ -235,17 +254,22 @@ bool build_persist(const Ctx& c, int cfg, int swizzle, Plan* p, Work* w) {
 // add_prologue). The caller's pointers and leading dimensions are checked at
 // launch, which runs the register-staged sibling of the same tiling on the
 // original operands when an operand that is not copied is not aligned.
-bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w) {
+bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, int unal, Plan* p, Work* w) {
   if (cfg < 0 || cfg >= N_DL_CFG) return false;
   const DlCfg& d = kDlCfg[cfg];
   const Shape& s = c.s;
   if (s.K < 1) return false;
+  // the register-load form: in place of the padding prologue, for row-major
+  // operands whose rows are not whole 16-byte chunks
+  if (unal && (!d.unal || s.layouts != AC_LAYOUT_ROW_ROW || s.K < 8 || s.N < 8 || ((s.K % 8) == 0 && (s.N % 8) == 0)))
+    return false;
   if (dl_lds_bytes(d) > c.hw.lds_bytes) return false;
   if (!build_tile(c, d.sibling, pk_req, swizzle, p, w)) return false;
   p->family = FAM_DL;
   p->cfg = cfg;
+  p->unal = unal;
   w->occ = occupancy(FAM_DL, cfg);
-  w->idx = IDX_DL + cfg;
+  w->idx = unal ? dlu_index(cfg) : IDX_DL + cfg;
   // LDS traffic per iteration (one TILE_BK of k): the stage written once by
   // the loads, A read once per column half and B once per row half (4 waves
   // in 2 x 2); the pipeline holds (stages - 1) * bk of k in flight
@@ -545,18 +569,20 @@ void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
   if (s.layouts & AC_LAYOUT_A_COL) copy(s.M, s.K, &p->ws_a_off);
   // the padding prologue of the direct-to-LDS kernels: a row-major operand
   // whose rows are not whole 16-byte chunks is copied zero-padded
-  else if (p->family == FAM_DL && (s.K % 8) != 0) copy(s.M, s.K, &p->ws_a_off);
+  else if (p->family == FAM_DL && !p->unal && (s.K % 8) != 0) copy(s.M, s.K, &p->ws_a_off);
   // the small-M kernel reads a column-major B in place (its MFMA fragments
   // are runs of k), so only the other families copy B
   if ((s.layouts & AC_LAYOUT_B_COL) && p->family != FAM_SKINNY_M) copy(s.K, s.N, &p->ws_b_off);
-  else if (!(s.layouts & AC_LAYOUT_B_COL) && p->family == FAM_DL && (s.N % 8) != 0) copy(s.K, s.N, &p->ws_b_off);
+  else if (!(s.layouts & AC_LAYOUT_B_COL) && p->family == FAM_DL && !p->unal && (s.N % 8) != 0)
+    copy(s.K, s.N, &p->ws_b_off);
   p->predicted += p->t_pro;
 }
 
 bool finish(const Ctx& c, Plan* p, const Work& w) {
   p->s = c.s;
   p->predicted = model_time(c.s, w, c.hw, c.compulsory);
-  p->variant_key = make_variant_key(p->family, p->cfg, p->swizzle, p->pk, c.s.dtype, (int)c.s.layouts);
+  p->variant_key = make_variant_key(p->family, p->cfg, p->swizzle, p->pk, c.s.dtype, (int)c.s.layouts) |
+                   ((uint64_t)(p->unal & 1) << 13);
   if (p->ws_bytes > ((int64_t)2 << 30)) return false;  // cap of the partials
   add_prologue(c.s, c.hw, p);
   return true;
@@ -628,50 +654,50 @@ adaptcore_hw_t default_hw() {
   h.search_open = 0;
   h.enable_streamk = 0;
   // Constants fitted to per-configuration timings of shapes of the
-  // dynamic-shape, decode-style and small-MN large-K workloads on one MI355X
-  // (squared log error of the model over every measured configuration),
-  // evaluated with the workgroups-per-CU that the device reports for each
-  // kernel, which is what the planner uses at run time. The
-  // launch cost is the measured per-kernel floor of back-to-back launches;
-  // the XCD-order factor is the measured geomean time ratio of the swizzled
-  // to the plain variant of a tile configuration (2,240 measured pairs).
+  // dynamic-shape, decode-style, small-MN large-K, write-bound and
+  // compute-bound workloads on one MI355X (squared log error of the model
+  // over every measured configuration of a seeded half of the 340 measured
+  // shapes; the other half is held out to check the ranking), evaluated with
+  // the workgroups-per-CU that the device reports for each kernel, which is
+  // what the planner uses at run time. The launch cost is the measured
+  // per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 1.413e-06;
+  h.t_mem_latency = 1.25e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 2.929e+10;
+  h.l2_bw_cu = 3.078e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 5.38e-33;
-  h.swizzle_gain = 0.935;
+  h.l2_hit = 5.895e-33;
+  h.swizzle_gain = 0.9239;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
-  // 20-21, stream-K 22-29, direct 30-32, persistent 33-43; 0 = analytic
-  // estimate, no timing data)
+  // 20-21, stream-K 22-29, direct 30-32, persistent 33-43, direct-to-LDS
+  // 44-54; 0 = analytic estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
-      2.914e-06, 2.083e-06, 1.999e-06, 9.358e-14, 1.874e-07, 9.358e-14, 5.407e-07, 3.958e-07,
-      1.119e-06, 9.358e-14, 9.358e-14, 1.258e-06, 1.297e-06, 1.372e-06, 1.402e-06, 1.945e-06,
-      2.035e-06, 6.562e-07, 5.774e-07, 7.79e-07, 2.24e-07, 1.964e-08, 4.516e-06, 2.397e-06,
-      3.032e-06, 9.358e-14, 8.328e-07, 9.315e-07, 5.998e-07, 4.265e-07, 2.493e-08, 9.358e-14,
-      9.358e-14, 2.932e-06, 2.063e-06, 0, 9.358e-14, 9.358e-14, 7.86e-07, 0,
-      0, 0, 0, 0, 0, 0, 0, 0,
-      0, 0, 0, 0, 0, 0, 0, 0,
+      2.921e-06, 2.093e-06, 2.085e-06, 4.781e-07, 7.899e-07, 3.627e-07, 5.406e-07, 4.085e-07,
+      1.175e-06, 9.358e-14, 9.358e-14, 1.198e-06, 1.312e-06, 1.179e-06, 1.195e-06, 2.063e-06,
+      2.134e-06, 6.25e-07, 6.25e-07, 8.576e-07, 7.298e-07, 3.675e-07, 4.322e-06, 2.457e-06,
+      2.575e-06, 1.506e-06, 1.068e-06, 1.252e-06, 3.603e-07, 4.532e-07, 3.102e-07, 9.358e-14,
+      9.358e-14, 2.803e-06, 2.071e-06, 0, 9.358e-14, 9.358e-14, 7.829e-07, 0,
+      0, 0, 0, 0, 1.951e-06, 6.346e-07, 1.225e-06, 2.385e-08,
+      1.951e-06, 1.957e-06, 7.592e-07, 6.202e-07, 1.39e-06, 9.754e-07, 1.008e-06, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      1.949e-06, 1.152e-06, 2.724e-06, 2.698e-06, 6.777e-07, 1.342e-06, 1.78e-07, 9.358e-14,
-      1.945e-06, 1.677e-06, 1.82e-06, 1.005e-06, 1.334e-06, 2.89e-06, 3.685e-06, 7.394e-06,
-      1e-05, 2.616e-07, 4.436e-08, 1.596e-06, 1.15e-06, 1.738e-06, 9.358e-14, 9.358e-14,
-      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 3.68e-06, 8.584e-06, 9.358e-14, 3.857e-07,
-      9.358e-14, 9.358e-14, 7.945e-07, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
-      0, 0, 0, 0, 0, 0, 0, 0,
-      0, 0, 0, 0, 0, 0, 0, 0,
+      3.009e-06, 1.431e-06, 2.85e-06, 2.859e-06, 1.394e-07, 9.095e-07, 6.2e-07, 9.272e-08,
+      2.07e-06, 1.691e-06, 2.215e-06, 1.996e-06, 1.67e-06, 3.744e-06, 4.034e-06, 9.374e-06,
+      1.237e-05, 4.519e-07, 2.232e-07, 1.467e-06, 1.258e-06, 8.775e-07, 9.358e-14, 9.358e-14,
+      9.358e-14, 9.358e-14, 9.358e-14, 2.2e-06, 5.333e-06, 8.943e-06, 9.358e-14, 2.373e-07,
+      9.358e-14, 1.706e-06, 2.327e-06, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
+      0, 0, 0, 0, 6.773e-06, 3.245e-06, 2.99e-06, 1.996e-06,
+      5.219e-06, 5.084e-06, 2.719e-06, 2.842e-06, 1.985e-06, 3.535e-07, 9.358e-14, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   // achieved fraction of the streaming rate for the output writes (0: 1)
   static const double kWr[AC_N_CFG] = {
-      0.8769, 1, 1, 1, 0.8662, 1, 1, 1,
-      1, 1, 1, 1, 1, 1, 1, 1,
-      1, 0.1506, 0.1648, 0.4695, 1, 1, 0.7675, 0.7711,
-      0.4256, 0.6809, 0.5186, 0.7474, 0.2449, 0.3769, 1, 0.696,
-      0.2869, 0.5725, 0.5876, 0, 0.5354, 0.5246, 0.6132, 0,
-      0, 0, 0, 0, 0, 0, 0, 0,
-      0, 0, 0, 0, 0, 0, 0, 0,
+      1, 1, 1, 0.9751, 0.5984, 0.4579, 1, 1,
+      1, 0.5015, 0.6661, 1, 1, 1, 1, 1,
+      1, 0.06294, 0.1201, 0.3006, 0.9997, 0.5074, 0.6995, 0.7196,
+      0.3366, 0.5965, 0.4149, 0.7958, 0.2185, 0.2677, 1, 0.1701,
+      0.1969, 0.558, 0.6042, 0, 0.3914, 0.334, 0.3866, 0,
+      0, 0, 0, 0, 0.9998, 0.9621, 1, 1,
+      0.7432, 0.6495, 1, 1, 0.9466, 1, 1, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   for (int i = 0; i < AC_N_CFG; ++i) {
     h.cfg_iter[i] = kIter[i];
@@ -757,25 +783,28 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
     }
   }
   // direct-to-LDS tile kernels: in the class-fixed search only once their
-  // costs are calibrated
+  // costs are calibrated (each form separately)
+  auto calibrated = [&](int idx) { return c.hw.search_open || (c.hw.cfg_iter[idx] > 0 && c.hw.cfg_wg[idx] > 0); };
   for (int cfg = 0; cfg < N_DL_CFG; ++cfg) {
-    const int idx = IDX_DL + cfg;
-    if (!c.hw.search_open && !(c.hw.cfg_iter[idx] > 0 && c.hw.cfg_wg[idx] > 0)) continue;
     const DlCfg& d = kDlCfg[cfg];
+    if (!calibrated(IDX_DL + cfg) && !(d.unal && calibrated(dlu_index(cfg)))) continue;
     if (d.bm > 2 * s.M || d.bn > 2 * s.N) continue;
     for (int sw = 0; sw < 2; ++sw) {
       const int64_t ntiles = cdiv(s.M, d.bm) * cdiv(s.N, d.bn);
       if (sw == 1 && ntiles < 16) continue;
-      {
-        Plan p;
-        Work w;
-        if (build_dl(c, cfg, 1, sw, &p, &w)) add(p, w);
-      }
-      for (int pk : kSplits) {
-        if ((int64_t)pk * ntiles > 8LL * c.hw.n_cu) break;
-        Plan p;
-        Work w;
-        if (build_dl(c, cfg, pk, sw, &p, &w)) add(p, w);
+      for (int un = 0; un < 2; ++un) {
+        if (!calibrated(un ? dlu_index(cfg) : IDX_DL + cfg)) continue;
+        {
+          Plan p;
+          Work w;
+          if (build_dl(c, cfg, 1, sw, un, &p, &w)) add(p, w);
+        }
+        for (int pk : kSplits) {
+          if ((int64_t)pk * ntiles > 8LL * c.hw.n_cu * d.occ) break;
+          Plan p;
+          Work w;
+          if (build_dl(c, cfg, pk, sw, un, &p, &w)) add(p, w);
+        }
       }
     }
   }
@@ -905,7 +934,7 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
       ok = pk == 1 && build_persist(c, cfg, sw, &p, &w);
       break;
     case FAM_DL:
-      ok = cfg < N_DL_CFG && pk >= 1 && build_dl(c, cfg, pk, sw, &p, &w);
+      ok = cfg < N_DL_CFG && pk >= 1 && build_dl(c, cfg, pk, sw, vk_unal(key), &p, &w);
       break;
   }
   if (!ok || !finish(c, &p, w)) return false;
@@ -1103,7 +1132,8 @@ static std::string kernel_names_fmt(const Plan& p) {
     }
     case FAM_DL: {
       const DlCfg& d = kDlCfg[p.cfg];
-      std::snprintf(buf, sizeof buf, "k_dl<%d, %d, %d, %d, %d>", d.bm, d.bn, d.bk, d.stages, p.pk > 1 ? 2 : obf);
+      std::snprintf(buf, sizeof buf, "%s<%d, %d, %d, %d, %d>", p.unal ? "k_dlu" : "k_dl", d.bm, d.bn, d.bk, d.stages,
+                    p.pk > 1 ? 2 : obf);
       std::string r(buf);
       if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
       return r;
@@ -1128,7 +1158,11 @@ int config_index(int family, int cfg) {
       return cfg >= 0 && cfg < N_DIRECT_CFG ? IDX_DIRECT + cfg : -1;
     case FAM_PERSIST:
       return cfg >= 0 && cfg < N_TILE_CFG && kPersistCfg[cfg] ? IDX_PERSIST + cfg : -1;
-    case FAM_DL:
+    case FAM_DL:  // cfg | 0x100: the register-load form
+      if ((cfg & 0x100) != 0) {
+        const int c = cfg & 0xFF;
+        return c < N_DL_CFG && kDlCfg[c].unal ? dlu_index(c) : -1;
+      }
       return cfg >= 0 && cfg < N_DL_CFG ? IDX_DL + cfg : -1;
     case FAM_BATCHED:
     case FAM_GROUPED:  // the tile kernel's costs

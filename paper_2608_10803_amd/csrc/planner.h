@@ -25,6 +25,7 @@ struct Plan {
   uint64_t shape_key = 0, variant_key = 0;
   int cls = AC_CLASS_COMMON;  // taxonomy template of the shape
   int family = FAM_TILE, cfg = 0, swizzle = 0;
+  int unal = 0;  // direct-to-LDS family: operand tiles loaded through registers (any alignment)
   int tile_m = 0, tile_n = 0, tile_k = 0;
   int pm = 0, pn = 0, pk = 1;
   int kper = 0;          // k-blocks per partition

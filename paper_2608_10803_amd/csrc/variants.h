@@ -80,22 +80,34 @@ inline int direct_tile(const DirectCfg& c) { return c.wk == 1 ? 64 : 32; }
 // Direct-to-LDS tile configurations (family FAM_DL): BM x BN output tile, 4
 // waves in a 2 x 2 grid, k-blocks of bk (32 or 64; splits stay in units of
 // TILE_BK), `stages` LDS stages (stages - 1 k-blocks of loads in flight);
-// one workgroup per CU. `sibling` is the register-staged tile configuration
-// of the same tiling, which runs the plan when the caller's operands are not
-// 16-byte aligned row by row.
+// `occ` workgroups per CU (two for the configurations whose LDS stages and
+// registers leave room for a second one). `sibling` is the register-staged
+// tile configuration of the same tiling, which runs the plan when the
+// caller's operands are not 16-byte aligned row by row. `unal`: the
+// configuration also has a form that loads its operand tiles through
+// registers at any alignment (K, N >= 8; VariantKey bit 13), in place of the
+// padding prologue.
 struct DlCfg {
-  int bm, bn, bk, stages, sibling;
+  int bm, bn, bk, stages, sibling, occ, unal;
 };
-constexpr DlCfg kDlCfg[] = {{256, 256, 64, 2, 0}, {256, 128, 64, 3, 1}, {128, 256, 64, 3, 2}, {128, 128, 64, 3, 3},
-                            {256, 256, 32, 4, 0}, {256, 256, 32, 5, 0}, {256, 128, 32, 4, 1}, {128, 256, 32, 4, 2}};
+constexpr DlCfg kDlCfg[] = {{256, 256, 64, 2, 0, 1, 0}, {256, 128, 64, 3, 1, 1, 0}, {128, 256, 64, 3, 2, 1, 0},
+                            {128, 128, 64, 3, 3, 1, 0}, {256, 256, 32, 4, 0, 1, 0}, {256, 256, 32, 5, 0, 1, 0},
+                            {256, 128, 32, 4, 1, 1, 0}, {128, 256, 32, 4, 2, 1, 0}, {256, 128, 32, 2, 1, 2, 1},
+                            {128, 128, 64, 2, 3, 2, 1}, {128, 128, 32, 2, 3, 2, 1}};
+constexpr bool dl_has_unal(int bm, int bn, int bk, int stages) {
+  for (const DlCfg& d : kDlCfg)
+    if (d.bm == bm && d.bn == bn && d.bk == bk && d.stages == stages) return d.unal != 0;
+  return false;
+}
 constexpr int N_DL_CFG = sizeof(kDlCfg) / sizeof(kDlCfg[0]);
 // leading dimensions of A and B the direct-to-LDS kernels address (elements)
 constexpr int64_t DL_MAX_LD = 1LL << 22;
 inline int dl_lds_bytes(const DlCfg& d) { return d.stages * (d.bm + d.bn) * d.bk * 2; }
 
 // 64-bit key of a configuration:
-//   bits  0- 3 family, 4-11 config index, 12 swizzle, 16-35 P_k (or the
-//   stream-K grid), 36-47 reserved, 48-51 dtype, 52-53 layouts.
+//   bits  0- 3 family, 4-11 config index, 12 swizzle, 13 operand loads
+//   through registers (direct-to-LDS family), 16-35 P_k (or the stream-K
+//   grid), 36-47 reserved, 48-51 dtype, 52-53 layouts.
 inline uint64_t make_variant_key(int family, int cfg, int swizzle, int pk, int dtype, int layouts) {
   return (uint64_t)(family & 0xF) | ((uint64_t)(cfg & 0xFF) << 4) | ((uint64_t)(swizzle & 1) << 12) |
          ((uint64_t)(pk & 0xFFFFF) << 16) | ((uint64_t)(dtype & 0xF) << 48) | ((uint64_t)(layouts & 0x3) << 52);
@@ -103,6 +115,7 @@ inline uint64_t make_variant_key(int family, int cfg, int swizzle, int pk, int d
 inline int vk_family(uint64_t k) { return (int)(k & 0xF); }
 inline int vk_cfg(uint64_t k) { return (int)((k >> 4) & 0xFF); }
 inline int vk_swizzle(uint64_t k) { return (int)((k >> 12) & 1); }
+inline int vk_unal(uint64_t k) { return (int)((k >> 13) & 1); }
 inline int vk_pk(uint64_t k) { return (int)((k >> 16) & 0xFFFFF); }
 inline int vk_dtype(uint64_t k) { return (int)((k >> 48) & 0xF); }
 inline int vk_layouts(uint64_t k) { return (int)((k >> 52) & 0x3); }

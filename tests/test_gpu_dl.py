@@ -28,7 +28,7 @@ pytestmark = pytest.mark.gpu
 
 F32, BF16 = ac.AC_BF16_F32OUT, ac.AC_BF16_BF16OUT
 F16F32, F16F16 = ac.AC_F16_F32OUT, ac.AC_F16_F16OUT
-DL_SIBLING = [0, 1, 2, 3, 0, 0, 1, 2]  # variants.h kDlCfg[i].sibling
+DL_SIBLING = [0, 1, 2, 3, 0, 0, 1, 2, 1, 3, 3]  # variants.h kDlCfg[i].sibling
 
 
 def note(*a):
@@ -47,9 +47,10 @@ def dl_candidates(M, N, K, dtype):
 
 
 def sibling_key(key):
-    """The tile-family key of a dl key: same tiling, split count, tile order."""
+    """The tile-family key of a dl key: same tiling, split count, tile order
+    (bit 13, the register-load form, has no tile-family counterpart)."""
     cfg = (key >> 4) & 0xFF
-    return (key & ~0xFFF) | (key & (1 << 12)) | (DL_SIBLING[cfg] << 4) | ac.AC_FAMILY_TILE
+    return (key & ~0x2FFF) | (key & (1 << 12)) | (DL_SIBLING[cfg] << 4) | ac.AC_FAMILY_TILE
 
 
 SHAPES = [(300, 264, 200), (513, 640, 1000), (257, 136, 136), (1024, 1024, 1024), (96, 4096, 8192),
@@ -169,11 +170,37 @@ def test_dl_column_major_operands(layouts):
         assert np.array_equal(outs[-2].view(np.uint64), outs[-1].view(np.uint64)), hex(key)
 
 
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32out", "bf16out"])
+@pytest.mark.parametrize("shape", [(300, 263, 517), (257, 136, 133), (130, 391, 4100), (640, 1000, 70), (70, 72, 9),
+                                   (200, 100, 8), (129, 255, 13)], ids=lambda s: "x".join(map(str, s)))
+def test_register_load_form(shape, dtype):
+    """The register-load form (k_dlu: operand rows at any alignment, no
+    padding prologue) of every configuration that has one, with the split
+    counts and tile orders: against the oracle and bit for bit against the
+    padded direct-load form of the same configuration, also with padded
+    leading dimensions and 2-byte offset pointers."""
+    M, N, K = shape
+    A, B = gen.operands(M, N, K, seed=7 * M + N + K)
+    ref = gemm_ref.gemm(A, B)
+    cands = [c for c in dl_candidates(M, N, K, dtype) if (c["variant_key"] >> 13) & 1]
+    assert cands, shape
+    for c in cands:
+        plan = forced_plan(M, N, K, dtype, c["variant_key"])
+        names = ac.adaptcore_plan_kernels(plan)
+        assert names[0].startswith("k_dlu<") and "k_pad16" not in names, names
+        padded = forced_plan(M, N, K, dtype, c["variant_key"] & ~(1 << 13))
+        for kw in [dict(), dict(lda=K + 3, ldb=N + 5, a_off=1, b_off=3)]:
+            vals, ok = run(plan, A, B, M, N, K, dtype, **kw)
+            check(vals, ok, A, B, dtype, ref=ref, label="%s %s %s" % (shape, kw, c))
+            v2, ok2 = run(padded, A, B, M, N, K, dtype, **kw)
+            assert ok2 and np.array_equal(vals.view(np.uint64), v2.view(np.uint64)), (shape, kw, c)
+
+
 def test_padding_prologue_in_the_plan():
     """A dl plan of a shape with K and N not multiples of 8 lists the two
     padding copies before its kernel and reserves their workspace."""
     M, N, K = 300, 263, 517
-    c = dl_candidates(M, N, K, BF16)[0]
+    c = [c for c in dl_candidates(M, N, K, BF16) if not (c["variant_key"] >> 13) & 1][0]  # direct loads
     plan = forced_plan(M, N, K, BF16, c["variant_key"])
     names = ac.adaptcore_plan_kernels(plan)
     assert names[:2] == ["k_pad16", "k_pad16"] and names[2].startswith("k_dl<"), names

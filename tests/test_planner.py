@@ -308,7 +308,9 @@ def test_fp16_plans():
             assert h16 != hb and d16["shape_key"] != db["shape_key"]
             assert (d16["family"], d16["tile_m"], d16["tile_n"], d16["pk"]) == (db["family"], db["tile_m"], db["tile_n"], db["pk"])
             k16, kb = ac.adaptcore_plan_kernels(h16), ac.adaptcore_plan_kernels(hb)
-            assert k16 == ["f16::" + k for k in kb], (k16, kb)
+            # the prologue copies move 16-bit patterns: shared by both formats
+            shared = ("k_pad16", "k_transpose16")
+            assert k16 == [k if k in shared else "f16::" + k for k in kb], (k16, kb)
     with pytest.raises(ac.AdaptCoreError) as e:
         ac.adaptcore_plan(4, 4, 4, 4)
     assert e.value.status == ac.AC_ERR_UNSUPPORTED
