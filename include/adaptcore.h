@@ -94,10 +94,13 @@ typedef enum {
   AC_FAMILY_PERSIST = 7,  /* persistent tile kernel: the next tile's first k-block is fetched
                              before the current tile's epilogue (K >= 8, N >= 8) */
   AC_FAMILY_BATCHED = 8,  /* the grouped kernel over a strided batch of equal shapes */
-  AC_FAMILY_DL = 9        /* tile kernel with operand tiles loaded straight into LDS through 2-3
-                             stages (Multi-Buffer); needs K, N multiples of 8 and, at run time,
-                             16-byte aligned rows of A and B (else the same tiling runs on
-                             AC_FAMILY_TILE) */
+  AC_FAMILY_DL = 9        /* tile kernel with operand tiles loaded straight into LDS through 2-5
+                             stages (Multi-Buffer), 32- to 256-row tiles. Rows of A and B that
+                             are not whole 16-byte chunks are copied zero-padded first (the
+                             Padding module), or loaded through registers (VariantKey bit 13);
+                             at run time, misaligned operands run the register-load form or the
+                             same tiling on AC_FAMILY_TILE. With P_k > 1 the partials are summed
+                             by the reduction kernel */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */

@@ -401,8 +401,10 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   g.kB = K;
   g.nB = N;
   // Direct-to-LDS plans: operands the plan does not copy must have 16-byte
-  // aligned rows of whole chunks; otherwise the register-staged sibling of
-  // the same tiling runs on the operands as given (no padding copies).
+  // aligned rows of whole chunks; otherwise the configuration's register-load
+  // form (if it has one, and the operands are row-major with K, N >= 8), else
+  // the register-staged sibling of the same tiling, runs on the operands as
+  // given (no padding copies).
   ac::Plan sib;
   const ac::Plan* run = &p;
   bool dl = p.family == ac::FAM_DL;
@@ -411,10 +413,17 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
     const bool b_ok = b_col || p.ws_b_off >= 0 || ac::dl_b_aligned(B, ldb, N);
     if (!(a_ok && b_ok)) {
       sib = p;
-      sib.family = ac::FAM_TILE;
-      sib.cfg = ac::kDlCfg[p.cfg].sibling;
+      const ac::DlCfg& d = ac::kDlCfg[p.cfg];
+      if (d.unal && !a_col && !b_col && K >= 8 && N >= 8) {
+        sib.unal = 1;
+      } else if (d.sibling >= 0) {
+        sib.family = ac::FAM_TILE;
+        sib.cfg = d.sibling;
+        dl = false;
+      } else {
+        return fail(AC_ERR_UNSUPPORTED, "operands not aligned for this configuration and no fallback applies");
+      }
       run = &sib;
-      dl = false;
     }
   }
   if (p.ws_bytes > 0) {
@@ -435,13 +444,14 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
       if (st != AC_OK) return st;
     }
     g.ws = reinterpret_cast<float*>(w.ptr);
-    // prologue: row-major copies of column-major operands (A: M x K, B: K x N)
     char* base = static_cast<char*>(w.ptr);
     // prologue: row-major copies of column-major operands, and zero-padded
-    // copies of unaligned row-major operands for direct-to-LDS plans (rows
-    // of K and N rounded up to 8)
+    // copies of unaligned row-major operands for the direct loads of a
+    // direct-to-LDS plan (rows of K and N rounded up to 8); the register-load
+    // form and the sibling read the row-major operands as given
+    const bool pads = dl && !run->unal;
     const int64_t K8 = (K + 7) / 8 * 8, N8 = (N + 7) / 8 * 8;
-    if (p.ws_a_off >= 0 && (a_col || dl)) {
+    if (p.ws_a_off >= 0 && (a_col || pads)) {
       uint16_t* a2 = reinterpret_cast<uint16_t*>(base + p.ws_a_off);
       const hipError_t e = a_col ? ac::launch_transpose16(g.A, lda, K, M, a2, K8, s)
                                  : ac::launch_pad16(g.A, lda, M, K, a2, K8, s);
@@ -449,19 +459,19 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
       g.A = a2;
       g.lda = K8;
     }
-    if (p.ws_b_off >= 0 && (b_col || dl)) {
+    if (p.ws_b_off >= 0 && (b_col || pads)) {
       uint16_t* b2 = reinterpret_cast<uint16_t*>(base + p.ws_b_off);
       const hipError_t e = b_col ? ac::launch_transpose16(g.B, ldb, N, K, b2, N8, s)
                                  : ac::launch_pad16(g.B, ldb, K, N, b2, N8, s);
       if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
       g.B = b2;
       g.ldb = N8;
-      if (dl) g.nB = N8;
+      if (pads) g.nB = N8;
     }
-    // the direct-to-LDS loop runs over whole 8-element chunks of A's rows
-    // (zeros past K in a copy); B's rows stay K. The register-load form
-    // reads the operands as given and zero-fills past K itself.
-    if (dl && !p.unal) g.K = K8;
+    // the direct loads run over whole 8-element chunks of A's rows (zeros
+    // past K in a copy); B's rows stay K. The register-load form reads the
+    // operands as given and zero-fills past K itself.
+    if (pads) g.K = K8;
   }
   const hipError_t e =
       ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(*run, g, s) : ac::launch_plan(*run, g, s);

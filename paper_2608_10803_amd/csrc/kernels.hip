@@ -2007,6 +2007,10 @@ constexpr bool tiles_match() {
 static_assert(tiles_match(), "tile kernels must follow kTileCfg");
 constexpr bool dl_siblings_match() {
   for (int i = 0; i < N_DL_CFG; ++i) {
+    if (kDlCfg[i].sibling < 0) {
+      if (!kDlCfg[i].unal) return false;  // some fallback must exist
+      continue;
+    }
     const TileCfg& t = kTileCfg[kDlCfg[i].sibling];
     if (t.bm != kDlCfg[i].bm || t.bn != kDlCfg[i].bn || t.ms != 32) return false;
   }

@@ -57,7 +57,10 @@ enum DlOut : int { DL_F32 = 0, DL_BF16 = 1, DL_PARTIAL = 2 };
 template <int BM, int BN, int BK_, int S_>
 struct Dl {
   static constexpr int BN_ = BN, BK = BK_, S = S_, NT = 256;
-  static constexpr int WTM = BM / 2, WTN = BN / 2;  // wave quadrant
+  // waves: 2 x 2 quadrants, or (tiles of at most 64 rows: the decode-style
+  // shapes) 1 x 4 along N
+  static constexpr int WM = BM >= 128 ? 2 : 1, WN = 4 / WM;
+  static constexpr int WTM = BM / WM, WTN = BN / WN;  // a wave's part of the tile
   static constexpr int TM = WTM / 32, TN = WTN / 32;
   static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BK * BN * 2;
   static constexpr int A_LPR = BK / 8;        // 16-byte chunks of an A row
@@ -73,13 +76,17 @@ struct Dl {
   // each): one workgroup's epilogue stores then overlap the other's loads
   // and MFMAs
   static constexpr int WPE = (S * (BM + BN) * BK * 2 <= 80 * 1024 && BM * BN <= 256 * 128) ? 2 : 1;
-  static_assert(BM % 64 == 0 && BN >= 128 && BN <= 512 && (BK == 32 || BK == 64), "tile");
+  static_assert(BM % 32 == 0 && BM >= 32 && BN >= 128 && BN <= 512 && (BK == 32 || BK == 64) && WTN % 32 == 0,
+                "tile");
   static_assert(3 * LOADS <= 63, "vmcnt range");
   // the bf16 epilogue's per-wave slab of 32 output rows goes into one stage
   // buffer per wave: A0, A1, B0, B1 if both kinds are large enough, else
-  // the first four of the kind that is
+  // the first four of the kind that is, else two slabs in each of B0, B1
   static constexpr int SLAB = 32 * CT_LD * 2;
-  static constexpr int SLAB_KIND = (SLAB <= A_BYTES && SLAB <= B_BYTES) ? 0 : (SLAB <= B_BYTES && S >= 4) ? 1 : 2;
+  static constexpr int SLAB_KIND = (SLAB <= A_BYTES && SLAB <= B_BYTES) ? 0
+                                   : (SLAB <= B_BYTES && S >= 4)        ? 1
+                                   : (2 * SLAB <= B_BYTES)              ? 3
+                                                                        : 2;
   static_assert(SLAB_KIND != 2 || (SLAB <= A_BYTES && S >= 4), "output slab fits a stage buffer");
 };
 
@@ -415,7 +422,7 @@ __device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
   const int nk = (int)((kend - kbeg + G::BK - 1) / G::BK);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / G::WN, wc = wave % G::WN;
 
   Tile t;
   t.init(g, m0, n0);
@@ -490,6 +497,8 @@ __device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
       slab = wave == 0 ? lA0 : wave == 1 ? lA1 : wave == 2 ? lB0 : lB1;
     else if constexpr (G::SLAB_KIND == 1)
       slab = wave == 0 ? lB0 : wave == 1 ? lB1 : wave == 2 ? lB2 : lB3;
+    else if constexpr (G::SLAB_KIND == 3)
+      slab = (wave < 2 ? lB0 : lB1) + (wave & 1) * G::SLAB;
     else
       slab = wave == 0 ? lA0 : wave == 1 ? lA1 : wave == 2 ? lA2 : lA3;
     uint16_t* ct = reinterpret_cast<uint16_t*>(slab);
@@ -596,7 +605,7 @@ int occ_dl() {
   const void* ks[6] = {reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_F32>),
                        reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_BF16>),
                        reinterpret_cast<const void*>(k_dl<BM, BN, BK, S, DL_PARTIAL>), nullptr, nullptr, nullptr};
-  if constexpr (dl_has_unal(BM, BN, BK, S)) {  // the register-load form shares the configuration's cost slot
+  if constexpr (dl_has_unal(BM, BN, BK, S)) {  // the register-load form: one occupancy for both
     ks[3] = reinterpret_cast<const void*>(k_dlu<BM, BN, BK, S, DL_F32>);
     ks[4] = reinterpret_cast<const void*>(k_dlu<BM, BN, BK, S, DL_BF16>);
     ks[5] = reinterpret_cast<const void*>(k_dlu<BM, BN, BK, S, DL_PARTIAL>);
@@ -614,7 +623,7 @@ typedef hipError_t (*DlLaunchFn)(const Plan&, const GemmArgs&, hipStream_t, bool
 typedef int (*DlOccFn)();
 #define DL_CFGS(X) X(256, 256, 64, 2), X(256, 128, 64, 3), X(128, 256, 64, 3), X(128, 128, 64, 3), X(256, 256, 32, 4), \
     X(256, 256, 32, 5), X(256, 128, 32, 4), X(128, 256, 32, 4), X(256, 128, 32, 2), X(128, 128, 64, 2),       \
-    X(128, 128, 32, 2)
+    X(128, 128, 32, 2), X(32, 256, 64, 4), X(64, 256, 64, 4), X(32, 128, 64, 4)
 #define DL_L(a, b, c, d) &launch_dl<a, b, c, d>
 #define DL_O(a, b, c, d) &occ_dl<a, b, c, d>
 #define DL_C(a, b, c, d) {a, b, c, d}

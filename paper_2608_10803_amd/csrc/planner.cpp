@@ -167,13 +167,16 @@ struct Ctx {
   bool unaligned;
 };
 
-bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w) {
-  const TileCfg& t = kTileCfg[cfg];
+// The output tiling shared by the tile kernels and the direct-to-LDS
+// kernels: bm x bn tiles, P_k partitions of whole 64-deep k-blocks, four
+// waves in wm x wn, each wave's part of the tile in ms x ms MFMA blocks.
+// Fills everything but the kernel's own identity (family, configuration,
+// occupancy, cost slot, prefetch depth).
+bool build_tiling(const Ctx& c, int bm, int bn, int wm, int wn, int ms, int pk_req, int swizzle, Plan* p, Work* w) {
   const Shape& s = c.s;
-  const int64_t tm = cdiv(s.M, t.bm), tn = cdiv(s.N, t.bn);
+  const int64_t tm = cdiv(s.M, bm), tn = cdiv(s.N, bn);
   const int64_t kt = cdiv(s.K, TILE_BK);
   if (tm * tn > (1LL << 31) - 1) return false;
-  if (tile_lds_bytes(t) > c.hw.lds_bytes) return false;
   int64_t pk = 1, kper = kt;
   if (pk_req > 1) {
     if (kt < 2) return false;
@@ -182,11 +185,9 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
     if (pk != pk_req) return false;  // an equivalent key with the effective P_k exists
     if (pk > 65535) return false;
   }
-  p->family = FAM_TILE;
-  p->cfg = cfg;
   p->swizzle = swizzle;
-  p->tile_m = t.bm;
-  p->tile_n = t.bn;
+  p->tile_m = bm;
+  p->tile_n = bn;
   p->tile_k = TILE_BK;
   p->pm = (int)tm;
   p->pn = (int)tn;
@@ -198,26 +199,35 @@ bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w
     p->n_launch = 2;
     p->ws_bytes = pk * s.M * ldw8(s.N) * 4;
   }
-  const int ks = t.ms == 32 ? 16 : 32, cyc = t.ms == 32 ? 32 : 16;
-  const int TM = t.bm / 2 / t.ms, TN = t.bn / 2 / t.ms;
+  const int ks = ms == 32 ? 16 : 32, cyc = ms == 32 ? 32 : 16;
+  const int TM = bm / wm / ms, TN = bn / wn / ms;
   const double bm_e = (double)s.M / tm, bn_e = (double)s.N / tn;
   w->units = tm * tn * pk;
-  w->occ = occupancy(FAM_TILE, cfg);
-  w->idx = IDX_TILE + cfg;
   w->L = (double)kper;
   w->bytes_it = (bm_e + bn_e) * TILE_BK * 2;
   w->mfma_it = (double)TM * TN * (TILE_BK / ks) * cyc;
-  w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (t.bm + t.bn) * TILE_BK * 2;
+  w->lds_it = 4.0 * (TM + TN) * (TILE_BK / ks) * 64 * 16 + (bm + bn) * TILE_BK * 2;
   w->out_unit = bm_e * bn_e * (pk == 1 ? c.cbytes : 4);
   w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
   if (pk > 1) {
     w->epi = (double)pk * s.M * s.N * 4;
     w->epi_out = (double)s.M * s.N * c.cbytes;
   }
-  w->prefetch = t.depth;
   w->total_read = (double)tm * tn * (bm_e + bn_e) * (double)s.K * 2;
   w->unaligned = c.unaligned;
   w->swizzle = swizzle != 0;
+  return true;
+}
+
+bool build_tile(const Ctx& c, int cfg, int pk_req, int swizzle, Plan* p, Work* w) {
+  const TileCfg& t = kTileCfg[cfg];
+  if (tile_lds_bytes(t) > c.hw.lds_bytes) return false;
+  if (!build_tiling(c, t.bm, t.bn, 2, 2, t.ms, pk_req, swizzle, p, w)) return false;
+  p->family = FAM_TILE;
+  p->cfg = cfg;
+  w->occ = occupancy(FAM_TILE, cfg);
+  w->idx = IDX_TILE + cfg;
+  w->prefetch = t.depth;
   return true;
 }
 
@@ -264,16 +274,18 @@ bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, int unal, Plan* p,
   if (unal && (!d.unal || s.layouts != AC_LAYOUT_ROW_ROW || s.K < 8 || s.N < 8 || ((s.K % 8) == 0 && (s.N % 8) == 0)))
     return false;
   if (dl_lds_bytes(d) > c.hw.lds_bytes) return false;
-  if (!build_tile(c, d.sibling, pk_req, swizzle, p, w)) return false;
+  // four waves in 2 x 2, or side by side along N for tiles of at most 64 rows
+  const int wm = d.bm >= 128 ? 2 : 1;
+  if (!build_tiling(c, d.bm, d.bn, wm, 4 / wm, 32, pk_req, swizzle, p, w)) return false;
   p->family = FAM_DL;
   p->cfg = cfg;
   p->unal = unal;
   w->occ = occupancy(FAM_DL, cfg);
   w->idx = unal ? dlu_index(cfg) : IDX_DL + cfg;
   // LDS traffic per iteration (one TILE_BK of k): the stage written once by
-  // the loads, A read once per column half and B once per row half (4 waves
-  // in 2 x 2); the pipeline holds (stages - 1) * bk of k in flight
-  w->lds_it = (double)(d.bm + d.bn) * TILE_BK * 2 * 3;
+  // the loads, A read by every wave column and B by every wave row; the
+  // pipeline holds (stages - 1) * bk of k in flight
+  w->lds_it = (double)(d.bm * (1 + 4 / wm) + d.bn * (1 + wm)) * TILE_BK * 2;
   w->prefetch = (double)(d.stages - 1) * d.bk / TILE_BK;
   w->unaligned = false;
   return true;
@@ -788,7 +800,9 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
   for (int cfg = 0; cfg < N_DL_CFG; ++cfg) {
     const DlCfg& d = kDlCfg[cfg];
     if (!calibrated(IDX_DL + cfg) && !(d.unal && calibrated(dlu_index(cfg)))) continue;
-    if (d.bm > 2 * s.M || d.bn > 2 * s.N) continue;
+    // a tile more than twice the matrix only adds padding (the 32-row decode
+    // tile is the smallest there is: any M)
+    if ((d.bm > 2 * s.M && d.bm > 32) || d.bn > 2 * s.N) continue;
     for (int sw = 0; sw < 2; ++sw) {
       const int64_t ntiles = cdiv(s.M, d.bm) * cdiv(s.N, d.bn);
       if (sw == 1 && ntiles < 16) continue;

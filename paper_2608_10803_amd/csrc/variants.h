@@ -78,28 +78,35 @@ constexpr int N_DIRECT_CFG = sizeof(kDirectCfg) / sizeof(kDirectCfg[0]);
 inline int direct_tile(const DirectCfg& c) { return c.wk == 1 ? 64 : 32; }
 
 // Direct-to-LDS tile configurations (family FAM_DL): BM x BN output tile, 4
-// waves in a 2 x 2 grid, k-blocks of bk (32 or 64; splits stay in units of
+// waves in a 2 x 2 grid (1 x 4 along N for tiles of at most 64 rows),
+// k-blocks of bk (32 or 64; splits stay in units of
 // TILE_BK), `stages` LDS stages (stages - 1 k-blocks of loads in flight);
 // `occ` workgroups per CU (two for the configurations whose LDS stages and
-// registers leave room for a second one). `sibling` is the register-staged
-// tile configuration of the same tiling, which runs the plan when the
-// caller's operands are not 16-byte aligned row by row. `unal`: the
-// configuration also has a form that loads its operand tiles through
-// registers at any alignment (K, N >= 8; VariantKey bit 13), in place of the
-// padding prologue.
+// registers leave room for a second one). `unal`: the configuration also
+// has a form that loads its operand tiles through registers at any
+// alignment (K, N >= 8; VariantKey bit 13), in place of the padding
+// prologue. When the caller's operands are not 16-byte aligned row by row,
+// a plan of the direct-load form runs its register-load form if it has one,
+// else `sibling`, the register-staged tile configuration of the same tiling
+// (-1: none).
 struct DlCfg {
   int bm, bn, bk, stages, sibling, occ, unal;
 };
 constexpr DlCfg kDlCfg[] = {{256, 256, 64, 2, 0, 1, 0}, {256, 128, 64, 3, 1, 1, 0}, {128, 256, 64, 3, 2, 1, 0},
                             {128, 128, 64, 3, 3, 1, 0}, {256, 256, 32, 4, 0, 1, 0}, {256, 256, 32, 5, 0, 1, 0},
                             {256, 128, 32, 4, 1, 1, 0}, {128, 256, 32, 4, 2, 1, 0}, {256, 128, 32, 2, 1, 2, 1},
-                            {128, 128, 64, 2, 3, 2, 1}, {128, 128, 32, 2, 3, 2, 1}};
+                            {128, 128, 64, 2, 3, 2, 1}, {128, 128, 32, 2, 3, 2, 1},
+                            // decode-style (few rows): 4 waves side by side along N, B streamed
+                            // through 3-4 stages; no tile kernel has their tiling, so their
+                            // register-load form is the fallback for unaligned operands
+                            {32, 256, 64, 4, -1, 1, 1}, {64, 256, 64, 4, -1, 1, 1}, {32, 128, 64, 4, -1, 2, 1}};
 constexpr bool dl_has_unal(int bm, int bn, int bk, int stages) {
   for (const DlCfg& d : kDlCfg)
     if (d.bm == bm && d.bn == bn && d.bk == bk && d.stages == stages) return d.unal != 0;
   return false;
 }
 constexpr int N_DL_CFG = sizeof(kDlCfg) / sizeof(kDlCfg[0]);
+
 // leading dimensions of A and B the direct-to-LDS kernels address (elements)
 constexpr int64_t DL_MAX_LD = 1LL << 22;
 inline int dl_lds_bytes(const DlCfg& d) { return d.stages * (d.bm + d.bn) * d.bk * 2; }
