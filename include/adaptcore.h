@@ -94,13 +94,17 @@ typedef enum {
   AC_FAMILY_PERSIST = 7,  /* persistent tile kernel: the next tile's first k-block is fetched
                              before the current tile's epilogue (K >= 8, N >= 8) */
   AC_FAMILY_BATCHED = 8,  /* the grouped kernel over a strided batch of equal shapes */
-  AC_FAMILY_DL = 9        /* tile kernel with operand tiles loaded straight into LDS through 2-5
+  AC_FAMILY_DL = 9,       /* tile kernel with operand tiles loaded straight into LDS through 2-5
                              stages (Multi-Buffer), 32- to 256-row tiles. Rows of A and B that
                              are not whole 16-byte chunks are copied zero-padded first (the
                              Padding module), or loaded through registers (VariantKey bit 13);
                              at run time, misaligned operands run the register-load form or the
                              same tiling on AC_FAMILY_TILE. With P_k > 1 the partials are summed
                              by the reduction kernel */
+  AC_FAMILY_TALL = 10     /* N <= 32, K a multiple of 8, A row-major: A streamed from HBM once
+                             through a direct-to-LDS pipeline of 64-k stages, B's transposed
+                             copy (a prologue) beside it; misaligned A at run time runs the same
+                             product on AC_FAMILY_SKINNY_N */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */
@@ -149,7 +153,7 @@ typedef struct {
  * the device's. The latency constants are the model's lambda / eta / BW of
  * Eq. 8, calibrated on the device. */
 /* Number of kernel configurations with calibrated costs (table size). */
-#define AC_N_CFG 64
+#define AC_N_CFG 96
 
 typedef struct {
   int32_t n_cu;          /* N_core: compute units */
@@ -191,7 +195,7 @@ typedef struct {
 } adaptcore_hw_t;
 
 /* Index of a kernel configuration in adaptcore_hw_t::cfg_iter / cfg_wg, or -1
- * (for AC_FAMILY_DL, cfg | 0x100 names the configuration's register-load
+ * (for AC_FAMILY_DL and AC_FAMILY_TALL, cfg | 0x100 names the configuration's register-load
  * form, VariantKey bit 13, which has a slot of its own). */
 int32_t adaptcore_config_index(int32_t family, int32_t cfg);
 

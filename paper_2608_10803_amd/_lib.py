@@ -12,7 +12,7 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libadaptcore.so")
 
-AC_N_CFG = 64  # calibrated cost table size (include/adaptcore.h)
+AC_N_CFG = 96  # calibrated cost table size (include/adaptcore.h)
 AC_OK = 0
 AC_ERR_INVALID_VALUE = -1
 AC_ERR_UNSUPPORTED = -2
@@ -32,10 +32,11 @@ AC_LAYOUT_B_COL = 2  # B stored column-major (ldb >= K)
 AC_LAYOUT_COL_COL = 3
 AC_A_ROWMAJOR, AC_A_COLMAJOR, AC_B_ROWMAJOR, AC_B_COLMAJOR = 0, AC_LAYOUT_A_COL, 0, AC_LAYOUT_B_COL
 (AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
- AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED, AC_FAMILY_DL) = range(10)
+ AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED, AC_FAMILY_DL, AC_FAMILY_TALL) = range(11)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
-FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped", "persist", "batched", "dl"]
+FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped", "persist", "batched", "dl",
+                "tall"]
 
 
 class AdaptCoreError(RuntimeError):

@@ -19,11 +19,13 @@ LIB = os.path.join(PKG, "libadaptcore.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["kernels.hip", "kernels_dl.hip", "planner.cpp", "adaptcore.cpp", "noalloc.hip"]
+SOURCES = ["kernels.hip", "kernels_dl.hip", "kernels_tall.hip", "planner.cpp", "adaptcore.cpp", "noalloc.hip"]
 # compilation units: (source, object name, extra flags); the kernels are
 # compiled once per input format (bf16, and fp16 in namespace ac::f16)
 UNITS = [("kernels.hip", "kernels.hip.o", []), ("kernels.hip", "kernels_f16.hip.o", ["-DAC_INPUT_F16=1"]),
          ("kernels_dl.hip", "kernels_dl.hip.o", []), ("kernels_dl.hip", "kernels_dl_f16.hip.o", ["-DAC_INPUT_F16=1"]),
+         ("kernels_tall.hip", "kernels_tall.hip.o", []),
+         ("kernels_tall.hip", "kernels_tall_f16.hip.o", ["-DAC_INPUT_F16=1"]),
          ("planner.cpp", "planner.cpp.o", []), ("adaptcore.cpp", "adaptcore.cpp.o", []),
          ("noalloc.hip", "noalloc.hip.o", [])]
 HEADERS = ["kernel_args.h", "variants.h", "planner.h", "registry.h", "noalloc.h", "device_common.h"]

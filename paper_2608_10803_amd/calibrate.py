@@ -163,9 +163,9 @@ def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=
     for si, (M, N, K) in enumerate(shapes):
         cands = ac.adaptcore_candidates(M, N, K, dtype, 0)
         if len(cands) > max_cands:
-            # the model's best, every direct-to-LDS and persistent configuration
+            # the model's best, every direct-to-LDS, persistent and tall configuration
             # with at most 4 splits, and a spread of the rest
-            must = [i for i, c in enumerate(cands) if c["family_name"] in ("dl", "persist") and c["pk"] <= 4]
+            must = [i for i, c in enumerate(cands) if c["family_name"] in ("dl", "persist", "tall") and c["pk"] <= 4]
             rest = max(max_cands - 20 - len(must), 10)
             idx = sorted(set(list(range(20)) + must + list(np.linspace(20, len(cands) - 1, rest).astype(int))))
             cands = [cands[i] for i in idx]
@@ -246,10 +246,11 @@ def evaluate(recs, hw, open_search=False):
 
 def config_of(key):
     """Index of the calibrated cost slot of a variant key (the register-load
-    form of a direct-to-LDS configuration, key bit 13, has its own)."""
+    form of a direct-to-LDS or tall-skinny configuration, key bit 13, has
+    its own)."""
     key = int(key)
     cfg = (key >> 4) & 0xFF
-    if (key & 0xF) == ac.AC_FAMILY_DL and (key >> 13) & 1:
+    if (key & 0xF) in (ac.AC_FAMILY_DL, ac.AC_FAMILY_TALL) and (key >> 13) & 1:
         cfg |= 0x100
     return ac.adaptcore_config_index(key & 0xF, cfg)
 

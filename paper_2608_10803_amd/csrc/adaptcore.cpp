@@ -389,15 +389,6 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   g.alpha = alpha;
   g.beta = beta;
   g.bias = bias;
-  g.pk = p.family == ac::FAM_STREAMK ? 1 : p.pk;
-  g.kper = p.kper;
-  g.tiles_m = p.pm;
-  g.tiles_n = p.pn;
-  g.swizzle = p.swizzle;
-  g.iters_per_wg = p.iters_per_wg;
-  g.sk_tiles = p.sk_tiles;
-  g.ws_pk = p.ws_pk;
-  g.grid = p.grid_x;
   g.kB = K;
   g.nB = N;
   // Direct-to-LDS plans: operands the plan does not copy must have 16-byte
@@ -426,11 +417,45 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
       run = &sib;
     }
   }
-  if (p.ws_bytes > 0) {
+  // Tall-skinny plans of the direct-load form need A with 16-byte aligned
+  // rows; otherwise the configuration's register-load form runs if it has
+  // one, else the skinny-N kernel (any alignment) with the same split count
+  // if it has one, else unsplit.
+  if (p.family == ac::FAM_TALL && !p.unal && !ac::tall_a_aligned(A, lda, K) && ac::kTallCfg[p.cfg].unal) {
+    sib = p;
+    sib.unal = 1;
+    run = &sib;
+  } else if (p.family == ac::FAM_TALL && !p.unal && !ac::tall_a_aligned(A, lda, K)) {
+    adaptcore_hw_t hw;
+    {
+      std::lock_guard<std::mutex> lk(g_mu);
+      hw = g_hw;
+    }
+    const int cfg = ac::kTallCfg[p.cfg].nt - 1;  // skinny-N configuration of the same column count
+    bool ok = false;
+    for (int pk : {p.pk, 1}) {
+      const uint64_t key = ac::make_variant_key(ac::FAM_SKINNY_N, cfg, 0, pk, p.s.dtype, (int)p.s.layouts);
+      if ((ok = ac::plan_for_key(p.s, hw, key, &sib))) break;
+    }
+    if (!ok) return fail(AC_ERR_UNSUPPORTED, "A not aligned for this plan and no fallback applies");
+    run = &sib;
+  }
+  // the launch fields, workspace and prologue of the plan that runs
+  const ac::Plan& q = *run;
+  g.pk = q.family == ac::FAM_STREAMK ? 1 : q.pk;
+  g.kper = q.kper;
+  g.tiles_m = q.pm;
+  g.tiles_n = q.pn;
+  g.swizzle = q.swizzle;
+  g.iters_per_wg = q.iters_per_wg;
+  g.sk_tiles = q.sk_tiles;
+  g.ws_pk = q.ws_pk;
+  g.grid = q.grid_x;
+  if (q.ws_bytes > 0) {
     Workspace w;
     if (fixed) {
-      if (p.ws_bytes > ac::NOALLOC_SCRATCH_BYTES)
-        return fail(AC_ERR_UNSUPPORTED, "the plan's workspace (" + std::to_string(p.ws_bytes) +
+      if (q.ws_bytes > ac::NOALLOC_SCRATCH_BYTES)
+        return fail(AC_ERR_UNSUPPORTED, "the plan's workspace (" + std::to_string(q.ws_bytes) +
                                             " bytes) exceeds the no-allocation scratch of " +
                                             std::to_string(ac::NOALLOC_SCRATCH_BYTES) + " bytes");
       int dev = 0;
@@ -440,7 +465,7 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
       w.ptr = static_cast<char*>(ptr);
       w.bytes = ac::NOALLOC_SCRATCH_BYTES;
     } else {
-      st = get_workspace(s, p.ws_bytes, &w);
+      st = get_workspace(s, q.ws_bytes, &w);
       if (st != AC_OK) return st;
     }
     g.ws = reinterpret_cast<float*>(w.ptr);
@@ -448,19 +473,29 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
     // prologue: row-major copies of column-major operands, and zero-padded
     // copies of unaligned row-major operands for the direct loads of a
     // direct-to-LDS plan (rows of K and N rounded up to 8); the register-load
-    // form and the sibling read the row-major operands as given
+    // form and the sibling read the row-major operands as given. A
+    // tall-skinny plan reads B's transposed copy (N x K8).
     const bool pads = dl && !run->unal;
+    const bool tall = q.family == ac::FAM_TALL;
     const int64_t K8 = (K + 7) / 8 * 8, N8 = (N + 7) / 8 * 8;
-    if (p.ws_a_off >= 0 && (a_col || pads)) {
-      uint16_t* a2 = reinterpret_cast<uint16_t*>(base + p.ws_a_off);
+    if (tall && q.ws_b_off >= 0) {
+      uint16_t* bt = reinterpret_cast<uint16_t*>(base + q.ws_b_off);
+      const hipError_t e = b_col ? ac::launch_pad16(g.B, ldb, N, K, bt, K8, s)
+                                 : ac::launch_transpose16(g.B, ldb, K, N, bt, K8, s);
+      if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+      g.B = bt;
+      g.ldb = K8;
+    }
+    if (q.ws_a_off >= 0 && (a_col || pads)) {
+      uint16_t* a2 = reinterpret_cast<uint16_t*>(base + q.ws_a_off);
       const hipError_t e = a_col ? ac::launch_transpose16(g.A, lda, K, M, a2, K8, s)
                                  : ac::launch_pad16(g.A, lda, M, K, a2, K8, s);
       if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
       g.A = a2;
       g.lda = K8;
     }
-    if (p.ws_b_off >= 0 && (b_col || pads)) {
-      uint16_t* b2 = reinterpret_cast<uint16_t*>(base + p.ws_b_off);
+    if (!tall && q.ws_b_off >= 0 && (b_col || pads)) {
+      uint16_t* b2 = reinterpret_cast<uint16_t*>(base + q.ws_b_off);
       const hipError_t e = b_col ? ac::launch_transpose16(g.B, ldb, N, K, b2, N8, s)
                                  : ac::launch_pad16(g.B, ldb, K, N, b2, N8, s);
       if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
@@ -476,7 +511,7 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   const hipError_t e =
       ac::dtype_f16_input(p.s.dtype) ? ac::f16::launch_plan(*run, g, s) : ac::launch_plan(*run, g, s);
   if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
-  st_launches.fetch_add((uint64_t)p.n_launch, std::memory_order_relaxed);
+  st_launches.fetch_add((uint64_t)q.n_launch, std::memory_order_relaxed);
   return AC_OK;
 }
 

@@ -150,3 +150,22 @@ __device__ __forceinline__ void tile_coords(int t, int tiles_m, int tiles_n, int
 // zero and drops stores.
 constexpr int32_t OOB_OFF = (int32_t)0x80000000u;  // past every tile's range
 constexpr uint32_t RSRC_WORD3 = 0x00020000u;      // raw buffer, 32-bit data
+
+// ---- LDS pipelines fed by direct-to-LDS loads (buffer_load ... lds)
+typedef __attribute__((address_space(3))) void lds_void;
+
+// A stage: chunk c (8 k) of row r sits at slot c ^ swz_a(r) of the row's
+// slots (8 for 64-deep, 4 for 32-deep blocks): the lanes that read 8 or 16
+// consecutive rows at one chunk fall on distinct banks, for 32 as for 64
+// banks.
+template <int BK>
+__device__ __forceinline__ int swz_a(int r) {
+  if constexpr (BK == 64)
+    return (r & 7) ^ ((r >> 3) & 1);
+  else
+    return ((r >> 1) & 3) ^ ((r >> 3) & 1);
+}
+
+// s_waitcnt immediate for vmcnt(n) alone (expcnt 7 and lgkmcnt 15 do not
+// wait; vmcnt bits 3:0 and 15:14)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }

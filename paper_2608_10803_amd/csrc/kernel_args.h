@@ -23,7 +23,8 @@ enum Family : int {
   FAM_PERSIST = 7,   // persistent tile kernel, next tile's first block fetched before the epilogue
   FAM_BATCHED = 8,   // the grouped kernel over a strided batch (every group the same shape)
   FAM_DL = 9,        // tile kernel with operand tiles loaded straight into LDS (multi-stage)
-  FAM_COUNT = 10
+  FAM_TALL = 10,     // N <= 32: A streamed once through a direct-to-LDS pipeline, B^T beside it
+  FAM_COUNT = 11
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N

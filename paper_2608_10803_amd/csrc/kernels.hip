@@ -2110,6 +2110,12 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       if (e != hipSuccess || p.pk == 1) return e;
       return launch_reduce(g, st, obf);
     }
+    case FAM_TALL: {
+      // g.B / g.ldb: the transposed copy of B the caller's prologue wrote
+      const hipError_t e = (launch_tall_main)(p, g, st);
+      if (e != hipSuccess || p.pk == 1) return e;
+      return launch_reduce(g, st, obf);
+    }
   }
   return hipErrorInvalidValue;
 }
@@ -2146,6 +2152,7 @@ void query_occupancy() {
   for (int i = 0; i < N_TILE_CFG; ++i)
     if (kPersistOcc[i]) set_runtime_occupancy(FAM_PERSIST, i, kPersistOcc[i]());
   query_occupancy_dl();
+  query_occupancy_tall();
 }
 
 #if AC_INPUT_F16

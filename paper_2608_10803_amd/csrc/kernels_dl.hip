@@ -47,7 +47,6 @@ namespace f16 {
 
 namespace {
 
-typedef __attribute__((address_space(3))) void lds_void;
 // the transpose read moves 16-bit patterns; its bf16 form serves fp16 too
 typedef __bf16 tr16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) tr16x4 lds_tr16x4;
@@ -90,26 +89,11 @@ struct Dl {
   static_assert(SLAB_KIND != 2 || (SLAB <= A_BYTES && S >= 4), "output slab fits a stage buffer");
 };
 
-// A stage: chunk c (8 k) of row r sits at slot c ^ swz_a(r) of the row's
-// slots (8 for 64-deep, 4 for 32-deep blocks): the lanes that read 8 or 16
-// consecutive rows at one chunk fall on distinct banks, for 32 as for 64
-// banks.
-template <int BK>
-__device__ __forceinline__ int swz_a(int r) {
-  if constexpr (BK == 64)
-    return (r & 7) ^ ((r >> 3) & 1);
-  else
-    return ((r >> 1) & 3) ^ ((r >> 3) & 1);
-}
 // B stage: chunk c of k-row r sits at slot c ^ f(r & 3), f = 0, 6, 12, 10.
 // One transpose read covers 4 consecutive k-rows and 2 (16 lanes) or 4 (32
 // lanes) consecutive chunks; f keeps those on distinct banks for both 32
 // and 64 banks.
 __device__ __forceinline__ int swz_b(int r) { return (0xAC60 >> (4 * (r & 3))) & 15; }
-
-// s_waitcnt immediate for vmcnt(n) alone (expcnt 7 and lgkmcnt 15 do not
-// wait; vmcnt bits 3:0 and 15:14)
-constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 // Workgroup barrier of the pipeline: this wave waits until at most `ahead`
 // (0 .. 3) later stages of its own loads are in flight and its LDS reads

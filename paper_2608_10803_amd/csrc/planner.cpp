@@ -38,6 +38,8 @@ int table_occ(int family, int cfg) {
       return kDirectCfg[cfg].occ;
     case FAM_DL:
       return kDlCfg[cfg].occ;
+    case FAM_TALL:
+      return kTallCfg[cfg].occ;
   }
   return 1;
 }
@@ -59,7 +61,19 @@ constexpr int n_dl_unal() {
   for (const DlCfg& d : kDlCfg) n += d.unal != 0;
   return n;
 }
-static_assert(IDX_DLU + n_dl_unal() <= AC_N_CFG, "calibrated cost tables");
+constexpr int IDX_TALL = IDX_DLU + n_dl_unal();
+constexpr int IDX_TALLU = IDX_TALL + N_TALL_CFG;  // the tall kernels' register-load forms
+constexpr int n_tall_unal() {
+  int n = 0;
+  for (const TallCfg& t : kTallCfg) n += t.unal != 0;
+  return n;
+}
+static_assert(IDX_TALLU + n_tall_unal() <= AC_N_CFG, "calibrated cost tables");
+int tallu_index(int cfg) {
+  int n = 0;
+  for (int i = 0; i < cfg; ++i) n += kTallCfg[i].unal != 0;
+  return IDX_TALLU + n;
+}
 // cost slot of the register-load form of a direct-to-LDS configuration
 int dlu_index(int cfg) {
   int n = 0;
@@ -287,6 +301,65 @@ bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, int unal, Plan* p,
   // pipeline holds (stages - 1) * bk of k in flight
   w->lds_it = (double)(d.bm * (1 + 4 / wm) + d.bn * (1 + wm)) * TILE_BK * 2;
   w->prefetch = (double)(d.stages - 1) * d.bk / TILE_BK;
+  w->unaligned = false;
+  return true;
+}
+
+// Tall-skinny streaming kernel: A (row-major, K a multiple of 8) read once
+// through the kernel's LDS pipeline, B through its transposed copy (the
+// prologue add_prologue prices); ceil(M / bm) x P_k workgroups, each a run
+// of 64-deep k-blocks.
+bool build_tall(const Ctx& c, int cfg, int pk_req, int unal, Plan* p, Work* w) {
+  if (cfg < 0 || cfg >= N_TALL_CFG) return false;
+  const TallCfg& t = kTallCfg[cfg];
+  const Shape& s = c.s;
+  if (s.N > 16 * t.nt || (t.nt > 1 && s.N <= 16 * (t.nt / 2))) return false;  // the narrowest that fits
+  if ((s.layouts & AC_LAYOUT_A_COL) || s.K < 8) return false;
+  // direct loads need rows of whole 16-byte chunks; the register-load form
+  // serves the other K
+  if (unal ? (!t.unal || (s.K % 8) == 0) : (s.K % 8) != 0) return false;
+  if (tall_lds_bytes(t) > c.hw.lds_bytes) return false;
+  const int64_t rbk = cdiv(s.M, t.bm), kb = cdiv(s.K, TILE_BK);
+  int64_t pk = 1, kper = kb;
+  if (pk_req > 1) {
+    if (kb < 2) return false;
+    kper = cdiv(kb, pk_req);
+    pk = cdiv(kb, kper);
+    if (pk != pk_req || pk > 65535) return false;
+  }
+  if (rbk > (1LL << 31) - 1) return false;
+  p->family = FAM_TALL;
+  p->cfg = cfg;
+  p->unal = unal;
+  p->tile_m = t.bm;
+  p->tile_n = 16 * t.nt;
+  p->tile_k = TILE_BK;
+  p->pm = (int)rbk;
+  p->pn = 1;
+  p->pk = (int)pk;
+  p->kper = (int)kper;
+  p->grid_x = (int)rbk;
+  p->grid_y = (int)pk;
+  if (pk > 1) {
+    p->n_launch = 2;
+    p->ws_bytes = pk * s.M * ldw8(s.N) * 4;
+  }
+  const double rows_e = (double)s.M / rbk;
+  w->units = rbk * pk;
+  w->occ = occupancy(FAM_TALL, cfg);
+  w->idx = unal ? tallu_index(cfg) : IDX_TALL + cfg;
+  w->L = (double)kper;
+  w->bytes_it = (rows_e + s.N) * TILE_BK * 2;
+  w->mfma_it = (double)(t.bm / 64) * t.nt * 2 * 16;  // two 32-k halves of 16x16x32 MFMAs per wave
+  w->lds_it = (double)(t.bm + 16 * t.nt) * TILE_BK * 2 * 2;  // written by the loads, read once
+  w->out_unit = rows_e * s.N * (pk == 1 ? c.cbytes : 4);
+  w->total_write = (double)s.M * s.N * (pk == 1 ? c.cbytes : 4.0 * pk);
+  if (pk > 1) {
+    w->epi = (double)pk * s.M * s.N * 4;
+    w->epi_out = (double)s.M * s.N * c.cbytes;
+  }
+  w->prefetch = t.stages - 1;
+  w->total_read = 2.0 * s.M * s.K + 2.0 * s.K * s.N * rbk;  // B^T read by every row block (from cache)
   w->unaligned = false;
   return true;
 }
@@ -583,8 +656,10 @@ void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
   // whose rows are not whole 16-byte chunks is copied zero-padded
   else if (p->family == FAM_DL && !p->unal && (s.K % 8) != 0) copy(s.M, s.K, &p->ws_a_off);
   // the small-M kernel reads a column-major B in place (its MFMA fragments
-  // are runs of k), so only the other families copy B
-  if ((s.layouts & AC_LAYOUT_B_COL) && p->family != FAM_SKINNY_M) copy(s.K, s.N, &p->ws_b_off);
+  // are runs of k), so only the other families copy B; the tall-skinny
+  // kernel reads B's transposed copy (N x K, rows padded to 8) in any case
+  if (p->family == FAM_TALL) copy(s.N, s.K, &p->ws_b_off);
+  else if ((s.layouts & AC_LAYOUT_B_COL) && p->family != FAM_SKINNY_M) copy(s.K, s.N, &p->ws_b_off);
   else if (!(s.layouts & AC_LAYOUT_B_COL) && p->family == FAM_DL && !p->unal && (s.N % 8) != 0)
     copy(s.K, s.N, &p->ws_b_off);
   p->predicted += p->t_pro;
@@ -822,6 +897,24 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
       }
     }
   }
+  // tall-skinny streaming kernels: in the class-fixed search once calibrated
+  for (int cfg = 0; cfg < N_TALL_CFG; ++cfg) {
+    const int un = (s.K % 8) != 0;  // the form this K takes
+    if (un && !kTallCfg[cfg].unal) continue;
+    if (!calibrated(un ? tallu_index(cfg) : IDX_TALL + cfg)) continue;
+    const int64_t rbk = cdiv(s.M, kTallCfg[cfg].bm);
+    {
+      Plan p;
+      Work w;
+      if (build_tall(c, cfg, 1, un, &p, &w)) add(p, w);
+    }
+    for (int pk : kSplits) {
+      if ((int64_t)pk * rbk > 8LL * c.hw.n_cu * kTallCfg[cfg].occ) break;
+      Plan p;
+      Work w;
+      if (build_tall(c, cfg, pk, un, &p, &w)) add(p, w);
+    }
+  }
   for (int cfg = 0; cfg < N_SKINNY_M_CFG; ++cfg) {
     const int64_t cb = cdiv(s.N, skinny_m_cols(kSkinnyMCfg[cfg]));
     {
@@ -949,6 +1042,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
       break;
     case FAM_DL:
       ok = cfg < N_DL_CFG && pk >= 1 && build_dl(c, cfg, pk, sw, vk_unal(key), &p, &w);
+      break;
+    case FAM_TALL:
+      ok = sw == 0 && pk >= 1 && build_tall(c, cfg, pk, vk_unal(key), &p, &w);
       break;
   }
   if (!ok || !finish(c, &p, w)) return false;
@@ -1085,7 +1181,9 @@ std::string kernel_names(const Plan& p) {
   }
   // the prologue (one copy kernel per copied operand: a transpose for a
   // column-major operand, the padding copy otherwise) runs first
-  if (p.ws_b_off >= 0) r = std::string((p.s.layouts & AC_LAYOUT_B_COL) ? "k_transpose16;" : "k_pad16;") + r;
+  // (the tall-skinny kernel's copy of B is B^T: a transpose of a row-major B)
+  const bool b_tr = ((p.s.layouts & AC_LAYOUT_B_COL) != 0) != (p.family == FAM_TALL);
+  if (p.ws_b_off >= 0) r = std::string(b_tr ? "k_transpose16;" : "k_pad16;") + r;
   if (p.ws_a_off >= 0) r = std::string((p.s.layouts & AC_LAYOUT_A_COL) ? "k_transpose16;" : "k_pad16;") + r;
   return r;
 }
@@ -1152,6 +1250,14 @@ static std::string kernel_names_fmt(const Plan& p) {
       if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
       return r;
     }
+    case FAM_TALL: {
+      const TallCfg& t = kTallCfg[p.cfg];
+      std::snprintf(buf, sizeof buf, "%s<%d, %d, %d, %d>", p.unal ? "k_tallu" : "k_tall", t.nt, t.bm, t.stages,
+                    p.pk > 1 ? 2 : obf);
+      std::string r(buf);
+      if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
+      return r;
+    }
   }
   return "";
 }
@@ -1178,6 +1284,12 @@ int config_index(int family, int cfg) {
         return c < N_DL_CFG && kDlCfg[c].unal ? dlu_index(c) : -1;
       }
       return cfg >= 0 && cfg < N_DL_CFG ? IDX_DL + cfg : -1;
+    case FAM_TALL:  // cfg | 0x100: the register-load form
+      if ((cfg & 0x100) != 0) {
+        const int c = cfg & 0xFF;
+        return c < N_TALL_CFG && kTallCfg[c].unal ? tallu_index(c) : -1;
+      }
+      return cfg >= 0 && cfg < N_TALL_CFG ? IDX_TALL + cfg : -1;
     case FAM_BATCHED:
     case FAM_GROUPED:  // the tile kernel's costs
       return cfg >= 0 && cfg < N_TILE_CFG && kGroupedCfg[cfg] ? IDX_TILE + cfg : -1;

@@ -25,6 +25,15 @@ hipError_t launch_pad16(const uint16_t* src, int64_t ld_src, int64_t rows, int64
                         int64_t ld_dst, hipStream_t st);
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
 void query_occupancy_dl();
+// Tall-skinny streaming kernel (kernels_tall.hip): A's alignment (16-byte
+// aligned rows of K, K a multiple of 8, lda below DL_MAX_LD), the operands'
+// (A and the transposed copy of B in g.B / g.ldb), and the main kernel of a
+// FAM_TALL plan (the B^T prologue and the split-K reduction are launched by
+// the caller and launch_plan).
+bool tall_a_aligned(const void* A, int64_t lda, int64_t K);
+bool tall_operands_aligned(const GemmArgs& g);
+hipError_t launch_tall_main(const Plan& p, const GemmArgs& g, hipStream_t st);
+void query_occupancy_tall();
 // Launch of a grouped or batched plan (families FAM_GROUPED, FAM_BATCHED).
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 // Reads the device's occupancy of every kernel into the planner.
@@ -39,6 +48,8 @@ namespace f16 {
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
 void query_occupancy_dl();
+hipError_t launch_tall_main(const Plan& p, const GemmArgs& g, hipStream_t st);
+void query_occupancy_tall();
 hipError_t launch_grouped_plan(const Plan& p, const GroupArgs& a, hipStream_t st);
 void query_occupancy();
 }  // namespace f16

@@ -109,6 +109,20 @@ constexpr int N_DL_CFG = sizeof(kDlCfg) / sizeof(kDlCfg[0]);
 
 // leading dimensions of A and B the direct-to-LDS kernels address (elements)
 constexpr int64_t DL_MAX_LD = 1LL << 22;
+
+// Tall-skinny streaming configurations (N <= 16 nt): a workgroup owns bm
+// rows of A and one K partition and streams them through `stages` LDS
+// stages of 64 k (A: bm x 64, B^T: 16 nt x 64) with direct-to-LDS loads;
+// occ workgroups per CU (what the LDS holds). unal: the configuration also
+// has a register-load form (A rows at any alignment, K not a multiple of
+// 8): `stages` blocks of loads in flight in registers, two LDS stages.
+struct TallCfg {
+  int nt, bm, stages, occ, unal;
+};
+constexpr TallCfg kTallCfg[] = {{1, 128, 4, 2, 1}, {1, 128, 6, 1, 1}, {1, 256, 4, 1, 0},
+                                {1, 64, 6, 2, 1},  {2, 128, 4, 2, 1}, {2, 256, 4, 1, 0}};
+constexpr int N_TALL_CFG = sizeof(kTallCfg) / sizeof(kTallCfg[0]);
+inline int tall_lds_bytes(const TallCfg& t) { return t.stages * (t.bm + 16 * t.nt) * 128; }
 inline int dl_lds_bytes(const DlCfg& d) { return d.stages * (d.bm + d.bn) * d.bk * 2; }
 
 // 64-bit key of a configuration:
