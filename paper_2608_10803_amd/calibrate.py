@@ -57,7 +57,7 @@ def sample_shapes(n_sweep=200, seed=11):
     order = sorted(range(len(sw)), key=lambda i: floor(sw[i]))
     pick = [sw[order[int(j)]] for j in np.linspace(0, len(sw) - 1, n_sweep)]
     return (pick + gen.skinny_m() + gen.small_mn_large_k() + write_bound_shapes() + split_k_shapes() +
-            compute_bound_shapes())
+            compute_bound_shapes() + tall_shapes())
 
 
 def compute_bound_shapes(n=30, seed=14):
@@ -72,6 +72,22 @@ def compute_bound_shapes(n=30, seed=14):
         F = 2.0 * M * N * K
         Bb = 2.0 * M * K + 2.0 * K * N + 2.0 * M * N
         if F / Bb >= 312.5 and M * N * K <= 2 ** 37:
+            out.append((M, N, K))
+    return out
+
+
+def tall_shapes(n=30, seed=16):
+    """Tall-skinny shapes (A the one large operand), drawn on their own: M
+    log-uniform in [1000, 100000], N uniform in 1..32, K log-uniform in
+    [64, 100000] (any parity, so both load forms of the tall kernels occur),
+    kept when A is at most 4 GiB. They fix the streaming kernels' costs."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        M = int(round(math.exp(rng.uniform(math.log(1000), math.log(100000)))))
+        N = int(rng.integers(1, 33))
+        K = int(round(math.exp(rng.uniform(math.log(64), math.log(100000)))))
+        if 2.0 * M * K <= 4 * 2 ** 30:
             out.append((M, N, K))
     return out
 
@@ -369,12 +385,16 @@ def main(argv):
         sk = set(split_k_shapes())
         cb = set(compute_bound_shapes())
         wb = set(write_bound_shapes())
+        ta = set(tall_shapes())
+        from workloads import gen
+        dec = {tuple(s) for s in gen.skinny_m()}
 
         def report(h):
             out = {}
             for name, rr in (("train", train), ("held_out", test)):
                 out[name] = {"class": evaluate(rr, h, False), "open": evaluate(rr, h, True)}
-                for tag, st in (("split_k", sk), ("compute_bound", cb), ("write_bound", wb)):
+                for tag, st in (("split_k", sk), ("compute_bound", cb), ("write_bound", wb), ("tall", ta),
+                                ("decode", dec)):
                     sub = [r for r in rr if (r["M"], r["N"], r["K"]) in st]
                     if sub:
                         out[name][tag] = evaluate(sub, h, False)

@@ -670,8 +670,8 @@ bool finish(const Ctx& c, Plan* p, const Work& w) {
   p->predicted = model_time(c.s, w, c.hw, c.compulsory);
   p->variant_key = make_variant_key(p->family, p->cfg, p->swizzle, p->pk, c.s.dtype, (int)c.s.layouts) |
                    ((uint64_t)(p->unal & 1) << 13);
-  if (p->ws_bytes > ((int64_t)2 << 30)) return false;  // cap of the partials
   add_prologue(c.s, c.hw, p);
+  if (p->ws_bytes > ((int64_t)2 << 30)) return false;  // cap of the workspace: partials and operand copies
   return true;
 }
 
@@ -741,51 +741,58 @@ adaptcore_hw_t default_hw() {
   h.search_open = 0;
   h.enable_streamk = 0;
   // Constants fitted to per-configuration timings of shapes of the
-  // dynamic-shape, decode-style, small-MN large-K, write-bound and
-  // compute-bound workloads on one MI355X (squared log error of the model
-  // over every measured configuration of a seeded half of the 340 measured
-  // shapes; the other half is held out to check the ranking), evaluated with
-  // the workgroups-per-CU that the device reports for each kernel, which is
-  // what the planner uses at run time. The launch cost is the measured
-  // per-kernel floor of back-to-back launches.
+  // dynamic-shape, decode-style, small-MN large-K, write-bound,
+  // compute-bound and tall-skinny workloads on one MI355X (squared log error
+  // of the model over every measured configuration of a seeded half of the
+  // 370 measured shapes; the other half is held out to check the ranking),
+  // evaluated with the workgroups-per-CU that the device reports for each
+  // kernel, which is what the planner uses at run time. The launch cost is
+  // the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 1.25e-06;
+  h.t_mem_latency = 1.215e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 3.078e+10;
+  h.l2_bw_cu = 3.528e+10;
   h.unaligned_eta = 1;
-  h.l2_hit = 5.895e-33;
-  h.swizzle_gain = 0.9239;
+  h.l2_hit = 5.128e-33;
+  h.swizzle_gain = 0.9092;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
   // 20-21, stream-K 22-29, direct 30-32, persistent 33-43, direct-to-LDS
-  // 44-54; 0 = analytic estimate, no timing data)
+  // 44-57 and their register-load forms 58-63, tall-skinny 64-69 and their
+  // register-load forms 70-73; 0 = analytic estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
-      2.921e-06, 2.093e-06, 2.085e-06, 4.781e-07, 7.899e-07, 3.627e-07, 5.406e-07, 4.085e-07,
-      1.175e-06, 9.358e-14, 9.358e-14, 1.198e-06, 1.312e-06, 1.179e-06, 1.195e-06, 2.063e-06,
-      2.134e-06, 6.25e-07, 6.25e-07, 8.576e-07, 7.298e-07, 3.675e-07, 4.322e-06, 2.457e-06,
-      2.575e-06, 1.506e-06, 1.068e-06, 1.252e-06, 3.603e-07, 4.532e-07, 3.102e-07, 9.358e-14,
-      9.358e-14, 2.803e-06, 2.071e-06, 0, 9.358e-14, 9.358e-14, 7.829e-07, 0,
-      0, 0, 0, 0, 1.951e-06, 6.346e-07, 1.225e-06, 2.385e-08,
-      1.951e-06, 1.957e-06, 7.592e-07, 6.202e-07, 1.39e-06, 9.754e-07, 1.008e-06, 0,
-      0, 0, 0, 0, 0, 0, 0, 0};
+      2.998e-06, 2.003e-06, 1.896e-06, 1.052e-06, 7.781e-07, 7.856e-07, 5.221e-07, 4.469e-07,
+      1.123e-06, 9.358e-14, 9.358e-14, 1.119e-06, 1.258e-06, 1.161e-06, 1.23e-06, 2.245e-06,
+      2.334e-06, 6.076e-07, 5.889e-07, 8.742e-07, 6.991e-07, 8.492e-07, 3.893e-06, 2.031e-06,
+      2.538e-06, 1.203e-06, 8.444e-07, 8.734e-07, 1.765e-07, 4.331e-07, 5.243e-07, 9.358e-14,
+      9.358e-14, 2.758e-06, 2.086e-06, 0, 9.358e-14, 9.358e-14, 7.719e-07, 0,
+      0, 0, 0, 0, 1.979e-06, 1.032e-06, 1.16e-06, 3.245e-08,
+      1.928e-06, 1.918e-06, 6.235e-07, 6.097e-07, 1.311e-06, 8.544e-07, 8.764e-07, 2.818e-09,
+      6.013e-07, 1.295e-07, 1.78e-06, 9.174e-07, 1.215e-06, 1.496e-06, 1.585e-06, 7.774e-07,
+      4.051e-07, 1.239e-07, 3.22e-07, 2.431e-07, 9.358e-14, 8.892e-08, 6.876e-07, 6.545e-07,
+      4.479e-07, 6.778e-07};
   static const double kWg[AC_N_CFG] = {
-      3.009e-06, 1.431e-06, 2.85e-06, 2.859e-06, 1.394e-07, 9.095e-07, 6.2e-07, 9.272e-08,
-      2.07e-06, 1.691e-06, 2.215e-06, 1.996e-06, 1.67e-06, 3.744e-06, 4.034e-06, 9.374e-06,
-      1.237e-05, 4.519e-07, 2.232e-07, 1.467e-06, 1.258e-06, 8.775e-07, 9.358e-14, 9.358e-14,
-      9.358e-14, 9.358e-14, 9.358e-14, 2.2e-06, 5.333e-06, 8.943e-06, 9.358e-14, 2.373e-07,
-      9.358e-14, 1.706e-06, 2.327e-06, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
-      0, 0, 0, 0, 6.773e-06, 3.245e-06, 2.99e-06, 1.996e-06,
-      5.219e-06, 5.084e-06, 2.719e-06, 2.842e-06, 1.985e-06, 3.535e-07, 9.358e-14, 0,
-      0, 0, 0, 0, 0, 0, 0, 0};
+      3.688e-06, 1.883e-06, 3.521e-06, 1.542e-06, 5.116e-08, 4.101e-08, 7.159e-07, 1.055e-07,
+      2.2e-06, 2.03e-06, 2.284e-06, 2.399e-06, 1.948e-06, 3.758e-06, 3.845e-06, 9.588e-06,
+      1.161e-05, 3.831e-07, 4.448e-07, 1.151e-06, 1.363e-06, 7.573e-07, 9.358e-14, 9.358e-14,
+      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 6.18e-06, 8.719e-06, 9.358e-14, 6.409e-07,
+      9.358e-14, 2.313e-07, 1.155e-06, 0, 9.358e-14, 9.358e-14, 2.277e-08, 0,
+      0, 0, 0, 0, 8.18e-06, 3.579e-06, 3.703e-06, 2.205e-06,
+      8.141e-06, 8.444e-06, 3.541e-06, 3.555e-06, 2.622e-07, 8.171e-07, 9.358e-14, 1.585e-06,
+      1.673e-06, 1.038e-06, 2.994e-06, 2.372e-06, 3.2e-07, 3.349e-06, 4.56e-06, 1.782e-06,
+      5.335e-07, 2.643e-06, 2.786e-06, 1.646e-06, 9.358e-14, 6.895e-07, 7.975e-07, 1.501e-06,
+      8.851e-07, 1.898e-06};
   // achieved fraction of the streaming rate for the output writes (0: 1)
   static const double kWr[AC_N_CFG] = {
-      1, 1, 1, 0.9751, 0.5984, 0.4579, 1, 1,
-      1, 0.5015, 0.6661, 1, 1, 1, 1, 1,
-      1, 0.06294, 0.1201, 0.3006, 0.9997, 0.5074, 0.6995, 0.7196,
-      0.3366, 0.5965, 0.4149, 0.7958, 0.2185, 0.2677, 1, 0.1701,
-      0.1969, 0.558, 0.6042, 0, 0.3914, 0.334, 0.3866, 0,
-      0, 0, 0, 0, 0.9998, 0.9621, 1, 1,
-      0.7432, 0.6495, 1, 1, 0.9466, 1, 1, 0,
-      0, 0, 0, 0, 0, 0, 0, 0};
+      1, 1, 1, 0.5848, 0.3916, 0.4206, 1, 1,
+      1, 0.5484, 0.6664, 1, 0.9998, 1, 1, 1,
+      1, 0.05122, 0.1124, 0.3069, 0.9997, 0.5216, 0.6117, 0.55,
+      0.3295, 0.4925, 0.3626, 0.4455, 0.2271, 0.2707, 1, 0.1986,
+      0.1266, 0.486, 0.5211, 0, 0.351, 0.3014, 0.3493, 0,
+      0, 0, 0, 0, 0.9998, 1, 1, 1,
+      0.9326, 0.7661, 1, 1, 0.492, 1, 1, 1,
+      1, 1, 0.743, 1, 0.9993, 1, 1, 1,
+      0.05, 0.1972, 0.1852, 0.147, 0.08733, 0.1308, 0.06128, 0.05,
+      0.05568, 0.1786};
   for (int i = 0; i < AC_N_CFG; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];

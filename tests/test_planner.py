@@ -182,13 +182,34 @@ def test_addmm_argument_validation():
     ac.adaptcore_addmm(ac.adaptcore_plan(0, 5, 7), 0, 7, 0x2000, 5, 0x3000, 5, 2.0, 0.5, 0x4000)
 
 
+def _copies(fam, M, N, K, layouts):
+    """The prologue copies a plan of this family makes: (kernel, rows,
+    columns) each, in launch order (A first)."""
+    a_col, b_col = layouts & 1, layouts & 2
+    out = []
+    if fam == ac.AC_FAMILY_TALL:  # B read as B^T (N x K): transposed from row-major, copied from column-major
+        return [("k_pad16" if b_col else "k_transpose16", N, K)]
+    dl = fam == ac.AC_FAMILY_DL
+    if a_col:
+        out.append(("k_transpose16", M, K))
+    elif dl and K % 8:
+        out.append(("k_pad16", M, K))
+    if b_col and fam != ac.AC_FAMILY_SKINNY_M:
+        out.append(("k_transpose16", K, N))
+    elif not b_col and dl and N % 8:
+        out.append(("k_pad16", K, N))
+    return out
+
+
 def test_layout_plans():
     """Column-major operands: a prologue copy per operand in the workspace
     (after the partials, 256-byte aligned, rows padded to 8), priced in the
     prediction -- except a column-major B under the small-M kernel, which
-    reads it in place. Every forced configuration keeps the row-major
-    configuration's kernels after the copies."""
-    for (M, N, K) in [(2100, 3000, 200), (640, 1000, 4096), (4, 4096, 4096), (37, 91, 333)]:
+    reads it in place; the direct-to-LDS kernels also pad unaligned
+    row-major operands, and the tall-skinny kernel always reads B's
+    transposed copy. Every forced configuration keeps the row-major
+    configuration's main kernels after the copies."""
+    for (M, N, K) in [(2100, 3000, 200), (640, 1000, 4096), (4, 4096, 4096), (37, 91, 333), (3000, 9, 1000)]:
         for layouts in (1, 2, 3):
             for c in ac.adaptcore_candidates(M, N, K, ac.AC_BF16_BF16OUT, layouts):
                 key = c["variant_key"]
@@ -197,22 +218,21 @@ def test_layout_plans():
                 h0 = ac.adaptcore_plan_variant(M, N, K, ac.AC_BF16_BF16OUT, 0, key & ~(3 << 52))
                 d, d0 = ac.adaptcore_plan_info(h), ac.adaptcore_plan_info(h0)
                 assert d["layouts"] == layouts
-                skinny = d["family"] == ac.AC_FAMILY_SKINNY_M
-                ws, copies = d0["workspace_bytes"], 0
-                if layouts & 1:
-                    ws = -(-ws // 256) * 256 + M * (-(-K // 8) * 8) * 2
-                    copies += 1
-                if layouts & 2 and not skinny:
-                    ws = -(-ws // 256) * 256 + K * (-(-N // 8) * 8) * 2
-                    copies += 1
+                fam = d["family"]
+                skinny = fam == ac.AC_FAMILY_SKINNY_M
+                ws = d["pk"] * M * (-(-N // 8) * 8) * 4 if d["pk"] > 1 else 0  # the split-K partials
+                copies = _copies(fam, M, N, K, layouts)
+                for _, rows, cols in copies:
+                    ws = -(-ws // 256) * 256 + rows * (-(-cols // 8) * 8) * 2
                 assert d["workspace_bytes"] == ws, (layouts, c)
-                assert (d["predicted_s"] > d0["predicted_s"]) == (copies > 0)
+                n0 = len(_copies(fam, M, N, K, 0))
+                assert (d["predicted_s"] > d0["predicted_s"]) == (len(copies) > n0) or fam == ac.AC_FAMILY_TALL
                 names = ac.adaptcore_plan_kernels(h)
-                assert names[:copies] == ["k_transpose16"] * copies
-                rest = ac.adaptcore_plan_kernels(h0)
+                assert names[:len(copies)] == [k for k, _, _ in copies], (names, copies)
+                rest = ac.adaptcore_plan_kernels(h0)[n0:]
                 if layouts & 2 and skinny:
                     rest = [n.replace("k_skinny_m<", "k_skinny_m_bt<") for n in rest]
-                assert names[copies:] == rest, (names, rest)
+                assert names[len(copies):] == rest, (names, rest)
         # the decode shape with B column-major picks the in-place small-M kernel
         if (M, N, K) == (4, 4096, 4096):
             names = ac.adaptcore_plan_kernels(ac.adaptcore_plan(M, N, K, ac.AC_BF16_BF16OUT, 2))
