@@ -405,7 +405,8 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
     if (!(a_ok && b_ok)) {
       sib = p;
       const ac::DlCfg& d = ac::kDlCfg[p.cfg];
-      if (d.unal && !a_col && !b_col && K >= 8 && N >= 8) {
+      // (column-major operands reach the kernel as aligned row-major copies)
+      if (d.unal && K >= 8 && N >= 8) {
         sib.unal = 1;
       } else if (d.sibling >= 0) {
         sib.family = ac::FAM_TILE;

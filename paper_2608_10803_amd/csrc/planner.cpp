@@ -288,6 +288,9 @@ bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, int unal, Plan* p,
   if (unal && (!d.unal || s.layouts != AC_LAYOUT_ROW_ROW || s.K < 8 || s.N < 8 || ((s.K % 8) == 0 && (s.N % 8) == 0)))
     return false;
   if (dl_lds_bytes(d) > c.hw.lds_bytes) return false;
+  // a tiling without a tile-family sibling falls back to its register-load
+  // form on misaligned operands, which needs K, N >= 8
+  if (d.sibling < 0 && (s.K < 8 || s.N < 8)) return false;
   // four waves in 2 x 2, or side by side along N for tiles of at most 64 rows
   const int wm = d.bm >= 128 ? 2 : 1;
   if (!build_tiling(c, d.bm, d.bn, wm, 4 / wm, 32, pk_req, swizzle, p, w)) return false;
