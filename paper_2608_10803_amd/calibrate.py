@@ -101,16 +101,17 @@ def split_shapes(shape_keys, seed=15):
     return train, set(keys) - train
 
 
-def write_bound_shapes(n=40, seed=12):
+def write_bound_shapes(n=50, seed=12):
     """Shapes whose traffic is mostly the output (large M x N, small K), drawn
     on their own (not from the sweep): M, N log-uniform in [2048, 100000], K
-    log-uniform in [8, 400], kept when C is at least half of the bytes and
-    at most 4 GiB. They fix the per-configuration write efficiency."""
+    log-uniform in [1, 400], kept when C is at least half of the bytes and
+    at most 4 GiB. They fix the per-configuration write efficiency, and
+    K <= 16 the small-K kernel's against the tile kernels'."""
     rng = np.random.default_rng(seed)
     out = []
     while len(out) < n:
         M, N = (int(round(math.exp(rng.uniform(math.log(2048), math.log(100000))))) for _ in range(2))
-        K = int(round(math.exp(rng.uniform(math.log(8), math.log(400)))))
+        K = int(round(math.exp(rng.uniform(0.0, math.log(400)))))
         c = 2.0 * M * N
         if c >= 0.5 * (2.0 * M * K + 2.0 * K * N + c) and c <= 4 * 2 ** 30:
             out.append((M, N, K))
