@@ -332,13 +332,57 @@ def time_plan(ac, torch, plan, M, N, K, dtype, copies=8, target_s=250e-6, steps=
     return statistics.median(ts)
 
 
+def time_read(ac, torch, nbytes, copies=8, target_s=250e-6, steps=5):
+    """Seconds per plain read of `nbytes` (the library's read probe), timed
+    like time_plan: graph-replayed batches cycling through copies of the
+    buffer, median over batches -- the achievable HBM read rate for the bytes
+    a streaming kernel must read."""
+    dev = torch.device("cuda")
+    nb = (nbytes + 15) // 16 * 16
+    nc = max(1, min(copies, (3 << 30) // nb))
+    buf = torch.empty(nc * nb // 2, dtype=torch.bfloat16, device=dev).uniform_(-1, 1)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    cs = torch.cuda.Stream()
+
+    def call(r):
+        ac.adaptcore_read_probe(buf.data_ptr() + (r % nc) * nb, nb, sink.data_ptr(), cs.cuda_stream)
+    for r in range(3):
+        call(r)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(cs):
+        e0.record()
+        call(0)
+        e1.record()
+    torch.cuda.synchronize()
+    R = int(min(64, max(4, math.ceil(target_s / max(e0.elapsed_time(e1) * 1e-3, 1e-7)))))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cs):
+        for r in range(R):
+            call(r)
+    g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(steps):
+        with torch.cuda.stream(cs):
+            e0.record()
+            g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3 / R)
+    del g, buf
+    return statistics.median(ts)
+
+
 def ablation_main(args):
     """The paper's two single-shape experiments replayed on MI355X (Section 6.3
     module ablation, Section 6.4 scalability), bf16 output:
       * modules on 12288 x 688 x 16991, added one at a time to the Common
         template's 128 x 128 tile: XCD-aware tile order, two k-blocks in
-        flight, split-K, the persistent kernel with next-tile preloading,
-        stream-K; then the best measured configuration and the model's pick;
+        flight, split-K; the direct-to-LDS tile with the Padding prologue
+        and with its register-load form instead, deeper LDS pipeline,
+        split-K; the persistent kernel with next-tile preloading, stream-K;
+        then the best measured configuration and the model's pick;
       * CU scaling on 3 x 256 x 87087: the MultiCoreSplitK kernel (small-M
         kernel, K split P_k ways) with P_k = c workgroups, i.e. c CUs busy."""
     import torch
@@ -367,6 +411,19 @@ def ablation_main(args):
               ("+ 2 k-blocks in flight", key(0, 8, 1, 1))]
     if splits:
         ladder.append(("+ split-K (model's best P_k = %d)" % splits[0]["pk"], splits[0]["variant_key"]))
+    # the Padding module (Table 2) against its in-kernel alternative on the
+    # direct-to-LDS kernels (K = 16991 is not a multiple of 8: the direct
+    # loads need A copied zero-padded first; the register-load form reads A
+    # as it is)
+    dl = [c for c in cands if c["family_name"] == "dl" and c["tile_m"] == 128 and c["tile_n"] == 128]
+    dl_split = sorted((c for c in dl if c["pk"] > 1 and not (c["variant_key"] >> 13) & 1),
+                      key=lambda c: c["predicted_s"])
+    ladder += [("direct-to-LDS 128x128x64, 2 LDS stages, Padding prologue (k_pad16 copy of A)", key(9, 9, 1, 1)),
+               ("the same, register-load form in place of the prologue", key(9, 9, 1, 1) | (1 << 13)),
+               ("direct-to-LDS 128x128x64, 3 LDS stages, Padding prologue", key(9, 3, 1, 1))]
+    if dl_split:
+        ladder.append(("+ split-K (model's best direct-to-LDS 128x128, P_k = %d)" % dl_split[0]["pk"],
+                       dl_split[0]["variant_key"]))
     ladder += [("persistent 128x128 with next-tile preloading", key(7, 3, 1, 1)),
                ("stream-K 128x128", next((c["variant_key"] for c in cands if c["family_name"] == "streamk"
                                          and c["tile_m"] == 128 and c["tile_n"] == 128), None))]
@@ -672,9 +729,13 @@ def main():
     # rate is taken over its launches in the timed region, every shape's
     # calls weighted by the R launches per batch as a profiler counts them:
     # algorithmic FLOPs or bytes of those launches / their time.
+    # (A workload whose every plan launches several kernels -- the decode
+    # shapes, all split K -- takes its plans whole: the "kernel" is then the
+    # plan's kernel list and the time the call's.)
     by_k = {}
+    single = any(";" not in r["kernel"] for r in rows)
     for i, r in enumerate(rows):
-        if ";" in r["kernel"]:
+        if single and ";" in r["kernel"]:
             continue
         e = by_k.setdefault(r["kernel"], {"pass": 0.0, "t": 0.0, "F": 0.0, "B": 0.0, "n": 0, "shapes": 0})
         e["pass"] += r["t"]
@@ -699,8 +760,11 @@ def main():
                      "launches_per_step": dom["n"], "avg_launch_us": round(dom["t"] / dom["n"] * 1e6, 2),
                      "share_of_pass": round(dom["pass"] / sum(r["t"] for r in rows), 3)})
 
+    names = {"sweep": "dynamic-shape sweep", "single": "the 512^3 case", "skinny": "the 21 decode shapes",
+             "splitk": "the 9 small-MN large-K shapes", "mfma": "the compute-bound shapes"}
     line = {
-        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s (geomean)",
+        "metric": METRIC.replace("dynamic-shape sweep", names[args.workload]), "value": round(value, 3),
+        "unit": "TFLOP/s (geomean)",
         "frac_geomean": round(frac, 4),
         "n_gpus": 1, "steps": K_steps, "warmup": args.warmup,
         "ms_per_step": round(wall / K_steps * 1e3, 2),
@@ -729,6 +793,17 @@ def main():
                             "timing": "one call after a 512 MiB read, bracketed by its own events"}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(shapes, cbytes)
+    if args.workload == "skinny":
+        # the decode shapes stream B: the plain read of B's bytes on this GPU
+        # is their practical ceiling
+        for r in rows:
+            r["t_read"] = time_read(ac, torch, 2 * r["K"] * r["N"])
+            r["read_frac"] = r["t_floor"] / r["t_read"]
+            r["vs_read"] = r["t_read"] / r["t"]
+        line["read_ceiling"] = {
+            "frac_geomean": round(gmean([r["read_frac"] for r in rows]), 4),
+            "kernel_vs_read_geomean": round(gmean([r["vs_read"] for r in rows]), 4),
+            "timing": "the library's read probe over B's bytes, same batching"}
     if args.per_shape:
         with open(args.per_shape, "w") as f:
             json.dump({"line": line, "rows": rows}, f)

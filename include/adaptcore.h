@@ -469,6 +469,17 @@ adaptcore_status adaptcore_cache_clear(void);
  * (timed in C, without any binding overhead). */
 adaptcore_status adaptcore_bench_lookup(int64_t n_keys, int64_t n_lookups, double* ns_per_lookup);
 
+/* Measurement reference, not part of the method: reads every byte of the
+ * device buffer `buf` once (16-byte non-temporal loads, 8 in flight per
+ * thread, two workgroups per CU) on `stream`, so that the time of a call is
+ * the achievable HBM read rate for that many bytes -- the practical ceiling
+ * of the kernels that stream one operand (the small-M / decode and
+ * tall-skinny paths). `buf` 16-byte aligned, `bytes` a multiple of 16 (else
+ * AC_ERR_INVALID_VALUE); `sink` a 4-byte aligned device word that is written
+ * only if the XOR of all the data equals 0x9E3779B9. AC_ERR_LAUNCH if the
+ * runtime rejects the launch. */
+adaptcore_status adaptcore_read_probe(const void* buf, int64_t bytes, void* sink, void* stream);
+
 /* Thread-local message of the last failure ("" if none). */
 const char* adaptcore_last_error(void);
 

@@ -181,6 +181,8 @@ def lib():
         L.adaptcore_cache_clear.restype = i32
         L.adaptcore_bench_lookup.argtypes = [i64, i64, ctypes.POINTER(d)]
         L.adaptcore_bench_lookup.restype = i32
+        L.adaptcore_read_probe.argtypes = [p, i64, p, p]
+        L.adaptcore_read_probe.restype = i32
         L.adaptcore_last_error.argtypes = []
         L.adaptcore_last_error.restype = ctypes.c_char_p
         L.adaptcore_last_status.argtypes = []
@@ -363,6 +365,11 @@ def adaptcore_stats():
 
 def adaptcore_cache_clear():
     return _check(lib().adaptcore_cache_clear())
+
+
+def adaptcore_read_probe(buf, nbytes, sink, stream=0):
+    """Measurement reference: read `nbytes` of the device buffer once."""
+    return _check(lib().adaptcore_read_probe(buf, nbytes, sink, stream))
 
 
 def adaptcore_bench_lookup(n_keys, n_lookups):

@@ -954,6 +954,16 @@ adaptcore_status adaptcore_cache_clear(void) {
   return AC_OK;
 }
 
+adaptcore_status adaptcore_read_probe(const void* buf, int64_t bytes, void* sink, void* stream) {
+  if (!buf || !sink || bytes < 0) return fail(AC_ERR_INVALID_VALUE, "bad argument");
+  adaptcore_status st = ensure_init();
+  if (st != AC_OK) return st;
+  const hipError_t e = ac::launch_read_probe(buf, bytes, sink, static_cast<hipStream_t>(stream));
+  if (e == hipErrorInvalidValue) return fail(AC_ERR_INVALID_VALUE, "buffer or size not 16-byte aligned");
+  if (e != hipSuccess) return fail(AC_ERR_LAUNCH, std::string("kernel launch failed: ") + hipGetErrorString(e));
+  return AC_OK;
+}
+
 adaptcore_status adaptcore_bench_lookup(int64_t n_keys, int64_t n_lookups, double* ns_per_lookup) {
   if (n_keys <= 0 || n_lookups <= 0 || !ns_per_lookup) return fail(AC_ERR_INVALID_VALUE, "bad argument");
   std::vector<std::tuple<int64_t, int64_t, int64_t>> keys;

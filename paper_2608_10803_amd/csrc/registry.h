@@ -43,6 +43,9 @@ void query_occupancy();
 // pitch ld_src >= cols); the pad of each dst row is written with zeros.
 hipError_t launch_transpose16(const uint16_t* src, int64_t ld_src, int64_t rows, int64_t cols, uint16_t* dst,
                               int64_t ld_dst, hipStream_t st);
+// Measurement reference (not part of the product): reads every byte of
+// `buf` once (16-byte aligned, `bytes` a multiple of 16).
+hipError_t launch_read_probe(const void* buf, int64_t bytes, void* sink, hipStream_t st);
 // the same kernels for fp16 inputs (dtypes 2 and 3)
 namespace f16 {
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
