@@ -374,6 +374,46 @@ def time_read(ac, torch, nbytes, copies=8, target_s=250e-6, steps=5):
     return statistics.median(ts)
 
 
+def time_torch_matmul(torch, M, N, K, copies=4, target_s=250e-6, steps=5):
+    """Seconds per torch.matmul of bf16 (M x K) @ (K x N) into bf16, timed
+    like time_plan (graph-replayed batches over operand copies): a reference
+    point from the platform's library GEMM, not part of the path."""
+    dev = torch.device("cuda")
+    na = max(1, min(copies, (3 << 30) // (2 * M * K)))
+    nb = max(1, min(copies, (3 << 30) // (2 * K * N)))
+    A = [torch.empty(M, K, dtype=torch.bfloat16, device=dev).uniform_(-1, 1) for _ in range(na)]
+    B = [torch.empty(K, N, dtype=torch.bfloat16, device=dev).uniform_(-1, 1) for _ in range(nb)]
+    C = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+    cs = torch.cuda.Stream()
+    with torch.cuda.stream(cs):
+        for r in range(3):
+            torch.matmul(A[r % na], B[r % nb], out=C)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(cs):
+        e0.record()
+        torch.matmul(A[0], B[0], out=C)
+        e1.record()
+    torch.cuda.synchronize()
+    R = int(min(64, max(4, math.ceil(target_s / max(e0.elapsed_time(e1) * 1e-3, 1e-7)))))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cs):
+        for r in range(R):
+            torch.matmul(A[r % na], B[r % nb], out=C)
+    g.replay()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(steps):
+        with torch.cuda.stream(cs):
+            e0.record()
+            g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3 / R)
+    del g, A, B, C
+    return statistics.median(ts)
+
+
 def ablation_main(args):
     """The paper's two single-shape experiments replayed on MI355X (Section 6.3
     module ablation, Section 6.4 scalability), bf16 output:
@@ -804,6 +844,13 @@ def main():
             "frac_geomean": round(gmean([r["read_frac"] for r in rows]), 4),
             "kernel_vs_read_geomean": round(gmean([r["vs_read"] for r in rows]), 4),
             "timing": "the library's read probe over B's bytes, same batching"}
+    if args.workload == "mfma":
+        # reference point: the platform's library GEMM on the same shapes
+        for r in rows:
+            r["t_torch"] = time_torch_matmul(torch, r["M"], r["N"], r["K"])
+            r["torch_frac"] = r["t_floor"] / r["t_torch"]
+        line["torch_matmul"] = {"frac_geomean": round(gmean([r["torch_frac"] for r in rows]), 4),
+                                "timing": "torch.matmul (bf16 out) on the same shapes, same batching"}
     if args.per_shape:
         with open(args.per_shape, "w") as f:
             json.dump({"line": line, "rows": rows}, f)
