@@ -74,6 +74,11 @@ __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
 }
 // fp32 -> the 16-bit output format, round to nearest even; NaN stays NaN
 __device__ __forceinline__ uint16_t to16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+// c + a.lo * b.lo + a.hi * b.hi for two packed pairs of inputs (v_dot2c_f32_f16)
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, a), __builtin_bit_cast(h2, b), c, false);
+}
 // the value of a 16-bit input element (low 16 bits of h)
 __device__ __forceinline__ float from16(uint32_t h) { return (float)__builtin_bit_cast(_Float16, (uint16_t)h); }
 #else
@@ -86,6 +91,11 @@ __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
                                                  0, 0);
 }
 __device__ __forceinline__ uint16_t to16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// c + a.lo * b.lo + a.hi * b.hi for two packed pairs of inputs (v_dot2c_f32_bf16)
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(b2, a), __builtin_bit_cast(b2, b), c, false);
+}
 __device__ __forceinline__ float from16(uint32_t h) { return __uint_as_float(h << 16); }
 #endif
 

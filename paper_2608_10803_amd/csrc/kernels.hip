@@ -31,6 +31,7 @@
 #include <type_traits>
 
 #include "kernel_args.h"
+#include "variants.h"
 
 #ifndef AC_INPUT_F16
 #define AC_INPUT_F16 0
@@ -1472,6 +1473,137 @@ __global__ __launch_bounds__(256) void k_smallk(GemmArgs g) {
   }
 }
 
+// Wide rows (the plan's tile_n = SMALLK_WIN_COLS): a workgroup owns a band of
+// R = g.kper rows and SMALLK_WIN_COLS columns, and per row writes the window
+// of the same width that starts at the 128-byte line boundary at or before
+// its first column. The windows of a row then tile it line by line, and no
+// line of C is written by two workgroups (but a row's first and last). A
+// line that two workgroups write in parts -- on different CUs, usually on
+// different XCDs -- is written back to memory twice in parts, and such
+// writes cost several times a whole line: with misaligned row starts, a
+// 16-byte-per-lane store pattern wrote at about 3.4 TB/s against 5.3 TB/s
+// for the same bytes in line-aligned rows. The window reaches up to 63
+// columns to the left of the workgroup's own, so every thread computes 8
+// columns of a range that starts 64 columns before them (256 threads: 64
+// halo + SMALLK_WIN_COLS columns). Groups of rows go through LDS in C's
+// format (after the AddMM epilogue) and are stored from there, shifted to
+// the window, as whole 16-byte (bf16) or 32-byte (fp32) segments. The sums
+// run over pairs of k in ascending order with the packed two-term dot
+// product (fp32 accumulator; half the instructions of single FMAs, which
+// bound this kernel on K > 4); pairs past K are skipped. The epilogue reads
+// C_old at every computed column; the halo columns outside the window
+// belong to the neighbouring workgroup, and their values are never stored.
+template <int KMAX, bool OBF>
+__global__ __launch_bounds__(256) void k_smallk_win(GemmArgs g) {
+  constexpr int H = KMAX / 8, RG = OBF ? 4 : 2;  // 16-byte chunks of an A row; rows per LDS round
+  constexpr int LE = OBF ? 64 : 32;     // elements of C per 128-byte line
+  constexpr int SW = OBF ? 4 : 8;       // dwords of a thread's 8 outputs
+  __shared__ u32x4 sA[SMALLK_MAX_ROWS * H];
+  __shared__ uint32_t sC[2][RG][256 * SW + 4];
+  const int tid = threadIdx.x;
+  const int64_t M = g.M, N = g.N, K = g.K, R = g.kper;
+  const int64_t c_own = (int64_t)blockIdx.x * SMALLK_WIN_COLS;
+  const int64_t c0 = c_own - 64 + 8 * tid;  // this thread's 8 computed columns
+  const int valid = c0 < 0 ? 0 : (int)min((int64_t)8, N - c0);
+  const int64_t r0 = (int64_t)blockIdx.y * R, r1 = min(r0 + R, M);
+  for (int64_t i = tid; i < (r1 - r0) * H; i += 256)
+    sA[i] = load_row(g.A + (r0 + i / H) * g.lda, (i % H) * 8, K);
+  // B rows 2i and 2i+1 of column j packed into one word (rows past K zero)
+  uint32_t bp[KMAX / 2][8];
+#pragma unroll
+  for (int i = 0; i < KMAX / 2; ++i) {
+    u32x4 v0 = u32x4{0u, 0u, 0u, 0u}, v1 = v0;
+    if (2 * i < K && valid > 0) v0 = load_row(g.B + (int64_t)(2 * i) * g.ldb, c0, N);
+    if (2 * i + 1 < K && valid > 0) v1 = load_row(g.B + (int64_t)(2 * i + 1) * g.ldb, c0, N);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      bp[i][2 * e] = __builtin_amdgcn_perm(v1[e], v0[e], 0x05040100u);      // low halves
+      bp[i][2 * e + 1] = __builtin_amdgcn_perm(v1[e], v0[e], 0x07060302u);  // high halves
+    }
+  }
+  __syncthreads();
+  for (int64_t rb = r0; rb < r1; rb += RG) {
+    const int par = (int)(((rb - r0) / RG) & 1);
+#pragma unroll
+    for (int r = 0; r < RG; ++r) {
+      const int64_t row = min(rb + r, r1 - 1);
+      const u32x4* a_row = sA + (row - r0) * H;
+      float acc[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+#pragma unroll
+      for (int i = 0; i < KMAX / 2; ++i) {
+        if (2 * i < K) {  // (uniform)
+          const uint32_t w = a_row[i / 4][i % 4];  // A elements 2i, 2i+1 of the row
+#pragma unroll
+          for (int j = 0; j < 8; ++j) acc[j] = dot2(w, bp[i][j], acc[j]);
+        }
+      }
+      epi_apply<OBF, 8>(g, acc, row, c0, valid);
+      uint32_t* dst = &sC[par][r][SW * tid];
+      if constexpr (OBF) {
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = (uint32_t)to16(acc[2 * e]) | ((uint32_t)to16(acc[2 * e + 1]) << 16);
+        *reinterpret_cast<u32x4*>(dst) = w;
+      } else {
+        *reinterpret_cast<f32x4*>(dst) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+        *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+      }
+    }
+    __syncthreads();
+    if (tid < SMALLK_WIN_COLS / 8) {
+#pragma unroll
+      for (int r = 0; r < RG; ++r) {
+        const int64_t row = rb + r;
+        if (row >= r1) break;
+        const int64_t rowoff = row * g.ldc;
+        // elements of C between the line boundary and the first own column
+        const int mu = (int)(((uintptr_t)g.C / (OBF ? 2 : 4) + rowoff + c_own) & (LE - 1));
+        const int o = 64 - mu + 8 * tid;  // offset of the window chunk in the computed range: 1 .. 2040
+        const int64_t col = c_own - mu + 8 * tid;
+        const uint32_t* src = &sC[par][r][0];
+        uint32_t y[SW];
+        if constexpr (OBF) {
+          const int d0 = o >> 1;
+          if (o & 1) {  // odd element offset: funnel pairs of dwords by 2 bytes
+            uint32_t x[5];
+#pragma unroll
+            for (int d = 0; d < 5; ++d) x[d] = src[d0 + d];
+#pragma unroll
+            for (int d = 0; d < 4; ++d) y[d] = __builtin_amdgcn_alignbyte(x[d + 1], x[d], 2);
+          } else {
+#pragma unroll
+            for (int d = 0; d < 4; ++d) y[d] = src[d0 + d];
+          }
+        } else {
+#pragma unroll
+          for (int d = 0; d < 8; ++d) y[d] = src[o + d];
+        }
+        if (col >= 0 && col + 8 <= N) {
+          if constexpr (OBF) {
+            const u32x4 w = u32x4{y[0], y[1], y[2], y[3]};
+            __builtin_memcpy(static_cast<uint16_t*>(g.C) + rowoff + col, &w, 16);
+          } else {
+            float* p = static_cast<float*>(g.C) + rowoff + col;
+            const u32x4 w0 = u32x4{y[0], y[1], y[2], y[3]}, w1 = u32x4{y[4], y[5], y[6], y[7]};
+            __builtin_memcpy(p, &w0, 16);
+            __builtin_memcpy(p + 4, &w1, 16);
+          }
+        } else {
+          for (int e = 0; e < 8; ++e) {
+            if (col + e < 0 || col + e >= N) continue;
+            if constexpr (OBF)
+              static_cast<uint16_t*>(g.C)[rowoff + col + e] = (uint16_t)(y[e >> 1] >> (16 * (e & 1)));
+            else
+              static_cast<uint32_t*>(g.C)[rowoff + col + e] = y[e];
+          }
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------- direct kernel
 // Latency-lean kernel for small problems: no LDS staging, no register
 // transposes. A wave computes one 32 x 32 block of C with 32x32x16 MFMAs,
@@ -1849,11 +1981,21 @@ hipError_t launch_skinny_n(const Plan& p, const GemmArgs& g, hipStream_t st, boo
 
 template <int KMAX>
 hipError_t launch_smallk(const Plan& p, const GemmArgs& g, hipStream_t st, bool obf) {
-  const dim3 grid(p.grid_x, 1), block(256);
-  if (obf)
-    hipLaunchKernelGGL((k_smallk<KMAX, true>), grid, block, 0, st, g);
-  else
-    hipLaunchKernelGGL((k_smallk<KMAX, false>), grid, block, 0, st, g);
+  const dim3 grid(p.grid_x, p.grid_y), block(256);
+  if (p.tile_n == SMALLK_WIN_COLS) {
+    // the windows must cover every column and the bands every row
+    if ((int64_t)p.grid_x * SMALLK_WIN_COLS < g.N + 63 || (int64_t)p.grid_y * g.kper < g.M || g.kper > SMALLK_MAX_ROWS)
+      return hipErrorInvalidValue;
+    if (obf)
+      hipLaunchKernelGGL((k_smallk_win<KMAX, true>), grid, block, 0, st, g);
+    else
+      hipLaunchKernelGGL((k_smallk_win<KMAX, false>), grid, block, 0, st, g);
+  } else {
+    if (obf)
+      hipLaunchKernelGGL((k_smallk<KMAX, true>), grid, block, 0, st, g);
+    else
+      hipLaunchKernelGGL((k_smallk<KMAX, false>), grid, block, 0, st, g);
+  }
   return hipGetLastError();
 }
 
@@ -1975,7 +2117,9 @@ const LaunchFn kSkinnyNFns[] = {&launch_skinny_n<1, 2>, &launch_skinny_n<2, 2>, 
 const OccFn kSkinnyNOcc[] = {&occ_skinny_n<1, 2>, &occ_skinny_n<2, 2>, &occ_skinny_n<4, 2>};
 template <int KMAX>
 int occ_smallk() {
-  return occ_of(k_smallk<KMAX, false>, k_smallk<KMAX, true>);
+  const int a = occ_of(k_smallk<KMAX, false>, k_smallk<KMAX, true>);
+  const int b = occ_of(k_smallk_win<KMAX, false>, k_smallk_win<KMAX, true>);
+  return a < b ? a : b;
 }
 template <int WK>
 int occ_direct() {

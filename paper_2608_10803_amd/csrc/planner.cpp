@@ -542,19 +542,25 @@ bool build_smallk(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   int64_t rpt = 4;
   while (rpt < SMALLK_MAX_ROWS && ncg * cdiv(s.M, 2 * rpt) >= (int64_t)c.hw.n_cu * 2048) rpt *= 2;
   const int64_t nrg = cdiv(s.M, rpt);
-  const int64_t wgs = cdiv(ncg * nrg, 256);
-  if (wgs > (1LL << 31) - 1) return false;
+  // wide rows: line-aligned windows of SMALLK_WIN_COLS columns per band of
+  // rpt rows (k_smallk_win); otherwise 256 consecutive threads of the
+  // (row run, column group) order
+  const bool win = s.N >= SMALLK_WIN_MIN_N && nrg <= 65535;
+  const int64_t gx = win ? cdiv(s.N + 63, SMALLK_WIN_COLS) : cdiv(ncg * nrg, 256);
+  const int64_t gy = win ? nrg : 1;
+  if (gx > (1LL << 31) - 1) return false;
   p->family = FAM_SMALLK;
   p->cfg = cfg;
   p->tile_m = (int)rpt;
-  p->tile_n = 8;
+  p->tile_n = win ? SMALLK_WIN_COLS : 8;
   p->tile_k = k.kmax;
   p->pm = (int)std::min<int64_t>(nrg, (1LL << 31) - 1);
-  p->pn = (int)ncg;
+  p->pn = (int)(win ? gx : ncg);
   p->pk = 1;
   p->kper = (int)rpt;
-  p->grid_x = (int)wgs;
-  p->grid_y = 1;
+  p->grid_x = (int)gx;
+  p->grid_y = (int)gy;
+  const int64_t wgs = gx * gy;
   w->units = wgs;
   w->occ = occupancy(FAM_SMALLK, cfg);
   w->idx = IDX_SMALLK + cfg;
@@ -564,7 +570,7 @@ bool build_smallk(const Ctx& c, int cfg, int pk_req, Plan* p, Work* w) {
   w->mfma_it = 4.0 * 8 * k.kmax * 4;  // FMA issue cycles of one wave (VALU, 4 cycles each)
   w->lds_it = 0;
   w->setup = 256.0 * s.K * 16.0;      // the B block of every thread
-  w->out_unit = 256.0 * rpt * 8 * c.cbytes;
+  w->out_unit = (win ? SMALLK_WIN_COLS : 256 * 8) * (double)rpt * c.cbytes;
   w->total_write = (double)s.M * s.N * c.cbytes;
   w->prefetch = 1;
   w->total_read = c.compulsory;  // re-reads of A rows and B rows stay in L1/L2
@@ -1233,7 +1239,8 @@ static std::string kernel_names_fmt(const Plan& p) {
       return r;
     }
     case FAM_SMALLK:
-      std::snprintf(buf, sizeof buf, "k_smallk<%d, %s>", kSmallKCfg[p.cfg].kmax, b);
+      std::snprintf(buf, sizeof buf, p.tile_n == SMALLK_WIN_COLS ? "k_smallk_win<%d, %s>" : "k_smallk<%d, %s>",
+                    kSmallKCfg[p.cfg].kmax, b);
       return buf;
     case FAM_PERSIST: {
       const TileCfg& t = kTileCfg[p.cfg];

@@ -66,6 +66,11 @@ struct SmallKCfg {
 constexpr SmallKCfg kSmallKCfg[] = {{8, 4}, {16, 2}};
 constexpr int N_SMALLK_CFG = sizeof(kSmallKCfg) / sizeof(kSmallKCfg[0]);
 constexpr int SMALLK_MAX_ROWS = 32;
+// Wide rows (N >= SMALLK_WIN_MIN_N): a workgroup covers a band of rows and
+// SMALLK_WIN_COLS columns (31 lines of bf16, 62 of fp32) and writes per row
+// the line-aligned window of that width (k_smallk_win).
+constexpr int SMALLK_WIN_COLS = 1984;
+constexpr int SMALLK_WIN_MIN_N = 1024;
 
 // Direct configurations: wk = 1: four waves cover 64 x 64 of C, each over
 // all of K; wk = 4 or 16: that many waves split the K range of one 32 x 32
