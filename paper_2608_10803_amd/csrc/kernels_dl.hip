@@ -12,20 +12,25 @@
 //           one column: the k-contiguous operand the MFMA needs, without the
 //           v_perm transposes of the register-staged kernel.
 //   C       4 waves in a 2 x 2 grid, each a (BM/2) x (BN/2) quadrant of
-//           32 x 32 x 16 MFMAs; fp32 accumulation in the accumulation
-//           registers; bf16 output converted through a per-wave LDS slab and
-//           written as whole 16-byte row segments.
+//           32 x 32 x 16 MFMAs (tiles of at most 64 rows: 4 waves side by
+//           side along N); fp32 accumulation in the accumulation registers;
+//           bf16 output converted through a per-wave LDS slab and written as
+//           whole 16-byte row segments.
 //
 // The swizzle of a stage is applied on the global side: a wave-wide LDS load
 // writes 1024 contiguous bytes (lane l to bytes 16l .. 16l+15), so each lane
 // fetches the global chunk that belongs at its slot.
 //
-// Operands must be row-major with 16-byte aligned rows (A and B base
+// k_dl needs row-major operands with 16-byte aligned rows (A and B base
 // addresses 16-byte aligned, lda and ldb multiples of 8 below 2^22) and K, N
-// multiples of 8; the launcher of the plan checks this and otherwise runs
-// the same tiling on the register-staged tile kernel. Chunks outside the
-// matrices (rows past M, columns past N, k past K) are read as zeros through
-// out-of-range buffer offsets, so edge tiles take the same path.
+// multiples of 8. A plan for other shapes either copies the operand
+// zero-padded first (k_pad16 below, the Padding module) or runs k_dlu, the
+// register-load form of the same tiling (16-byte loads at any 2-byte
+// alignment, two LDS stages); an operand found misaligned at run time takes
+// k_dlu, or the register-staged tile kernel of the same tiling where the
+// configuration has no k_dlu. Chunks outside the matrices (rows past M,
+// columns past N, k past K) are read as zeros through out-of-range buffer
+// offsets, so edge tiles take the same path.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
