@@ -6,7 +6,9 @@ are obtained by profiling. This module
 
   * measures every legal configuration of a sample of shapes on the GPU
     (`measure`, run on the device: per-call time of back-to-back calls
-    replayed from a HIP graph, operands rotating through distinct copies),
+    replayed from a HIP graph, operands rotating through distinct copies,
+    caches flushed before every timed replay as the benchmark's other shapes
+    do between its replays),
   * fits the profile constants so that the model's predictions match the
     measurements in log space (`fit`, host only), and
   * reports how well the model ranks: how often its choice is the measured
@@ -41,6 +43,7 @@ from . import _lib as ac
 FIT_FIELDS = ["t_mem_latency", "hbm_eta", "l2_bw_cu", "unaligned_eta", "l2_hit", "swizzle_gain"]
 BOUNDS = {"hbm_eta": (0.3, 1.0), "unaligned_eta": (0.3, 1.0), "l2_hit": (0.0, 0.99), "swizzle_gain": (0.5, 1.0)}
 N_CFG = ac.AC_N_CFG
+FLUSH_BYTES = 512 << 20
 
 
 def sample_shapes(n_sweep=200, seed=11):
@@ -174,6 +177,11 @@ def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=
     C = torch.empty(maxC // 2, dtype=torch.bfloat16, device=dev)
     s = torch.cuda.Stream()
     ac.adaptcore_reserve_workspace(s.cuda_stream, 2 << 30)
+    # read between timed replays: evicts the L2s and the 256 MB Infinity Cache,
+    # so that every replay starts from the state the benchmark's replays do
+    # (there, the other shapes' batches run in between)
+    flush = torch.zeros(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    red = torch.empty(1, dtype=torch.float32, device=dev)
     warm_up(A, B, C, s)
     recs = []
     t0 = time.time()
@@ -206,6 +214,7 @@ def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=
             ts = []
             for _ in range(3):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.sum(flush, dim=0, keepdim=True, out=red)
                 e0.record()
                 g.replay()
                 e1.record()
