@@ -17,8 +17,10 @@ are obtained by profiling. This module
     for the open search.
 
     python -m paper_2608_10803_amd.calibrate measure OUT.json   (GPU)
-    python -m paper_2608_10803_amd.calibrate fit RECORDS.json   (after init on
-        the GPU machine, so that the planner prices with the device's occupancies)
+    python -m paper_2608_10803_amd.calibrate fit RECORDS.json [--near F]
+        (after init on the GPU machine, so that the planner prices with the
+        device's occupancies; --near F fits only configurations within F
+        times their shape's fastest)
     python -m paper_2608_10803_amd.calibrate emit FIT.json      (C++ defaults)
 
 `fit` holds half of the measured shapes out: the profile is fitted on a
@@ -294,14 +296,23 @@ def _log_errors(hw, meas, keys_filter=None):
     return np.array(err)
 
 
-def fit(recs, hw0=None, rounds=3, iters=300, log=print):
-    """Fit the profile: minimise the squared log error of the model over all
-    measured configurations. Alternates a Nelder-Mead search over the global
-    constants (launch, latency, bandwidth, cache hit rate) with one over the
-    three constants of each kernel configuration (iteration cost, workgroup
-    cost, write efficiency) on that configuration's records."""
+def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
+    """Fit the profile: minimise the squared log error of the model over the
+    measured configurations (with `near`, only those within that factor of
+    their shape's fastest: the ranking depends on the model being right
+    about the competitive candidates, not about configurations many times
+    slower). Alternates a Nelder-Mead search over the global constants
+    (launch, latency, bandwidth, cache hit rate) with one over the three
+    constants of each kernel configuration (iteration cost, workgroup cost,
+    write efficiency) on that configuration's records."""
     from scipy.optimize import minimize
     hw0 = (hw0 or ac.adaptcore_get_hw()).copy()
+    if near:
+        best = {}
+        for r in recs:
+            sk = (r["M"], r["N"], r["K"], r["dtype"])
+            best[sk] = min(best.get(sk, r["t"]), r["t"])
+        recs = [r for r in recs if r["t"] <= near * best[(r["M"], r["N"], r["K"], r["dtype"])]]
     meas = _by_shape(recs)
     by_cfg = {}
     for r in recs:
@@ -398,21 +409,25 @@ def main(argv):
         ta = set(tall_shapes())
         from workloads import gen
         dec = {tuple(s) for s in gen.skinny_m()}
+        tiny = {(r["M"], r["N"], r["K"]) for r in recs
+                if max(2.0 * r["M"] * r["N"] * r["K"] / 2.5e15,
+                       (2.0 * r["M"] * r["K"] + 2.0 * r["K"] * r["N"] + 2.0 * r["M"] * r["N"]) / 8e12) < 1e-6}
 
         def report(h):
             out = {}
             for name, rr in (("train", train), ("held_out", test)):
                 out[name] = {"class": evaluate(rr, h, False), "open": evaluate(rr, h, True)}
                 for tag, st in (("split_k", sk), ("compute_bound", cb), ("write_bound", wb), ("tall", ta),
-                                ("decode", dec)):
+                                ("decode", dec), ("floor_below_1us", tiny)):
                     sub = [r for r in rr if (r["M"], r["N"], r["K"]) in st]
                     if sub:
                         out[name][tag] = evaluate(sub, h, False)
             return out
         before = report(hw0)
-        h, stats = fit(train, hw0, log=lambda m: print(m, file=sys.stderr))
+        near = float(argv[argv.index("--near") + 1]) if "--near" in argv else None
+        h, stats = fit(train, hw0, log=lambda m: print(m, file=sys.stderr), near=near)
         after = report(h)
-        out = {"profile": h.as_dict(), "fit": stats, "before": before, "after": after,
+        out = {"profile": h.as_dict(), "fit": stats, "near": near, "before": before, "after": after,
                "records": len(recs), "shapes": len(_by_shape(recs)), "train_shapes": len(train_keys),
                "held_out_shapes": len(test_keys)}
         print(json.dumps(out, indent=1))
