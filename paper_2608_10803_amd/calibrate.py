@@ -296,6 +296,16 @@ def _log_errors(hw, meas, keys_filter=None):
     return np.array(err)
 
 
+def near_records(recs, near):
+    """The records whose time is within `near` times the fastest measured
+    configuration of the same shape."""
+    best = {}
+    for r in recs:
+        sk = (r["M"], r["N"], r["K"], r["dtype"])
+        best[sk] = min(best.get(sk, r["t"]), r["t"])
+    return [r for r in recs if r["t"] <= near * best[(r["M"], r["N"], r["K"], r["dtype"])]]
+
+
 def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
     """Fit the profile: minimise the squared log error of the model over the
     measured configurations (with `near`, only those within that factor of
@@ -308,11 +318,7 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
     from scipy.optimize import minimize
     hw0 = (hw0 or ac.adaptcore_get_hw()).copy()
     if near:
-        best = {}
-        for r in recs:
-            sk = (r["M"], r["N"], r["K"], r["dtype"])
-            best[sk] = min(best.get(sk, r["t"]), r["t"])
-        recs = [r for r in recs if r["t"] <= near * best[(r["M"], r["N"], r["K"], r["dtype"])]]
+        recs = near_records(recs, near)
     meas = _by_shape(recs)
     by_cfg = {}
     for r in recs:
