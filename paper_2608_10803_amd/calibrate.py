@@ -246,10 +246,14 @@ def predictions(hw, shapes_keys, open_search):
     h = hw.copy()
     h.search_open = 1 if open_search else 0
     h.enable_streamk = 1
+    prev = ac.adaptcore_get_hw()
     ac.adaptcore_set_hw(h)
     out = {}
-    for (M, N, K, dt) in shapes_keys:
-        out[(M, N, K, dt)] = {c["variant_key"]: c["predicted_s"] for c in ac.adaptcore_candidates(M, N, K, dt, 0)}
+    try:
+        for (M, N, K, dt) in shapes_keys:
+            out[(M, N, K, dt)] = {c["variant_key"]: c["predicted_s"] for c in ac.adaptcore_candidates(M, N, K, dt, 0)}
+    finally:
+        ac.adaptcore_set_hw(prev)  # the caller's profile stays in force
     return out
 
 

@@ -220,7 +220,10 @@ def test_layout_plans():
                 assert d["layouts"] == layouts
                 fam = d["family"]
                 skinny = fam == ac.AC_FAMILY_SKINNY_M
-                ws = d["pk"] * M * (-(-N // 8) * 8) * 4 if d["pk"] > 1 else 0  # the split-K partials
+                # the split-K partials (stream-K: its fp32 tile slots, as in the row-major plan)
+                ws = d["pk"] * M * (-(-N // 8) * 8) * 4 if d["pk"] > 1 else 0
+                if fam == ac.AC_FAMILY_STREAMK:
+                    ws = d0["workspace_bytes"]
                 copies = _copies(fam, M, N, K, layouts)
                 for _, rows, cols in copies:
                     ws = -(-ws // 256) * 256 + rows * (-(-cols // 8) * 8) * 2
