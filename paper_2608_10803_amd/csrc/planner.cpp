@@ -751,14 +751,15 @@ adaptcore_hw_t default_hw() {
   h.enable_streamk = 0;
   // Constants fitted to per-configuration timings of shapes of the
   // dynamic-shape, decode-style, small-MN large-K, write-bound,
-  // compute-bound and tall-skinny workloads on one MI355X (squared log error
-  // of the model over every measured configuration of a seeded half of the
-  // 370 measured shapes; the other half is held out to check the ranking),
-  // evaluated with the workgroups-per-CU that the device reports for each
-  // kernel, which is what the planner uses at run time. The launch cost is
-  // the measured per-kernel floor of back-to-back launches.
+  // compute-bound and tall-skinny workloads on one MI355X, each replay timed
+  // after the caches were flushed (squared log error of the model over the
+  // configurations within 2x of their shape's fastest, on a seeded half of
+  // the 380 measured shapes; the other half is held out to check the
+  // ranking), evaluated with the workgroups-per-CU that the device reports
+  // for each kernel, which is what the planner uses at run time. The launch
+  // cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 1.215e-06;
+  h.t_mem_latency = 1.216e-06;
   h.hbm_eta = 1;
   h.l2_bw_cu = 3.528e+10;
   h.unaligned_eta = 1;
@@ -769,39 +770,45 @@ adaptcore_hw_t default_hw() {
   // 44-57 and their register-load forms 58-63, tall-skinny 64-69 and their
   // register-load forms 70-73; 0 = analytic estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
-      2.998e-06, 2.003e-06, 1.896e-06, 1.052e-06, 7.781e-07, 7.856e-07, 5.221e-07, 4.469e-07,
-      1.123e-06, 9.358e-14, 9.358e-14, 1.119e-06, 1.258e-06, 1.161e-06, 1.23e-06, 2.245e-06,
-      2.334e-06, 6.076e-07, 5.889e-07, 8.742e-07, 6.991e-07, 8.492e-07, 3.893e-06, 2.031e-06,
-      2.538e-06, 1.203e-06, 8.444e-07, 8.734e-07, 1.765e-07, 4.331e-07, 5.243e-07, 9.358e-14,
-      9.358e-14, 2.758e-06, 2.086e-06, 0, 9.358e-14, 9.358e-14, 7.719e-07, 0,
-      0, 0, 0, 0, 1.979e-06, 1.032e-06, 1.16e-06, 3.245e-08,
-      1.928e-06, 1.918e-06, 6.235e-07, 6.097e-07, 1.311e-06, 8.544e-07, 8.764e-07, 2.818e-09,
-      6.013e-07, 1.295e-07, 1.78e-06, 9.174e-07, 1.215e-06, 1.496e-06, 1.585e-06, 7.774e-07,
-      4.051e-07, 1.239e-07, 3.22e-07, 2.431e-07, 9.358e-14, 8.892e-08, 6.876e-07, 6.545e-07,
-      4.479e-07, 6.778e-07};
+      3.113e-06, 2.304e-06, 1.952e-06, 1.041e-06, 9.358e-14, 7.837e-07, 5.585e-07, 3.664e-07,
+      1.154e-06, 9.358e-14, 9.358e-14, 1.087e-06, 1.289e-06, 1.161e-06, 1.321e-06, 1.62e-06,
+      1.074e-06, 6.368e-07, 5.896e-07, 6.08e-07, 5.642e-08, 9.358e-14, 3.423e-06, 2.178e-06,
+      1.944e-06, 9.358e-14, 8.634e-07, 1.01e-06, 7.001e-13, 5.216e-07, 5.243e-07, 9.358e-14,
+      5.85e-07, 2.812e-06, 2.04e-06, 0, 9.358e-14, 9.358e-14, 7.369e-07, 0,
+      0, 0, 0, 0, 2.31e-06, 1.311e-06, 1.316e-06, 1.364e-08,
+      2.257e-06, 2.266e-06, 3.156e-07, 2.823e-07, 9.358e-14, 9.358e-14, 8.97e-07, 2.247e-09,
+      5.594e-07, 9.358e-14, 1.7e-06, 9.358e-14, 6.681e-07, 1.751e-06, 1.706e-06, 7.754e-07,
+      4.053e-07, 5.859e-09, 6.636e-08, 2.444e-07, 9.358e-14, 9.358e-14, 7.328e-07, 7.249e-07,
+      4.041e-07, 8.273e-07, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      3.688e-06, 1.883e-06, 3.521e-06, 1.542e-06, 5.116e-08, 4.101e-08, 7.159e-07, 1.055e-07,
-      2.2e-06, 2.03e-06, 2.284e-06, 2.399e-06, 1.948e-06, 3.758e-06, 3.845e-06, 9.588e-06,
-      1.161e-05, 3.831e-07, 4.448e-07, 1.151e-06, 1.363e-06, 7.573e-07, 9.358e-14, 9.358e-14,
-      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 6.18e-06, 8.719e-06, 9.358e-14, 6.409e-07,
-      9.358e-14, 2.313e-07, 1.155e-06, 0, 9.358e-14, 9.358e-14, 2.277e-08, 0,
-      0, 0, 0, 0, 8.18e-06, 3.579e-06, 3.703e-06, 2.205e-06,
-      8.141e-06, 8.444e-06, 3.541e-06, 3.555e-06, 2.622e-07, 8.171e-07, 9.358e-14, 1.585e-06,
-      1.673e-06, 1.038e-06, 2.994e-06, 2.372e-06, 3.2e-07, 3.349e-06, 4.56e-06, 1.782e-06,
-      5.335e-07, 2.643e-06, 2.786e-06, 1.646e-06, 9.358e-14, 6.895e-07, 7.975e-07, 1.501e-06,
-      8.851e-07, 1.898e-06};
+      2.781e-06, 1.275e-06, 3.272e-06, 1.962e-06, 2.365e-06, 6.991e-07, 1.433e-06, 1.166e-06,
+      2.684e-06, 2.719e-06, 2.81e-06, 1.519e-06, 1.383e-06, 2.846e-06, 4.792e-06, 3.69e-06,
+      1.848e-05, 1.935e-06, 2.827e-06, 8.367e-06, 3.002e-06, 9.358e-14, 9.358e-14, 9.358e-14,
+      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 1.037e-05, 3.348e-06, 3.769e-07, 1.525e-06,
+      2.801e-08, 9.358e-14, 1.031e-07, 0, 9.358e-14, 9.358e-14, 5.737e-07, 0,
+      0, 0, 0, 0, 6.044e-06, 2.706e-06, 2.874e-06, 2.351e-06,
+      5.878e-06, 7.09e-06, 3.362e-06, 3.44e-06, 4.843e-06, 2.438e-06, 9.358e-14, 1.696e-06,
+      1.43e-06, 1.579e-06, 1.866e-06, 3.984e-06, 1.226e-06, 3.411e-06, 5.373e-06, 3.252e-06,
+      1.699e-06, 3.794e-06, 4.639e-06, 2.261e-06, 9.358e-14, 7.861e-06, 3.122e-06, 3.859e-06,
+      3.122e-06, 3.405e-06, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0};
   // achieved fraction of the streaming rate for the output writes (0: 1)
   static const double kWr[AC_N_CFG] = {
-      1, 1, 1, 0.5848, 0.3916, 0.4206, 1, 1,
-      1, 0.5484, 0.6664, 1, 0.9998, 1, 1, 1,
-      1, 0.05122, 0.1124, 0.3069, 0.9997, 0.5216, 0.6117, 0.55,
-      0.3295, 0.4925, 0.3626, 0.4455, 0.2271, 0.2707, 1, 0.1986,
-      0.1266, 0.486, 0.5211, 0, 0.351, 0.3014, 0.3493, 0,
-      0, 0, 0, 0, 0.9998, 1, 1, 1,
-      0.9326, 0.7661, 1, 1, 0.492, 1, 1, 1,
-      1, 1, 0.743, 1, 0.9993, 1, 1, 1,
-      0.05, 0.1972, 0.1852, 0.147, 0.08733, 0.1308, 0.06128, 0.05,
-      0.05568, 0.1786};
+      1, 1, 1, 1, 0.6885, 1, 1, 1,
+      1, 1, 1, 0.9999, 0.9998, 1, 1, 1,
+      1, 0.05476, 0.1179, 0.9999, 0.8746, 1, 0.5463, 0.6325,
+      0.2984, 0.493, 0.4437, 0.4734, 1, 1, 1, 0.171,
+      0.09067, 0.5706, 0.6075, 0, 0.425, 0.3672, 0.4155, 0,
+      0, 0, 0, 0, 0.9998, 0.9996, 0.9994, 1,
+      1, 1, 1, 1, 1, 1, 1, 1,
+      1, 1, 0.6356, 0.9992, 1, 0.9999, 1, 1,
+      0.05, 0.1836, 0.1754, 0.07925, 0.05035, 0.2436, 0.06885, 0.1301,
+      0.1035, 0.4903, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0,
+      0, 0, 0, 0, 0, 0, 0, 0};
   for (int i = 0; i < AC_N_CFG; ++i) {
     h.cfg_iter[i] = kIter[i];
     h.cfg_wg[i] = kWg[i];
