@@ -101,10 +101,20 @@ typedef enum {
                              at run time, misaligned operands run the register-load form or the
                              same tiling on AC_FAMILY_TILE. With P_k > 1 the partials are summed
                              by the reduction kernel */
-  AC_FAMILY_TALL = 10     /* N <= 32, K a multiple of 8, A row-major: A streamed from HBM once
-                             through a direct-to-LDS pipeline of 64-k stages, B's transposed
-                             copy (a prologue) beside it; misaligned A at run time runs the same
-                             product on AC_FAMILY_SKINNY_N */
+  AC_FAMILY_TALL = 10,    /* N <= 32, A row-major: A streamed from HBM once through a
+                             direct-to-LDS pipeline of 64-k stages, B's transposed copy (a
+                             prologue) beside it; K not a multiple of 8 takes the register-load
+                             form (VariantKey bit 13); misaligned A at run time runs that form,
+                             or the same product on AC_FAMILY_SKINNY_N */
+  AC_FAMILY_DL_OFFCHIP = 11 /* off-chip accumulation (the SingleCoreSplitK and HybridSplitK
+                             templates, Section 4.2, Eqs. 3 and 5): a workgroup owns a
+                             512 x 256 super-tile (two 256 x 256 tiles of AC_FAMILY_DL, whose
+                             fp32 accumulator, 512 KiB, exceeds the 256 KiB of registers) and,
+                             for each k1 slice of K in turn, computes both halves and flushes
+                             their partial sums to the workspace; the reduction kernel adds the
+                             slices. VariantKey: cfg = DL configuration | log2(workgroups along
+                             K) << 4 (0: SingleCoreSplitK, > 0: HybridSplitK), P_k = slices.
+                             Offered in the two off-chip templates and in the open search */
 } adaptcore_family;
 
 typedef struct adaptcore_plan_s adaptcore_plan_t; /* opaque, owned by the library */

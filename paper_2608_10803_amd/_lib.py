@@ -32,11 +32,11 @@ AC_LAYOUT_B_COL = 2  # B stored column-major (ldb >= K)
 AC_LAYOUT_COL_COL = 3
 AC_A_ROWMAJOR, AC_A_COLMAJOR, AC_B_ROWMAJOR, AC_B_COLMAJOR = 0, AC_LAYOUT_A_COL, 0, AC_LAYOUT_B_COL
 (AC_FAMILY_TILE, AC_FAMILY_SKINNY_M, AC_FAMILY_SKINNY_N, AC_FAMILY_STREAMK, AC_FAMILY_SMALLK, AC_FAMILY_DIRECT,
- AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED, AC_FAMILY_DL, AC_FAMILY_TALL) = range(11)
+ AC_FAMILY_GROUPED, AC_FAMILY_PERSIST, AC_FAMILY_BATCHED, AC_FAMILY_DL, AC_FAMILY_TALL, AC_FAMILY_DL_OFFCHIP) = range(12)
 
 CLASS_NAMES = ["Common", "SingleCoreSplitK", "MultiCoreSplitK", "HybridSplitK"]
 FAMILY_NAMES = ["tile", "skinny_m", "skinny_n", "streamk", "smallk", "direct", "grouped", "persist", "batched", "dl",
-                "tall"]
+                "tall", "offchip"]
 
 
 class AdaptCoreError(RuntimeError):

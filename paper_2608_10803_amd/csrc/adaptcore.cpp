@@ -396,15 +396,34 @@ adaptcore_status run_matmul(const adaptcore_plan_t* plan, const void* A, int64_t
   // form (if it has one, and the operands are row-major with K, N >= 8), else
   // the register-staged sibling of the same tiling, runs on the operands as
   // given (no padding copies).
-  ac::Plan sib;
-  const ac::Plan* run = &p;
-  bool dl = p.family == ac::FAM_DL;
-  if (dl && !p.unal) {  // (the register-load form takes any alignment)
+  // Off-chip accumulation plans load like the direct-to-LDS ones; with such
+  // operands the direct-to-LDS split-K plan of the same slices (same
+  // partials, same sum) runs instead, with its own fallbacks below.
+  ac::Plan sib, dl_base;
+  const ac::Plan* src = &p;
+  if (p.family == ac::FAM_DLSC) {
     const bool a_ok = a_col || p.ws_a_off >= 0 || ac::dl_a_aligned(A, lda, K);
     const bool b_ok = b_col || p.ws_b_off >= 0 || ac::dl_b_aligned(B, ldb, N);
     if (!(a_ok && b_ok)) {
-      sib = p;
-      const ac::DlCfg& d = ac::kDlCfg[p.cfg];
+      adaptcore_hw_t hw;
+      {
+        std::lock_guard<std::mutex> lk(g_mu);
+        hw = g_hw;
+      }
+      const uint64_t key = ac::make_variant_key(ac::FAM_DL, p.cfg & 0xF, 0, p.pk, p.s.dtype, (int)p.s.layouts);
+      if (!ac::plan_for_key(p.s, hw, key, &dl_base))
+        return fail(AC_ERR_UNSUPPORTED, "operands not aligned for this plan and no fallback applies");
+      src = &dl_base;
+    }
+  }
+  const ac::Plan* run = src;
+  bool dl = src->family == ac::FAM_DL || src->family == ac::FAM_DLSC;
+  if (src->family == ac::FAM_DL && !src->unal) {  // (the register-load form takes any alignment)
+    const bool a_ok = a_col || src->ws_a_off >= 0 || ac::dl_a_aligned(A, lda, K);
+    const bool b_ok = b_col || src->ws_b_off >= 0 || ac::dl_b_aligned(B, ldb, N);
+    if (!(a_ok && b_ok)) {
+      sib = *src;
+      const ac::DlCfg& d = ac::kDlCfg[src->cfg];
       // (column-major operands reach the kernel as aligned row-major copies)
       if (d.unal && K >= 8 && N >= 8) {
         sib.unal = 1;

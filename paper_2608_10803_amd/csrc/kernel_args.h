@@ -24,7 +24,8 @@ enum Family : int {
   FAM_BATCHED = 8,   // the grouped kernel over a strided batch (every group the same shape)
   FAM_DL = 9,        // tile kernel with operand tiles loaded straight into LDS (multi-stage)
   FAM_TALL = 10,     // N <= 32: A streamed once through a direct-to-LDS pipeline, B^T beside it
-  FAM_COUNT = 11
+  FAM_DLSC = 11,     // off-chip accumulation: a workgroup's 2-tile super-tile, partials flushed per k1 slice
+  FAM_COUNT = 12
 };
 
 // Arguments of every GEMM kernel. A is M x K row-major (lda), B is K x N

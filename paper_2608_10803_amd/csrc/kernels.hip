@@ -2260,6 +2260,12 @@ hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st) {
       if (e != hipSuccess || p.pk == 1) return e;
       return launch_reduce(g, st, obf);
     }
+    case FAM_DLSC: {
+      // every slice's partials, then the reduction over the slices
+      const hipError_t e = (launch_dl_sc_main)(p, g, st);
+      if (e != hipSuccess) return e;
+      return launch_reduce(g, st, obf);
+    }
   }
   return hipErrorInvalidValue;
 }

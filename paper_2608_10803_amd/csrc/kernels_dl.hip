@@ -380,8 +380,10 @@ __device__ __forceinline__ void compute_stage(const char* sA, const char* sB, f3
   if constexpr (std::is_same<Loads, RegLoads<G>>::value) nxt.finish();  // registers -> the next stage
 }
 
+// One output tile (tile coordinates tm, tn) over K partition `split` of the
+// plan's kper-block partitions.
 template <int BM, int BN, int BK, int S, int OUT, bool RG>
-__device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
+__device__ __forceinline__ void dl_tile(const GemmArgs& g, int tm, int tn, int split) {
   typedef Dl<BM, BN, BK, S> G;
   typedef typename std::conditional<RG, DlTileU<G>, DlTile<G>>::type Tile;
   typedef typename std::conditional<RG, RegLoads<G>, StageLoads<G>>::type Loads;
@@ -397,15 +399,9 @@ __device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
   __shared__ __attribute__((aligned(1024))) char lB4[G::B_BYTES];
   static_assert(S >= 2 && S <= 5, "stages");
 
-  const int ntiles = g.tiles_m * g.tiles_n;
-  int tile = blockIdx.x;
-  if (g.swizzle) tile = xcd_remap(tile, ntiles);
-  int tm, tn;
-  tile_coords(tile, g.tiles_m, g.tiles_n, g.swizzle, tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
-  // this workgroup's K partition: kper blocks of the plan's 64-deep granule,
-  // a whole number of this kernel's k-blocks
-  const int split = blockIdx.y;
+  // the K partition: kper blocks of the plan's 64-deep granule, a whole
+  // number of this kernel's k-blocks
   const int64_t kbeg = min((int64_t)split * g.kper * 64, g.K);
   const int64_t kend = min(kbeg + (int64_t)g.kper * 64, g.K);
   const int nk = (int)((kend - kbeg + G::BK - 1) / G::BK);
@@ -552,6 +548,18 @@ __device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
   }
 }
 
+// a workgroup per output tile (blockIdx.x, in the plan's tile order) and K
+// partition (blockIdx.y)
+template <int BM, int BN, int BK, int S, int OUT, bool RG>
+__device__ __forceinline__ void dl_kernel(const GemmArgs& g) {
+  const int ntiles = g.tiles_m * g.tiles_n;
+  int tile = blockIdx.x;
+  if (g.swizzle) tile = xcd_remap(tile, ntiles);
+  int tm, tn;
+  tile_coords(tile, g.tiles_m, g.tiles_n, g.swizzle, tm, tn);
+  dl_tile<BM, BN, BK, S, OUT, RG>(g, tm, tn, (int)blockIdx.y);
+}
+
 // the kernels: operand tiles loaded straight into LDS (k_dl), or through
 // registers at any alignment (k_dlu)
 template <int BM, int BN, int BK, int S, int OUT>
@@ -563,6 +571,39 @@ template <int BM, int BN, int BK, int S, int OUT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Dl<BM, BN, BK, S>::WPE, Dl<BM, BN, BK, S>::WPE)))
 void k_dlu(GemmArgs g) {
   dl_kernel<BM, BN, BK, S, OUT, true>(g);
+}
+
+// Off-chip accumulation (the SingleCoreSplitK and HybridSplitK templates of
+// Section 4.2; write volume of Eqs. 3 and 5): a workgroup owns a super-tile
+// of two vertically adjacent tiles, 2BM x BN, whose fp32 accumulator does not
+// fit the registers, and takes the plan's P_k k1-slices of K in order --
+// all of them (gridDim.y = 1: SingleCoreSplitK) or its share of them
+// (gridDim.y workgroups along K: HybridSplitK). For every slice it computes
+// the upper tile, flushes its partial sums to the slice's fp32 partial buffer
+// in the workspace, then the lower tile (whose B slice the upper one has just
+// brought into the L2); the reduction kernel then adds the slices. Each tile
+// of each slice is the direct-to-LDS tile kernel's own computation of that
+// partition, so the result has the bits of the split-K plan with the same
+// partitions.
+template <int BM, int BN, int BK, int S>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Dl<BM, BN, BK, S>::WPE, Dl<BM, BN, BK, S>::WPE)))
+void k_dl_sc(GemmArgs g) {
+  const int sup = blockIdx.x;
+  const int stm = sup / g.tiles_n, tn = sup - stm * g.tiles_n;
+  const int per = g.pk / (int)gridDim.y;  // slices of this workgroup
+  for (int q = 0; q < per; ++q) {
+    const int split = (int)blockIdx.y * per + q;
+#pragma unroll 1
+    for (int h = 0; h < 2; ++h) {
+      const int tm = 2 * stm + h;
+      if (tm >= g.tiles_m) break;
+      // the previous tile's loads and stores are complete and no wave still
+      // reads its LDS stages
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+      __syncthreads();
+      dl_tile<BM, BN, BK, S, DL_PARTIAL, false>(g, tm, tn, split);
+    }
+  }
 }
 
 template <int BM, int BN, int BK, int S>
@@ -636,7 +677,24 @@ constexpr bool dl_occ_match() {
 }
 static_assert(dl_occ_match(), "the table's workgroups per CU must be those the kernels are built for");
 
+// the off-chip accumulation kernels: super-tiles of the 256 x 256 tiles
+// (DL configurations 0 and 4), whose 512 KiB fp32 accumulator exceeds the
+// registers
+template <int BM, int BN, int BK, int S>
+hipError_t launch_dl_sc(const Plan& p, const GemmArgs& g, hipStream_t st) {
+  hipLaunchKernelGGL((k_dl_sc<BM, BN, BK, S>), dim3(p.grid_x, p.grid_y), dim3(256), 0, st, g);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_dl_sc_main(const Plan& p, const GemmArgs& g, hipStream_t st) {
+  const int cfg = p.cfg & 0xF, kc = 1 << (p.cfg >> 4);
+  if (p.family != FAM_DLSC || (cfg != 0 && cfg != 4) || p.grid_y != kc || p.pk < 2 || p.pk % kc != 0 ||
+      g.pk != p.pk || (int64_t)p.grid_x != (int64_t)((g.tiles_m + 1) / 2) * g.tiles_n || !ac::dl_operands_aligned(g))
+    return hipErrorInvalidValue;
+  return cfg == 0 ? launch_dl_sc<256, 256, 64, 2>(p, g, st) : launch_dl_sc<256, 256, 32, 4>(p, g, st);
+}
 
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st) {
   if (p.family != FAM_DL || p.cfg < 0 || p.cfg >= N_DL_CFG) return hipErrorInvalidValue;

@@ -40,6 +40,8 @@ int table_occ(int family, int cfg) {
       return kDlCfg[cfg].occ;
     case FAM_TALL:
       return kTallCfg[cfg].occ;
+    case FAM_DLSC:
+      return kDlCfg[cfg & 0xF].occ;
   }
   return 1;
 }
@@ -181,6 +183,9 @@ struct Ctx {
   bool unaligned;
 };
 
+// bytes of B (K x N, 16-bit)
+inline double s_bytes_b(const Ctx& c) { return 2.0 * (double)c.s.K * (double)c.s.N; }
+
 // The output tiling shared by the tile kernels and the direct-to-LDS
 // kernels: bm x bn tiles, P_k partitions of whole 64-deep k-blocks, four
 // waves in wm x wn, each wave's part of the tile in ms x ms MFMA blocks.
@@ -305,6 +310,36 @@ bool build_dl(const Ctx& c, int cfg, int pk_req, int swizzle, int unal, Plan* p,
   w->lds_it = (double)(d.bm * (1 + 4 / wm) + d.bn * (1 + wm)) * TILE_BK * 2;
   w->prefetch = (double)(d.stages - 1) * d.bk / TILE_BK;
   w->unaligned = false;
+  return true;
+}
+
+// Off-chip accumulation (SingleCoreSplitK / HybridSplitK, Section 4.2): the
+// super-tile of two vertically adjacent 256 x 256 tiles of DL configuration
+// `key_cfg & 0xF` (0 or 4), whose fp32 accumulator (512 KiB) exceeds S_acc;
+// the P_k k1-slices of K are taken by kc = 1 << (key_cfg >> 4) workgroups
+// along K (kc = 1: SingleCoreSplitK), each flushing its tiles' partial sums
+// after every slice (write volume 4 MN P_k + 2 MN, Eqs. 3 and 5), then the
+// reduction kernel adds the slices. The tiling, partial workspace and padding
+// prologue are those of the direct-to-LDS split-K plan with the same slices.
+bool build_dlsc(const Ctx& c, int key_cfg, int pk_req, Plan* p, Work* w) {
+  const int cfg = key_cfg & 0xF, kcl = key_cfg >> 4;
+  if ((cfg != 0 && cfg != 4) || kcl > 10 || pk_req < 2) return false;
+  const int kc = 1 << kcl;
+  if (pk_req % kc != 0 || pk_req / kc < 2) return false;  // at least two slices per workgroup
+  if (!build_dl(c, cfg, pk_req, 0, 0, p, w)) return false;
+  const int64_t tm = p->pm, tn = p->pn, sup_m = cdiv(tm, 2);
+  if (sup_m * tn > (1LL << 31) - 1) return false;
+  const double per = (double)(pk_req / kc) * (tm > 1 ? 2.0 : 1.0);  // tiles x slices of a workgroup
+  p->family = FAM_DLSC;
+  p->cfg = key_cfg;
+  p->grid_x = (int)(sup_m * tn);
+  p->grid_y = kc;
+  w->units = sup_m * tn * kc;
+  w->L *= per;
+  w->out_unit *= per;
+  // B's slice is read from HBM once per super-tile (the lower tile finds it
+  // in the L2), A's rows once per column of super-tiles
+  w->total_read -= (double)(tm - sup_m) * (double)s_bytes_b(c);
   return true;
 }
 
@@ -663,13 +698,13 @@ void add_prologue(const Shape& s, const adaptcore_hw_t& hw, Plan* p) {
   if (s.layouts & AC_LAYOUT_A_COL) copy(s.M, s.K, &p->ws_a_off);
   // the padding prologue of the direct-to-LDS kernels: a row-major operand
   // whose rows are not whole 16-byte chunks is copied zero-padded
-  else if (p->family == FAM_DL && !p->unal && (s.K % 8) != 0) copy(s.M, s.K, &p->ws_a_off);
+  else if ((p->family == FAM_DL || p->family == FAM_DLSC) && !p->unal && (s.K % 8) != 0) copy(s.M, s.K, &p->ws_a_off);
   // the small-M kernel reads a column-major B in place (its MFMA fragments
   // are runs of k), so only the other families copy B; the tall-skinny
   // kernel reads B's transposed copy (N x K, rows padded to 8) in any case
   if (p->family == FAM_TALL) copy(s.N, s.K, &p->ws_b_off);
   else if ((s.layouts & AC_LAYOUT_B_COL) && p->family != FAM_SKINNY_M) copy(s.K, s.N, &p->ws_b_off);
-  else if (!(s.layouts & AC_LAYOUT_B_COL) && p->family == FAM_DL && !p->unal && (s.N % 8) != 0)
+  else if (!(s.layouts & AC_LAYOUT_B_COL) && (p->family == FAM_DL || p->family == FAM_DLSC) && !p->unal && (s.N % 8) != 0)
     copy(s.K, s.N, &p->ws_b_off);
   p->predicted += p->t_pro;
 }
@@ -822,6 +857,10 @@ void set_runtime_occupancy(int family, int cfg, int occ) {
 }
 
 int occupancy(int family, int cfg) {
+  if (family == FAM_DLSC) {  // the direct-to-LDS configuration's kernel, looping
+    family = FAM_DL;
+    cfg &= 0xF;
+  }
   const int o = g_occ[family][cfg].load(std::memory_order_relaxed);
   return o > 0 ? o : table_occ(family, cfg);
 }
@@ -920,6 +959,25 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
       }
     }
   }
+  // off-chip accumulation: super-tiles of the 256 x 256 direct-to-LDS tiles
+  // with 2 to 32 k1-slices, taken by 1 (SingleCoreSplitK) or more
+  // (HybridSplitK) workgroups along K; the class-fixed search keeps them for
+  // the two off-chip templates only (enumerate)
+  for (int cfg : {0, 4}) {
+    const DlCfg& d = kDlCfg[cfg];
+    if (!calibrated(IDX_DL + cfg) || d.bm > 2 * s.M || d.bn > 2 * s.N) continue;
+    const int64_t kt = cdiv(s.K, TILE_BK), sup = cdiv(cdiv(s.M, d.bm), 2) * cdiv(s.N, d.bn);
+    for (int pk : kSplits) {
+      if (pk > 32 || pk > kt) break;
+      for (int kcl = 0; (1 << kcl) <= pk / 2; ++kcl) {
+        if (pk % (1 << kcl) != 0) continue;
+        if ((int64_t)(1 << kcl) * sup > 8LL * c.hw.n_cu * d.occ) break;
+        Plan p;
+        Work w;
+        if (build_dlsc(c, cfg | (kcl << 4), pk, &p, &w)) add(p, w);
+      }
+    }
+  }
   // tall-skinny streaming kernels: in the class-fixed search once calibrated
   for (int cfg = 0; cfg < N_TALL_CFG; ++cfg) {
     const int un = (s.K % 8) != 0;  // the form this K takes
@@ -1013,8 +1071,12 @@ std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_o
     // keeps its split variants even when the taxonomy's base tile fills the
     // GPU.
     const bool ksplit = cls == AC_CLASS_MULTI_CORE_SPLITK || cls == AC_CLASS_HYBRID_SPLITK;
+    const bool offchip = cls == AC_CLASS_SINGLE_CORE_SPLITK || cls == AC_CLASS_HYBRID_SPLITK;
     for (const Plan& p : all) {
-      const bool pk_split = p.family == FAM_STREAMK ? true : p.pk > 1;
+      // off-chip accumulation only in its templates; its K is split across
+      // workgroups only in HybridSplitK (SingleCoreSplitK keeps k = K)
+      if (p.family == FAM_DLSC && !offchip) continue;
+      const bool pk_split = p.family == FAM_STREAMK ? true : p.family == FAM_DLSC ? p.grid_y > 1 : p.pk > 1;
       const bool tile_idle = p.tile_m > 0 && p.tile_n > 0 &&
                              cdiv(s.M, p.tile_m) * cdiv(s.N, p.tile_n) < (int64_t)hw.n_cu;
       if (ksplit || tile_idle || !pk_split) sel.push_back(p);
@@ -1068,6 +1130,9 @@ bool plan_for_key(const Shape& s, const adaptcore_hw_t& hw, uint64_t key, Plan* 
       break;
     case FAM_TALL:
       ok = sw == 0 && pk >= 1 && build_tall(c, cfg, pk, vk_unal(key), &p, &w);
+      break;
+    case FAM_DLSC:
+      ok = sw == 0 && vk_unal(key) == 0 && build_dlsc(c, cfg, pk, &p, &w);
       break;
   }
   if (!ok || !finish(c, &p, w)) return false;
@@ -1274,6 +1339,11 @@ static std::string kernel_names_fmt(const Plan& p) {
       if (p.pk > 1) r += std::string(";k_reduce<") + b + ">";
       return r;
     }
+    case FAM_DLSC: {
+      const DlCfg& d = kDlCfg[p.cfg & 0xF];
+      std::snprintf(buf, sizeof buf, "k_dl_sc<%d, %d, %d, %d>", d.bm, d.bn, d.bk, d.stages);
+      return std::string(buf) + ";k_reduce<" + b + ">";
+    }
     case FAM_TALL: {
       const TallCfg& t = kTallCfg[p.cfg];
       std::snprintf(buf, sizeof buf, "%s<%d, %d, %d, %d>", p.unal ? "k_tallu" : "k_tall", t.nt, t.bm, t.stages,
@@ -1314,6 +1384,8 @@ int config_index(int family, int cfg) {
         return c < N_TALL_CFG && kTallCfg[c].unal ? tallu_index(c) : -1;
       }
       return cfg >= 0 && cfg < N_TALL_CFG ? IDX_TALL + cfg : -1;
+    case FAM_DLSC:  // the direct-to-LDS configuration's costs (the same tile code)
+      return ((cfg & 0xF) == 0 || (cfg & 0xF) == 4) && (cfg >> 4) <= 10 ? IDX_DL + (cfg & 0xF) : -1;
     case FAM_BATCHED:
     case FAM_GROUPED:  // the tile kernel's costs
       return cfg >= 0 && cfg < N_TILE_CFG && kGroupedCfg[cfg] ? IDX_TILE + cfg : -1;

@@ -24,6 +24,7 @@ bool dl_b_aligned(const void* B, int64_t ldb, int64_t nB);
 hipError_t launch_pad16(const uint16_t* src, int64_t ld_src, int64_t rows, int64_t cols, uint16_t* dst,
                         int64_t ld_dst, hipStream_t st);
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
+hipError_t launch_dl_sc_main(const Plan& p, const GemmArgs& g, hipStream_t st);
 void query_occupancy_dl();
 // Tall-skinny streaming kernel (kernels_tall.hip): A's alignment (16-byte
 // aligned rows of K, K a multiple of 8, lda below DL_MAX_LD), the operands'
@@ -50,6 +51,7 @@ hipError_t launch_read_probe(const void* buf, int64_t bytes, void* sink, hipStre
 namespace f16 {
 hipError_t launch_plan(const Plan& p, const GemmArgs& g, hipStream_t st);
 hipError_t launch_dl_main(const Plan& p, const GemmArgs& g, hipStream_t st);
+hipError_t launch_dl_sc_main(const Plan& p, const GemmArgs& g, hipStream_t st);
 void query_occupancy_dl();
 hipError_t launch_tall_main(const Plan& p, const GemmArgs& g, hipStream_t st);
 void query_occupancy_tall();

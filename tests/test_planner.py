@@ -375,3 +375,52 @@ def test_set_override_is_thread_local_and_leaves_the_cache():
     assert all(o == 0 and h == chosen for o, h in seen_other_thread)
     assert ac.adaptcore_plan(*s) == chosen
     assert ac.adaptcore_stats()["entries"] == entries
+
+
+def _with_hw(**fields):
+    hw = ac.adaptcore_get_hw()
+    h = ac.adaptcore_get_hw()
+    for k, v in fields.items():
+        setattr(h, k, v)
+    ac.adaptcore_set_hw(h)
+    return hw
+
+
+def test_offchip_templates_and_their_candidates():
+    """Off-chip accumulation (SingleCoreSplitK / HybridSplitK): with the
+    default capacities no menu tile overflows the registers, so the class
+    search never offers it (the open search does); with a smaller
+    accumulator capacity the templates arise, SingleCoreSplitK keeps k = K
+    per workgroup (one workgroup along K) and HybridSplitK also splits K
+    across workgroups. Write volume (Eqs. 3 and 5): P_k fp32 partial slices of
+    M x N in the workspace, then one output write by the reduction."""
+    BF = ac.AC_BF16_BF16OUT
+    s = (8192, 8192, 2048)
+    assert not [c for c in ac.adaptcore_candidates(*s, BF, 0) if c["family_name"] == "offchip"]
+    hw = _with_hw(search_open=1)
+    try:
+        assert [c for c in ac.adaptcore_candidates(*s, BF, 0) if c["family_name"] == "offchip"]
+    finally:
+        ac.adaptcore_set_hw(hw)
+    hw = _with_hw(s_acc_bytes=128 * 1024)
+    try:
+        plan = ac.adaptcore_plan_info(ac.adaptcore_plan_variant(*s, BF, 0, ac.adaptcore_candidates(*s, BF, 0)[0]
+                                                                ["variant_key"]))
+        assert plan["cls_name"] == "SingleCoreSplitK"
+        off = [c for c in ac.adaptcore_candidates(*s, BF, 0) if c["family_name"] == "offchip"]
+        assert off and all(c["grid_y"] == 1 and c["pk"] >= 2 for c in off)
+        for c in off:
+            d = ac.adaptcore_plan_info(ac.adaptcore_plan_variant(*s, BF, 0, c["variant_key"]))
+            assert d["workspace_bytes"] == d["pk"] * s[0] * s[1] * 4
+            assert d["grid_x"] == (-(-s[0] // 256) + 1) // 2 * -(-s[1] // 256)
+    finally:
+        ac.adaptcore_set_hw(hw)
+    hw = _with_hw(s_acc_bytes=32 * 1024)
+    try:
+        s = (512, 512, 65536)
+        cands = ac.adaptcore_candidates(*s, BF, 0)
+        assert cands[0]["cls"] == 3  # HybridSplitK
+        off = [c for c in cands if c["family_name"] == "offchip"]
+        assert any(c["grid_y"] > 1 for c in off) and all(c["pk"] % c["grid_y"] == 0 for c in off)
+    finally:
+        ac.adaptcore_set_hw(hw)
