@@ -423,6 +423,9 @@ def ablation_main(args):
         and with its register-load form instead, deeper LDS pipeline,
         split-K; the persistent kernel with next-tile preloading, stream-K;
         then the best measured configuration and the model's pick;
+      * off-chip accumulation (SingleCoreSplitK / HybridSplitK super-tiles)
+        on the worked cases of Section 4.3 and the ablation shape, beside the
+        default plan;
       * CU scaling on 3 x 256 x 87087: the MultiCoreSplitK kernel (small-M
         kernel, K split P_k ways) with P_k = c workgroups, i.e. c CUs busy."""
     import torch
@@ -494,6 +497,33 @@ def ablation_main(args):
                  "pred_us": round(ac.adaptcore_plan_info(pick)["predicted_s"] * 1e6, 1)})
     out["module_ablation"] = {"shape": [M, N, K], "t_floor_us": round(tf * 1e6, 2),
                               "bound": "mfma" if F / Bb >= PEAK_FLOPS / PEAK_BW else "hbm", "rows": rows}
+
+    # -- off-chip accumulation (the SingleCoreSplitK / HybridSplitK templates)
+    # on the paper's two worked cases of Section 4.3 and the ablation shape:
+    # the model's 8 best off-chip candidates timed beside the default plan
+    offc = []
+    h2 = hw.copy()
+    h2.search_open = 1
+    for (M, N, K) in [(4096, 4096, 1024), (256, 256, 8192), (12288, 688, 16991)]:
+        F, Bb, tf = roof(M, N, K, 2)
+        pick = ac.adaptcore_plan(M, N, K, bf)
+        tp = time_plan(ac, torch, pick, M, N, K, bf)
+        pick_kernels = ac.adaptcore_plan_kernels(pick)  # (a profile change retires the plan)
+        ac.adaptcore_set_hw(h2)
+        cands = [c for c in ac.adaptcore_candidates(M, N, K, bf, 0) if c["family_name"] == "offchip"][:8]
+        rows_o = []
+        for c in cands:
+            plan = ac.adaptcore_plan_variant(M, N, K, bf, 0, c["variant_key"])
+            t = time_plan(ac, torch, plan, M, N, K, bf, steps=3)
+            rows_o.append({"kernels": ac.adaptcore_plan_kernels(plan), "slices": c["pk"], "workgroups_along_k": c["grid_y"],
+                           "template": "SingleCoreSplitK" if c["grid_y"] == 1 else "HybridSplitK",
+                           "us": round(t * 1e6, 1), "frac": round(tf / t, 4), "pred_us": round(c["predicted_s"] * 1e6, 1)})
+        ac.adaptcore_set_hw(hw)
+        offc.append({"shape": [M, N, K], "t_floor_us": round(tf * 1e6, 2),
+                     "model_pick": {"kernels": pick_kernels, "us": round(tp * 1e6, 1),
+                                    "frac": round(tf / tp, 4)}, "offchip": rows_o})
+        print("offchip", offc[-1], file=sys.stderr, flush=True)
+    out["offchip_accumulation"] = offc
 
     # -- CU scaling
     M, N, K = 3, 256, 87087

@@ -788,7 +788,7 @@ adaptcore_hw_t default_hw() {
   // dynamic-shape, decode-style, small-MN large-K, write-bound,
   // compute-bound and tall-skinny workloads on one MI355X, each replay timed
   // after the caches were flushed (squared log error of the model over the
-  // configurations within 2x of their shape's fastest, on a seeded half of
+  // configurations within 1.5x of their shape's fastest, on a seeded half of
   // the 380 measured shapes; the other half is held out to check the
   // ranking), evaluated with the workgroups-per-CU that the device reports
   // for each kernel, which is what the planner uses at run time. The launch
@@ -796,7 +796,7 @@ adaptcore_hw_t default_hw() {
   h.t_launch = 1.9e-06;
   h.t_mem_latency = 1.216e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 3.528e+10;
+  h.l2_bw_cu = 3.529e+10;
   h.unaligned_eta = 1;
   h.l2_hit = 5.128e-33;
   h.swizzle_gain = 0.9092;
@@ -805,43 +805,43 @@ adaptcore_hw_t default_hw() {
   // 44-57 and their register-load forms 58-63, tall-skinny 64-69 and their
   // register-load forms 70-73; 0 = analytic estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
-      3.113e-06, 2.304e-06, 1.952e-06, 1.041e-06, 9.358e-14, 7.837e-07, 5.585e-07, 3.664e-07,
-      1.154e-06, 9.358e-14, 9.358e-14, 1.087e-06, 1.289e-06, 1.161e-06, 1.321e-06, 1.62e-06,
-      1.074e-06, 6.368e-07, 5.896e-07, 6.08e-07, 5.642e-08, 9.358e-14, 3.423e-06, 2.178e-06,
-      1.944e-06, 9.358e-14, 8.634e-07, 1.01e-06, 7.001e-13, 5.216e-07, 5.243e-07, 9.358e-14,
-      5.85e-07, 2.812e-06, 2.04e-06, 0, 9.358e-14, 9.358e-14, 7.369e-07, 0,
-      0, 0, 0, 0, 2.31e-06, 1.311e-06, 1.316e-06, 1.364e-08,
-      2.257e-06, 2.266e-06, 3.156e-07, 2.823e-07, 9.358e-14, 9.358e-14, 8.97e-07, 2.247e-09,
-      5.594e-07, 9.358e-14, 1.7e-06, 9.358e-14, 6.681e-07, 1.751e-06, 1.706e-06, 7.754e-07,
-      4.053e-07, 5.859e-09, 6.636e-08, 2.444e-07, 9.358e-14, 9.358e-14, 7.328e-07, 7.249e-07,
-      4.041e-07, 8.273e-07, 0, 0, 0, 0, 0, 0,
+      3.121e-06, 2.398e-06, 2.005e-06, 1.055e-06, 9.358e-14, 7.856e-07, 6.264e-07, 3.795e-07,
+      1.22e-06, 9.358e-14, 9.358e-14, 1.105e-06, 1.339e-06, 1.44e-06, 1.345e-06, 1.546e-06,
+      7.293e-07, 5.271e-07, 5.172e-07, 6.181e-07, 5.559e-08, 9.358e-14, 2.409e-06, 9.358e-14,
+      1.935e-06, 9.358e-14, 1.526e-06, 1.329e-06, 9.358e-14, 5.343e-07, 5.275e-07, 6.703e-07,
+      1.942e-07, 2.773e-06, 2.027e-06, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
+      0, 0, 0, 0, 2.271e-06, 1.317e-06, 1.282e-06, 1.011e-08,
+      2.255e-06, 2.187e-06, 2.218e-07, 1.889e-07, 9.358e-14, 9.358e-14, 9.358e-14, 2.837e-09,
+      4.378e-07, 5.173e-07, 1.703e-06, 9.358e-14, 4.242e-07, 1.773e-06, 1.773e-06, 7.562e-07,
+      9.358e-14, 2.714e-13, 2.532e-13, 2.592e-07, 7.958e-07, 2.764e-13, 7.332e-07, 7.197e-07,
+      3.971e-07, 8.296e-07, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      2.781e-06, 1.275e-06, 3.272e-06, 1.962e-06, 2.365e-06, 6.991e-07, 1.433e-06, 1.166e-06,
-      2.684e-06, 2.719e-06, 2.81e-06, 1.519e-06, 1.383e-06, 2.846e-06, 4.792e-06, 3.69e-06,
-      1.848e-05, 1.935e-06, 2.827e-06, 8.367e-06, 3.002e-06, 9.358e-14, 9.358e-14, 9.358e-14,
-      9.358e-14, 9.358e-14, 9.358e-14, 9.358e-14, 1.037e-05, 3.348e-06, 3.769e-07, 1.525e-06,
-      2.801e-08, 9.358e-14, 1.031e-07, 0, 9.358e-14, 9.358e-14, 5.737e-07, 0,
-      0, 0, 0, 0, 6.044e-06, 2.706e-06, 2.874e-06, 2.351e-06,
-      5.878e-06, 7.09e-06, 3.362e-06, 3.44e-06, 4.843e-06, 2.438e-06, 9.358e-14, 1.696e-06,
-      1.43e-06, 1.579e-06, 1.866e-06, 3.984e-06, 1.226e-06, 3.411e-06, 5.373e-06, 3.252e-06,
-      1.699e-06, 3.794e-06, 4.639e-06, 2.261e-06, 9.358e-14, 7.861e-06, 3.122e-06, 3.859e-06,
-      3.122e-06, 3.405e-06, 0, 0, 0, 0, 0, 0,
+      2.704e-06, 1.248e-06, 4.969e-06, 1.957e-06, 2.325e-06, 7.621e-07, 1.596e-06, 1.176e-06,
+      3.07e-06, 2.749e-06, 3.132e-06, 1.576e-06, 6.747e-07, 9.358e-14, 4.817e-06, 6.022e-06,
+      1.492e-05, 3.416e-06, 5.886e-06, 8.492e-06, 3.016e-06, 9.358e-14, 5.336e-05, 9.358e-14,
+      7.779e-10, 9.358e-14, 1.389e-06, 1.031e-06, 9.358e-14, 4.344e-06, 5.098e-07, 9.358e-14,
+      1.049e-09, 9.358e-14, 1.015e-06, 0, 9.358e-14, 9.358e-14, 2.478e-06, 0,
+      0, 0, 0, 0, 5.156e-06, 2.636e-06, 3.046e-06, 1.702e-06,
+      4.98e-06, 7.97e-06, 3.207e-06, 3.348e-06, 4.19e-06, 2.221e-06, 1.485e-06, 2.563e-06,
+      5.112e-07, 1.093e-06, 2.63e-06, 3.979e-06, 1.666e-06, 3.696e-06, 6.181e-06, 3.168e-06,
+      4.377e-06, 4.86e-06, 5.723e-06, 2.721e-06, 2.079e-06, 1.039e-05, 3.978e-06, 4.933e-06,
+      3.703e-06, 2.346e-06, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   // achieved fraction of the streaming rate for the output writes (0: 1)
   static const double kWr[AC_N_CFG] = {
-      1, 1, 1, 1, 0.6885, 1, 1, 1,
-      1, 1, 1, 0.9999, 0.9998, 1, 1, 1,
-      1, 0.05476, 0.1179, 0.9999, 0.8746, 1, 0.5463, 0.6325,
-      0.2984, 0.493, 0.4437, 0.4734, 1, 1, 1, 0.171,
-      0.09067, 0.5706, 0.6075, 0, 0.425, 0.3672, 0.4155, 0,
-      0, 0, 0, 0, 0.9998, 0.9996, 0.9994, 1,
+      1, 1, 1, 1, 0.6662, 1, 1, 1,
+      1, 0.6654, 0.6664, 0.9999, 0.9998, 1, 1, 1,
+      1, 0.05755, 1, 0.9999, 0.8759, 1, 1, 0.6346,
+      0.2985, 0.5709, 1, 0.7509, 0.07753, 1, 1, 0.151,
+      0.06691, 0.5667, 0.6535, 0, 0.4715, 0.399, 0.4581, 0,
+      0, 0, 0, 0, 0.9998, 0.9996, 0.9993, 1,
       1, 1, 1, 1, 1, 1, 1, 1,
-      1, 1, 0.6356, 0.9992, 1, 0.9999, 1, 1,
-      0.05, 0.1836, 0.1754, 0.07925, 0.05035, 0.2436, 0.06885, 0.1301,
-      0.1035, 0.4903, 0, 0, 0, 0, 0, 0,
+      1, 1, 1, 0.9977, 1, 0.9999, 1, 1,
+      0.1876, 1, 1, 0.08185, 1, 1, 0.1286, 1,
+      1, 0.1727, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   for (int i = 0; i < AC_N_CFG; ++i) {
