@@ -653,7 +653,7 @@ typedef hipError_t (*DlLaunchFn)(const Plan&, const GemmArgs&, hipStream_t, bool
 typedef int (*DlOccFn)();
 #define DL_CFGS(X) X(256, 256, 64, 2), X(256, 128, 64, 3), X(128, 256, 64, 3), X(128, 128, 64, 3), X(256, 256, 32, 4), \
     X(256, 256, 32, 5), X(256, 128, 32, 4), X(128, 256, 32, 4), X(256, 128, 32, 2), X(128, 128, 64, 2),       \
-    X(128, 128, 32, 2), X(32, 256, 64, 4), X(64, 256, 64, 4), X(32, 128, 64, 4)
+    X(128, 128, 32, 2), X(32, 256, 64, 4), X(64, 256, 64, 4), X(32, 128, 64, 4), X(64, 512, 32, 2)
 #define DL_L(a, b, c, d) &launch_dl<a, b, c, d>
 #define DL_O(a, b, c, d) &occ_dl<a, b, c, d>
 #define DL_C(a, b, c, d) {a, b, c, d}

@@ -802,8 +802,8 @@ adaptcore_hw_t default_hw() {
   h.swizzle_gain = 0.9092;
   // per configuration (tile 0-10, skinny-M 11-16, skinny-N 17-19, small-K
   // 20-21, stream-K 22-29, direct 30-32, persistent 33-43, direct-to-LDS
-  // 44-57 and their register-load forms 58-63, tall-skinny 64-69 and their
-  // register-load forms 70-73; 0 = analytic estimate, no timing data)
+  // 44-58 and their register-load forms 59-65, tall-skinny 66-71 and their
+  // register-load forms 72-75; 0 = analytic estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
       3.121e-06, 2.398e-06, 2.005e-06, 1.055e-06, 9.358e-14, 7.856e-07, 6.264e-07, 3.795e-07,
       1.22e-06, 9.358e-14, 9.358e-14, 1.105e-06, 1.339e-06, 1.44e-06, 1.345e-06, 1.546e-06,
@@ -812,9 +812,9 @@ adaptcore_hw_t default_hw() {
       1.942e-07, 2.773e-06, 2.027e-06, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
       0, 0, 0, 0, 2.271e-06, 1.317e-06, 1.282e-06, 1.011e-08,
       2.255e-06, 2.187e-06, 2.218e-07, 1.889e-07, 9.358e-14, 9.358e-14, 9.358e-14, 2.837e-09,
-      4.378e-07, 5.173e-07, 1.703e-06, 9.358e-14, 4.242e-07, 1.773e-06, 1.773e-06, 7.562e-07,
-      9.358e-14, 2.714e-13, 2.532e-13, 2.592e-07, 7.958e-07, 2.764e-13, 7.332e-07, 7.197e-07,
-      3.971e-07, 8.296e-07, 0, 0, 0, 0, 0, 0,
+      4.378e-07, 5.173e-07, 0, 1.703e-06, 9.358e-14, 4.242e-07, 1.773e-06, 1.773e-06,
+      7.562e-07, 0, 9.358e-14, 2.714e-13, 2.532e-13, 2.592e-07, 7.958e-07, 2.764e-13,
+      7.332e-07, 7.197e-07, 3.971e-07, 8.296e-07, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
@@ -825,9 +825,9 @@ adaptcore_hw_t default_hw() {
       1.049e-09, 9.358e-14, 1.015e-06, 0, 9.358e-14, 9.358e-14, 2.478e-06, 0,
       0, 0, 0, 0, 5.156e-06, 2.636e-06, 3.046e-06, 1.702e-06,
       4.98e-06, 7.97e-06, 3.207e-06, 3.348e-06, 4.19e-06, 2.221e-06, 1.485e-06, 2.563e-06,
-      5.112e-07, 1.093e-06, 2.63e-06, 3.979e-06, 1.666e-06, 3.696e-06, 6.181e-06, 3.168e-06,
-      4.377e-06, 4.86e-06, 5.723e-06, 2.721e-06, 2.079e-06, 1.039e-05, 3.978e-06, 4.933e-06,
-      3.703e-06, 2.346e-06, 0, 0, 0, 0, 0, 0,
+      5.112e-07, 1.093e-06, 0, 2.63e-06, 3.979e-06, 1.666e-06, 3.696e-06, 6.181e-06,
+      3.168e-06, 0, 4.377e-06, 4.86e-06, 5.723e-06, 2.721e-06, 2.079e-06, 1.039e-05,
+      3.978e-06, 4.933e-06, 3.703e-06, 2.346e-06, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   // achieved fraction of the streaming rate for the output writes (0: 1)
@@ -839,9 +839,9 @@ adaptcore_hw_t default_hw() {
       0.06691, 0.5667, 0.6535, 0, 0.4715, 0.399, 0.4581, 0,
       0, 0, 0, 0, 0.9998, 0.9996, 0.9993, 1,
       1, 1, 1, 1, 1, 1, 1, 1,
-      1, 1, 1, 0.9977, 1, 0.9999, 1, 1,
-      0.1876, 1, 1, 0.08185, 1, 1, 0.1286, 1,
-      1, 0.1727, 0, 0, 0, 0, 0, 0,
+      1, 1, 0, 1, 0.9977, 1, 0.9999, 1,
+      1, 0, 0.1876, 1, 1, 0.08185, 1, 1,
+      0.1286, 1, 1, 0.1727, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   for (int i = 0; i < AC_N_CFG; ++i) {

@@ -104,7 +104,10 @@ constexpr DlCfg kDlCfg[] = {{256, 256, 64, 2, 0, 1, 0}, {256, 128, 64, 3, 1, 1, 
                             // decode-style (few rows): 4 waves side by side along N, B streamed
                             // through 3-4 stages; no tile kernel has their tiling, so their
                             // register-load form is the fallback for unaligned operands
-                            {32, 256, 64, 4, -1, 1, 1}, {64, 256, 64, 4, -1, 1, 1}, {32, 128, 64, 4, -1, 2, 1}};
+                            {32, 256, 64, 4, -1, 1, 1}, {64, 256, 64, 4, -1, 1, 1}, {32, 128, 64, 4, -1, 2, 1},
+                            // a wide two-per-CU tile for write-bound shapes: 1 KB row segments of
+                            // bf16 C per tile, so fewer lines shared with the neighbouring tiles
+                            {64, 512, 32, 2, -1, 2, 1}};
 constexpr bool dl_has_unal(int bm, int bn, int bk, int stages) {
   for (const DlCfg& d : kDlCfg)
     if (d.bm == bm && d.bn == bn && d.bk == bk && d.stages == stages) return d.unal != 0;

@@ -30,7 +30,7 @@ pytestmark = pytest.mark.gpu
 
 F32, BF16 = ac.AC_BF16_F32OUT, ac.AC_BF16_BF16OUT
 F16F32, F16F16 = ac.AC_F16_F32OUT, ac.AC_F16_F16OUT
-DL_SIBLING = [0, 1, 2, 3, 0, 0, 1, 2, 1, 3, 3, -1, -1, -1]  # variants.h kDlCfg[i].sibling
+DL_SIBLING = [0, 1, 2, 3, 0, 0, 1, 2, 1, 3, 3, -1, -1, -1, -1]  # variants.h kDlCfg[i].sibling
 
 
 def note(*a):
