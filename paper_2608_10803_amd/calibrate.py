@@ -19,8 +19,8 @@ are obtained by profiling. This module
     python -m paper_2608_10803_amd.calibrate measure OUT.json   (GPU)
     python -m paper_2608_10803_amd.calibrate fit RECORDS.json [--near F]
         (after init on the GPU machine, so that the planner prices with the
-        device's occupancies; --near F fits only configurations within F
-        times their shape's fastest)
+        device's occupancies; --near F fits exactly only configurations
+        within F times their shape's fastest, the others one-sided)
     python -m paper_2608_10803_amd.calibrate emit FIT.json      (C++ defaults)
 
 `fit` holds half of the measured shapes out: the profile is fitted on a
@@ -287,7 +287,11 @@ def config_of(key):
     return ac.adaptcore_config_index(key & 0xF, cfg)
 
 
-def _log_errors(hw, meas, keys_filter=None):
+def _log_errors(hw, meas, keys_filter=None, far=None):
+    """log(predicted / measured) of every measured configuration; for the
+    (shape, key) pairs in `far` only an underestimate counts (0 otherwise):
+    a slow configuration must not look fast, but how slow it looks does not
+    matter to the ranking."""
     pred = predictions(hw, list(meas), True)
     err = []
     for sk, mt in meas.items():
@@ -296,7 +300,10 @@ def _log_errors(hw, meas, keys_filter=None):
                 continue
             p = pred[sk].get(k)
             if p:
-                err.append(math.log(p / t))
+                e = math.log(p / t)
+                if far is not None and (sk, k) in far:
+                    e = min(e, 0.0)
+                err.append(e)
     return np.array(err)
 
 
@@ -312,25 +319,28 @@ def near_records(recs, near):
 
 def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
     """Fit the profile: minimise the squared log error of the model over the
-    measured configurations (with `near`, only those within that factor of
-    their shape's fastest: the ranking depends on the model being right
-    about the competitive candidates, not about configurations many times
-    slower). Alternates a Nelder-Mead search over the global constants
+    measured configurations (with `near`, exactly only for those within that
+    factor of their shape's fastest, and for the others only where the model
+    underestimates them: the ranking depends on the model being right about
+    the competitive candidates and on no slow one looking fast, not on how
+    slow the slow ones look). Alternates a Nelder-Mead search over the global constants
     (launch, latency, bandwidth, cache hit rate) with one over the three
     constants of each kernel configuration (iteration cost, workgroup cost,
     write efficiency) on that configuration's records."""
     from scipy.optimize import minimize
     hw0 = (hw0 or ac.adaptcore_get_hw()).copy()
-    if near:
-        recs = near_records(recs, near)
     meas = _by_shape(recs)
+    far = None
+    if near:
+        kept = {((r["M"], r["N"], r["K"], r["dtype"]), r["key"]) for r in near_records(recs, near)}
+        far = {(sk, k) for sk, mt in meas.items() for k in mt if (sk, k) not in kept}
     by_cfg = {}
     for r in recs:
         by_cfg.setdefault(config_of(r["key"]), set()).add(r["key"])
     cur = hw0.copy()
 
     def loss_all(h):
-        e = _log_errors(h, meas)
+        e = _log_errors(h, meas, far=far)
         return float(np.mean(np.square(e)))
 
     def make_global(x, base):
@@ -363,9 +373,9 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
             def loss_cfg(x):
                 h = cur.copy()
                 put(h, x)
-                e = _log_errors(h, sub, keys)
+                e = _log_errors(h, sub, keys, far=far)
                 return float(np.mean(np.square(e))) if len(e) else 0.0
-            if not len(_log_errors(cur, sub, keys)):
+            if not len(_log_errors(cur, sub, keys, far=far)):
                 continue  # none of this configuration's records is a candidate now
             # (an uncalibrated efficiency starts inside its range: Nelder-Mead's
             # first simplex is too small around 0 to leave the bound at 1)

@@ -794,9 +794,9 @@ adaptcore_hw_t default_hw() {
   // for each kernel, which is what the planner uses at run time. The launch
   // cost is the measured per-kernel floor of back-to-back launches.
   h.t_launch = 1.9e-06;
-  h.t_mem_latency = 1.216e-06;
+  h.t_mem_latency = 1.217e-06;
   h.hbm_eta = 1;
-  h.l2_bw_cu = 3.529e+10;
+  h.l2_bw_cu = 3.532e+10;
   h.unaligned_eta = 1;
   h.l2_hit = 5.128e-33;
   h.swizzle_gain = 0.9092;
@@ -805,43 +805,43 @@ adaptcore_hw_t default_hw() {
   // 44-58 and their register-load forms 59-65, tall-skinny 66-71 and their
   // register-load forms 72-75; 0 = analytic estimate, no timing data)
   static const double kIter[AC_N_CFG] = {
-      3.121e-06, 2.398e-06, 2.005e-06, 1.055e-06, 9.358e-14, 7.856e-07, 6.264e-07, 3.795e-07,
-      1.22e-06, 9.358e-14, 9.358e-14, 1.105e-06, 1.339e-06, 1.44e-06, 1.345e-06, 1.546e-06,
-      7.293e-07, 5.271e-07, 5.172e-07, 6.181e-07, 5.559e-08, 9.358e-14, 2.409e-06, 9.358e-14,
-      1.935e-06, 9.358e-14, 1.526e-06, 1.329e-06, 9.358e-14, 5.343e-07, 5.275e-07, 6.703e-07,
-      1.942e-07, 2.773e-06, 2.027e-06, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
-      0, 0, 0, 0, 2.271e-06, 1.317e-06, 1.282e-06, 1.011e-08,
-      2.255e-06, 2.187e-06, 2.218e-07, 1.889e-07, 9.358e-14, 9.358e-14, 9.358e-14, 2.837e-09,
-      4.378e-07, 5.173e-07, 0, 1.703e-06, 9.358e-14, 4.242e-07, 1.773e-06, 1.773e-06,
-      7.562e-07, 0, 9.358e-14, 2.714e-13, 2.532e-13, 2.592e-07, 7.958e-07, 2.764e-13,
-      7.332e-07, 7.197e-07, 3.971e-07, 8.296e-07, 0, 0, 0, 0,
+      3.202e-06, 2.343e-06, 2.297e-06, 1.067e-06, 9.358e-14, 8.208e-07, 6.285e-07, 8.829e-07,
+      1.211e-06, 9.358e-14, 9.358e-14, 1.614e-06, 1.54e-06, 1.247e-06, 1.319e-06, 6.514e-06,
+      4.154e-06, 7.299e-07, 7.763e-07, 1.263e-06, 9.358e-14, 9.358e-14, 2.884e-07, 2.128e-06,
+      7.211e-06, 2.01e-06, 1.913e-06, 1.532e-06, 5.342e-10, 7.214e-07, 9.015e-07, 8.849e-07,
+      2.567e-07, 2.833e-06, 2.176e-06, 0, 9.358e-14, 9.358e-14, 9.358e-14, 0,
+      0, 0, 0, 0, 2.071e-06, 1.291e-06, 1.309e-06, 3.586e-09,
+      2.166e-06, 2.115e-06, 1.967e-07, 2.405e-07, 8.638e-07, 9.358e-14, 9.358e-14, 5.205e-10,
+      2.543e-07, 5.736e-07, 9.358e-14, 1.737e-06, 9.358e-14, 9.358e-14, 1.743e-06, 1.775e-06,
+      9.591e-07, 2.893e-06, 9.358e-14, 4.613e-13, 9.358e-14, 3.233e-07, 7.773e-07, 3.027e-13,
+      7.236e-07, 7.183e-07, 4.089e-07, 8.225e-07, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   static const double kWg[AC_N_CFG] = {
-      2.704e-06, 1.248e-06, 4.969e-06, 1.957e-06, 2.325e-06, 7.621e-07, 1.596e-06, 1.176e-06,
-      3.07e-06, 2.749e-06, 3.132e-06, 1.576e-06, 6.747e-07, 9.358e-14, 4.817e-06, 6.022e-06,
-      1.492e-05, 3.416e-06, 5.886e-06, 8.492e-06, 3.016e-06, 9.358e-14, 5.336e-05, 9.358e-14,
-      7.779e-10, 9.358e-14, 1.389e-06, 1.031e-06, 9.358e-14, 4.344e-06, 5.098e-07, 9.358e-14,
-      1.049e-09, 9.358e-14, 1.015e-06, 0, 9.358e-14, 9.358e-14, 2.478e-06, 0,
-      0, 0, 0, 0, 5.156e-06, 2.636e-06, 3.046e-06, 1.702e-06,
-      4.98e-06, 7.97e-06, 3.207e-06, 3.348e-06, 4.19e-06, 2.221e-06, 1.485e-06, 2.563e-06,
-      5.112e-07, 1.093e-06, 0, 2.63e-06, 3.979e-06, 1.666e-06, 3.696e-06, 6.181e-06,
-      3.168e-06, 0, 4.377e-06, 4.86e-06, 5.723e-06, 2.721e-06, 2.079e-06, 1.039e-05,
-      3.978e-06, 4.933e-06, 3.703e-06, 2.346e-06, 0, 0, 0, 0,
+      2.811e-06, 1.7e-06, 5.176e-06, 2.515e-06, 2.787e-06, 1.129e-06, 1.657e-06, 3.096e-07,
+      3.643e-06, 3.33e-06, 3.424e-06, 2.401e-06, 2.429e-06, 6.703e-06, 7.161e-06, 9.791e-06,
+      4.684e-05, 3.724e-06, 4.512e-06, 2.73e-05, 3.654e-06, 4.658e-06, 5.219e-05, 9.358e-14,
+      1e-09, 9.358e-14, 4.328e-06, 9.358e-14, 1.326e-05, 3.699e-05, 9.358e-14, 9.358e-14,
+      3.839e-08, 9.358e-14, 9.358e-14, 0, 9.358e-14, 9.358e-14, 2.042e-06, 0,
+      0, 0, 0, 0, 7.505e-06, 4.832e-06, 5.656e-06, 3.277e-06,
+      1.355e-05, 1.46e-05, 5.308e-06, 5.586e-06, 3.896e-06, 2.767e-06, 1.733e-06, 3.16e-06,
+      2.93e-06, 1.309e-06, 3.332e-06, 2.74e-06, 4.905e-06, 2.538e-06, 5.649e-06, 8.669e-06,
+      3.265e-06, 6.21e-07, 5.178e-06, 5.17e-06, 5.49e-06, 2.134e-06, 2.866e-06, 1.055e-05,
+      4.831e-06, 5.186e-06, 3.93e-06, 2.981e-06, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   // achieved fraction of the streaming rate for the output writes (0: 1)
   static const double kWr[AC_N_CFG] = {
       1, 1, 1, 1, 0.6662, 1, 1, 1,
-      1, 0.6654, 0.6664, 0.9999, 0.9998, 1, 1, 1,
-      1, 0.05755, 1, 0.9999, 0.8759, 1, 1, 0.6346,
-      0.2985, 0.5709, 1, 0.7509, 0.07753, 1, 1, 0.151,
-      0.06691, 0.5667, 0.6535, 0, 0.4715, 0.399, 0.4581, 0,
-      0, 0, 0, 0, 0.9998, 0.9996, 0.9993, 1,
-      1, 1, 1, 1, 1, 1, 1, 1,
-      1, 1, 0, 1, 0.9977, 1, 0.9999, 1,
-      1, 0, 0.1876, 1, 1, 0.08185, 1, 1,
-      0.1286, 1, 1, 0.1727, 0, 0, 0, 0,
+      1, 0.6619, 0.6664, 0.9999, 1, 0.9997, 1, 0.9999,
+      0.9996, 1, 1, 0.9999, 0.9369, 1, 0.2732, 0.5701,
+      0.281, 0.6292, 1, 0.6475, 0.05, 1, 1, 1,
+      0.05, 0.5744, 0.6389, 0, 0.4172, 0.3277, 0.4146, 0,
+      0, 0, 0, 0, 0.4079, 0.9994, 0.9991, 1,
+      1, 1, 1, 1, 0.8409, 1, 0.8467, 1,
+      1, 1, 0.8875, 0.6279, 0.9941, 0.8532, 0.9999, 1,
+      1, 1, 1, 1, 0.1873, 1, 1, 1,
+      0.1588, 1, 1, 0.1698, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0,
       0, 0, 0, 0, 0, 0, 0, 0};
   for (int i = 0; i < AC_N_CFG; ++i) {
@@ -920,7 +920,7 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
   for (int cfg = 0; cfg < N_TILE_CFG; ++cfg) {
     if (!kPersistCfg[cfg]) continue;
     const int idx = IDX_PERSIST + cfg;
-    if (!c.hw.search_open && !(c.hw.cfg_iter[idx] > 0 && c.hw.cfg_wg[idx] > 0)) continue;
+    if (!c.hw.search_open && (!kPersistSearch[cfg] || !(c.hw.cfg_iter[idx] > 0 && c.hw.cfg_wg[idx] > 0))) continue;
     const TileCfg& t = kTileCfg[cfg];
     if ((t.bm > 2 * s.M && t.bm > 32) || (t.bn > 2 * s.N && t.bn > 32)) continue;
     const int64_t ntiles = cdiv(s.M, t.bm) * cdiv(s.N, t.bn);

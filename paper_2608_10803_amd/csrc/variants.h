@@ -35,6 +35,13 @@ static_assert(sizeof(kGroupedCfg) / sizeof(kGroupedCfg[0]) == N_TILE_CFG, "group
 // global loads ahead, carried across tiles): the depth-1 configurations.
 constexpr bool kPersistCfg[] = {true, true, false, true, true, true, false, false, false, false, false};
 static_assert(sizeof(kPersistCfg) / sizeof(kPersistCfg[0]) == N_TILE_CFG, "persistent configurations");
+// Persistent configurations the class-fixed search offers (the open search
+// and forced keys offer every one). The 256 x 256 one is left out: timed on
+// the calibration shapes it was the fastest configuration on 3 of 49 (by at
+// most 7 %), while the latency model prices it about 15 % low on write-bound
+// shapes, where the two-per-CU direct-to-LDS tiles are faster.
+constexpr bool kPersistSearch[] = {false, true, false, true, true, true, false, false, false, false, false};
+static_assert(sizeof(kPersistSearch) / sizeof(kPersistSearch[0]) == N_TILE_CFG, "persistent search menu");
 
 // Small-M Copy configurations: M <= 16*mt rows, wkw waves split the k-range
 // of a workgroup (the others split its columns); a workgroup covers

@@ -424,3 +424,22 @@ def test_offchip_templates_and_their_candidates():
         assert any(c["grid_y"] > 1 for c in off) and all(c["pk"] % c["grid_y"] == 0 for c in off)
     finally:
         ac.adaptcore_set_hw(hw)
+
+
+def test_persistent_256_tile_only_in_the_open_search():
+    """The persistent 256 x 256 tile is measured rarely fastest and is left
+    out of the class-fixed search; the open search and forced keys keep it."""
+    BF = ac.AC_BF16_BF16OUT
+    s = (20000, 20000, 128)
+    def pp256(cands):
+        return [c for c in cands if c["family_name"] == "persist" and c["tile_m"] == 256 and c["tile_n"] == 256]
+    assert not pp256(ac.adaptcore_candidates(*s, BF, 0))
+    assert [c for c in ac.adaptcore_candidates(*s, BF, 0) if c["family_name"] == "persist"]
+    hw = _with_hw(search_open=1)
+    try:
+        opened = pp256(ac.adaptcore_candidates(*s, BF, 0))
+        assert opened
+        key = opened[0]["variant_key"]
+    finally:
+        ac.adaptcore_set_hw(hw)
+    assert ac.adaptcore_plan_kernels(ac.adaptcore_plan_variant(*s, BF, 0, key))[0].startswith("k_tile_pp<256, 256")
