@@ -17,10 +17,15 @@ are obtained by profiling. This module
     for the open search.
 
     python -m paper_2608_10803_amd.calibrate measure OUT.json   (GPU)
-    python -m paper_2608_10803_amd.calibrate fit RECORDS.json [--near F]
-        (after init on the GPU machine, so that the planner prices with the
+        [--family NAME --shapes-from RECORDS.json: only that family's
+        configurations, on the shapes where RECORDS.json has them]
+    python -m paper_2608_10803_amd.calibrate splice OLD.json NEW.json OUT.json
+        (NEW's records replace OLD's of the same family and shape)
+    python -m paper_2608_10803_amd.calibrate fit RECORDS.json [--near F] [--family NAME]
+        (after init on the device, so that the planner prices with the
         device's occupancies; --near F fits exactly only configurations
-        within F times their shape's fastest, the others one-sided)
+        within F times their shape's fastest, the others one-sided; --family
+        refits only that family's configurations, the rest of the profile held)
     python -m paper_2608_10803_amd.calibrate emit FIT.json      (C++ defaults)
 
 `fit` holds half of the measured shapes out: the profile is fitted on a
@@ -160,9 +165,10 @@ def warm_up(A, B, C, stream, seconds=2.0):
         torch.cuda.synchronize()
 
 
-def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=print):
-    """Time every legal configuration of each shape (GPU). Writes a JSON list
-    of records {M, N, K, key, family, cfg fields, t}."""
+def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=print, family=None):
+    """Time every legal configuration of each shape (GPU), or with `family`
+    only that family's. Writes a JSON list of records {M, N, K, key, family,
+    cfg fields, t}."""
     import torch
     ac.adaptcore_init()
     shapes = shapes or sample_shapes()
@@ -189,6 +195,8 @@ def measure(out_path, shapes=None, dtype=ac.AC_BF16_BF16OUT, max_cands=100, log=
     t0 = time.time()
     for si, (M, N, K) in enumerate(shapes):
         cands = ac.adaptcore_candidates(M, N, K, dtype, 0)
+        if family:
+            cands = [c for c in cands if c["family_name"] == family]
         if len(cands) > max_cands:
             # the model's best, every direct-to-LDS, persistent and tall configuration
             # with at most 4 splits, and a spread of the rest
@@ -317,7 +325,7 @@ def near_records(recs, near):
     return [r for r in recs if r["t"] <= near * best[(r["M"], r["N"], r["K"], r["dtype"])]]
 
 
-def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
+def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None, only=None):
     """Fit the profile: minimise the squared log error of the model over the
     measured configurations (with `near`, exactly only for those within that
     factor of their shape's fastest, and for the others only where the model
@@ -326,7 +334,10 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
     slow the slow ones look). Alternates a Nelder-Mead search over the global constants
     (launch, latency, bandwidth, cache hit rate) with one over the three
     constants of each kernel configuration (iteration cost, workgroup cost,
-    write efficiency) on that configuration's records."""
+    write efficiency) on that configuration's records. With `only` (a set of
+    configuration indices) the global constants and every other
+    configuration are held, and one round refits those configurations alone
+    (after a change to their kernels)."""
     from scipy.optimize import minimize
     hw0 = (hw0 or ac.adaptcore_get_hw()).copy()
     meas = _by_shape(recs)
@@ -353,14 +364,15 @@ def fit(recs, hw0=None, rounds=3, iters=300, log=print, near=None):
 
     l0 = loss_all(cur)
     evals = 0
-    for rnd in range(rounds):
-        base = cur.copy()
-        res = minimize(lambda x: loss_all(make_global(x, base)), np.zeros(len(FIT_FIELDS)), method="Nelder-Mead",
-                       options={"maxiter": iters, "xatol": 1e-3, "fatol": 1e-5})
-        cur = make_global(res.x, base)
-        evals += res.nfev
+    for rnd in range(1 if only else rounds):
+        if not only:
+            base = cur.copy()
+            res = minimize(lambda x: loss_all(make_global(x, base)), np.zeros(len(FIT_FIELDS)),
+                           method="Nelder-Mead", options={"maxiter": iters, "xatol": 1e-3, "fatol": 1e-5})
+            cur = make_global(res.x, base)
+            evals += res.nfev
         for idx in sorted(by_cfg):
-            if idx < 0:
+            if idx < 0 or (only and idx not in only):
                 continue
             keys = by_cfg[idx]
             sub = {sk: mt for sk, mt in meas.items() if any(k in keys for k in mt)}
@@ -413,8 +425,24 @@ def emit_cpp(profile):
 
 
 def main(argv):
+    fam = argv[argv.index("--family") + 1] if "--family" in argv else None
     if len(argv) >= 2 and argv[0] == "measure":
-        measure(argv[1])
+        shapes = None
+        if "--shapes-from" in argv:
+            with open(argv[argv.index("--shapes-from") + 1]) as f:
+                old = json.load(f)
+            shapes = sorted({(r["M"], r["N"], r["K"]) for r in old if fam is None or r["family"] == fam})
+        measure(argv[1], shapes, family=fam)
+    elif len(argv) >= 4 and argv[0] == "splice":
+        # OLD NEW OUT: NEW's records replace OLD's of the same family on the same shapes
+        with open(argv[1]) as f:
+            old = json.load(f)
+        with open(argv[2]) as f:
+            new = json.load(f)
+        drop = {(r["M"], r["N"], r["K"], r["dtype"], r["family"]) for r in new}
+        out = [r for r in old if (r["M"], r["N"], r["K"], r["dtype"], r["family"]) not in drop] + new
+        with open(argv[3], "w") as f:
+            json.dump(out, f)
     elif len(argv) >= 2 and argv[0] == "fit":
         with open(argv[1]) as f:
             recs = json.load(f)
@@ -445,7 +473,8 @@ def main(argv):
             return out
         before = report(hw0)
         near = float(argv[argv.index("--near") + 1]) if "--near" in argv else None
-        h, stats = fit(train, hw0, log=lambda m: print(m, file=sys.stderr), near=near)
+        only = {config_of(r["key"]) for r in train if r["family"] == fam} if fam else None
+        h, stats = fit(train, hw0, log=lambda m: print(m, file=sys.stderr), near=near, only=only)
         after = report(h)
         out = {"profile": h.as_dict(), "fit": stats, "near": near, "before": before, "after": after,
                "records": len(recs), "shapes": len(_by_shape(recs)), "train_shapes": len(train_keys),

@@ -181,6 +181,7 @@ struct Ctx {
   double compulsory;
   int cbytes;
   bool unaligned;
+  int cls = -1;  // the shape's class when the search is class-fixed (-1: every candidate)
 };
 
 // bytes of B (K x N, 16-bit)
@@ -963,9 +964,11 @@ static void enumerate_all(const Ctx& c, std::vector<Plan>& out) {
   // with 2 to 32 k1-slices, taken by 1 (SingleCoreSplitK) or more
   // (HybridSplitK) workgroups along K; the class-fixed search keeps them for
   // the two off-chip templates only (enumerate)
+  const bool offchip = c.hw.search_open || c.cls < 0 || c.cls == AC_CLASS_SINGLE_CORE_SPLITK ||
+                       c.cls == AC_CLASS_HYBRID_SPLITK;
   for (int cfg : {0, 4}) {
     const DlCfg& d = kDlCfg[cfg];
-    if (!calibrated(IDX_DL + cfg) || d.bm > 2 * s.M || d.bn > 2 * s.N) continue;
+    if (!offchip || !calibrated(IDX_DL + cfg) || d.bm > 2 * s.M || d.bn > 2 * s.N) continue;
     const int64_t kt = cdiv(s.K, TILE_BK), sup = cdiv(cdiv(s.M, d.bm), 2) * cdiv(s.N, d.bn);
     for (int pk : kSplits) {
       if (pk > 32 || pk > kt) break;
@@ -1052,7 +1055,7 @@ std::vector<Plan> enumerate(const Shape& s, const adaptcore_hw_t& hw, int* cls_o
   if (cls_out) *cls_out = cls;
   const double compulsory = 2.0 * s.M * s.K + 2.0 * s.K * s.N;
   const bool unaligned = (s.K % 8) != 0 || (s.N % 8) != 0;
-  Ctx c{s, hw, compulsory, out_bytes(s.dtype), unaligned};
+  Ctx c{s, hw, compulsory, out_bytes(s.dtype), unaligned, cls};
   std::vector<Plan> all;
   enumerate_all(c, all);
   std::vector<Plan> sel;

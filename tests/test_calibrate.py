@@ -63,3 +63,38 @@ def test_regret_of_a_wrong_choice():
     assert ev["top1"] == 0.0
     assert ev["regret_geomean"] == pytest.approx(1.5) and ev["regret_max"] == pytest.approx(1.5)
     assert math.isclose(ev["within_10pct"], 0.0)
+
+
+def test_splice_replaces_one_family_on_the_remeasured_shapes(tmp_path):
+    import json
+    old = [dict(M=1, N=2, K=3, dtype=BF16, family="direct", key=1, t=1.0),
+           dict(M=1, N=2, K=3, dtype=BF16, family="tile", key=2, t=2.0),
+           dict(M=4, N=5, K=6, dtype=BF16, family="direct", key=1, t=3.0)]
+    new = [dict(M=1, N=2, K=3, dtype=BF16, family="direct", key=1, t=0.5),
+           dict(M=1, N=2, K=3, dtype=BF16, family="direct", key=3, t=0.7)]
+    paths = [tmp_path / n for n in ("old.json", "new.json", "out.json")]
+    for p, recs in zip(paths, (old, new)):
+        p.write_text(json.dumps(recs))
+    cal.main(["splice"] + [str(p) for p in paths])
+    out = json.loads(paths[2].read_text())
+    got = sorted((r["M"], r["family"], r["key"], r["t"]) for r in out)
+    assert got == [(1, "direct", 1, 0.5), (1, "direct", 3, 0.7), (1, "tile", 2, 2.0), (4, "direct", 1, 3.0)]
+
+
+def test_family_refit_holds_the_rest_of_the_profile():
+    """Time one family's candidates at three times the model's price: a
+    refit of that family alone lowers the loss and leaves the global
+    constants and every other configuration's constants as they were."""
+    hw = ac.adaptcore_get_hw()
+    fam = "direct"
+    recs = records(lambda c: c["predicted_s"] * (3.0 if c["family_name"] == fam else 1.0))
+    only = {cal.config_of(r["key"]) for r in recs if r["family"] == fam}
+    assert only
+    h, stats = cal.fit(recs, hw, log=lambda m: None, only=only)
+    assert stats["loss_after"] < stats["loss_before"]
+    for name in cal.FIT_FIELDS:
+        assert getattr(h, name) == getattr(hw, name), name
+    for i in range(ac.AC_N_CFG):
+        if i not in only:
+            assert (h.cfg_iter[i], h.cfg_wg[i], h.cfg_wr[i]) == (hw.cfg_iter[i], hw.cfg_wg[i], hw.cfg_wr[i]), i
+    assert any(h.cfg_iter[i] != hw.cfg_iter[i] or h.cfg_wg[i] != hw.cfg_wg[i] for i in only)
