@@ -1616,7 +1616,8 @@ __global__ __launch_bounds__(256) void k_smallk_win(GemmArgs g) {
 // (their results are never stored); k past K reads as zero. WK = 1: the four
 // waves cover a 64 x 64 block of C, each over all of K. WK = 4 or 16: the WK
 // waves split the 32-k blocks of one 32 x 32 block evenly and wave 0 adds
-// the partial sums in wave order through LDS.
+// the partial sums in wave order through LDS (a partition of one block is
+// wave 0's alone, and the others leave at once).
 template <int WK, int OUT>
 __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) {
   constexpr int U = 4;  // 32-k blocks whose loads are issued together
@@ -1711,11 +1712,17 @@ __global__ __launch_bounds__(WK == 1 ? 256 : 64 * WK) void k_direct(GemmArgs g) 
   }
 
   if constexpr (WK > 1) {
-    if (wave > 0) red[(wave - 1) * 64 + lane] = acc;
-    __syncthreads();
-    if (wave != 0) return;
+    if (pb1 - pb0 <= 1) {
+      // (uniform over the workgroup) at most one 32-k block: wave 0 holds
+      // the whole sum and the other waves have none to add
+      if (wave != 0) return;
+    } else {
+      if (wave > 0) red[(wave - 1) * 64 + lane] = acc;
+      __syncthreads();
+      if (wave != 0) return;
 #pragma unroll
-    for (int w = 1; w < WK; ++w) acc += red[(w - 1) * 64 + lane];
+      for (int w = 1; w < WK; ++w) acc += red[(w - 1) * 64 + lane];
+    }
   }
   // (operands swapped: the MFMA forms the transposed block) the lane holds
   // row m0 + lane % 32 and, for q = 0..3, the four consecutive columns
